@@ -1,0 +1,25 @@
+"""fp64 CPU oracle for the batched 6-DOF underwater-vehicle rollout step.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path (the HIP library and its
+Python binding) imports, calls or links anything under this directory; only the tests,
+the smoke check and the CPU-baseline leg of the benchmark do.
+
+The oracle is the method written out plainly, step by step, in NumPy float64,
+vectorised over environments, with the textbook matrix forms (6x6 mass, Coriolis and
+damping matrices, a linear solve) where the GPU path uses hand-expanded cross products.
+It shares no code with the HIP path: its only inputs are the seeded data in
+``workloads`` and counter-based Philox draws it computes itself.
+
+Modules
+  rng       Philox4x32-10, uniform / affine maps, Shoemake rotations, Box-Muller
+  dynamics  Fossen 6-DOF equations of motion (paper Sec. III-C, the model behind the
+            MPC baseline) and classic RK4 with quaternion renormalisation
+  env       reset / domain randomisation, references, observation, reward, auto-reset,
+            batch statistics, rollouts (paper Sec. III-A, III-B, IV-A)
+  mlp       bf16 round-to-nearest-even, policy / value MLP forward, Gaussian log-prob
+  gae       generalised advantage estimation (the PPO learner of Sec. II-A)
+
+Every function is pinned by a ``-m "not gpu"`` test against closed forms, invariants,
+special cases or an independent library; see the test files under ``tests/``.
+"""
+from . import rng, dynamics, mlp, gae, env  # noqa: F401

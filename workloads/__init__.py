@@ -1,0 +1,156 @@
+"""Seeded synthetic inputs shared by the CPU oracle, the tests and the benchmark.
+
+This module holds data only: vehicle constants, the thruster allocation table, the
+five workload presets and seeded policy/value weights.  It contains none of the
+method's arithmetic (no dynamics, no random-draw maps, no network evaluation), so the
+oracle and the HIP path can both take their inputs from here without sharing code.
+
+Vehicle numbers: the 6-DOF vehicle used by the benchmark workloads (mass, inertia,
+added mass, linear and quadratic damping, weight, buoyancy, centre of buoyancy 0.02 m
+above the centre of gravity, 8 thrusters of at most 40 N).  The paper names its vehicle
+(a BlueROV2 Heavy) and says thrust commands reach the thrusters through an allocation
+matrix (Sec. IV-B, real-world experiments) but gives neither the geometry nor the
+matrix, so the thruster geometry below is this project's constant.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "VEHICLE", "THRUSTER_POS", "THRUSTER_DIR", "ALLOC", "EPISODE_LEN",
+    "FLAG_DR", "FLAG_CURRENT", "FLAG_LISSAJOUS", "FLAG_STAGGER", "FLAG_TRAJ_STATE",
+    "MODE_EXTERNAL", "MODE_RANDOM", "MODE_POLICY_MEAN", "MODE_POLICY_SAMPLE",
+    "CONFIGS", "config", "mlp_weights", "vehicle_variant", "random_states",
+]
+
+# --- vehicle (fp32 values; every consumer promotes them exactly) -------------------
+# The body frame has its origin at the centre of gravity, so r_g = 0 by construction.
+VEHICLE = {
+    "m": np.float32(11.5),
+    "inertia": np.array([0.16, 0.16, 0.16], np.float32),
+    "added_mass": np.array([5.5, 12.7, 14.6, 0.12, 0.12, 0.12], np.float32),
+    "lin_damp": np.array([4.0, 6.2, 5.2, 0.07, 0.07, 0.07], np.float32),
+    "quad_damp": np.array([18.2, 21.7, 37.0, 1.5, 1.5, 1.5], np.float32),
+    "W": np.float32(112.8),
+    "B": np.float32(114.8),
+    # body frame is forward-right-down, so "0.02 m above the CoG" is -z
+    "r_b": np.array([0.0, 0.0, -0.02], np.float32),
+    "f_max": np.float32(40.0),
+}
+
+# --- thruster geometry (project constant, FRD body frame, metres) ------------------
+# Four horizontal thrusters at 45 degrees in the x-y plane, four vertical thrusters.
+_C45 = 0.70710678118654752
+THRUSTER_POS = np.array([
+    [0.156, 0.111, 0.0], [0.156, -0.111, 0.0], [-0.156, 0.111, 0.0], [-0.156, -0.111, 0.0],
+    [0.120, 0.218, 0.0], [0.120, -0.218, 0.0], [-0.120, 0.218, 0.0], [-0.120, -0.218, 0.0],
+], np.float64)
+THRUSTER_DIR = np.array([
+    [_C45, -_C45, 0.0], [_C45, _C45, 0.0], [_C45, _C45, 0.0], [_C45, -_C45, 0.0],
+    [0.0, 0.0, 1.0], [0.0, 0.0, 1.0], [0.0, 0.0, 1.0], [0.0, 0.0, 1.0],
+], np.float64)
+
+# 6x8 allocation table, row-major, rows = (X, Y, Z, K, M, N), column i = [d_i ; r_i x d_i].
+# Written out as literals (the geometry above is the documentation; a test re-derives it).
+_Y = 0.18879751  # 0.267 * cos(45 deg)
+ALLOC = np.array([
+    [_C45, _C45, _C45, _C45, 0.0, 0.0, 0.0, 0.0],
+    [-_C45, _C45, _C45, -_C45, 0.0, 0.0, 0.0, 0.0],
+    [0.0, 0.0, 0.0, 0.0, 1.0, 1.0, 1.0, 1.0],
+    [0.0, 0.0, 0.0, 0.0, 0.218, -0.218, 0.218, -0.218],
+    [0.0, 0.0, 0.0, 0.0, -0.120, -0.120, 0.120, 0.120],
+    [-_Y, _Y, -_Y, _Y, 0.0, 0.0, 0.0, 0.0],
+], np.float32)
+
+EPISODE_LEN = 500
+
+# --- flags and action modes (same values as the C header) -------------------------
+FLAG_DR = 1           # per-env mass / added-mass / damping scales at reset
+FLAG_CURRENT = 2      # per-env constant ocean current at reset
+FLAG_LISSAJOUS = 4    # per-env Lissajous position reference plus yaw ramp
+FLAG_STAGGER = 8      # initial episode step of env i is i mod episode length
+FLAG_TRAJ_STATE = 16  # record the state trajectory in rollouts
+
+MODE_EXTERNAL = 0
+MODE_RANDOM = 1
+MODE_POLICY_MEAN = 2
+MODE_POLICY_SAMPLE = 3
+
+# --- the five workloads ------------------------------------------------------------
+# c1 small parity case; c2 randomised open loop; c3 closed loop with the policy;
+# c4 the headline: 16384 envs, 4 RK4 substeps per 0.04 s control step, Lissajous
+# references; c5 PPO rollout of 65536 envs x 64 steps plus GAE.
+CONFIGS = {
+    "c1": dict(name="c1", n_envs=64, T=200, substeps=1, dt_control=0.02, seed=1,
+               flags=0, mode=MODE_RANDOM, policy=False, value=False),
+    "c2": dict(name="c2", n_envs=4096, T=1000, substeps=1, dt_control=0.02, seed=2,
+               flags=FLAG_DR | FLAG_CURRENT, mode=MODE_RANDOM, policy=False, value=False),
+    "c3": dict(name="c3", n_envs=4096, T=1000, substeps=1, dt_control=0.02, seed=3,
+               flags=FLAG_DR | FLAG_CURRENT, mode=MODE_POLICY_MEAN, policy=True, value=False),
+    "c4": dict(name="c4", n_envs=16384, T=2000, substeps=4, dt_control=0.04, seed=4,
+               flags=FLAG_DR | FLAG_CURRENT | FLAG_LISSAJOUS, mode=MODE_POLICY_MEAN,
+               policy=True, value=False),
+    "c5": dict(name="c5", n_envs=65536, T=64, substeps=1, dt_control=0.02, seed=5,
+               flags=FLAG_DR | FLAG_CURRENT | FLAG_STAGGER, mode=MODE_POLICY_SAMPLE,
+               policy=True, value=True, gamma=0.99, lam=0.95),
+}
+for _c in CONFIGS.values():
+    _c.setdefault("episode_len", EPISODE_LEN)
+    _c.setdefault("env_offset", 0)
+
+POLICY_SEED = 7
+VALUE_SEED = 8
+LOG_STD = -0.5
+OBS_DIM, ACT_DIM, HIDDEN = 23, 8, 256
+
+
+def config(name: str, **overrides) -> dict:
+    """A copy of a preset with fields overridden (e.g. a smaller n_envs or T)."""
+    c = dict(CONFIGS[name])
+    c.update(overrides)
+    return c
+
+
+def vehicle_variant(**overrides) -> dict:
+    """A copy of VEHICLE with selected fields replaced (fp32), for closed-form cases."""
+    v = {k: (np.array(x, np.float32) if np.ndim(x) else np.float32(x)) for k, x in VEHICLE.items()}
+    for k, x in overrides.items():
+        v[k] = np.array(x, np.float32) if np.ndim(x) else np.float32(x)
+    return v
+
+
+def mlp_weights(n_out: int, seed: int, n_in: int = OBS_DIM, hidden: int = HIDDEN) -> dict:
+    """Seeded MLP parameters n_in -> hidden -> hidden -> n_out.
+
+    Weights: N(0, 1/fan_in) from NumPy PCG64, rounded fp64 -> fp32 -> bf16 (round to
+    nearest even, by torch's conversion).  Returned as uint16 bf16 bit patterns in
+    PyTorch Linear layout W[out][in], row-major.  Biases: U[-0.1, 0.1] in fp32.
+    log_std: -0.5 for every action dimension.
+    """
+    import torch
+
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shapes = [(hidden, n_in), (hidden, hidden), (n_out, hidden)]
+    out = {}
+    for i, (o, k) in enumerate(shapes, start=1):
+        w = rng.standard_normal((o, k)) / math.sqrt(k)
+        wb = torch.from_numpy(w.astype(np.float32)).to(torch.bfloat16)
+        out[f"W{i}"] = wb.view(torch.int16).numpy().view(np.uint16).copy()
+    for i, o in enumerate([hidden, hidden, n_out], start=1):
+        out[f"b{i}"] = rng.uniform(-0.1, 0.1, size=o).astype(np.float32)
+    out["log_std"] = np.full(ACT_DIM, LOG_STD, np.float32)
+    out["n_in"], out["hidden"], out["n_out"] = n_in, hidden, n_out
+    return out
+
+
+def random_states(n: int, seed: int, pos_scale=2.0, vel_scale=1.0, rate_scale=1.0) -> np.ndarray:
+    """Seeded fp32 states [13][n] (p, unit q, v, w) for one-step parity cases."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    p = rng.uniform(-pos_scale, pos_scale, (3, n))
+    q = rng.standard_normal((4, n))
+    q /= np.linalg.norm(q, axis=0, keepdims=True)
+    v = rng.uniform(-vel_scale, vel_scale, (3, n))
+    w = rng.uniform(-rate_scale, rate_scale, (3, n))
+    return np.concatenate([p, q, v, w]).astype(np.float32)
