@@ -1,0 +1,187 @@
+/*
+ * auv.h - C interface of libauv, the batched 6-DOF underwater-vehicle rollout on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * What is computed: many independent copies of one vehicle model stepped in a single
+ * batch, each with its own random initial conditions and randomisation parameters
+ * (paper Sec. III-A), observed through body-frame errors (Sec. III-B1) and driven by a
+ * policy network (Sec. II-A, IV).  One control step of one environment:
+ *   1. action a (caller's, Philox-uniform, or the policy MLP's mean / Gaussian sample);
+ *      u = clip(a, -1, 1); thrust f = f_max u; body wrench tau = T f (6x8 allocation)
+ *   2. `substeps` classic RK4 substeps of the Fossen 6-DOF equations of motion (the model
+ *      of Sec. III-C) with added mass, Coriolis, linear + quadratic damping, restoring
+ *      forces with the buoyancy centre offset (Sec. V-A) and a constant ocean current
+ *   3. episode step + 1; reference pose (episode goal, or Lissajous + yaw ramp)
+ *   4. observation [R^T(p_ref - p), R_err[:,0], R_err[:,1], v, omega, u], R_err = R^T R_ref
+ *   5. reward -|R^T(p_ref - p)| - 0.5 theta_err - 0.01 |u|^2 (shape of Sec. III-B3)
+ *   6. at the episode length: automatic reset with fresh Philox draws (Sec. IV-A1)
+ *
+ * Conventions: world NED, body forward-right-down with origin at the centre of gravity,
+ * Hamilton quaternion (w, x, y, z) body -> world.  State rows: p(3) q(4) v(3) omega(3).
+ *
+ * Memory: every device buffer is allocated and owned by the caller; the library keeps
+ * non-owning pointers and never allocates device memory.  Layouts are structure of
+ * arrays with the environment index fastest: [k][N] or [k][T][N].  Device pointers must
+ * be 16-byte aligned.  All fp32 unless stated.
+ *
+ * Errors: every function returns AUV_OK (0) or a negative code; nothing throws or aborts
+ * across the interface.  Arguments are checked before anything is enqueued; a failed
+ * check returns AUV_EINVAL and enqueues nothing.  auv_last_error() gives a message for
+ * the calling thread's last failure.  Launch failures return AUV_ELAUNCH.
+ *
+ * Streams: `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ * call is asynchronous on that stream unless stated.  A handle is not thread-safe.
+ */
+#ifndef AUV_H
+#define AUV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  AUV_OK = 0,
+  AUV_EINVAL = -1,   /* bad argument: nothing was enqueued */
+  AUV_ENODEV = -2,   /* no usable HIP device */
+  AUV_ELAUNCH = -3,  /* kernel launch failed */
+  AUV_ERUNTIME = -4  /* other HIP runtime error */
+};
+
+/* Action sources. */
+enum {
+  AUV_ACT_EXTERNAL = 0,     /* caller's actions */
+  AUV_ACT_RANDOM = 1,       /* Philox uniform in [-1, 1), counter (env, global step, 1, b) */
+  AUV_ACT_POLICY_MEAN = 2,  /* policy MLP output mu */
+  AUV_ACT_POLICY_SAMPLE = 3 /* mu + exp(log_std) eps, eps Box-Muller from (env, step, 2, b) */
+};
+
+/* Configuration flags. */
+enum {
+  AUV_F_DR = 1,        /* mass (and inertia), added mass, damping scaled by U[0.8, 1.2] */
+  AUV_F_CURRENT = 2,   /* constant world-frame current, U[-0.3, 0.3] m/s per axis */
+  AUV_F_LISSAJOUS = 4, /* Lissajous position reference and level yaw ramp */
+  AUV_F_STAGGER = 8    /* at auv_reset, ep_step of env i starts at (global id) mod H */
+};
+
+#define AUV_OBS_DIM 23
+#define AUV_ACT_DIM 8
+#define AUV_STATE_DIM 13
+#define AUV_PARAM_DIM 24
+#define AUV_HIDDEN 256
+#define AUV_ENVS_PER_GROUP 64 /* environments per workgroup; stats partials per group */
+
+typedef struct auv_env auv_env; /* opaque; host memory owned by the library */
+
+typedef struct {
+  int32_t n_envs;      /* N >= 1 */
+  int32_t substeps;    /* S >= 1 RK4 substeps per control step */
+  int32_t episode_len; /* H >= 1 control steps per episode */
+  float dt_control;    /* control period in seconds, > 0 */
+  uint64_t seed;       /* Philox key = (seed & 0xffffffff, seed >> 32) */
+  uint32_t flags;      /* AUV_F_* */
+  uint32_t env_offset; /* global id of local env 0 (Philox counter word 0 = global id) */
+} auv_config;
+
+/* Vehicle constants, copied by value into every launch.  Diagonal matrices are given by
+ * their diagonals in the order (surge, sway, heave, roll, pitch, yaw). */
+typedef struct {
+  float m;              /* rigid-body mass, kg */
+  float inertia[3];     /* rigid-body inertia diagonal about the CoG, kg m^2 */
+  float added_mass[6];  /* diagonal added mass M_A */
+  float lin_damp[6];    /* diagonal linear damping D_L */
+  float quad_damp[6];   /* diagonal quadratic damping D_Q (force = D_Q |nu| nu) */
+  float W, B;           /* weight and buoyancy, N */
+  float r_b[3];         /* centre of buoyancy in body axes, m */
+  float f_max;          /* thrust per thruster at |u| = 1, N */
+  float alloc[48];      /* 6x8 allocation table T, row-major: tau = T f */
+} auv_vehicle;
+
+/* Environment state buffers (device, caller-owned, each N-strided). */
+typedef struct {
+  float* state;       /* [13][N] p, q, v, omega */
+  float* params;      /* [24][N] s_m s_a s_d, c_w(3), p_goal(3), q_goal(4), A(3), f(3),
+                         phase(3), yaw_rate, yaw0 */
+  int32_t* ep_step;   /* [N] control steps taken in the current episode */
+  uint32_t* episode;  /* [N] episode index (Philox counter word 1 of the reset draws) */
+  float* obs;         /* [23][N] current observation; rows 15..22 = previous clipped action */
+} auv_env_buffers;
+
+/* MLP n_in=23 -> 256 -> 256 -> n_out, tanh hidden layers, linear output.  Every layer's
+ * input is rounded to bf16 (nearest even); accumulation is fp32; biases fp32. */
+typedef struct {
+  const uint16_t* w;     /* device bf16 bits: W1[256][23], W2[256][256], W3[n_out][256],
+                            contiguous, row-major (out, in) */
+  const float* b;        /* device: b1[256], b2[256], b3[n_out] contiguous */
+  const float* log_std;  /* device [8]; needed for AUV_ACT_POLICY_SAMPLE, else may be NULL */
+  int32_t n_out;         /* 8 for the policy, 1 for a value net */
+} auv_mlp;
+
+/* Optional per-step outputs of auv_rollout (device, caller-owned; any may be NULL). */
+typedef struct {
+  float* obs;        /* [23][T][N] observation o_t each action was chosen on */
+  float* act;        /* [8][T][N] action a_t before clipping */
+  float* logp;       /* [T][N] Gaussian log-prob of a_t (AUV_ACT_POLICY_SAMPLE only) */
+  float* value;      /* [T][N] V(o_t) (needs a value net) */
+  float* reward;     /* [T][N] */
+  float* done;       /* [T][N] 1.0 where the episode ended at step t, else 0.0 */
+  float* last_value; /* [N] V(o_T) bootstrap value (needs a value net) */
+  float* traj_state; /* [13][T+1][N] state before step 0 and after every step */
+  float* stats;      /* [3][T] per step: sum of reward, sum of done, sum of |dp| */
+  float* stats_work; /* workspace for stats: auv_stats_work_floats(N, T) floats */
+} auv_rollout_buffers;
+
+/* Number of floats of the stats workspace for N envs and T steps (3 T ceil(N/64)). */
+int64_t auv_stats_work_floats(int32_t n_envs, int32_t T);
+
+/* Validates the configuration and buffers and creates a handle.  Makes no GPU call and
+ * allocates no device memory.  global_step starts at 0. */
+int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buffers* bufs,
+               auv_env** out);
+int auv_destroy(auv_env* env);
+
+/* Resets every environment: episode 0, ep_step 0 (or staggered), Philox reset draws
+ * (counter (global id, episode, 0, 0..7)), velocities 0, previous action 0, observation;
+ * global_step back to 0. */
+int auv_reset(auv_env* env, void* stream);
+
+/* One control step of every environment with AUV_ACT_EXTERNAL (actions [8][N] device)
+ * or AUV_ACT_RANDOM (actions ignored).  reward [N] fp32, done [N] uint8 and
+ * stats [3] (sums over envs) are optional outputs; stats needs stats_work
+ * (auv_stats_work_floats(N, 1) floats).  global_step += 1. */
+int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_t* done,
+             float* stats, float* stats_work, void* stream);
+
+/* T control steps of every environment in one launch.  Modes: AUV_ACT_RANDOM (actions
+ * from Philox), AUV_ACT_EXTERNAL (actions from rbufs->act, read as [8][T][N]),
+ * AUV_ACT_POLICY_MEAN / AUV_ACT_POLICY_SAMPLE (policy required; value optional).
+ * global_step += T. */
+int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy,
+                const auv_mlp* value, const auv_rollout_buffers* rbufs, void* stream);
+
+/* Generalised advantage estimation over a [T][N] rollout (backward scan per env):
+ * delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t, V_T = last_value;
+ * A_t = delta_t + gamma lambda (1 - d_t) A_{t+1}, A_T = 0; ret_t = A_t + V_t. */
+int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value,
+            const float* done, const float* last_value, float gamma, float lambda,
+            float* adv, float* ret, void* stream);
+
+/* Stand-alone MLP forward: obs [23][N] -> out [n_out][N] (same arithmetic as inside
+ * auv_rollout). */
+int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float* out,
+                    void* stream);
+
+/* Host-side step counter (Philox counter word 1 of action and noise draws); set it to
+ * resume a saved run bit-exactly together with the state buffers. */
+int64_t auv_get_global_step(const auv_env* env);
+int auv_set_global_step(auv_env* env, int64_t step);
+
+/* Message for the calling thread's last error ("" if none). */
+const char* auv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AUV_H */

@@ -89,7 +89,7 @@ class Env:
         self.flags = int(cfg["flags"])
         self.H = int(cfg["episode_len"])
         self.S = int(cfg["substeps"])
-        self.dt = float(cfg["dt_control"])
+        self.dt = float(np.float32(cfg["dt_control"]))   # the control period is an fp32 input
         self.veh_data = vehicle
         self.alloc = _f64(alloc)                   # [6, 8]
         self.f_max = float(_f64(vehicle["f_max"]))

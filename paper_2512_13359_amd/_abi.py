@@ -1,0 +1,181 @@
+"""ctypes binding of libauv's C interface (include/auv.h), same names, marshalling only.
+
+Device buffers are torch tensors on the GPU; the binding passes their addresses and the
+current HIP stream.  Every compute step runs in libauv's HIP kernels; if the library is
+missing the import of this module fails loudly (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libauv.so")
+
+AUV_OK, AUV_EINVAL, AUV_ENODEV, AUV_ELAUNCH, AUV_ERUNTIME = 0, -1, -2, -3, -4
+AUV_ACT_EXTERNAL, AUV_ACT_RANDOM, AUV_ACT_POLICY_MEAN, AUV_ACT_POLICY_SAMPLE = 0, 1, 2, 3
+AUV_F_DR, AUV_F_CURRENT, AUV_F_LISSAJOUS, AUV_F_STAGGER = 1, 2, 4, 8
+OBS_DIM, ACT_DIM, STATE_DIM, PARAM_DIM, HIDDEN, ENVS_PER_GROUP = 23, 8, 13, 24, 256, 64
+
+_f = ctypes.c_float
+_vp = ctypes.c_void_p
+
+
+class AuvConfig(ctypes.Structure):
+    _fields_ = [("n_envs", ctypes.c_int32), ("substeps", ctypes.c_int32),
+                ("episode_len", ctypes.c_int32), ("dt_control", _f), ("seed", ctypes.c_uint64),
+                ("flags", ctypes.c_uint32), ("env_offset", ctypes.c_uint32)]
+
+
+class AuvVehicle(ctypes.Structure):
+    _fields_ = [("m", _f), ("inertia", _f * 3), ("added_mass", _f * 6), ("lin_damp", _f * 6),
+                ("quad_damp", _f * 6), ("W", _f), ("B", _f), ("r_b", _f * 3), ("f_max", _f),
+                ("alloc", _f * 48)]
+
+
+class AuvEnvBuffers(ctypes.Structure):
+    _fields_ = [("state", _vp), ("params", _vp), ("ep_step", _vp), ("episode", _vp), ("obs", _vp)]
+
+
+class AuvMlp(ctypes.Structure):
+    _fields_ = [("w", _vp), ("b", _vp), ("log_std", _vp), ("n_out", ctypes.c_int32)]
+
+
+class AuvRolloutBuffers(ctypes.Structure):
+    _fields_ = [(k, _vp) for k in ("obs", "act", "logp", "value", "reward", "done", "last_value",
+                                   "traj_state", "stats", "stats_work")]
+
+
+class AuvError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libauv error {code}: {msg}")
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2512_13359_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, P = ctypes.c_int32, ctypes.c_int64, ctypes.POINTER
+    sig = {
+        "auv_stats_work_floats": (i64, [i32, i32]),
+        "auv_create": (ctypes.c_int, [P(AuvConfig), P(AuvVehicle), P(AuvEnvBuffers), P(_vp)]),
+        "auv_destroy": (ctypes.c_int, [_vp]),
+        "auv_reset": (ctypes.c_int, [_vp, _vp]),
+        "auv_step": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "auv_rollout": (ctypes.c_int, [_vp, i32, ctypes.c_int, P(AuvMlp), P(AuvMlp), P(AuvRolloutBuffers), _vp]),
+        "auv_gae": (ctypes.c_int, [i32, i32, _vp, _vp, _vp, _vp, _f, _f, _vp, _vp, _vp]),
+        "auv_mlp_forward": (ctypes.c_int, [P(AuvMlp), i32, _vp, _vp, _vp]),
+        "auv_get_global_step": (i64, [_vp]),
+        "auv_set_global_step": (ctypes.c_int, [_vp, i64]),
+        "auv_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    return lib
+
+
+lib = _load()
+
+
+def _check(rc: int) -> None:
+    if rc != AUV_OK:
+        raise AuvError(rc, lib.auv_last_error().decode())
+
+
+def ptr(t) -> int | None:
+    """Device address of a tensor (None for None)."""
+    return None if t is None else t.data_ptr()
+
+
+def stream_ptr(stream=None) -> int | None:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream or None
+
+
+# ---- the C entry points, same names ---------------------------------------------------
+
+def auv_stats_work_floats(n_envs: int, T: int) -> int:
+    return int(lib.auv_stats_work_floats(n_envs, T))
+
+
+def auv_create(cfg: AuvConfig, veh: AuvVehicle, bufs: AuvEnvBuffers) -> int:
+    h = _vp()
+    _check(lib.auv_create(ctypes.byref(cfg), ctypes.byref(veh), ctypes.byref(bufs), ctypes.byref(h)))
+    return h.value
+
+
+def auv_destroy(h: int) -> None:
+    _check(lib.auv_destroy(h))
+
+
+def auv_reset(h: int, stream=None) -> None:
+    _check(lib.auv_reset(h, stream_ptr(stream)))
+
+
+def auv_step(h: int, mode: int, actions=None, reward=None, done=None, stats=None,
+             stats_work=None, stream=None) -> None:
+    _check(lib.auv_step(h, mode, ptr(actions), ptr(reward), ptr(done), ptr(stats), ptr(stats_work),
+                        stream_ptr(stream)))
+
+
+def auv_rollout(h: int, T: int, mode: int, policy: AuvMlp | None = None, value: AuvMlp | None = None,
+                rbufs: AuvRolloutBuffers | None = None, stream=None) -> None:
+    _check(lib.auv_rollout(h, T, mode, None if policy is None else ctypes.byref(policy),
+                           None if value is None else ctypes.byref(value),
+                           None if rbufs is None else ctypes.byref(rbufs), stream_ptr(stream)))
+
+
+def auv_gae(T: int, n_envs: int, reward, value, done, last_value, gamma: float, lam: float,
+            adv, ret, stream=None) -> None:
+    _check(lib.auv_gae(T, n_envs, ptr(reward), ptr(value), ptr(done), ptr(last_value), gamma, lam,
+                       ptr(adv), ptr(ret), stream_ptr(stream)))
+
+
+def auv_mlp_forward(net: AuvMlp, n_envs: int, obs, out, stream=None) -> None:
+    _check(lib.auv_mlp_forward(ctypes.byref(net), n_envs, ptr(obs), ptr(out), stream_ptr(stream)))
+
+
+def auv_get_global_step(h: int) -> int:
+    return int(lib.auv_get_global_step(h))
+
+
+def auv_set_global_step(h: int, step: int) -> None:
+    _check(lib.auv_set_global_step(h, step))
+
+
+def auv_last_error() -> str:
+    return lib.auv_last_error().decode()
+
+
+# ---- struct builders (marshalling) ---------------------------------------------------
+
+def make_config(n_envs, substeps, episode_len, dt_control, seed, flags, env_offset=0) -> AuvConfig:
+    return AuvConfig(n_envs, substeps, episode_len, float(np.float32(dt_control)), seed, flags, env_offset)
+
+
+def make_vehicle(vehicle: dict, alloc) -> AuvVehicle:
+    v = AuvVehicle()
+    v.m = float(vehicle["m"])
+    for name in ("inertia", "added_mass", "lin_damp", "quad_damp", "r_b"):
+        arr = np.asarray(vehicle[name], np.float32).ravel()
+        getattr(v, name)[:] = [float(x) for x in arr]
+    v.W, v.B, v.f_max = float(vehicle["W"]), float(vehicle["B"]), float(vehicle["f_max"])
+    v.alloc[:] = [float(x) for x in np.asarray(alloc, np.float32).ravel()]
+    return v
+
+
+def make_mlp(w, b, log_std, n_out: int) -> AuvMlp:
+    return AuvMlp(ptr(w), ptr(b), ptr(log_std), n_out)
+
+
+def make_env_buffers(state, params, ep_step, episode, obs) -> AuvEnvBuffers:
+    return AuvEnvBuffers(ptr(state), ptr(params), ptr(ep_step), ptr(episode), ptr(obs))
+
+
+def make_rollout_buffers(**kw) -> AuvRolloutBuffers:
+    return AuvRolloutBuffers(**{k: ptr(v) for k, v in kw.items()})

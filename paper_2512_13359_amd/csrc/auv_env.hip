@@ -1,0 +1,418 @@
+// libauv: environment kernels (reset, lane-per-environment step loop, statistics,
+// GAE) and the C interface.  The policy-driven fused rollout lives in auv_policy.hip.
+#include <cmath>
+#include <cstring>
+
+#include "auv_internal.hpp"
+
+using namespace auv;
+
+namespace auv {
+
+static thread_local std::string g_err;
+
+int set_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(AUV_ELAUNCH, "%s: launch failed: %s", what, hipGetErrorString(e));
+  return AUV_OK;
+}
+
+// ------------------------------------------------------------------------ kernels --
+
+__global__ __launch_bounds__(256) void k_reset(VehArgs V, EnvArgs E) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= E.n) return;
+  const uint32_t gid = E.env_offset + (uint32_t)i;
+  const int ep = (E.flags & F_STAGGER) ? (int)(gid % (uint32_t)E.H) : 0;
+  State x;
+  Params P;
+  reset_draws(E, gid, 0u, x, P);
+  float pr[3], qr[4], o[15], dist, theta;
+  reference(E, P, ep, pr, qr);
+  observe(x, pr, qr, o, dist, theta);
+  const int n = E.n;
+  store_state(E.state, (size_t)n, (size_t)i, x);
+  store_params(E.params, n, i, P);
+  E.ep_step[i] = ep;
+  E.episode[i] = 0u;
+#pragma unroll
+  for (int k = 0; k < 15; ++k) E.obs[k * n + i] = o[k];
+#pragma unroll
+  for (int k = 15; k < OBS; ++k) E.obs[k * n + i] = 0.0f;
+}
+
+// T control steps, one lane per environment, state in registers for the whole launch.
+// Block = one wave = one group of 64 environments (one stats partial per step).
+template <bool EXTERNAL>
+__global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
+                                                 StepOut O) {
+  const int lane = threadIdx.x;
+  const int i = blockIdx.x * 64 + lane;
+  const int n = E.n;
+  const size_t N = (size_t)n, TN = (size_t)T * N;
+  const bool valid = i < n;
+  const uint32_t gid = E.env_offset + (uint32_t)i;
+  const int G = gridDim.x, g = blockIdx.x;
+
+  State x;
+  Params P;
+  int ep = 0;
+  uint32_t episode = 0;
+  float obs[OBS];
+  if (valid) {
+    load_state(E.state, n, i, x);
+    load_params(E.params, n, i, P);
+    ep = E.ep_step[i];
+    episode = E.episode[i];
+#pragma unroll
+    for (int k = 0; k < OBS; ++k) obs[k] = E.obs[k * n + i];
+  } else {  // idle lanes step a harmless dummy vehicle
+    x = State{{0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}};
+    P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
+#pragma unroll
+    for (int k = 0; k < OBS; ++k) obs[k] = 0.0f;
+  }
+  Model M;
+  make_model(V, P, M);
+  bool dirty = false;
+  if (O.traj && valid) store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, x);
+
+  for (int t = 0; t < T; ++t) {
+    const size_t ti = (size_t)t * N + (size_t)i;
+    if (O.obs && valid) {
+#pragma unroll
+      for (int k = 0; k < OBS; ++k) O.obs[k * TN + ti] = obs[k];
+    }
+    float a[ACT];
+    if (EXTERNAL) {
+#pragma unroll
+      for (int k = 0; k < ACT; ++k) a[k] = valid ? O.act[k * TN + ti] : 0.0f;
+    } else {
+      const uint32_t step = gstep0 + (uint32_t)t;
+      const U4 r0 = philox(U4{gid, step, 1u, 0u}, E.key0, E.key1);
+      const U4 r1 = philox(U4{gid, step, 1u, 1u}, E.key0, E.key1);
+      const uint32_t wd[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+      for (int k = 0; k < ACT; ++k) a[k] = 2.0f * u01(wd[k]) - 1.0f;
+      if (O.act && valid) {
+#pragma unroll
+        for (int k = 0; k < ACT; ++k) O.act[k * TN + ti] = a[k];
+      }
+    }
+    float u[ACT], usq = 0.0f;
+#pragma unroll
+    for (int k = 0; k < ACT; ++k) {
+      u[k] = fminf(fmaxf(a[k], -1.0f), 1.0f);
+      usq += u[k] * u[k];
+    }
+    float tau[6];
+    wrench(V, u, tau);
+    for (int s = 0; s < E.substeps; ++s) rk4(V, M, P.cw, tau, E.h, x);
+    ep += 1;
+    float pr[3], qr[4], dist, theta;
+    reference(E, P, ep, pr, qr);
+    observe(x, pr, qr, obs, dist, theta);
+#pragma unroll
+    for (int k = 0; k < ACT; ++k) obs[15 + k] = u[k];
+    const float reward = -dist - 0.5f * theta - 0.01f * usq;
+    const bool done = (ep == E.H);
+    if (O.stats_work) {
+      const float sr = wave_sum(valid ? reward : 0.0f);
+      const float sd = wave_sum((valid && done) ? 1.0f : 0.0f);
+      const float sp = wave_sum(valid ? dist : 0.0f);
+      if (lane == 0) {
+        O.stats_work[((size_t)0 * T + t) * G + g] = sr;
+        O.stats_work[((size_t)1 * T + t) * G + g] = sd;
+        O.stats_work[((size_t)2 * T + t) * G + g] = sp;
+      }
+    }
+    if (valid) {
+      if (O.reward) O.reward[ti] = reward;
+      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
+      if (O.done_u8) O.done_u8[i] = done ? 1 : 0;
+    }
+    if (done) {
+      episode += 1u;
+      reset_draws(E, gid, episode, x, P);
+      make_model(V, P, M);
+      ep = 0;
+      reference(E, P, ep, pr, qr);
+      observe(x, pr, qr, obs, dist, theta);
+#pragma unroll
+      for (int k = 15; k < OBS; ++k) obs[k] = 0.0f;
+      dirty = true;
+    }
+    if (O.traj && valid) store_state(O.traj + (size_t)(t + 1) * N, (size_t)(T + 1) * N, (size_t)i, x);
+  }
+  if (!valid) return;
+  store_state(E.state, N, (size_t)i, x);
+  E.ep_step[i] = ep;
+  E.episode[i] = episode;
+#pragma unroll
+  for (int k = 0; k < OBS; ++k) E.obs[k * n + i] = obs[k];
+  if (dirty) store_params(E.params, n, i, P);
+}
+
+__global__ __launch_bounds__(256) void k_stats_reduce(const float* __restrict__ work, int T, int G,
+                                                      float* __restrict__ stats) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= 3 * T) return;
+  const float* p = work + (size_t)j * G;
+  float s = 0.0f;
+  for (int g = 0; g < G; ++g) s += p[g];
+  stats[j] = s;
+}
+
+// Backward GAE scan, one lane per environment, [T][N] layout (coalesced over envs).
+// Loads a chunk of steps ahead so that many reads are in flight per lane.
+constexpr int GAE_CHUNK = 16;
+__global__ __launch_bounds__(256) void k_gae(int T, int n, const float* __restrict__ rew,
+                                             const float* __restrict__ val, const float* __restrict__ dn,
+                                             const float* __restrict__ last, float gamma, float gl,
+                                             float* __restrict__ adv, float* __restrict__ ret) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const size_t N = (size_t)n;
+  float next_v = last[i], next_a = 0.0f;
+  for (int t1 = T; t1 > 0; t1 -= GAE_CHUNK) {
+    const int t0 = t1 > GAE_CHUNK ? t1 - GAE_CHUNK : 0;
+    float r[GAE_CHUNK], v[GAE_CHUNK], d[GAE_CHUNK];
+#pragma unroll
+    for (int c = 0; c < GAE_CHUNK; ++c) {
+      const int t = t0 + c;
+      if (t < t1) {
+        const size_t ti = (size_t)t * N + i;
+        r[c] = rew[ti]; v[c] = val[ti]; d[c] = dn[ti];
+      }
+    }
+#pragma unroll
+    for (int c = GAE_CHUNK - 1; c >= 0; --c) {
+      const int t = t0 + c;
+      if (t < t1) {
+        const float nd = 1.0f - d[c];
+        const float delta = r[c] + gamma * nd * next_v - v[c];
+        next_a = delta + gl * nd * next_a;
+        const size_t ti = (size_t)t * N + i;
+        adv[ti] = next_a;
+        ret[ti] = next_a + v[c];
+        next_v = v[c];
+      }
+    }
+  }
+}
+
+int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s) {
+  hipLaunchKernelGGL(k_stats_reduce, dim3((3 * T + 255) / 256), dim3(256), 0, s, work, T, G, stats);
+  return check_launch("stats reduce");
+}
+
+}  // namespace auv
+
+// ------------------------------------------------------------------ C interface ----
+
+static int validate_env_ptrs(const auv_env_buffers* b) {
+  const void* ptrs[5] = {b->state, b->params, b->ep_step, b->episode, b->obs};
+  const char* names[5] = {"state", "params", "ep_step", "episode", "obs"};
+  for (int k = 0; k < 5; ++k) {
+    if (!ptrs[k]) return set_error(AUV_EINVAL, "auv_create: buffer '%s' is NULL", names[k]);
+    if (!aligned16(ptrs[k])) return set_error(AUV_EINVAL, "auv_create: buffer '%s' is not 16-byte aligned", names[k]);
+  }
+  return AUV_OK;
+}
+
+extern "C" {
+
+const char* auv_last_error(void) { return auv::g_err.c_str(); }
+
+int64_t auv_stats_work_floats(int32_t n_envs, int32_t T) {
+  if (n_envs <= 0 || T <= 0) return 0;
+  return (int64_t)3 * T * groups_of(n_envs);
+}
+
+int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buffers* bufs,
+               auv_env** out) {
+  if (!cfg || !veh || !bufs || !out) return set_error(AUV_EINVAL, "auv_create: NULL argument");
+  *out = nullptr;
+  if (cfg->n_envs <= 0 || cfg->n_envs > (1 << 26))
+    return set_error(AUV_EINVAL, "auv_create: n_envs must be in [1, 2^26], got %d", cfg->n_envs);
+  if (cfg->substeps < 1 || cfg->substeps > 1024)
+    return set_error(AUV_EINVAL, "auv_create: substeps must be in [1, 1024], got %d", cfg->substeps);
+  if (cfg->episode_len < 1)
+    return set_error(AUV_EINVAL, "auv_create: episode_len must be >= 1, got %d", cfg->episode_len);
+  if (!(cfg->dt_control > 0.0f) || !std::isfinite(cfg->dt_control))
+    return set_error(AUV_EINVAL, "auv_create: dt_control must be a positive finite number");
+  if (cfg->flags & ~(uint32_t)(AUV_F_DR | AUV_F_CURRENT | AUV_F_LISSAJOUS | AUV_F_STAGGER))
+    return set_error(AUV_EINVAL, "auv_create: unknown flag bits 0x%x", cfg->flags);
+  if ((uint64_t)cfg->env_offset + (uint64_t)cfg->n_envs > (1ull << 32))
+    return set_error(AUV_EINVAL, "auv_create: env_offset + n_envs exceeds 2^32");
+  const float* vf = &veh->m;
+  for (size_t k = 0; k < sizeof(auv_vehicle) / sizeof(float); ++k)
+    if (!std::isfinite(vf[k])) return set_error(AUV_EINVAL, "auv_create: vehicle field %zu is not finite", k);
+  if (!(veh->m > 0.0f)) return set_error(AUV_EINVAL, "auv_create: mass must be positive");
+  for (int k = 0; k < 3; ++k)
+    if (!(veh->inertia[k] > 0.0f)) return set_error(AUV_EINVAL, "auv_create: inertia must be positive");
+  for (int k = 0; k < 6; ++k)
+    if (veh->added_mass[k] < 0.0f || veh->lin_damp[k] < 0.0f || veh->quad_damp[k] < 0.0f)
+      return set_error(AUV_EINVAL, "auv_create: added mass and damping must be non-negative");
+  if (int rc = validate_env_ptrs(bufs)) return rc;
+
+  auv_env* e = new (std::nothrow) auv_env;
+  if (!e) return set_error(AUV_ERUNTIME, "auv_create: out of host memory");
+  e->cfg = *cfg;
+  VehArgs& V = e->veh;
+  V.m = veh->m;
+  std::memcpy(V.inertia, veh->inertia, sizeof V.inertia);
+  std::memcpy(V.added_mass, veh->added_mass, sizeof V.added_mass);
+  std::memcpy(V.lin_damp, veh->lin_damp, sizeof V.lin_damp);
+  std::memcpy(V.quad_damp, veh->quad_damp, sizeof V.quad_damp);
+  V.BmW = veh->B - veh->W;
+  for (int k = 0; k < 3; ++k) V.Brb[k] = veh->B * veh->r_b[k];
+  V.f_max = veh->f_max;
+  std::memcpy(V.alloc, veh->alloc, sizeof V.alloc);
+  EnvArgs& E = e->E;
+  E.state = bufs->state;
+  E.params = bufs->params;
+  E.ep_step = bufs->ep_step;
+  E.episode = bufs->episode;
+  E.obs = bufs->obs;
+  E.n = cfg->n_envs;
+  E.substeps = cfg->substeps;
+  E.H = cfg->episode_len;
+  E.dt = cfg->dt_control;
+  E.h = cfg->dt_control / (float)cfg->substeps;
+  E.key0 = (uint32_t)(cfg->seed & 0xffffffffu);
+  E.key1 = (uint32_t)(cfg->seed >> 32);
+  E.flags = cfg->flags;
+  E.env_offset = cfg->env_offset;
+  e->global_step = 0;
+  *out = e;
+  return AUV_OK;
+}
+
+int auv_destroy(auv_env* env) {
+  delete env;
+  return AUV_OK;
+}
+
+int64_t auv_get_global_step(const auv_env* env) { return env ? env->global_step : -1; }
+
+int auv_set_global_step(auv_env* env, int64_t step) {
+  if (!env) return set_error(AUV_EINVAL, "auv_set_global_step: NULL handle");
+  if (step < 0) return set_error(AUV_EINVAL, "auv_set_global_step: negative step");
+  env->global_step = step;
+  return AUV_OK;
+}
+
+int auv_reset(auv_env* env, void* stream) {
+  if (!env) return set_error(AUV_EINVAL, "auv_reset: NULL handle");
+  const int n = env->E.n;
+  hipLaunchKernelGGL(k_reset, dim3((n + 255) / 256), dim3(256), 0, (hipStream_t)stream, env->veh, env->E);
+  if (int rc = check_launch("auv_reset")) return rc;
+  env->global_step = 0;
+  return AUV_OK;
+}
+
+static int launch_env_loop(auv_env* env, int T, int mode, const StepOut& O, hipStream_t s) {
+  const int G = groups_of(env->E.n);
+  const uint32_t g0 = (uint32_t)(env->global_step & 0xffffffffu);
+  if (mode == AUV_ACT_EXTERNAL)
+    hipLaunchKernelGGL(k_env_loop<true>, dim3(G), dim3(64), 0, s, env->veh, env->E, T, g0, O);
+  else
+    hipLaunchKernelGGL(k_env_loop<false>, dim3(G), dim3(64), 0, s, env->veh, env->E, T, g0, O);
+  return check_launch("environment loop");
+}
+
+int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_t* done,
+             float* stats, float* stats_work, void* stream) {
+  if (!env) return set_error(AUV_EINVAL, "auv_step: NULL handle");
+  if (mode != AUV_ACT_EXTERNAL && mode != AUV_ACT_RANDOM)
+    return set_error(AUV_EINVAL, "auv_step: mode %d not supported (external or random; use auv_rollout for policy modes)", mode);
+  if (mode == AUV_ACT_EXTERNAL && (!actions || !aligned16(actions)))
+    return set_error(AUV_EINVAL, "auv_step: external mode needs a 16-byte aligned actions buffer");
+  if ((stats == nullptr) != (stats_work == nullptr))
+    return set_error(AUV_EINVAL, "auv_step: stats and stats_work must be given together");
+  StepOut O{};
+  O.act = const_cast<float*>(actions);
+  O.reward = reward;
+  O.done_u8 = done;
+  O.stats_work = stats_work;
+  hipStream_t s = (hipStream_t)stream;
+  if (int rc = launch_env_loop(env, 1, mode, O, s)) return rc;
+  if (stats)
+    if (int rc = launch_stats_reduce(stats_work, 1, groups_of(env->E.n), stats, s)) return rc;
+  env->global_step += 1;
+  return AUV_OK;
+}
+
+int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const auv_mlp* value,
+                const auv_rollout_buffers* rb, void* stream) {
+  if (!env) return set_error(AUV_EINVAL, "auv_rollout: NULL handle");
+  if (T < 1) return set_error(AUV_EINVAL, "auv_rollout: T must be >= 1, got %d", T);
+  if ((int64_t)T * env->E.n * 23 > ((int64_t)1 << 40))
+    return set_error(AUV_EINVAL, "auv_rollout: T * N too large");
+  auv_rollout_buffers none{};
+  if (!rb) rb = &none;
+  if ((rb->stats == nullptr) != (rb->stats_work == nullptr))
+    return set_error(AUV_EINVAL, "auv_rollout: stats and stats_work must be given together");
+  const void* outs[10] = {rb->obs, rb->act, rb->logp, rb->value, rb->reward, rb->done,
+                          rb->last_value, rb->traj_state, rb->stats, rb->stats_work};
+  for (int k = 0; k < 10; ++k)
+    if (outs[k] && !aligned16(outs[k])) return set_error(AUV_EINVAL, "auv_rollout: output buffer %d not 16-byte aligned", k);
+  hipStream_t s = (hipStream_t)stream;
+  if (mode == AUV_ACT_EXTERNAL || mode == AUV_ACT_RANDOM) {
+    if (mode == AUV_ACT_EXTERNAL && !rb->act)
+      return set_error(AUV_EINVAL, "auv_rollout: external mode reads actions from rbufs->act");
+    if (policy || value || rb->logp || rb->value || rb->last_value)
+      return set_error(AUV_EINVAL, "auv_rollout: networks, logp and value outputs need a policy mode");
+    StepOut O{};
+    O.obs = rb->obs;
+    O.act = rb->act;
+    O.reward = rb->reward;
+    O.done = rb->done;
+    O.traj = rb->traj_state;
+    O.stats_work = rb->stats_work;
+    if (int rc = launch_env_loop(env, T, mode, O, s)) return rc;
+  } else if (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE) {
+    if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
+  } else {
+    return set_error(AUV_EINVAL, "auv_rollout: unknown mode %d", mode);
+  }
+  if (rb->stats)
+    if (int rc = launch_stats_reduce(rb->stats_work, T, groups_of(env->E.n), rb->stats, s)) return rc;
+  env->global_step += T;
+  return AUV_OK;
+}
+
+int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value, const float* done,
+            const float* last_value, float gamma, float lambda, float* adv, float* ret, void* stream) {
+  if (T < 1 || n_envs < 1) return set_error(AUV_EINVAL, "auv_gae: T and n_envs must be >= 1");
+  const void* p[6] = {reward, value, done, last_value, adv, ret};
+  for (int k = 0; k < 6; ++k)
+    if (!p[k] || !aligned16(p[k])) return set_error(AUV_EINVAL, "auv_gae: buffer %d NULL or misaligned", k);
+  if (!std::isfinite(gamma) || !std::isfinite(lambda))
+    return set_error(AUV_EINVAL, "auv_gae: gamma and lambda must be finite");
+  hipLaunchKernelGGL(k_gae, dim3((n_envs + 255) / 256), dim3(256), 0, (hipStream_t)stream, T, n_envs,
+                     reward, value, done, last_value, gamma, gamma * lambda, adv, ret);
+  return check_launch("auv_gae");
+}
+
+int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float* out, void* stream) {
+  if (!net || !obs || !out) return set_error(AUV_EINVAL, "auv_mlp_forward: NULL argument");
+  if (n_envs < 1) return set_error(AUV_EINVAL, "auv_mlp_forward: n_envs must be >= 1");
+  if (!aligned16(obs) || !aligned16(out)) return set_error(AUV_EINVAL, "auv_mlp_forward: misaligned buffer");
+  return launch_mlp_forward(net, n_envs, obs, out, (hipStream_t)stream);
+}
+
+}  // extern "C"

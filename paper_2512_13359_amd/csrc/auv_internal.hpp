@@ -1,0 +1,46 @@
+// Host-side internals shared by the translation units of libauv.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/auv.h"
+#include "auv_device.hpp"
+
+struct auv_env {
+  auv_config cfg;
+  auv::VehArgs veh;
+  auv::EnvArgs E;
+  int64_t global_step;
+};
+
+namespace auv {
+
+// Per-step output pointers of the environment loop; any may be null.
+struct StepOut {
+  float* obs;          // [23][T][N] observation each action was chosen on
+  float* act;          // [8][T][N] action before clipping (input in external mode)
+  float* reward;       // [T][N]
+  float* done;         // [T][N] as 0 / 1
+  uint8_t* done_u8;    // [N] (single-step form)
+  float* traj;         // [13][T+1][N]
+  float* stats_work;   // [3][T][G] per-group partial sums
+};
+
+int set_error(int code, const char* fmt, ...);
+bool aligned16(const void* p);
+int check_launch(const char* what);
+
+inline int groups_of(int n) { return (n + 63) / 64; }
+
+// launches implemented in auv_policy.hip
+int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy,
+                          const auv_mlp* value, const auv_rollout_buffers* rb, hipStream_t s);
+int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, hipStream_t s);
+int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s);
+
+}  // namespace auv
