@@ -28,6 +28,18 @@ struct EnvArgs {
   uint32_t key0, key1, flags, env_offset;
 };
 
+// Per-step output pointers of the environment loops; any may be null.
+struct StepOut {
+  float* obs;          // [23][T][N] observation each action was chosen on
+  float* act;          // [8][T][N] action before clipping (input in external mode)
+  float* logp;         // [T][N] log-prob of the sampled action
+  float* reward;       // [T][N]
+  float* done;         // [T][N] as 0 / 1
+  uint8_t* done_u8;    // [N] (single-step form)
+  float* traj;         // [13][T+1][N]
+  float* stats_work;   // [3][T][G] per-group partial sums
+};
+
 constexpr uint32_t F_DR = 1, F_CURRENT = 2, F_LISSAJOUS = 4, F_STAGGER = 8;
 constexpr int OBS = 23, ACT = 8, NS = 13, NP = 24;
 

@@ -60,40 +60,18 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
                                                  StepOut O) {
   const int lane = threadIdx.x;
   const int i = blockIdx.x * 64 + lane;
-  const int n = E.n;
-  const size_t N = (size_t)n, TN = (size_t)T * N;
-  const bool valid = i < n;
+  const size_t N = (size_t)E.n, TN = (size_t)T * N;
+  const bool valid = i < E.n;
   const uint32_t gid = E.env_offset + (uint32_t)i;
-  const int G = gridDim.x, g = blockIdx.x;
-
-  State x;
-  Params P;
-  int ep = 0;
-  uint32_t episode = 0;
-  float obs[OBS];
-  if (valid) {
-    load_state(E.state, n, i, x);
-    load_params(E.params, n, i, P);
-    ep = E.ep_step[i];
-    episode = E.episode[i];
-#pragma unroll
-    for (int k = 0; k < OBS; ++k) obs[k] = E.obs[k * n + i];
-  } else {  // idle lanes step a harmless dummy vehicle
-    x = State{{0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}};
-    P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
-#pragma unroll
-    for (int k = 0; k < OBS; ++k) obs[k] = 0.0f;
-  }
-  Model M;
-  make_model(V, P, M);
-  bool dirty = false;
-  if (O.traj && valid) store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, x);
+  Lane L;
+  lane_load(V, E, i, valid, L);
+  if (O.traj && valid) store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, L.x);
 
   for (int t = 0; t < T; ++t) {
     const size_t ti = (size_t)t * N + (size_t)i;
     if (O.obs && valid) {
 #pragma unroll
-      for (int k = 0; k < OBS; ++k) O.obs[k * TN + ti] = obs[k];
+      for (int k = 0; k < OBS; ++k) O.obs[k * TN + ti] = L.obs[k];
     }
     float a[ACT];
     if (EXTERNAL) {
@@ -111,58 +89,12 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
         for (int k = 0; k < ACT; ++k) O.act[k * TN + ti] = a[k];
       }
     }
-    float u[ACT], usq = 0.0f;
-#pragma unroll
-    for (int k = 0; k < ACT; ++k) {
-      u[k] = fminf(fmaxf(a[k], -1.0f), 1.0f);
-      usq += u[k] * u[k];
-    }
-    float tau[6];
-    wrench(V, u, tau);
-    for (int s = 0; s < E.substeps; ++s) rk4(V, M, P.cw, tau, E.h, x);
-    ep += 1;
-    float pr[3], qr[4], dist, theta;
-    reference(E, P, ep, pr, qr);
-    observe(x, pr, qr, obs, dist, theta);
-#pragma unroll
-    for (int k = 0; k < ACT; ++k) obs[15 + k] = u[k];
-    const float reward = -dist - 0.5f * theta - 0.01f * usq;
-    const bool done = (ep == E.H);
-    if (O.stats_work) {
-      const float sr = wave_sum(valid ? reward : 0.0f);
-      const float sd = wave_sum((valid && done) ? 1.0f : 0.0f);
-      const float sp = wave_sum(valid ? dist : 0.0f);
-      if (lane == 0) {
-        O.stats_work[((size_t)0 * T + t) * G + g] = sr;
-        O.stats_work[((size_t)1 * T + t) * G + g] = sd;
-        O.stats_work[((size_t)2 * T + t) * G + g] = sp;
-      }
-    }
-    if (valid) {
-      if (O.reward) O.reward[ti] = reward;
-      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
-      if (O.done_u8) O.done_u8[i] = done ? 1 : 0;
-    }
-    if (done) {
-      episode += 1u;
-      reset_draws(E, gid, episode, x, P);
-      make_model(V, P, M);
-      ep = 0;
-      reference(E, P, ep, pr, qr);
-      observe(x, pr, qr, obs, dist, theta);
-#pragma unroll
-      for (int k = 15; k < OBS; ++k) obs[k] = 0.0f;
-      dirty = true;
-    }
-    if (O.traj && valid) store_state(O.traj + (size_t)(t + 1) * N, (size_t)(T + 1) * N, (size_t)i, x);
+    float reward, dist;
+    bool done;
+    lane_step(V, E, gid, a, L, reward, done, dist);
+    lane_outputs(O, T, N, t, i, valid, lane, blockIdx.x, gridDim.x, reward, done, dist, L.x);
   }
-  if (!valid) return;
-  store_state(E.state, N, (size_t)i, x);
-  E.ep_step[i] = ep;
-  E.episode[i] = episode;
-#pragma unroll
-  for (int k = 0; k < OBS; ++k) E.obs[k * n + i] = obs[k];
-  if (dirty) store_params(E.params, n, i, P);
+  if (valid) lane_store(E, i, L);
 }
 
 __global__ __launch_bounds__(256) void k_stats_reduce(const float* __restrict__ work, int T, int G,

@@ -10,6 +10,7 @@
 
 #include "../../include/auv.h"
 #include "auv_device.hpp"
+#include "env_lane.hpp"
 
 struct auv_env {
   auv_config cfg;
@@ -19,17 +20,6 @@ struct auv_env {
 };
 
 namespace auv {
-
-// Per-step output pointers of the environment loop; any may be null.
-struct StepOut {
-  float* obs;          // [23][T][N] observation each action was chosen on
-  float* act;          // [8][T][N] action before clipping (input in external mode)
-  float* reward;       // [T][N]
-  float* done;         // [T][N] as 0 / 1
-  uint8_t* done_u8;    // [N] (single-step form)
-  float* traj;         // [13][T+1][N]
-  float* stats_work;   // [3][T][G] per-group partial sums
-};
 
 int set_error(int code, const char* fmt, ...);
 bool aligned16(const void* p);

@@ -108,20 +108,21 @@ def test_c2_full_size_sampled_envs():
 
 
 def test_one_step_from_identical_state():
-    """One control step from bit-identical fp32 states (random poses, velocities and
-    randomisation), external actions including out-of-range ones: 1e-4 per component."""
+    """One control step from the same seeded fp32 states on both sides (random poses and
+    velocities; each side's own randomisation draws from the same seed), external seeded
+    actions including out-of-range ones: 1e-4 per component."""
     require_gpu()
     n = 3000 + 5
     cfg = W.config("c4", n_envs=n)
     announce(f"one step from identical state n={n} (c4 model, 4 substeps)")
-    g, _ = _reset_pair(cfg)
+    g, o = _reset_pair(cfg)
     x0 = W.random_states(n, seed=3)
+    ep0 = ((np.arange(n) * 7) % 499).astype(np.int32)
     g.state.copy_(torch.from_numpy(x0))
-    g.ep_step.copy_(torch.from_numpy((np.arange(n) * 7) % 499).to(torch.int32))
+    g.ep_step.copy_(torch.from_numpy(ep0))
+    o.x = x0.astype(np.float64)
+    o.ep_step = ep0.astype(np.int64)
     acts = np.random.default_rng(5).uniform(-1.3, 1.3, (8, n)).astype(np.float32)
-    params = host(g.params)
-    o = oracle_env(cfg)
-    o.load(x0, params, host(g.ep_step), host(g.episode), np.zeros((8, n)))
     reward, done, _ = g.step(W.MODE_EXTERNAL, torch.from_numpy(acts).cuda())
     r_o, d_o, _, obs_o = o.step(acts.astype(np.float64))
     x = host(g.state)

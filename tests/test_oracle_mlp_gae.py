@@ -139,3 +139,40 @@ def test_gae_equals_truncated_sum_definition():
                     break
                 f *= g * lam
             assert adv[t, i] == pytest.approx(s, abs=1e-10)
+
+
+def test_mlp_candidates_reduce_to_forward_without_ambiguity():
+    net = W.mlp_weights(8, W.POLICY_SEED)
+    x = np.random.default_rng(7).normal(size=(23, 300))
+    y, cands = omlp.mlp_candidates(x, net, 0.0)
+    assert np.array_equal(y, omlp.mlp_forward(x, net)) and cands == {}
+    y, cands = omlp.mlp_candidates(x, net, 1e-6)
+    assert 0 < len(cands) < 300
+    for c, ys in cands.items():
+        assert ys.shape[0] == 8 and ys.shape[1] >= 2
+        # the plain forward is one of the valid outputs (up to fp64 summation order)
+        assert np.min(np.max(np.abs(ys - y[:, c:c + 1]), axis=0)) < 1e-12
+    assert np.all(omlp.nearest_valid_error(y, x, net, 1e-6) < 1e-12)
+
+
+def test_mlp_candidates_contain_both_roundings_of_a_tie():
+    """Hidden-1 value exactly at a bf16 midpoint (bias makes tanh land there): both
+    roundings must appear among the valid outputs."""
+    import math
+    W1 = np.zeros((256, 23)); W1[5, 0] = 1.0
+    W2 = np.zeros((256, 256)); W2[9, 5] = 1.0
+    W3 = np.zeros((8, 256)); W3[2, 9] = 1.0
+    net = _net(8, W1, W2, W3)
+    mid = 0.5 + 2.0 ** -9                       # midpoint between bf16 0.5 and 0.50390625
+    net["b1"][:] = 0.0
+    obs = np.zeros((23, 1))
+    obs[0, 0] = 0.0
+    net["b1"][5] = np.float32(math.atanh(mid))  # tanh(b1) ~ mid (within fp32 of b1)
+    h = math.tanh(float(net["b1"][5]))
+    assert abs(h - mid) < 1e-7
+    y, cands = omlp.mlp_candidates(obs, net, 1e-6)
+    assert 0 in cands
+    outs = sorted(set(np.round(cands[0][2], 12)))
+    want = sorted({round(math.tanh(0.5), 12), round(math.tanh(0.50390625), 12)})
+    got_h2 = [float(torch.tensor(v, dtype=torch.float64).to(torch.bfloat16).double()) for v in want]
+    assert len(outs) == 2 and np.allclose(outs, got_h2)
