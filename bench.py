@@ -1,0 +1,196 @@
+"""Benchmark of the batched AUV rollout on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
+
+One bench step is one auv_rollout launch over the whole workload: for the headline
+workload (16384 envs x 2000 control steps, 4 RK4 substeps per 0.04 s step, Lissajous
+references, randomisation and current, bf16 MFMA policy mean, per-step batch statistics)
+that is 32.8 M env-steps of physics + policy.  Inputs (env state, weights) are resident
+in HBM before the timed region.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "env-steps/sec (physics+policy) at 16384 envs; % of FP32/MFMA roofline"
+
+# Algorithmic work per env-step of the headline workload (formula counts, padding
+# excluded): bf16 MFMA FLOP of the 23-256-256-8 MLP, fp32 VALU FLOP of physics +
+# observation + reward, transcendental ops (512 tanh = exp + reciprocal each).
+F_MFMA = 2 * (23 * 256 + 256 * 256 + 256 * 8)      # 146,944
+F_VALU = 4815
+N_TRANS = 1024
+# MI355X peaks: published dense bf16 MFMA and fp32 vector rates; transcendentals
+# (v_exp_f32, v_rcp_f32) issue at half the fp32 lane rate on gfx950 (8 cycles per wave64
+# instruction, measured): 256 CU x 4 SIMD x 16 lanes x 2.4 GHz / 2.
+P_MFMA = 2.5e15
+P_VALU = 157.3e12
+P_TRANS = 256 * 4 * 16 * 2.4e9 / 2
+HBM_PEAK = 8.0e12
+
+KERNEL_SOURCES = ["auv_device.hpp", "env_lane.hpp", "mlp_mfma.hpp", "auv_policy.hip", "auv_env.hip"]
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_policy_rollout_c4_counters.txt")
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2512_13359_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the rollout kernel from the committed counter summary,
+    or None if it is missing or was taken on different kernel sources."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    kv = {}
+    for line in open(COUNTERS_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg: dict, n_steps: int) -> dict:
+    """The fp64 oracle on a bounded sample of the same workload (host cores)."""
+    import threadpoolctl
+
+    import workloads as W
+    from oracle import env as oenv
+
+    n = cfg["n_envs"]
+    cores = len(os.sched_getaffinity(0))
+    with threadpoolctl.threadpool_limits(limits=cores):
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        pol = W.mlp_weights(8, W.POLICY_SEED)
+        e = oenv.Env(cfg, W.VEHICLE, W.ALLOC)
+        e.reset()
+        t0 = time.perf_counter()
+        e.rollout(n_steps, cfg["mode"], policy=pol)
+        dt = time.perf_counter() - t0
+    return {"value": n * n_steps / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} envs x {n_steps} control steps of the same workload (fp64 NumPy, "
+                      f"{dt:.1f} s)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="c4", choices=["c3", "c4"])
+    ap.add_argument("--cpu-steps", type=int, default=10, help="oracle control steps for the CPU baseline (0: skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run one plain device copy of MIB MiB (counter calibration) and exit")
+    args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        src = torch.ones(args.calibrate_copy * (1 << 18), device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes": src.numel() * 4}))
+        return 0
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (the rollout has no cross-GPU step to measure); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, upload_mlp
+
+    torch.cuda.set_device(0)
+    cfg = W.config(args.workload)
+    n, T = cfg["n_envs"], cfg["T"]
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.reset()
+    pol = upload_mlp(W.mlp_weights(8, W.POLICY_SEED))
+    bufs = env.rollout_buffers(T, record=("stats",))
+    for _ in range(args.warmup):
+        env.rollout(T, cfg["mode"], policy=pol, bufs=bufs)
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record()
+        env.rollout(T, cfg["mode"], policy=pol, bufs=bufs)
+        ends[k].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_s = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / args.steps * 1e-3
+    stats = bufs["stats"].cpu().numpy()
+    assert stats.shape == (3, T) and (stats == stats).all(), "non-finite statistics"
+
+    env_steps = n * T
+    value = env_steps * args.steps / wall
+    per_env_step_s = launch_s / env_steps
+    t_lb = F_MFMA / P_MFMA + F_VALU / P_VALU + N_TRANS / P_TRANS
+    f_alg = F_MFMA + F_VALU
+    traffic = recorded_traffic()
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "env-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+bf16",
+        "data": "synthetic (seeded Philox resets, seeded N(0,1/fan_in) bf16 weights)",
+        "config": {
+            "workload": f"{args.workload}: {n} envs x {T} control steps, {cfg['substeps']} RK4 substeps per "
+                        f"{cfg['dt_control']} s step, randomisation + current"
+                        + (", Lissajous references" if cfg["flags"] & W.FLAG_LISSAJOUS else "")
+                        + ", bf16 MFMA policy 23-256-256-8 (mean), batch statistics",
+            "n_envs": n, "control_steps": T, "substeps": cfg["substeps"],
+            "env_steps_per_launch": env_steps,
+        },
+        "roofline": {
+            "bound": "alu",
+            "achieved": f_alg / per_env_step_s / 1e12,
+            "peak": f_alg / t_lb / 1e12,
+            "unit": "TFLOP/s",
+            "frac": t_lb / per_env_step_s,
+            "traffic": traffic,
+            "kernel": "k_policy_rollout",
+            "launch_ms": launch_s * 1e3,
+            "per_env_step": {"mfma_flop": F_MFMA, "valu_flop": F_VALU, "trans_ops": N_TRANS},
+            "unit_utilisation": {
+                "mfma": F_MFMA / per_env_step_s / P_MFMA,
+                "valu": F_VALU / per_env_step_s / P_VALU,
+                "trans": N_TRANS / per_env_step_s / P_TRANS,
+            },
+            "max_of_units_frac": max(F_MFMA / P_MFMA, F_VALU / P_VALU, N_TRANS / P_TRANS) / per_env_step_s,
+        },
+    }
+    if args.cpu_steps > 0:
+        line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -4,17 +4,17 @@
  *
  * What is computed: many independent copies of one vehicle model stepped in a single
  * batch, each with its own random initial conditions and randomisation parameters
- * (paper Sec. III-A), observed through body-frame errors (Sec. III-B1) and driven by a
- * policy network (Sec. II-A, IV).  One control step of one environment:
+ * (paper Sec. IV-A), observed through body-frame errors (Sec. IV-B) and driven by a
+ * policy network (Sec. III-A, V).  One control step of one environment:
  *   1. action a (caller's, Philox-uniform, or the policy MLP's mean / Gaussian sample);
  *      u = clip(a, -1, 1); thrust f = f_max u; body wrench tau = T f (6x8 allocation)
  *   2. `substeps` classic RK4 substeps of the Fossen 6-DOF equations of motion (the model
- *      of Sec. III-C) with added mass, Coriolis, linear + quadratic damping, restoring
- *      forces with the buoyancy centre offset (Sec. V-A) and a constant ocean current
+ *      of Sec. IV-D, Eq. 8) with added mass, Coriolis, linear + quadratic damping, restoring
+ *      forces with the buoyancy centre offset (Sec. VI-A) and a constant ocean current
  *   3. episode step + 1; reference pose (episode goal, or Lissajous + yaw ramp)
  *   4. observation [R^T(p_ref - p), R_err[:,0], R_err[:,1], v, omega, u], R_err = R^T R_ref
- *   5. reward -|R^T(p_ref - p)| - 0.5 theta_err - 0.01 |u|^2 (shape of Sec. III-B3)
- *   6. at the episode length: automatic reset with fresh Philox draws (Sec. IV-A1)
+ *   5. reward -|R^T(p_ref - p)| - 0.5 theta_err - 0.01 |u|^2 (shape of Sec. IV-B, Eqs. 2-5)
+ *   6. at the episode length: automatic reset with fresh Philox draws (Sec. V-A)
  *
  * Conventions: world NED, body forward-right-down with origin at the centre of gravity,
  * Hamilton quaternion (w, x, y, z) body -> world.  State rows: p(3) q(4) v(3) omega(3).

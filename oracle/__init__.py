@@ -12,12 +12,12 @@ It shares no code with the HIP path: its only inputs are the seeded data in
 
 Modules
   rng       Philox4x32-10, uniform / affine maps, Shoemake rotations, Box-Muller
-  dynamics  Fossen 6-DOF equations of motion (paper Sec. III-C, the model behind the
+  dynamics  Fossen 6-DOF equations of motion (paper Sec. IV-D, Eq. 8, the model behind the
             MPC baseline) and classic RK4 with quaternion renormalisation
   env       reset / domain randomisation, references, observation, reward, auto-reset,
-            batch statistics, rollouts (paper Sec. III-A, III-B, IV-A)
+            batch statistics, rollouts (paper Sec. IV-A, IV-B, IV-C, V-A)
   mlp       bf16 round-to-nearest-even, policy / value MLP forward, Gaussian log-prob
-  gae       generalised advantage estimation (the PPO learner of Sec. II-A)
+  gae       generalised advantage estimation (the PPO learner of Sec. III-A)
 
 Every function is pinned by a ``-m "not gpu"`` test against closed forms, invariants,
 special cases or an independent library; see the test files under ``tests/``.

@@ -1,10 +1,10 @@
 """Fossen 6-DOF equations of motion and RK4 (oracle side, float64).
 
 The paper's MPC baseline steps the nonlinear 6-DOF equations of motion of Fossen
-(Sec. III-C, "Model Predictive Controller Baseline"); the rollout uses the same model
+(Sec. IV-D, Eq. 8, "Model Predictive Controller Baseline"); the rollout uses the same model
 with added mass, Coriolis and centripetal terms, linear and quadratic damping,
 restoring forces from weight and buoyancy with the centre of buoyancy offset from the
-centre of gravity (the offset the paper names as its main sim-to-real gap, Sec. V-A),
+centre of gravity (the offset the paper names as its main sim-to-real gap, Sec. VI-A),
 and a constant irrotational ocean current.
 
 Conventions: world frame NED (z down), body frame forward-right-down with its origin at

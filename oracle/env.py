@@ -2,12 +2,12 @@
 auto-reset, batch statistics and rollouts (oracle side, float64).
 
 Paper passages: many independent environments in one batch, each with its own random
-initial conditions and randomisation parameters (Sec. III-A); the error-based
-observation in the body frame with body velocities (Sec. III-B1), here in its 23-value
+initial conditions and randomisation parameters (Sec. IV-A); the error-based
+observation in the body frame with body velocities (Sec. IV-B), here in its 23-value
 form with two columns of the error rotation matrix (the rotation-matrix attitude error
-converged fastest, Sec. IV-A3) and the previous action; the reward shape of Sec. III-B3
-(position error, attitude error, action effort), here -|dp| - 0.5 theta - 0.01 |u|^2;
-a random reference per episode (Sec. IV-A1); fixed-length episodes with automatic reset.
+converged fastest, Sec. V-A) and the previous action; the reward shape of Sec. IV-B
+(Eqs. 2-5: position error, attitude error, action effort), here -|dp| - 0.5 theta - 0.01 |u|^2;
+a random reference per episode (Sec. V-A); fixed-length episodes with automatic reset.
 
 Step order for env i at control step t (the paper gives none; this is the reading):
   1. action a (caller's, Philox uniform, or policy mean / sample); u = clip(a, -1, 1);
@@ -39,7 +39,7 @@ F32_PI = float(np.float32(math.pi))
 
 # Reset draw map: word index -> (lo, span) of an fp32 affine draw lo + span*u.
 # Ranges: mass / added mass / damping scales U[0.8, 1.2]; current U[-0.3, 0.3] m/s per
-# axis; positions U[-2, 2] m (the paper's reference range, Sec. IV-A1); Lissajous
+# axis; positions U[-2, 2] m (the paper's reference range, Sec. V-A); Lissajous
 # amplitude U[0.5, 2] m, frequency U[0.02, 0.1] Hz, phase U[0, 2 pi); yaw rate
 # U[-0.1, 0.1] rad/s; initial reference yaw U[-pi, pi).
 R_SCALE = (0.8, 0.4)

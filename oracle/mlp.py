@@ -1,6 +1,6 @@
 """Policy / value MLP forward and Gaussian log-probability (oracle side).
 
-The paper trains Flax policy and value networks with PPO (Sec. II-A, IV) without giving
+The paper trains Flax policy and value networks with PPO (Sec. III-A, V) without giving
 their sizes; the workloads here use 23 -> 256 -> 256 -> n_out with tanh hidden layers and
 a linear output (the Gaussian mean for the policy, V for the value net).
 

@@ -6,7 +6,7 @@ multiplications with the published multipliers, xor-ed with the key, and a Weyl 
 of the key between rounds.  Written here from that published definition in plain
 Python integers (scalar form) and in NumPy uint64 (vector form).
 
-The paper randomises every environment independently at reset (Sec. III-A, III-C);
+The paper randomises every environment independently at reset (Sec. IV-A, IV-C);
 keying every draw by (seed, env id, episode or step, tag, block) makes each draw
 reproducible in isolation, which is what lets the GPU path match it bit for bit.
 

@@ -9,7 +9,7 @@ Vehicle numbers: the 6-DOF vehicle used by the benchmark workloads (mass, inerti
 added mass, linear and quadratic damping, weight, buoyancy, centre of buoyancy 0.02 m
 above the centre of gravity, 8 thrusters of at most 40 N).  The paper names its vehicle
 (a BlueROV2 Heavy) and says thrust commands reach the thrusters through an allocation
-matrix (Sec. IV-B, real-world experiments) but gives neither the geometry nor the
+matrix (Sec. V-B, real-world experiments) but gives neither the geometry nor the
 matrix, so the thruster geometry below is this project's constant.
 """
 from __future__ import annotations
