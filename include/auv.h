@@ -132,7 +132,7 @@ typedef struct {
   float* stats_work; /* workspace for stats: auv_stats_work_floats(N, T) floats */
 } auv_rollout_buffers;
 
-/* Number of floats of the stats workspace for N envs and T steps (3 T ceil(N/64)). */
+/* Number of floats of the stats workspace for N envs and T steps (3 T 4 ceil(N/64)). */
 int64_t auv_stats_work_floats(int32_t n_envs, int32_t T);
 
 /* Validates the configuration and buffers and creates a handle.  Makes no GPU call and

@@ -37,7 +37,7 @@ struct StepOut {
   float* done;         // [T][N] as 0 / 1
   uint8_t* done_u8;    // [N] (single-step form)
   float* traj;         // [13][T+1][N]
-  float* stats_work;   // [3][T][G] per-group partial sums
+  float* stats_work;   // [3][G][T] per-group partial sums
 };
 
 constexpr uint32_t F_DR = 1, F_CURRENT = 2, F_LISSAJOUS = 4, F_STAGGER = 8;
@@ -228,6 +228,31 @@ __device__ __forceinline__ void wrench(const VehArgs& V, const float u[8], float
   }
 }
 
+// ------------------------------------------------------ sine and cosine in turns --
+// sin(2 pi f) for |f| <= 1/4 turn: Taylor series of sin y, y = 2 pi f in [-pi/2, pi/2],
+// through y^13 (truncation below 7e-10, under fp32 rounding).
+__device__ __forceinline__ float sin_quarter(float f) {
+  const float y = 6.28318530717958648f * f;
+  const float y2 = y * y;
+  float p = 1.0f / 6227020800.0f;
+  p = __builtin_fmaf(p, y2, -1.0f / 39916800.0f);
+  p = __builtin_fmaf(p, y2, 1.0f / 362880.0f);
+  p = __builtin_fmaf(p, y2, -1.0f / 5040.0f);
+  p = __builtin_fmaf(p, y2, 1.0f / 120.0f);
+  p = __builtin_fmaf(p, y2, -1.0f / 6.0f);
+  return __builtin_fmaf(p * y2, y, y);
+}
+
+// sin and cos of 2 pi x for x in turns: exact reduction to r = x - rint(x) in
+// [-1/2, 1/2], then sin(2 pi r) = sin_quarter(r) or sin_quarter(+-1/2 - r) and
+// cos(2 pi r) = sin_quarter(1/4 - |r|).
+__device__ __forceinline__ void sincos_turns(float x, float* s, float* c) {
+  const float r = x - rintf(x);
+  const float a = fabsf(r);
+  *s = sin_quarter(a > 0.25f ? copysignf(0.5f, r) - r : r);
+  *c = sin_quarter(0.25f - a);
+}
+
 // --------------------------------------------------------------- reset draws --------
 // 32 words from blocks (gid, episode, 0, 0..7).  Word map: 0-2 scales, 3-5 current,
 // 6-8 p0, 9-11 q0 (Shoemake), 12-14 p_goal, 15-17 q_goal, 18-20 amplitude,
@@ -268,16 +293,21 @@ __device__ __forceinline__ void reset_draws(const EnvArgs& E, uint32_t gid, uint
 }
 
 // ---------------------------------------------------- reference / obs / reward ------
+// Lissajous: p_goal + A sin(2 pi f t + phase), yaw psi0 + psi_dot t, evaluated in turns
+// (f t + phase / 2 pi and psi / 4 pi).
 __device__ __forceinline__ void reference(const EnvArgs& E, const Params& P, int ep_step,
                                           float pr[3], float qr[4]) {
   if (E.flags & F_LISSAJOUS) {
     const float t = (float)ep_step * E.dt;
+    constexpr float INV_2PI = 0.159154943091895336f, INV_4PI = 0.0795774715459476679f;
 #pragma unroll
-    for (int i = 0; i < 3; ++i)
-      pr[i] = P.pg[i] + P.amp[i] * sinf(6.28318530717958648f * P.freq[i] * t + P.phase[i]);
-    const float psi = P.yaw0 + P.yaw_rate * t;
+    for (int i = 0; i < 3; ++i) {
+      float s, c;
+      sincos_turns(__builtin_fmaf(P.freq[i], t, P.phase[i] * INV_2PI), &s, &c);
+      pr[i] = __builtin_fmaf(P.amp[i], s, P.pg[i]);
+    }
     float s, c;
-    sincosf(0.5f * psi, &s, &c);
+    sincos_turns(__builtin_fmaf(P.yaw_rate, t, P.yaw0) * INV_4PI, &s, &c);
     qr[0] = c; qr[1] = 0.0f; qr[2] = 0.0f; qr[3] = s;
   } else {
 #pragma unroll

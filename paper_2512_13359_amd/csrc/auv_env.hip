@@ -64,6 +64,7 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
   const bool valid = i < E.n;
   const uint32_t gid = E.env_offset + (uint32_t)i;
   Lane L;
+  StatsBuf SB{};
   lane_load(V, E, i, valid, L);
   if (O.traj && valid) store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, L.x);
 
@@ -92,19 +93,21 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
     float reward, dist;
     bool done;
     lane_step(V, E, gid, a, L, reward, done, dist);
-    lane_outputs(O, T, N, t, i, valid, lane, blockIdx.x, gridDim.x, reward, done, dist, L.x);
+    lane_outputs(O, SB, T, N, t, i, valid, lane, blockIdx.x, gridDim.x, reward, done, dist, L.x);
   }
   if (valid) lane_store(E, i, L);
 }
 
+// stats[s][t] = sum over groups g (in order) of work[s][g][t].
 __global__ __launch_bounds__(256) void k_stats_reduce(const float* __restrict__ work, int T, int G,
                                                       float* __restrict__ stats) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= 3 * T) return;
-  const float* p = work + (size_t)j * G;
-  float s = 0.0f;
-  for (int g = 0; g < G; ++g) s += p[g];
-  stats[j] = s;
+  const int s = j / T, t = j - s * T;
+  const float* p = work + (size_t)s * G * T + t;
+  float acc = 0.0f;
+  for (int g = 0; g < G; ++g) acc += p[(size_t)g * T];
+  stats[j] = acc;
 }
 
 // Backward GAE scan, one lane per environment, [T][N] layout (coalesced over envs).
@@ -170,7 +173,7 @@ const char* auv_last_error(void) { return auv::g_err.c_str(); }
 
 int64_t auv_stats_work_floats(int32_t n_envs, int32_t T) {
   if (n_envs <= 0 || T <= 0) return 0;
-  return (int64_t)3 * T * groups_of(n_envs);
+  return (int64_t)3 * T * stats_groups(n_envs);
 }
 
 int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buffers* bufs,
@@ -283,7 +286,7 @@ int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_
   hipStream_t s = (hipStream_t)stream;
   if (int rc = launch_env_loop(env, 1, mode, O, s)) return rc;
   if (stats)
-    if (int rc = launch_stats_reduce(stats_work, 1, groups_of(env->E.n), stats, s)) return rc;
+    if (int rc = launch_stats_reduce(stats_work, 1, groups_of(env->E.n), stats, s)) return rc;   // one partial per wave of 64
   env->global_step += 1;
   return AUV_OK;
 }
@@ -316,13 +319,15 @@ int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const 
     O.traj = rb->traj_state;
     O.stats_work = rb->stats_work;
     if (int rc = launch_env_loop(env, T, mode, O, s)) return rc;
+    if (rb->stats)
+      if (int rc = launch_stats_reduce(rb->stats_work, T, groups_of(env->E.n), rb->stats, s)) return rc;
   } else if (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE) {
     if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
+    if (rb->stats)   // one partial per wave of 16 environments
+      if (int rc = launch_stats_reduce(rb->stats_work, T, stats_groups(env->E.n), rb->stats, s)) return rc;
   } else {
     return set_error(AUV_EINVAL, "auv_rollout: unknown mode %d", mode);
   }
-  if (rb->stats)
-    if (int rc = launch_stats_reduce(rb->stats_work, T, groups_of(env->E.n), rb->stats, s)) return rc;
   env->global_step += T;
   return AUV_OK;
 }

@@ -26,6 +26,8 @@ bool aligned16(const void* p);
 int check_launch(const char* what);
 
 inline int groups_of(int n) { return (n + 63) / 64; }
+// statistics partials: one per wave; the policy rollout has four waves per 64 envs
+inline int stats_groups(int n) { return 4 * groups_of(n); }
 
 // launches implemented in auv_policy.hip
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy,

@@ -4,12 +4,33 @@
 
 #include "auv_internal.hpp"
 #include "mlp_mfma.hpp"
+#include "quad_env.hpp"
 
 namespace auv {
 
-// One workgroup = 4 waves = 64 environments for all T steps.  Wave 0 runs the
-// environments (one lane each, state in registers); all four waves run the MLP on
-// MFMA with their weight slices in registers.  Three barriers per step:
+// Observation features of one environment written by the four lanes of its quad into the
+// layer-1 operand (bf16 element stores; features 23..31 stay zero).
+__device__ __forceinline__ void put_obs_quad(MlpShared& S, int nt, int r, int c, const quad::QObs& o, float v,
+                                             float om, float u0, float u1) {
+  __bf16* xs = reinterpret_cast<__bf16*>(&S.x[0][0]);
+  auto put = [&](int k, float x) {
+    const int g = (k >> 2) & 3, j = 4 * (k >> 4) + (k & 3);
+    xs[((nt * 64 + 16 * g + r) << 3) + j] = (__bf16)x;
+  };
+  if (c < 3) {
+    put(c, o.dpb);
+    put(3 + c, o.c0);
+    put(6 + c, o.c1);
+    put(9 + c, v);
+    put(12 + c, om);
+  }
+  put(15 + 2 * c, u0);
+  put(16 + 2 * c, u1);
+}
+
+// One workgroup = 4 waves = 64 environments for all T steps.  All four waves step their
+// 16 environments with four lanes each (quad layout, quad_env.hpp) and all four run the
+// MLP on MFMA with their weight slices in registers.  Three barriers per step:
 //   obs in LDS -> layer 1 -> hidden-1 in LDS -> layers 2, 3 -> partials in LDS -> physics.
 template <bool SAMPLE>
 __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
@@ -17,71 +38,175 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
                                                            const float* __restrict__ b,
                                                            const float* __restrict__ log_std) {
   __shared__ MlpShared S;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   MlpRegs R;
   mlp_load(w, b, ACT, wave, lane, R, S);
-  const int i = blockIdx.x * 64 + lane;
+  S.x[tid >> 6][lane] = bf16x8{};
+  const quad::QK K = quad::make_qk(lane, V);
+  const int c = K.c;
+  const int slot = lane >> 2;              // environment within this wave's tile
+  const int env = 16 * wave + slot;        // environment within the workgroup
+  const int i = blockIdx.x * 64 + env;
   const bool valid = i < E.n;
   const size_t N = (size_t)E.n, TN = (size_t)T * N;
   const uint32_t gid = E.env_offset + (uint32_t)i;
-  Lane L;
-  float lsd[ACT], sig[ACT];
-  if (wave == 0) {
-    lane_load(V, E, i, valid, L);
-    if (O.traj && valid) store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, L.x);
-    mlp_put_obs(L.obs, lane, S);
-    if (SAMPLE) {
-#pragma unroll
-      for (int k = 0; k < ACT; ++k) { lsd[k] = log_std[k]; sig[k] = expf(lsd[k]); }
-    }
+  const int cv = c < 3 ? c : 0;            // a valid component row for lane 3's loads
+  const quad::QAlloc A = quad::make_alloc(V, c);
+
+  float p, q, v, om, u0, u1;
+  int ep = 0;
+  uint32_t episode = 0;
+  Params P;
+  quad::QObs ob;
+  if (valid) {
+    p = c < 3 ? E.state[cv * N + i] : 0.0f;
+    q = E.state[(c < 3 ? 4 + c : 3) * N + i];
+    v = c < 3 ? E.state[(7 + cv) * N + i] : 0.0f;
+    om = c < 3 ? E.state[(10 + cv) * N + i] : 0.0f;
+    load_params(E.params, E.n, i, P);
+    ep = E.ep_step[i];
+    episode = E.episode[i];
+    ob.dpb = c < 3 ? E.obs[cv * N + i] : 0.0f;
+    ob.c0 = c < 3 ? E.obs[(3 + cv) * N + i] : 0.0f;
+    ob.c1 = c < 3 ? E.obs[(6 + cv) * N + i] : 0.0f;
+    u0 = E.obs[(15 + 2 * c) * N + i];
+    u1 = E.obs[(16 + 2 * c) * N + i];
+  } else {  // idle environments step a harmless dummy vehicle and are never stored
+    p = v = om = u0 = u1 = 0.0f;
+    q = c == 3 ? 1.0f : 0.0f;
+    P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
+    ob = quad::QObs{0, 0, 0};
   }
+  quad::QModel M;
+  quad::QRef F;
+  quad::make_lane_consts(V, K, P, M, F);
+  bool dirty = false;
+  float lsd0 = 0.0f, lsd1 = 0.0f, sig0 = 0.0f, sig1 = 0.0f;
+  if (SAMPLE) {
+    lsd0 = log_std[2 * c];
+    lsd1 = log_std[2 * c + 1];
+    sig0 = expf(lsd0);
+    sig1 = expf(lsd1);
+  }
+  auto store_traj = [&](int t1) {
+    if (O.traj && valid) {
+      const size_t base = (size_t)t1 * N + i, st = (size_t)(T + 1) * N;
+      if (c < 3) {
+        O.traj[c * st + base] = p;
+        O.traj[(7 + c) * st + base] = v;
+        O.traj[(10 + c) * st + base] = om;
+      }
+      O.traj[(c < 3 ? 4 + c : 3) * st + base] = q;
+    }
+  };
+  store_traj(0);
+  StatsBuf SB{};
+  __syncthreads();                          // S.x zeroed, biases staged
+  put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
   __syncthreads();
+  OwnH1 H;
   for (int t = 0; t < T; ++t) {
-    mlp_layer1(R, S, wave, lane);
+    mlp_layer1(R, S, wave, lane, H);
     __syncthreads();
-    mlp_layer23(R, S, wave, lane);
+    mlp_layer23(R, S, wave, lane, H);
     __syncthreads();
-    if (wave == 0) {
-      const size_t ti = (size_t)t * N + (size_t)i;
-      if (O.obs && valid) {
-#pragma unroll
-        for (int k = 0; k < OBS; ++k) O.obs[k * TN + ti] = L.obs[k];
+    const size_t ti = (size_t)t * N + (size_t)i;
+    if (O.obs && valid) {
+      if (c < 3) {
+        O.obs[c * TN + ti] = ob.dpb;
+        O.obs[(3 + c) * TN + ti] = ob.c0;
+        O.obs[(6 + c) * TN + ti] = ob.c1;
+        O.obs[(9 + c) * TN + ti] = v;
+        O.obs[(12 + c) * TN + ti] = om;
       }
-      float a[ACT];
-#pragma unroll
-      for (int k = 0; k < ACT; ++k) a[k] = mlp_out(S, lane, k);
-      if (SAMPLE) {
-        const uint32_t step = gstep0 + (uint32_t)t;
-        const U4 r0 = philox(U4{gid, step, 2u, 0u}, E.key0, E.key1);
-        const U4 r1 = philox(U4{gid, step, 2u, 1u}, E.key0, E.key1);
-        const uint32_t wd[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
-        float lp = 0.0f;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const float rad = sqrtf(-2.0f * logf(u01_open0(wd[2 * k])));
-          float s, c;
-          sincospif(2.0f * u01(wd[2 * k + 1]), &s, &c);
-          const float e0 = rad * c, e1 = rad * s;
-          a[2 * k] += sig[2 * k] * e0;
-          a[2 * k + 1] += sig[2 * k + 1] * e1;
-          lp += (-0.5f * e0 * e0 - lsd[2 * k]) + (-0.5f * e1 * e1 - lsd[2 * k + 1]);
-        }
-        lp -= 4.0f * 1.83787706640934548f;   // 8 * 0.5 * ln(2 pi)
-        if (O.logp && valid) O.logp[ti] = lp;
-      }
-      if (O.act && valid) {
-#pragma unroll
-        for (int k = 0; k < ACT; ++k) O.act[k * TN + ti] = a[k];
-      }
-      float reward, dist;
-      bool done;
-      lane_step(V, E, gid, a, L, reward, done, dist);
-      lane_outputs(O, T, N, t, i, valid, lane, blockIdx.x, gridDim.x, reward, done, dist, L.x);
-      mlp_put_obs(L.obs, lane, S);
+      O.obs[(15 + 2 * c) * TN + ti] = u0;
+      O.obs[(16 + 2 * c) * TN + ti] = u1;
     }
+    // policy output for this lane's two action components (fixed-order partial sums)
+    float a0, a1;
+    {
+      float s0 = S.mu[0][env][2 * c], s1 = S.mu[0][env][2 * c + 1];
+#pragma unroll
+      for (int ww = 1; ww < 4; ++ww) {
+        s0 += S.mu[ww][env][2 * c];
+        s1 += S.mu[ww][env][2 * c + 1];
+      }
+      a0 = S.b3[2 * c] + s0;
+      a1 = S.b3[2 * c + 1] + s1;
+    }
+    if (SAMPLE) {
+      // lane c draws the Box-Muller pair k = c from words (2c, 2c+1): block c / 2
+      const uint32_t step = gstep0 + (uint32_t)t;
+      const U4 r = philox(U4{gid, step, 2u, (uint32_t)(c >> 1)}, E.key0, E.key1);
+      const uint32_t w0 = (c & 1) ? r.z : r.x, w1 = (c & 1) ? r.w : r.y;
+      const float rad = sqrtf(-2.0f * logf(u01_open0(w0)));
+      float sn, cs;
+      sincos_turns(u01(w1), &sn, &cs);
+      const float e0 = rad * cs, e1 = rad * sn;
+      a0 = __builtin_fmaf(sig0, e0, a0);
+      a1 = __builtin_fmaf(sig1, e1, a1);
+      const float lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) - 4.0f * 1.83787706640934548f;
+      if (O.logp && valid && c == 0) O.logp[ti] = lp;
+    }
+    if (O.act && valid) {
+      O.act[(2 * c) * TN + ti] = a0;
+      O.act[(2 * c + 1) * TN + ti] = a1;
+    }
+    float tf, tm, usq;
+    quad::wrench(A, a0, a1, u0, u1, tf, tm, usq);
+    for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tf, tm, E.h, p, q, v, om);
+    ep += 1;
+    float pr, qr, dist, theta;
+    quad::reference(E, K, F, ep, pr, qr);
+    quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
+    const float reward = -dist - 0.5f * theta - 0.01f * usq;
+    const bool done = (ep == E.H);
+    const bool lead = valid && c == 0;
+    if (O.stats_work)
+      stats_push(SB, O.stats_work, T, t, lane, 4 * blockIdx.x + wave, 4 * gridDim.x, lead ? reward : 0.0f,
+                 (lead && done) ? 1.0f : 0.0f, lead ? dist : 0.0f);
+    if (lead) {
+      if (O.reward) O.reward[ti] = reward;
+      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
+    }
+    if (done) {  // the whole quad takes this branch
+      episode += 1u;
+      State xs;
+      reset_draws(E, gid, episode, xs, P);
+      quad::make_lane_consts(V, K, P, M, F);
+      ep = 0;
+      p = quad::pick(K, xs.p[0], xs.p[1], xs.p[2], 0.0f);
+      q = quad::pick(K, xs.q[1], xs.q[2], xs.q[3], xs.q[0]);
+      v = om = 0.0f;
+      u0 = u1 = 0.0f;
+      quad::reference(E, K, F, 0, pr, qr);
+      quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
+      dirty = true;
+    }
+    store_traj(t + 1);
+    put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
     __syncthreads();
   }
-  if (wave == 0 && valid) lane_store(E, i, L);
+  if (!valid) return;
+  if (c < 3) {
+    E.state[c * N + i] = p;
+    E.state[(7 + c) * N + i] = v;
+    E.state[(10 + c) * N + i] = om;
+    E.obs[c * N + i] = ob.dpb;
+    E.obs[(3 + c) * N + i] = ob.c0;
+    E.obs[(6 + c) * N + i] = ob.c1;
+    E.obs[(9 + c) * N + i] = v;
+    E.obs[(12 + c) * N + i] = om;
+  }
+  E.state[(c < 3 ? 4 + c : 3) * N + i] = q;
+  E.obs[(15 + 2 * c) * N + i] = u0;
+  E.obs[(16 + 2 * c) * N + i] = u1;
+  if (c == 0) {
+    E.ep_step[i] = ep;
+    E.episode[i] = episode;
+    if (dirty) store_params(E.params, E.n, i, P);
+  }
 }
 
 // Stand-alone MLP forward over obs [23][n] -> out [n_out][n]; persistent over 64-env
@@ -90,7 +215,8 @@ __global__ __launch_bounds__(256, 1) void k_mlp(const uint16_t* __restrict__ w, 
                                                 int n_out, int n, const float* __restrict__ obs,
                                                 float* __restrict__ out) {
   __shared__ MlpShared S;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   MlpRegs R;
   mlp_load(w, b, n_out, wave, lane, R, S);
   const int tiles = (n + 63) / 64;
@@ -105,12 +231,15 @@ __global__ __launch_bounds__(256, 1) void k_mlp(const uint16_t* __restrict__ w, 
       mlp_put_obs(o, lane, S);
     }
     __syncthreads();
-    mlp_layer1(R, S, wave, lane);
+    OwnH1 H;
+    mlp_layer1(R, S, wave, lane, H);
     __syncthreads();
-    mlp_layer23(R, S, wave, lane);
+    mlp_layer23(R, S, wave, lane, H);
     __syncthreads();
     if (wave == 0 && valid) {
-      for (int k = 0; k < n_out; ++k) out[k * N + i] = mlp_out(S, lane, k);
+      float y[NOUT_PAD];
+      mlp_out8(S, lane, y);
+      for (int k = 0; k < n_out; ++k) out[k * N + i] = y[k];
     }
     __syncthreads();
   }

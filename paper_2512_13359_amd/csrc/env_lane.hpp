@@ -84,21 +84,33 @@ __device__ __forceinline__ void lane_step(const VehArgs& V, const EnvArgs& E, ui
   }
 }
 
-// Per-step outputs shared by the environment loops.
-__device__ __forceinline__ void lane_outputs(const StepOut& O, int T, size_t N, int t, int i, bool valid,
-                                             int lane, int g, int G, float reward, bool done, float dist,
-                                             const State& x) {
-  const size_t ti = (size_t)t * N + (size_t)i;
-  if (O.stats_work) {
-    const float sr = wave_sum(valid ? reward : 0.0f);
-    const float sd = wave_sum((valid && done) ? 1.0f : 0.0f);
-    const float sp = wave_sum(valid ? dist : 0.0f);
-    if (lane == 0) {
-      O.stats_work[((size_t)0 * T + t) * G + g] = sr;
-      O.stats_work[((size_t)1 * T + t) * G + g] = sd;
-      O.stats_work[((size_t)2 * T + t) * G + g] = sp;
+// Per-step batch statistics of one group of 64 environments: the three wave sums of
+// step t are parked in lane (t mod 64) and written as one coalesced row of up to 64 steps
+// ([3][G][T] layout), so each step costs no memory traffic of its own.
+struct StatsBuf { float v[3]; };
+
+__device__ __forceinline__ void stats_push(StatsBuf& B, float* __restrict__ work, int T, int t, int lane,
+                                           int g, int G, float r, float d, float p) {
+  const float sr = wave_sum(r), sd = wave_sum(d), sp = wave_sum(p);
+  const int slot = t & 63;
+  if (lane == slot) { B.v[0] = sr; B.v[1] = sd; B.v[2] = sp; }
+  if (slot == 63 || t == T - 1) {
+    const int t0 = t - slot;
+    if (lane <= slot) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s) work[((size_t)s * G + g) * T + t0 + lane] = B.v[s];
     }
   }
+}
+
+// Per-step outputs shared by the environment loops.
+__device__ __forceinline__ void lane_outputs(const StepOut& O, StatsBuf& B, int T, size_t N, int t, int i,
+                                             bool valid, int lane, int g, int G, float reward, bool done,
+                                             float dist, const State& x) {
+  const size_t ti = (size_t)t * N + (size_t)i;
+  if (O.stats_work)
+    stats_push(B, O.stats_work, T, t, lane, g, G, valid ? reward : 0.0f, (valid && done) ? 1.0f : 0.0f,
+               valid ? dist : 0.0f);
   if (valid) {
     if (O.reward) O.reward[ti] = reward;
     if (O.done) O.done[ti] = done ? 1.0f : 0.0f;

@@ -7,7 +7,9 @@
 // and D[m = 4 g + i][n = r] for i = 0..3.
 //
 // Wave w owns output features [64 w, 64 w + 64) of both hidden layers (4 M-tiles) and the
-// input slice [64 w, 64 w + 64) of the output layer (split K).  Within a 32-wide K tile,
+// input slice [64 w, 64 w + 64) of the output layer (split K).  Its layer-2 weights are
+// kept in K-tile order 2w, 2w+1, 2w+2, ... (mod 8), so its own two hidden-1 tiles come
+// first, straight from registers.  Within a 32-wide K tile,
 // slot (g, j) holds feature 16 (j / 4) + 4 g + (j % 4); with that order a lane's four
 // D values of M-tiles 2c and 2c + 1 are exactly its eight B values of the next layer's
 // K tile c, so a hidden layer's output becomes the next layer's operand without any
@@ -34,18 +36,22 @@ __device__ __forceinline__ f32x4 mfma(const bf16x8& a, const bf16x8& b, const f3
 
 __device__ __forceinline__ __bf16 bf16_of_bits(uint16_t b) { return __builtin_bit_cast(__bf16, b); }
 
-// tanh(x) = 1 - 2 / (1 + e^{2x}); saturates correctly at both ends (e -> inf gives 1,
-// e -> 0 gives -1).  Absolute error a few 1e-7.
-__device__ __forceinline__ float tanh_fast(float x) {
-  const float e = __builtin_amdgcn_exp2f(x * 2.88539008177792681f);   // 2 log2(e)
-  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + e);
+constexpr float TWO_LOG2E = 2.88539008177792681f;   // 2 log2(e)
+
+// tanh(d + b) = 1 - 2 / (1 + 2^{(d + b) 2 log2 e}) with bk = b * 2 log2 e folded into
+// one fma; saturates correctly at both ends (2^x -> inf gives 1, -> 0 gives -1).
+// Absolute error a few 1e-7.
+__device__ __forceinline__ float tanh_bias(float d, float bk) {
+  const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(d, TWO_LOG2E, bk));
+  return __builtin_fmaf(-2.0f, __builtin_amdgcn_rcpf(1.0f + e), 1.0f);
 }
 
 struct MlpShared {
-  bf16x8 x[4][64];          // layer-1 operand: [env tile][lane], K = 32 (23 used)
-  bf16x8 h[8][4][64];       // hidden-1 operand: [K tile][env tile][lane]
-  float mu[4][4][NOUT_PAD][16];  // output partials: [wave][env tile][row][env]
-  float b1[HID], b2[HID], b3[16];
+  bf16x8 x[4][64];               // layer-1 operand: [env tile][lane], K = 32 (23 used)
+  bf16x8 h[8][4][64];            // hidden-1 operand: [K tile][env tile][lane]
+  float mu[4][64][NOUT_PAD];     // output partials: [wave][env][row]
+  float b1k[HID], b2k[HID];      // hidden biases times 2 log2 e
+  float b3[16];
 };
 
 struct MlpRegs {
@@ -70,9 +76,11 @@ __device__ __forceinline__ void mlp_load(const uint16_t* __restrict__ w, const f
       R.w1[mt][j] = k < 23 ? bf16_of_bits(W1[row * 23 + k]) : bf16_of_bits(0);
     }
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt)
+    for (int kk = 0; kk < 8; ++kk) {
+      const int kt = (2 * wave + kk) & 7;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) R.w2[mt][kt][j] = bf16_of_bits(W2[row * HID + 32 * kt + kslot(g, j)]);
+      for (int j = 0; j < 8; ++j) R.w2[mt][kk][j] = bf16_of_bits(W2[row * HID + 32 * kt + kslot(g, j)]);
+    }
   }
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) {
@@ -82,8 +90,8 @@ __device__ __forceinline__ void mlp_load(const uint16_t* __restrict__ w, const f
       R.w3[kk][j] = r < n_out ? bf16_of_bits(W3[r * HID + 32 * kt + kslot(g, j)]) : bf16_of_bits(0);
   }
   const int tid = wave * 64 + lane;
-  S.b1[tid] = b[tid];
-  S.b2[tid] = b[HID + tid];
+  S.b1k[tid] = b[tid] * TWO_LOG2E;
+  S.b2k[tid] = b[HID + tid] * TWO_LOG2E;
   if (tid < 16) S.b3[tid] = tid < n_out ? b[2 * HID + tid] : 0.0f;
 }
 
@@ -102,65 +110,71 @@ __device__ __forceinline__ void mlp_put_obs(const float o[23], int env, MlpShare
   }
 }
 
-__device__ __forceinline__ void act_to_frag(const f32x4& d, const f32x4& bias, int half, bf16x8& frag) {
+__device__ __forceinline__ void act_to_frag(const f32x4& d, const f32x4& bk, int half, bf16x8& frag) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) frag[4 * half + i] = (__bf16)tanh_fast(d[i] + bias[i]);
+  for (int i = 0; i < 4; ++i) frag[4 * half + i] = (__bf16)tanh_bias(d[i], bk[i]);
 }
 
-// Layer 1 (reads S.x) -> this wave's K tiles of the hidden-1 operand into S.h.
-// Requires a barrier before (S.x written) and after (S.h read by every wave).
-__device__ __forceinline__ void mlp_layer1(const MlpRegs& R, MlpShared& S, int wave, int lane) {
+// This wave's two K tiles of the hidden-1 operand, for every env tile (kept in registers
+// between layer 1 and layer 2).
+struct OwnH1 { bf16x8 f[2][4]; };
+
+// Layer 1 (reads S.x) -> this wave's K tiles of the hidden-1 operand, into S.h (for the
+// other waves) and into H (for itself).  Requires a barrier before (S.x written) and
+// after (S.h read by every wave).
+__device__ __forceinline__ void mlp_layer1(const MlpRegs& R, MlpShared& S, int wave, int lane, OwnH1& H) {
   const int g = lane >> 4;
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
     const bf16x8 x = S.x[nt][lane];
-    bf16x8 f0, f1;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const f32x4 d = mfma(R.w1[mt], x, f32x4{0, 0, 0, 0});
-      const f32x4 bias = *reinterpret_cast<const f32x4*>(&S.b1[64 * wave + 16 * mt + 4 * g]);
-      act_to_frag(d, bias, mt & 1, mt < 2 ? f0 : f1);
+      const f32x4 bk = *reinterpret_cast<const f32x4*>(&S.b1k[64 * wave + 16 * mt + 4 * g]);
+      act_to_frag(d, bk, mt & 1, H.f[mt >> 1][nt]);
     }
-    S.h[2 * wave][nt][lane] = f0;
-    S.h[2 * wave + 1][nt][lane] = f1;
+    S.h[2 * wave][nt][lane] = H.f[0][nt];
+    S.h[2 * wave + 1][nt][lane] = H.f[1][nt];
   }
 }
 
-// Layer 2 (reads S.h) and this wave's split-K part of layer 3 into S.mu.
-// Requires a barrier after (S.mu read by the consumer).
-__device__ __forceinline__ void mlp_layer23(const MlpRegs& R, MlpShared& S, int wave, int lane) {
+// Layer 2 (reads the other waves' K tiles from S.h) and this wave's split-K part of
+// layer 3 into S.mu.  Requires a barrier after (S.mu read by the consumer).
+__device__ __forceinline__ void mlp_layer23(const MlpRegs& R, MlpShared& S, int wave, int lane, const OwnH1& H) {
   const int g = lane >> 4, r = lane & 15;
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
     bf16x8 hb[8];
+    hb[0] = H.f[0][nt];
+    hb[1] = H.f[1][nt];
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt) hb[kt] = S.h[kt][nt][lane];
+    for (int kk = 2; kk < 8; ++kk) hb[kk] = S.h[(2 * wave + kk) & 7][nt][lane];
     bf16x8 f0, f1;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       f32x4 acc = {0, 0, 0, 0};
 #pragma unroll
-      for (int kt = 0; kt < 8; ++kt) acc = mfma(R.w2[mt][kt], hb[kt], acc);
-      const f32x4 bias = *reinterpret_cast<const f32x4*>(&S.b2[64 * wave + 16 * mt + 4 * g]);
-      act_to_frag(acc, bias, mt & 1, mt < 2 ? f0 : f1);
+      for (int kk = 0; kk < 8; ++kk) acc = mfma(R.w2[mt][kk], hb[kk], acc);
+      const f32x4 bk = *reinterpret_cast<const f32x4*>(&S.b2k[64 * wave + 16 * mt + 4 * g]);
+      act_to_frag(acc, bk, mt & 1, mt < 2 ? f0 : f1);
     }
     f32x4 o = mfma(R.w3[0], f0, f32x4{0, 0, 0, 0});
     o = mfma(R.w3[1], f1, o);
-    if (g < 2) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) S.mu[wave][nt][4 * g + i][r] = o[i];
-    }
+    if (g < 2) *reinterpret_cast<f32x4*>(&S.mu[wave][16 * nt + r][4 * g]) = o;
   }
 }
 
-// Output row o of environment env: bias + the four waves' partials in fixed order.
-__device__ __forceinline__ float mlp_out(const MlpShared& S, int env, int o) {
-  const int nt = env >> 4, r = env & 15;
-  float s = S.mu[0][nt][o][r];
-  s += S.mu[1][nt][o][r];
-  s += S.mu[2][nt][o][r];
-  s += S.mu[3][nt][o][r];
-  return S.b3[o] + s;
+// All outputs of environment env: bias + the four waves' partials in fixed order.
+__device__ __forceinline__ void mlp_out8(const MlpShared& S, int env, float y[NOUT_PAD]) {
+  f32x4 lo = *reinterpret_cast<const f32x4*>(&S.mu[0][env][0]);
+  f32x4 hi = *reinterpret_cast<const f32x4*>(&S.mu[0][env][4]);
+#pragma unroll
+  for (int w = 1; w < 4; ++w) {
+    lo += *reinterpret_cast<const f32x4*>(&S.mu[w][env][0]);
+    hi += *reinterpret_cast<const f32x4*>(&S.mu[w][env][4]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { y[i] = S.b3[i] + lo[i]; y[4 + i] = S.b3[4 + i] + hi[i]; }
 }
 
 }  // namespace auv

@@ -1,0 +1,274 @@
+// Environment step with four lanes per environment ("quad" layout) for the fused policy
+// rollout, so that a workgroup's four waves share the physics of its 64 environments.
+//
+// Lane l serves environment slot l / 4 of its wave and component c = l % 4: lanes c = 0,
+// 1, 2 hold the x, y, z components of every 3-vector (p, v, omega, and derived vectors)
+// and the vector part of the quaternion; lane 3 holds the quaternion's scalar part and
+// zero in every 3-vector.  Cross products and dot products across the four lanes use DPP
+// quad permutations (no LDS, no waits).  The arithmetic is the same as the one-lane-per-
+// environment form in auv_device.hpp; only its distribution over lanes differs.
+#pragma once
+
+#include "auv_device.hpp"
+
+namespace auv {
+namespace quad {
+
+constexpr int QP(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
+constexpr int P1 = QP(1, 2, 0, 3);    // lane c reads component c+1 (mod 3)
+constexpr int P2 = QP(2, 0, 1, 3);    // lane c reads component c+2 (mod 3)
+constexpr int SW1 = QP(1, 0, 3, 2), SW2 = QP(2, 3, 0, 1);
+constexpr int BC0 = QP(0, 0, 0, 0), BC1 = QP(1, 1, 1, 1), BC2 = QP(2, 2, 2, 2), BC3 = QP(3, 3, 3, 3);
+constexpr int XE3 = QP(1, 0, 2, 3);   // (e x e3) = (e_y, -e_x, 0)
+constexpr int XE1 = QP(0, 2, 1, 3);   // (e x e1) = (0, e_z, -e_y)
+constexpr int XE2 = QP(2, 1, 0, 3);   // (e x e2) = (-e_z, 0, e_x)
+
+template <int C>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), C, 0xF, 0xF, true));
+}
+
+// sum over the four lanes of a quad, every lane gets it
+__device__ __forceinline__ float qsum(float x) {
+  x += dpp<SW1>(x);
+  return x + dpp<SW2>(x);
+}
+
+struct Perm { float p1, p2; };
+__device__ __forceinline__ Perm perm(float x) { return Perm{dpp<P1>(x), dpp<P2>(x)}; }
+// (a x b)_c = a_{c+1} b_{c+2} - a_{c+2} b_{c+1}, b given by its two rotations
+__device__ __forceinline__ float cross(float a, const Perm& b) { return dpp<P1>(a) * b.p2 - dpp<P2>(a) * b.p1; }
+
+// Per-lane constants of the layout.
+struct QK {
+  int c;
+  float m3;    // 1 in vector lanes, 0 in lane 3
+  float d2;    // e3 (1 in lane 2)
+  float sx3;   // sign pattern of e x e3: (+1, -1, 0, 0)
+  float sx1;   // sign pattern of e x e1: (0, +1, -1, 0)
+  float sx2;   // sign pattern of e x e2: (-1, 0, +1, 0)
+  float e1, e2;
+  float BmW;
+};
+
+__device__ __forceinline__ QK make_qk(int lane, const VehArgs& V) {
+  QK K;
+  K.c = lane & 3;
+  K.m3 = K.c < 3 ? 1.0f : 0.0f;
+  K.d2 = K.c == 2 ? 1.0f : 0.0f;
+  K.e1 = K.c == 0 ? 1.0f : 0.0f;
+  K.e2 = K.c == 1 ? 1.0f : 0.0f;
+  K.sx3 = K.c == 0 ? 1.0f : (K.c == 1 ? -1.0f : 0.0f);
+  K.sx1 = K.c == 1 ? 1.0f : (K.c == 2 ? -1.0f : 0.0f);
+  K.sx2 = K.c == 0 ? -1.0f : (K.c == 2 ? 1.0f : 0.0f);
+  K.BmW = V.BmW;
+  return K;
+}
+
+// Per-lane (component c) model constants of one environment; zero in lane 3.
+struct QModel {
+  float Mlin, iMlin, A1, DLl, DQl;   // linear DOF c
+  float Mang, iMang, DLa, DQa;       // angular DOF c
+  float cw;                          // world current
+  Perm cwP;                          // its rotations
+  Perm BrbP;                         // rotations of B r_b
+};
+
+// Per-lane reference data: lanes 0-2 the Lissajous position component (in turns), lane 3
+// the yaw ramp (psi / 4 pi, in turns); goal pose in quad layout.
+struct QRef {
+  float pg, amp, fr, ph;   // p_goal_c, A_c, f_c [turns / s], phase_c / 2 pi  (lane 3: 0, 0, yaw rate / 4 pi, yaw0 / 4 pi)
+  float qg;                // goal quaternion, quad layout
+};
+
+// Thrust allocation rows of lane c: tau_f[c] = sum_j Tf[j] u_j, tau_m[c] = sum_j Tm[j] u_j
+// (f_max folded in; zero in lane 3).
+struct QAlloc { float Tf[8], Tm[8]; };
+
+__device__ __forceinline__ QAlloc make_alloc(const VehArgs& V, int c) {
+  QAlloc A;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    float f = 0.0f, m = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+      f = c == r ? V.alloc[r * 8 + j] * V.f_max : f;
+      m = c == r ? V.alloc[(3 + r) * 8 + j] * V.f_max : m;
+    }
+    A.Tf[j] = f;
+    A.Tm[j] = m;
+  }
+  return A;
+}
+
+// Component c of (x0, x1, x2) with x3 in lane 3, by 0/1 weights (arithmetic rather than an
+// index, which would put the source arrays in scratch memory).
+__device__ __forceinline__ float pick(const QK& K, float x0, float x1, float x2, float x3) {
+  const float w0 = K.c == 0 ? 1.0f : 0.0f, w1 = K.c == 1 ? 1.0f : 0.0f, w2 = K.c == 2 ? 1.0f : 0.0f;
+  return __builtin_fmaf(w0, x0, __builtin_fmaf(w1, x1, __builtin_fmaf(w2, x2, (1.0f - K.m3) * x3)));
+}
+
+// Scalar (one-lane) parameters -> this lane's model and reference constants.
+__device__ __forceinline__ void make_lane_consts(const VehArgs& V, const QK& K, const Params& P, QModel& M,
+                                                 QRef& F) {
+  Model S;
+  make_model(V, P, S);
+  M.Mlin = pick(K, S.Mlin[0], S.Mlin[1], S.Mlin[2], 0.0f);
+  M.iMlin = pick(K, S.iMlin[0], S.iMlin[1], S.iMlin[2], 0.0f);
+  M.A1 = pick(K, S.A1[0], S.A1[1], S.A1[2], 0.0f);
+  M.DLl = pick(K, S.DL[0], S.DL[1], S.DL[2], 0.0f);
+  M.DQl = pick(K, S.DQ[0], S.DQ[1], S.DQ[2], 0.0f);
+  M.Mang = pick(K, S.Mang[0], S.Mang[1], S.Mang[2], 0.0f);
+  M.iMang = pick(K, S.iMang[0], S.iMang[1], S.iMang[2], 0.0f);
+  M.DLa = pick(K, S.DL[3], S.DL[4], S.DL[5], 0.0f);
+  M.DQa = pick(K, S.DQ[3], S.DQ[4], S.DQ[5], 0.0f);
+  M.cw = pick(K, P.cw[0], P.cw[1], P.cw[2], 0.0f);
+  M.cwP = perm(M.cw);
+  M.BrbP = perm(pick(K, V.Brb[0], V.Brb[1], V.Brb[2], 0.0f));
+  constexpr float INV_2PI = 0.159154943091895336f, INV_4PI = 0.0795774715459476679f;
+  F.pg = pick(K, P.pg[0], P.pg[1], P.pg[2], 0.0f);
+  F.amp = pick(K, P.amp[0], P.amp[1], P.amp[2], 0.0f);
+  F.fr = pick(K, P.freq[0], P.freq[1], P.freq[2], P.yaw_rate * INV_4PI);
+  F.ph = pick(K, P.phase[0] * INV_2PI, P.phase[1] * INV_2PI, P.phase[2] * INV_2PI, P.yaw0 * INV_4PI);
+  F.qg = pick(K, P.qg[1], P.qg[2], P.qg[3], P.qg[0]);
+}
+
+// ------------------------------------------------------------ Fossen right side ----
+// Same equations as auv::rhs, one component per lane.  R x = s x + 2 (e.x) e + 2 w (e x x)
+// and R^T x = s x + 2 (e.x) e - 2 w (e x x) with s = 1 - 2 e.e (the Euler-Rodrigues
+// matrix I + 2 w S(e) + 2 S(e)^2 applied to a vector).
+__device__ __forceinline__ void rhs(const QK& K, const QModel& M, float tf, float tm, float q, float v,
+                                    float om, float& dp, float& dq, float& dv, float& dw) {
+  const float e = q * K.m3;
+  const float wb = dpp<BC3>(q);
+  const float s = __builtin_fmaf(-2.0f, qsum(e * e), 1.0f);
+  const Perm eP = perm(e);
+  // dp = R v
+  const float ev = qsum(e * v);
+  const float exv = -cross(v, eP);
+  dp = __builtin_fmaf(s, v, 2.0f * __builtin_fmaf(ev, e, wb * exv));
+  // c_b = R^T c_w
+  const float ec = qsum(e * M.cw);
+  const float excw = -cross(M.cw, eP);
+  const float cb = __builtin_fmaf(s, M.cw, 2.0f * __builtin_fmaf(ec, e, -wb * excw));
+  // k = R^T e3
+  const float ez = dpp<BC2>(e);
+  const float exe3 = dpp<XE3>(e) * K.sx3;
+  const float k = __builtin_fmaf(s, K.d2, 2.0f * __builtin_fmaf(ez, e, -wb * exe3));
+  const float vr = v - cb;
+  const Perm wP = perm(om);
+  // linear: tau_f - w x (Mlin vr) - (DL + DQ |vr|) vr - (B - W) k
+  const float a = M.Mlin * vr;
+  float F = tf + cross(a, wP);
+  F = __builtin_fmaf(-__builtin_fmaf(M.DQl, fabsf(vr), M.DLl), vr, F);
+  F = __builtin_fmaf(-K.BmW, k, F);
+  // angular: tau_m - w x (Mang w) - vr x (A1 vr) - B r_b x k - (DL + DQ |w|) w
+  const float b = M.Mang * om;
+  const float c = M.A1 * vr;
+  const Perm vrP = perm(vr);
+  float G = tm + cross(b, wP) + cross(c, vrP) + cross(k, M.BrbP);
+  G = __builtin_fmaf(-__builtin_fmaf(M.DQa, fabsf(om), M.DLa), om, G);
+  dv = __builtin_fmaf(F, M.iMlin, cross(cb, wP));
+  dw = G * M.iMang;
+  // dq = 1/2 q (x) (0, w): vector part 1/2 (w om + e x om), scalar part -1/2 e.om
+  const float eo = qsum(e * om);
+  const float exo = -cross(om, eP);
+  dq = K.c < 3 ? 0.5f * __builtin_fmaf(wb, om, exo) : -0.5f * eo;
+}
+
+__device__ __forceinline__ void rk4(const QK& K, const QModel& M, float tf, float tm, float h, float& p, float& q,
+                                    float& v, float& om) {
+  float dp, dq, dv, dw;
+  rhs(K, M, tf, tm, q, v, om, dp, dq, dv, dw);
+  float ap = dp, aq = dq, av = dv, aw = dw;
+#pragma unroll
+  for (int stage = 1; stage < 4; ++stage) {
+    const float cs = (stage == 3) ? h : 0.5f * h;
+    rhs(K, M, tf, tm, __builtin_fmaf(cs, dq, q), __builtin_fmaf(cs, dv, v), __builtin_fmaf(cs, dw, om), dp, dq, dv,
+        dw);
+    const float wgt = (stage == 3) ? 1.0f : 2.0f;
+    ap = __builtin_fmaf(wgt, dp, ap);
+    aq = __builtin_fmaf(wgt, dq, aq);
+    av = __builtin_fmaf(wgt, dv, av);
+    aw = __builtin_fmaf(wgt, dw, aw);
+  }
+  const float h6 = h * (1.0f / 6.0f);
+  p = __builtin_fmaf(h6, ap, p);
+  q = __builtin_fmaf(h6, aq, q);
+  v = __builtin_fmaf(h6, av, v);
+  om = __builtin_fmaf(h6, aw, om);
+  q *= rsqrtf(qsum(q * q));
+}
+
+// --------------------------------------------------- reference, observation ----------
+__device__ __forceinline__ void reference(const EnvArgs& E, const QK& K, const QRef& F, int ep_step, float& pr,
+                                          float& qr) {
+  if (E.flags & F_LISSAJOUS) {
+    const float t = (float)ep_step * E.dt;
+    float s, c;
+    sincos_turns(__builtin_fmaf(F.fr, t, F.ph), &s, &c);
+    pr = K.m3 * __builtin_fmaf(F.amp, s, F.pg);
+    const float sy = dpp<BC3>(s), cy = dpp<BC3>(c);
+    qr = K.c == 3 ? cy : (K.c == 2 ? sy : 0.0f);
+  } else {
+    pr = F.pg;
+    qr = F.qg;
+  }
+}
+
+// Rotation helpers for a quaternion in quad layout.
+struct QRot { float e, wb, s; Perm eP; };
+__device__ __forceinline__ QRot qrot(const QK& K, float q) {
+  QRot r;
+  r.e = q * K.m3;
+  r.wb = dpp<BC3>(q);
+  r.s = __builtin_fmaf(-2.0f, qsum(r.e * r.e), 1.0f);
+  r.eP = perm(r.e);
+  return r;
+}
+__device__ __forceinline__ float rot_T(const QRot& r, float x) {   // R^T x
+  const float ex = qsum(r.e * x);
+  return __builtin_fmaf(r.s, x, 2.0f * __builtin_fmaf(ex, r.e, r.wb * cross(x, r.eP)));
+}
+
+// Observation components of this lane, |dp| and the attitude-error angle.
+struct QObs { float dpb, c0, c1; };
+__device__ __forceinline__ void observe(const QK& K, float p, float q, float v, float om, float pr, float qr,
+                                        QObs& o, float& dist, float& theta) {
+  const QRot R = qrot(K, q);
+  o.dpb = rot_T(R, pr - p);
+  // columns 0 and 1 of R_ref: R_ref e1 = s e1 + 2 e_x e + 2 w (e x e1), same for e2
+  const QRot Rr = qrot(K, qr);
+  const float r0 = __builtin_fmaf(Rr.s, K.e1, 2.0f * __builtin_fmaf(dpp<BC0>(Rr.e), Rr.e, Rr.wb * dpp<XE1>(Rr.e) * K.sx1));
+  const float r1 = __builtin_fmaf(Rr.s, K.e2, 2.0f * __builtin_fmaf(dpp<BC1>(Rr.e), Rr.e, Rr.wb * dpp<XE2>(Rr.e) * K.sx2));
+  o.c0 = rot_T(R, r0);
+  o.c1 = rot_T(R, r1);
+  dist = sqrtf(qsum(o.dpb * o.dpb));
+  // q_err = q^* (x) q_ref: scalar w wr + e.er, vector w er - wr e - e x er
+  const float ew = qsum(q * qr);
+  const float vec = __builtin_fmaf(R.wb, Rr.e, -Rr.wb * R.e) - cross(R.e, Rr.eP);
+  theta = 2.0f * atan2f(sqrtf(qsum(vec * vec)), fabsf(ew));
+  (void)v;
+  (void)om;
+}
+
+// Clip this lane's two actions, broadcast all eight across the quad, body wrench.
+__device__ __forceinline__ void wrench(const QAlloc& A, float a0, float a1, float& u0, float& u1, float& tf,
+                                       float& tm, float& usq) {
+  u0 = fminf(fmaxf(a0, -1.0f), 1.0f);
+  u1 = fminf(fmaxf(a1, -1.0f), 1.0f);
+  const float u[8] = {dpp<BC0>(u0), dpp<BC0>(u1), dpp<BC1>(u0), dpp<BC1>(u1),
+                      dpp<BC2>(u0), dpp<BC2>(u1), dpp<BC3>(u0), dpp<BC3>(u1)};
+  float f = 0.0f, m = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    f = __builtin_fmaf(A.Tf[j], u[j], f);
+    m = __builtin_fmaf(A.Tm[j], u[j], m);
+  }
+  tf = f;
+  tm = m;
+  usq = qsum(__builtin_fmaf(u0, u0, u1 * u1));
+}
+
+}  // namespace quad
+}  // namespace auv

@@ -85,8 +85,8 @@ def test_argument_errors_before_any_launch():
     assert rc == A.AUV_EINVAL
     assert A.auv_get_global_step(h) == 0
     A.auv_destroy(h)
-    assert A.auv_stats_work_floats(4096, 10) == 3 * 10 * 64
-    assert A.auv_stats_work_floats(65, 2) == 3 * 2 * 2
+    assert A.auv_stats_work_floats(4096, 10) == 3 * 10 * 4 * 64
+    assert A.auv_stats_work_floats(65, 2) == 3 * 2 * 4 * 2
 
 
 def test_binding_structs_match_header_sizes():
