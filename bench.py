@@ -36,7 +36,7 @@ P_VALU = 157.3e12
 P_TRANS = 256 * 4 * 16 * 2.4e9 / 2
 HBM_PEAK = 8.0e12
 
-KERNEL_SOURCES = ["auv_device.hpp", "env_lane.hpp", "mlp_mfma.hpp", "auv_policy.hip", "auv_env.hip"]
+KERNEL_SOURCES = ["auv_device.hpp", "env_lane.hpp", "quad_env.hpp", "mlp_mfma.hpp", "auv_policy.hip", "auv_env.hip"]
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_policy_rollout_c4_counters.txt")
 
 

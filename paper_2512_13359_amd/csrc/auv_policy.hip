@@ -28,12 +28,13 @@ __device__ __forceinline__ void put_obs_quad(MlpShared& S, int nt, int r, int c,
   put(16 + 2 * c, u1);
 }
 
-// One workgroup = 4 waves = 64 environments for all T steps.  All four waves step their
-// 16 environments with four lanes each (quad layout, quad_env.hpp) and all four run the
-// MLP on MFMA with their weight slices in registers.  Three barriers per step:
+// One workgroup = 8 waves = 64 environments for all T steps.  Waves 0-3 step 16
+// environments each with four lanes per environment (quad layout, quad_env.hpp); all
+// eight waves run the MLP on MFMA with their weight slices in registers (two per SIMD,
+// so MFMA and tanh of different waves overlap).  Three barriers per step:
 //   obs in LDS -> layer 1 -> hidden-1 in LDS -> layers 2, 3 -> partials in LDS -> physics.
 template <bool SAMPLE>
-__global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
+__global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
                                                            StepOut O, const uint16_t* __restrict__ w,
                                                            const float* __restrict__ b,
                                                            const float* __restrict__ log_std) {
@@ -42,23 +43,31 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   MlpRegs R;
   mlp_load(w, b, ACT, wave, lane, R, S);
-  S.x[tid >> 6][lane] = bf16x8{};
+  if (tid < 256) S.x[tid >> 6][lane] = bf16x8{};
+  const bool phys = wave < 4;              // physics waves (wave-uniform)
   const quad::QK K = quad::make_qk(lane, V);
   const int c = K.c;
   const int slot = lane >> 2;              // environment within this wave's tile
   const int env = 16 * wave + slot;        // environment within the workgroup
   const int i = blockIdx.x * 64 + env;
-  const bool valid = i < E.n;
+  const bool valid = phys && i < E.n;
   const size_t N = (size_t)E.n, TN = (size_t)T * N;
   const uint32_t gid = E.env_offset + (uint32_t)i;
   const int cv = c < 3 ? c : 0;            // a valid component row for lane 3's loads
-  const quad::QAlloc A = quad::make_alloc(V, c);
+  if (tid < 64) {                          // allocation rows x f_max into LDS
+    const int row = tid >> 3, j = tid & 7;
+    const int src = row < 3 ? row : (row >= 4 && row < 7 ? row - 1 : -1);
+    S.alloc[row][j] = src >= 0 ? V.alloc[src * 8 + j] * V.f_max : 0.0f;
+  }
 
   float p, q, v, om, u0, u1;
   int ep = 0;
   uint32_t episode = 0;
-  Params P;
   quad::QObs ob;
+  quad::QModel M;
+  quad::QRef F;
+  {
+  Params P;
   if (valid) {
     p = c < 3 ? E.state[cv * N + i] : 0.0f;
     q = E.state[(c < 3 ? 4 + c : 3) * N + i];
@@ -78,10 +87,8 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
     P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
     ob = quad::QObs{0, 0, 0};
   }
-  quad::QModel M;
-  quad::QRef F;
   quad::make_lane_consts(V, K, P, M, F);
-  bool dirty = false;
+  }
   float lsd0 = 0.0f, lsd1 = 0.0f, sig0 = 0.0f, sig1 = 0.0f;
   if (SAMPLE) {
     lsd0 = log_std[2 * c];
@@ -103,7 +110,7 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
   store_traj(0);
   StatsBuf SB{};
   __syncthreads();                          // S.x zeroed, biases staged
-  put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
+  if (phys) put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
   __syncthreads();
   OwnH1 H;
   for (int t = 0; t < T; ++t) {
@@ -111,6 +118,7 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
     __syncthreads();
     mlp_layer23(R, S, wave, lane, H);
     __syncthreads();
+    if (phys) {
     const size_t ti = (size_t)t * N + (size_t)i;
     if (O.obs && valid) {
       if (c < 3) {
@@ -128,7 +136,7 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
     {
       float s0 = S.mu[0][env][2 * c], s1 = S.mu[0][env][2 * c + 1];
 #pragma unroll
-      for (int ww = 1; ww < 4; ++ww) {
+      for (int ww = 1; ww < MLP_WAVES; ++ww) {
         s0 += S.mu[ww][env][2 * c];
         s1 += S.mu[ww][env][2 * c + 1];
       }
@@ -154,7 +162,14 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
       O.act[(2 * c + 1) * TN + ti] = a1;
     }
     float tf, tm, usq;
-    quad::wrench(A, a0, a1, u0, u1, tf, tm, usq);
+    {
+      float Tf[8], Tm[8];
+      *reinterpret_cast<f32x4*>(&Tf[0]) = *reinterpret_cast<const f32x4*>(&S.alloc[c][0]);
+      *reinterpret_cast<f32x4*>(&Tf[4]) = *reinterpret_cast<const f32x4*>(&S.alloc[c][4]);
+      *reinterpret_cast<f32x4*>(&Tm[0]) = *reinterpret_cast<const f32x4*>(&S.alloc[4 + c][0]);
+      *reinterpret_cast<f32x4*>(&Tm[4]) = *reinterpret_cast<const f32x4*>(&S.alloc[4 + c][4]);
+      quad::wrench(Tf, Tm, a0, a1, u0, u1, tf, tm, usq);
+    }
     for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tf, tm, E.h, p, q, v, om);
     ep += 1;
     float pr, qr, dist, theta;
@@ -173,8 +188,10 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
     if (done) {  // the whole quad takes this branch
       episode += 1u;
       State xs;
+      Params P;
       reset_draws(E, gid, episode, xs, P);
       quad::make_lane_consts(V, K, P, M, F);
+      if (valid && c == 0) store_params(E.params, E.n, i, P);
       ep = 0;
       p = quad::pick(K, xs.p[0], xs.p[1], xs.p[2], 0.0f);
       q = quad::pick(K, xs.q[1], xs.q[2], xs.q[3], xs.q[0]);
@@ -182,10 +199,10 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
       u0 = u1 = 0.0f;
       quad::reference(E, K, F, 0, pr, qr);
       quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
-      dirty = true;
     }
     store_traj(t + 1);
     put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
+    }
     __syncthreads();
   }
   if (!valid) return;
@@ -205,13 +222,12 @@ __global__ __launch_bounds__(256, 1) void k_policy_rollout(VehArgs V, EnvArgs E,
   if (c == 0) {
     E.ep_step[i] = ep;
     E.episode[i] = episode;
-    if (dirty) store_params(E.params, E.n, i, P);
   }
 }
 
 // Stand-alone MLP forward over obs [23][n] -> out [n_out][n]; persistent over 64-env
 // tiles so each workgroup loads the weights once.
-__global__ __launch_bounds__(256, 1) void k_mlp(const uint16_t* __restrict__ w, const float* __restrict__ b,
+__global__ __launch_bounds__(MLP_THREADS, 1) void k_mlp(const uint16_t* __restrict__ w, const float* __restrict__ b,
                                                 int n_out, int n, const float* __restrict__ obs,
                                                 float* __restrict__ out) {
   __shared__ MlpShared S;
@@ -263,7 +279,7 @@ static int mlp_grid(int n) {
 
 int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, hipStream_t s) {
   if (int rc = check_mlp(net, 0, "auv_mlp_forward")) return rc;
-  hipLaunchKernelGGL(k_mlp, dim3(mlp_grid(n)), dim3(256), 0, s, (const uint16_t*)net->w, net->b, net->n_out, n,
+  hipLaunchKernelGGL(k_mlp, dim3(mlp_grid(n)), dim3(MLP_THREADS), 0, s, (const uint16_t*)net->w, net->b, net->n_out, n,
                      obs, out);
   return check_launch("auv_mlp_forward");
 }
@@ -296,10 +312,10 @@ int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, 
   const dim3 grid(groups_of(n));
   const uint16_t* w = (const uint16_t*)policy->w;
   if (sample)
-    hipLaunchKernelGGL(k_policy_rollout<true>, grid, dim3(256), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
+    hipLaunchKernelGGL(k_policy_rollout<true>, grid, dim3(MLP_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
                        policy->log_std);
   else
-    hipLaunchKernelGGL(k_policy_rollout<false>, grid, dim3(256), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
+    hipLaunchKernelGGL(k_policy_rollout<false>, grid, dim3(MLP_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
                        policy->log_std);
   if (int rc = check_launch("policy rollout")) return rc;
   if (value) {

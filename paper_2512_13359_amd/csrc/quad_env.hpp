@@ -81,26 +81,6 @@ struct QRef {
   float qg;                // goal quaternion, quad layout
 };
 
-// Thrust allocation rows of lane c: tau_f[c] = sum_j Tf[j] u_j, tau_m[c] = sum_j Tm[j] u_j
-// (f_max folded in; zero in lane 3).
-struct QAlloc { float Tf[8], Tm[8]; };
-
-__device__ __forceinline__ QAlloc make_alloc(const VehArgs& V, int c) {
-  QAlloc A;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    float f = 0.0f, m = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 3; ++r) {
-      f = c == r ? V.alloc[r * 8 + j] * V.f_max : f;
-      m = c == r ? V.alloc[(3 + r) * 8 + j] * V.f_max : m;
-    }
-    A.Tf[j] = f;
-    A.Tm[j] = m;
-  }
-  return A;
-}
-
 // Component c of (x0, x1, x2) with x3 in lane 3, by 0/1 weights (arithmetic rather than an
 // index, which would put the source arrays in scratch memory).
 __device__ __forceinline__ float pick(const QK& K, float x0, float x1, float x2, float x3) {
@@ -252,9 +232,10 @@ __device__ __forceinline__ void observe(const QK& K, float p, float q, float v, 
   (void)om;
 }
 
-// Clip this lane's two actions, broadcast all eight across the quad, body wrench.
-__device__ __forceinline__ void wrench(const QAlloc& A, float a0, float a1, float& u0, float& u1, float& tf,
-                                       float& tm, float& usq) {
+// Clip this lane's two actions, broadcast all eight across the quad, body wrench with
+// this lane's force and moment rows Tf, Tm of the allocation table (f_max folded in).
+__device__ __forceinline__ void wrench(const float Tf[8], const float Tm[8], float a0, float a1, float& u0,
+                                       float& u1, float& tf, float& tm, float& usq) {
   u0 = fminf(fmaxf(a0, -1.0f), 1.0f);
   u1 = fminf(fmaxf(a1, -1.0f), 1.0f);
   const float u[8] = {dpp<BC0>(u0), dpp<BC0>(u1), dpp<BC1>(u0), dpp<BC1>(u1),
@@ -262,8 +243,8 @@ __device__ __forceinline__ void wrench(const QAlloc& A, float a0, float a1, floa
   float f = 0.0f, m = 0.0f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    f = __builtin_fmaf(A.Tf[j], u[j], f);
-    m = __builtin_fmaf(A.Tm[j], u[j], m);
+    f = __builtin_fmaf(Tf[j], u[j], f);
+    m = __builtin_fmaf(Tm[j], u[j], m);
   }
   tf = f;
   tm = m;
