@@ -390,10 +390,39 @@ __device__ __forceinline__ void store_params(float* __restrict__ s, int n, int i
 }
 
 // Sum over the 64 lanes of a wave in a fixed butterfly order (every lane gets the sum).
+// DPP lane moves for reductions (GCN row = 16 lanes): rotate right within each row, and
+// broadcast lane 15 / 31 into the following row(s) (rows outside row_mask read zero).
+constexpr int DPP_ROW_ROR4 = 0x124, DPP_ROW_ROR8 = 0x128, DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+constexpr int DPP_QUAD_SWAP1 = 0xB1, DPP_QUAD_SWAP2 = 0x4E;   // quad_perm [1,0,3,2], [2,3,0,1]
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW_MASK, 0xF,
+                                                               ROW_MASK == 0xF));
+}
+
+// Sum of one value per row position over the four rows of a wave, with every lane of a row
+// holding its row's total on entry: the total lands in lane 63 and is returned wave-uniform.
+__device__ __forceinline__ float rows_sum(float v) {
+  v += dpp_move<DPP_ROW_BCAST15, 0xA>(v);   // rows 1, 3 += rows 0, 2
+  v += dpp_move<DPP_ROW_BCAST31, 0xC>(v);   // rows 2, 3 += row 1
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+// Sum over the 64 lanes of a wave (wave-uniform result).
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  v += dpp_move<DPP_QUAD_SWAP1>(v);
+  v += dpp_move<DPP_QUAD_SWAP2>(v);
+  v += dpp_move<DPP_ROW_ROR4>(v);
+  v += dpp_move<DPP_ROW_ROR8>(v);
+  return rows_sum(v);
+}
+
+// Sum over the quads of a wave of a value that is the same in the four lanes of each quad.
+__device__ __forceinline__ float wave_sum_quads(float v) {
+  v += dpp_move<DPP_ROW_ROR4>(v);
+  v += dpp_move<DPP_ROW_ROR8>(v);
+  return rows_sum(v);
 }
 
 }  // namespace auv

@@ -45,7 +45,7 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
   mlp_load(w, b, ACT, wave, lane, R, S);
   if (tid < 256) S.x[tid >> 6][lane] = bf16x8{};
   const bool phys = wave < 4;              // physics waves (wave-uniform)
-  const quad::QK K = quad::make_qk(lane, V);
+  const quad::QK K = quad::make_qk(lane);
   const int c = K.c;
   const int slot = lane >> 2;              // environment within this wave's tile
   const int env = 16 * wave + slot;        // environment within the workgroup
@@ -134,14 +134,19 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
     // policy output for this lane's two action components (fixed-order partial sums)
     float a0, a1;
     {
-      float s0 = S.mu[0][env][2 * c], s1 = S.mu[0][env][2 * c + 1];
+      float2 m[MLP_WAVES];
+#pragma unroll
+      for (int ww = 0; ww < MLP_WAVES; ++ww) m[ww] = *reinterpret_cast<const float2*>(&S.mu[ww][env][2 * c]);
+      const float2 bb = *reinterpret_cast<const float2*>(&S.b3[2 * c]);
+      __builtin_amdgcn_sched_barrier(0);   // issue all LDS reads before the first add
+      float s0 = m[0].x, s1 = m[0].y;
 #pragma unroll
       for (int ww = 1; ww < MLP_WAVES; ++ww) {
-        s0 += S.mu[ww][env][2 * c];
-        s1 += S.mu[ww][env][2 * c + 1];
+        s0 += m[ww].x;
+        s1 += m[ww].y;
       }
-      a0 = S.b3[2 * c] + s0;
-      a1 = S.b3[2 * c + 1] + s1;
+      a0 = bb.x + s0;
+      a1 = bb.y + s1;
     }
     if (SAMPLE) {
       // lane c draws the Box-Muller pair k = c from words (2c, 2c+1): block c / 2
@@ -170,7 +175,8 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
       *reinterpret_cast<f32x4*>(&Tm[4]) = *reinterpret_cast<const f32x4*>(&S.alloc[4 + c][4]);
       quad::wrench(Tf, Tm, a0, a1, u0, u1, tf, tm, usq);
     }
-    for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tf, tm, E.h, p, q, v, om);
+    const float tfi = tf * M.iMlin;
+    for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, p, q, v, om);
     ep += 1;
     float pr, qr, dist, theta;
     quad::reference(E, K, F, ep, pr, qr);
@@ -178,9 +184,10 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
     const float reward = -dist - 0.5f * theta - 0.01f * usq;
     const bool done = (ep == E.H);
     const bool lead = valid && c == 0;
-    if (O.stats_work)
-      stats_push(SB, O.stats_work, T, t, lane, 4 * blockIdx.x + wave, 4 * gridDim.x, lead ? reward : 0.0f,
-                 (lead && done) ? 1.0f : 0.0f, lead ? dist : 0.0f);
+    if (O.stats_work)   // reward, done and dist are the same in the four lanes of a quad
+      stats_park(SB, O.stats_work, T, t, lane, 4 * blockIdx.x + wave, 4 * gridDim.x,
+                 wave_sum_quads(valid ? reward : 0.0f), wave_sum_quads((valid && done) ? 1.0f : 0.0f),
+                 wave_sum_quads(valid ? dist : 0.0f));
     if (lead) {
       if (O.reward) O.reward[ti] = reward;
       if (O.done) O.done[ti] = done ? 1.0f : 0.0f;

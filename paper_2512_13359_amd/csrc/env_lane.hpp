@@ -89,9 +89,8 @@ __device__ __forceinline__ void lane_step(const VehArgs& V, const EnvArgs& E, ui
 // ([3][G][T] layout), so each step costs no memory traffic of its own.
 struct StatsBuf { float v[3]; };
 
-__device__ __forceinline__ void stats_push(StatsBuf& B, float* __restrict__ work, int T, int t, int lane,
-                                           int g, int G, float r, float d, float p) {
-  const float sr = wave_sum(r), sd = wave_sum(d), sp = wave_sum(p);
+__device__ __forceinline__ void stats_park(StatsBuf& B, float* __restrict__ work, int T, int t, int lane,
+                                           int g, int G, float sr, float sd, float sp) {
   const int slot = t & 63;
   if (lane == slot) { B.v[0] = sr; B.v[1] = sd; B.v[2] = sp; }
   if (slot == 63 || t == T - 1) {
@@ -101,6 +100,11 @@ __device__ __forceinline__ void stats_push(StatsBuf& B, float* __restrict__ work
       for (int s = 0; s < 3; ++s) work[((size_t)s * G + g) * T + t0 + lane] = B.v[s];
     }
   }
+}
+
+__device__ __forceinline__ void stats_push(StatsBuf& B, float* __restrict__ work, int T, int t, int lane,
+                                           int g, int G, float r, float d, float p) {
+  stats_park(B, work, T, t, lane, g, G, wave_sum(r), wave_sum(d), wave_sum(p));
 }
 
 // Per-step outputs shared by the environment loops.

@@ -19,7 +19,6 @@ constexpr int P1 = QP(1, 2, 0, 3);    // lane c reads component c+1 (mod 3)
 constexpr int P2 = QP(2, 0, 1, 3);    // lane c reads component c+2 (mod 3)
 constexpr int SW1 = QP(1, 0, 3, 2), SW2 = QP(2, 3, 0, 1);
 constexpr int BC0 = QP(0, 0, 0, 0), BC1 = QP(1, 1, 1, 1), BC2 = QP(2, 2, 2, 2), BC3 = QP(3, 3, 3, 3);
-constexpr int XE3 = QP(1, 0, 2, 3);   // (e x e3) = (e_y, -e_x, 0)
 constexpr int XE1 = QP(0, 2, 1, 3);   // (e x e1) = (0, e_z, -e_y)
 constexpr int XE2 = QP(2, 1, 0, 3);   // (e x e2) = (-e_z, 0, e_x)
 
@@ -28,8 +27,10 @@ __device__ __forceinline__ float dpp(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), C, 0xF, 0xF, true));
 }
 
-// sum over the four lanes of a quad, every lane gets it
+// sum over the four lanes of a quad, every lane gets it.  Not contracted with the product
+// that usually feeds it: an fma would need the swapped value as its own moved operand.
 __device__ __forceinline__ float qsum(float x) {
+#pragma clang fp contract(off)
   x += dpp<SW1>(x);
   return x + dpp<SW2>(x);
 }
@@ -43,35 +44,39 @@ __device__ __forceinline__ float cross(float a, const Perm& b) { return dpp<P1>(
 struct QK {
   int c;
   float m3;    // 1 in vector lanes, 0 in lane 3
+  float m3x2;  // 2 m3
   float d2;    // e3 (1 in lane 2)
-  float sx3;   // sign pattern of e x e3: (+1, -1, 0, 0)
   float sx1;   // sign pattern of e x e1: (0, +1, -1, 0)
   float sx2;   // sign pattern of e x e2: (-1, 0, +1, 0)
   float e1, e2;
-  float BmW;
+  float hm3;   // 1/2 in vector lanes
+  float hs3;   // -1/2 in lane 3
 };
 
-__device__ __forceinline__ QK make_qk(int lane, const VehArgs& V) {
+__device__ __forceinline__ QK make_qk(int lane) {
   QK K;
   K.c = lane & 3;
   K.m3 = K.c < 3 ? 1.0f : 0.0f;
+  K.m3x2 = 2.0f * K.m3;
   K.d2 = K.c == 2 ? 1.0f : 0.0f;
   K.e1 = K.c == 0 ? 1.0f : 0.0f;
   K.e2 = K.c == 1 ? 1.0f : 0.0f;
-  K.sx3 = K.c == 0 ? 1.0f : (K.c == 1 ? -1.0f : 0.0f);
   K.sx1 = K.c == 1 ? 1.0f : (K.c == 2 ? -1.0f : 0.0f);
   K.sx2 = K.c == 0 ? -1.0f : (K.c == 2 ? 1.0f : 0.0f);
-  K.BmW = V.BmW;
+  K.hm3 = 0.5f * K.m3;
+  K.hs3 = K.c == 3 ? -0.5f : 0.0f;
   return K;
 }
 
-// Per-lane (component c) model constants of one environment; zero in lane 3.
+// Per-lane (component c) model constants of one environment; zero in lane 3.  Indices of
+// the neighbouring components are taken mod 3 (c+1, c+2).
 struct QModel {
-  float Mlin, iMlin, A1, DLl, DQl;   // linear DOF c
-  float Mang, iMang, DLa, DQa;       // angular DOF c
-  float cw;                          // world current
-  Perm cwP;                          // its rotations
-  Perm BrbP;                         // rotations of B r_b
+  float iMlin;                       // 1 / (m + added mass), linear DOF c
+  float KA1, KA2n;                   // Mlin_c / Mlin_{c+2}, -Mlin_c / Mlin_{c+1}
+  float DLi, DQi, BmWi;              // linear damping and (B - W), divided by Mlin_c
+  float Mang, iMang, A1, DLa, DQa;   // angular DOF c; A1 = linear added mass (Munk term)
+  float cw, cw1, cw2;                // world current, its components c+1 and c+2
+  float Brb1, Brb2n;                 // (B r_b)_{c+1}, -(B r_b)_{c+2}
 };
 
 // Per-lane reference data: lanes 0-2 the Lissajous position component (in turns), lane 3
@@ -93,18 +98,26 @@ __device__ __forceinline__ void make_lane_consts(const VehArgs& V, const QK& K, 
                                                  QRef& F) {
   Model S;
   make_model(V, P, S);
-  M.Mlin = pick(K, S.Mlin[0], S.Mlin[1], S.Mlin[2], 0.0f);
-  M.iMlin = pick(K, S.iMlin[0], S.iMlin[1], S.iMlin[2], 0.0f);
-  M.A1 = pick(K, S.A1[0], S.A1[1], S.A1[2], 0.0f);
-  M.DLl = pick(K, S.DL[0], S.DL[1], S.DL[2], 0.0f);
-  M.DQl = pick(K, S.DQ[0], S.DQ[1], S.DQ[2], 0.0f);
-  M.Mang = pick(K, S.Mang[0], S.Mang[1], S.Mang[2], 0.0f);
-  M.iMang = pick(K, S.iMang[0], S.iMang[1], S.iMang[2], 0.0f);
-  M.DLa = pick(K, S.DL[3], S.DL[4], S.DL[5], 0.0f);
-  M.DQa = pick(K, S.DQ[3], S.DQ[4], S.DQ[5], 0.0f);
-  M.cw = pick(K, P.cw[0], P.cw[1], P.cw[2], 0.0f);
-  M.cwP = perm(M.cw);
-  M.BrbP = perm(pick(K, V.Brb[0], V.Brb[1], V.Brb[2], 0.0f));
+  // component c, c+1 and c+2 (mod 3) of a 3-vector given by its three entries
+  auto c0 = [&](const float* x) { return pick(K, x[0], x[1], x[2], 0.0f); };
+  auto c1 = [&](const float* x) { return pick(K, x[1], x[2], x[0], 0.0f); };
+  auto c2 = [&](const float* x) { return pick(K, x[2], x[0], x[1], 0.0f); };
+  M.iMlin = c0(S.iMlin);
+  M.KA1 = c0(S.Mlin) * c2(S.iMlin);
+  M.KA2n = -(c0(S.Mlin) * c1(S.iMlin));
+  M.DLi = c0(S.DL) * M.iMlin;
+  M.DQi = c0(S.DQ) * M.iMlin;
+  M.BmWi = V.BmW * M.iMlin;
+  M.Mang = c0(S.Mang);
+  M.iMang = c0(S.iMang);
+  M.A1 = c0(S.A1);
+  M.DLa = c0(S.DL + 3);
+  M.DQa = c0(S.DQ + 3);
+  M.cw = c0(P.cw);
+  M.cw1 = c1(P.cw);
+  M.cw2 = c2(P.cw);
+  M.Brb1 = c1(V.Brb);
+  M.Brb2n = -c2(V.Brb);
   constexpr float INV_2PI = 0.159154943091895336f, INV_4PI = 0.0795774715459476679f;
   F.pg = pick(K, P.pg[0], P.pg[1], P.pg[2], 0.0f);
   F.amp = pick(K, P.amp[0], P.amp[1], P.amp[2], 0.0f);
@@ -114,57 +127,68 @@ __device__ __forceinline__ void make_lane_consts(const VehArgs& V, const QK& K, 
 }
 
 // ------------------------------------------------------------ Fossen right side ----
-// Same equations as auv::rhs, one component per lane.  R x = s x + 2 (e.x) e + 2 w (e x x)
-// and R^T x = s x + 2 (e.x) e - 2 w (e x x) with s = 1 - 2 e.e (the Euler-Rodrigues
-// matrix I + 2 w S(e) + 2 S(e)^2 applied to a vector).
-__device__ __forceinline__ void rhs(const QK& K, const QModel& M, float tf, float tm, float q, float v,
+// Same equations as auv::rhs, one component per lane.  Rotation by the stage quaternion
+// (w, e), not renormalised: R x = s x + 2 (e.x) e + 2 w (e x x) and R^T x = s x +
+// 2 (e.x) e - 2 w (e x x) with s = 1 - 2 e.e (the Euler-Rodrigues matrix I + 2 w S(e) +
+// 2 S(e)^2 applied to a vector).
+//
+// Cross products cost no lane moves of their own: with P1, P2 the quad permutations that
+// read component c+1, c+2,  x x y = P1(x . P1 y) - P2(x . P2 y)  (elementwise products);
+// the permutations are linear, and a per-component factor f moves inside them as
+// f . P1(z) = P1(z . P2 f), f . P2(z) = P2(z . P1 f).  So each output that is a sum of
+// cross products (scaled or not) takes one P1 and one P2, fused into its final adds.  The
+// force equation is divided by the mass first (tfi = tau_f / Mlin and the constants of
+// QModel), so that its cross product and the current's c_b x w share those two moves.
+__device__ __forceinline__ void rhs(const QK& K, const QModel& M, float tfi, float tm, float q, float v,
                                     float om, float& dp, float& dq, float& dv, float& dw) {
   const float e = q * K.m3;
-  const float wb = dpp<BC3>(q);
+  const float E2 = q * K.m3x2;                        // 2 e
+  const float wb = dpp<BC3>(q);                       // w in every lane
+  const float e1 = dpp<P1>(e), e2 = dpp<P2>(e);       // e_{c+1}, e_{c+2}
+  const float wb2 = wb + wb;
+  const float g1 = wb2 * e1, g2 = wb2 * e2;
   const float s = __builtin_fmaf(-2.0f, qsum(e * e), 1.0f);
-  const Perm eP = perm(e);
-  // dp = R v
-  const float ev = qsum(e * v);
-  const float exv = -cross(v, eP);
-  dp = __builtin_fmaf(s, v, 2.0f * __builtin_fmaf(ev, e, wb * exv));
-  // c_b = R^T c_w
-  const float ec = qsum(e * M.cw);
-  const float excw = -cross(M.cw, eP);
-  const float cb = __builtin_fmaf(s, M.cw, 2.0f * __builtin_fmaf(ec, e, -wb * excw));
-  // k = R^T e3
-  const float ez = dpp<BC2>(e);
-  const float exe3 = dpp<XE3>(e) * K.sx3;
-  const float k = __builtin_fmaf(s, K.d2, 2.0f * __builtin_fmaf(ez, e, -wb * exe3));
+  // dp = R v, with 2 w (e x v) = P2(g2 v) - P1(g1 v)
+  dp = __builtin_fmaf(qsum(E2 * v), e, s * v) + dpp<P2>(g2 * v) + dpp<P1>(-(g1 * v));
+  // c_b = R^T c_w, with e x c_w = e1 cw2 - e2 cw1
+  float cb = __builtin_fmaf(qsum(E2 * M.cw), e, s * M.cw);
+  cb = __builtin_fmaf(-g1, M.cw2, cb);
+  cb = __builtin_fmaf(g2, M.cw1, cb);
+  // k = R^T e3, with e x e3 = (e_y, -e_x, 0) = e1 [c = 0] - e2 [c = 1]
+  float k = __builtin_fmaf(dpp<BC2>(E2), e, s * K.d2);
+  k = __builtin_fmaf(-g1, K.e1, k);
+  k = __builtin_fmaf(g2, K.e2, k);
   const float vr = v - cb;
-  const Perm wP = perm(om);
-  // linear: tau_f - w x (Mlin vr) - (DL + DQ |vr|) vr - (B - W) k
-  const float a = M.Mlin * vr;
-  float F = tf + cross(a, wP);
-  F = __builtin_fmaf(-__builtin_fmaf(M.DQl, fabsf(vr), M.DLl), vr, F);
-  F = __builtin_fmaf(-K.BmW, k, F);
-  // angular: tau_m - w x (Mang w) - vr x (A1 vr) - B r_b x k - (DL + DQ |w|) w
+  const float w1 = dpp<P1>(om), w2 = dpp<P2>(om);
+  const float r1 = dpp<P1>(vr), r2 = dpp<P2>(vr);
+  // dv = (tau_f + (Mlin vr) x w - (DL + DQ |vr|) vr - (B - W) k) / Mlin + c_b x w
+  const float al = w1 * __builtin_fmaf(vr, M.KA1, cb);
+  const float be = w2 * __builtin_fmaf(vr, M.KA2n, -cb);
+  float fb = __builtin_fmaf(-__builtin_fmaf(M.DQi, fabsf(vr), M.DLi), vr, tfi);
+  fb = __builtin_fmaf(-M.BmWi, k, fb);
+  dv = fb + dpp<P1>(al) + dpp<P2>(be);
+  // dw = (tau_m + (Mang w) x w + (A1 vr) x vr + k x (B r_b) - (DL + DQ |w|) w) / Mang
   const float b = M.Mang * om;
-  const float c = M.A1 * vr;
-  const Perm vrP = perm(vr);
-  float G = tm + cross(b, wP) + cross(c, vrP) + cross(k, M.BrbP);
-  G = __builtin_fmaf(-__builtin_fmaf(M.DQa, fabsf(om), M.DLa), om, G);
-  dv = __builtin_fmaf(F, M.iMlin, cross(cb, wP));
-  dw = G * M.iMang;
+  const float a1 = M.A1 * vr;
+  const float ga = __builtin_fmaf(k, M.Brb1, __builtin_fmaf(a1, r1, b * w1));
+  const float gb = __builtin_fmaf(k, M.Brb2n, __builtin_fmaf(-a1, r2, -(b * w2)));
+  const float G = __builtin_fmaf(-__builtin_fmaf(M.DQa, fabsf(om), M.DLa), om, tm);
+  dw = (G + dpp<P1>(ga) + dpp<P2>(gb)) * M.iMang;
   // dq = 1/2 q (x) (0, w): vector part 1/2 (w om + e x om), scalar part -1/2 e.om
-  const float eo = qsum(e * om);
-  const float exo = -cross(om, eP);
-  dq = K.c < 3 ? 0.5f * __builtin_fmaf(wb, om, exo) : -0.5f * eo;
+  const float exo = __builtin_fmaf(e1, w2, -(e2 * w1));
+  dq = __builtin_fmaf(K.hs3, qsum(e * om), K.hm3 * __builtin_fmaf(wb, om, exo));
 }
 
-__device__ __forceinline__ void rk4(const QK& K, const QModel& M, float tf, float tm, float h, float& p, float& q,
+// One RK4 substep of length h with the wrench held (tfi = tau_f / Mlin).
+__device__ __forceinline__ void rk4(const QK& K, const QModel& M, float tfi, float tm, float h, float& p, float& q,
                                     float& v, float& om) {
   float dp, dq, dv, dw;
-  rhs(K, M, tf, tm, q, v, om, dp, dq, dv, dw);
+  rhs(K, M, tfi, tm, q, v, om, dp, dq, dv, dw);
   float ap = dp, aq = dq, av = dv, aw = dw;
 #pragma unroll
   for (int stage = 1; stage < 4; ++stage) {
     const float cs = (stage == 3) ? h : 0.5f * h;
-    rhs(K, M, tf, tm, __builtin_fmaf(cs, dq, q), __builtin_fmaf(cs, dv, v), __builtin_fmaf(cs, dw, om), dp, dq, dv,
+    rhs(K, M, tfi, tm, __builtin_fmaf(cs, dq, q), __builtin_fmaf(cs, dv, v), __builtin_fmaf(cs, dw, om), dp, dq, dv,
         dw);
     const float wgt = (stage == 3) ? 1.0f : 2.0f;
     ap = __builtin_fmaf(wgt, dp, ap);
@@ -219,8 +243,10 @@ __device__ __forceinline__ void observe(const QK& K, float p, float q, float v, 
   o.dpb = rot_T(R, pr - p);
   // columns 0 and 1 of R_ref: R_ref e1 = s e1 + 2 e_x e + 2 w (e x e1), same for e2
   const QRot Rr = qrot(K, qr);
-  const float r0 = __builtin_fmaf(Rr.s, K.e1, 2.0f * __builtin_fmaf(dpp<BC0>(Rr.e), Rr.e, Rr.wb * dpp<XE1>(Rr.e) * K.sx1));
-  const float r1 = __builtin_fmaf(Rr.s, K.e2, 2.0f * __builtin_fmaf(dpp<BC1>(Rr.e), Rr.e, Rr.wb * dpp<XE2>(Rr.e) * K.sx2));
+  const float r0 =
+      __builtin_fmaf(Rr.s, K.e1, 2.0f * __builtin_fmaf(dpp<BC0>(Rr.e), Rr.e, Rr.wb * dpp<XE1>(Rr.e) * K.sx1));
+  const float r1 =
+      __builtin_fmaf(Rr.s, K.e2, 2.0f * __builtin_fmaf(dpp<BC1>(Rr.e), Rr.e, Rr.wb * dpp<XE2>(Rr.e) * K.sx2));
   o.c0 = rot_T(R, r0);
   o.c1 = rot_T(R, r1);
   dist = sqrtf(qsum(o.dpb * o.dpb));
