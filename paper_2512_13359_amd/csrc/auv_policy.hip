@@ -4,13 +4,34 @@
 
 #include "auv_internal.hpp"
 #include "mlp_mfma.hpp"
+#include "mlp_tile.hpp"
 #include "quad_env.hpp"
 
 namespace auv {
 
+// Fused rollout workgroup: ROLLOUT_MLP_WAVES MLP waves of ROLLOUT_FPW hidden features each,
+// then four physics waves (one 16-environment tile each, 64 environments in all).
+constexpr int ROLLOUT_FPW = 64;
+constexpr int ROLLOUT_MLP_WAVES = HID / ROLLOUT_FPW;
+constexpr int ROLLOUT_KO = ROLLOUT_FPW / 32;   // K tiles of hidden features per MLP wave
+constexpr int ROLLOUT_THREADS = 64 * (ROLLOUT_MLP_WAVES + 4);
+
+// Shared memory of one rollout workgroup (64 environments = four 16-environment tiles).
+struct RolloutShared {
+  bf16x8 x[4][64];                          // layer-1 operand per tile: K = 32 (23 used) x 16 envs
+  bf16x8 h[8][4][64];                       // hidden-1 operand [K tile][tile][lane]
+  float mu[4][ROLLOUT_MLP_WAVES][16][NOUT_PAD];   // output partials [tile][MLP wave][env][row]
+  float b1k[HID];                           // hidden-1 biases x 2 log2 e
+  float b3[16];                             // output biases
+  float alloc[8][8];                        // thrust rows x f_max: force rows 0-2, moment rows 4-6
+  unsigned obs_ready[4];                    // per tile: observations published (1 + steps done)
+  unsigned h1_ready[4];                     // per tile: MLP waves done with hidden 1 (all, each step)
+  unsigned mu_ready[4];                     // per tile: MLP waves done with the output (all, each step)
+};
+
 // Observation features of one environment written by the four lanes of its quad into the
-// layer-1 operand (bf16 element stores; features 23..31 stay zero).
-__device__ __forceinline__ void put_obs_quad(MlpShared& S, int nt, int r, int c, const quad::QObs& o, float v,
+// layer-1 operand of tile nt (bf16 element stores; features 23..31 stay zero).
+__device__ __forceinline__ void put_obs_quad(RolloutShared& S, int nt, int r, int c, const quad::QObs& o, float v,
                                              float om, float u0, float u1) {
   __bf16* xs = reinterpret_cast<__bf16*>(&S.x[0][0]);
   auto put = [&](int k, float x) {
@@ -28,37 +49,94 @@ __device__ __forceinline__ void put_obs_quad(MlpShared& S, int nt, int r, int c,
   put(16 + 2 * c, u1);
 }
 
-// One workgroup = 8 waves = 64 environments for all T steps.  Waves 0-3 step 16
-// environments each with four lanes per environment (quad layout, quad_env.hpp); all
-// eight waves run the MLP on MFMA with their weight slices in registers (two per SIMD,
-// so MFMA and tanh of different waves overlap).  Three barriers per step:
-//   obs in LDS -> layer 1 -> hidden-1 in LDS -> layers 2, 3 -> partials in LDS -> physics.
+// Point-to-point ordering between the waves of a workgroup through LDS counters: the
+// producer's LDS writes complete before its count is raised; the consumer polls with
+// s_sleep.  Every wait is bounded: a wait that would never end (a defect) gives up after
+// about a second of polling, and the caller abandons the rollout.
+constexpr uint32_t SYNC_SPIN_LIMIT = 1u << 22;
+
+__device__ __forceinline__ void publish(unsigned* counter, int lane) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  if (lane == 0) __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ bool wait_for(const unsigned* counter, unsigned target) {
+  for (uint32_t spin = 0; spin < SYNC_SPIN_LIMIT; ++spin) {
+    const unsigned seen =
+        __builtin_amdgcn_readfirstlane(__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+    if (seen >= target) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      return true;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return false;
+}
+
+// MLP wave m: for every step and tile in order, layer 1 as soon as the tile's observations
+// are published, layers 2 and 3 once every MLP wave has published its hidden-1 K tiles of
+// that tile.
+__device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const uint16_t* __restrict__ w,
+                                                 const float* __restrict__ b, int m, int lane) {
+  const int g = lane >> 4, r = lane & 15;
+  const unsigned NW = ROLLOUT_MLP_WAVES;
+  TileMlpRegs<ROLLOUT_FPW> R;
+  tile_mlp_load<ROLLOUT_FPW>(w, b, ACT, m, lane, R);
+  for (int t = 0; t < T; ++t) {
+#pragma unroll 1
+    for (int k = 0; k < 4; ++k) {
+      if (!wait_for(&S.obs_ready[k], (unsigned)t + 1)) return;
+      bf16x8 own[ROLLOUT_KO];
+      tile_layer1<ROLLOUT_FPW>(R, S.x[k][lane], S.b1k, m, lane, own);
+#pragma unroll
+      for (int ii = 0; ii < ROLLOUT_KO; ++ii) S.h[ROLLOUT_KO * m + ii][k][lane] = own[ii];
+      publish(&S.h1_ready[k], lane);
+      if (!wait_for(&S.h1_ready[k], NW * (unsigned)(t + 1))) return;
+      const f32x4 o = tile_layer23<ROLLOUT_FPW>(R, own, [&](int kt) { return S.h[kt][k][lane]; }, m);
+      if (g < 2) *reinterpret_cast<f32x4*>(&S.mu[k][m][r][4 * g]) = o;
+      publish(&S.mu_ready[k], lane);
+    }
+  }
+}
+
+// One workgroup = 64 environments for all T steps.  The first ROLLOUT_MLP_WAVES waves are
+// MLP waves (weights in registers, rollout_mlp_wave); the last four are physics waves,
+// each stepping one tile of 16 environments with four lanes per environment (quad layout,
+// quad_env.hpp).  Each tile runs its own chain obs -> MLP -> action -> physics -> obs,
+// ordered by LDS counters instead of workgroup barriers, so the physics of one tile
+// overlaps the MLP of the others; every SIMD holds MLP waves and one physics wave.
 template <bool SAMPLE>
-__global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
+__global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
                                                            StepOut O, const uint16_t* __restrict__ w,
                                                            const float* __restrict__ b,
                                                            const float* __restrict__ log_std) {
-  __shared__ MlpShared S;
+  __shared__ RolloutShared S;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  MlpRegs R;
-  mlp_load(w, b, ACT, wave, lane, R, S);
   if (tid < 256) S.x[tid >> 6][lane] = bf16x8{};
-  const bool phys = wave < 4;              // physics waves (wave-uniform)
-  const quad::QK K = quad::make_qk(lane);
-  const int c = K.c;
-  const int slot = lane >> 2;              // environment within this wave's tile
-  const int env = 16 * wave + slot;        // environment within the workgroup
-  const int i = blockIdx.x * 64 + env;
-  const bool valid = phys && i < E.n;
-  const size_t N = (size_t)E.n, TN = (size_t)T * N;
-  const uint32_t gid = E.env_offset + (uint32_t)i;
-  const int cv = c < 3 ? c : 0;            // a valid component row for lane 3's loads
-  if (tid < 64) {                          // allocation rows x f_max into LDS
+  if (tid < HID) S.b1k[tid] = b[tid] * TWO_LOG2E;
+  if (tid < 16) S.b3[tid] = tid < ACT ? b[2 * HID + tid] : 0.0f;
+  if (tid < 64) {                          // allocation rows x f_max
     const int row = tid >> 3, j = tid & 7;
     const int src = row < 3 ? row : (row >= 4 && row < 7 ? row - 1 : -1);
     S.alloc[row][j] = src >= 0 ? V.alloc[src * 8 + j] * V.f_max : 0.0f;
   }
+  if (tid < 4) S.obs_ready[tid] = S.h1_ready[tid] = S.mu_ready[tid] = 0u;
+  __syncthreads();
+  if (wave < ROLLOUT_MLP_WAVES) {
+    rollout_mlp_wave(S, T, w, b, wave, lane);
+    return;
+  }
+
+  const int k = wave - ROLLOUT_MLP_WAVES;  // this physics wave's tile
+  const quad::QK K = quad::make_qk(lane);
+  const int c = K.c;
+  const int slot = lane >> 2;              // environment within the tile
+  const int i = blockIdx.x * 64 + 16 * k + slot;
+  const bool valid = i < E.n;
+  const size_t N = (size_t)E.n, TN = (size_t)T * N;
+  const uint32_t gid = E.env_offset + (uint32_t)i;
+  const int cv = c < 3 ? c : 0;            // a valid component row for lane 3's loads
 
   float p, q, v, om, u0, u1;
   int ep = 0;
@@ -109,18 +187,23 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
   };
   store_traj(0);
   StatsBuf SB{};
-  __syncthreads();                          // S.x zeroed, biases staged
-  if (phys) put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
-  __syncthreads();
-  OwnH1 H;
+  float st_r = 0.0f, st_d = 0.0f, st_p = 0.0f;   // this wave's statistics of the previous step
+  put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
+  publish(&S.obs_ready[k], lane);
   for (int t = 0; t < T; ++t) {
-    mlp_layer1(R, S, wave, lane, H);
-    __syncthreads();
-    mlp_layer23(R, S, wave, lane, H);
-    __syncthreads();
-    if (phys) {
     const size_t ti = (size_t)t * N + (size_t)i;
-    if (O.obs && valid) {
+    // Work that does not need the action, done while the MLP waves evaluate the policy:
+    // the first RK4 stage without the wrench (it enters the derivative additively), the
+    // reference of the next step, and the previous step's batch statistics.
+    float dp1, dq1, dv1, dw1;
+    quad::rhs(K, M, 0.0f, 0.0f, q, v, om, dp1, dq1, dv1, dw1);
+    float pr, qr;
+    quad::reference(E, K, F, ep + 1, pr, qr);
+    if (O.stats_work && t > 0) {   // reward, done and dist are the same in the four lanes of a quad
+      const float sr = wave_sum_quads(st_r), sd = wave_sum_quads(st_d), sp = wave_sum_quads(st_p);
+      stats_park(SB, O.stats_work, T, t - 1, lane, 4 * blockIdx.x + k, 4 * gridDim.x, sr, sd, sp);
+    }
+    if (O.obs && valid) {                  // o_t, recorded while the MLP waves work on it
       if (c < 3) {
         O.obs[c * TN + ti] = ob.dpb;
         O.obs[(3 + c) * TN + ti] = ob.c0;
@@ -131,36 +214,41 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
       O.obs[(15 + 2 * c) * TN + ti] = u0;
       O.obs[(16 + 2 * c) * TN + ti] = u1;
     }
+    if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1))) {   // abandoned: poison
+      p = q = v = om = __builtin_nanf("");
+      break;
+    }
     // policy output for this lane's two action components (fixed-order partial sums)
     float a0, a1;
     {
-      float2 m[MLP_WAVES];
+      float2 mm[ROLLOUT_MLP_WAVES];
 #pragma unroll
-      for (int ww = 0; ww < MLP_WAVES; ++ww) m[ww] = *reinterpret_cast<const float2*>(&S.mu[ww][env][2 * c]);
+      for (int ww = 0; ww < ROLLOUT_MLP_WAVES; ++ww)
+        mm[ww] = *reinterpret_cast<const float2*>(&S.mu[k][ww][slot][2 * c]);
       const float2 bb = *reinterpret_cast<const float2*>(&S.b3[2 * c]);
       __builtin_amdgcn_sched_barrier(0);   // issue all LDS reads before the first add
-      float s0 = m[0].x, s1 = m[0].y;
+      float s0 = mm[0].x, s1 = mm[0].y;
 #pragma unroll
-      for (int ww = 1; ww < MLP_WAVES; ++ww) {
-        s0 += m[ww].x;
-        s1 += m[ww].y;
+      for (int ww = 1; ww < ROLLOUT_MLP_WAVES; ++ww) {
+        s0 += mm[ww].x;
+        s1 += mm[ww].y;
       }
       a0 = bb.x + s0;
       a1 = bb.y + s1;
     }
+    float lp = 0.0f;
     if (SAMPLE) {
       // lane c draws the Box-Muller pair k = c from words (2c, 2c+1): block c / 2
       const uint32_t step = gstep0 + (uint32_t)t;
-      const U4 r = philox(U4{gid, step, 2u, (uint32_t)(c >> 1)}, E.key0, E.key1);
-      const uint32_t w0 = (c & 1) ? r.z : r.x, w1 = (c & 1) ? r.w : r.y;
+      const U4 rr = philox(U4{gid, step, 2u, (uint32_t)(c >> 1)}, E.key0, E.key1);
+      const uint32_t w0 = (c & 1) ? rr.z : rr.x, w1 = (c & 1) ? rr.w : rr.y;
       const float rad = sqrtf(-2.0f * logf(u01_open0(w0)));
       float sn, cs;
       sincos_turns(u01(w1), &sn, &cs);
       const float e0 = rad * cs, e1 = rad * sn;
       a0 = __builtin_fmaf(sig0, e0, a0);
       a1 = __builtin_fmaf(sig1, e1, a1);
-      const float lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) - 4.0f * 1.83787706640934548f;
-      if (O.logp && valid && c == 0) O.logp[ti] = lp;
+      lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) - 4.0f * 1.83787706640934548f;
     }
     if (O.act && valid) {
       O.act[(2 * c) * TN + ti] = a0;
@@ -176,22 +264,18 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
       quad::wrench(Tf, Tm, a0, a1, u0, u1, tf, tm, usq);
     }
     const float tfi = tf * M.iMlin;
-    for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, p, q, v, om);
+    if (E.substeps > 0) {
+      quad::rk4_from(K, M, tfi, tm, E.h, p, q, v, om, dp1, dq1, dv1 + tfi, __builtin_fmaf(tm, M.iMang, dw1));
+      for (int s = 1; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, p, q, v, om);
+    }
     ep += 1;
-    float pr, qr, dist, theta;
-    quad::reference(E, K, F, ep, pr, qr);
+    float dist, theta;
     quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
     const float reward = -dist - 0.5f * theta - 0.01f * usq;
     const bool done = (ep == E.H);
-    const bool lead = valid && c == 0;
-    if (O.stats_work)   // reward, done and dist are the same in the four lanes of a quad
-      stats_park(SB, O.stats_work, T, t, lane, 4 * blockIdx.x + wave, 4 * gridDim.x,
-                 wave_sum_quads(valid ? reward : 0.0f), wave_sum_quads((valid && done) ? 1.0f : 0.0f),
-                 wave_sum_quads(valid ? dist : 0.0f));
-    if (lead) {
-      if (O.reward) O.reward[ti] = reward;
-      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
-    }
+    st_r = valid ? reward : 0.0f;
+    st_d = (valid && done) ? 1.0f : 0.0f;
+    st_p = valid ? dist : 0.0f;
     if (done) {  // the whole quad takes this branch
       episode += 1u;
       State xs;
@@ -207,10 +291,20 @@ __global__ __launch_bounds__(MLP_THREADS, 1) void k_policy_rollout(VehArgs V, En
       quad::reference(E, K, F, 0, pr, qr);
       quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
     }
-    store_traj(t + 1);
-    put_obs_quad(S, wave, slot, c, ob, v, om, u0, u1);
+    put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
+    publish(&S.obs_ready[k], lane);
+    // global outputs of step t after the observation is published
+    const bool lead = valid && c == 0;
+    if (SAMPLE && O.logp && lead) O.logp[ti] = lp;
+    if (lead) {
+      if (O.reward) O.reward[ti] = reward;
+      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
     }
-    __syncthreads();
+    store_traj(t + 1);
+  }
+  if (O.stats_work && T > 0) {
+    const float sr = wave_sum_quads(st_r), sd = wave_sum_quads(st_d), sp = wave_sum_quads(st_p);
+    stats_park(SB, O.stats_work, T, T - 1, lane, 4 * blockIdx.x + k, 4 * gridDim.x, sr, sd, sp);
   }
   if (!valid) return;
   if (c < 3) {
@@ -319,10 +413,10 @@ int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, 
   const dim3 grid(groups_of(n));
   const uint16_t* w = (const uint16_t*)policy->w;
   if (sample)
-    hipLaunchKernelGGL(k_policy_rollout<true>, grid, dim3(MLP_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
+    hipLaunchKernelGGL(k_policy_rollout<true>, grid, dim3(ROLLOUT_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
                        policy->log_std);
   else
-    hipLaunchKernelGGL(k_policy_rollout<false>, grid, dim3(MLP_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
+    hipLaunchKernelGGL(k_policy_rollout<false>, grid, dim3(ROLLOUT_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
                        policy->log_std);
   if (int rc = check_launch("policy rollout")) return rc;
   if (value) {

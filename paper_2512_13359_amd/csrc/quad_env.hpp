@@ -179,11 +179,10 @@ __device__ __forceinline__ void rhs(const QK& K, const QModel& M, float tfi, flo
   dq = __builtin_fmaf(K.hs3, qsum(e * om), K.hm3 * __builtin_fmaf(wb, om, exo));
 }
 
-// One RK4 substep of length h with the wrench held (tfi = tau_f / Mlin).
-__device__ __forceinline__ void rk4(const QK& K, const QModel& M, float tfi, float tm, float h, float& p, float& q,
-                                    float& v, float& om) {
-  float dp, dq, dv, dw;
-  rhs(K, M, tfi, tm, q, v, om, dp, dq, dv, dw);
+// One RK4 substep of length h with the wrench held (tfi = tau_f / Mlin), given the
+// derivative (dp, dq, dv, dw) at the substep's start.
+__device__ __forceinline__ void rk4_from(const QK& K, const QModel& M, float tfi, float tm, float h, float& p,
+                                         float& q, float& v, float& om, float dp, float dq, float dv, float dw) {
   float ap = dp, aq = dq, av = dv, aw = dw;
 #pragma unroll
   for (int stage = 1; stage < 4; ++stage) {
@@ -202,6 +201,13 @@ __device__ __forceinline__ void rk4(const QK& K, const QModel& M, float tfi, flo
   v = __builtin_fmaf(h6, av, v);
   om = __builtin_fmaf(h6, aw, om);
   q *= rsqrtf(qsum(q * q));
+}
+
+__device__ __forceinline__ void rk4(const QK& K, const QModel& M, float tfi, float tm, float h, float& p, float& q,
+                                    float& v, float& om) {
+  float dp, dq, dv, dw;
+  rhs(K, M, tfi, tm, q, v, om, dp, dq, dv, dw);
+  rk4_from(K, M, tfi, tm, h, p, q, v, om, dp, dq, dv, dw);
 }
 
 // --------------------------------------------------- reference, observation ----------
