@@ -187,22 +187,37 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
   };
   store_traj(0);
   StatsBuf SB{};
-  float st_r = 0.0f, st_d = 0.0f, st_p = 0.0f;   // this wave's statistics of the previous step
+  // terms of the previous step's reward, finished in the next step's policy wait
+  float pv_q = 0.0f, pv_qr = 0.0f, pv_dist = 0.0f, pv_usq = 0.0f;
+  bool pv_done = false;
+  auto finish_step = [&](int t1) {   // reward, outputs and statistics of step t1
+    const float theta = quad::attitude_error(K, pv_q, pv_qr);
+    const float reward = -pv_dist - 0.5f * theta - 0.01f * pv_usq;
+    const size_t t1i = (size_t)t1 * N + (size_t)i;
+    if (valid && c == 0) {
+      if (O.reward) O.reward[t1i] = reward;
+      if (O.done) O.done[t1i] = pv_done ? 1.0f : 0.0f;
+    }
+    if (O.stats_work) {   // reward, done and dist are the same in the four lanes of a quad
+      const float sr = wave_sum_quads(valid ? reward : 0.0f);
+      const float sd = wave_sum_quads((valid && pv_done) ? 1.0f : 0.0f);
+      const float sp = wave_sum_quads(valid ? pv_dist : 0.0f);
+      stats_park(SB, O.stats_work, T, t1, lane, 4 * blockIdx.x + k, 4 * gridDim.x, sr, sd, sp);
+    }
+  };
   put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
   publish(&S.obs_ready[k], lane);
   for (int t = 0; t < T; ++t) {
     const size_t ti = (size_t)t * N + (size_t)i;
     // Work that does not need the action, done while the MLP waves evaluate the policy:
     // the first RK4 stage without the wrench (it enters the derivative additively), the
-    // reference of the next step, and the previous step's batch statistics.
+    // reference of the next step, and the previous step's reward and statistics.
     float dp1, dq1, dv1, dw1;
     quad::rhs(K, M, 0.0f, 0.0f, q, v, om, dp1, dq1, dv1, dw1);
     float pr, qr;
     quad::reference(E, K, F, ep + 1, pr, qr);
-    if (O.stats_work && t > 0) {   // reward, done and dist are the same in the four lanes of a quad
-      const float sr = wave_sum_quads(st_r), sd = wave_sum_quads(st_d), sp = wave_sum_quads(st_p);
-      stats_park(SB, O.stats_work, T, t - 1, lane, 4 * blockIdx.x + k, 4 * gridDim.x, sr, sd, sp);
-    }
+    quad::QRefCols rc = quad::ref_columns(K, qr);
+    if (t > 0) finish_step(t - 1);
     if (O.obs && valid) {                  // o_t, recorded while the MLP waves work on it
       if (c < 3) {
         O.obs[c * TN + ti] = ob.dpb;
@@ -236,7 +251,7 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
       a0 = bb.x + s0;
       a1 = bb.y + s1;
     }
-    float lp = 0.0f;
+    float e0 = 0.0f, e1 = 0.0f;
     if (SAMPLE) {
       // lane c draws the Box-Muller pair k = c from words (2c, 2c+1): block c / 2
       const uint32_t step = gstep0 + (uint32_t)t;
@@ -245,10 +260,10 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
       const float rad = sqrtf(-2.0f * logf(u01_open0(w0)));
       float sn, cs;
       sincos_turns(u01(w1), &sn, &cs);
-      const float e0 = rad * cs, e1 = rad * sn;
+      e0 = rad * cs;
+      e1 = rad * sn;
       a0 = __builtin_fmaf(sig0, e0, a0);
       a1 = __builtin_fmaf(sig1, e1, a1);
-      lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) - 4.0f * 1.83787706640934548f;
     }
     if (O.act && valid) {
       O.act[(2 * c) * TN + ti] = a0;
@@ -269,13 +284,14 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
       for (int s = 1; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, p, q, v, om);
     }
     ep += 1;
-    float dist, theta;
-    quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
-    const float reward = -dist - 0.5f * theta - 0.01f * usq;
+    float dist;
+    quad::observe(K, p, q, pr, rc, ob, dist);
     const bool done = (ep == E.H);
-    st_r = valid ? reward : 0.0f;
-    st_d = (valid && done) ? 1.0f : 0.0f;
-    st_p = valid ? dist : 0.0f;
+    pv_q = q;
+    pv_qr = qr;
+    pv_dist = dist;
+    pv_usq = usq;
+    pv_done = done;
     if (done) {  // the whole quad takes this branch
       episode += 1u;
       State xs;
@@ -289,23 +305,19 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
       v = om = 0.0f;
       u0 = u1 = 0.0f;
       quad::reference(E, K, F, 0, pr, qr);
-      quad::observe(K, p, q, v, om, pr, qr, ob, dist, theta);
+      rc = quad::ref_columns(K, qr);
+      quad::observe(K, p, q, pr, rc, ob, dist);
     }
     put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
     publish(&S.obs_ready[k], lane);
-    // global outputs of step t after the observation is published
-    const bool lead = valid && c == 0;
-    if (SAMPLE && O.logp && lead) O.logp[ti] = lp;
-    if (lead) {
-      if (O.reward) O.reward[ti] = reward;
-      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
+    // outputs of step t that the next observation does not need
+    if (SAMPLE && O.logp) {
+      const float lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) - 4.0f * 1.83787706640934548f;
+      if (valid && c == 0) O.logp[ti] = lp;
     }
     store_traj(t + 1);
   }
-  if (O.stats_work && T > 0) {
-    const float sr = wave_sum_quads(st_r), sd = wave_sum_quads(st_d), sp = wave_sum_quads(st_p);
-    stats_park(SB, O.stats_work, T, T - 1, lane, 4 * blockIdx.x + k, 4 * gridDim.x, sr, sd, sp);
-  }
+  if (T > 0) finish_step(T - 1);
   if (!valid) return;
   if (c < 3) {
     E.state[c * N + i] = p;

@@ -241,27 +241,37 @@ __device__ __forceinline__ float rot_T(const QRot& r, float x) {   // R^T x
   return __builtin_fmaf(r.s, x, 2.0f * __builtin_fmaf(ex, r.e, r.wb * cross(x, r.eP)));
 }
 
-// Observation components of this lane, |dp| and the attitude-error angle.
+// Columns 0 and 1 of the reference rotation R(q_ref), this lane's component:
+// R_ref e1 = s e1 + 2 e_x e + 2 w (e x e1), likewise for e2.  Depends only on the reference.
+struct QRefCols { float r0, r1; };
+__device__ __forceinline__ QRefCols ref_columns(const QK& K, float qr) {
+  const QRot Rr = qrot(K, qr);
+  QRefCols o;
+  o.r0 = __builtin_fmaf(Rr.s, K.e1, 2.0f * __builtin_fmaf(dpp<BC0>(Rr.e), Rr.e, Rr.wb * dpp<XE1>(Rr.e) * K.sx1));
+  o.r1 = __builtin_fmaf(Rr.s, K.e2, 2.0f * __builtin_fmaf(dpp<BC1>(Rr.e), Rr.e, Rr.wb * dpp<XE2>(Rr.e) * K.sx2));
+  return o;
+}
+
+// Observation components of this lane (body-frame position error and the body-frame
+// reference columns) and |dp|.
 struct QObs { float dpb, c0, c1; };
-__device__ __forceinline__ void observe(const QK& K, float p, float q, float v, float om, float pr, float qr,
-                                        QObs& o, float& dist, float& theta) {
+__device__ __forceinline__ void observe(const QK& K, float p, float q, float pr, const QRefCols& rc, QObs& o,
+                                        float& dist) {
   const QRot R = qrot(K, q);
   o.dpb = rot_T(R, pr - p);
-  // columns 0 and 1 of R_ref: R_ref e1 = s e1 + 2 e_x e + 2 w (e x e1), same for e2
-  const QRot Rr = qrot(K, qr);
-  const float r0 =
-      __builtin_fmaf(Rr.s, K.e1, 2.0f * __builtin_fmaf(dpp<BC0>(Rr.e), Rr.e, Rr.wb * dpp<XE1>(Rr.e) * K.sx1));
-  const float r1 =
-      __builtin_fmaf(Rr.s, K.e2, 2.0f * __builtin_fmaf(dpp<BC1>(Rr.e), Rr.e, Rr.wb * dpp<XE2>(Rr.e) * K.sx2));
-  o.c0 = rot_T(R, r0);
-  o.c1 = rot_T(R, r1);
+  o.c0 = rot_T(R, rc.r0);
+  o.c1 = rot_T(R, rc.r1);
   dist = sqrtf(qsum(o.dpb * o.dpb));
-  // q_err = q^* (x) q_ref: scalar w wr + e.er, vector w er - wr e - e x er
+}
+
+// Attitude-error angle 2 atan2(|vec(q_err)|, |scalar(q_err)|) of q_err = q^* (x) q_ref:
+// scalar w wr + e.er, vector w er - wr e - e x er.
+__device__ __forceinline__ float attitude_error(const QK& K, float q, float qr) {
+  const float e = q * K.m3, er = qr * K.m3;
+  const float wb = dpp<BC3>(q), wr = dpp<BC3>(qr);
   const float ew = qsum(q * qr);
-  const float vec = __builtin_fmaf(R.wb, Rr.e, -Rr.wb * R.e) - cross(R.e, Rr.eP);
-  theta = 2.0f * atan2f(sqrtf(qsum(vec * vec)), fabsf(ew));
-  (void)v;
-  (void)om;
+  const float vec = __builtin_fmaf(wb, er, -wr * e) - cross(e, perm(er));
+  return 2.0f * atan2f(sqrtf(qsum(vec * vec)), fabsf(ew));
 }
 
 // Clip this lane's two actions, broadcast all eight across the quad, body wrench with
