@@ -50,10 +50,11 @@ __device__ __forceinline__ void put_obs_quad(RolloutShared& S, int nt, int r, in
 }
 
 // Point-to-point ordering between the waves of a workgroup through LDS counters: the
-// producer's LDS writes complete before its count is raised; the consumer polls with
-// s_sleep.  Every wait is bounded: a wait that would never end (a defect) gives up after
-// about a second of polling, and the caller abandons the rollout.
-constexpr uint32_t SYNC_SPIN_LIMIT = 1u << 22;
+// producer's LDS writes complete before its count is raised; the consumer polls (each poll
+// is an LDS round trip, a few VALU slots).  Every wait is bounded: a wait that would never
+// end (a defect) gives up after about a second of polling, and the caller abandons the
+// rollout.
+constexpr uint32_t SYNC_SPIN_LIMIT = 1u << 24;
 
 __device__ __forceinline__ void publish(unsigned* counter, int lane) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -68,7 +69,6 @@ __device__ __forceinline__ bool wait_for(const unsigned* counter, unsigned targe
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
       return true;
     }
-    __builtin_amdgcn_s_sleep(1);
   }
   return false;
 }
@@ -91,8 +91,10 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
 #pragma unroll
       for (int ii = 0; ii < ROLLOUT_KO; ++ii) S.h[ROLLOUT_KO * m + ii][k][lane] = own[ii];
       publish(&S.h1_ready[k], lane);
+      f32x4 acc[ROLLOUT_FPW / 16];
+      tile_layer2_own<ROLLOUT_FPW>(R, own, acc);   // overlaps the wait for the other waves
       if (!wait_for(&S.h1_ready[k], NW * (unsigned)(t + 1))) return;
-      const f32x4 o = tile_layer23<ROLLOUT_FPW>(R, own, [&](int kt) { return S.h[kt][k][lane]; }, m);
+      const f32x4 o = tile_layer23<ROLLOUT_FPW>(R, acc, [&](int kt) { return S.h[kt][k][lane]; }, m);
       if (g < 2) *reinterpret_cast<f32x4*>(&S.mu[k][m][r][4 * g]) = o;
       publish(&S.mu_ready[k], lane);
     }

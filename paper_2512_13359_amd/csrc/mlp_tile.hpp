@@ -77,20 +77,27 @@ __device__ __forceinline__ void tile_layer1(const TileMlpRegs<FPW>& R, const bf1
   }
 }
 
-// Layers 2 and 3 of one tile.  hk(kt) = the tile's hidden-1 K-tile kt fragment of this
-// lane (the other waves' tiles, from LDS).  Returns this wave's split-K share of the
-// output: lane (g, r) holds rows 4g..4g+3 for environment r of the tile (rows >= n_out
-// are zero).
-template <int FPW, class HK>
-__device__ __forceinline__ f32x4 tile_layer23(const TileMlpRegs<FPW>& R, const bf16x8 own[FPW / 32], HK hk, int m) {
+// Layer 2 of one tile, the part from this wave's own hidden-1 K tiles (needs no other
+// wave): starts the accumulators acc[M-tile].
+template <int FPW>
+__device__ __forceinline__ void tile_layer2_own(const TileMlpRegs<FPW>& R, const bf16x8 own[FPW / 32],
+                                                f32x4 acc[FPW / 16]) {
   constexpr int MT = FPW / 16, KO = FPW / 32;
-  f32x4 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     acc[mt] = mfma(R.w2[mt][0], own[0], f32x4{0, 0, 0, 0});
 #pragma unroll
     for (int kk = 1; kk < KO; ++kk) acc[mt] = mfma(R.w2[mt][kk], own[kk], acc[mt]);
   }
+}
+
+// Rest of layer 2 and layer 3 of one tile.  hk(kt) = the tile's hidden-1 K-tile kt
+// fragment of this lane (the other waves' tiles, from LDS).  Returns this wave's split-K
+// share of the output: lane (g, r) holds rows 4g..4g+3 for environment r of the tile
+// (rows >= n_out are zero).
+template <int FPW, class HK>
+__device__ __forceinline__ f32x4 tile_layer23(const TileMlpRegs<FPW>& R, f32x4 acc[FPW / 16], HK hk, int m) {
+  constexpr int MT = FPW / 16, KO = FPW / 32;
 #pragma unroll
   for (int kk = KO; kk < 8; ++kk) {
     const bf16x8 hb = hk((KO * m + kk) & 7);
