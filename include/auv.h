@@ -156,7 +156,9 @@ int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_
 /* T control steps of every environment in one launch.  Modes: AUV_ACT_RANDOM (actions
  * from Philox), AUV_ACT_EXTERNAL (actions from rbufs->act, read as [8][T][N]),
  * AUV_ACT_POLICY_MEAN / AUV_ACT_POLICY_SAMPLE (policy required; value optional).
- * global_step += T. */
+ * global_step += T.  In the policy modes the waves of a workgroup order their work through
+ * bounded waits; should one never complete (a defect, not an input condition), the launch
+ * still ends and the affected environments' state is NaN. */
 int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy,
                 const auv_mlp* value, const auv_rollout_buffers* rbufs, void* stream);
 
@@ -167,8 +169,9 @@ int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value,
             const float* done, const float* last_value, float gamma, float lambda,
             float* adv, float* ret, void* stream);
 
-/* Stand-alone MLP forward: obs [23][N] -> out [n_out][N] (same arithmetic as inside
- * auv_rollout). */
+/* Stand-alone MLP forward: obs [23][N] -> out [n_out][N] (same bf16 quantisation points
+ * as inside auv_rollout; the output layer's split-K partials are added in a different
+ * grouping, so the two agree to fp32 rounding). */
 int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float* out,
                     void* stream);
 

@@ -98,16 +98,40 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
   if (valid) lane_store(E, i, L);
 }
 
-// stats[s][t] = sum over groups g (in order) of work[s][g][t].
-__global__ __launch_bounds__(256) void k_stats_reduce(const float* __restrict__ work, int T, int G,
-                                                      float* __restrict__ stats) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= 3 * T) return;
-  const int s = j / T, t = j - s * T;
+// stats[s][t] = sum over groups g of work[s][g][t].  A block covers 64 consecutive (s, t)
+// (one per lane, coalesced rows); each of its waves sums a contiguous slice of the groups
+// with eight loads in flight, then the slices are added in wave order.  The order is fixed
+// by G alone, so repeated runs give identical sums.
+constexpr int RED_WAVES = 16;
+__global__ __launch_bounds__(64 * RED_WAVES) void k_stats_reduce(const float* __restrict__ work, int T, int G,
+                                                                float* __restrict__ stats) {
+  __shared__ float part[RED_WAVES][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + lane;
+  const bool ok = j < 3 * T;
+  const int s = ok ? j / T : 0, t = ok ? j - s * T : 0;
   const float* p = work + (size_t)s * G * T + t;
+  const int chunk = (G + RED_WAVES - 1) / RED_WAVES;
+  const int g0 = w * chunk, g1 = min(G, g0 + chunk);
   float acc = 0.0f;
-  for (int g = 0; g < G; ++g) acc += p[(size_t)g * T];
-  stats[j] = acc;
+  if (ok) {
+    int g = g0;
+    for (; g + 8 <= g1; g += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(size_t)(g + u) * T];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    for (; g < g1; ++g) acc += p[(size_t)g * T];
+  }
+  part[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && ok) {
+    float tot = part[0][lane];
+    for (int q = 1; q < RED_WAVES; ++q) tot += part[q][lane];
+    stats[j] = tot;
+  }
 }
 
 // Backward GAE scan, one lane per environment, [T][N] layout (coalesced over envs).
@@ -149,7 +173,7 @@ __global__ __launch_bounds__(256) void k_gae(int T, int n, const float* __restri
 }
 
 int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s) {
-  hipLaunchKernelGGL(k_stats_reduce, dim3((3 * T + 255) / 256), dim3(256), 0, s, work, T, G, stats);
+  hipLaunchKernelGGL(k_stats_reduce, dim3((3 * T + 63) / 64), dim3(64 * RED_WAVES), 0, s, work, T, G, stats);
   return check_launch("stats reduce");
 }
 
