@@ -89,6 +89,63 @@ def cpu_baseline(cfg: dict, n_steps: int) -> dict:
                       f"{dt:.1f} s)"}
 
 
+def c5_measure(reps: int = 3) -> dict:
+    """PPO-buffer workload (65536 envs x 64 steps, sampled actions, value head, staggered
+    episodes): rollout time and write bandwidth of the structure-of-arrays buffer, then the
+    GAE scan with its inputs evicted from the Infinity Cache (cold) and resident (warm)."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, upload_mlp
+    from paper_2512_13359_amd import _abi as A
+
+    cfg = W.config("c5")
+    n, T = cfg["n_envs"], cfg["T"]
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    pol = upload_mlp(W.mlp_weights(8, W.POLICY_SEED))
+    val = upload_mlp(W.mlp_weights(1, W.VALUE_SEED))
+    bufs = env.rollout_buffers(T, record=("obs", "act", "logp", "value", "reward", "done", "last_value"))
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    times = []
+    for k in range(reps + 1):
+        env.reset()
+        torch.cuda.synchronize()
+        e0, e1 = ev(), ev()
+        e0.record()
+        env.rollout(T, cfg["mode"], policy=pol, value=val, bufs=bufs)
+        e1.record()
+        torch.cuda.synchronize()
+        if k:
+            times.append(e0.elapsed_time(e1) * 1e-3)
+    t_roll = sorted(times)[len(times) // 2]
+    buf_bytes = (A.OBS_DIM + A.ACT_DIM + 4) * 4 * T * n + 4 * n
+    adv = torch.empty(T, n, device="cuda")
+    ret = torch.empty(T, n, device="cuda")
+    scratch = torch.empty(1 << 27, device="cuda")   # 512 MiB, evicts the 256 MB Infinity Cache
+    gae_bytes = 20 * T * n + 4 * n
+    res = {}
+    for kind in ("cold", "warm"):
+        ts = []
+        for _ in range(reps):
+            if kind == "cold":
+                scratch.fill_(1.0)
+            torch.cuda.synchronize()
+            e0, e1 = ev(), ev()
+            e0.record()
+            A.auv_gae(T, n, bufs["reward"], bufs["value"], bufs["done"], bufs["last_value"], 0.99, 0.95, adv, ret)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        res[kind] = sorted(ts)[len(ts) // 2]
+    return {"workload": f"c5: {n} envs x {T} steps, sampled actions + value head, staggered episodes, "
+                        f"PPO buffer (obs 23, act 8, logp, value, reward, done fp32), GAE gamma 0.99 lambda 0.95",
+            "rollout_ms": t_roll * 1e3, "env_steps_per_s": n * T / t_roll,
+            "buffer_bytes": buf_bytes, "buffer_write_GBps": buf_bytes / t_roll / 1e9,
+            "gae_bytes": gae_bytes, "gae_ms_cold": res["cold"] * 1e3, "gae_GBps_cold": gae_bytes / res["cold"] / 1e9,
+            "gae_ms_warm": res["warm"] * 1e3, "gae_GBps_warm": gae_bytes / res["warm"] / 1e9,
+            "gae_hbm_frac_cold": gae_bytes / res["cold"] / 8e12}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -96,6 +153,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c4", choices=["c3", "c4"])
     ap.add_argument("--cpu-steps", type=int, default=10, help="oracle control steps for the CPU baseline (0: skip)")
+    ap.add_argument("--no-c5", action="store_true", help="skip the PPO-buffer (c5) rollout and GAE measurement")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -186,6 +244,8 @@ def main() -> int:
             "max_of_units_frac": max(F_MFMA / P_MFMA, F_VALU / P_VALU, N_TRANS / P_TRANS) / per_env_step_s,
         },
     }
+    if not args.no_c5:
+        line["c5"] = c5_measure()
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
     print(json.dumps(line), flush=True)

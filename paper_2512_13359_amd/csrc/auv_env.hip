@@ -135,8 +135,27 @@ __global__ __launch_bounds__(64 * RED_WAVES) void k_stats_reduce(const float* __
 }
 
 // Backward GAE scan, one lane per environment, [T][N] layout (coalesced over envs).
-// Loads a chunk of steps ahead so that many reads are in flight per lane.
-constexpr int GAE_CHUNK = 16;
+// Streams the steps backwards in chunks of GAE_CHUNK with the next chunk's loads issued
+// before the current chunk is scanned, so about 2 x 3 x GAE_CHUNK loads per lane are in
+// flight (the scan is HBM-bound: 20 B per env-step).
+constexpr int GAE_CHUNK = 32;
+
+struct GaeChunk { float r[GAE_CHUNK], v[GAE_CHUNK], d[GAE_CHUNK]; };
+
+__device__ __forceinline__ void gae_load(GaeChunk& c, int t0, int t1, size_t N, int i, const float* __restrict__ rew,
+                                         const float* __restrict__ val, const float* __restrict__ dn) {
+#pragma unroll
+  for (int k = 0; k < GAE_CHUNK; ++k) {
+    const int t = t0 + k;
+    if (t < t1) {
+      const size_t ti = (size_t)t * N + i;
+      c.r[k] = rew[ti];
+      c.v[k] = val[ti];
+      c.d[k] = dn[ti];
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_gae(int T, int n, const float* __restrict__ rew,
                                              const float* __restrict__ val, const float* __restrict__ dn,
                                              const float* __restrict__ last, float gamma, float gl,
@@ -145,30 +164,28 @@ __global__ __launch_bounds__(256) void k_gae(int T, int n, const float* __restri
   if (i >= n) return;
   const size_t N = (size_t)n;
   float next_v = last[i], next_a = 0.0f;
-  for (int t1 = T; t1 > 0; t1 -= GAE_CHUNK) {
-    const int t0 = t1 > GAE_CHUNK ? t1 - GAE_CHUNK : 0;
-    float r[GAE_CHUNK], v[GAE_CHUNK], d[GAE_CHUNK];
+  int t1 = T, t0 = T > GAE_CHUNK ? T - GAE_CHUNK : 0;
+  GaeChunk cur, nxt;
+  gae_load(cur, t0, t1, N, i, rew, val, dn);
+  while (t1 > 0) {
+    const int u1 = t0, u0 = u1 > GAE_CHUNK ? u1 - GAE_CHUNK : 0;
+    if (u1 > 0) gae_load(nxt, u0, u1, N, i, rew, val, dn);
 #pragma unroll
-    for (int c = 0; c < GAE_CHUNK; ++c) {
-      const int t = t0 + c;
+    for (int k = GAE_CHUNK - 1; k >= 0; --k) {
+      const int t = t0 + k;
       if (t < t1) {
-        const size_t ti = (size_t)t * N + i;
-        r[c] = rew[ti]; v[c] = val[ti]; d[c] = dn[ti];
-      }
-    }
-#pragma unroll
-    for (int c = GAE_CHUNK - 1; c >= 0; --c) {
-      const int t = t0 + c;
-      if (t < t1) {
-        const float nd = 1.0f - d[c];
-        const float delta = r[c] + gamma * nd * next_v - v[c];
+        const float nd = 1.0f - cur.d[k];
+        const float delta = cur.r[k] + gamma * nd * next_v - cur.v[k];
         next_a = delta + gl * nd * next_a;
         const size_t ti = (size_t)t * N + i;
         adv[ti] = next_a;
-        ret[ti] = next_a + v[c];
-        next_v = v[c];
+        ret[ti] = next_a + cur.v[k];
+        next_v = cur.v[k];
       }
     }
+    cur = nxt;
+    t1 = u1;
+    t0 = u0;
   }
 }
 

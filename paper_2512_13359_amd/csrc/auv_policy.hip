@@ -340,39 +340,74 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
   }
 }
 
-// Stand-alone MLP forward over obs [23][n] -> out [n_out][n]; persistent over 64-env
-// tiles so each workgroup loads the weights once.
-__global__ __launch_bounds__(MLP_THREADS, 1) void k_mlp(const uint16_t* __restrict__ w, const float* __restrict__ b,
-                                                int n_out, int n, const float* __restrict__ obs,
-                                                float* __restrict__ out) {
-  __shared__ MlpShared S;
+// Stand-alone MLP forward over obs [23][n] -> out [n_out][n]: workgroups of four MLP waves
+// (64 hidden features each, weights in registers, mlp_tile.hpp), two per CU, persistent
+// over 16-environment tiles.  Each wave builds the tile's layer-1 operand straight from
+// HBM (the next tile's loads are issued before this tile's math); hidden 1 and the output
+// partials meet in LDS with two barriers per tile.
+constexpr int FWD_WAVES = 4;
+constexpr int FWD_THREADS = 64 * FWD_WAVES;
+
+__global__ __launch_bounds__(FWD_THREADS, 2) void k_mlp(const uint16_t* __restrict__ w, const float* __restrict__ b,
+                                                        int n_out, int n, const float* __restrict__ obs,
+                                                        float* __restrict__ out) {
+  __shared__ bf16x8 h[8][64];                     // hidden-1 operand of the tile [K tile][lane]
+  __shared__ float mu[FWD_WAVES][16][NOUT_PAD];   // output partials [wave][env][row]
+  __shared__ float b1k[HID];
+  __shared__ float b3[16];
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  MlpRegs R;
-  mlp_load(w, b, n_out, wave, lane, R, S);
-  const int tiles = (n + 63) / 64;
+  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  TileMlpRegs<64> R;
+  tile_mlp_load<64>(w, b, n_out, m, lane, R);
+  if (tid < HID) b1k[tid] = b[tid] * TWO_LOG2E;
+  if (tid < 16) b3[tid] = tid < n_out ? b[2 * HID + tid] : 0.0f;
+  __syncthreads();
   const size_t N = (size_t)n;
-  for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-    const int i = tile * 64 + lane;
-    const bool valid = i < n;
-    if (wave == 0) {
-      float o[OBS];
+  const int tiles = (n + 15) / 16;
+  // This lane's 8 layer-1 operand values of a tile: unconditional loads from a clamped,
+  // valid address (so that they stay in flight while the previous tile is computed), masked
+  // to zero when converted.
+  struct XRaw { float v[8]; };
+  auto load_x = [&](int tile) {
+    XRaw x;
+    const int i = min(tile * 16 + r, n - 1);
 #pragma unroll
-      for (int k = 0; k < OBS; ++k) o[k] = valid ? obs[k * N + i] : 0.0f;
-      mlp_put_obs(o, lane, S);
+    for (int j = 0; j < 8; ++j) x.v[j] = obs[min(kslot(g, j), OBS - 1) * N + i];
+    return x;
+  };
+  auto to_operand = [&](const XRaw& x, int tile) {
+    bf16x8 o;
+    const bool ok = tile < tiles && tile * 16 + r < n;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = (__bf16)((ok && kslot(g, j) < OBS) ? x.v[j] : 0.0f);
+    return o;
+  };
+  XRaw xr = load_x(blockIdx.x);
+  for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const bf16x8 x = to_operand(xr, tile);
+    xr = load_x(tile + gridDim.x);   // next tile, in flight during this one
+    bf16x8 own[2];
+    tile_layer1<64>(R, x, b1k, m, lane, own);
+    h[2 * m][lane] = own[0];
+    h[2 * m + 1][lane] = own[1];
+    f32x4 acc[4];
+    tile_layer2_own<64>(R, own, acc);
+    __syncthreads();                              // h complete
+    const f32x4 o = tile_layer23<64>(R, acc, [&](int kt) { return h[kt][lane]; }, m);
+    if (g < 2) *reinterpret_cast<f32x4*>(&mu[m][r][4 * g]) = o;
+    __syncthreads();                              // mu complete; h free for the next tile
+    if (m == 0) {                                 // rows g and g + 4 of env r, partials in wave order
+      const int i = tile * 16 + r;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int row = g + 4 * hh;
+        float y = mu[0][r][row];
+#pragma unroll
+        for (int q = 1; q < FWD_WAVES; ++q) y += mu[q][r][row];
+        if (row < n_out && i < n) out[row * N + i] = b3[row] + y;
+      }
     }
-    __syncthreads();
-    OwnH1 H;
-    mlp_layer1(R, S, wave, lane, H);
-    __syncthreads();
-    mlp_layer23(R, S, wave, lane, H);
-    __syncthreads();
-    if (wave == 0 && valid) {
-      float y[NOUT_PAD];
-      mlp_out8(S, lane, y);
-      for (int k = 0; k < n_out; ++k) out[k * N + i] = y[k];
-    }
-    __syncthreads();
   }
 }
 
@@ -387,14 +422,14 @@ static int check_mlp(const auv_mlp* net, int n_out_want, const char* what) {
   return AUV_OK;
 }
 
-static int mlp_grid(int n) {
-  const int tiles = (n + 63) / 64;
+static int mlp_grid(int n) {   // two resident workgroups per CU
+  const int tiles = (n + 15) / 16;
   return tiles < 512 ? tiles : 512;
 }
 
 int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, hipStream_t s) {
   if (int rc = check_mlp(net, 0, "auv_mlp_forward")) return rc;
-  hipLaunchKernelGGL(k_mlp, dim3(mlp_grid(n)), dim3(MLP_THREADS), 0, s, (const uint16_t*)net->w, net->b, net->n_out, n,
+  hipLaunchKernelGGL(k_mlp, dim3(mlp_grid(n)), dim3(FWD_THREADS), 0, s, (const uint16_t*)net->w, net->b, net->n_out, n,
                      obs, out);
   return check_launch("auv_mlp_forward");
 }
