@@ -146,6 +146,37 @@ def c5_measure(reps: int = 3) -> dict:
             "gae_hbm_frac_cold": gae_bytes / res["cold"] / 8e12}
 
 
+def small_configs_measure(reps: int = 3) -> dict:
+    """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
+    4096 envs occupy 64 of the 256 CUs, so these are occupancy-capped by N."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, upload_mlp
+
+    out = {}
+    pol = upload_mlp(W.mlp_weights(8, W.POLICY_SEED))
+    for name in ("c2", "c3"):
+        cfg = W.config(name)
+        n, T = cfg["n_envs"], cfg["T"]
+        env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+        bufs = env.rollout_buffers(T, record=("stats",))
+        ts = []
+        for k in range(reps + 1):
+            env.reset()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            env.rollout(T, cfg["mode"], policy=pol if cfg["mode"] >= W.MODE_POLICY_MEAN else None, bufs=bufs)
+            e1.record()
+            torch.cuda.synchronize()
+            if k:
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+        t = sorted(ts)[len(ts) // 2]
+        out[name] = {"n_envs": n, "control_steps": T, "launch_ms": t * 1e3, "env_steps_per_s": n * T / t}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -246,6 +277,7 @@ def main() -> int:
     }
     if not args.no_c5:
         line["c5"] = c5_measure()
+        line.update(small_configs_measure())
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
     print(json.dumps(line), flush=True)

@@ -228,3 +228,38 @@ def test_policy_rollout_deterministic_and_resumable(nets):
     b.rollout(17, W.MODE_POLICY_SAMPLE, policy=dpol)
     for k in ("state", "params", "ep_step", "episode", "obs"):
         assert torch.equal(getattr(a, k), getattr(b, k)), k
+
+
+@pytest.mark.parametrize("n,T", [(1, 5), (17, 3), (64 + 5, 1)])
+def test_policy_rollout_small_and_ragged(nets, n, T):
+    """Single environment, a tile that is only partly filled, one-step launches: valid
+    actions, the oracle's control step under them, statistics equal to the per-env sums."""
+    pol, _, dpol, _ = nets
+    announce(f"policy rollout small n={n} T={T}")
+    cfg = W.config("c4", n_envs=n, T=T)
+    g, got = _policy_rollout(cfg, T, dpol, ("obs", "act", "reward", "done", "traj_state", "stats"))
+    assert _check_mu_on_gpu_obs(pol, got) <= TOL_VALID
+    o = oracle_env(cfg)
+    o.reset()
+    rec = o.rollout(T, W.MODE_EXTERNAL, external=np.transpose(got["act"], (1, 0, 2)).astype(np.float64),
+                    record_state=True)
+    traj = got["traj_state"].copy()
+    traj[3:7] = quat_aligned(traj[3:7], rec["traj_state"][3:7])
+    assert rel_err(traj, rec["traj_state"]).max() <= 1e-4 * T
+    assert rel_err(got["reward"], rec["reward"]).max() <= 1e-3
+    assert np.allclose(got["stats"][0], got["reward"].astype(np.float64).sum(1), rtol=1e-5, atol=1e-4)
+    assert np.isfinite(got["stats"]).all()
+
+
+def test_policy_rollout_rejects_zero_steps(nets):
+    """T = 0 is an argument error: nothing is enqueued and the state stays as it was."""
+    from paper_2512_13359_amd import _abi as A
+    _, _, dpol, _ = nets
+    cfg = W.config("c4", n_envs=100, T=4)
+    g = gpu_env(cfg)
+    g.reset()
+    before = {k: getattr(g, k).clone() for k in ("state", "params", "ep_step", "episode", "obs")}
+    with pytest.raises(A.AuvError):
+        g.rollout(0, W.MODE_POLICY_MEAN, policy=dpol)
+    for k, v in before.items():
+        assert torch.equal(getattr(g, k), v), k
