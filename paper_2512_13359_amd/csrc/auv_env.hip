@@ -365,7 +365,7 @@ int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const 
   } else if (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE) {
     if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
     if (rb->stats)   // one partial per wave of 16 environments
-      if (int rc = launch_stats_reduce(rb->stats_work, T, stats_groups(env->E.n), rb->stats, s)) return rc;
+      if (int rc = launch_stats_reduce(rb->stats_work, T, rollout_stats_groups(env->E.n), rb->stats, s)) return rc;
   } else {
     return set_error(AUV_EINVAL, "auv_rollout: unknown mode %d", mode);
   }

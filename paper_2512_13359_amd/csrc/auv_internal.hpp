@@ -26,8 +26,11 @@ bool aligned16(const void* p);
 int check_launch(const char* what);
 
 inline int groups_of(int n) { return (n + 63) / 64; }
-// statistics partials: one per wave; the policy rollout has four waves per 64 envs
+// statistics partials: one per physics wave; the policy rollout has up to four physics
+// waves per 64 envs (the workspace is sized for that many)
 inline int stats_groups(int n) { return 4 * groups_of(n); }
+// partials the policy rollout actually writes for n envs (<= stats_groups(n))
+int rollout_stats_groups(int n);
 
 // launches implemented in auv_policy.hip
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy,

@@ -10,13 +10,16 @@
 namespace auv {
 
 // Fused rollout workgroup: ROLLOUT_MLP_WAVES MLP waves of ROLLOUT_FPW hidden features each,
-// then four physics waves (one 16-environment tile each, 64 environments in all).
+// then TPW physics waves (one 16-environment tile each; TPW = 1, 2 or 4 tiles per
+// workgroup, chosen so that small batches still spread over every CU).
 constexpr int ROLLOUT_FPW = 64;
 constexpr int ROLLOUT_MLP_WAVES = HID / ROLLOUT_FPW;
 constexpr int ROLLOUT_KO = ROLLOUT_FPW / 32;   // K tiles of hidden features per MLP wave
-constexpr int ROLLOUT_THREADS = 64 * (ROLLOUT_MLP_WAVES + 4);
+constexpr int ROLLOUT_MAX_TILES = 4;
+template <int TPW>
+constexpr int rollout_threads() { return 64 * (ROLLOUT_MLP_WAVES + TPW); }
 
-// Shared memory of one rollout workgroup (64 environments = four 16-environment tiles).
+// Shared memory of one rollout workgroup (up to four 16-environment tiles).
 struct RolloutShared {
   bf16x8 x[4][64];                          // layer-1 operand per tile: K = 32 (23 used) x 16 envs
   bf16x8 h[8][4][64];                       // hidden-1 operand [K tile][tile][lane]
@@ -76,6 +79,7 @@ __device__ __forceinline__ bool wait_for(const unsigned* counter, unsigned targe
 // MLP wave m: for every step and tile in order, layer 1 as soon as the tile's observations
 // are published, layers 2 and 3 once every MLP wave has published its hidden-1 K tiles of
 // that tile.
+template <int TPW>
 __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const uint16_t* __restrict__ w,
                                                  const float* __restrict__ b, int m, int lane) {
   const int g = lane >> 4, r = lane & 15;
@@ -84,7 +88,7 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
   tile_mlp_load<ROLLOUT_FPW>(w, b, ACT, m, lane, R);
   for (int t = 0; t < T; ++t) {
 #pragma unroll 1
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < TPW; ++k) {
       if (!wait_for(&S.obs_ready[k], (unsigned)t + 1)) return;
       bf16x8 own[ROLLOUT_KO];
       tile_layer1<ROLLOUT_FPW>(R, S.x[k][lane], S.b1k, m, lane, own);
@@ -101,14 +105,14 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
   }
 }
 
-// One workgroup = 64 environments for all T steps.  The first ROLLOUT_MLP_WAVES waves are
-// MLP waves (weights in registers, rollout_mlp_wave); the last four are physics waves,
+// One workgroup = 16 TPW environments for all T steps.  The first ROLLOUT_MLP_WAVES waves
+// are MLP waves (weights in registers, rollout_mlp_wave); the last TPW are physics waves,
 // each stepping one tile of 16 environments with four lanes per environment (quad layout,
 // quad_env.hpp).  Each tile runs its own chain obs -> MLP -> action -> physics -> obs,
 // ordered by LDS counters instead of workgroup barriers, so the physics of one tile
-// overlaps the MLP of the others; every SIMD holds MLP waves and one physics wave.
-template <bool SAMPLE>
-__global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
+// overlaps the MLP of the others; with four tiles every SIMD holds one wave of each kind.
+template <bool SAMPLE, int TPW>
+__global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
                                                            StepOut O, const uint16_t* __restrict__ w,
                                                            const float* __restrict__ b,
                                                            const float* __restrict__ log_std) {
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
   if (tid < 4) S.obs_ready[tid] = S.h1_ready[tid] = S.mu_ready[tid] = 0u;
   __syncthreads();
   if (wave < ROLLOUT_MLP_WAVES) {
-    rollout_mlp_wave(S, T, w, b, wave, lane);
+    rollout_mlp_wave<TPW>(S, T, w, b, wave, lane);
     return;
   }
 
@@ -134,7 +138,7 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
   const quad::QK K = quad::make_qk(lane);
   const int c = K.c;
   const int slot = lane >> 2;              // environment within the tile
-  const int i = blockIdx.x * 64 + 16 * k + slot;
+  const int i = blockIdx.x * (16 * TPW) + 16 * k + slot;
   const bool valid = i < E.n;
   const size_t N = (size_t)E.n, TN = (size_t)T * N;
   const uint32_t gid = E.env_offset + (uint32_t)i;
@@ -204,7 +208,7 @@ __global__ __launch_bounds__(ROLLOUT_THREADS, 1) void k_policy_rollout(VehArgs V
       const float sr = wave_sum_quads(valid ? reward : 0.0f);
       const float sd = wave_sum_quads((valid && pv_done) ? 1.0f : 0.0f);
       const float sp = wave_sum_quads(valid ? pv_dist : 0.0f);
-      stats_park(SB, O.stats_work, T, t1, lane, 4 * blockIdx.x + k, 4 * gridDim.x, sr, sd, sp);
+      stats_park(SB, O.stats_work, T, t1, lane, TPW * blockIdx.x + k, TPW * gridDim.x, sr, sd, sp);
     }
   };
   put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
@@ -434,6 +438,42 @@ int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, 
   return check_launch("auv_mlp_forward");
 }
 
+// Tiles per workgroup: four where the batch fills every CU with 64 envs, fewer (down to one
+// 16-env tile) for smaller batches, so that they still use every CU (one workgroup fits a
+// CU at a time).
+static int compute_units() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 256;
+  return cus;
+}
+
+static int rollout_tiles_per_group(int n) {
+  const int cus = compute_units();
+  return n >= cus * 64 ? 4 : (n >= cus * 32 ? 2 : 1);
+}
+
+int rollout_stats_groups(int n) {
+  const int tpw = rollout_tiles_per_group(n);
+  return tpw * ((n + 16 * tpw - 1) / (16 * tpw));
+}
+
+template <bool SAMPLE>
+static void launch_rollout_kernel(int tpw, int n, hipStream_t s, const VehArgs& V, const EnvArgs& E, int T, uint32_t g0,
+                                  const StepOut& O, const uint16_t* w, const float* b, const float* log_std) {
+  const dim3 grid((n + 16 * tpw - 1) / (16 * tpw));
+  if (tpw == 4)
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 4>), grid, dim3(rollout_threads<4>()), 0, s, V, E, T, g0, O, w, b,
+                       log_std);
+  else if (tpw == 2)
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 2>), grid, dim3(rollout_threads<2>()), 0, s, V, E, T, g0, O, w, b,
+                       log_std);
+  else
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 1>), grid, dim3(rollout_threads<1>()), 0, s, V, E, T, g0, O, w, b,
+                       log_std);
+}
+
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, const auv_mlp* value,
                           const auv_rollout_buffers* rb, hipStream_t s) {
   if (int rc = check_mlp(policy, ACT, "auv_rollout policy")) return rc;
@@ -459,14 +499,12 @@ int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, 
   O.traj = rb->traj_state;
   O.stats_work = rb->stats_work;
   const uint32_t g0 = (uint32_t)(env->global_step & 0xffffffffu);
-  const dim3 grid(groups_of(n));
+  const int tpw = rollout_tiles_per_group(n);
   const uint16_t* w = (const uint16_t*)policy->w;
   if (sample)
-    hipLaunchKernelGGL(k_policy_rollout<true>, grid, dim3(ROLLOUT_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
-                       policy->log_std);
+    launch_rollout_kernel<true>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
   else
-    hipLaunchKernelGGL(k_policy_rollout<false>, grid, dim3(ROLLOUT_THREADS), 0, s, env->veh, env->E, T, g0, O, w, policy->b,
-                       policy->log_std);
+    launch_rollout_kernel<false>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
   if (int rc = check_launch("policy rollout")) return rc;
   if (value) {
     // V(o_t) for every recorded observation, then the bootstrap value V(o_T)
