@@ -180,6 +180,12 @@ int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float*
 int64_t auv_get_global_step(const auv_env* env);
 int auv_set_global_step(auv_env* env, int64_t step);
 
+/* Bound on the number of polls of one wait between the waves of a policy-rollout
+ * workgroup (0 restores the default, about one second of polling).  Only for exercising the
+ * abandonment path described under auv_rollout: with a tiny bound the launch gives up early,
+ * ends normally and leaves NaN state. */
+int auv_set_sync_poll_limit(auv_env* env, uint32_t polls);
+
 /* Message for the calling thread's last error ("" if none). */
 const char* auv_last_error(void);
 

@@ -70,6 +70,7 @@ def _load() -> ctypes.CDLL:
         "auv_mlp_forward": (ctypes.c_int, [P(AuvMlp), i32, _vp, _vp, _vp]),
         "auv_get_global_step": (i64, [_vp]),
         "auv_set_global_step": (ctypes.c_int, [_vp, i64]),
+        "auv_set_sync_poll_limit": (ctypes.c_int, [_vp, ctypes.c_uint32]),
         "auv_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -146,6 +147,10 @@ def auv_get_global_step(h: int) -> int:
 
 def auv_set_global_step(h: int, step: int) -> None:
     _check(lib.auv_set_global_step(h, step))
+
+
+def auv_set_sync_poll_limit(h: int, polls: int) -> None:
+    _check(lib.auv_set_sync_poll_limit(h, polls))
 
 
 def auv_last_error() -> str:

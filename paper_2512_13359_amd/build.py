@@ -1,6 +1,7 @@
 """Build libauv.so for gfx950 with hipcc (in-tree, next to this file).
 
-    python -m paper_2512_13359_amd.build
+    python paper_2512_13359_amd/build.py   (as a script: importing the package would load the
+    library being rebuilt; __graft_entry__.build() loads this file by path)
 """
 from __future__ import annotations
 

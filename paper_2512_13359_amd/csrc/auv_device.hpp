@@ -26,6 +26,7 @@ struct EnvArgs {
   int32_t n, substeps, H;
   float dt, h;
   uint32_t key0, key1, flags, env_offset;
+  uint32_t sync_polls;   // bound on the polls of one inter-wave wait (fused policy rollout)
 };
 
 // Per-step output pointers of the environment loops; any may be null.

@@ -272,6 +272,7 @@ int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buff
   E.key1 = (uint32_t)(cfg->seed >> 32);
   E.flags = cfg->flags;
   E.env_offset = cfg->env_offset;
+  E.sync_polls = AUV_DEFAULT_SYNC_POLLS;
   e->global_step = 0;
   *out = e;
   return AUV_OK;
@@ -288,6 +289,12 @@ int auv_set_global_step(auv_env* env, int64_t step) {
   if (!env) return set_error(AUV_EINVAL, "auv_set_global_step: NULL handle");
   if (step < 0) return set_error(AUV_EINVAL, "auv_set_global_step: negative step");
   env->global_step = step;
+  return AUV_OK;
+}
+
+int auv_set_sync_poll_limit(auv_env* env, uint32_t polls) {
+  if (!env) return set_error(AUV_EINVAL, "auv_set_sync_poll_limit: NULL handle");
+  env->E.sync_polls = polls ? polls : AUV_DEFAULT_SYNC_POLLS;
   return AUV_OK;
 }
 

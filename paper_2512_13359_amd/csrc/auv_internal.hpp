@@ -26,6 +26,10 @@ bool aligned16(const void* p);
 int check_launch(const char* what);
 
 inline int groups_of(int n) { return (n + 63) / 64; }
+
+// Default bound on the polls of one inter-wave wait of the fused policy rollout (each poll is
+// an LDS round trip: about a second in all).
+constexpr uint32_t AUV_DEFAULT_SYNC_POLLS = 1u << 24;
 // statistics partials: one per physics wave; the policy rollout has up to four physics
 // waves per 64 envs (the workspace is sized for that many)
 inline int stats_groups(int n) { return 4 * groups_of(n); }

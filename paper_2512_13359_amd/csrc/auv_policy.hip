@@ -17,19 +17,23 @@ constexpr int ROLLOUT_MLP_WAVES = HID / ROLLOUT_FPW;
 constexpr int ROLLOUT_KO = ROLLOUT_FPW / 32;   // K tiles of hidden features per MLP wave
 constexpr int ROLLOUT_MAX_TILES = 4;
 template <int TPW>
-constexpr int rollout_threads() { return 64 * (ROLLOUT_MLP_WAVES + TPW); }
+constexpr int rollout_threads() {
+  static_assert(TPW >= 1 && TPW <= ROLLOUT_MAX_TILES && 64 * (ROLLOUT_MLP_WAVES + TPW) >= HID,
+                "tiles per workgroup out of range (the setup needs at least 256 threads)");
+  return 64 * (ROLLOUT_MLP_WAVES + TPW);
+}
 
 // Shared memory of one rollout workgroup (up to four 16-environment tiles).
 struct RolloutShared {
-  bf16x8 x[4][64];                          // layer-1 operand per tile: K = 32 (23 used) x 16 envs
-  bf16x8 h[8][4][64];                       // hidden-1 operand [K tile][tile][lane]
-  float mu[4][ROLLOUT_MLP_WAVES][16][NOUT_PAD];   // output partials [tile][MLP wave][env][row]
+  bf16x8 x[ROLLOUT_MAX_TILES][64];          // layer-1 operand per tile: K = 32 (23 used) x 16 envs
+  bf16x8 h[8][ROLLOUT_MAX_TILES][64];       // hidden-1 operand [K tile][tile][lane]
+  float mu[ROLLOUT_MAX_TILES][ROLLOUT_MLP_WAVES][16][NOUT_PAD];   // output partials [tile][MLP wave][env][row]
   float b1k[HID];                           // hidden-1 biases x 2 log2 e
   float b3[16];                             // output biases
   float alloc[8][8];                        // thrust rows x f_max: force rows 0-2, moment rows 4-6
-  unsigned obs_ready[4];                    // per tile: observations published (1 + steps done)
-  unsigned h1_ready[4];                     // per tile: MLP waves done with hidden 1 (all, each step)
-  unsigned mu_ready[4];                     // per tile: MLP waves done with the output (all, each step)
+  unsigned obs_ready[ROLLOUT_MAX_TILES];    // per tile: observations published (1 + steps done)
+  unsigned h1_ready[ROLLOUT_MAX_TILES];     // per tile: MLP waves done with hidden 1 (all, each step)
+  unsigned mu_ready[ROLLOUT_MAX_TILES];     // per tile: MLP waves done with the output (all, each step)
 };
 
 // Observation features of one environment written by the four lanes of its quad into the
@@ -54,18 +58,17 @@ __device__ __forceinline__ void put_obs_quad(RolloutShared& S, int nt, int r, in
 
 // Point-to-point ordering between the waves of a workgroup through LDS counters: the
 // producer's LDS writes complete before its count is raised; the consumer polls (each poll
-// is an LDS round trip, a few VALU slots).  Every wait is bounded: a wait that would never
-// end (a defect) gives up after about a second of polling, and the caller abandons the
-// rollout.
-constexpr uint32_t SYNC_SPIN_LIMIT = 1u << 24;
+// is an LDS round trip, a few VALU slots).  Every wait is bounded (EnvArgs::sync_polls,
+// about a second of polling by default): a wait that would never end (a defect) gives up
+// and the caller abandons the rollout.
 
 __device__ __forceinline__ void publish(unsigned* counter, int lane) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   if (lane == 0) __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-__device__ __forceinline__ bool wait_for(const unsigned* counter, unsigned target) {
-  for (uint32_t spin = 0; spin < SYNC_SPIN_LIMIT; ++spin) {
+__device__ __forceinline__ bool wait_for(const unsigned* counter, unsigned target, uint32_t polls) {
+  for (uint32_t spin = 0; spin < polls; ++spin) {
     const unsigned seen =
         __builtin_amdgcn_readfirstlane(__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
     if (seen >= target) {
@@ -81,7 +84,7 @@ __device__ __forceinline__ bool wait_for(const unsigned* counter, unsigned targe
 // that tile.
 template <int TPW>
 __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const uint16_t* __restrict__ w,
-                                                 const float* __restrict__ b, int m, int lane) {
+                                                 const float* __restrict__ b, int m, int lane, uint32_t polls) {
   const int g = lane >> 4, r = lane & 15;
   const unsigned NW = ROLLOUT_MLP_WAVES;
   TileMlpRegs<ROLLOUT_FPW> R;
@@ -89,7 +92,7 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
   for (int t = 0; t < T; ++t) {
 #pragma unroll 1
     for (int k = 0; k < TPW; ++k) {
-      if (!wait_for(&S.obs_ready[k], (unsigned)t + 1)) return;
+      if (!wait_for(&S.obs_ready[k], (unsigned)t + 1, polls)) return;
       bf16x8 own[ROLLOUT_KO];
       tile_layer1<ROLLOUT_FPW>(R, S.x[k][lane], S.b1k, m, lane, own);
 #pragma unroll
@@ -97,7 +100,7 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
       publish(&S.h1_ready[k], lane);
       f32x4 acc[ROLLOUT_FPW / 16];
       tile_layer2_own<ROLLOUT_FPW>(R, own, acc);   // overlaps the wait for the other waves
-      if (!wait_for(&S.h1_ready[k], NW * (unsigned)(t + 1))) return;
+      if (!wait_for(&S.h1_ready[k], NW * (unsigned)(t + 1), polls)) return;
       const f32x4 o = tile_layer23<ROLLOUT_FPW>(R, acc, [&](int kt) { return S.h[kt][k][lane]; }, m);
       if (g < 2) *reinterpret_cast<f32x4*>(&S.mu[k][m][r][4 * g]) = o;
       publish(&S.mu_ready[k], lane);
@@ -119,7 +122,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   __shared__ RolloutShared S;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  if (tid < 256) S.x[tid >> 6][lane] = bf16x8{};
+  if (tid < 64 * ROLLOUT_MAX_TILES) S.x[tid >> 6][lane] = bf16x8{};
   if (tid < HID) S.b1k[tid] = b[tid] * TWO_LOG2E;
   if (tid < 16) S.b3[tid] = tid < ACT ? b[2 * HID + tid] : 0.0f;
   if (tid < 64) {                          // allocation rows x f_max
@@ -127,10 +130,10 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     const int src = row < 3 ? row : (row >= 4 && row < 7 ? row - 1 : -1);
     S.alloc[row][j] = src >= 0 ? V.alloc[src * 8 + j] * V.f_max : 0.0f;
   }
-  if (tid < 4) S.obs_ready[tid] = S.h1_ready[tid] = S.mu_ready[tid] = 0u;
+  if (tid < ROLLOUT_MAX_TILES) S.obs_ready[tid] = S.h1_ready[tid] = S.mu_ready[tid] = 0u;
   __syncthreads();
   if (wave < ROLLOUT_MLP_WAVES) {
-    rollout_mlp_wave<TPW>(S, T, w, b, wave, lane);
+    rollout_mlp_wave<TPW>(S, T, w, b, wave, lane, E.sync_polls);
     return;
   }
 
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       O.obs[(15 + 2 * c) * TN + ti] = u0;
       O.obs[(16 + 2 * c) * TN + ti] = u1;
     }
-    if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1))) {   // abandoned: poison
+    if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1), E.sync_polls)) {   // abandoned: poison
       p = q = v = om = __builtin_nanf("");
       break;
     }

@@ -263,3 +263,23 @@ def test_policy_rollout_rejects_zero_steps(nets):
         g.rollout(0, W.MODE_POLICY_MEAN, policy=dpol)
     for k, v in before.items():
         assert torch.equal(getattr(g, k), v), k
+
+
+def test_abandoned_waits_end_the_launch(nets):
+    """With a one-poll bound, the workgroup's waits give up: the launch still ends normally
+    and the abandoned environments hold NaN (never a hang).  The default bound restores
+    normal results."""
+    from paper_2512_13359_amd import _abi as A
+    _, _, dpol, _ = nets
+    announce("abandoned waits")
+    cfg = W.config("c4", n_envs=128, T=20)
+    g = gpu_env(cfg)
+    g.reset()
+    A.auv_set_sync_poll_limit(g.handle, 1)
+    g.rollout(20, W.MODE_POLICY_MEAN, policy=dpol)
+    st = host(g.state)
+    assert np.isnan(st).any()
+    A.auv_set_sync_poll_limit(g.handle, 0)
+    g.reset()
+    g.rollout(20, W.MODE_POLICY_MEAN, policy=dpol)
+    assert np.isfinite(host(g.state)).all()
