@@ -36,7 +36,9 @@ P_VALU = 157.3e12
 P_TRANS = 256 * 4 * 16 * 2.4e9 / 2
 HBM_PEAK = 8.0e12
 
-KERNEL_SOURCES = ["auv_device.hpp", "env_lane.hpp", "quad_env.hpp", "mlp_mfma.hpp", "auv_policy.hip", "auv_env.hip"]
+# The translation unit of the rollout kernel (auv_policy.hip and everything it includes).
+KERNEL_SOURCES = ["auv_policy.hip", "auv_internal.hpp", "auv_device.hpp", "env_lane.hpp", "quad_env.hpp",
+                  "mlp_mfma.hpp", "mlp_tile.hpp"]
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_policy_rollout_c4_counters.txt")
 
 
@@ -183,7 +185,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c4", choices=["c3", "c4"])
-    ap.add_argument("--cpu-steps", type=int, default=10, help="oracle control steps for the CPU baseline (0: skip)")
+    ap.add_argument("--cpu-steps", type=int, default=50, help="oracle control steps for the CPU baseline (0: skip)")
     ap.add_argument("--no-c5", action="store_true", help="skip the PPO-buffer (c5) rollout and GAE measurement")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")

@@ -86,7 +86,11 @@ struct Model {
   float DL[6], DQ[6];
 };
 
+// Every product is rounded before it is added (no contraction): the constants are built at
+// more than one place in a kernel (load and in-kernel reset), and a fused multiply-add
+// chosen differently at each would make a resumed run differ from an uninterrupted one.
 __device__ __forceinline__ void make_model(const VehArgs& V, const Params& P, Model& M) {
+#pragma clang fp contract(off)
   const float m = P.s[0] * V.m;
 #pragma unroll
   for (int i = 0; i < 3; ++i) {

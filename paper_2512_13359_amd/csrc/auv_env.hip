@@ -4,6 +4,7 @@
 #include <cstring>
 
 #include "auv_internal.hpp"
+#include "quad_env.hpp"
 
 using namespace auv;
 
@@ -96,6 +97,79 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
     lane_outputs(O, SB, T, N, t, i, valid, lane, blockIdx.x, gridDim.x, reward, done, dist, L.x);
   }
   if (valid) lane_store(E, i, L);
+}
+
+// The same T control steps in the quad layout of quad_env.hpp (lanes 4e .. 4e + 3 hold
+// environment e's x, y, z components and the quaternion's scalar part): a one-wave block
+// steps 16 environments and writes one stats partial per step.  It spends about twice the
+// instructions per environment of k_env_loop but makes four times the waves, so it is the
+// faster loop while the batch leaves SIMDs idle.
+template <bool EXTERNAL>
+__global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, uint32_t gstep0, StepOut O) {
+  __shared__ float alloc[8][8];
+  const int lane = threadIdx.x;
+  quad::stage_alloc(V, alloc, lane);
+  __syncthreads();
+  const quad::QK K = quad::make_qk(lane);
+  const int c = K.c;
+  const int i = blockIdx.x * 16 + (lane >> 2);
+  const bool valid = i < E.n;
+  const size_t N = (size_t)E.n, TN = (size_t)T * N;
+  const uint32_t gid = E.env_offset + (uint32_t)i;
+  float Tf[8], Tm[8];
+  quad::alloc_rows(alloc, c, Tf, Tm);
+  quad::QEnv X;
+  quad::QModel M;
+  quad::QRef F;
+  quad::load_env(V, E, K, i, valid, X, M, F);
+  if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, c, X);
+  StatsBuf SB{};
+  for (int t = 0; t < T; ++t) {
+    const size_t ti = (size_t)t * N + (size_t)i;
+    if (O.obs && valid) quad::store_obs(O.obs, TN, ti, c, X);
+    float a0, a1;   // action components 2c and 2c + 1
+    if (EXTERNAL) {
+      a0 = valid ? O.act[(2 * c) * TN + ti] : 0.0f;
+      a1 = valid ? O.act[(2 * c + 1) * TN + ti] : 0.0f;
+    } else {        // words (x, y) or (z, w) of Philox block c / 2 of this step
+      const U4 r = philox(U4{gid, gstep0 + (uint32_t)t, 1u, (uint32_t)(c >> 1)}, E.key0, E.key1);
+      a0 = 2.0f * u01((c & 1) ? r.z : r.x) - 1.0f;
+      a1 = 2.0f * u01((c & 1) ? r.w : r.y) - 1.0f;
+      if (O.act && valid) {
+        O.act[(2 * c) * TN + ti] = a0;
+        O.act[(2 * c + 1) * TN + ti] = a1;
+      }
+    }
+    float tf, tm, usq;
+    quad::wrench(Tf, Tm, a0, a1, X.u0, X.u1, tf, tm, usq);
+    const float tfi = tf * M.iMlin;
+    for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, X.p, X.q, X.v, X.om);
+    X.ep += 1;
+    float pr, qr, dist;
+    quad::reference(E, K, F, X.ep, pr, qr);
+    quad::QRefCols rc = quad::ref_columns(K, qr);
+    quad::observe(K, X.p, X.q, pr, rc, X.ob, dist);
+    const float theta = quad::attitude_error(K, X.q, qr);
+    const float reward = -dist - 0.5f * theta - 0.01f * usq;
+    const bool done = (X.ep == E.H);
+    if (done) {   // the whole quad
+      float dist0;
+      quad::new_episode(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist0);
+    }
+    if (O.stats_work) {   // reward, done and dist are the same in the four lanes of a quad
+      const float sr = wave_sum_quads(valid ? reward : 0.0f);
+      const float sd = wave_sum_quads((valid && done) ? 1.0f : 0.0f);
+      const float sp = wave_sum_quads(valid ? dist : 0.0f);
+      stats_park(SB, O.stats_work, T, t, lane, blockIdx.x, gridDim.x, sr, sd, sp);
+    }
+    if (valid && c == 0) {
+      if (O.reward) O.reward[ti] = reward;
+      if (O.done) O.done[ti] = done ? 1.0f : 0.0f;
+      if (O.done_u8) O.done_u8[i] = done ? 1 : 0;
+    }
+    if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)(t + 1) * N + i, c, X);
+  }
+  if (valid) quad::store_env(E, c, i, X);
 }
 
 // stats[s][t] = sum over groups g of work[s][g][t].  A block covers 64 consecutive (s, t)
@@ -193,6 +267,20 @@ int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream
   hipLaunchKernelGGL(k_stats_reduce, dim3((3 * T + 63) / 64), dim3(64 * RED_WAVES), 0, s, work, T, G, stats);
   return check_launch("stats reduce");
 }
+
+int compute_units() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 256;
+  return cus;
+}
+
+// The quad-layout loop while n leaves fewer than two lane-per-environment waves per SIMD
+// (n <= 32 envs per SIMD, four SIMDs per CU).
+static bool env_loop_is_quad(int n) { return n <= 32 * 4 * compute_units(); }
+
+int env_loop_stats_groups(int n) { return env_loop_is_quad(n) ? (n + 15) / 16 : groups_of(n); }
 
 }  // namespace auv
 
@@ -307,13 +395,24 @@ int auv_reset(auv_env* env, void* stream) {
   return AUV_OK;
 }
 
+
 static int launch_env_loop(auv_env* env, int T, int mode, const StepOut& O, hipStream_t s) {
-  const int G = groups_of(env->E.n);
+  const int n = env->E.n;
   const uint32_t g0 = (uint32_t)(env->global_step & 0xffffffffu);
-  if (mode == AUV_ACT_EXTERNAL)
-    hipLaunchKernelGGL(k_env_loop<true>, dim3(G), dim3(64), 0, s, env->veh, env->E, T, g0, O);
-  else
-    hipLaunchKernelGGL(k_env_loop<false>, dim3(G), dim3(64), 0, s, env->veh, env->E, T, g0, O);
+  const bool ext = (mode == AUV_ACT_EXTERNAL);
+  if (env_loop_is_quad(n)) {
+    const dim3 grid((n + 15) / 16);
+    if (ext)
+      hipLaunchKernelGGL(k_env_quad<true>, grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+    else
+      hipLaunchKernelGGL(k_env_quad<false>, grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+  } else {
+    const dim3 grid(groups_of(n));
+    if (ext)
+      hipLaunchKernelGGL(k_env_loop<true>, grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+    else
+      hipLaunchKernelGGL(k_env_loop<false>, grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+  }
   return check_launch("environment loop");
 }
 
@@ -334,7 +433,7 @@ int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_
   hipStream_t s = (hipStream_t)stream;
   if (int rc = launch_env_loop(env, 1, mode, O, s)) return rc;
   if (stats)
-    if (int rc = launch_stats_reduce(stats_work, 1, groups_of(env->E.n), stats, s)) return rc;   // one partial per wave of 64
+    if (int rc = launch_stats_reduce(stats_work, 1, env_loop_stats_groups(env->E.n), stats, s)) return rc;
   env->global_step += 1;
   return AUV_OK;
 }
@@ -368,7 +467,7 @@ int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const 
     O.stats_work = rb->stats_work;
     if (int rc = launch_env_loop(env, T, mode, O, s)) return rc;
     if (rb->stats)
-      if (int rc = launch_stats_reduce(rb->stats_work, T, groups_of(env->E.n), rb->stats, s)) return rc;
+      if (int rc = launch_stats_reduce(rb->stats_work, T, env_loop_stats_groups(env->E.n), rb->stats, s)) return rc;
   } else if (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE) {
     if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
     if (rb->stats)   // one partial per wave of 16 environments

@@ -35,6 +35,10 @@ constexpr uint32_t AUV_DEFAULT_SYNC_POLLS = 1u << 24;
 inline int stats_groups(int n) { return 4 * groups_of(n); }
 // partials the policy rollout actually writes for n envs (<= stats_groups(n))
 int rollout_stats_groups(int n);
+// partials the random / external environment loop writes for n envs (<= stats_groups(n))
+int env_loop_stats_groups(int n);
+// compute units of the current device (256 if the query fails)
+int compute_units();
 
 // launches implemented in auv_policy.hip
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy,

@@ -125,11 +125,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   if (tid < 64 * ROLLOUT_MAX_TILES) S.x[tid >> 6][lane] = bf16x8{};
   if (tid < HID) S.b1k[tid] = b[tid] * TWO_LOG2E;
   if (tid < 16) S.b3[tid] = tid < ACT ? b[2 * HID + tid] : 0.0f;
-  if (tid < 64) {                          // allocation rows x f_max
-    const int row = tid >> 3, j = tid & 7;
-    const int src = row < 3 ? row : (row >= 4 && row < 7 ? row - 1 : -1);
-    S.alloc[row][j] = src >= 0 ? V.alloc[src * 8 + j] * V.f_max : 0.0f;
-  }
+  quad::stage_alloc(V, S.alloc, tid);
   if (tid < ROLLOUT_MAX_TILES) S.obs_ready[tid] = S.h1_ready[tid] = S.mu_ready[tid] = 0u;
   __syncthreads();
   if (wave < ROLLOUT_MLP_WAVES) {
@@ -145,37 +141,11 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   const bool valid = i < E.n;
   const size_t N = (size_t)E.n, TN = (size_t)T * N;
   const uint32_t gid = E.env_offset + (uint32_t)i;
-  const int cv = c < 3 ? c : 0;            // a valid component row for lane 3's loads
 
-  float p, q, v, om, u0, u1;
-  int ep = 0;
-  uint32_t episode = 0;
-  quad::QObs ob;
+  quad::QEnv X;
   quad::QModel M;
   quad::QRef F;
-  {
-  Params P;
-  if (valid) {
-    p = c < 3 ? E.state[cv * N + i] : 0.0f;
-    q = E.state[(c < 3 ? 4 + c : 3) * N + i];
-    v = c < 3 ? E.state[(7 + cv) * N + i] : 0.0f;
-    om = c < 3 ? E.state[(10 + cv) * N + i] : 0.0f;
-    load_params(E.params, E.n, i, P);
-    ep = E.ep_step[i];
-    episode = E.episode[i];
-    ob.dpb = c < 3 ? E.obs[cv * N + i] : 0.0f;
-    ob.c0 = c < 3 ? E.obs[(3 + cv) * N + i] : 0.0f;
-    ob.c1 = c < 3 ? E.obs[(6 + cv) * N + i] : 0.0f;
-    u0 = E.obs[(15 + 2 * c) * N + i];
-    u1 = E.obs[(16 + 2 * c) * N + i];
-  } else {  // idle environments step a harmless dummy vehicle and are never stored
-    p = v = om = u0 = u1 = 0.0f;
-    q = c == 3 ? 1.0f : 0.0f;
-    P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
-    ob = quad::QObs{0, 0, 0};
-  }
-  quad::make_lane_consts(V, K, P, M, F);
-  }
+  quad::load_env(V, E, K, i, valid, X, M, F);
   float lsd0 = 0.0f, lsd1 = 0.0f, sig0 = 0.0f, sig1 = 0.0f;
   if (SAMPLE) {
     lsd0 = log_std[2 * c];
@@ -184,15 +154,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     sig1 = expf(lsd1);
   }
   auto store_traj = [&](int t1) {
-    if (O.traj && valid) {
-      const size_t base = (size_t)t1 * N + i, st = (size_t)(T + 1) * N;
-      if (c < 3) {
-        O.traj[c * st + base] = p;
-        O.traj[(7 + c) * st + base] = v;
-        O.traj[(10 + c) * st + base] = om;
-      }
-      O.traj[(c < 3 ? 4 + c : 3) * st + base] = q;
-    }
+    if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)t1 * N + i, c, X);
   };
   store_traj(0);
   StatsBuf SB{};
@@ -214,7 +176,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       stats_park(SB, O.stats_work, T, t1, lane, TPW * blockIdx.x + k, TPW * gridDim.x, sr, sd, sp);
     }
   };
-  put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
+  put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
   publish(&S.obs_ready[k], lane);
   for (int t = 0; t < T; ++t) {
     const size_t ti = (size_t)t * N + (size_t)i;
@@ -222,24 +184,14 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     // the first RK4 stage without the wrench (it enters the derivative additively), the
     // reference of the next step, and the previous step's reward and statistics.
     float dp1, dq1, dv1, dw1;
-    quad::rhs(K, M, 0.0f, 0.0f, q, v, om, dp1, dq1, dv1, dw1);
+    quad::rhs(K, M, 0.0f, 0.0f, X.q, X.v, X.om, dp1, dq1, dv1, dw1);
     float pr, qr;
-    quad::reference(E, K, F, ep + 1, pr, qr);
+    quad::reference(E, K, F, X.ep + 1, pr, qr);
     quad::QRefCols rc = quad::ref_columns(K, qr);
     if (t > 0) finish_step(t - 1);
-    if (O.obs && valid) {                  // o_t, recorded while the MLP waves work on it
-      if (c < 3) {
-        O.obs[c * TN + ti] = ob.dpb;
-        O.obs[(3 + c) * TN + ti] = ob.c0;
-        O.obs[(6 + c) * TN + ti] = ob.c1;
-        O.obs[(9 + c) * TN + ti] = v;
-        O.obs[(12 + c) * TN + ti] = om;
-      }
-      O.obs[(15 + 2 * c) * TN + ti] = u0;
-      O.obs[(16 + 2 * c) * TN + ti] = u1;
-    }
+    if (O.obs && valid) quad::store_obs(O.obs, TN, ti, c, X);   // o_t, recorded while the MLP waves work on it
     if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1), E.sync_polls)) {   // abandoned: poison
-      p = q = v = om = __builtin_nanf("");
+      X.p = X.q = X.v = X.om = __builtin_nanf("");
       break;
     }
     // policy output for this lane's two action components (fixed-order partial sums)
@@ -281,43 +233,25 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     float tf, tm, usq;
     {
       float Tf[8], Tm[8];
-      *reinterpret_cast<f32x4*>(&Tf[0]) = *reinterpret_cast<const f32x4*>(&S.alloc[c][0]);
-      *reinterpret_cast<f32x4*>(&Tf[4]) = *reinterpret_cast<const f32x4*>(&S.alloc[c][4]);
-      *reinterpret_cast<f32x4*>(&Tm[0]) = *reinterpret_cast<const f32x4*>(&S.alloc[4 + c][0]);
-      *reinterpret_cast<f32x4*>(&Tm[4]) = *reinterpret_cast<const f32x4*>(&S.alloc[4 + c][4]);
-      quad::wrench(Tf, Tm, a0, a1, u0, u1, tf, tm, usq);
+      quad::alloc_rows(S.alloc, c, Tf, Tm);
+      quad::wrench(Tf, Tm, a0, a1, X.u0, X.u1, tf, tm, usq);
     }
     const float tfi = tf * M.iMlin;
     if (E.substeps > 0) {
-      quad::rk4_from(K, M, tfi, tm, E.h, p, q, v, om, dp1, dq1, dv1 + tfi, __builtin_fmaf(tm, M.iMang, dw1));
-      for (int s = 1; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, p, q, v, om);
+      quad::rk4_from(K, M, tfi, tm, E.h, X.p, X.q, X.v, X.om, dp1, dq1, dv1 + tfi, __builtin_fmaf(tm, M.iMang, dw1));
+      for (int s = 1; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, X.p, X.q, X.v, X.om);
     }
-    ep += 1;
+    X.ep += 1;
     float dist;
-    quad::observe(K, p, q, pr, rc, ob, dist);
-    const bool done = (ep == E.H);
-    pv_q = q;
+    quad::observe(K, X.p, X.q, pr, rc, X.ob, dist);
+    const bool done = (X.ep == E.H);
+    pv_q = X.q;
     pv_qr = qr;
     pv_dist = dist;
     pv_usq = usq;
     pv_done = done;
-    if (done) {  // the whole quad takes this branch
-      episode += 1u;
-      State xs;
-      Params P;
-      reset_draws(E, gid, episode, xs, P);
-      quad::make_lane_consts(V, K, P, M, F);
-      if (valid && c == 0) store_params(E.params, E.n, i, P);
-      ep = 0;
-      p = quad::pick(K, xs.p[0], xs.p[1], xs.p[2], 0.0f);
-      q = quad::pick(K, xs.q[1], xs.q[2], xs.q[3], xs.q[0]);
-      v = om = 0.0f;
-      u0 = u1 = 0.0f;
-      quad::reference(E, K, F, 0, pr, qr);
-      rc = quad::ref_columns(K, qr);
-      quad::observe(K, p, q, pr, rc, ob, dist);
-    }
-    put_obs_quad(S, k, slot, c, ob, v, om, u0, u1);
+    if (done) quad::new_episode(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist);   // the whole quad
+    put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
     publish(&S.obs_ready[k], lane);
     // outputs of step t that the next observation does not need
     if (SAMPLE && O.logp) {
@@ -327,24 +261,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     store_traj(t + 1);
   }
   if (T > 0) finish_step(T - 1);
-  if (!valid) return;
-  if (c < 3) {
-    E.state[c * N + i] = p;
-    E.state[(7 + c) * N + i] = v;
-    E.state[(10 + c) * N + i] = om;
-    E.obs[c * N + i] = ob.dpb;
-    E.obs[(3 + c) * N + i] = ob.c0;
-    E.obs[(6 + c) * N + i] = ob.c1;
-    E.obs[(9 + c) * N + i] = v;
-    E.obs[(12 + c) * N + i] = om;
-  }
-  E.state[(c < 3 ? 4 + c : 3) * N + i] = q;
-  E.obs[(15 + 2 * c) * N + i] = u0;
-  E.obs[(16 + 2 * c) * N + i] = u1;
-  if (c == 0) {
-    E.ep_step[i] = ep;
-    E.episode[i] = episode;
-  }
+  if (valid) quad::store_env(E, c, i, X);
 }
 
 // Stand-alone MLP forward over obs [23][n] -> out [n_out][n]: workgroups of four MLP waves
@@ -444,14 +361,6 @@ int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, 
 // Tiles per workgroup: four where the batch fills every CU with 64 envs, fewer (down to one
 // 16-env tile) for smaller batches, so that they still use every CU (one workgroup fits a
 // CU at a time).
-static int compute_units() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    return 256;
-  return cus;
-}
-
 static int rollout_tiles_per_group(int n) {
   const int cus = compute_units();
   return n >= cus * 64 ? 4 : (n >= cus * 32 ? 2 : 1);

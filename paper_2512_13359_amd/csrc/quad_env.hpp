@@ -293,5 +293,124 @@ __device__ __forceinline__ void wrench(const float Tf[8], const float Tm[8], flo
   usq = qsum(__builtin_fmaf(u0, u0, u1 * u1));
 }
 
+
+// ------------------------------------------------------ allocation table in LDS ----
+// Rows c = 0..2: force row c, rows 4 + c: moment row c, each x f_max; rows 3 and 7 zero
+// (lane 3 of a quad reads them).  Written by the first 64 threads of the block.
+__device__ __forceinline__ void stage_alloc(const VehArgs& V, float (*alloc)[8], int tid) {
+  if (tid < 64) {
+    const int row = tid >> 3, j = tid & 7;
+    const int src = row < 3 ? row : (row >= 4 && row < 7 ? row - 1 : -1);
+    alloc[row][j] = src >= 0 ? V.alloc[src * 8 + j] * V.f_max : 0.0f;
+  }
+}
+
+__device__ __forceinline__ void alloc_rows(const float (*alloc)[8], int c, float Tf[8], float Tm[8]) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  *reinterpret_cast<f4*>(&Tf[0]) = *reinterpret_cast<const f4*>(&alloc[c][0]);
+  *reinterpret_cast<f4*>(&Tf[4]) = *reinterpret_cast<const f4*>(&alloc[c][4]);
+  *reinterpret_cast<f4*>(&Tm[0]) = *reinterpret_cast<const f4*>(&alloc[4 + c][0]);
+  *reinterpret_cast<f4*>(&Tm[4]) = *reinterpret_cast<const f4*>(&alloc[4 + c][4]);
+}
+
+// ------------------------------------------------- one environment, quad layout ----
+// What a lane holds of its environment between control steps.  Observation rows of the
+// environment: 0-2 dp_b, 3-5 and 6-8 the two reference columns, 9-11 v, 12-14 omega,
+// 15-22 the previous clipped action (lane c: rows 15 + 2c, 16 + 2c).
+struct QEnv {
+  float p, q, v, om;   // position, quaternion (lane 3: scalar part), body velocities
+  float u0, u1;        // this lane's two components of the previous clipped action
+  int ep;              // control steps into the episode
+  uint32_t episode;
+  QObs ob;
+};
+
+// Buffers of environment i -> lane; an idle environment (i >= n) gets a harmless dummy
+// vehicle at rest that is stepped but never stored.
+__device__ __forceinline__ void load_env(const VehArgs& V, const EnvArgs& E, const QK& K, int i, bool valid,
+                                         QEnv& X, QModel& M, QRef& F) {
+  const int c = K.c, cv = c < 3 ? c : 0;   // cv: a valid row for lane 3's loads
+  const size_t N = (size_t)E.n;
+  Params P;
+  if (valid) {
+    X.p = c < 3 ? E.state[cv * N + i] : 0.0f;
+    X.q = E.state[(c < 3 ? 4 + c : 3) * N + i];
+    X.v = c < 3 ? E.state[(7 + cv) * N + i] : 0.0f;
+    X.om = c < 3 ? E.state[(10 + cv) * N + i] : 0.0f;
+    load_params(E.params, E.n, i, P);
+    X.ep = E.ep_step[i];
+    X.episode = E.episode[i];
+    X.ob.dpb = c < 3 ? E.obs[cv * N + i] : 0.0f;
+    X.ob.c0 = c < 3 ? E.obs[(3 + cv) * N + i] : 0.0f;
+    X.ob.c1 = c < 3 ? E.obs[(6 + cv) * N + i] : 0.0f;
+    X.u0 = E.obs[(15 + 2 * c) * N + i];
+    X.u1 = E.obs[(16 + 2 * c) * N + i];
+  } else {
+    X.p = X.v = X.om = X.u0 = X.u1 = 0.0f;
+    X.q = c == 3 ? 1.0f : 0.0f;
+    X.ep = 0;
+    X.episode = 0;
+    P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
+    X.ob = QObs{0, 0, 0};
+  }
+  make_lane_consts(V, K, P, M, F);
+}
+
+// The observation of X into rows k of obs[k * stride + at].
+__device__ __forceinline__ void store_obs(float* __restrict__ obs, size_t stride, size_t at, int c, const QEnv& X) {
+  if (c < 3) {
+    obs[c * stride + at] = X.ob.dpb;
+    obs[(3 + c) * stride + at] = X.ob.c0;
+    obs[(6 + c) * stride + at] = X.ob.c1;
+    obs[(9 + c) * stride + at] = X.v;
+    obs[(12 + c) * stride + at] = X.om;
+  }
+  obs[(15 + 2 * c) * stride + at] = X.u0;
+  obs[(16 + 2 * c) * stride + at] = X.u1;
+}
+
+// The 13 state rows of X into s[k * stride + at] (p, q = (w, x, y, z), v, omega).
+__device__ __forceinline__ void store_state(float* __restrict__ s, size_t stride, size_t at, int c, const QEnv& X) {
+  if (c < 3) {
+    s[c * stride + at] = X.p;
+    s[(7 + c) * stride + at] = X.v;
+    s[(10 + c) * stride + at] = X.om;
+  }
+  s[(c < 3 ? 4 + c : 3) * stride + at] = X.q;
+}
+
+// Lane -> buffers of environment i (state, current observation, counters).
+__device__ __forceinline__ void store_env(const EnvArgs& E, int c, int i, const QEnv& X) {
+  const size_t N = (size_t)E.n;
+  store_state(E.state, N, (size_t)i, c, X);
+  store_obs(E.obs, N, (size_t)i, c, X);
+  if (c == 0) {
+    E.ep_step[i] = X.ep;
+    E.episode[i] = X.episode;
+  }
+}
+
+// Auto-reset of a finished episode (the whole quad calls it): fresh draws for the next
+// episode, step 0, previous action 0, and the observation of the new initial state
+// (pr, qr, rc: its reference).  The new parameters are stored at once.
+__device__ __forceinline__ void new_episode(const VehArgs& V, const EnvArgs& E, const QK& K, uint32_t gid, int i,
+                                            bool valid, QEnv& X, QModel& M, QRef& F, float& pr, float& qr,
+                                            QRefCols& rc, float& dist) {
+  X.episode += 1u;
+  State xs;
+  Params P;
+  reset_draws(E, gid, X.episode, xs, P);
+  make_lane_consts(V, K, P, M, F);
+  if (valid && K.c == 0) store_params(E.params, E.n, i, P);
+  X.ep = 0;
+  X.p = pick(K, xs.p[0], xs.p[1], xs.p[2], 0.0f);
+  X.q = pick(K, xs.q[1], xs.q[2], xs.q[3], xs.q[0]);
+  X.v = X.om = 0.0f;
+  X.u0 = X.u1 = 0.0f;
+  reference(E, K, F, 0, pr, qr);
+  rc = ref_columns(K, qr);
+  observe(K, X.p, X.q, pr, rc, X.ob, dist);
+}
+
 }  // namespace quad
 }  // namespace auv

@@ -107,6 +107,44 @@ def test_c2_full_size_sampled_envs():
         assert rel_err(got["reward"][-50:, sl], rec["reward"][-50:]).max() <= 1e-3
 
 
+def test_lane_layout_loop_large_batch():
+    """Above 32 envs per SIMD (four SIMDs per CU) the random / external loop keeps one
+    environment per lane instead of four lanes per environment.  A batch just past that
+    size with a ragged last wave and short episodes (auto-resets inside the run): random
+    actions bit-exact, dones exact, rewards and end states of three 64-env slices within
+    1e-3 of the oracle, then one external-action step."""
+    require_gpu()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n, T, H = 128 * cus + 1000 + 7, 40, 15
+    cfg = W.config("c2", n_envs=n, episode_len=H)
+    announce(f"lane-per-env loop n={n} T={T} H={H}")
+    g = gpu_env(cfg)
+    g.reset()
+    bufs = g.rollout_buffers(T, record=("act", "reward", "done", "stats"))
+    g.rollout(T, W.MODE_RANDOM, bufs=bufs)
+    got = {k: host(v) for k, v in bufs.items()}
+    s = got["stats"]
+    assert np.allclose(s[0], got["reward"].astype(np.float64).sum(1), rtol=1e-5, atol=1e-3)
+    assert np.array_equal(s[1], got["done"].sum(1))
+    acts = np.random.default_rng(9).uniform(-1.3, 1.3, (8, n)).astype(np.float32)
+    reward, done, _ = g.step(W.MODE_EXTERNAL, torch.from_numpy(acts).cuda())
+    state = host(g.state)
+    for off in (0, n // 2 + 11, n - 64):
+        o = oracle_env(W.config("c2", n_envs=64, env_offset=off, episode_len=H))
+        o.reset()
+        rec = o.rollout(T, W.MODE_RANDOM)
+        sl = slice(off, off + 64)
+        assert np.array_equal(got["act"][:, :, sl], rec["act"].astype(np.float32))
+        assert np.array_equal(got["done"][:, sl], rec["done"].astype(np.float32))
+        assert rel_err(got["reward"][:, sl], rec["reward"]).max() <= 1e-3
+        r_o, d_o, _, _ = o.step(acts[:, sl].astype(np.float64))
+        assert np.array_equal(host(done)[sl].astype(bool), d_o)
+        assert rel_err(host(reward)[sl], r_o).max() <= 1e-3
+        x = state[:, sl].copy()
+        x[3:7] = quat_aligned(x[3:7], o.x[3:7])
+        assert rel_err(x, o.x).max() <= 1e-3
+
+
 def test_one_step_from_identical_state():
     """One control step from the same seeded fp32 states on both sides (random poses and
     velocities; each side's own randomisation draws from the same seed), external seeded
