@@ -186,6 +186,84 @@ int auv_set_global_step(auv_env* env, int64_t step);
  * ends normally and leaves NaN state. */
 int auv_set_sync_poll_limit(auv_env* env, uint32_t polls);
 
+/* ---- PPO update of the policy and value MLPs on one minibatch ------------------------
+ * The clipped-surrogate objective of PPO (Schulman et al. 2017; the on-policy learner of
+ * paper Sec. II-B and III-A, which gives no hyperparameters), over minibatch samples b:
+ *   logp_b = sum_j [-((a_jb - mu_jb) / sigma_j)^2 / 2 - log sigma_j - log(2 pi) / 2],
+ *            sigma = exp(log_std), mu = policy(o_b)
+ *   rho_b  = exp(logp_b - logp_old_b)
+ *   A^_b   = (A_b - mean A) / (std A + 1e-8) over the minibatch (population std) when
+ *            normalize_adv, else A_b
+ *   L = -(1/B) sum_b min(rho_b A^_b, clip(rho_b, 1 - eps, 1 + eps) A^_b)
+ *       + (c_v / 2) (1/B) sum_b (V(o_b) - R_b)^2 - c_e sum_j (log sigma_j + (1 + log 2 pi) / 2)
+ * The gradient of min() flows through the unclipped term where it is the smaller (ties
+ * included).  The forward uses the bf16 weights and quantisation points of auv_mlp; the
+ * backward rounds dL/dy, dz2 and dz1 to bf16 before each product (bf16 MFMA, fp32
+ * accumulation); bias gradients and the tanh derivatives use the unrounded fp32 values.
+ *
+ * A network's parameters are one fp32 vector packed W1[256][23] | W2[256][256] |
+ * W3[n_out][256] | b1[256] | b2[256] | b3[n_out] | log_std[8] (policy only), row-major;
+ * gradients and Adam moments use the same packing.  The auv_mlp a rollout or auv_ppo_grad
+ * reads is a view of it: w = the bf16 copy of W1 | W2 | W3 (auv_ppo_net.w_bf16),
+ * b = theta + AUV_PPO_NW(n_out), log_std = theta + AUV_PPO_NW(n_out) + 512 + n_out. */
+#define AUV_PPO_NW(n_out) (256 * 23 + 256 * 256 + (n_out) * 256)
+#define AUV_PPO_NPARAM(n_out) (AUV_PPO_NW(n_out) + 512 + (n_out) + ((n_out) == 8 ? 8 : 0))
+
+typedef struct {
+  float clip_eps;      /* eps of the clipped surrogate, > 0 */
+  float vf_coef;       /* c_v >= 0 */
+  float ent_coef;      /* c_e (entropy bonus) */
+  float max_grad_norm; /* global-norm clipping over both networks' gradients; <= 0: off */
+  float lr, beta1, beta2, adam_eps; /* Adam (Kingma and Ba, Algorithm 1): lr > 0, 0 <= beta < 1, eps > 0 */
+  int32_t normalize_adv;            /* nonzero: normalise advantages over the minibatch */
+} auv_ppo_config;
+
+/* The rollout buffer a minibatch is drawn from (device, fp32, M = T N samples; sample
+ * s = t N + i is column s of every row, as auv_rollout and auv_gae write them). */
+typedef struct {
+  const float* obs;  /* [23][M] */
+  const float* act;  /* [8][M] actions before clipping */
+  const float* logp; /* [M] log-prob of the action under the policy that acted */
+  const float* adv;  /* [M] advantages */
+  const float* ret;  /* [M] returns (value targets) */
+  int64_t M;         /* 1 <= M < 2^31 */
+} auv_ppo_batch;
+
+/* One trainable network (device, caller-owned). */
+typedef struct {
+  float* theta;     /* fp32 parameters, packed as above */
+  float* adam_m;    /* Adam first moments, same packing */
+  float* adam_v;    /* Adam second moments */
+  uint16_t* w_bf16; /* bf16 copy of W1 | W2 | W3 (what the auv_mlp view's w points at) */
+  int32_t n_out;    /* 8 (policy) or 1 (value) */
+} auv_ppo_net;
+
+/* Bytes of device workspace auv_ppo_grad needs for a minibatch of B samples (-1 for B
+ * outside [1, 2^24]); about 1.5 KB per sample plus 80 MB. */
+int64_t auv_ppo_work_bytes(int32_t B);
+
+/* Loss and gradients of one minibatch: entries idx[0..B-1] (int32 sample indices into the
+ * batch; values outside [0, M) are clamped into it).  Overwrites grad_policy
+ * [AUV_PPO_NPARAM(8)], grad_value [AUV_PPO_NPARAM(1)] and stats [8]: surrogate loss, value
+ * loss, entropy, approximate KL (mean of logp_old - logp), fraction of samples whose
+ * gradient the clip removes, squared gradient norms of policy and value, and the clipping
+ * factor auv_ppo_adam applies.  work: auv_ppo_work_bytes(B) bytes, 16-byte aligned.  Reads
+ * of obs / act are coalesced when idx runs in blocks of 16 consecutive samples.  The
+ * result is deterministic (same inputs, same bits).  AUV_EINVAL, nothing enqueued: B
+ * outside [1, 2^24], NULL or misaligned pointers, a network other than 23-256-256-8 (with
+ * log_std) / 23-256-256-1, or a config out of range. */
+int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp* value,
+                 const auv_ppo_batch* batch, const int32_t* idx, int32_t B, float* grad_policy,
+                 float* grad_value, float* stats, void* work, void* stream);
+
+/* One Adam step (t >= 1: steps so far, this one included) of both networks on the
+ * gradients of auv_ppo_grad times stats[7]: rewrites theta, adam_m, adam_v and the bf16
+ * weight copies (round to nearest even).  AUV_EINVAL, nothing enqueued, for t < 1, NULL or
+ * misaligned pointers, wrong n_out, or a config out of range. */
+int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy,
+                 const auv_ppo_net* value, const float* grad_policy, const float* grad_value,
+                 const float* stats, void* stream);
+
 /* Message for the calling thread's last error ("" if none). */
 const char* auv_last_error(void);
 

@@ -48,6 +48,29 @@ class AuvRolloutBuffers(ctypes.Structure):
                                    "traj_state", "stats", "stats_work")]
 
 
+class AuvPpoConfig(ctypes.Structure):
+    _fields_ = [("clip_eps", _f), ("vf_coef", _f), ("ent_coef", _f), ("max_grad_norm", _f), ("lr", _f),
+                ("beta1", _f), ("beta2", _f), ("adam_eps", _f), ("normalize_adv", ctypes.c_int32)]
+
+
+class AuvPpoBatch(ctypes.Structure):
+    _fields_ = [("obs", _vp), ("act", _vp), ("logp", _vp), ("adv", _vp), ("ret", _vp), ("M", ctypes.c_int64)]
+
+
+class AuvPpoNet(ctypes.Structure):
+    _fields_ = [("theta", _vp), ("adam_m", _vp), ("adam_v", _vp), ("w_bf16", _vp), ("n_out", ctypes.c_int32)]
+
+
+def ppo_nw(n_out: int) -> int:
+    """AUV_PPO_NW: packed offset of b1 (the weight matrices' length)."""
+    return 256 * 23 + 256 * 256 + n_out * 256
+
+
+def ppo_nparam(n_out: int) -> int:
+    """AUV_PPO_NPARAM: length of a network's packed parameter vector."""
+    return ppo_nw(n_out) + 512 + n_out + (8 if n_out == 8 else 0)
+
+
 class AuvError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"libauv error {code}: {msg}")
@@ -71,6 +94,10 @@ def _load() -> ctypes.CDLL:
         "auv_get_global_step": (i64, [_vp]),
         "auv_set_global_step": (ctypes.c_int, [_vp, i64]),
         "auv_set_sync_poll_limit": (ctypes.c_int, [_vp, ctypes.c_uint32]),
+        "auv_ppo_work_bytes": (i64, [i32]),
+        "auv_ppo_grad": (ctypes.c_int, [P(AuvPpoConfig), P(AuvMlp), P(AuvMlp), P(AuvPpoBatch), _vp, i32, _vp, _vp,
+                                        _vp, _vp, _vp]),
+        "auv_ppo_adam": (ctypes.c_int, [P(AuvPpoConfig), i64, P(AuvPpoNet), P(AuvPpoNet), _vp, _vp, _vp, _vp]),
         "auv_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -153,6 +180,23 @@ def auv_set_sync_poll_limit(h: int, polls: int) -> None:
     _check(lib.auv_set_sync_poll_limit(h, polls))
 
 
+def auv_ppo_work_bytes(B: int) -> int:
+    return int(lib.auv_ppo_work_bytes(B))
+
+
+def auv_ppo_grad(cfg: AuvPpoConfig, policy: AuvMlp, value: AuvMlp, batch: AuvPpoBatch, idx, B: int,
+                 grad_policy, grad_value, stats, work, stream=None) -> None:
+    _check(lib.auv_ppo_grad(ctypes.byref(cfg), ctypes.byref(policy), ctypes.byref(value), ctypes.byref(batch),
+                            ptr(idx), B, ptr(grad_policy), ptr(grad_value), ptr(stats), ptr(work),
+                            stream_ptr(stream)))
+
+
+def auv_ppo_adam(cfg: AuvPpoConfig, t: int, policy: AuvPpoNet, value: AuvPpoNet, grad_policy, grad_value,
+                 stats, stream=None) -> None:
+    _check(lib.auv_ppo_adam(ctypes.byref(cfg), t, ctypes.byref(policy), ctypes.byref(value), ptr(grad_policy),
+                            ptr(grad_value), ptr(stats), stream_ptr(stream)))
+
+
 def auv_last_error() -> str:
     return lib.auv_last_error().decode()
 
@@ -180,6 +224,15 @@ def make_mlp(w, b, log_std, n_out: int) -> AuvMlp:
 
 def make_env_buffers(state, params, ep_step, episode, obs) -> AuvEnvBuffers:
     return AuvEnvBuffers(ptr(state), ptr(params), ptr(ep_step), ptr(episode), ptr(obs))
+
+
+def make_ppo_config(clip_eps=0.2, vf_coef=0.5, ent_coef=0.0, max_grad_norm=0.5, lr=3e-4, beta1=0.9,
+                    beta2=0.999, adam_eps=1e-8, normalize_adv=True) -> AuvPpoConfig:
+    return AuvPpoConfig(clip_eps, vf_coef, ent_coef, max_grad_norm, lr, beta1, beta2, adam_eps, int(bool(normalize_adv)))
+
+
+def make_ppo_batch(obs, act, logp, adv, ret, M: int) -> AuvPpoBatch:
+    return AuvPpoBatch(ptr(obs), ptr(act), ptr(logp), ptr(adv), ptr(ret), M)
 
 
 def make_rollout_buffers(**kw) -> AuvRolloutBuffers:

@@ -1,0 +1,756 @@
+// PPO update of the policy and value MLPs on one minibatch: the clipped-surrogate
+// objective of PPO (Schulman et al. 2017, the on-policy learner of paper Sec. II-B and
+// III-A), its gradient through both 23-256-256-n_out networks on bf16 MFMA, global-norm
+// gradient clipping and Adam (Kingma and Ba, Algorithm 1).
+//
+// Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 32):
+//   k_adv_stats     mean and 1 / (std + 1e-8) of the minibatch's advantages (one block)
+//   k_fwd_bwd<n>    per 16-sample tile: forward, loss, dL/dy, dz2 = (W3^T q(dL/dy)) (1 - h2^2);
+//                   writes q(dz2) and q(h1) for the next two kernels; accumulates dW3, db2,
+//                   db3, d log_std and the loss sums per workgroup
+//   k_dz1           per tile: dh1 = W2^T q(dz2), dz1 = dh1 (1 - h1^2) with h1 recomputed from
+//                   the input; accumulates dW1 = q(dz1) q(x)^T and db1 per workgroup
+//   k_dw2           dW2 = q(dz2) q(h1)^T, split over the samples (K), one 256 x 256 partial
+//                   per workgroup held in accumulator registers
+//   k_reduce        fixed-order sums of the per-workgroup partials -> packed gradient, and
+//                   per-block sums of squares
+//   k_finalize      loss statistics, gradient norms, the clipping factor
+//   k_adam          one Adam step and the bf16 weight copy
+// Every sum has a fixed order, so a call is bit-for-bit repeatable.
+//
+// MFMA operand layouts as in mlp_mfma.hpp (v_mfma_f32_16x16x32_bf16; lane l = 16 g + r;
+// K slot (g, j) stands for logical index kslot(g, j) = 16 (j / 4) + 4 g + j % 4).  In the
+// weight-gradient products the contraction runs over samples: slot (g, j) of a 32-sample
+// step is sample kslot(g, j), so a lane's first four slots are samples 4g..4g+3 of the
+// first 16-sample tile and its last four the same samples of the second tile.  Activations
+// come out of a product as D fragments (lane (g, r): features 4g..4g+3 of an M-tile, sample
+// r); a per-wave LDS transpose turns them into "half fragments" (lane (g, r): feature r of a
+// 16-feature tile, samples 4g..4g+3 of a 16-sample tile, 8 bytes).
+#include <cmath>
+
+#include "auv_internal.hpp"
+#include "mlp_mfma.hpp"
+#include "mlp_tile.hpp"
+
+namespace auv {
+namespace ppo {
+
+constexpr int NW = 4;               // waves per workgroup, 64 hidden features each
+constexpr int THREADS = 64 * NW;
+constexpr int TPAD = 20;            // bf16 row stride of the transpose buffers (8-byte aligned rows)
+constexpr int STATS = 4;            // per-workgroup loss sums: surrogate, log-ratio, clipped count, squared error
+constexpr float LOG_2PI = 1.83787706640934548f;
+
+struct Hp {
+  float clip_eps, vf_coef, ent_coef, max_grad_norm;
+  float inv_B;
+  int normalize;
+};
+
+struct Batch {
+  const float* obs;
+  const float* act;
+  const float* logp;
+  const float* adv;
+  const float* ret;
+  size_t M;
+};
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));   // four bf16: a half fragment
+
+// Workspace of one call (offsets in bytes from the caller's buffer; every part 256-aligned).
+struct Work {
+  float* advstat;       // [2] mean, 1 / (std + 1e-8)
+  bf16x8* dz2_frag;     // [Bp/16][8 K tiles][64 lanes] q(dz2) as layer-2 B fragments
+  u32x2* dz2_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz2) half fragments
+  u32x2* h1_half;       // [Bp/16][16 feature tiles][64 lanes] q(h1) half fragments
+  float* part_w3t;      // [G][256 f][16 j] dW3^T
+  float* part_b2;       // [G][256]
+  float* part_b3;       // [G][16]
+  float* part_ls;       // [G][16]
+  float* part_stats;    // [2 nets][G][STATS]
+  float* part_w1;       // [G][256 k][32 i]
+  float* part_b1;       // [G][256]
+  float* part_w2;       // [G][256 m][256 k]
+  float* part_ss;       // [2 nets][reduce blocks]
+};
+
+constexpr int MAX_GROUPS = 256;
+constexpr int RED_THREADS = 256;
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline int padded(int B) { return (B + 31) / 32 * 32; }
+inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * HID + n_out + (n_out == 8 ? 8 : 0); }
+inline int red_blocks(int n_out) { return (nparam(n_out) + RED_THREADS - 1) / RED_THREADS; }
+
+// Byte offsets of the workspace parts for a minibatch of B; returns the total.
+inline size_t work_layout(int B, size_t off[13]) {
+  const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
+  const size_t sizes[13] = {2 * sizeof(float),
+                            Bp * HID * 2, Bp * HID * 2, Bp * HID * 2,
+                            G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
+                            G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
+                            2 * (size_t)red_blocks(8) * 4};
+  size_t o = 0;
+  for (int k = 0; k < 13; ++k) {
+    off[k] = o;
+    o += align256(sizes[k]);
+  }
+  return o;
+}
+
+inline Work work_at(void* base, int B) {
+  size_t off[13];
+  work_layout(B, off);
+  char* p = (char*)base;
+  Work W;
+  W.advstat = (float*)(p + off[0]);
+  W.dz2_frag = (bf16x8*)(p + off[1]);
+  W.dz2_half = (u32x2*)(p + off[2]);
+  W.h1_half = (u32x2*)(p + off[3]);
+  W.part_w3t = (float*)(p + off[4]);
+  W.part_b2 = (float*)(p + off[5]);
+  W.part_b3 = (float*)(p + off[6]);
+  W.part_ls = (float*)(p + off[7]);
+  W.part_stats = (float*)(p + off[8]);
+  W.part_w1 = (float*)(p + off[9]);
+  W.part_b1 = (float*)(p + off[10]);
+  W.part_w2 = (float*)(p + off[11]);
+  W.part_ss = (float*)(p + off[12]);
+  return W;
+}
+
+// ------------------------------------------------------------------ device helpers ----
+// Sum over the 16 lanes of a DPP row (rotations by 8, 4, 2, 1); every lane gets the sum.
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dpp_move<0x128>(v);
+  v += dpp_move<0x124>(v);
+  v += dpp_move<0x122>(v);
+  v += dpp_move<0x121>(v);
+  return v;
+}
+
+__device__ __forceinline__ u32x2 half_of(const __bf16* T, int row, int g) {
+  return *reinterpret_cast<const u32x2*>(&T[row * TPAD + 4 * g]);
+}
+
+// Eight bf16 from two half fragments (first: K slots 0-3, second: slots 4-7).
+__device__ __forceinline__ bf16x8 join(u32x2 a, u32x2 b) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
+}
+
+__device__ __forceinline__ bf16x8 low_half(u32x2 a) { return join(a, u32x2{0u, 0u}); }
+
+// D-fragment values v[mt][i] (feature 16 mt + 4 g + i, sample r), rounded to bf16, into
+// this wave's transpose buffer T[feature][sample].
+__device__ __forceinline__ void put_d(__bf16* T, int g, int r, const f32x4 v[4]) {
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) T[(16 * mt + 4 * g + i) * TPAD + r] = (__bf16)v[mt][i];
+}
+
+// The same for B fragments of two K tiles (feature 32 kt + kslot(g, j), sample r).
+__device__ __forceinline__ void put_b(__bf16* T, int g, int r, const bf16x8 f[2]) {
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) T[(32 * kt + kslot(g, j)) * TPAD + r] = f[kt][j];
+}
+
+// Buffer sample of minibatch entry b (indices outside [0, M) are clamped into it).
+__device__ __forceinline__ int sample_of(const int32_t* __restrict__ idx, int b, int M) {
+  return min(max(idx[b], 0), M - 1);
+}
+
+// Layer-1 operand of a tile: lane (g, r) holds input features kslot(g, j) of sample s
+// (zero beyond the 23 inputs and for padding samples).
+__device__ __forceinline__ bf16x8 input_frag(const Batch& D, bool valid, int s, int g) {
+  bf16x8 x;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int k = kslot(g, j);
+    x[j] = (__bf16)((valid && k < 23) ? D.obs[(size_t)k * D.M + (size_t)s] : 0.0f);
+  }
+  return x;
+}
+
+// ------------------------------------------------------------------ kernels ----------
+__global__ __launch_bounds__(1024) void k_adv_stats(const float* __restrict__ adv, const int32_t* __restrict__ idx,
+                                                    int B, int M, float* __restrict__ out) {
+  __shared__ double red[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  auto block_sum = [&](double v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    __syncthreads();
+    if (lane == 0) red[w] = v;
+    __syncthreads();
+    double s = 0.0;
+    for (int k = 0; k < 16; ++k) s += red[k];
+    return s;
+  };
+  double s = 0.0;
+  for (int b = tid; b < B; b += 1024) s += (double)adv[sample_of(idx, b, M)];
+  const double mean = block_sum(s) / B;
+  double q = 0.0;
+  for (int b = tid; b < B; b += 1024) {
+    const double d = (double)adv[sample_of(idx, b, M)] - mean;
+    q += d * d;
+  }
+  const double var = block_sum(q) / B;
+  if (tid == 0) {
+    out[0] = (float)mean;
+    out[1] = (float)(1.0 / (sqrt(var) + 1e-8));
+  }
+}
+
+template <int NOUT>
+struct FwdShared {
+  bf16x8 h[8][64];            // hidden-1 tiles of the current sample tile [K tile][lane]
+  f32x4 o[NW][64];            // output split-K partials [wave][lane]
+  float b1k[HID];
+  float b3[16];
+  __bf16 T[NW][64 * TPAD];    // per-wave transpose buffer [feature][sample]
+  __bf16 Gy[NW][8 * TPAD];    // per-wave q(dL/dy) transposed [output row][sample]
+};
+
+// Forward, loss and the output-side backward of one network over 16-sample tiles (wave m
+// owns hidden features 64 m .. 64 m + 63).  NOUT = 8: the policy and the clipped
+// surrogate; NOUT = 1: the value net and the squared error.
+template <int NOUT>
+__global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restrict__ w, const float* __restrict__ b,
+                                                         const float* __restrict__ log_std, Batch D,
+                                                         const int32_t* __restrict__ idx, int B, int tiles, Hp hp,
+                                                         Work W, int net) {
+  __shared__ FwdShared<NOUT> S;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  TileMlpRegs<64> R;
+  tile_mlp_load<64>(w, b, NOUT, m, lane, R);
+  // W3^T fragments: A[f = 64 m + 16 mt + r][slot (g, j)] = W3[kslot(g, j)][f]
+  const uint16_t* W3 = w + HID * 23 + HID * HID;
+  bf16x8 w3t[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = kslot(g, j);
+      w3t[mt][j] = k < NOUT ? bf16_of_bits(W3[k * HID + 64 * m + 16 * mt + r]) : bf16_of_bits(0);
+    }
+  if (tid < HID) S.b1k[tid] = b[tid] * TWO_LOG2E;
+  if (tid < 16) S.b3[tid] = tid < NOUT ? b[2 * HID + tid] : 0.0f;
+  // policy: this lane's four action rows 4g .. 4g+3 (lanes g < 2)
+  float ls[4] = {0, 0, 0, 0}, ivar[4] = {0, 0, 0, 0};
+  if (NOUT == 8 && g < 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ls[i] = log_std[4 * g + i];
+      ivar[i] = expf(-2.0f * ls[i]);
+    }
+  }
+  float mean = 0.0f, inv_std = 1.0f;
+  if (NOUT == 8 && hp.normalize) {
+    mean = W.advstat[0];
+    inv_std = W.advstat[1];
+  }
+  f32x4 dw3[4], db2[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) dw3[mt] = db2[mt] = f32x4{0, 0, 0, 0};
+  float db3[4] = {0, 0, 0, 0}, dls[4] = {0, 0, 0, 0}, st[STATS] = {0, 0, 0, 0};
+  __bf16* T = S.T[m];
+  __bf16* Gy = S.Gy[m];
+  __syncthreads();
+
+  for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
+    const int b_r = t * 16 + r;
+    const bool valid = b_r < B;
+    const int s = valid ? sample_of(idx, b_r, (int)D.M) : 0;
+    // ---- forward
+    const bf16x8 x = input_frag(D, valid, s, g);
+    bf16x8 own[2];
+    tile_layer1<64>(R, x, S.b1k, m, lane, own);
+    S.h[2 * m][lane] = own[0];
+    S.h[2 * m + 1][lane] = own[1];
+    put_b(T, g, r, own);                      // q(h1) -> half fragments for dW2
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft) W.h1_half[((size_t)t * 16 + 4 * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
+    __syncthreads();
+    f32x4 acc[4];
+    tile_layer2_own<64>(R, own, acc);
+#pragma unroll
+    for (int kk = 2; kk < 8; ++kk) {
+      const bf16x8 hb = S.h[(2 * m + kk) & 7][lane];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[mt] = mfma(R.w2[mt][kk], hb, acc[mt]);
+    }
+    f32x4 h2[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) h2[mt][i] = tanh_bias(acc[mt][i], R.b2[mt][i]);
+    bf16x8 u2[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        u2[kt][i] = (__bf16)h2[2 * kt][i];
+        u2[kt][4 + i] = (__bf16)h2[2 * kt + 1][i];
+      }
+    f32x4 o = f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) o = mfma(R.w3[kt], u2[kt], o);
+    S.o[m][lane] = o;
+    put_b(T, g, r, u2);                       // q(h2) -> half fragments for dW3
+    __syncthreads();
+    f32x4 y = *reinterpret_cast<const f32x4*>(&S.b3[4 * g]);
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) y += S.o[ww][lane];
+
+    // ---- loss: dL/dy for this lane's output rows 4g .. 4g+3 of sample r
+    float gy[4] = {0, 0, 0, 0};
+    if (NOUT == 8) {
+      float a[4], d[4], zz[4], part = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = (valid && g < 2) ? D.act[(size_t)(4 * g + i) * D.M + (size_t)s] : 0.0f;
+        d[i] = g < 2 ? a[i] - y[i] : 0.0f;
+        zz[i] = d[i] * d[i] * ivar[i];
+        part += -0.5f * zz[i] - ls[i];
+      }
+      const float logp = part + __shfl_xor(part, 16) - 4.0f * LOG_2PI;   // lanes r and r + 16
+      const bool lv = valid && g < 2;
+      const float lpo = lv ? D.logp[s] : 0.0f;
+      const float ah = lv ? (hp.normalize ? (D.adv[s] - mean) * inv_std : D.adv[s]) : 0.0f;
+      const float rho = expf(logp - lpo);
+      const float unc = rho * ah;
+      const float clp = fminf(fmaxf(rho, 1.0f - hp.clip_eps), 1.0f + hp.clip_eps) * ah;
+      const bool active = unc <= clp;
+      const float coef = (lv && active) ? -ah * rho * hp.inv_B : 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gy[i] = coef * d[i] * ivar[i];
+      if (m == 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          db3[i] += gy[i];
+          dls[i] += coef * (zz[i] - 1.0f);
+        }
+        if (lv && g == 0) {
+          st[0] += -fminf(unc, clp);
+          st[1] += lpo - logp;
+          st[2] += active ? 0.0f : 1.0f;
+        }
+      }
+    } else {
+      if (valid && g == 0) {
+        const float e = y[0] - D.ret[s];
+        gy[0] = hp.vf_coef * hp.inv_B * e;
+        if (m == 0) {
+          db3[0] += gy[0];
+          st[3] += e * e;
+        }
+      }
+    }
+    bf16x8 gyf;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) gyf[j] = (__bf16)(j < 4 ? gy[j] : 0.0f);
+
+    // ---- dW3^T += q(h2) q(gy)^T over the tile's samples (K slots 4..7 empty)
+    if (g < 2) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Gy[(4 * g + i) * TPAD + r] = gyf[i];
+    }
+    const bf16x8 bgy = r < NOUT ? low_half(half_of(Gy, r, g)) : bf16x8{};
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) dw3[mt] = mfma(low_half(half_of(T, 16 * mt + r, g)), bgy, dw3[mt]);
+
+    // ---- dz2 = (W3^T q(gy)) (1 - h2^2), this wave's features
+    f32x4 dz[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const f32x4 dh = mfma(w3t[mt], gyf, f32x4{0, 0, 0, 0});
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dz[mt][i] = dh[i] * (1.0f - h2[mt][i] * h2[mt][i]);
+      db2[mt] += dz[mt];
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {          // layer-2 B fragments of K tiles 2m, 2m+1
+      bf16x8 f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[i] = (__bf16)dz[2 * kt][i];
+        f[4 + i] = (__bf16)dz[2 * kt + 1][i];
+      }
+      W.dz2_frag[((size_t)t * 8 + 2 * m + kt) * 64 + lane] = f;
+    }
+    put_d(T, g, r, dz);
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft) W.dz2_half[((size_t)t * 16 + 4 * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
+  }
+
+  // ---- per-workgroup partials
+  const int wg = blockIdx.x;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int f = 64 * m + 16 * mt + 4 * g + i;
+      W.part_w3t[((size_t)wg * HID + f) * 16 + r] = dw3[mt][i];
+      const float v = row_sum16(db2[mt][i]);
+      if (r == 0) W.part_b2[(size_t)wg * HID + f] = v;
+    }
+  if (m == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v = row_sum16(db3[i]), u = row_sum16(dls[i]);
+      if (r == 0 && g < 2) {
+        W.part_b3[wg * 16 + 4 * g + i] = v;
+        W.part_ls[wg * 16 + 4 * g + i] = u;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < STATS; ++q) {
+      const float v = row_sum16(st[q]);
+      if (lane == 0) W.part_stats[((size_t)net * MAX_GROUPS + wg) * STATS + q] = v;
+    }
+  }
+}
+
+// dh1 = W2^T q(dz2) for this wave's hidden-1 features k (64 m .. 64 m + 63), dz1, and the
+// layer-1 weight and bias gradients.
+__global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__ w, const float* __restrict__ b,
+                                                    Batch D, const int32_t* __restrict__ idx, int B, int tiles,
+                                                    Work W) {
+  __shared__ __attribute__((aligned(16))) float b1k[HID];            // read as f32x4
+  __shared__ __attribute__((aligned(16))) __bf16 Ts[NW][64 * TPAD];  // rows read as 8-byte halves
+  __shared__ __attribute__((aligned(16))) __bf16 Xs[NW][32 * TPAD];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  const uint16_t* W1 = w;
+  const uint16_t* W2 = w + HID * 23;
+  bf16x8 w1[4], w2t[4][8];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) {
+    const int k = 64 * m + 16 * mt + r;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = kslot(g, j);
+      w1[mt][j] = i < 23 ? bf16_of_bits(W1[k * 23 + i]) : bf16_of_bits(0);
+    }
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) w2t[mt][kt][j] = bf16_of_bits(W2[(32 * kt + kslot(g, j)) * HID + k]);
+  }
+  if (tid < HID) b1k[tid] = b[tid] * TWO_LOG2E;
+  f32x4 dw1[4][2], db1[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) {
+    db1[mt] = dw1[mt][0] = dw1[mt][1] = f32x4{0, 0, 0, 0};
+  }
+  __bf16* T = Ts[m];
+  __bf16* X = Xs[m];
+  __syncthreads();
+  f32x4 b1[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) b1[mt] = *reinterpret_cast<const f32x4*>(&b1k[64 * m + 16 * mt + 4 * g]);
+
+  for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
+    const int b_r = t * 16 + r;
+    const bool valid = b_r < B;
+    const int s = valid ? sample_of(idx, b_r, (int)D.M) : 0;
+    bf16x8 zf[8];
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt) zf[kt] = W.dz2_frag[((size_t)t * 8 + kt) * 64 + lane];
+    const bf16x8 x = input_frag(D, valid, s, g);
+    f32x4 acc[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) acc[mt] = f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[mt] = mfma(w2t[mt][kt], zf[kt], acc[mt]);
+    f32x4 dz[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const f32x4 z1 = mfma(w1[mt], x, f32x4{0, 0, 0, 0});
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float h = tanh_bias(z1[i], b1[mt][i]);
+        dz[mt][i] = acc[mt][i] * (1.0f - h * h);
+      }
+      db1[mt] += dz[mt];
+    }
+    // dW1 += q(dz1) q(x)^T over the tile's samples (K slots 4..7 empty)
+    put_d(T, g, r, dz);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) X[kslot(g, j) * TPAD + r] = x[j];
+    bf16x8 bx[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) bx[nt] = low_half(half_of(X, 16 * nt + r, g));
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const bf16x8 a = low_half(half_of(T, 16 * mt + r, g));
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) dw1[mt][nt] = mfma(a, bx[nt], dw1[mt][nt]);
+    }
+  }
+
+  const int wg = blockIdx.x;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = 64 * m + 16 * mt + 4 * g + i;
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) W.part_w1[((size_t)wg * HID + k) * 32 + 16 * nt + r] = dw1[mt][nt][i];
+      const float v = row_sum16(db1[mt][i]);
+      if (r == 0) W.part_b1[(size_t)wg * HID + k] = v;
+    }
+}
+
+// dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup: wave m owns rows
+// 64 m .. 64 m + 63 (4 M-tiles) and all 256 columns (16 N-tiles).  The next step's
+// fragments are loaded before the current step's 64 products.
+__global__ __launch_bounds__(THREADS, 1) void k_dw2(const u32x2* __restrict__ dz2_half, const u32x2* __restrict__ h1_half,
+                                                    int steps, float* __restrict__ part_w2) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  const int per = (steps + gridDim.x - 1) / gridDim.x;
+  const int u0 = blockIdx.x * per, u1 = min(steps, u0 + per);
+  f32x4 acc[4][16];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 16; ++nt) acc[mt][nt] = f32x4{0, 0, 0, 0};
+  auto at = [&](int tile, int ft) { return ((size_t)tile * 16 + ft) * 64 + lane; };
+  bf16x8 A[4], Bf[16];
+  auto load = [&](int u, bf16x8* a, bf16x8* bb) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) a[mt] = join(dz2_half[at(2 * u, 4 * m + mt)], dz2_half[at(2 * u + 1, 4 * m + mt)]);
+#pragma unroll
+    for (int nt = 0; nt < 16; ++nt) bb[nt] = join(h1_half[at(2 * u, nt)], h1_half[at(2 * u + 1, nt)]);
+  };
+  if (u0 < u1) load(u0, A, Bf);
+  for (int u = u0; u < u1; ++u) {
+    bf16x8 An[4], Bn[16];
+    if (u + 1 < u1) load(u + 1, An, Bn);
+#pragma unroll
+    for (int nt = 0; nt < 16; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[mt], Bf[nt], acc[mt][nt]);
+    if (u + 1 < u1) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) A[mt] = An[mt];
+#pragma unroll
+      for (int nt = 0; nt < 16; ++nt) Bf[nt] = Bn[nt];
+    }
+  }
+  float* out = part_w2 + (size_t)blockIdx.x * HID * HID;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int nt = 0; nt < 16; ++nt) out[(64 * m + 16 * mt + 4 * g + i) * HID + 16 * nt + r] = acc[mt][nt][i];
+}
+
+// Packed gradient of one network = fixed-order sums of the partials; per-block sums of
+// squares for the global norm.  G1: forward/backward groups (dW3, db2, db3, d log_std),
+// G2: dz1 groups (dW1, db1), G3: dW2 groups.
+__global__ __launch_bounds__(RED_THREADS) void k_reduce(int n_out, int G1, int G2, int G3, Work W, float ent_coef,
+                                                        float* __restrict__ grad, float* __restrict__ ss) {
+  __shared__ float red[RED_THREADS / 64];
+  const int e = blockIdx.x * RED_THREADS + threadIdx.x;
+  const int nW1 = HID * 23, nW2 = HID * HID, nW3 = n_out * HID;
+  const int P = nW1 + nW2 + nW3 + 2 * HID + n_out + (n_out == 8 ? 8 : 0);
+  float v = 0.0f;
+  if (e < P) {
+    int q = e;
+    if (q < nW1) {
+      const int k = q / 23, i = q - 23 * k;
+      for (int wg = 0; wg < G2; ++wg) v += W.part_w1[((size_t)wg * HID + k) * 32 + i];
+    } else if ((q -= nW1) < nW2) {
+      for (int wg = 0; wg < G3; ++wg) v += W.part_w2[(size_t)wg * HID * HID + q];
+    } else if ((q -= nW2) < nW3) {
+      const int j = q / HID, f = q - HID * j;
+      for (int wg = 0; wg < G1; ++wg) v += W.part_w3t[((size_t)wg * HID + f) * 16 + j];
+    } else if ((q -= nW3) < HID) {
+      for (int wg = 0; wg < G2; ++wg) v += W.part_b1[(size_t)wg * HID + q];
+    } else if ((q -= HID) < HID) {
+      for (int wg = 0; wg < G1; ++wg) v += W.part_b2[(size_t)wg * HID + q];
+    } else if ((q -= HID) < n_out) {
+      for (int wg = 0; wg < G1; ++wg) v += W.part_b3[wg * 16 + q];
+    } else {
+      q -= n_out;
+      for (int wg = 0; wg < G1; ++wg) v += W.part_ls[wg * 16 + q];
+      v -= ent_coef;
+    }
+    grad[e] = v;
+  }
+  const float s2 = wave_sum(v * v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s2;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    for (int k = 0; k < RED_THREADS / 64; ++k) t += red[k];
+    ss[blockIdx.x] = t;
+  }
+}
+
+// stats: [0] surrogate loss, [1] value loss, [2] entropy, [3] approx KL, [4] clipped
+// fraction, [5] |grad policy|^2, [6] |grad value|^2, [7] clipping factor.  One wave; every
+// sum in a fixed order.
+__global__ __launch_bounds__(64) void k_finalize(int G1p, int G1v, Work W, int nbp, int nbv, int rb,
+                                                 const float* __restrict__ log_std, Hp hp, float* __restrict__ stats) {
+  const int lane = threadIdx.x;
+  float sp = 0.0f, sv = 0.0f, pg = 0.0f, kl = 0.0f, cl = 0.0f, vs = 0.0f;
+  for (int k = lane; k < nbp; k += 64) sp += W.part_ss[k];
+  for (int k = lane; k < nbv; k += 64) sv += W.part_ss[rb + k];
+  for (int k = lane; k < G1p; k += 64) {
+    const float* q = W.part_stats + (size_t)k * STATS;
+    pg += q[0];
+    kl += q[1];
+    cl += q[2];
+  }
+  for (int k = lane; k < G1v; k += 64) vs += W.part_stats[((size_t)MAX_GROUPS + k) * STATS + 3];
+  sp = wave_sum(sp);
+  sv = wave_sum(sv);
+  pg = wave_sum(pg);
+  kl = wave_sum(kl);
+  cl = wave_sum(cl);
+  vs = wave_sum(vs);
+  if (lane == 0) {
+    float ent = 0.0f;
+    for (int j = 0; j < 8; ++j) ent += log_std[j] + 0.5f * (1.0f + LOG_2PI);
+    stats[0] = pg * hp.inv_B;
+    stats[1] = 0.5f * hp.vf_coef * vs * hp.inv_B;
+    stats[2] = ent;
+    stats[3] = kl * hp.inv_B;
+    stats[4] = cl * hp.inv_B;
+    stats[5] = sp;
+    stats[6] = sv;
+    stats[7] = hp.max_grad_norm > 0.0f ? fminf(1.0f, hp.max_grad_norm / (sqrtf(sp + sv) + 1e-6f)) : 1.0f;
+  }
+}
+
+// One Adam step on P packed parameters with gradient grad * stats[7]; the first nW (the
+// weight matrices) are also written to the bf16 copy, rounded to nearest even.
+__global__ __launch_bounds__(256) void k_adam(int P, int nW, float* __restrict__ theta, float* __restrict__ mom,
+                                              float* __restrict__ vel, uint16_t* __restrict__ wbf,
+                                              const float* __restrict__ grad, const float* __restrict__ stats,
+                                              float lr, float b1, float b2, float eps, float bc1, float bc2) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= P) return;
+  const float g = grad[e] * stats[7];
+  const float m = b1 * mom[e] + (1.0f - b1) * g;
+  const float v = b2 * vel[e] + (1.0f - b2) * g * g;
+  const float th = theta[e] - lr * (m / bc1) / (sqrtf(v / bc2) + eps);
+  mom[e] = m;
+  vel[e] = v;
+  theta[e] = th;
+  if (e < nW) wbf[e] = __builtin_bit_cast(uint16_t, (__bf16)th);
+}
+
+}  // namespace ppo
+}  // namespace auv
+
+// ------------------------------------------------------------------ C interface ----
+using namespace auv;
+
+static int check_net(const auv_mlp* n, int n_out, const char* what) {
+  if (!n || !n->w || !n->b) return set_error(AUV_EINVAL, "%s: NULL network or weights", what);
+  if (n->n_out != n_out) return set_error(AUV_EINVAL, "%s: n_out must be %d, got %d", what, n_out, n->n_out);
+  if (!aligned16(n->w) || !aligned16(n->b)) return set_error(AUV_EINVAL, "%s: weights not 16-byte aligned", what);
+  return AUV_OK;
+}
+
+static int check_ppo_config(const auv_ppo_config* c) {
+  if (!c) return set_error(AUV_EINVAL, "PPO: NULL config");
+  if (!(c->clip_eps > 0.0f) || !(c->vf_coef >= 0.0f) || !(c->lr > 0.0f) || !(c->beta1 >= 0.0f && c->beta1 < 1.0f) ||
+      !(c->beta2 >= 0.0f && c->beta2 < 1.0f) || !(c->adam_eps > 0.0f) || !std::isfinite(c->ent_coef) ||
+      !std::isfinite(c->max_grad_norm))
+    return set_error(AUV_EINVAL, "PPO: config out of range (clip_eps > 0, vf_coef >= 0, lr > 0, 0 <= betas < 1, adam_eps > 0)");
+  return AUV_OK;
+}
+
+constexpr int32_t PPO_MAX_B = 1 << 24;
+
+extern "C" {
+
+int64_t auv_ppo_work_bytes(int32_t B) {
+  if (B < 1 || B > PPO_MAX_B) return -1;
+  size_t off[13];
+  return (int64_t)ppo::work_layout(B, off);
+}
+
+int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp* value, const auv_ppo_batch* batch,
+                 const int32_t* idx, int32_t B, float* grad_policy, float* grad_value, float* stats, void* work,
+                 void* stream) {
+  if (int rc = check_ppo_config(cfg)) return rc;
+  if (int rc = check_net(policy, ACT, "auv_ppo_grad policy")) return rc;
+  if (int rc = check_net(value, 1, "auv_ppo_grad value")) return rc;
+  if (!policy->log_std || !aligned16(policy->log_std)) return set_error(AUV_EINVAL, "auv_ppo_grad: policy needs an aligned log_std");
+  if (B < 1 || B > PPO_MAX_B) return set_error(AUV_EINVAL, "auv_ppo_grad: B must be in [1, %d], got %d", PPO_MAX_B, B);
+  if (!batch || batch->M < 1 || batch->M > INT32_MAX) return set_error(AUV_EINVAL, "auv_ppo_grad: batch M must be in [1, 2^31)");
+  const void* ptrs[10] = {batch->obs, batch->act, batch->logp, batch->adv, batch->ret, idx, grad_policy, grad_value, stats, work};
+  for (int k = 0; k < 10; ++k)
+    if (!ptrs[k] || !aligned16(ptrs[k])) return set_error(AUV_EINVAL, "auv_ppo_grad: pointer %d NULL or not 16-byte aligned", k);
+  hipStream_t s = (hipStream_t)stream;
+  const int tiles = ppo::padded(B) / 16, steps = ppo::padded(B) / 32;
+  const int cus = std::min(compute_units(), ppo::MAX_GROUPS);
+  const int G1 = std::min(cus, tiles), G3 = std::min(cus, steps);
+  const ppo::Work W = ppo::work_at(work, B);
+  const ppo::Hp hp{cfg->clip_eps, cfg->vf_coef, cfg->ent_coef, cfg->max_grad_norm, 1.0f / (float)B, cfg->normalize_adv ? 1 : 0};
+  const ppo::Batch D{batch->obs, batch->act, batch->logp, batch->adv, batch->ret, (size_t)batch->M};
+  const int rb = ppo::red_blocks(ACT);
+  if (hp.normalize) hipLaunchKernelGGL(ppo::k_adv_stats, dim3(1), dim3(1024), 0, s, batch->adv, idx, B, (int)batch->M, W.advstat);
+  hipLaunchKernelGGL(ppo::k_fwd_bwd<8>, dim3(G1), dim3(ppo::THREADS), 0, s, policy->w, policy->b, policy->log_std, D, idx,
+                     B, tiles, hp, W, 0);
+  hipLaunchKernelGGL(ppo::k_dz1, dim3(G1), dim3(ppo::THREADS), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
+  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(ppo::THREADS), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(ppo::RED_THREADS), 0, s, ACT, G1, G1, G3, W, cfg->ent_coef,
+                     grad_policy, W.part_ss);
+  hipLaunchKernelGGL(ppo::k_fwd_bwd<1>, dim3(G1), dim3(ppo::THREADS), 0, s, value->w, value->b, (const float*)nullptr, D,
+                     idx, B, tiles, hp, W, 1);
+  hipLaunchKernelGGL(ppo::k_dz1, dim3(G1), dim3(ppo::THREADS), 0, s, value->w, value->b, D, idx, B, tiles, W);
+  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(ppo::THREADS), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(ppo::RED_THREADS), 0, s, 1, G1, G1, G3, W, 0.0f,
+                     grad_value, W.part_ss + rb);
+  hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, G1, G1, W, rb, ppo::red_blocks(1), rb, policy->log_std, hp,
+                     stats);
+  return check_launch("auv_ppo_grad");
+}
+
+int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy, const auv_ppo_net* value,
+                 const float* grad_policy, const float* grad_value, const float* stats, void* stream) {
+  if (int rc = check_ppo_config(cfg)) return rc;
+  if (t < 1) return set_error(AUV_EINVAL, "auv_ppo_adam: t must be >= 1");
+  const auv_ppo_net* nets[2] = {policy, value};
+  const float* grads[2] = {grad_policy, grad_value};
+  const int n_outs[2] = {ACT, 1};
+  if (!stats || !aligned16(stats)) return set_error(AUV_EINVAL, "auv_ppo_adam: stats NULL or not aligned");
+  for (int k = 0; k < 2; ++k) {
+    const auv_ppo_net* n = nets[k];
+    if (!n || n->n_out != n_outs[k]) return set_error(AUV_EINVAL, "auv_ppo_adam: network %d missing or n_out != %d", k, n_outs[k]);
+    const void* ptrs[5] = {n->theta, n->adam_m, n->adam_v, n->w_bf16, grads[k]};
+    for (int q = 0; q < 5; ++q)
+      if (!ptrs[q] || !aligned16(ptrs[q])) return set_error(AUV_EINVAL, "auv_ppo_adam: network %d pointer %d NULL or not aligned", k, q);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  const float bc1 = (float)(1.0 - std::pow((double)cfg->beta1, (double)t));
+  const float bc2 = (float)(1.0 - std::pow((double)cfg->beta2, (double)t));
+  for (int k = 0; k < 2; ++k) {
+    const int P = ppo::nparam(n_outs[k]), nW = HID * 23 + HID * HID + n_outs[k] * HID;
+    hipLaunchKernelGGL(ppo::k_adam, dim3((P + 255) / 256), dim3(256), 0, s, P, nW, nets[k]->theta, nets[k]->adam_m,
+                       nets[k]->adam_v, nets[k]->w_bf16, grads[k], stats, cfg->lr, cfg->beta1, cfg->beta2, cfg->adam_eps,
+                       bc1, bc2);
+  }
+  return check_launch("auv_ppo_adam");
+}
+
+}  // extern "C"

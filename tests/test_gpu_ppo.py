@@ -1,0 +1,210 @@
+"""GPU parity of the PPO update (auv_ppo_grad, auv_ppo_adam) against the fp64 oracle
+(oracle/ppo.py with the bf16 quantisation points of the MFMA path), through the C
+interface.
+
+Inputs: seeded draws (workloads.ppo_draws) turned into actions and old log-probabilities
+by the oracle's own policy evaluation; target ratios stay 0.03 away from the clip bounds so
+that the GPU and the oracle take every clipping decision the same way.
+
+Tolerance of the gradients.  The oracle's quantised gradient differs from the exact one by
+about 1-2 units of 2^-8 of each tensor's scale (bf16 rounding of layer inputs and of the
+back-propagated values; pinned in test_oracle_ppo).  The GPU computes the same quantised
+quantity; it differs from the oracle only where its fp32 value before a bf16 rounding
+falls on the other side of a rounding midpoint than the oracle's fp64 value, and by fp32
+accumulation.  Those differences are a fraction of the quantisation effect itself, so each
+tensor must agree to 2^-8 of its scale (max-abs) and 2^-9 in norm."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import ppo as oppo
+from oracle.mlp import bf16_bits_to_f64, bf16_round
+from tests.gpu_util import announce, host, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = {8: (23, 256, 8, True), 1: (23, 256, 1, False)}
+
+
+def _oracle_params(net: dict) -> dict:
+    p = {k: bf16_bits_to_f64(net[k]) for k in ("W1", "W2", "W3")}
+    for k in ("b1", "b2", "b3"):
+        p[k] = np.asarray(net[k], np.float32).astype(np.float64)
+    if "log_std" in net and p["W3"].shape[0] == 8:
+        p["log_std"] = np.asarray(net["log_std"], np.float32).astype(np.float64)
+    return p
+
+
+def _buffer(M: int, seed: int, pol: dict):
+    """Synthetic rollout buffer: act = mu + sigma eps and logp_old from the oracle policy."""
+    d = W.ppo_draws(M, seed)
+    mu, _ = oppo.mlp_forward_cache(d["obs"].astype(np.float64), pol, quantize=True)
+    sig = np.exp(pol["log_std"])[:, None]
+    act = (mu + sig * d["eps"]).astype(np.float32)
+    logp = oppo.gaussian_logp(act.astype(np.float64), mu, pol["log_std"])
+    logp_old = (logp - np.log(d["ratio"])).astype(np.float32)
+    return dict(obs=d["obs"], act=act, logp=logp_old, adv=d["adv"], ret=d["ret"])
+
+
+@pytest.fixture(scope="module")
+def setup():
+    require_gpu()
+    from paper_2512_13359_amd import PpoLearner
+    netp = W.mlp_weights(8, W.POLICY_SEED)
+    netv = W.mlp_weights(1, W.VALUE_SEED)
+    pol, val = _oracle_params(netp), _oracle_params(netv)
+    M = 6000
+    buf = _buffer(M, 11, pol)
+    dev = {k: torch.from_numpy(np.ascontiguousarray(v)).cuda() for k, v in buf.items()}
+    return netp, netv, pol, val, buf, dev, M, PpoLearner
+
+
+def _check_grads(got: np.ndarray, want: np.ndarray, n_out: int, what: str):
+    g, w = oppo.unpack(got, *SHAPES[n_out]), oppo.unpack(want, *SHAPES[n_out])
+    for k in g:
+        scale = np.abs(w[k]).max()
+        err = np.abs(g[k] - w[k]).max()
+        nerr = np.linalg.norm(g[k] - w[k]) / max(np.linalg.norm(w[k]), 1e-30)
+        print(f"    {what} {k}: max-abs {err / scale / 2 ** -8:.3f} x 2^-8 of scale, norm {nerr / 2 ** -9:.3f} x 2^-9")
+        assert err <= 2.0 ** -8 * scale, (what, k, err / scale)
+        assert nerr <= 2.0 ** -9, (what, k, nerr)
+
+
+@pytest.mark.parametrize("B,normalize", [(1000, True), (1000, False), (64, True), (17, True), (1, False)])
+def test_ppo_grad_parity(setup, B, normalize):
+    netp, netv, pol, val, buf, dev, M, PpoLearner = setup
+    announce(f"ppo grad parity B={B} normalize={normalize}")
+    L = PpoLearner(netp, netv, normalize_adv=normalize, ent_coef=0.01)
+    idx = W.ppo_minibatch_idx(M, B, seed=B)
+    batch = L.batch(dev["obs"], dev["act"], dev["logp"], dev["adv"], dev["ret"])
+    L.grad(batch, torch.from_numpy(idx).cuda())
+    st = host(L.stats)
+    cols = idx.astype(np.int64)
+    want = oppo.ppo_loss_grad(buf["obs"][:, cols], buf["act"][:, cols], buf["logp"][cols], buf["adv"][cols],
+                              buf["ret"][cols], pol, val, dict(normalize_adv=normalize, ent_coef=0.01),
+                              quantize=True)
+    _check_grads(host(L.pol.grad), want["grad_pol"], 8, "policy")
+    _check_grads(host(L.val.grad), want["grad_val"], 1, "value")
+    assert abs(st[0] - want["pg_loss"]) <= 2e-3 * max(1.0, abs(want["pg_loss"]))
+    assert abs(st[1] - want["v_loss"]) <= 2e-3 * max(1.0, abs(want["v_loss"]))
+    assert abs(st[2] - want["entropy"]) <= 1e-5 * abs(want["entropy"])
+    assert abs(st[3] - want["approx_kl"]) <= 2e-3
+    assert st[4] == pytest.approx(want["clip_frac"], abs=0.5 / B)
+    gp, gv = host(L.pol.grad).astype(np.float64), host(L.val.grad).astype(np.float64)
+    assert st[5] == pytest.approx(np.sum(gp * gp), rel=1e-4)
+    assert st[6] == pytest.approx(np.sum(gv * gv), rel=1e-4)
+    assert st[7] == pytest.approx(oppo.clip_scale([gp, gv], 0.5), rel=1e-6)
+
+
+def test_ppo_grad_deterministic_and_block_independent(setup):
+    """Same inputs, same bits; and the result does not depend on how the minibatch is
+    ordered within its 16-sample tiles beyond fp32 summation order (permuted tiles give
+    the same gradient to fp32 rounding)."""
+    netp, netv, pol, val, buf, dev, M, PpoLearner = setup
+    announce("ppo grad determinism")
+    L = PpoLearner(netp, netv)
+    idx = W.ppo_minibatch_idx(M, 4096, seed=3)
+    batch = L.batch(dev["obs"], dev["act"], dev["logp"], dev["adv"], dev["ret"])
+    L.grad(batch, torch.from_numpy(idx).cuda())
+    a = host(L.pol.grad).copy(), host(L.val.grad).copy(), host(L.stats).copy()
+    L.grad(batch, torch.from_numpy(idx).cuda())
+    b = host(L.pol.grad), host(L.val.grad), host(L.stats)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    perm = np.random.default_rng(0).permutation(idx.size // 16)
+    idx2 = idx.reshape(-1, 16)[perm].ravel()
+    L.grad(batch, torch.from_numpy(np.ascontiguousarray(idx2)).cuda())
+    c = host(L.pol.grad)
+    assert np.max(np.abs(c - a[0])) <= 1e-5 * np.abs(a[0]).max()
+
+
+def test_ppo_adam_parity_two_steps(setup):
+    """Two Adam steps from seeded parameters and moments on seeded gradients with a
+    clipping factor: theta, m, v to fp32 rounding of the fp64 update; the bf16 copy is the
+    round-to-nearest-even of the GPU's own fp32 theta, bit for bit."""
+    netp, netv, pol, val, buf, dev, M, PpoLearner = setup
+    announce("ppo adam parity")
+    from paper_2512_13359_amd import _abi as A
+    L = PpoLearner(netp, netv, lr=1e-3)
+    r = np.random.default_rng(5)
+    # the device receives the hyperparameters as fp32: the oracle takes those values exactly
+    hp = {k: float(np.float32(v)) for k, v in dict(lr=1e-3, beta1=0.9, beta2=0.999, adam_eps=1e-8).items()}
+    ref = {}
+    for net in (L.pol, L.val):
+        P = A.ppo_nparam(net.n_out)
+        th = host(net.theta).astype(np.float64)
+        m0 = (r.standard_normal(P) * 1e-3).astype(np.float32)
+        v0 = (r.random(P) * 1e-6).astype(np.float32)
+        net.adam_m.copy_(torch.from_numpy(m0))
+        net.adam_v.copy_(torch.from_numpy(v0))
+        ref[net.n_out] = [th, m0.astype(np.float64), v0.astype(np.float64)]
+    stats = torch.zeros(8, device="cuda")
+    scales = {}
+    for t, scale in ((1, 0.37), (2, 1.0)):
+        stats[7] = scale
+        L.stats.copy_(stats)
+        for net in (L.pol, L.val):
+            g = (r.standard_normal(net.theta.numel()) * 10.0 ** r.uniform(-5, -1, net.theta.numel())).astype(np.float32)
+            net.grad.copy_(torch.from_numpy(g))
+            th, m, v = ref[net.n_out]
+            gs = np.float32(scale) * g.astype(np.float64)
+            # sums of the magnitudes of every term a moment has accumulated (the fp32 rounding
+            # of each step is relative to its terms and carries into the next step)
+            sm0, sv0 = scales.get(net.n_out, (np.abs(m), v))
+            scales[net.n_out] = (hp["beta1"] * sm0 + (1 - hp["beta1"]) * np.abs(gs),
+                                 hp["beta2"] * sv0 + (1 - hp["beta2"]) * gs * gs)
+            ref[net.n_out] = list(oppo.adam_step(th, g.astype(np.float64), m, v, t, hp, scale=np.float32(scale)))
+        L.t = t - 1
+        L.step()
+        for net in (L.pol, L.val):
+            th, m, v = ref[net.n_out]
+            gt, gm, gv = host(net.theta), host(net.adam_m), host(net.adam_v)
+            sm, sv = scales[net.n_out]
+            rm = np.abs(gm - m) / sm
+            rv = np.abs(gv - v) / (sv + 1e-30)
+            rt = np.abs(gt - th) / (2e-7 * np.abs(th) + 1e-3 * hp["lr"])
+            k = int(np.argmax(rm))
+            print(f"    t={t} n_out={net.n_out}: m {rm.max():.3g} (at {k}: got {gm[k]!r} want {m[k]!r} scale {sm[k]!r}), "
+                  f"v {rv.max():.3g}, theta {rt.max():.3g}")
+            assert rm.max() <= 4e-7 and rv.max() <= 4e-7 and rt.max() <= 1.0
+            bits = host(net.w_bf16).view(np.uint16)
+            want_bits = bf16_round(gt[:net.nw].astype(np.float64)).astype(np.float32).view(np.uint32) >> 16
+            assert np.array_equal(bits, want_bits.astype(np.uint16))
+
+
+def test_ppo_invalid_arguments(setup):
+    netp, netv, pol, val, buf, dev, M, PpoLearner = setup
+    from paper_2512_13359_amd import AuvError, _abi as A
+    L = PpoLearner(netp, netv)
+    batch = L.batch(dev["obs"], dev["act"], dev["logp"], dev["adv"], dev["ret"])
+    idx = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(AuvError):
+        A.auv_ppo_grad(L.cfg, L.pol.mlp, L.val.mlp, batch, idx, 0, L.pol.grad, L.val.grad, L.stats, L.work(16))
+    with pytest.raises(AuvError):   # networks swapped: wrong n_out
+        A.auv_ppo_grad(L.cfg, L.val.mlp, L.pol.mlp, batch, idx, 16, L.pol.grad, L.val.grad, L.stats, L.work(16))
+    with pytest.raises(AuvError):
+        A.auv_ppo_adam(L.cfg, 0, L.pol.net, L.val.net, L.pol.grad, L.val.grad, L.stats)
+    assert A.auv_ppo_work_bytes(0) == -1
+
+
+def test_ppo_full_minibatch_size(setup):
+    """The benchmark's minibatch (262144 samples, the launch configuration it times) from a
+    larger buffer: every gradient tensor and loss statistic against the oracle."""
+    netp, netv, pol, val, _, _, _, PpoLearner = setup
+    B = W.PPO["B"]
+    M = B + 16 * 256
+    announce(f"ppo full minibatch B={B} M={M}")
+    buf = _buffer(M, 12, pol)
+    dev = {k: torch.from_numpy(np.ascontiguousarray(v)).cuda() for k, v in buf.items()}
+    L = PpoLearner(netp, netv)
+    idx = W.ppo_minibatch_idx(M, B, seed=7)
+    L.grad(L.batch(dev["obs"], dev["act"], dev["logp"], dev["adv"], dev["ret"]), torch.from_numpy(idx).cuda())
+    st = host(L.stats)
+    cols = idx.astype(np.int64)
+    want = oppo.ppo_loss_grad(buf["obs"][:, cols], buf["act"][:, cols], buf["logp"][cols], buf["adv"][cols],
+                              buf["ret"][cols], pol, val, quantize=True)
+    _check_grads(host(L.pol.grad), want["grad_pol"], 8, "policy")
+    _check_grads(host(L.val.grad), want["grad_val"], 1, "value")
+    assert abs(st[0] - want["pg_loss"]) <= 2e-3 * max(1.0, abs(want["pg_loss"]))
+    assert st[4] == pytest.approx(want["clip_frac"], abs=0.5 / B)

@@ -23,6 +23,7 @@ __all__ = [
     "FLAG_DR", "FLAG_CURRENT", "FLAG_LISSAJOUS", "FLAG_STAGGER", "FLAG_TRAJ_STATE",
     "MODE_EXTERNAL", "MODE_RANDOM", "MODE_POLICY_MEAN", "MODE_POLICY_SAMPLE",
     "CONFIGS", "config", "mlp_weights", "vehicle_variant", "random_states",
+    "PPO", "ppo_draws", "ppo_minibatch_idx",
 ]
 
 # --- vehicle (fp32 values; every consumer promotes them exactly) -------------------
@@ -154,3 +155,38 @@ def random_states(n: int, seed: int, pos_scale=2.0, vel_scale=1.0, rate_scale=1.
     v = rng.uniform(-vel_scale, vel_scale, (3, n))
     w = rng.uniform(-rate_scale, rate_scale, (3, n))
     return np.concatenate([p, q, v, w]).astype(np.float32)
+
+
+# --- PPO update workload -----------------------------------------------------------
+# One update epoch over a c5-sized rollout buffer (65536 envs x 64 steps = 4194304 samples)
+# in 16 minibatches of 262144; hyperparameters of common PPO practice (the paper gives none).
+PPO = dict(M=65536 * 64, B=262144, epochs=4, clip_eps=0.2, vf_coef=0.5, ent_coef=0.0,
+           max_grad_norm=0.5, lr=3e-4, beta1=0.9, beta2=0.999, adam_eps=1e-8, normalize_adv=True)
+
+
+def ppo_draws(M: int, seed: int) -> dict:
+    """Seeded raw draws for a synthetic rollout buffer of M samples: observations with the
+    ranges of the environment's rows (body-frame position error, rotation columns,
+    velocities, previous action), standard-normal action noise, advantages, returns, and
+    target probability ratios in [0.6, 1.4] kept 0.03 away from 0.8 and 1.2 (so that a
+    clipping decision never sits at a boundary).  The caller forms actions and old
+    log-probabilities from these with its own policy evaluation."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    lo = np.array([-3.0] * 3 + [-1.0] * 6 + [-1.0] * 3 + [-1.5] * 3 + [-1.0] * 8)
+    obs = rng.uniform(lo[:, None], -lo[:, None], (23, M)).astype(np.float32)
+    eps = rng.standard_normal((8, M))
+    adv = (2.0 * rng.standard_normal(M) + 0.3).astype(np.float32)
+    ret = rng.standard_normal(M).astype(np.float32)
+    ratio = rng.uniform(0.6, 1.4, M)
+    near = (np.abs(ratio - 0.8) < 0.03) | (np.abs(ratio - 1.2) < 0.03)
+    ratio[near] = 1.0 + 0.5 * (ratio[near] - 1.0)
+    return dict(obs=obs, eps=eps, adv=adv, ret=ret, ratio=ratio)
+
+
+def ppo_minibatch_idx(M: int, B: int, seed: int) -> np.ndarray:
+    """B sample indices: a seeded permutation of the buffer's 16-sample blocks (16
+    consecutive envs of one step), cut to B entries (int32)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    blocks = rng.permutation(M // 16)
+    idx = (blocks[:, None] * 16 + np.arange(16)[None, :]).ravel()
+    return idx[:B].astype(np.int32)
