@@ -148,6 +148,55 @@ def c5_measure(reps: int = 3) -> dict:
             "gae_hbm_frac_cold": gae_bytes / res["cold"] / 8e12}
 
 
+# algorithmic MFMA work of one PPO sample: forward and backward (dW and dX products, no
+# input gradient) of the 23-256-256-8 policy and the 23-256-256-1 value net
+PPO_FLOP_PER_SAMPLE = (2 * (23 * 256 + 256 * 256 + 256 * 8) + 2 * 2 * 8 * 256 + 2 * 2 * 256 * 256 + 2 * 256 * 23
+                       + 2 * (23 * 256 + 256 * 256 + 256) + 2 * 2 * 256 + 2 * 2 * 256 * 256 + 2 * 256 * 23)
+
+
+def ppo_measure(reps: int = 5) -> dict:
+    """PPO update (gradient of both networks + Adam) on minibatches of 262144 samples drawn
+    in 16-sample blocks from a c5-sized buffer (65536 envs x 64 steps) of synthetic data."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import PpoLearner
+
+    P = W.PPO
+    M, B = P["M"], P["B"]
+    g = torch.Generator(device="cuda").manual_seed(21)
+    obs = torch.rand(23, M, device="cuda", generator=g) * 2 - 1
+    act = torch.randn(8, M, device="cuda", generator=g) * 0.6
+    logp = torch.randn(M, device="cuda", generator=g) * 0.1 - 6.0
+    adv = torch.randn(M, device="cuda", generator=g)
+    ret = torch.randn(M, device="cuda", generator=g)
+    hp = {k: P[k] for k in ("clip_eps", "vf_coef", "ent_coef", "max_grad_norm", "lr", "beta1", "beta2", "adam_eps",
+                            "normalize_adv")}
+    L = PpoLearner(W.mlp_weights(8, W.POLICY_SEED), W.mlp_weights(1, W.VALUE_SEED), **hp)
+    batch = L.batch(obs, act, logp, adv, ret)
+    idx = [torch.from_numpy(W.ppo_minibatch_idx(M, B, seed=100 + k)).cuda() for k in range(reps + 1)]
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    times = []
+    for k in range(reps + 1):
+        torch.cuda.synchronize()
+        e0, e1 = ev(), ev()
+        e0.record()
+        L.update(batch, idx[k])
+        e1.record()
+        torch.cuda.synchronize()
+        if k:
+            times.append(e0.elapsed_time(e1) * 1e-3)
+    t = sorted(times)[len(times) // 2]
+    st = L.stats.cpu().numpy()
+    assert (st == st).all(), "non-finite PPO statistics"
+    ach = PPO_FLOP_PER_SAMPLE * B / t
+    return {"workload": f"PPO update: minibatch {B} of a {M}-sample buffer (16-sample blocks), clipped surrogate "
+                        f"+ value loss, both 23-256-256 MLPs forward + backward on bf16 MFMA, global-norm clip, Adam",
+            "minibatch": B, "update_ms": t * 1e3, "samples_per_s": B / t,
+            "mfma_flop_per_sample": PPO_FLOP_PER_SAMPLE, "achieved_TFLOPs": ach / 1e12,
+            "frac_of_bf16_peak": ach / P_MFMA}
+
+
 def small_configs_measure(reps: int = 3) -> dict:
     """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
     4096 envs occupy 64 of the 256 CUs, so these are occupancy-capped by N."""
@@ -187,6 +236,8 @@ def main() -> int:
     ap.add_argument("--workload", default="c4", choices=["c3", "c4"])
     ap.add_argument("--cpu-steps", type=int, default=50, help="oracle control steps for the CPU baseline (0: skip)")
     ap.add_argument("--no-c5", action="store_true", help="skip the PPO-buffer (c5) rollout and GAE measurement")
+    ap.add_argument("--no-ppo", action="store_true", help="skip the PPO-update measurement")
+    ap.add_argument("--ppo-only", action="store_true", help="only measure the PPO update and print it")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -210,6 +261,9 @@ def main() -> int:
     from paper_2512_13359_amd import AuvEnv, upload_mlp
 
     torch.cuda.set_device(0)
+    if args.ppo_only:
+        print(json.dumps({"ppo": ppo_measure()}), flush=True)
+        return 0
     cfg = W.config(args.workload)
     n, T = cfg["n_envs"], cfg["T"]
     env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
@@ -280,6 +334,8 @@ def main() -> int:
     if not args.no_c5:
         line["c5"] = c5_measure()
         line.update(small_configs_measure())
+    if not args.no_ppo and not args.no_c5:
+        line["ppo"] = ppo_measure()
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
     print(json.dumps(line), flush=True)

@@ -4,7 +4,8 @@
 // gradient clipping and Adam (Kingma and Ba, Algorithm 1).
 //
 // Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 32):
-//   k_adv_stats     mean and 1 / (std + 1e-8) of the minibatch's advantages (one block)
+//   k_adv_partial   per-block sums of the minibatch's advantages and their squares (fp64)
+//   k_adv_final     mean and 1 / (std + 1e-8) from those sums
 //   k_fwd_bwd<n>    per 16-sample tile: forward, loss, dL/dy, dz2 = (W3^T q(dL/dy)) (1 - h2^2);
 //                   writes q(dz2) and q(h1) for the next two kernels; accumulates dW3, db2,
 //                   db3, d log_std and the loss sums per workgroup
@@ -61,6 +62,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));   // four bf16: a ha
 // Workspace of one call (offsets in bytes from the caller's buffer; every part 256-aligned).
 struct Work {
   float* advstat;       // [2] mean, 1 / (std + 1e-8)
+  double* adv_part;     // [ADV_BLOCKS][2] sums of A and A^2
   bf16x8* dz2_frag;     // [Bp/16][8 K tiles][64 lanes] q(dz2) as layer-2 B fragments
   u32x2* dz2_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz2) half fragments
   u32x2* h1_half;       // [Bp/16][16 feature tiles][64 lanes] q(h1) half fragments
@@ -76,23 +78,25 @@ struct Work {
 };
 
 constexpr int MAX_GROUPS = 256;
-constexpr int RED_THREADS = 256;
+constexpr int RED_ELEMS = 64;       // gradient entries per reduce block (one per lane; 4 waves split the partials)
+constexpr int ADV_BLOCKS = 256;
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline int padded(int B) { return (B + 31) / 32 * 32; }
 inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * HID + n_out + (n_out == 8 ? 8 : 0); }
-inline int red_blocks(int n_out) { return (nparam(n_out) + RED_THREADS - 1) / RED_THREADS; }
+inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_ELEMS; }
 
 // Byte offsets of the workspace parts for a minibatch of B; returns the total.
-inline size_t work_layout(int B, size_t off[13]) {
+constexpr int WORK_PARTS = 14;
+inline size_t work_layout(int B, size_t off[WORK_PARTS]) {
   const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
-  const size_t sizes[13] = {2 * sizeof(float),
+  const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS,
                             Bp * HID * 2, Bp * HID * 2, Bp * HID * 2,
                             G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
                             G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
                             2 * (size_t)red_blocks(8) * 4};
   size_t o = 0;
-  for (int k = 0; k < 13; ++k) {
+  for (int k = 0; k < WORK_PARTS; ++k) {
     off[k] = o;
     o += align256(sizes[k]);
   }
@@ -100,23 +104,24 @@ inline size_t work_layout(int B, size_t off[13]) {
 }
 
 inline Work work_at(void* base, int B) {
-  size_t off[13];
+  size_t off[WORK_PARTS];
   work_layout(B, off);
   char* p = (char*)base;
   Work W;
   W.advstat = (float*)(p + off[0]);
-  W.dz2_frag = (bf16x8*)(p + off[1]);
-  W.dz2_half = (u32x2*)(p + off[2]);
-  W.h1_half = (u32x2*)(p + off[3]);
-  W.part_w3t = (float*)(p + off[4]);
-  W.part_b2 = (float*)(p + off[5]);
-  W.part_b3 = (float*)(p + off[6]);
-  W.part_ls = (float*)(p + off[7]);
-  W.part_stats = (float*)(p + off[8]);
-  W.part_w1 = (float*)(p + off[9]);
-  W.part_b1 = (float*)(p + off[10]);
-  W.part_w2 = (float*)(p + off[11]);
-  W.part_ss = (float*)(p + off[12]);
+  W.adv_part = (double*)(p + off[1]);
+  W.dz2_frag = (bf16x8*)(p + off[2]);
+  W.dz2_half = (u32x2*)(p + off[3]);
+  W.h1_half = (u32x2*)(p + off[4]);
+  W.part_w3t = (float*)(p + off[5]);
+  W.part_b2 = (float*)(p + off[6]);
+  W.part_b3 = (float*)(p + off[7]);
+  W.part_ls = (float*)(p + off[8]);
+  W.part_stats = (float*)(p + off[9]);
+  W.part_w1 = (float*)(p + off[10]);
+  W.part_b1 = (float*)(p + off[11]);
+  W.part_w2 = (float*)(p + off[12]);
+  W.part_ss = (float*)(p + off[13]);
   return W;
 }
 
@@ -164,43 +169,87 @@ __device__ __forceinline__ int sample_of(const int32_t* __restrict__ idx, int b,
   return min(max(idx[b], 0), M - 1);
 }
 
-// Layer-1 operand of a tile: lane (g, r) holds input features kslot(g, j) of sample s
-// (zero beyond the 23 inputs and for padding samples).
-__device__ __forceinline__ bf16x8 input_frag(const Batch& D, bool valid, int s, int g) {
+// What lane (g, r) reads of tile sample r: observation rows kslot(g, j), action rows
+// 4g .. 4g+3 (policy lanes g < 2), log-prob, advantage and return.  Every load is issued
+// unconditionally from a valid address (rows and entries clamped), so a tile's loads can be
+// in flight while the previous tile is computed; what lies outside is masked on use.
+struct TileIn {
+  float x[8], a[4], lp, ad, rt;
+};
+
+// Raw index of entry r of tile t (entries past B read entry B - 1).  Loaded a tile ahead of
+// its use, unconditionally, and clamped into [0, M) only where it is used.
+__device__ __forceinline__ int raw_index(const int32_t* __restrict__ idx, int t, int r, int B) {
+  return idx[min(t * 16 + r, B - 1)];
+}
+
+__device__ __forceinline__ int clamp_sample(int raw, int M) { return min(max(raw, 0), M - 1); }
+
+template <bool POLICY, bool VALUE>
+__device__ __forceinline__ void tile_in_load(const Batch& D, int s, int g, TileIn& in) {
+  const size_t M = D.M, ss = (size_t)s;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(g, j), 22) * M + ss];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) in.a[i] = POLICY ? D.act[(size_t)((4 * g + i) & 7) * M + ss] : 0.0f;
+  in.lp = POLICY ? D.logp[ss] : 0.0f;
+  in.ad = POLICY ? D.adv[ss] : 0.0f;
+  in.rt = VALUE ? D.ret[ss] : 0.0f;
+}
+
+// Layer-1 operand: input features kslot(g, j), zero beyond the 23 inputs and for padding
+// samples.
+__device__ __forceinline__ bf16x8 input_frag(const TileIn& in, bool valid, int g) {
   bf16x8 x;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int k = kslot(g, j);
-    x[j] = (__bf16)((valid && k < 23) ? D.obs[(size_t)k * D.M + (size_t)s] : 0.0f);
-  }
+  for (int j = 0; j < 8; ++j) x[j] = (__bf16)((valid && kslot(g, j) < 23) ? in.x[j] : 0.0f);
   return x;
 }
 
 // ------------------------------------------------------------------ kernels ----------
-__global__ __launch_bounds__(1024) void k_adv_stats(const float* __restrict__ adv, const int32_t* __restrict__ idx,
-                                                    int B, int M, float* __restrict__ out) {
-  __shared__ double red[16];
+// Advantage sums over the minibatch: block k sums entries k*256 + tid (stride 256 blocks x
+// 256 threads) in fp64, in a fixed order.
+__global__ __launch_bounds__(256) void k_adv_partial(const float* __restrict__ adv, const int32_t* __restrict__ idx,
+                                                     int B, int M, double* __restrict__ part) {
+  __shared__ double red[4][2];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  auto block_sum = [&](double v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-    __syncthreads();
-    if (lane == 0) red[w] = v;
-    __syncthreads();
-    double s = 0.0;
-    for (int k = 0; k < 16; ++k) s += red[k];
-    return s;
-  };
-  double s = 0.0;
-  for (int b = tid; b < B; b += 1024) s += (double)adv[sample_of(idx, b, M)];
-  const double mean = block_sum(s) / B;
-  double q = 0.0;
-  for (int b = tid; b < B; b += 1024) {
-    const double d = (double)adv[sample_of(idx, b, M)] - mean;
-    q += d * d;
+  double s1 = 0.0, s2 = 0.0;
+  for (int b = blockIdx.x * 256 + tid; b < B; b += ADV_BLOCKS * 256) {
+    const double x = (double)adv[sample_of(idx, b, M)];
+    s1 += x;
+    s2 += x * x;
   }
-  const double var = block_sum(q) / B;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    s1 += __shfl_xor(s1, o);
+    s2 += __shfl_xor(s2, o);
+  }
+  if (lane == 0) {
+    red[w][0] = s1;
+    red[w][1] = s2;
+  }
+  __syncthreads();
   if (tid == 0) {
+    part[2 * blockIdx.x] = red[0][0] + red[1][0] + red[2][0] + red[3][0];
+    part[2 * blockIdx.x + 1] = red[0][1] + red[1][1] + red[2][1] + red[3][1];
+  }
+}
+
+// mean = S1 / B, population variance = S2 / B - mean^2, inv_std = 1 / (sqrt(var) + 1e-8).
+__global__ __launch_bounds__(64) void k_adv_final(const double* __restrict__ part, int B, float* __restrict__ out) {
+  const int lane = threadIdx.x;
+  double s1 = 0.0, s2 = 0.0;
+  for (int k = lane; k < ADV_BLOCKS; k += 64) {
+    s1 += part[2 * k];
+    s2 += part[2 * k + 1];
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    s1 += __shfl_xor(s1, o);
+    s2 += __shfl_xor(s2, o);
+  }
+  if (lane == 0) {
+    const double mean = s1 / B, var = fmax(s2 / B - mean * mean, 0.0);
     out[0] = (float)mean;
     out[1] = (float)(1.0 / (sqrt(var) + 1e-8));
   }
@@ -262,14 +311,26 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
   float db3[4] = {0, 0, 0, 0}, dls[4] = {0, 0, 0, 0}, st[STATS] = {0, 0, 0, 0};
   __bf16* T = S.T[m];
   __bf16* Gy = S.Gy[m];
+  const int Mi = (int)D.M;
+  // inputs of this workgroup's first tile, and the raw indices of its second.  Every
+  // prefetch below is unconditional (tile and entry indices clamped): a load under a branch
+  // whose result is used at the join would make the wave wait for all loads in flight.
+  TileIn cur;
+  tile_in_load<NOUT == 8, NOUT == 1>(D, clamp_sample(raw_index(idx, blockIdx.x, r, B), Mi), g, cur);
+  int raw_nxt = raw_index(idx, blockIdx.x + gridDim.x, r, B);
   __syncthreads();
 
-  for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
-    const int b_r = t * 16 + r;
-    const bool valid = b_r < B;
-    const int s = valid ? sample_of(idx, b_r, (int)D.M) : 0;
+  // The tile body is peeled for the workgroup's first tile so that every path into the
+  // loop arrives with the same memory operations in flight (loads of the next tile, then
+  // this tile's stores): the waits inside then cover only the loads they need.
+  auto tile = [&](int t) __attribute__((always_inline)) {
+    const bool valid = t * 16 + r < B;
+    // next tile's inputs (its indices were loaded one tile ago) and the indices after it
+    TileIn nxt;
+    tile_in_load<NOUT == 8, NOUT == 1>(D, clamp_sample(raw_nxt, Mi), g, nxt);
+    const int raw_nxt2 = raw_index(idx, t + 2 * gridDim.x, r, B);
     // ---- forward
-    const bf16x8 x = input_frag(D, valid, s, g);
+    const bf16x8 x = input_frag(cur, valid, g);
     bf16x8 own[2];
     tile_layer1<64>(R, x, S.b1k, m, lane, own);
     S.h[2 * m][lane] = own[0];
@@ -315,15 +376,15 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
       float a[4], d[4], zz[4], part = 0.0f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        a[i] = (valid && g < 2) ? D.act[(size_t)(4 * g + i) * D.M + (size_t)s] : 0.0f;
+        a[i] = (valid && g < 2) ? cur.a[i] : 0.0f;
         d[i] = g < 2 ? a[i] - y[i] : 0.0f;
         zz[i] = d[i] * d[i] * ivar[i];
         part += -0.5f * zz[i] - ls[i];
       }
       const float logp = part + __shfl_xor(part, 16) - 4.0f * LOG_2PI;   // lanes r and r + 16
       const bool lv = valid && g < 2;
-      const float lpo = lv ? D.logp[s] : 0.0f;
-      const float ah = lv ? (hp.normalize ? (D.adv[s] - mean) * inv_std : D.adv[s]) : 0.0f;
+      const float lpo = lv ? cur.lp : 0.0f;
+      const float ah = lv ? (hp.normalize ? (cur.ad - mean) * inv_std : cur.ad) : 0.0f;
       const float rho = expf(logp - lpo);
       const float unc = rho * ah;
       const float clp = fminf(fmaxf(rho, 1.0f - hp.clip_eps), 1.0f + hp.clip_eps) * ah;
@@ -345,7 +406,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
       }
     } else {
       if (valid && g == 0) {
-        const float e = y[0] - D.ret[s];
+        const float e = y[0] - cur.rt;
         gy[0] = hp.vf_coef * hp.inv_B * e;
         if (m == 0) {
           db3[0] += gy[0];
@@ -388,6 +449,12 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
     put_d(T, g, r, dz);
 #pragma unroll
     for (int ft = 0; ft < 4; ++ft) W.dz2_half[((size_t)t * 16 + 4 * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
+    cur = nxt;
+    raw_nxt = raw_nxt2;
+  };
+  if ((int)blockIdx.x < tiles) {
+    tile(blockIdx.x);
+    for (int t = blockIdx.x + gridDim.x; t < tiles; t += gridDim.x) tile(t);
   }
 
   // ---- per-workgroup partials
@@ -457,15 +524,31 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
   f32x4 b1[4];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) b1[mt] = *reinterpret_cast<const f32x4*>(&b1k[64 * m + 16 * mt + 4 * g]);
-
-  for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
-    const int b_r = t * 16 + r;
-    const bool valid = b_r < B;
-    const int s = valid ? sample_of(idx, b_r, (int)D.M) : 0;
-    bf16x8 zf[8];
+  // inputs and q(dz2) fragments of the first tile, raw indices of the second (prefetches
+  // unconditional, as in k_fwd_bwd)
+  const int Mi = (int)D.M;
+  TileIn cur;
+  bf16x8 zf[8];
+  auto load_dz2 = [&](int t, bf16x8* z) {
+    const size_t tc = (size_t)min(t, tiles - 1);
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt) zf[kt] = W.dz2_frag[((size_t)t * 8 + kt) * 64 + lane];
-    const bf16x8 x = input_frag(D, valid, s, g);
+    for (int kt = 0; kt < 8; ++kt) z[kt] = W.dz2_frag[(tc * 8 + kt) * 64 + lane];
+  };
+  tile_in_load<false, false>(D, clamp_sample(raw_index(idx, blockIdx.x, r, B), Mi), g, cur);
+  load_dz2(blockIdx.x, zf);
+  int raw_nxt = raw_index(idx, blockIdx.x + gridDim.x, r, B);
+
+  // The tile body is peeled for the workgroup's first tile so that every path into the
+  // loop arrives with the same memory operations in flight (loads of the next tile, then
+  // this tile's stores): the waits inside then cover only the loads they need.
+  auto tile = [&](int t) __attribute__((always_inline)) {
+    const bool valid = t * 16 + r < B;
+    TileIn nxt;
+    bf16x8 zn[8];
+    tile_in_load<false, false>(D, clamp_sample(raw_nxt, Mi), g, nxt);
+    load_dz2(t + gridDim.x, zn);
+    const int raw_nxt2 = raw_index(idx, t + 2 * gridDim.x, r, B);
+    const bf16x8 x = input_frag(cur, valid, g);
     f32x4 acc[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) acc[mt] = f32x4{0, 0, 0, 0};
@@ -497,6 +580,14 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) dw1[mt][nt] = mfma(a, bx[nt], dw1[mt][nt]);
     }
+    cur = nxt;
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt) zf[kt] = zn[kt];
+    raw_nxt = raw_nxt2;
+  };
+  if ((int)blockIdx.x < tiles) {
+    tile(blockIdx.x);
+    for (int t = blockIdx.x + gridDim.x; t < tiles; t += gridDim.x) tile(t);
   }
 
   const int wg = blockIdx.x;
@@ -513,10 +604,13 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
 }
 
 // dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup: wave m owns rows
-// 64 m .. 64 m + 63 (4 M-tiles) and all 256 columns (16 N-tiles).  The next step's
-// fragments are loaded before the current step's 64 products.
+// 64 m .. 64 m + 63 (4 M-tiles, its A fragments loaded directly) and all 256 columns (16
+// N-tiles).  The 16 B fragments of a step are shared: wave m loads N-tiles 4m .. 4m+3 and
+// stores them in LDS (two buffers, one barrier per step), every wave reads all 16.  The
+// next step's loads are issued before the current step's 64 products.
 __global__ __launch_bounds__(THREADS, 1) void k_dw2(const u32x2* __restrict__ dz2_half, const u32x2* __restrict__ h1_half,
                                                     int steps, float* __restrict__ part_w2) {
+  __shared__ bf16x8 Bs[2][16][64];
   const int tid = threadIdx.x, lane = tid & 63;
   const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
@@ -527,27 +621,33 @@ __global__ __launch_bounds__(THREADS, 1) void k_dw2(const u32x2* __restrict__ dz
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
     for (int nt = 0; nt < 16; ++nt) acc[mt][nt] = f32x4{0, 0, 0, 0};
-  auto at = [&](int tile, int ft) { return ((size_t)tile * 16 + ft) * 64 + lane; };
-  bf16x8 A[4], Bf[16];
-  auto load = [&](int u, bf16x8* a, bf16x8* bb) {
+  if (u0 < u1) {
+    auto at = [&](int tile, int ft) { return ((size_t)tile * 16 + ft) * 64 + lane; };
+    auto load = [&](int u, bf16x8* a, bf16x8* bo) {
+      u = min(u, u1 - 1);   // unconditional (the last step is read again)
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) a[mt] = join(dz2_half[at(2 * u, 4 * m + mt)], dz2_half[at(2 * u + 1, 4 * m + mt)]);
+      for (int mt = 0; mt < 4; ++mt) a[mt] = join(dz2_half[at(2 * u, 4 * m + mt)], dz2_half[at(2 * u + 1, 4 * m + mt)]);
 #pragma unroll
-    for (int nt = 0; nt < 16; ++nt) bb[nt] = join(h1_half[at(2 * u, nt)], h1_half[at(2 * u + 1, nt)]);
-  };
-  if (u0 < u1) load(u0, A, Bf);
-  for (int u = u0; u < u1; ++u) {
-    bf16x8 An[4], Bn[16];
-    if (u + 1 < u1) load(u + 1, An, Bn);
+      for (int q = 0; q < 4; ++q) bo[q] = join(h1_half[at(2 * u, 4 * m + q)], h1_half[at(2 * u + 1, 4 * m + q)]);
+    };
+    bf16x8 A[4], Bo[4];
+    load(u0, A, Bo);
+    int buf = 0;
+    for (int u = u0; u < u1; ++u) {
 #pragma unroll
-    for (int nt = 0; nt < 16; ++nt)
+      for (int q = 0; q < 4; ++q) Bs[buf][4 * m + q][lane] = Bo[q];
+      __syncthreads();   // this step's B fragments visible; readers of this buffer two steps ago are done
+      bf16x8 An[4];
+      load(u + 1, An, Bo);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[mt], Bf[nt], acc[mt][nt]);
-    if (u + 1 < u1) {
+      for (int nt = 0; nt < 16; ++nt) {
+        const bf16x8 bf = Bs[buf][nt][lane];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[mt], bf, acc[mt][nt]);
+      }
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) A[mt] = An[mt];
-#pragma unroll
-      for (int nt = 0; nt < 16; ++nt) Bf[nt] = Bn[nt];
+      buf ^= 1;
     }
   }
   float* out = part_w2 + (size_t)blockIdx.x * HID * HID;
@@ -559,46 +659,60 @@ __global__ __launch_bounds__(THREADS, 1) void k_dw2(const u32x2* __restrict__ dz
       for (int nt = 0; nt < 16; ++nt) out[(64 * m + 16 * mt + 4 * g + i) * HID + 16 * nt + r] = acc[mt][nt][i];
 }
 
-// Packed gradient of one network = fixed-order sums of the partials; per-block sums of
-// squares for the global norm.  G1: forward/backward groups (dW3, db2, db3, d log_std),
-// G2: dz1 groups (dW1, db1), G3: dW2 groups.
-__global__ __launch_bounds__(RED_THREADS) void k_reduce(int n_out, int G1, int G2, int G3, Work W, float ent_coef,
-                                                        float* __restrict__ grad, float* __restrict__ ss) {
-  __shared__ float red[RED_THREADS / 64];
-  const int e = blockIdx.x * RED_THREADS + threadIdx.x;
+// Packed gradient of one network = fixed-order sums of the partials, and per-block sums of
+// squares for the global norm.  A block owns 64 gradient entries (one per lane); its four
+// waves each sum a contiguous quarter of the workgroup partials with eight loads in flight,
+// then wave 0 adds the quarters in wave order.  G1: forward/backward groups (dW3, db2, db3,
+// d log_std), G2: dz1 groups (dW1, db1), G3: dW2 groups.
+__global__ __launch_bounds__(256) void k_reduce(int n_out, int G1, int G2, int G3, Work W, float ent_coef,
+                                                float* __restrict__ grad, float* __restrict__ ss) {
+  __shared__ float part[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int e = blockIdx.x * RED_ELEMS + lane;
   const int nW1 = HID * 23, nW2 = HID * HID, nW3 = n_out * HID;
   const int P = nW1 + nW2 + nW3 + 2 * HID + n_out + (n_out == 8 ? 8 : 0);
-  float v = 0.0f;
+  const float* src = W.part_b2;
+  size_t stride = 0;
+  int G = 0;
+  float add = 0.0f;
   if (e < P) {
     int q = e;
     if (q < nW1) {
       const int k = q / 23, i = q - 23 * k;
-      for (int wg = 0; wg < G2; ++wg) v += W.part_w1[((size_t)wg * HID + k) * 32 + i];
+      src = W.part_w1 + k * 32 + i, stride = (size_t)HID * 32, G = G2;
     } else if ((q -= nW1) < nW2) {
-      for (int wg = 0; wg < G3; ++wg) v += W.part_w2[(size_t)wg * HID * HID + q];
+      src = W.part_w2 + q, stride = (size_t)HID * HID, G = G3;
     } else if ((q -= nW2) < nW3) {
       const int j = q / HID, f = q - HID * j;
-      for (int wg = 0; wg < G1; ++wg) v += W.part_w3t[((size_t)wg * HID + f) * 16 + j];
+      src = W.part_w3t + f * 16 + j, stride = (size_t)HID * 16, G = G1;
     } else if ((q -= nW3) < HID) {
-      for (int wg = 0; wg < G2; ++wg) v += W.part_b1[(size_t)wg * HID + q];
+      src = W.part_b1 + q, stride = HID, G = G2;
     } else if ((q -= HID) < HID) {
-      for (int wg = 0; wg < G1; ++wg) v += W.part_b2[(size_t)wg * HID + q];
+      src = W.part_b2 + q, stride = HID, G = G1;
     } else if ((q -= HID) < n_out) {
-      for (int wg = 0; wg < G1; ++wg) v += W.part_b3[wg * 16 + q];
+      src = W.part_b3 + q, stride = 16, G = G1;
     } else {
-      q -= n_out;
-      for (int wg = 0; wg < G1; ++wg) v += W.part_ls[wg * 16 + q];
-      v -= ent_coef;
+      src = W.part_ls + (q - n_out), stride = 16, G = G1, add = -ent_coef;
     }
-    grad[e] = v;
   }
-  const float s2 = wave_sum(v * v);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s2;
+  const int g0 = w * G / 4, g1 = (w + 1) * G / 4;
+  float acc = 0.0f;
+  int wg = g0;
+  for (; wg + 8 <= g1; wg += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[(size_t)(wg + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; wg < g1; ++wg) acc += src[(size_t)wg * stride];
+  part[w][lane] = acc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float t = 0.0f;
-    for (int k = 0; k < RED_THREADS / 64; ++k) t += red[k];
-    ss[blockIdx.x] = t;
+  if (w == 0) {
+    const float v = e < P ? part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane] + add : 0.0f;
+    if (e < P) grad[e] = v;
+    const float s2 = wave_sum(v * v);
+    if (lane == 0) ss[blockIdx.x] = s2;
   }
 }
 
@@ -684,7 +798,7 @@ extern "C" {
 
 int64_t auv_ppo_work_bytes(int32_t B) {
   if (B < 1 || B > PPO_MAX_B) return -1;
-  size_t off[13];
+  size_t off[ppo::WORK_PARTS];
   return (int64_t)ppo::work_layout(B, off);
 }
 
@@ -708,18 +822,22 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
   const ppo::Hp hp{cfg->clip_eps, cfg->vf_coef, cfg->ent_coef, cfg->max_grad_norm, 1.0f / (float)B, cfg->normalize_adv ? 1 : 0};
   const ppo::Batch D{batch->obs, batch->act, batch->logp, batch->adv, batch->ret, (size_t)batch->M};
   const int rb = ppo::red_blocks(ACT);
-  if (hp.normalize) hipLaunchKernelGGL(ppo::k_adv_stats, dim3(1), dim3(1024), 0, s, batch->adv, idx, B, (int)batch->M, W.advstat);
+  if (hp.normalize) {
+    hipLaunchKernelGGL(ppo::k_adv_partial, dim3(ppo::ADV_BLOCKS), dim3(256), 0, s, batch->adv, idx, B, (int)batch->M,
+                       W.adv_part);
+    hipLaunchKernelGGL(ppo::k_adv_final, dim3(1), dim3(64), 0, s, W.adv_part, B, W.advstat);
+  }
   hipLaunchKernelGGL(ppo::k_fwd_bwd<8>, dim3(G1), dim3(ppo::THREADS), 0, s, policy->w, policy->b, policy->log_std, D, idx,
                      B, tiles, hp, W, 0);
   hipLaunchKernelGGL(ppo::k_dz1, dim3(G1), dim3(ppo::THREADS), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(ppo::THREADS), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(ppo::RED_THREADS), 0, s, ACT, G1, G1, G3, W, cfg->ent_coef,
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, G1, G1, G3, W, cfg->ent_coef,
                      grad_policy, W.part_ss);
   hipLaunchKernelGGL(ppo::k_fwd_bwd<1>, dim3(G1), dim3(ppo::THREADS), 0, s, value->w, value->b, (const float*)nullptr, D,
                      idx, B, tiles, hp, W, 1);
   hipLaunchKernelGGL(ppo::k_dz1, dim3(G1), dim3(ppo::THREADS), 0, s, value->w, value->b, D, idx, B, tiles, W);
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(ppo::THREADS), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(ppo::RED_THREADS), 0, s, 1, G1, G1, G3, W, 0.0f,
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, G1, G1, G3, W, 0.0f,
                      grad_value, W.part_ss + rb);
   hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, G1, G1, W, rb, ppo::red_blocks(1), rb, policy->log_std, hp,
                      stats);
