@@ -36,8 +36,7 @@
 namespace auv {
 namespace ppo {
 
-constexpr int NW = 4;               // waves per workgroup, 64 hidden features each
-constexpr int THREADS = 64 * NW;
+constexpr int FPW = 32;             // hidden features per wave of the per-tile kernels (HID / FPW waves)
 constexpr int TPAD = 20;            // bf16 row stride of the transpose buffers (8-byte aligned rows)
 constexpr int STATS = 4;            // per-workgroup loss sums: surrogate, log-ratio, clipped count, squared error
 constexpr float LOG_2PI = 1.83787706640934548f;
@@ -82,7 +81,10 @@ constexpr int RED_ELEMS = 64;       // gradient entries per reduce block (one pe
 constexpr int ADV_BLOCKS = 256;
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-inline int padded(int B) { return (B + 31) / 32 * 32; }
+constexpr int DW2_WAVES = 8, DW2_DEPTH = 4;
+// Minibatch padded to whole rounds of the dW2 loop (DW2_DEPTH steps of 32 samples); padding
+// samples carry zero dz2 and so add nothing.
+inline int padded(int B) { return (B + 32 * DW2_DEPTH - 1) / (32 * DW2_DEPTH) * (32 * DW2_DEPTH); }
 inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * HID + n_out + (n_out == 8 ? 8 : 0); }
 inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_ELEMS; }
 
@@ -149,17 +151,19 @@ __device__ __forceinline__ bf16x8 low_half(u32x2 a) { return join(a, u32x2{0u, 0
 
 // D-fragment values v[mt][i] (feature 16 mt + 4 g + i, sample r), rounded to bf16, into
 // this wave's transpose buffer T[feature][sample].
-__device__ __forceinline__ void put_d(__bf16* T, int g, int r, const f32x4 v[4]) {
+template <int MT>
+__device__ __forceinline__ void put_d(__bf16* T, int g, int r, const f32x4 v[MT]) {
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) T[(16 * mt + 4 * g + i) * TPAD + r] = (__bf16)v[mt][i];
 }
 
-// The same for B fragments of two K tiles (feature 32 kt + kslot(g, j), sample r).
-__device__ __forceinline__ void put_b(__bf16* T, int g, int r, const bf16x8 f[2]) {
+// The same for B fragments of KO K tiles (feature 32 kt + kslot(g, j), sample r).
+template <int KO>
+__device__ __forceinline__ void put_b(__bf16* T, int g, int r, const bf16x8 f[KO]) {
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
+  for (int kt = 0; kt < KO; ++kt)
 #pragma unroll
     for (int j = 0; j < 8; ++j) T[(32 * kt + kslot(g, j)) * TPAD + r] = f[kt][j];
 }
@@ -255,39 +259,42 @@ __global__ __launch_bounds__(64) void k_adv_final(const double* __restrict__ par
   }
 }
 
-template <int NOUT>
+template <int FPW>
 struct FwdShared {
-  bf16x8 h[8][64];            // hidden-1 tiles of the current sample tile [K tile][lane]
-  f32x4 o[NW][64];            // output split-K partials [wave][lane]
+  static constexpr int NWV = HID / FPW;
+  bf16x8 h[8][64];             // hidden-1 tiles of the current sample tile [K tile][lane]
+  f32x4 o[NWV][64];            // output split-K partials [wave][lane]
   float b1k[HID];
   float b3[16];
-  __bf16 T[NW][64 * TPAD];    // per-wave transpose buffer [feature][sample]
-  __bf16 Gy[NW][8 * TPAD];    // per-wave q(dL/dy) transposed [output row][sample]
+  __bf16 T[NWV][FPW * TPAD];   // per-wave transpose buffer [feature][sample]
+  __bf16 Gy[NWV][8 * TPAD];    // per-wave q(dL/dy) transposed [output row][sample]
 };
 
-// Forward, loss and the output-side backward of one network over 16-sample tiles (wave m
-// owns hidden features 64 m .. 64 m + 63).  NOUT = 8: the policy and the clipped
-// surrogate; NOUT = 1: the value net and the squared error.
-template <int NOUT>
-__global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restrict__ w, const float* __restrict__ b,
+// Forward, loss and the output-side backward of one network over 16-sample tiles: HID / FPW
+// waves, wave m owning hidden features FPW m .. FPW m + FPW - 1 (MT = FPW / 16 M-tiles, KO =
+// FPW / 32 K tiles of the next layer).  NOUT = 8: the policy and the clipped surrogate;
+// NOUT = 1: the value net and the squared error.
+template <int NOUT, int FPW>
+__global__ __launch_bounds__(64 * HID / FPW, 1) void k_fwd_bwd(const uint16_t* __restrict__ w, const float* __restrict__ b,
                                                          const float* __restrict__ log_std, Batch D,
                                                          const int32_t* __restrict__ idx, int B, int tiles, Hp hp,
                                                          Work W, int net) {
-  __shared__ FwdShared<NOUT> S;
+  constexpr int NWV = HID / FPW, MT = FPW / 16, KO = FPW / 32;
+  __shared__ FwdShared<FPW> S;
   const int tid = threadIdx.x, lane = tid & 63;
   const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
-  TileMlpRegs<64> R;
-  tile_mlp_load<64>(w, b, NOUT, m, lane, R);
-  // W3^T fragments: A[f = 64 m + 16 mt + r][slot (g, j)] = W3[kslot(g, j)][f]
+  TileMlpRegs<FPW> R;
+  tile_mlp_load<FPW>(w, b, NOUT, m, lane, R);
+  // W3^T fragments: A[f = FPW m + 16 mt + r][slot (g, j)] = W3[kslot(g, j)][f]
   const uint16_t* W3 = w + HID * 23 + HID * HID;
-  bf16x8 w3t[4];
+  bf16x8 w3t[MT];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int k = kslot(g, j);
-      w3t[mt][j] = k < NOUT ? bf16_of_bits(W3[k * HID + 64 * m + 16 * mt + r]) : bf16_of_bits(0);
+      w3t[mt][j] = k < NOUT ? bf16_of_bits(W3[k * HID + FPW * m + 16 * mt + r]) : bf16_of_bits(0);
     }
   if (tid < HID) S.b1k[tid] = b[tid] * TWO_LOG2E;
   if (tid < 16) S.b3[tid] = tid < NOUT ? b[2 * HID + tid] : 0.0f;
@@ -305,9 +312,9 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
     mean = W.advstat[0];
     inv_std = W.advstat[1];
   }
-  f32x4 dw3[4], db2[4];
+  f32x4 dw3[MT], db2[MT];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) dw3[mt] = db2[mt] = f32x4{0, 0, 0, 0};
+  for (int mt = 0; mt < MT; ++mt) dw3[mt] = db2[mt] = f32x4{0, 0, 0, 0};
   float db3[4] = {0, 0, 0, 0}, dls[4] = {0, 0, 0, 0}, st[STATS] = {0, 0, 0, 0};
   __bf16* T = S.T[m];
   __bf16* Gy = S.Gy[m];
@@ -331,30 +338,30 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
     const int raw_nxt2 = raw_index(idx, t + 2 * gridDim.x, r, B);
     // ---- forward
     const bf16x8 x = input_frag(cur, valid, g);
-    bf16x8 own[2];
-    tile_layer1<64>(R, x, S.b1k, m, lane, own);
-    S.h[2 * m][lane] = own[0];
-    S.h[2 * m + 1][lane] = own[1];
-    put_b(T, g, r, own);                      // q(h1) -> half fragments for dW2
+    bf16x8 own[KO];
+    tile_layer1<FPW>(R, x, S.b1k, m, lane, own);
 #pragma unroll
-    for (int ft = 0; ft < 4; ++ft) W.h1_half[((size_t)t * 16 + 4 * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
+    for (int kt = 0; kt < KO; ++kt) S.h[KO * m + kt][lane] = own[kt];
+    put_b<KO>(T, g, r, own);                  // q(h1) -> half fragments for dW2
+#pragma unroll
+    for (int ft = 0; ft < MT; ++ft) W.h1_half[((size_t)t * 16 + MT * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
     __syncthreads();
-    f32x4 acc[4];
-    tile_layer2_own<64>(R, own, acc);
+    f32x4 acc[MT];
+    tile_layer2_own<FPW>(R, own, acc);
 #pragma unroll
-    for (int kk = 2; kk < 8; ++kk) {
-      const bf16x8 hb = S.h[(2 * m + kk) & 7][lane];
+    for (int kk = KO; kk < 8; ++kk) {
+      const bf16x8 hb = S.h[(KO * m + kk) & 7][lane];
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[mt] = mfma(R.w2[mt][kk], hb, acc[mt]);
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma(R.w2[mt][kk], hb, acc[mt]);
     }
-    f32x4 h2[4];
+    f32x4 h2[MT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) h2[mt][i] = tanh_bias(acc[mt][i], R.b2[mt][i]);
-    bf16x8 u2[2];
+    bf16x8 u2[KO];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KO; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         u2[kt][i] = (__bf16)h2[2 * kt][i];
@@ -362,13 +369,13 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
       }
     f32x4 o = f32x4{0, 0, 0, 0};
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) o = mfma(R.w3[kt], u2[kt], o);
+    for (int kt = 0; kt < KO; ++kt) o = mfma(R.w3[kt], u2[kt], o);
     S.o[m][lane] = o;
-    put_b(T, g, r, u2);                       // q(h2) -> half fragments for dW3
+    put_b<KO>(T, g, r, u2);                   // q(h2) -> half fragments for dW3
     __syncthreads();
     f32x4 y = *reinterpret_cast<const f32x4*>(&S.b3[4 * g]);
 #pragma unroll
-    for (int ww = 0; ww < NW; ++ww) y += S.o[ww][lane];
+    for (int ww = 0; ww < NWV; ++ww) y += S.o[ww][lane];
 
     // ---- loss: dL/dy for this lane's output rows 4g .. 4g+3 of sample r
     float gy[4] = {0, 0, 0, 0};
@@ -425,30 +432,30 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
     }
     const bf16x8 bgy = r < NOUT ? low_half(half_of(Gy, r, g)) : bf16x8{};
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) dw3[mt] = mfma(low_half(half_of(T, 16 * mt + r, g)), bgy, dw3[mt]);
+    for (int mt = 0; mt < MT; ++mt) dw3[mt] = mfma(low_half(half_of(T, 16 * mt + r, g)), bgy, dw3[mt]);
 
     // ---- dz2 = (W3^T q(gy)) (1 - h2^2), this wave's features
-    f32x4 dz[4];
+    f32x4 dz[MT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
       const f32x4 dh = mfma(w3t[mt], gyf, f32x4{0, 0, 0, 0});
 #pragma unroll
       for (int i = 0; i < 4; ++i) dz[mt][i] = dh[i] * (1.0f - h2[mt][i] * h2[mt][i]);
       db2[mt] += dz[mt];
     }
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {          // layer-2 B fragments of K tiles 2m, 2m+1
+    for (int kt = 0; kt < KO; ++kt) {         // layer-2 B fragments of this wave's K tiles
       bf16x8 f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         f[i] = (__bf16)dz[2 * kt][i];
         f[4 + i] = (__bf16)dz[2 * kt + 1][i];
       }
-      W.dz2_frag[((size_t)t * 8 + 2 * m + kt) * 64 + lane] = f;
+      W.dz2_frag[((size_t)t * 8 + KO * m + kt) * 64 + lane] = f;
     }
-    put_d(T, g, r, dz);
+    put_d<MT>(T, g, r, dz);
 #pragma unroll
-    for (int ft = 0; ft < 4; ++ft) W.dz2_half[((size_t)t * 16 + 4 * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
+    for (int ft = 0; ft < MT; ++ft) W.dz2_half[((size_t)t * 16 + MT * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
     cur = nxt;
     raw_nxt = raw_nxt2;
   };
@@ -460,10 +467,10 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
   // ---- per-workgroup partials
   const int wg = blockIdx.x;
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int f = 64 * m + 16 * mt + 4 * g + i;
+      const int f = FPW * m + 16 * mt + 4 * g + i;
       W.part_w3t[((size_t)wg * HID + f) * 16 + r] = dw3[mt][i];
       const float v = row_sum16(db2[mt][i]);
       if (r == 0) W.part_b2[(size_t)wg * HID + f] = v;
@@ -485,23 +492,25 @@ __global__ __launch_bounds__(THREADS, 1) void k_fwd_bwd(const uint16_t* __restri
   }
 }
 
-// dh1 = W2^T q(dz2) for this wave's hidden-1 features k (64 m .. 64 m + 63), dz1, and the
-// layer-1 weight and bias gradients.
-__global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__ w, const float* __restrict__ b,
-                                                    Batch D, const int32_t* __restrict__ idx, int B, int tiles,
-                                                    Work W) {
-  __shared__ __attribute__((aligned(16))) float b1k[HID];            // read as f32x4
-  __shared__ __attribute__((aligned(16))) __bf16 Ts[NW][64 * TPAD];  // rows read as 8-byte halves
-  __shared__ __attribute__((aligned(16))) __bf16 Xs[NW][32 * TPAD];
+// dh1 = W2^T q(dz2) for this wave's hidden-1 features k (FPW m .. FPW m + FPW - 1), dz1, and
+// the layer-1 weight and bias gradients.
+template <int FPW>
+__global__ __launch_bounds__(64 * HID / FPW, 1) void k_dz1(const uint16_t* __restrict__ w, const float* __restrict__ b,
+                                                           Batch D, const int32_t* __restrict__ idx, int B, int tiles,
+                                                           Work W) {
+  constexpr int NWV = HID / FPW, MT = FPW / 16;
+  __shared__ __attribute__((aligned(16))) float b1k[HID];              // read as f32x4
+  __shared__ __attribute__((aligned(16))) __bf16 Ts[NWV][FPW * TPAD];  // rows read as 8-byte halves
+  __shared__ __attribute__((aligned(16))) __bf16 Xs[NWV][32 * TPAD];
   const int tid = threadIdx.x, lane = tid & 63;
   const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
   const uint16_t* W1 = w;
   const uint16_t* W2 = w + HID * 23;
-  bf16x8 w1[4], w2t[4][8];
+  bf16x8 w1[MT], w2t[MT][8];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
-    const int k = 64 * m + 16 * mt + r;
+  for (int mt = 0; mt < MT; ++mt) {
+    const int k = FPW * m + 16 * mt + r;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int i = kslot(g, j);
@@ -513,17 +522,17 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
       for (int j = 0; j < 8; ++j) w2t[mt][kt][j] = bf16_of_bits(W2[(32 * kt + kslot(g, j)) * HID + k]);
   }
   if (tid < HID) b1k[tid] = b[tid] * TWO_LOG2E;
-  f32x4 dw1[4][2], db1[4];
+  f32x4 dw1[MT][2], db1[MT];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
+  for (int mt = 0; mt < MT; ++mt) {
     db1[mt] = dw1[mt][0] = dw1[mt][1] = f32x4{0, 0, 0, 0};
   }
   __bf16* T = Ts[m];
   __bf16* X = Xs[m];
   __syncthreads();
-  f32x4 b1[4];
+  f32x4 b1[MT];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) b1[mt] = *reinterpret_cast<const f32x4*>(&b1k[64 * m + 16 * mt + 4 * g]);
+  for (int mt = 0; mt < MT; ++mt) b1[mt] = *reinterpret_cast<const f32x4*>(&b1k[FPW * m + 16 * mt + 4 * g]);
   // inputs and q(dz2) fragments of the first tile, raw indices of the second (prefetches
   // unconditional, as in k_fwd_bwd)
   const int Mi = (int)D.M;
@@ -549,16 +558,16 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
     load_dz2(t + gridDim.x, zn);
     const int raw_nxt2 = raw_index(idx, t + 2 * gridDim.x, r, B);
     const bf16x8 x = input_frag(cur, valid, g);
-    f32x4 acc[4];
+    f32x4 acc[MT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) acc[mt] = f32x4{0, 0, 0, 0};
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0, 0, 0, 0};
 #pragma unroll
     for (int kt = 0; kt < 8; ++kt)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[mt] = mfma(w2t[mt][kt], zf[kt], acc[mt]);
-    f32x4 dz[4];
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma(w2t[mt][kt], zf[kt], acc[mt]);
+    f32x4 dz[MT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
       const f32x4 z1 = mfma(w1[mt], x, f32x4{0, 0, 0, 0});
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -568,14 +577,14 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
       db1[mt] += dz[mt];
     }
     // dW1 += q(dz1) q(x)^T over the tile's samples (K slots 4..7 empty)
-    put_d(T, g, r, dz);
+    put_d<MT>(T, g, r, dz);
 #pragma unroll
     for (int j = 0; j < 8; ++j) X[kslot(g, j) * TPAD + r] = x[j];
     bf16x8 bx[2];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) bx[nt] = low_half(half_of(X, 16 * nt + r, g));
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
       const bf16x8 a = low_half(half_of(T, 16 * mt + r, g));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) dw1[mt][nt] = mfma(a, bx[nt], dw1[mt][nt]);
@@ -592,10 +601,10 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
 
   const int wg = blockIdx.x;
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int k = 64 * m + 16 * mt + 4 * g + i;
+      const int k = FPW * m + 16 * mt + 4 * g + i;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) W.part_w1[((size_t)wg * HID + k) * 32 + 16 * nt + r] = dw1[mt][nt][i];
       const float v = row_sum16(db1[mt][i]);
@@ -603,52 +612,62 @@ __global__ __launch_bounds__(THREADS, 1) void k_dz1(const uint16_t* __restrict__
     }
 }
 
-// dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup: wave m owns rows
-// 64 m .. 64 m + 63 (4 M-tiles, its A fragments loaded directly) and all 256 columns (16
-// N-tiles).  The 16 B fragments of a step are shared: wave m loads N-tiles 4m .. 4m+3 and
-// stores them in LDS (two buffers, one barrier per step), every wave reads all 16.  The
-// next step's loads are issued before the current step's 64 products.
-__global__ __launch_bounds__(THREADS, 1) void k_dw2(const u32x2* __restrict__ dz2_half, const u32x2* __restrict__ h1_half,
-                                                    int steps, float* __restrict__ part_w2) {
+// dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup.  Eight waves, two per
+// SIMD: wave w owns rows 64 (w % 4) .. + 63 (4 M-tiles, A fragments loaded directly) and
+// columns 128 (w / 4) .. + 127 (8 N-tiles), 128 accumulators.  The 16 B fragments of a step
+// are shared: wave w loads N-tiles 2w, 2w+1 into LDS (two buffers, one barrier per step) and
+// reads its eight.  A step's 32 products take far less time than a load's latency, so loads
+// run DW2_DEPTH steps ahead in a ring of register sets (the loop unrolled by DW2_DEPTH); they
+// are unconditional (the step index clamped) so that every wait covers only its own set.
+__global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restrict__ dz2_half,
+                                                           const u32x2* __restrict__ h1_half, int steps,
+                                                           float* __restrict__ part_w2) {
   __shared__ bf16x8 Bs[2][16][64];
   const int tid = threadIdx.x, lane = tid & 63;
-  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int mr = w & 3, nc = w >> 2;
   const int g = lane >> 4, r = lane & 15;
-  const int per = (steps + gridDim.x - 1) / gridDim.x;
+  const int per = (steps / DW2_DEPTH + gridDim.x - 1) / gridDim.x * DW2_DEPTH;   // steps % DW2_DEPTH == 0
   const int u0 = blockIdx.x * per, u1 = min(steps, u0 + per);
-  f32x4 acc[4][16];
+  f32x4 acc[4][8];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 16; ++nt) acc[mt][nt] = f32x4{0, 0, 0, 0};
+    for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = f32x4{0, 0, 0, 0};
   if (u0 < u1) {
     auto at = [&](int tile, int ft) { return ((size_t)tile * 16 + ft) * 64 + lane; };
-    auto load = [&](int u, bf16x8* a, bf16x8* bo) {
-      u = min(u, u1 - 1);   // unconditional (the last step is read again)
+    bf16x8 A[DW2_DEPTH][4], Bo[DW2_DEPTH][2];
+    auto load = [&](int u, int j) __attribute__((always_inline)) {
+      u = min(u, u1 - 1);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) a[mt] = join(dz2_half[at(2 * u, 4 * m + mt)], dz2_half[at(2 * u + 1, 4 * m + mt)]);
+      for (int mt = 0; mt < 4; ++mt)
+        A[j][mt] = join(dz2_half[at(2 * u, 4 * mr + mt)], dz2_half[at(2 * u + 1, 4 * mr + mt)]);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) bo[q] = join(h1_half[at(2 * u, 4 * m + q)], h1_half[at(2 * u + 1, 4 * m + q)]);
+      for (int q = 0; q < 2; ++q) Bo[j][q] = join(h1_half[at(2 * u, 2 * w + q)], h1_half[at(2 * u + 1, 2 * w + q)]);
     };
-    bf16x8 A[4], Bo[4];
-    load(u0, A, Bo);
-    int buf = 0;
-    for (int u = u0; u < u1; ++u) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Bs[buf][4 * m + q][lane] = Bo[q];
-      __syncthreads();   // this step's B fragments visible; readers of this buffer two steps ago are done
-      bf16x8 An[4];
-      load(u + 1, An, Bo);
+    for (int j = 0; j < DW2_DEPTH; ++j) load(u0 + j, j);
+    // u1 - u0 is a multiple of DW2_DEPTH (padded minibatch, rounded share), so a round has no
+    // branch; the first round is peeled so that both paths into the loop header have the same
+    // loads in flight (the prologue's own load order would otherwise set the header's wait).
+    auto round = [&](int u) __attribute__((always_inline)) {
 #pragma unroll
-      for (int nt = 0; nt < 16; ++nt) {
-        const bf16x8 bf = Bs[buf][nt][lane];
+      for (int j = 0; j < DW2_DEPTH; ++j) {
+        const int b = j & 1;
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[mt], bf, acc[mt][nt]);
+        for (int q = 0; q < 2; ++q) Bs[b][2 * w + q][lane] = Bo[j][q];
+        __syncthreads();   // this step's B fragments visible; readers of this buffer two steps ago are done
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) {
+          const bf16x8 bf = Bs[b][8 * nc + nt][lane];
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[j][mt], bf, acc[mt][nt]);
+        }
+        load(u + j + DW2_DEPTH, j);
       }
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) A[mt] = An[mt];
-      buf ^= 1;
-    }
+    };
+    round(u0);
+    for (int u = u0 + DW2_DEPTH; u < u1; u += DW2_DEPTH) round(u);
   }
   float* out = part_w2 + (size_t)blockIdx.x * HID * HID;
 #pragma unroll
@@ -656,7 +675,7 @@ __global__ __launch_bounds__(THREADS, 1) void k_dw2(const u32x2* __restrict__ dz
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int nt = 0; nt < 16; ++nt) out[(64 * m + 16 * mt + 4 * g + i) * HID + 16 * nt + r] = acc[mt][nt][i];
+      for (int nt = 0; nt < 8; ++nt) out[(64 * mr + 16 * mt + 4 * g + i) * HID + 128 * nc + 16 * nt + r] = acc[mt][nt][i];
 }
 
 // Packed gradient of one network = fixed-order sums of the partials, and per-block sums of
@@ -817,7 +836,7 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
   hipStream_t s = (hipStream_t)stream;
   const int tiles = ppo::padded(B) / 16, steps = ppo::padded(B) / 32;
   const int cus = std::min(compute_units(), ppo::MAX_GROUPS);
-  const int G1 = std::min(cus, tiles), G3 = std::min(cus, steps);
+  const int G1 = std::min(cus, tiles), G3 = std::min(cus, steps / ppo::DW2_DEPTH);
   const ppo::Work W = ppo::work_at(work, B);
   const ppo::Hp hp{cfg->clip_eps, cfg->vf_coef, cfg->ent_coef, cfg->max_grad_norm, 1.0f / (float)B, cfg->normalize_adv ? 1 : 0};
   const ppo::Batch D{batch->obs, batch->act, batch->logp, batch->adv, batch->ret, (size_t)batch->M};
@@ -827,16 +846,17 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
                        W.adv_part);
     hipLaunchKernelGGL(ppo::k_adv_final, dim3(1), dim3(64), 0, s, W.adv_part, B, W.advstat);
   }
-  hipLaunchKernelGGL(ppo::k_fwd_bwd<8>, dim3(G1), dim3(ppo::THREADS), 0, s, policy->w, policy->b, policy->log_std, D, idx,
+  constexpr int FPW = ppo::FPW, TH = 64 * HID / FPW;
+  hipLaunchKernelGGL((ppo::k_fwd_bwd<8, FPW>), dim3(G1), dim3(TH), 0, s, policy->w, policy->b, policy->log_std, D, idx,
                      B, tiles, hp, W, 0);
-  hipLaunchKernelGGL(ppo::k_dz1, dim3(G1), dim3(ppo::THREADS), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
-  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(ppo::THREADS), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+  hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
+  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, G1, G1, G3, W, cfg->ent_coef,
                      grad_policy, W.part_ss);
-  hipLaunchKernelGGL(ppo::k_fwd_bwd<1>, dim3(G1), dim3(ppo::THREADS), 0, s, value->w, value->b, (const float*)nullptr, D,
+  hipLaunchKernelGGL((ppo::k_fwd_bwd<1, FPW>), dim3(G1), dim3(TH), 0, s, value->w, value->b, (const float*)nullptr, D,
                      idx, B, tiles, hp, W, 1);
-  hipLaunchKernelGGL(ppo::k_dz1, dim3(G1), dim3(ppo::THREADS), 0, s, value->w, value->b, D, idx, B, tiles, W);
-  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(ppo::THREADS), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+  hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, value->w, value->b, D, idx, B, tiles, W);
+  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, G1, G1, G3, W, 0.0f,
                      grad_value, W.part_ss + rb);
   hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, G1, G1, W, rb, ppo::red_blocks(1), rb, policy->log_std, hp,
