@@ -208,3 +208,65 @@ def test_ppo_full_minibatch_size(setup):
     _check_grads(host(L.val.grad), want["grad_val"], 1, "value")
     assert abs(st[0] - want["pg_loss"]) <= 2e-3 * max(1.0, abs(want["pg_loss"]))
     assert st[4] == pytest.approx(want["clip_frac"], abs=0.5 / B)
+
+
+def test_adam_writes_the_weights_the_rollout_reads(setup):
+    """After an Adam step the auv_mlp view of a PpoNet (bf16 copy + fp32 tail of theta) is the
+    updated network: auv_mlp_forward through it matches the oracle forward of the updated
+    parameters (nearest valid bf16 output)."""
+    netp, netv, pol, val, buf, dev, M, PpoLearner = setup
+    announce("ppo view after adam")
+    from oracle.mlp import nearest_valid_error
+    from paper_2512_13359_amd import _abi as A
+    L = PpoLearner(netp, netv, lr=1e-2)
+    idx = W.ppo_minibatch_idx(M, 512, seed=9)
+    L.update(L.batch(dev["obs"], dev["act"], dev["logp"], dev["adv"], dev["ret"]), torch.from_numpy(idx).cuda())
+    th = host(L.pol.theta)
+    new = dict(netp)
+    wb = host(L.pol.w_bf16).view(np.uint16)
+    n1, n2 = 256 * 23, 256 * 256
+    new["W1"], new["W2"], new["W3"] = wb[:n1].reshape(256, 23), wb[n1:n1 + n2].reshape(256, 256), wb[n1 + n2:].reshape(8, 256)
+    nw = L.pol.nw
+    new["b1"], new["b2"], new["b3"] = th[nw:nw + 256], th[nw + 256:nw + 512], th[nw + 512:nw + 520]
+    assert not np.array_equal(wb[:n1], netp["W1"].ravel())           # the step changed the weights
+    obs = buf["obs"][:, :300]
+    out = torch.empty(8, 300, device="cuda")
+    A.auv_mlp_forward(L.pol.mlp, 300, dev["obs"][:, :300].contiguous(), out)
+    err = nearest_valid_error(host(out), obs.astype(np.float64), new, 1e-6)
+    assert err.max() <= 2e-4, err.max()
+
+
+def test_ppo_training_loop_on_rollouts():
+    """Rollout with sampling and the value head, GAE, then PPO epochs over the rollout buffer,
+    all through the C interface: statistics finite, the loss on a fixed minibatch falls over a
+    few updates, and the next rollout runs on the updated weights."""
+    require_gpu()
+    announce("ppo training loop on c5-shaped rollouts")
+    from paper_2512_13359_amd import AuvEnv, PpoLearner
+    from paper_2512_13359_amd import _abi as A
+    cfg = W.config("c5", n_envs=2048, T=32)
+    n, T = cfg["n_envs"], cfg["T"]
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.reset()
+    L = PpoLearner(W.mlp_weights(8, W.POLICY_SEED), W.mlp_weights(1, W.VALUE_SEED), lr=1e-3)
+    bufs = env.rollout_buffers(T, record=("obs", "act", "logp", "value", "reward", "done", "last_value"), value=True)
+    env.rollout(T, W.MODE_POLICY_SAMPLE, policy={"struct": L.pol.mlp}, value={"struct": L.val.mlp}, bufs=bufs)
+    adv = torch.empty(T, n, device="cuda")
+    ret = torch.empty(T, n, device="cuda")
+    A.auv_gae(T, n, bufs["reward"], bufs["value"], bufs["done"], bufs["last_value"], 0.99, 0.95, adv, ret)
+    M = T * n
+    batch = L.batch(bufs["obs"].reshape(23, M), bufs["act"].reshape(8, M), bufs["logp"].reshape(M), adv.reshape(M),
+                    ret.reshape(M))
+    fixed = torch.from_numpy(W.ppo_minibatch_idx(M, 8192, seed=0)).cuda()
+    L.grad(batch, fixed)
+    first = host(L.stats).copy()
+    assert abs(first[3]) < 1e-3            # ratio 1 on fresh samples: approx KL ~ 0 (bf16 policy re-evaluated)
+    for k in range(6):
+        L.update(batch, fixed)
+    L.grad(batch, fixed)
+    last = host(L.stats)
+    assert np.all(np.isfinite(last))
+    assert last[0] + last[1] < first[0] + first[1]
+    env.rollout(T, W.MODE_POLICY_SAMPLE, policy={"struct": L.pol.mlp}, value={"struct": L.val.mlp}, bufs=bufs)
+    r = host(bufs["reward"])
+    assert np.all(np.isfinite(r))
