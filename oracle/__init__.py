@@ -18,10 +18,12 @@ Modules
             batch statistics, rollouts (paper Sec. IV-A, IV-B, IV-C, V-A)
   mlp       bf16 round-to-nearest-even, policy / value MLP forward, Gaussian log-prob
   gae       generalised advantage estimation (the PPO learner of Sec. III-A)
+  paper_task the paper's own training task: 12-D axis-angle observation, 6-D wrench action,
+            five-term reward with an action moving average, gravity randomisation
   ppo       clipped-surrogate PPO objective, its gradient through both MLPs (with the
             bf16 quantisation points of the MFMA path), global-norm clipping, Adam
 
 Every function is pinned by a ``-m "not gpu"`` test against closed forms, invariants,
 special cases or an independent library; see the test files under ``tests/``.
 """
-from . import rng, dynamics, mlp, gae, env, ppo  # noqa: F401
+from . import rng, dynamics, mlp, gae, env, ppo, paper_task  # noqa: F401

@@ -120,7 +120,7 @@ class Vehicle:
         """Restoring vector g(q) = [(B - W) k ; B r_b x k], k = R^T e_3 (the world down
         direction in body axes); it sits on the left-hand side of the equations."""
         k = R[:, 2, :]                                                 # row 3 of R = R^T e3
-        f = (self.B - self.W) * k
+        f = np.reshape(self.B - self.W, (-1, 1)) * k                   # W: one value or one per env
         mom = self.B * np.cross(np.broadcast_to(self.r_b, k.shape), k)
         return np.concatenate([f, mom], axis=1)
 
