@@ -197,6 +197,39 @@ def ppo_measure(reps: int = 5) -> dict:
             "frac_of_bf16_peak": ach / P_MFMA}
 
 
+def paper_task_measure(reps: int = 3) -> dict:
+    """The paper's own task (12-D observation, 6-D wrench, five-term reward) at the paper's
+    training scale: 4096 envs x one 512-step episode, policy mean (12-256-256-6) and random
+    actions; env-steps/s per launch."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, upload_mlp
+
+    cfg = W.config("c6")
+    n, T = cfg["n_envs"], cfg["T"]
+    pol = upload_mlp(W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12))
+    out = {"workload": f"c6: paper task, {n} envs x {T} steps (one episode), {cfg['substeps']} RK4 substeps "
+                       f"per {cfg['dt_control']} s, gravity randomisation, goals within 2 m / 60 deg"}
+    for name, mode, p in (("policy", W.MODE_POLICY_MEAN, pol), ("random", W.MODE_RANDOM, None)):
+        env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+        env.set_task(W.PAPER_TASK)
+        ts = []
+        for k in range(reps + 1):
+            env.reset()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            env.rollout(T, mode, policy=p)
+            e1.record()
+            torch.cuda.synchronize()
+            if k:
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+        t = sorted(ts)[len(ts) // 2]
+        out[name] = {"launch_ms": t * 1e3, "env_steps_per_s": n * T / t}
+    return out
+
+
 def small_configs_measure(reps: int = 3) -> dict:
     """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
     4096 envs occupy 64 of the 256 CUs, so these are occupancy-capped by N."""
@@ -336,6 +369,7 @@ def main() -> int:
         line.update(small_configs_measure())
     if not args.no_ppo and not args.no_c5:
         line["ppo"] = ppo_measure()
+        line["c6"] = paper_task_measure()
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
     print(json.dumps(line), flush=True)

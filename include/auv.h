@@ -186,6 +186,43 @@ int auv_set_global_step(auv_env* env, int64_t step);
  * ends normally and leaves NaN state. */
 int auv_set_sync_poll_limit(auv_env* env, uint32_t polls);
 
+/* ---- The paper's own training task ------------------------------------------------------
+ * By default an environment runs the workload task described at the top.  AUV_TASK_PAPER
+ * switches it to the task the paper trains on (Sec. IV-B observation / action / reward,
+ * Sec. IV-C randomisation, Sec. V-A references):
+ *   action a in R^6 (rows 0-2 forces, 3-5 torques), u = clip(a, -1, 1),
+ *     body wrench [f_max u_0:3, tau_max u_3:6] (no thruster allocation)
+ *   observation (rows 0-11 of the obs buffers): body-frame position error R^T(p_goal - p),
+ *     rotation vector of q^* (x) q_goal (shortest rotation), v, omega; rows 12-17 of the env
+ *     obs buffer hold the moving average of past clipped actions (state), rows 18-22 are 0;
+ *     recorded rollout observations have zeros in rows 12-22
+ *   reward -w_pos |D dp|^2 - w_att |dtheta|^2 - w_act |u_3:6|^2 - w_vel |omega|^2
+ *     - w_mavg |u - abar|^2, then abar <- beta abar + (1 - beta) u (abar = 0 at an episode start)
+ *   reset: at rest at the origin, level; goal position U[-2, 2]^3 (reset words 12-14); goal
+ *     attitude q_z(yaw) q_y(pitch) q_x(roll), each angle U[-euler_max, euler_max] (words
+ *     15-17); weight gamma W with gamma U[gamma_lo, gamma_lo + gamma_span] (word 0, kept in
+ *     params row 13); buoyancy centre at the centre of gravity (r_b ignored); no other
+ *     randomisation, no current, goal pose constant over the episode
+ *   random actions: action c <- word 2c, action 3 + c <- word 2c + 1 of the random-action
+ *   counter; sampled actions: the Box-Muller pair of words (2c, 2c + 1) gives the noise of
+ *   actions c and 3 + c.  The policy is a 23-256-256-8 network whose W1 columns 12-22 and
+ *   W3 rows 6-7 are zero (a 12-256-256-6 network).  Batches of any size use the quad-layout
+ *   loop.  Set the task before auv_reset. */
+enum { AUV_TASK_WORKLOAD = 0, AUV_TASK_PAPER = 1 };
+
+typedef struct {
+  int32_t kind;          /* AUV_TASK_* */
+  float f_max, tau_max;  /* N, N m at |u| = 1 (> 0) */
+  float w_pos, d_pos[3], w_att, w_act, w_vel, w_mavg;   /* reward weights (>= 0) */
+  float beta;            /* moving-average factor, 0 <= beta < 1 */
+  float gamma_lo, gamma_span;   /* gravity factor range, gamma_lo > 0, span >= 0 */
+  float euler_max;       /* goal Euler angle bound, rad, 0 <= euler_max <= pi */
+} auv_task;
+
+/* Selects the task of a handle (no GPU call).  AUV_EINVAL for values out of range, or for
+ * AUV_TASK_PAPER with AUV_F_DR, AUV_F_CURRENT or AUV_F_LISSAJOUS set (not part of that task). */
+int auv_set_task(auv_env* env, const auv_task* task);
+
 /* ---- PPO update of the policy and value MLPs on one minibatch ------------------------
  * The clipped-surrogate objective of PPO (Schulman et al. 2017; the on-policy learner of
  * paper Sec. II-B and III-A, which gives no hyperparameters), over minibatch samples b:

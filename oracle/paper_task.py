@@ -17,15 +17,16 @@ Readings where the paper is silent (the same on both sides):
   * dynamics: the Fossen model of the other workloads (dynamics.py) with the buoyancy centre
     at the centre of gravity (r_b = 0), no current, no mass / damping randomisation; the
     gravity factor gamma scales the weight: W = gamma W0, gamma ~ U[0.95, 1.05]
-  * wrench tau = [F_max u_0:3, tau_max u_3:6], u = clip(a, -1, 1), F_max 60 N, tau_max 10 N m
+  * wrench tau = [F_max u_0:3, tau_max u_3:6], u = clip(a, -1, 1)
   * reset: p0 = 0, q0 = identity, v = omega = 0; goal position U[-2, 2]^3; goal attitude from
     Z-Y-X Euler angles (roll, pitch, yaw) each U[-60, 60] degrees, q = q_z(yaw) q_y(pitch) q_x(roll)
   * attitude error: q_err = q^* (x) q_ref (body frame), taken with a non-negative scalar part;
     axis-angle vector = angle * axis, angle = 2 atan2(|vec|, w)
-  * reward weights w_pos 1, D = diag(1, 1, 1.5), w_att 0.5, w_act 0.01 (on the normalised
-    torque commands u_3:6), w_vel 0.05, w_mavg 0.1; the action average is an exponential
-    moving average of past clipped actions, abar <- 0.8 abar + 0.2 u after each step's reward,
-    zero at an episode start
+  * w_act weighs the normalised torque commands u_3:6; the action average is an exponential
+    moving average of past clipped actions, abar <- beta abar + (1 - beta) u after each step's
+    reward, zero at an episode start
+  * the constants (F_max, tau_max, weights, D, beta, gravity and angle ranges) come in a task
+    dict (workloads.PAPER_TASK); every value is an fp32 number promoted exactly
   * step order as in env.py; done at ep_step == H; a done env is reset and observed afresh
 """
 from __future__ import annotations
@@ -42,20 +43,7 @@ from .env import _f64
 MODE_EXTERNAL, MODE_RANDOM, MODE_POLICY_MEAN, MODE_POLICY_SAMPLE = 0, 1, 2, 3
 FLAG_STAGGER = 8
 
-# task constants (fp32 values, promoted exactly)
-F_MAX = float(np.float32(60.0))
-TAU_MAX = float(np.float32(10.0))
-W_POS = float(np.float32(1.0))
-D_POS = np.array([1.0, 1.0, 1.5], np.float32).astype(np.float64)
-W_ATT = float(np.float32(0.5))
-W_ACT = float(np.float32(0.01))
-W_VEL = float(np.float32(0.05))
-W_MAVG = float(np.float32(0.1))
-BETA = float(np.float32(0.8))
-R_GFAC = (0.95, 0.1)                                 # U[0.95, 1.05]
 R_POS = (-2.0, 4.0)
-_DEG60 = float(np.float32(math.pi / 3.0))
-R_EULER = (-_DEG60, float(np.float32(2.0 * np.float32(math.pi / 3.0))))
 W_GFAC, W_PGOAL, W_EULER = 0, 12, 15                 # Philox reset words (block layout of env.py)
 N_RESET_BLOCKS = 8
 
@@ -90,8 +78,24 @@ def axis_angle_error(q, q_ref):
     return k[None, :] * e[1:4]
 
 
+class Task:
+    """The task constants as fp32 values promoted exactly: the gravity factor is drawn as
+    lo + span u and the Euler angles as -e + (2e) u with fp32 (lo, span)."""
+
+    def __init__(self, t: dict):
+        f = lambda x: float(np.float32(x))  # noqa: E731
+        self.f_max, self.tau_max = f(t["f_max"]), f(t["tau_max"])
+        self.w_pos, self.w_att, self.w_act = f(t["w_pos"]), f(t["w_att"]), f(t["w_act"])
+        self.w_vel, self.w_mavg, self.beta = f(t["w_vel"]), f(t["w_mavg"]), f(t["beta"])
+        self.d_pos = np.asarray(t["d_pos"], np.float32).astype(np.float64)
+        self.r_gfac = (t["gamma_lo"], t["gamma_span"])
+        e = np.float32(t["euler_max"])
+        self.r_euler = (-float(e), float(np.float32(2.0) * e))
+
+
 class PaperEnv:
-    def __init__(self, cfg: dict, vehicle: dict):
+    def __init__(self, cfg: dict, vehicle: dict, task: dict):
+        self.tk = Task(task)
         self.n = n = int(cfg["n_envs"])
         self.ids = np.arange(n, dtype=np.int64) + int(cfg.get("env_offset", 0))
         self.seed = int(cfg["seed"])
@@ -124,9 +128,9 @@ class PaperEnv:
         w = rng.words(self.seed, self.ids[idx], self.episode[idx], 0, N_RESET_BLOCKS)
         u = rng.uniform01(w)
         aff = lambda r, j: _f64(rng.affine_f32(r[0], r[1], u[j]))  # noqa: E731
-        self.gfac[idx] = aff(R_GFAC, W_GFAC)
+        self.gfac[idx] = aff(self.tk.r_gfac, W_GFAC)
         self.p_goal[:, idx] = np.stack([aff(R_POS, W_PGOAL + i) for i in range(3)])
-        e = [aff(R_EULER, W_EULER + i) for i in range(3)]
+        e = [aff(self.tk.r_euler, W_EULER + i) for i in range(3)]
         self.q_goal[:, idx] = euler_zyx_quat(e[0], e[1], e[2])
         self.x[:, idx] = 0.0
         self.x[3, idx] = 1.0
@@ -152,16 +156,17 @@ class PaperEnv:
     def step(self, actions):
         """actions [6, n] before clipping -> (reward [n], done [n], stats (3,), obs [12, n]);
         stats = sums of reward, done and |dp_b|."""
+        k = self.tk
         u = np.clip(np.asarray(actions, np.float64), -1.0, 1.0)
-        tau = np.concatenate([F_MAX * u[0:3], TAU_MAX * u[3:6]])
+        tau = np.concatenate([k.f_max * u[0:3], k.tau_max * u[3:6]])
         self.x = dyn.integrate(self.x, tau, self.veh, self.c_w, self.dt, self.S)
         self.ep_step += 1
         obs = self.observe()
         dp, dth, om = obs[0:3], obs[3:6], obs[9:12]
-        reward = (-W_POS * np.sum((D_POS[:, None] * dp) ** 2, axis=0) - W_ATT * np.sum(dth * dth, axis=0)
-                  - W_ACT * np.sum(u[3:6] ** 2, axis=0) - W_VEL * np.sum(om * om, axis=0)
-                  - W_MAVG * np.sum((u - self.abar) ** 2, axis=0))
-        self.abar = BETA * self.abar + (1.0 - BETA) * u
+        reward = (-k.w_pos * np.sum((k.d_pos[:, None] * dp) ** 2, axis=0) - k.w_att * np.sum(dth * dth, axis=0)
+                  - k.w_act * np.sum(u[3:6] ** 2, axis=0) - k.w_vel * np.sum(om * om, axis=0)
+                  - k.w_mavg * np.sum((u - self.abar) ** 2, axis=0))
+        self.abar = k.beta * self.abar + (1.0 - k.beta) * u
         done = self.ep_step == self.H
         stats = np.array([reward.sum(), float(done.sum()), np.linalg.norm(dp, axis=0).sum()])
         idx = np.nonzero(done)[0]

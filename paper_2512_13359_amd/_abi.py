@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "libauv.so")
 AUV_OK, AUV_EINVAL, AUV_ENODEV, AUV_ELAUNCH, AUV_ERUNTIME = 0, -1, -2, -3, -4
 AUV_ACT_EXTERNAL, AUV_ACT_RANDOM, AUV_ACT_POLICY_MEAN, AUV_ACT_POLICY_SAMPLE = 0, 1, 2, 3
 AUV_F_DR, AUV_F_CURRENT, AUV_F_LISSAJOUS, AUV_F_STAGGER = 1, 2, 4, 8
+AUV_TASK_WORKLOAD, AUV_TASK_PAPER = 0, 1
 OBS_DIM, ACT_DIM, STATE_DIM, PARAM_DIM, HIDDEN, ENVS_PER_GROUP = 23, 8, 13, 24, 256, 64
 
 _f = ctypes.c_float
@@ -46,6 +47,12 @@ class AuvMlp(ctypes.Structure):
 class AuvRolloutBuffers(ctypes.Structure):
     _fields_ = [(k, _vp) for k in ("obs", "act", "logp", "value", "reward", "done", "last_value",
                                    "traj_state", "stats", "stats_work")]
+
+
+class AuvTask(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("f_max", _f), ("tau_max", _f), ("w_pos", _f), ("d_pos", _f * 3),
+                ("w_att", _f), ("w_act", _f), ("w_vel", _f), ("w_mavg", _f), ("beta", _f), ("gamma_lo", _f),
+                ("gamma_span", _f), ("euler_max", _f)]
 
 
 class AuvPpoConfig(ctypes.Structure):
@@ -94,6 +101,7 @@ def _load() -> ctypes.CDLL:
         "auv_get_global_step": (i64, [_vp]),
         "auv_set_global_step": (ctypes.c_int, [_vp, i64]),
         "auv_set_sync_poll_limit": (ctypes.c_int, [_vp, ctypes.c_uint32]),
+        "auv_set_task": (ctypes.c_int, [_vp, P(AuvTask)]),
         "auv_ppo_work_bytes": (i64, [i32]),
         "auv_ppo_grad": (ctypes.c_int, [P(AuvPpoConfig), P(AuvMlp), P(AuvMlp), P(AuvPpoBatch), _vp, i32, _vp, _vp,
                                         _vp, _vp, _vp]),
@@ -180,6 +188,10 @@ def auv_set_sync_poll_limit(h: int, polls: int) -> None:
     _check(lib.auv_set_sync_poll_limit(h, polls))
 
 
+def auv_set_task(h: int, task: AuvTask) -> None:
+    _check(lib.auv_set_task(h, ctypes.byref(task)))
+
+
 def auv_ppo_work_bytes(B: int) -> int:
     return int(lib.auv_ppo_work_bytes(B))
 
@@ -224,6 +236,18 @@ def make_mlp(w, b, log_std, n_out: int) -> AuvMlp:
 
 def make_env_buffers(state, params, ep_step, episode, obs) -> AuvEnvBuffers:
     return AuvEnvBuffers(ptr(state), ptr(params), ptr(ep_step), ptr(episode), ptr(obs))
+
+
+def make_task(task: dict) -> AuvTask:
+    """auv_task from a dict (kind, f_max, tau_max, w_pos, d_pos, w_att, w_act, w_vel, w_mavg, beta,
+    gamma_lo, gamma_span, euler_max)."""
+    t = AuvTask()
+    for k, v in task.items():
+        if k == "d_pos":
+            t.d_pos[:] = [float(x) for x in v]
+        else:
+            setattr(t, k, v)
+    return t
 
 
 def make_ppo_config(clip_eps=0.2, vf_coef=0.5, ent_coef=0.0, max_grad_norm=0.5, lr=3e-4, beta1=0.9,

@@ -13,9 +13,22 @@ struct VehArgs {
   float m, inertia[3], added_mass[6], lin_damp[6], quad_damp[6];
   float BmW;     // B - W
   float Brb[3];  // B * r_b
+  float B, W;    // buoyancy and weight (the paper task scales W per environment)
   float f_max;
   float alloc[48];
 };
+
+// The paper's own training task (selected by EnvArgs::task): normalised 6-D body wrench,
+// five-term reward with an exponential moving average of past actions, gravity factor
+// per environment, goal attitude from Euler angles.
+struct TaskArgs {
+  float f_max, tau_max;                 // wrench at |u| = 1 (N, N m)
+  float w_pos, d_pos[3], w_att, w_act, w_vel, w_mavg;
+  float beta;                           // moving average: abar <- beta abar + (1 - beta) u
+  float g_lo, g_span;                   // gravity factor U[g_lo, g_lo + g_span]
+  float eul_lo, eul_span;               // goal roll, pitch, yaw U[eul_lo, eul_lo + eul_span]
+};
+constexpr uint32_t TASK_WORKLOAD = 0, TASK_PAPER = 1;
 
 struct EnvArgs {
   float* state;
@@ -27,6 +40,8 @@ struct EnvArgs {
   float dt, h;
   uint32_t key0, key1, flags, env_offset;
   uint32_t sync_polls;   // bound on the polls of one inter-wave wait (fused policy rollout)
+  uint32_t task;         // TASK_WORKLOAD or TASK_PAPER
+  TaskArgs tk;
 };
 
 // Per-step output pointers of the environment loops; any may be null.
@@ -295,6 +310,46 @@ __device__ __forceinline__ void reset_draws(const EnvArgs& E, uint32_t gid, uint
   shoemake(u01(wd[15]), u01(wd[16]), u01(wd[17]), P.qg);
   P.yaw_rate = affine(-0.1f, 0.2f, u01(wd[27]));
   P.yaw0 = affine(-3.14159274f, 6.28318548f, u01(wd[28]));
+}
+
+// Reset of the paper task: the vehicle at rest at the origin, level; goal position
+// U[-2, 2]^3 (words 12-14), goal attitude q_z(yaw) q_y(pitch) q_x(roll) from Euler angles
+// (words 15-17), gravity factor (word 0, kept in parameter row 13); no other
+// randomisation.  Same counters as reset_draws (only blocks 0, 3 and 4 are needed).
+__device__ __forceinline__ void paper_reset_draws(const EnvArgs& E, uint32_t gid, uint32_t episode, State& x,
+                                                  Params& P) {
+  const U4 b0 = philox(U4{gid, episode, 0u, 0u}, E.key0, E.key1);
+  const U4 b3 = philox(U4{gid, episode, 0u, 3u}, E.key0, E.key1);
+  const U4 b4 = philox(U4{gid, episode, 0u, 4u}, E.key0, E.key1);
+  const uint32_t pw[3] = {b3.x, b3.y, b3.z};          // words 12, 13, 14
+  const uint32_t ew[3] = {b3.w, b4.x, b4.y};          // words 15, 16, 17: roll, pitch, yaw
+  float half[3];
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    P.s[i] = 1.0f;
+    P.cw[i] = 0.0f;
+    P.pg[i] = affine(-2.0f, 4.0f, u01(pw[i]));
+    P.amp[i] = 0.0f;
+    P.freq[i] = 0.0f;
+    P.phase[i] = 0.0f;
+    half[i] = 0.5f * affine(E.tk.eul_lo, E.tk.eul_span, u01(ew[i]));
+    x.p[i] = 0.0f;
+    x.v[i] = 0.0f;
+    x.w[i] = 0.0f;
+  }
+  P.amp[0] = affine(E.tk.g_lo, E.tk.g_span, u01(b0.x));
+  P.yaw_rate = 0.0f;
+  P.yaw0 = 0.0f;
+  float sr, cr, sp, cp, sy, cy;
+  sincosf(half[0], &sr, &cr);
+  sincosf(half[1], &sp, &cp);
+  sincosf(half[2], &sy, &cy);
+  P.qg[0] = cy * cp * cr + sy * sp * sr;
+  P.qg[1] = cy * cp * sr - sy * sp * cr;
+  P.qg[2] = cy * sp * cr + sy * cp * sr;
+  P.qg[3] = sy * cp * cr - cy * sp * sr;
+  x.q[0] = 1.0f;
+  x.q[1] = x.q[2] = x.q[3] = 0.0f;
 }
 
 // ---------------------------------------------------- reference / obs / reward ------

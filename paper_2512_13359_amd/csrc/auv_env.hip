@@ -39,6 +39,27 @@ __global__ __launch_bounds__(256) void k_reset(VehArgs V, EnvArgs E) {
   const int ep = (E.flags & F_STAGGER) ? (int)(gid % (uint32_t)E.H) : 0;
   State x;
   Params P;
+  if (E.task == TASK_PAPER) {
+    // the paper task starts at rest at the origin, level: dp_b = p_goal and the attitude
+    // error is the rotation vector of q_goal (scalar part made non-negative)
+    paper_reset_draws(E, gid, 0u, x, P);
+    const float sg = P.qg[0] < 0.0f ? -1.0f : 1.0f, w = fabsf(P.qg[0]);
+    const float n2 = P.qg[1] * P.qg[1] + P.qg[2] * P.qg[2] + P.qg[3] * P.qg[3], nn = sqrtf(n2);
+    const float k = sg * (nn > 0.0f ? 2.0f * atan2f(nn, w) / nn : 2.0f / w);
+    const int n = E.n;
+    store_state(E.state, (size_t)n, (size_t)i, x);
+    store_params(E.params, n, i, P);
+    E.ep_step[i] = ep;
+    E.episode[i] = 0u;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      E.obs[j * n + i] = P.pg[j];
+      E.obs[(3 + j) * n + i] = k * P.qg[1 + j];
+    }
+#pragma unroll
+    for (int j = 6; j < OBS; ++j) E.obs[j * n + i] = 0.0f;
+    return;
+  }
   reset_draws(E, gid, 0u, x, P);
   float pr[3], qr[4], o[15], dist, theta;
   reference(E, P, ep, pr, qr);
@@ -103,8 +124,10 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
 // environment e's x, y, z components and the quaternion's scalar part): a one-wave block
 // steps 16 environments and writes one stats partial per step.  It spends about twice the
 // instructions per environment of k_env_loop but makes four times the waves, so it is the
-// faster loop while the batch leaves SIMDs idle.
-template <bool EXTERNAL>
+// faster loop while the batch leaves SIMDs idle.  PAPER: the paper's own task (6-D wrench
+// action, lane c < 3 holding action components c and 3 + c; 12-D observation; five-term
+// reward with the action moving average; gravity factor), which only this loop runs.
+template <bool EXTERNAL, bool PAPER>
 __global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, uint32_t gstep0, StepOut O) {
   __shared__ float alloc[8][8];
   const int lane = threadIdx.x;
@@ -118,43 +141,62 @@ __global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, ui
   const uint32_t gid = E.env_offset + (uint32_t)i;
   float Tf[8], Tm[8];
   quad::alloc_rows(alloc, c, Tf, Tm);
+  const float dc = quad::pick(K, E.tk.d_pos[0], E.tk.d_pos[1], E.tk.d_pos[2], 0.0f);
+  // action rows of this lane: (2c, 2c+1), or (c, 3+c) for lanes 0-2 of the paper task
+  const int ra0 = PAPER ? c : 2 * c, ra1 = PAPER ? 3 + c : 2 * c + 1;
+  const bool acts = !PAPER || c < 3;
   quad::QEnv X;
   quad::QModel M;
   quad::QRef F;
-  quad::load_env(V, E, K, i, valid, X, M, F);
+  quad::load_env<PAPER>(V, E, K, i, valid, X, M, F);
   if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, c, X);
   StatsBuf SB{};
   for (int t = 0; t < T; ++t) {
     const size_t ti = (size_t)t * N + (size_t)i;
-    if (O.obs && valid) quad::store_obs(O.obs, TN, ti, c, X);
-    float a0, a1;   // action components 2c and 2c + 1
+    if (O.obs && valid) quad::store_obs<PAPER>(O.obs, TN, ti, c, X, false);
+    float a0, a1;
     if (EXTERNAL) {
-      a0 = valid ? O.act[(2 * c) * TN + ti] : 0.0f;
-      a1 = valid ? O.act[(2 * c + 1) * TN + ti] : 0.0f;
+      a0 = (valid && acts) ? O.act[ra0 * TN + ti] : 0.0f;
+      a1 = (valid && acts) ? O.act[ra1 * TN + ti] : 0.0f;
     } else {        // words (x, y) or (z, w) of Philox block c / 2 of this step
       const U4 r = philox(U4{gid, gstep0 + (uint32_t)t, 1u, (uint32_t)(c >> 1)}, E.key0, E.key1);
-      a0 = 2.0f * u01((c & 1) ? r.z : r.x) - 1.0f;
-      a1 = 2.0f * u01((c & 1) ? r.w : r.y) - 1.0f;
-      if (O.act && valid) {
-        O.act[(2 * c) * TN + ti] = a0;
-        O.act[(2 * c + 1) * TN + ti] = a1;
+      a0 = acts ? 2.0f * u01((c & 1) ? r.z : r.x) - 1.0f : 0.0f;
+      a1 = acts ? 2.0f * u01((c & 1) ? r.w : r.y) - 1.0f : 0.0f;
+      if (O.act && valid && acts) {
+        O.act[ra0 * TN + ti] = a0;
+        O.act[ra1 * TN + ti] = a1;
       }
     }
-    float tf, tm, usq;
-    quad::wrench(Tf, Tm, a0, a1, X.u0, X.u1, tf, tm, usq);
+    float tf, tm, usq = 0.0f, uf = 0.0f, ut = 0.0f;
+    if (PAPER) {
+      uf = fminf(fmaxf(a0, -1.0f), 1.0f);
+      ut = fminf(fmaxf(a1, -1.0f), 1.0f);
+      tf = E.tk.f_max * uf;
+      tm = E.tk.tau_max * ut;
+    } else {
+      quad::wrench(Tf, Tm, a0, a1, X.u0, X.u1, tf, tm, usq);
+    }
     const float tfi = tf * M.iMlin;
     for (int s = 0; s < E.substeps; ++s) quad::rk4(K, M, tfi, tm, E.h, X.p, X.q, X.v, X.om);
     X.ep += 1;
-    float pr, qr, dist;
+    float pr, qr, dist, reward;
     quad::reference(E, K, F, X.ep, pr, qr);
-    quad::QRefCols rc = quad::ref_columns(K, qr);
-    quad::observe(K, X.p, X.q, pr, rc, X.ob, dist);
-    const float theta = quad::attitude_error(K, X.q, qr);
-    const float reward = -dist - 0.5f * theta - 0.01f * usq;
+    quad::QRefCols rc;
+    if (PAPER) {
+      quad::observe_paper(K, X.p, X.q, pr, qr, X.ob, dist);
+      reward = quad::paper_reward(E.tk, dc, X.ob, X.om, uf, ut, X.u0, X.u1);
+      X.u0 = __builtin_fmaf(E.tk.beta, X.u0, (1.0f - E.tk.beta) * uf);
+      X.u1 = __builtin_fmaf(E.tk.beta, X.u1, (1.0f - E.tk.beta) * ut);
+    } else {
+      rc = quad::ref_columns(K, qr);
+      quad::observe(K, X.p, X.q, pr, rc, X.ob, dist);
+      const float theta = quad::attitude_error(K, X.q, qr);
+      reward = -dist - 0.5f * theta - 0.01f * usq;
+    }
     const bool done = (X.ep == E.H);
     if (done) {   // the whole quad
       float dist0;
-      quad::new_episode(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist0);
+      quad::new_episode<PAPER>(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist0);
     }
     if (O.stats_work) {   // reward, done and dist are the same in the four lanes of a quad
       const float sr = wave_sum_quads(valid ? reward : 0.0f);
@@ -169,7 +211,7 @@ __global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, ui
     }
     if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)(t + 1) * N + i, c, X);
   }
-  if (valid) quad::store_env(E, c, i, X);
+  if (valid) quad::store_env<PAPER>(E, c, i, X);
 }
 
 // stats[s][t] = sum over groups g of work[s][g][t].  A block covers 64 consecutive (s, t)
@@ -280,7 +322,9 @@ int compute_units() {
 // (n <= 32 envs per SIMD, four SIMDs per CU).
 static bool env_loop_is_quad(int n) { return n <= 32 * 4 * compute_units(); }
 
-int env_loop_stats_groups(int n) { return env_loop_is_quad(n) ? (n + 15) / 16 : groups_of(n); }
+int env_loop_stats_groups(const EnvArgs& E) {
+  return (E.task == TASK_PAPER || env_loop_is_quad(E.n)) ? (E.n + 15) / 16 : groups_of(E.n);
+}
 
 }  // namespace auv
 
@@ -342,6 +386,8 @@ int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buff
   std::memcpy(V.lin_damp, veh->lin_damp, sizeof V.lin_damp);
   std::memcpy(V.quad_damp, veh->quad_damp, sizeof V.quad_damp);
   V.BmW = veh->B - veh->W;
+  V.B = veh->B;
+  V.W = veh->W;
   for (int k = 0; k < 3; ++k) V.Brb[k] = veh->B * veh->r_b[k];
   V.f_max = veh->f_max;
   std::memcpy(V.alloc, veh->alloc, sizeof V.alloc);
@@ -361,6 +407,8 @@ int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buff
   E.flags = cfg->flags;
   E.env_offset = cfg->env_offset;
   E.sync_polls = AUV_DEFAULT_SYNC_POLLS;
+  E.task = TASK_WORKLOAD;
+  E.tk = TaskArgs{};
   e->global_step = 0;
   *out = e;
   return AUV_OK;
@@ -377,6 +425,42 @@ int auv_set_global_step(auv_env* env, int64_t step) {
   if (!env) return set_error(AUV_EINVAL, "auv_set_global_step: NULL handle");
   if (step < 0) return set_error(AUV_EINVAL, "auv_set_global_step: negative step");
   env->global_step = step;
+  return AUV_OK;
+}
+
+int auv_set_task(auv_env* env, const auv_task* t) {
+  if (!env || !t) return set_error(AUV_EINVAL, "auv_set_task: NULL argument");
+  if (t->kind == AUV_TASK_WORKLOAD) {
+    env->E.task = TASK_WORKLOAD;
+    return AUV_OK;
+  }
+  if (t->kind != AUV_TASK_PAPER) return set_error(AUV_EINVAL, "auv_set_task: unknown task kind %d", t->kind);
+  if (env->E.flags & (F_DR | F_CURRENT | F_LISSAJOUS))
+    return set_error(AUV_EINVAL, "auv_set_task: the paper task has no DR / CURRENT / LISSAJOUS flags");
+  const float w[9] = {t->w_pos, t->d_pos[0], t->d_pos[1], t->d_pos[2], t->w_att, t->w_act, t->w_vel, t->w_mavg, t->gamma_span};
+  for (float x : w)
+    if (!(x >= 0.0f) || !std::isfinite(x)) return set_error(AUV_EINVAL, "auv_set_task: weights and spans must be finite and >= 0");
+  if (!(t->f_max > 0.0f) || !(t->tau_max > 0.0f) || !std::isfinite(t->f_max) || !std::isfinite(t->tau_max))
+    return set_error(AUV_EINVAL, "auv_set_task: f_max and tau_max must be finite and > 0");
+  if (!(t->beta >= 0.0f && t->beta < 1.0f)) return set_error(AUV_EINVAL, "auv_set_task: beta must be in [0, 1)");
+  if (!(t->gamma_lo > 0.0f) || !std::isfinite(t->gamma_lo)) return set_error(AUV_EINVAL, "auv_set_task: gamma_lo must be > 0");
+  if (!(t->euler_max >= 0.0f && t->euler_max <= 3.14159274f))
+    return set_error(AUV_EINVAL, "auv_set_task: euler_max must be in [0, pi]");
+  TaskArgs& k = env->E.tk;
+  k.f_max = t->f_max;
+  k.tau_max = t->tau_max;
+  k.w_pos = t->w_pos;
+  for (int j = 0; j < 3; ++j) k.d_pos[j] = t->d_pos[j];
+  k.w_att = t->w_att;
+  k.w_act = t->w_act;
+  k.w_vel = t->w_vel;
+  k.w_mavg = t->w_mavg;
+  k.beta = t->beta;
+  k.g_lo = t->gamma_lo;
+  k.g_span = t->gamma_span;
+  k.eul_lo = -t->euler_max;
+  k.eul_span = 2.0f * t->euler_max;
+  env->E.task = TASK_PAPER;
   return AUV_OK;
 }
 
@@ -400,12 +484,18 @@ static int launch_env_loop(auv_env* env, int T, int mode, const StepOut& O, hipS
   const int n = env->E.n;
   const uint32_t g0 = (uint32_t)(env->global_step & 0xffffffffu);
   const bool ext = (mode == AUV_ACT_EXTERNAL);
-  if (env_loop_is_quad(n)) {
+  if (env->E.task == TASK_PAPER) {
     const dim3 grid((n + 15) / 16);
     if (ext)
-      hipLaunchKernelGGL(k_env_quad<true>, grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+      hipLaunchKernelGGL((k_env_quad<true, true>), grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
     else
-      hipLaunchKernelGGL(k_env_quad<false>, grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+      hipLaunchKernelGGL((k_env_quad<false, true>), grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+  } else if (env_loop_is_quad(n)) {
+    const dim3 grid((n + 15) / 16);
+    if (ext)
+      hipLaunchKernelGGL((k_env_quad<true, false>), grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
+    else
+      hipLaunchKernelGGL((k_env_quad<false, false>), grid, dim3(64), 0, s, env->veh, env->E, T, g0, O);
   } else {
     const dim3 grid(groups_of(n));
     if (ext)
@@ -433,7 +523,7 @@ int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_
   hipStream_t s = (hipStream_t)stream;
   if (int rc = launch_env_loop(env, 1, mode, O, s)) return rc;
   if (stats)
-    if (int rc = launch_stats_reduce(stats_work, 1, env_loop_stats_groups(env->E.n), stats, s)) return rc;
+    if (int rc = launch_stats_reduce(stats_work, 1, env_loop_stats_groups(env->E), stats, s)) return rc;
   env->global_step += 1;
   return AUV_OK;
 }
@@ -467,7 +557,7 @@ int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const 
     O.stats_work = rb->stats_work;
     if (int rc = launch_env_loop(env, T, mode, O, s)) return rc;
     if (rb->stats)
-      if (int rc = launch_stats_reduce(rb->stats_work, T, env_loop_stats_groups(env->E.n), rb->stats, s)) return rc;
+      if (int rc = launch_stats_reduce(rb->stats_work, T, env_loop_stats_groups(env->E), rb->stats, s)) return rc;
   } else if (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE) {
     if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
     if (rb->stats)   // one partial per wave of 16 environments

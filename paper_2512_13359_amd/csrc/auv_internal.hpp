@@ -36,7 +36,7 @@ inline int stats_groups(int n) { return 4 * groups_of(n); }
 // partials the policy rollout actually writes for n envs (<= stats_groups(n))
 int rollout_stats_groups(int n);
 // partials the random / external environment loop writes for n envs (<= stats_groups(n))
-int env_loop_stats_groups(int n);
+int env_loop_stats_groups(const EnvArgs& E);
 // compute units of the current device (256 if the query fails)
 int compute_units();
 

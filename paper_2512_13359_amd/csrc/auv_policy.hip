@@ -56,6 +56,23 @@ __device__ __forceinline__ void put_obs_quad(RolloutShared& S, int nt, int r, in
   put(16 + 2 * c, u1);
 }
 
+// The paper task's 12 observation features (rows 0-2 dp_b, 3-5 rotation vector, 6-8 v, 9-11
+// omega); the other operand elements stay zero.
+__device__ __forceinline__ void put_obs_quad_paper(RolloutShared& S, int nt, int r, int c, const quad::QObs& o,
+                                                   float v, float om) {
+  __bf16* xs = reinterpret_cast<__bf16*>(&S.x[0][0]);
+  auto put = [&](int k, float x) {
+    const int g = (k >> 2) & 3, j = 4 * (k >> 4) + (k & 3);
+    xs[((nt * 64 + 16 * g + r) << 3) + j] = (__bf16)x;
+  };
+  if (c < 3) {
+    put(c, o.dpb);
+    put(3 + c, o.c0);
+    put(6 + c, v);
+    put(9 + c, om);
+  }
+}
+
 // Point-to-point ordering between the waves of a workgroup through LDS counters: the
 // producer's LDS writes complete before its count is raised; the consumer polls (each poll
 // is an LDS round trip, a few VALU slots).  Every wait is bounded (EnvArgs::sync_polls,
@@ -114,7 +131,7 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
 // quad_env.hpp).  Each tile runs its own chain obs -> MLP -> action -> physics -> obs,
 // ordered by LDS counters instead of workgroup barriers, so the physics of one tile
 // overlaps the MLP of the others; with four tiles every SIMD holds one wave of each kind.
-template <bool SAMPLE, int TPW>
+template <bool SAMPLE, int TPW, bool PAPER>
 __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
                                                            StepOut O, const uint16_t* __restrict__ w,
                                                            const float* __restrict__ b,
@@ -145,11 +162,15 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   quad::QEnv X;
   quad::QModel M;
   quad::QRef F;
-  quad::load_env(V, E, K, i, valid, X, M, F);
+  quad::load_env<PAPER>(V, E, K, i, valid, X, M, F);
+  // action rows of this lane: (2c, 2c+1), or (c, 3+c) for lanes 0-2 of the paper task
+  const int ra0 = PAPER ? c : 2 * c, ra1 = PAPER ? 3 + c : 2 * c + 1;
+  const bool acts = !PAPER || c < 3;
+  const float dc = quad::pick(K, E.tk.d_pos[0], E.tk.d_pos[1], E.tk.d_pos[2], 0.0f);
   float lsd0 = 0.0f, lsd1 = 0.0f, sig0 = 0.0f, sig1 = 0.0f;
-  if (SAMPLE) {
-    lsd0 = log_std[2 * c];
-    lsd1 = log_std[2 * c + 1];
+  if (SAMPLE && acts) {
+    lsd0 = log_std[ra0];
+    lsd1 = log_std[ra1];
     sig0 = expf(lsd0);
     sig1 = expf(lsd1);
   }
@@ -159,11 +180,16 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   store_traj(0);
   StatsBuf SB{};
   // terms of the previous step's reward, finished in the next step's policy wait
-  float pv_q = 0.0f, pv_qr = 0.0f, pv_dist = 0.0f, pv_usq = 0.0f;
+  float pv_q = 0.0f, pv_qr = 0.0f, pv_dist = 0.0f, pv_usq = 0.0f, pv_reward = 0.0f;
   bool pv_done = false;
   auto finish_step = [&](int t1) {   // reward, outputs and statistics of step t1
-    const float theta = quad::attitude_error(K, pv_q, pv_qr);
-    const float reward = -pv_dist - 0.5f * theta - 0.01f * pv_usq;
+    float reward;
+    if (PAPER) {
+      reward = pv_reward;              // computed with the step (it needs the pre-step moving average)
+    } else {
+      const float theta = quad::attitude_error(K, pv_q, pv_qr);
+      reward = -pv_dist - 0.5f * theta - 0.01f * pv_usq;
+    }
     const size_t t1i = (size_t)t1 * N + (size_t)i;
     if (valid && c == 0) {
       if (O.reward) O.reward[t1i] = reward;
@@ -176,7 +202,10 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       stats_park(SB, O.stats_work, T, t1, lane, TPW * blockIdx.x + k, TPW * gridDim.x, sr, sd, sp);
     }
   };
-  put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
+  if (PAPER)
+    put_obs_quad_paper(S, k, slot, c, X.ob, X.v, X.om);
+  else
+    put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
   publish(&S.obs_ready[k], lane);
   for (int t = 0; t < T; ++t) {
     const size_t ti = (size_t)t * N + (size_t)i;
@@ -187,16 +216,33 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     quad::rhs(K, M, 0.0f, 0.0f, X.q, X.v, X.om, dp1, dq1, dv1, dw1);
     float pr, qr;
     quad::reference(E, K, F, X.ep + 1, pr, qr);
-    quad::QRefCols rc = quad::ref_columns(K, qr);
+    quad::QRefCols rc;
+    if (!PAPER) rc = quad::ref_columns(K, qr);
     if (t > 0) finish_step(t - 1);
-    if (O.obs && valid) quad::store_obs(O.obs, TN, ti, c, X);   // o_t, recorded while the MLP waves work on it
+    if (O.obs && valid) quad::store_obs<PAPER>(O.obs, TN, ti, c, X, false);   // o_t, recorded while the MLP waves work on it
     if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1), E.sync_polls)) {   // abandoned: poison
       X.p = X.q = X.v = X.om = __builtin_nanf("");
       break;
     }
     // policy output for this lane's two action components (fixed-order partial sums)
     float a0, a1;
-    {
+    if (PAPER) {          // rows c and 3 + c (lane 3: none)
+      const int r0 = acts ? ra0 : 0, r1 = acts ? ra1 : 0;
+      float m0[ROLLOUT_MLP_WAVES], m1[ROLLOUT_MLP_WAVES];
+#pragma unroll
+      for (int ww = 0; ww < ROLLOUT_MLP_WAVES; ++ww) {
+        m0[ww] = S.mu[k][ww][slot][r0];
+        m1[ww] = S.mu[k][ww][slot][r1];
+      }
+      float s0 = m0[0], s1 = m1[0];
+#pragma unroll
+      for (int ww = 1; ww < ROLLOUT_MLP_WAVES; ++ww) {
+        s0 += m0[ww];
+        s1 += m1[ww];
+      }
+      a0 = acts ? S.b3[r0] + s0 : 0.0f;
+      a1 = acts ? S.b3[r1] + s1 : 0.0f;
+    } else {
       float2 mm[ROLLOUT_MLP_WAVES];
 #pragma unroll
       for (int ww = 0; ww < ROLLOUT_MLP_WAVES; ++ww)
@@ -221,17 +267,22 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       const float rad = sqrtf(-2.0f * logf(u01_open0(w0)));
       float sn, cs;
       sincos_turns(u01(w1), &sn, &cs);
-      e0 = rad * cs;
-      e1 = rad * sn;
+      e0 = acts ? rad * cs : 0.0f;
+      e1 = acts ? rad * sn : 0.0f;
       a0 = __builtin_fmaf(sig0, e0, a0);
       a1 = __builtin_fmaf(sig1, e1, a1);
     }
-    if (O.act && valid) {
-      O.act[(2 * c) * TN + ti] = a0;
-      O.act[(2 * c + 1) * TN + ti] = a1;
+    if (O.act && valid && acts) {
+      O.act[ra0 * TN + ti] = a0;
+      O.act[ra1 * TN + ti] = a1;
     }
-    float tf, tm, usq;
-    {
+    float tf, tm, usq = 0.0f, uf = 0.0f, ut = 0.0f;
+    if (PAPER) {
+      uf = fminf(fmaxf(a0, -1.0f), 1.0f);
+      ut = fminf(fmaxf(a1, -1.0f), 1.0f);
+      tf = E.tk.f_max * uf;
+      tm = E.tk.tau_max * ut;
+    } else {
       float Tf[8], Tm[8];
       quad::alloc_rows(S.alloc, c, Tf, Tm);
       quad::wrench(Tf, Tm, a0, a1, X.u0, X.u1, tf, tm, usq);
@@ -243,25 +294,36 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     }
     X.ep += 1;
     float dist;
-    quad::observe(K, X.p, X.q, pr, rc, X.ob, dist);
+    if (PAPER) {
+      quad::observe_paper(K, X.p, X.q, pr, qr, X.ob, dist);
+      pv_reward = quad::paper_reward(E.tk, dc, X.ob, X.om, uf, ut, X.u0, X.u1);
+      X.u0 = __builtin_fmaf(E.tk.beta, X.u0, (1.0f - E.tk.beta) * uf);
+      X.u1 = __builtin_fmaf(E.tk.beta, X.u1, (1.0f - E.tk.beta) * ut);
+    } else {
+      quad::observe(K, X.p, X.q, pr, rc, X.ob, dist);
+    }
     const bool done = (X.ep == E.H);
     pv_q = X.q;
     pv_qr = qr;
     pv_dist = dist;
     pv_usq = usq;
     pv_done = done;
-    if (done) quad::new_episode(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist);   // the whole quad
-    put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
+    if (done) quad::new_episode<PAPER>(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist);   // the whole quad
+    if (PAPER)
+      put_obs_quad_paper(S, k, slot, c, X.ob, X.v, X.om);
+    else
+      put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
     publish(&S.obs_ready[k], lane);
     // outputs of step t that the next observation does not need
-    if (SAMPLE && O.logp) {
-      const float lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) - 4.0f * 1.83787706640934548f;
+    if (SAMPLE && O.logp) {   // lane 3 of the paper task adds zeros
+      const float lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) -
+                       (PAPER ? 3.0f : 4.0f) * 1.83787706640934548f;
       if (valid && c == 0) O.logp[ti] = lp;
     }
     store_traj(t + 1);
   }
   if (T > 0) finish_step(T - 1);
-  if (valid) quad::store_env(E, c, i, X);
+  if (valid) quad::store_env<PAPER>(E, c, i, X);
 }
 
 // Stand-alone MLP forward over obs [23][n] -> out [n_out][n]: workgroups of four MLP waves
@@ -371,19 +433,19 @@ int rollout_stats_groups(int n) {
   return tpw * ((n + 16 * tpw - 1) / (16 * tpw));
 }
 
-template <bool SAMPLE>
+template <bool SAMPLE, bool PAPER>
 static void launch_rollout_kernel(int tpw, int n, hipStream_t s, const VehArgs& V, const EnvArgs& E, int T, uint32_t g0,
                                   const StepOut& O, const uint16_t* w, const float* b, const float* log_std) {
   const dim3 grid((n + 16 * tpw - 1) / (16 * tpw));
   if (tpw == 4)
-    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 4>), grid, dim3(rollout_threads<4>()), 0, s, V, E, T, g0, O, w, b,
-                       log_std);
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 4, PAPER>), grid, dim3(rollout_threads<4>()), 0, s, V, E, T, g0, O,
+                       w, b, log_std);
   else if (tpw == 2)
-    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 2>), grid, dim3(rollout_threads<2>()), 0, s, V, E, T, g0, O, w, b,
-                       log_std);
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 2, PAPER>), grid, dim3(rollout_threads<2>()), 0, s, V, E, T, g0, O,
+                       w, b, log_std);
   else
-    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 1>), grid, dim3(rollout_threads<1>()), 0, s, V, E, T, g0, O, w, b,
-                       log_std);
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 1, PAPER>), grid, dim3(rollout_threads<1>()), 0, s, V, E, T, g0, O,
+                       w, b, log_std);
 }
 
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, const auv_mlp* value,
@@ -413,10 +475,15 @@ int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, 
   const uint32_t g0 = (uint32_t)(env->global_step & 0xffffffffu);
   const int tpw = rollout_tiles_per_group(n);
   const uint16_t* w = (const uint16_t*)policy->w;
-  if (sample)
-    launch_rollout_kernel<true>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
+  const bool paper = env->E.task == TASK_PAPER;
+  if (sample && paper)
+    launch_rollout_kernel<true, true>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
+  else if (sample)
+    launch_rollout_kernel<true, false>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
+  else if (paper)
+    launch_rollout_kernel<false, true>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
   else
-    launch_rollout_kernel<false>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
+    launch_rollout_kernel<false, false>(tpw, n, s, env->veh, env->E, T, g0, O, w, policy->b, policy->log_std);
   if (int rc = check_launch("policy rollout")) return rc;
   if (value) {
     // V(o_t) for every recorded observation, then the bootstrap value V(o_T)

@@ -93,7 +93,10 @@ __device__ __forceinline__ float pick(const QK& K, float x0, float x1, float x2,
   return __builtin_fmaf(w0, x0, __builtin_fmaf(w1, x1, __builtin_fmaf(w2, x2, (1.0f - K.m3) * x3)));
 }
 
-// Scalar (one-lane) parameters -> this lane's model and reference constants.
+// Scalar (one-lane) parameters -> this lane's model and reference constants.  PAPER: the
+// paper task's weight gamma W (gamma in parameter row 13) and the buoyancy centre at the
+// centre of gravity (no restoring moment).
+template <bool PAPER = false>
 __device__ __forceinline__ void make_lane_consts(const VehArgs& V, const QK& K, const Params& P, QModel& M,
                                                  QRef& F) {
   Model S;
@@ -107,7 +110,7 @@ __device__ __forceinline__ void make_lane_consts(const VehArgs& V, const QK& K, 
   M.KA2n = -(c0(S.Mlin) * c1(S.iMlin));
   M.DLi = c0(S.DL) * M.iMlin;
   M.DQi = c0(S.DQ) * M.iMlin;
-  M.BmWi = V.BmW * M.iMlin;
+  M.BmWi = (PAPER ? __builtin_fmaf(-P.amp[0], V.W, V.B) : V.BmW) * M.iMlin;
   M.Mang = c0(S.Mang);
   M.iMang = c0(S.iMang);
   M.A1 = c0(S.A1);
@@ -116,8 +119,8 @@ __device__ __forceinline__ void make_lane_consts(const VehArgs& V, const QK& K, 
   M.cw = c0(P.cw);
   M.cw1 = c1(P.cw);
   M.cw2 = c2(P.cw);
-  M.Brb1 = c1(V.Brb);
-  M.Brb2n = -c2(V.Brb);
+  M.Brb1 = PAPER ? 0.0f : c1(V.Brb);
+  M.Brb2n = PAPER ? 0.0f : -c2(V.Brb);
   constexpr float INV_2PI = 0.159154943091895336f, INV_4PI = 0.0795774715459476679f;
   F.pg = pick(K, P.pg[0], P.pg[1], P.pg[2], 0.0f);
   F.amp = pick(K, P.amp[0], P.amp[1], P.amp[2], 0.0f);
@@ -274,6 +277,35 @@ __device__ __forceinline__ float attitude_error(const QK& K, float q, float qr) 
   return 2.0f * atan2f(sqrtf(qsum(vec * vec)), fabsf(ew));
 }
 
+// Observation of the paper task: body-frame position error and the rotation vector of
+// q_err = q^* (x) q_ref (shortest rotation: the sign of the scalar part folded in), this
+// lane's components in o.dpb and o.c0; |dp| in dist.
+__device__ __forceinline__ void observe_paper(const QK& K, float p, float q, float pr, float qr, QObs& o,
+                                              float& dist) {
+  const QRot R = qrot(K, q);
+  o.dpb = rot_T(R, pr - p);
+  const float e = R.e, er = qr * K.m3;
+  const float wr = dpp<BC3>(qr);
+  const float ew = qsum(q * qr);                                   // scalar part of q_err
+  const float vec = __builtin_fmaf(R.wb, er, -wr * e) - cross(e, perm(er));
+  const float n = sqrtf(qsum(vec * vec)), aw = fabsf(ew);
+  const float k = n > 0.0f ? 2.0f * atan2f(n, aw) / n : 2.0f / aw;
+  o.c0 = (ew < 0.0f ? -k : k) * vec;
+  o.c1 = 0.0f;
+  dist = sqrtf(qsum(o.dpb * o.dpb));
+}
+
+// Reward of the paper task from the post-step observation (dp_b, rotation vector, omega),
+// this lane's clipped force / torque commands (uf, ut: components c and 3 + c) and their
+// moving averages before this step (af, at); lane 3 holds zeros.  dc = D_c.
+__device__ __forceinline__ float paper_reward(const TaskArgs& T, float dc, const QObs& o, float om, float uf,
+                                              float ut, float af, float at) {
+  const float dpw = dc * o.dpb, df = uf - af, dt = ut - at;
+  const float pos = qsum(dpw * dpw), att = qsum(o.c0 * o.c0), act = qsum(ut * ut), vel = qsum(om * om);
+  const float mavg = qsum(__builtin_fmaf(df, df, dt * dt));
+  return -T.w_pos * pos - T.w_att * att - T.w_act * act - T.w_vel * vel - T.w_mavg * mavg;
+}
+
 // Clip this lane's two actions, broadcast all eight across the quad, body wrench with
 // this lane's force and moment rows Tf, Tm of the allocation table (f_max folded in).
 __device__ __forceinline__ void wrench(const float Tf[8], const float Tm[8], float a0, float a1, float& u0,
@@ -326,7 +358,10 @@ struct QEnv {
 };
 
 // Buffers of environment i -> lane; an idle environment (i >= n) gets a harmless dummy
-// vehicle at rest that is stepped but never stored.
+// vehicle at rest that is stepped but never stored.  PAPER: observation rows 0-2 dp_b, 3-5
+// rotation vector, 6-8 v, 9-11 omega, 12-14 / 15-17 the moving averages of the force /
+// torque commands (state, kept in u0 / u1 of lanes 0-2).
+template <bool PAPER = false>
 __device__ __forceinline__ void load_env(const VehArgs& V, const EnvArgs& E, const QK& K, int i, bool valid,
                                          QEnv& X, QModel& M, QRef& F) {
   const int c = K.c, cv = c < 3 ? c : 0;   // cv: a valid row for lane 3's loads
@@ -342,9 +377,15 @@ __device__ __forceinline__ void load_env(const VehArgs& V, const EnvArgs& E, con
     X.episode = E.episode[i];
     X.ob.dpb = c < 3 ? E.obs[cv * N + i] : 0.0f;
     X.ob.c0 = c < 3 ? E.obs[(3 + cv) * N + i] : 0.0f;
-    X.ob.c1 = c < 3 ? E.obs[(6 + cv) * N + i] : 0.0f;
-    X.u0 = E.obs[(15 + 2 * c) * N + i];
-    X.u1 = E.obs[(16 + 2 * c) * N + i];
+    if (PAPER) {
+      X.ob.c1 = 0.0f;
+      X.u0 = c < 3 ? E.obs[(12 + cv) * N + i] : 0.0f;
+      X.u1 = c < 3 ? E.obs[(15 + cv) * N + i] : 0.0f;
+    } else {
+      X.ob.c1 = c < 3 ? E.obs[(6 + cv) * N + i] : 0.0f;
+      X.u0 = E.obs[(15 + 2 * c) * N + i];
+      X.u1 = E.obs[(16 + 2 * c) * N + i];
+    }
   } else {
     X.p = X.v = X.om = X.u0 = X.u1 = 0.0f;
     X.q = c == 3 ? 1.0f : 0.0f;
@@ -353,11 +394,29 @@ __device__ __forceinline__ void load_env(const VehArgs& V, const EnvArgs& E, con
     P = Params{{1, 1, 1}, {0, 0, 0}, {0, 0, 0}, {1, 0, 0, 0}, {0, 0, 0}, {0, 0, 0}, {0, 0, 0}, 0, 0};
     X.ob = QObs{0, 0, 0};
   }
-  make_lane_consts(V, K, P, M, F);
+  make_lane_consts<PAPER>(V, K, P, M, F);
 }
 
-// The observation of X into rows k of obs[k * stride + at].
-__device__ __forceinline__ void store_obs(float* __restrict__ obs, size_t stride, size_t at, int c, const QEnv& X) {
+// The observation of X into rows k of obs[k * stride + at].  PAPER: the 12 observation
+// rows, then with `state` the moving-average rows 12-17, else zeros in rows 12-22.
+template <bool PAPER = false>
+__device__ __forceinline__ void store_obs(float* __restrict__ obs, size_t stride, size_t at, int c, const QEnv& X,
+                                          bool state = true) {
+  if (PAPER) {   // a record (state false) gets zeros in rows 12-22
+    if (c < 3) {
+      obs[c * stride + at] = X.ob.dpb;
+      obs[(3 + c) * stride + at] = X.ob.c0;
+      obs[(6 + c) * stride + at] = X.v;
+      obs[(9 + c) * stride + at] = X.om;
+      obs[(12 + c) * stride + at] = state ? X.u0 : 0.0f;
+      obs[(15 + c) * stride + at] = state ? X.u1 : 0.0f;
+      if (!state) obs[(18 + c) * stride + at] = 0.0f;
+    } else if (!state) {
+      obs[21 * stride + at] = 0.0f;
+      obs[22 * stride + at] = 0.0f;
+    }
+    return;
+  }
   if (c < 3) {
     obs[c * stride + at] = X.ob.dpb;
     obs[(3 + c) * stride + at] = X.ob.c0;
@@ -380,10 +439,11 @@ __device__ __forceinline__ void store_state(float* __restrict__ s, size_t stride
 }
 
 // Lane -> buffers of environment i (state, current observation, counters).
+template <bool PAPER = false>
 __device__ __forceinline__ void store_env(const EnvArgs& E, int c, int i, const QEnv& X) {
   const size_t N = (size_t)E.n;
   store_state(E.state, N, (size_t)i, c, X);
-  store_obs(E.obs, N, (size_t)i, c, X);
+  store_obs<PAPER>(E.obs, N, (size_t)i, c, X);
   if (c == 0) {
     E.ep_step[i] = X.ep;
     E.episode[i] = X.episode;
@@ -393,14 +453,18 @@ __device__ __forceinline__ void store_env(const EnvArgs& E, int c, int i, const 
 // Auto-reset of a finished episode (the whole quad calls it): fresh draws for the next
 // episode, step 0, previous action 0, and the observation of the new initial state
 // (pr, qr, rc: its reference).  The new parameters are stored at once.
+template <bool PAPER = false>
 __device__ __forceinline__ void new_episode(const VehArgs& V, const EnvArgs& E, const QK& K, uint32_t gid, int i,
                                             bool valid, QEnv& X, QModel& M, QRef& F, float& pr, float& qr,
                                             QRefCols& rc, float& dist) {
   X.episode += 1u;
   State xs;
   Params P;
-  reset_draws(E, gid, X.episode, xs, P);
-  make_lane_consts(V, K, P, M, F);
+  if (PAPER)
+    paper_reset_draws(E, gid, X.episode, xs, P);
+  else
+    reset_draws(E, gid, X.episode, xs, P);
+  make_lane_consts<PAPER>(V, K, P, M, F);
   if (valid && K.c == 0) store_params(E.params, E.n, i, P);
   X.ep = 0;
   X.p = pick(K, xs.p[0], xs.p[1], xs.p[2], 0.0f);
@@ -408,8 +472,12 @@ __device__ __forceinline__ void new_episode(const VehArgs& V, const EnvArgs& E, 
   X.v = X.om = 0.0f;
   X.u0 = X.u1 = 0.0f;
   reference(E, K, F, 0, pr, qr);
-  rc = ref_columns(K, qr);
-  observe(K, X.p, X.q, pr, rc, X.ob, dist);
+  if (PAPER) {
+    observe_paper(K, X.p, X.q, pr, qr, X.ob, dist);
+  } else {
+    rc = ref_columns(K, qr);
+    observe(K, X.p, X.q, pr, rc, X.ob, dist);
+  }
 }
 
 }  // namespace quad

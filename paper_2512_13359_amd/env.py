@@ -8,9 +8,29 @@ import torch
 from . import _abi as A
 
 
+def pad_to_kernel_layout(net: dict) -> dict:
+    """A 12-input or 6-output network in the 23-input / 8-output layout the kernels read:
+    zero W1 columns past the inputs, zero W3 rows, b3 entries and log_std past the outputs
+    (exactly the same function on the inputs it has)."""
+    W1 = np.asarray(net["W1"], np.uint16)
+    W3 = np.asarray(net["W3"], np.uint16)
+    out = dict(net)
+    if W1.shape[1] < 23:
+        out["W1"] = np.concatenate([W1, np.zeros((W1.shape[0], 23 - W1.shape[1]), np.uint16)], axis=1)
+    if 1 < W3.shape[0] < 8:
+        k = W3.shape[0]
+        out["W3"] = np.concatenate([W3, np.zeros((8 - k, W3.shape[1]), np.uint16)])
+        out["b3"] = np.concatenate([np.asarray(net["b3"], np.float32), np.zeros(8 - k, np.float32)])
+        if "log_std" in net:
+            out["log_std"] = np.concatenate([np.asarray(net["log_std"], np.float32)[:k], np.zeros(8 - k, np.float32)])
+    return out
+
+
 def upload_mlp(net: dict, device="cuda") -> dict:
     """Copy an MLP parameter dict (bf16 bits W1, W2, W3; fp32 b1, b2, b3; log_std) into
-    contiguous device buffers in the layout auv_mlp expects."""
+    contiguous device buffers in the layout auv_mlp expects (12-input / 6-output networks of
+    the paper task are padded, see pad_to_kernel_layout)."""
+    net = pad_to_kernel_layout(net)
     w = np.concatenate([np.asarray(net[k], np.uint16).ravel() for k in ("W1", "W2", "W3")])
     b = np.concatenate([np.asarray(net[k], np.float32).ravel() for k in ("b1", "b2", "b3")])
     n_out = int(np.asarray(net["W3"]).shape[0])
@@ -57,6 +77,11 @@ class AuvEnv:
     @global_step.setter
     def global_step(self, step: int):
         A.auv_set_global_step(self.handle, step)
+
+    def set_task(self, task: dict):
+        """Select the task (a dict for make_task, e.g. workloads.PAPER_TASK); before reset()."""
+        self._task = A.make_task(task)
+        A.auv_set_task(self.handle, self._task)
 
     def reset(self):
         A.auv_reset(self.handle)

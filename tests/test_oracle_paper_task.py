@@ -16,7 +16,7 @@ from oracle import paper_task as P
 def _env(n=16, **kw):
     cfg = dict(n_envs=n, seed=6, flags=0, episode_len=512, substeps=2, dt_control=0.05)
     cfg.update(kw)
-    e = P.PaperEnv(cfg, W.VEHICLE)
+    e = P.PaperEnv(cfg, W.VEHICLE, W.PAPER_TASK)
     e.reset()
     return e
 
@@ -68,10 +68,10 @@ def test_restoring_force_and_wrench_initial_accelerations():
     assert np.allclose(d[9], want, rtol=1e-12, atol=1e-15)
     assert abs(d[9, 1]) < 1e-12
     tau = np.zeros((6, 3))
-    tau[0], tau[3] = P.F_MAX, P.TAU_MAX
+    tau[0], tau[3] = e.tk.f_max, e.tk.tau_max
     d = dyn.rhs(x, tau, e.veh, e.c_w)
-    assert abs(d[7, 1] - P.F_MAX / (float(v["m"]) + float(v["added_mass"][0]))) < 1e-12
-    assert abs(d[10, 1] - P.TAU_MAX / (float(v["inertia"][0]) + float(v["added_mass"][3]))) < 1e-12
+    assert abs(d[7, 1] - e.tk.f_max / (float(v["m"]) + float(v["added_mass"][0]))) < 1e-12
+    assert abs(d[10, 1] - e.tk.tau_max / (float(v["inertia"][0]) + float(v["added_mass"][3]))) < 1e-12
 
 
 def test_reward_terms_closed_forms():
@@ -90,20 +90,20 @@ def test_reward_terms_closed_forms():
     r, d, s, obs = e.step(a)
     assert abs(r[0]) < 1e-30 and np.all(np.abs(obs[:, 0]) < 1e-15)   # gamma W = B up to rounding
     u1 = np.clip(a[:, 1], -1, 1)
-    want1 = (-P.W_POS * np.sum((P.D_POS * obs[0:3, 1]) ** 2) - P.W_ATT * np.sum(obs[3:6, 1] ** 2)
-             - P.W_VEL * np.sum(obs[9:12, 1] ** 2) - P.W_MAVG * np.sum(u1 ** 2))
+    want1 = (-e.tk.w_pos * np.sum((e.tk.d_pos * obs[0:3, 1]) ** 2) - e.tk.w_att * np.sum(obs[3:6, 1] ** 2)
+             - e.tk.w_vel * np.sum(obs[9:12, 1] ** 2) - e.tk.w_mavg * np.sum(u1 ** 2))
     assert abs(r[1] - want1) < 1e-12
-    assert abs(r[2] - (-P.W_ACT * 1.0 - P.W_MAVG * 1.0 - P.W_ATT * np.sum(obs[3:6, 2] ** 2)
-                       - P.W_VEL * np.sum(obs[9:12, 2] ** 2) - P.W_POS * np.sum((P.D_POS * obs[0:3, 2]) ** 2))) < 1e-12
-    assert np.allclose(e.abar[:, 2], (1 - P.BETA) * np.clip(a[:, 2], -1, 1))
+    assert abs(r[2] - (-e.tk.w_act * 1.0 - e.tk.w_mavg * 1.0 - e.tk.w_att * np.sum(obs[3:6, 2] ** 2)
+                       - e.tk.w_vel * np.sum(obs[9:12, 2] ** 2) - e.tk.w_pos * np.sum((e.tk.d_pos * obs[0:3, 2]) ** 2))) < 1e-12
+    assert np.allclose(e.abar[:, 2], (1 - e.tk.beta) * np.clip(a[:, 2], -1, 1))
     # env 3's position term dominates and uses D_z = 1.5
-    assert r[3] == pytest.approx(-P.W_POS * (1.5 * obs[2, 3]) ** 2 - P.W_ATT * np.sum(obs[3:6, 3] ** 2)
-                                 - P.W_VEL * np.sum(obs[9:12, 3] ** 2) - P.W_POS * np.sum(obs[0:2, 3] ** 2), rel=1e-12)
+    assert r[3] == pytest.approx(-e.tk.w_pos * (1.5 * obs[2, 3]) ** 2 - e.tk.w_att * np.sum(obs[3:6, 3] ** 2)
+                                 - e.tk.w_vel * np.sum(obs[9:12, 3] ** 2) - e.tk.w_pos * np.sum(obs[0:2, 3] ** 2), rel=1e-12)
     assert obs[2, 3] == pytest.approx(-0.3, abs=1e-3)
     # constant action for k steps: abar = u (1 - beta^k)
     for k in range(2, 6):
         e.step(a)
-        assert np.allclose(e.abar[:, 1], np.clip(a[:, 1], -1, 1) * (1 - P.BETA ** k), rtol=1e-12)
+        assert np.allclose(e.abar[:, 1], np.clip(a[:, 1], -1, 1) * (1 - e.tk.beta ** k), rtol=1e-12)
 
 
 def test_episode_end_and_reset():

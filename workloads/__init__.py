@@ -23,7 +23,7 @@ __all__ = [
     "FLAG_DR", "FLAG_CURRENT", "FLAG_LISSAJOUS", "FLAG_STAGGER", "FLAG_TRAJ_STATE",
     "MODE_EXTERNAL", "MODE_RANDOM", "MODE_POLICY_MEAN", "MODE_POLICY_SAMPLE",
     "CONFIGS", "config", "mlp_weights", "vehicle_variant", "random_states",
-    "PPO", "ppo_draws", "ppo_minibatch_idx",
+    "PPO", "ppo_draws", "ppo_minibatch_idx", "PAPER_TASK",
 ]
 
 # --- vehicle (fp32 values; every consumer promotes them exactly) -------------------
@@ -97,6 +97,11 @@ CONFIGS = {
                flags=FLAG_DR | FLAG_CURRENT | FLAG_STAGGER, mode=MODE_POLICY_SAMPLE,
                policy=True, value=True, gamma=0.99, lam=0.95),
 }
+# c6: the paper's own training task (12-D observation, 6-D wrench, five-term reward, gravity
+# randomisation) at the paper's training scale: 4096 envs, one 512-step episode.
+CONFIGS["c6"] = dict(name="c6", n_envs=4096, T=512, substeps=2, dt_control=0.05, seed=6, flags=0,
+                     mode=MODE_POLICY_MEAN, policy=True, value=False, episode_len=512)
+
 for _c in CONFIGS.values():
     _c.setdefault("episode_len", EPISODE_LEN)
     _c.setdefault("env_offset", 0)
@@ -190,3 +195,11 @@ def ppo_minibatch_idx(M: int, B: int, seed: int) -> np.ndarray:
     blocks = rng.permutation(M // 16)
     idx = (blocks[:, None] * 16 + np.arange(16)[None, :]).ravel()
     return idx[:B].astype(np.int32)
+
+
+# --- the paper task's constants (Sec. IV-B / IV-C; the values the paper leaves open are this
+# project's choice: wrench limits within the thrusters' envelope, reward weights) -----------
+PAPER_TASK = dict(kind=1, f_max=60.0, tau_max=10.0, w_pos=1.0, d_pos=(1.0, 1.0, 1.5), w_att=0.5,
+                  w_act=0.01, w_vel=0.05, w_mavg=0.1, beta=0.8, gamma_lo=0.95, gamma_span=0.1,
+                  euler_max=float(np.float32(math.pi / 3.0)))
+PAPER_POLICY_SEED = 9
