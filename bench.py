@@ -230,6 +230,61 @@ def paper_task_measure(reps: int = 3) -> dict:
     return out
 
 
+def paper_training_measure(reps: int = 2, epochs: int = 4, minibatch: int = 262144) -> dict:
+    """One PPO training iteration on the paper's own task at its training scale: a sampled
+    rollout of 4096 envs x one 512-step episode with the value head, GAE, then `epochs`
+    passes of minibatch updates (gradient + Adam) over the 2.1 M samples."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, PpoLearner
+    from paper_2512_13359_amd import _abi as A
+
+    cfg = W.config("c6")
+    n, T = cfg["n_envs"], cfg["T"]
+    M = n * T
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.set_task(W.PAPER_TASK)
+    env.reset()
+    P = W.PPO
+    L = PpoLearner(W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.VALUE_SEED, n_in=12),
+                   **{k: P[k] for k in ("clip_eps", "vf_coef", "ent_coef", "max_grad_norm", "lr", "beta1", "beta2",
+                                        "adam_eps", "normalize_adv")})
+    bufs = env.rollout_buffers(T, record=("obs", "act", "logp", "value", "reward", "done", "last_value"), value=True)
+    adv = torch.empty(T, n, device="cuda")
+    ret = torch.empty(T, n, device="cuda")
+    batch = L.batch(bufs["obs"].reshape(23, M), bufs["act"].reshape(8, M), bufs["logp"].reshape(M), adv.reshape(M),
+                    ret.reshape(M))
+    n_mb = M // minibatch
+    idx = [torch.from_numpy(W.ppo_minibatch_idx(M, M, seed=200 + e)).cuda() for e in range(epochs)]
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    times, parts = [], []
+    for k in range(reps + 1):
+        torch.cuda.synchronize()
+        e = [ev() for _ in range(4)]
+        e[0].record()
+        env.rollout(T, W.MODE_POLICY_SAMPLE, policy={"struct": L.pol.mlp}, value={"struct": L.val.mlp}, bufs=bufs)
+        e[1].record()
+        A.auv_gae(T, n, bufs["reward"], bufs["value"], bufs["done"], bufs["last_value"], 0.99, 0.95, adv, ret)
+        e[2].record()
+        for ep in range(epochs):
+            for j in range(n_mb):
+                L.update(batch, idx[ep][j * minibatch:(j + 1) * minibatch])
+        e[3].record()
+        torch.cuda.synchronize()
+        if k:
+            times.append(e[0].elapsed_time(e[3]) * 1e-3)
+            parts.append([e[i].elapsed_time(e[i + 1]) for i in range(3)])
+    st = L.stats.cpu().numpy()
+    assert (st == st).all(), "non-finite PPO statistics"
+    t = sorted(times)[len(times) // 2]
+    p = parts[times.index(t)]
+    return {"workload": f"paper task PPO iteration: {n} envs x {T}-step episode (sampled, value head), GAE, "
+                        f"{epochs} epochs x {n_mb} minibatches of {minibatch}",
+            "iteration_ms": t * 1e3, "rollout_ms": p[0], "gae_ms": p[1], "ppo_ms": p[2],
+            "hundred_episodes_s": 100 * t}
+
+
 def small_configs_measure(reps: int = 3) -> dict:
     """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
     4096 envs occupy 64 of the 256 CUs, so these are occupancy-capped by N."""
@@ -271,6 +326,7 @@ def main() -> int:
     ap.add_argument("--no-c5", action="store_true", help="skip the PPO-buffer (c5) rollout and GAE measurement")
     ap.add_argument("--no-ppo", action="store_true", help="skip the PPO-update measurement")
     ap.add_argument("--ppo-only", action="store_true", help="only measure the PPO update and print it")
+    ap.add_argument("--paper-only", action="store_true", help="only measure the paper task (c6, training iteration)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -296,6 +352,9 @@ def main() -> int:
     torch.cuda.set_device(0)
     if args.ppo_only:
         print(json.dumps({"ppo": ppo_measure()}), flush=True)
+        return 0
+    if args.paper_only:
+        print(json.dumps({"c6": paper_task_measure(), "paper_training": paper_training_measure()}), flush=True)
         return 0
     cfg = W.config(args.workload)
     n, T = cfg["n_envs"], cfg["T"]
@@ -370,6 +429,7 @@ def main() -> int:
     if not args.no_ppo and not args.no_c5:
         line["ppo"] = ppo_measure()
         line["c6"] = paper_task_measure()
+        line["paper_training"] = paper_training_measure()
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
     print(json.dumps(line), flush=True)

@@ -253,6 +253,9 @@ typedef struct {
   float max_grad_norm; /* global-norm clipping over both networks' gradients; <= 0: off */
   float lr, beta1, beta2, adam_eps; /* Adam (Kingma and Ba, Algorithm 1): lr > 0, 0 <= beta < 1, eps > 0 */
   int32_t normalize_adv;            /* nonzero: normalise advantages over the minibatch */
+  int32_t n_actions;                /* actions of the policy, 1..8 (0 means 8): the loss uses
+                                       outputs 0..n_actions-1; the others (zero padding) get zero
+                                       gradients, so a padded 6-action policy stays padded */
 } auv_ppo_config;
 
 /* The rollout buffer a minibatch is drawn from (device, fp32, M = T N samples; sample

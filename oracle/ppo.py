@@ -26,7 +26,7 @@ the bias gradients sum the unrounded values, and the tanh derivatives use the un
 activations.  Products are exact (float64).  With quantize=False every q is the identity.
 
 Parameter packing (the same as the device buffers): W1 [H][n_in] | W2 [H][H] | W3 [n_out][H]
-| b1 [H] | b2 [H] | b3 [n_out] | log_std [8] (policy only), row-major, float.
+| b1 [H] | b2 [H] | b3 [n_out] | log_std [n_out] (policy only), row-major, float.
 """
 from __future__ import annotations
 
@@ -53,7 +53,7 @@ def unpack(theta: np.ndarray, n_in: int, hidden: int, n_out: int, with_log_std: 
     shapes = [("W1", (hidden, n_in)), ("W2", (hidden, hidden)), ("W3", (n_out, hidden)),
               ("b1", (hidden,)), ("b2", (hidden,)), ("b3", (n_out,))]
     if with_log_std:
-        shapes.append(("log_std", (8,)))
+        shapes.append(("log_std", (n_out,)))
     out, o = {}, 0
     for k, s in shapes:
         n = int(np.prod(s))

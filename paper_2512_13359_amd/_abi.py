@@ -57,7 +57,8 @@ class AuvTask(ctypes.Structure):
 
 class AuvPpoConfig(ctypes.Structure):
     _fields_ = [("clip_eps", _f), ("vf_coef", _f), ("ent_coef", _f), ("max_grad_norm", _f), ("lr", _f),
-                ("beta1", _f), ("beta2", _f), ("adam_eps", _f), ("normalize_adv", ctypes.c_int32)]
+                ("beta1", _f), ("beta2", _f), ("adam_eps", _f), ("normalize_adv", ctypes.c_int32),
+                ("n_actions", ctypes.c_int32)]
 
 
 class AuvPpoBatch(ctypes.Structure):
@@ -251,8 +252,9 @@ def make_task(task: dict) -> AuvTask:
 
 
 def make_ppo_config(clip_eps=0.2, vf_coef=0.5, ent_coef=0.0, max_grad_norm=0.5, lr=3e-4, beta1=0.9,
-                    beta2=0.999, adam_eps=1e-8, normalize_adv=True) -> AuvPpoConfig:
-    return AuvPpoConfig(clip_eps, vf_coef, ent_coef, max_grad_norm, lr, beta1, beta2, adam_eps, int(bool(normalize_adv)))
+                    beta2=0.999, adam_eps=1e-8, normalize_adv=True, n_actions=8) -> AuvPpoConfig:
+    return AuvPpoConfig(clip_eps, vf_coef, ent_coef, max_grad_norm, lr, beta1, beta2, adam_eps, int(bool(normalize_adv)),
+                        n_actions)
 
 
 def make_ppo_batch(obs, act, logp, adv, ret, M: int) -> AuvPpoBatch:

@@ -45,6 +45,7 @@ struct Hp {
   float clip_eps, vf_coef, ent_coef, max_grad_norm;
   float inv_B;
   int normalize;
+  int n_act;    // policy outputs in the loss (the rest is zero padding)
 };
 
 struct Batch {
@@ -383,12 +384,13 @@ __global__ __launch_bounds__(64 * HID / FPW, 1) void k_fwd_bwd(const uint16_t* _
       float a[4], d[4], zz[4], part = 0.0f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        a[i] = (valid && g < 2) ? cur.a[i] : 0.0f;
-        d[i] = g < 2 ? a[i] - y[i] : 0.0f;
+        const bool used = g < 2 && 4 * g + i < hp.n_act;
+        a[i] = (valid && used) ? cur.a[i] : 0.0f;
+        d[i] = used ? a[i] - y[i] : 0.0f;
         zz[i] = d[i] * d[i] * ivar[i];
-        part += -0.5f * zz[i] - ls[i];
+        part += used ? -0.5f * zz[i] - ls[i] : 0.0f;
       }
-      const float logp = part + __shfl_xor(part, 16) - 4.0f * LOG_2PI;   // lanes r and r + 16
+      const float logp = part + __shfl_xor(part, 16) - 0.5f * (float)hp.n_act * LOG_2PI;   // lanes r and r + 16
       const bool lv = valid && g < 2;
       const float lpo = lv ? cur.lp : 0.0f;
       const float ah = lv ? (hp.normalize ? (cur.ad - mean) * inv_std : cur.ad) : 0.0f;
@@ -403,7 +405,7 @@ __global__ __launch_bounds__(64 * HID / FPW, 1) void k_fwd_bwd(const uint16_t* _
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           db3[i] += gy[i];
-          dls[i] += coef * (zz[i] - 1.0f);
+          dls[i] += 4 * g + i < hp.n_act ? coef * (zz[i] - 1.0f) : 0.0f;
         }
         if (lv && g == 0) {
           st[0] += -fminf(unc, clp);
@@ -683,7 +685,7 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
 // waves each sum a contiguous quarter of the workgroup partials with eight loads in flight,
 // then wave 0 adds the quarters in wave order.  G1: forward/backward groups (dW3, db2, db3,
 // d log_std), G2: dz1 groups (dW1, db1), G3: dW2 groups.
-__global__ __launch_bounds__(256) void k_reduce(int n_out, int G1, int G2, int G3, Work W, float ent_coef,
+__global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, int G2, int G3, Work W, float ent_coef,
                                                 float* __restrict__ grad, float* __restrict__ ss) {
   __shared__ float part[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -711,7 +713,7 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int G1, int G2, int G
     } else if ((q -= HID) < n_out) {
       src = W.part_b3 + q, stride = 16, G = G1;
     } else {
-      src = W.part_ls + (q - n_out), stride = 16, G = G1, add = -ent_coef;
+      src = W.part_ls + (q - n_out), stride = 16, G = G1, add = q - n_out < n_act ? -ent_coef : 0.0f;
     }
   }
   const int g0 = w * G / 4, g1 = (w + 1) * G / 4;
@@ -759,7 +761,7 @@ __global__ __launch_bounds__(64) void k_finalize(int G1p, int G1v, Work W, int n
   vs = wave_sum(vs);
   if (lane == 0) {
     float ent = 0.0f;
-    for (int j = 0; j < 8; ++j) ent += log_std[j] + 0.5f * (1.0f + LOG_2PI);
+    for (int j = 0; j < hp.n_act; ++j) ent += log_std[j] + 0.5f * (1.0f + LOG_2PI);
     stats[0] = pg * hp.inv_B;
     stats[1] = 0.5f * hp.vf_coef * vs * hp.inv_B;
     stats[2] = ent;
@@ -808,6 +810,7 @@ static int check_ppo_config(const auv_ppo_config* c) {
       !(c->beta2 >= 0.0f && c->beta2 < 1.0f) || !(c->adam_eps > 0.0f) || !std::isfinite(c->ent_coef) ||
       !std::isfinite(c->max_grad_norm))
     return set_error(AUV_EINVAL, "PPO: config out of range (clip_eps > 0, vf_coef >= 0, lr > 0, 0 <= betas < 1, adam_eps > 0)");
+  if (c->n_actions < 0 || c->n_actions > ACT) return set_error(AUV_EINVAL, "PPO: n_actions must be in [0, 8]");
   return AUV_OK;
 }
 
@@ -838,7 +841,8 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
   const int cus = std::min(compute_units(), ppo::MAX_GROUPS);
   const int G1 = std::min(cus, tiles), G3 = std::min(cus, steps / ppo::DW2_DEPTH);
   const ppo::Work W = ppo::work_at(work, B);
-  const ppo::Hp hp{cfg->clip_eps, cfg->vf_coef, cfg->ent_coef, cfg->max_grad_norm, 1.0f / (float)B, cfg->normalize_adv ? 1 : 0};
+  const ppo::Hp hp{cfg->clip_eps, cfg->vf_coef,       cfg->ent_coef, cfg->max_grad_norm, 1.0f / (float)B,
+                   cfg->normalize_adv ? 1 : 0, cfg->n_actions ? cfg->n_actions : ACT};
   const ppo::Batch D{batch->obs, batch->act, batch->logp, batch->adv, batch->ret, (size_t)batch->M};
   const int rb = ppo::red_blocks(ACT);
   if (hp.normalize) {
@@ -851,13 +855,13 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
                      B, tiles, hp, W, 0);
   hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, G1, G1, G3, W, cfg->ent_coef,
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G3, W, cfg->ent_coef,
                      grad_policy, W.part_ss);
   hipLaunchKernelGGL((ppo::k_fwd_bwd<1, FPW>), dim3(G1), dim3(TH), 0, s, value->w, value->b, (const float*)nullptr, D,
                      idx, B, tiles, hp, W, 1);
   hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, value->w, value->b, D, idx, B, tiles, W);
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, G1, G1, G3, W, 0.0f,
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, G1, G1, G3, W, 0.0f,
                      grad_value, W.part_ss + rb);
   hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, G1, G1, W, rb, ppo::red_blocks(1), rb, policy->log_std, hp,
                      stats);

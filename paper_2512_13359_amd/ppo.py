@@ -16,6 +16,9 @@ class PpoNet:
     read."""
 
     def __init__(self, net: dict, device="cuda"):
+        from .env import pad_to_kernel_layout
+        self.n_actions = int(np.asarray(net["W3"]).shape[0])   # before padding (6 for the paper task)
+        net = pad_to_kernel_layout(net)
         n_out = int(np.asarray(net["W3"]).shape[0])
         self.n_out = n_out
         self.nw = A.ppo_nw(n_out)
@@ -44,6 +47,7 @@ class PpoLearner:
     def __init__(self, policy: dict, value: dict, device="cuda", **hp):
         self.pol = PpoNet(policy, device)
         self.val = PpoNet(value, device)
+        hp.setdefault("n_actions", self.pol.n_actions)
         self.cfg = A.make_ppo_config(**hp)
         self.t = 0
         self.device = device

@@ -270,3 +270,97 @@ def test_ppo_training_loop_on_rollouts():
     env.rollout(T, W.MODE_POLICY_SAMPLE, policy={"struct": L.pol.mlp}, value={"struct": L.val.mlp}, bufs=bufs)
     r = host(bufs["reward"])
     assert np.all(np.isfinite(r))
+
+
+def _pad_grad(g: np.ndarray, n_in: int, n_out: int, policy: bool) -> np.ndarray:
+    """Gradient of a 12-input / 6-output network in the padded 23 / 8 device layout."""
+    p = oppo.unpack(g, n_in, 256, n_out, policy)
+    q = {"W1": np.zeros((256, 23)), "W2": p["W2"], "b1": p["b1"], "b2": p["b2"]}
+    q["W1"][:, :n_in] = p["W1"]
+    no = 8 if n_out > 1 else 1
+    q["W3"] = np.zeros((no, 256))
+    q["W3"][:n_out] = p["W3"]
+    q["b3"] = np.zeros(no)
+    q["b3"][:n_out] = p["b3"]
+    if policy:
+        q["log_std"] = np.zeros(8)
+        q["log_std"][:n_out] = p["log_std"]
+    return oppo.pack(q)
+
+
+def test_ppo_six_action_policy_of_the_paper_task():
+    """The paper task's 12-256-256-6 policy and 12-256-256-1 value net in the padded layout:
+    gradients against the oracle of the unpadded networks (padding entries exactly zero),
+    with NaN in the unused action rows and zeros in observation rows 12-22 (as a paper-task
+    rollout records them)."""
+    require_gpu()
+    announce("ppo six-action policy")
+    from paper_2512_13359_amd import PpoLearner
+    netp = W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12)
+    netv = W.mlp_weights(1, W.VALUE_SEED, n_in=12)
+    pol, val = _oracle_params(netp), _oracle_params(netv)
+    pol["log_std"] = np.asarray(netp["log_std"], np.float32)[:6].astype(np.float64)
+    M, B = 5000, 2000
+    d = W.ppo_draws(M, 21)
+    obs12 = d["obs"][:12]
+    mu, _ = oppo.mlp_forward_cache(obs12.astype(np.float64), pol, quantize=True)
+    act6 = (mu + np.exp(pol["log_std"])[:, None] * d["eps"][:6]).astype(np.float32)
+    logp = (oppo.gaussian_logp(act6.astype(np.float64), mu, pol["log_std"]) - np.log(d["ratio"])).astype(np.float32)
+    obs23 = np.zeros((23, M), np.float32)
+    obs23[:12] = obs12
+    act8 = np.full((8, M), np.nan, np.float32)
+    act8[:6] = act6
+    dev = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in (obs23, act8, logp, d["adv"], d["ret"])]
+    L = PpoLearner(netp, netv, ent_coef=0.01)
+    assert L.cfg.n_actions == 6
+    idx = W.ppo_minibatch_idx(M, B, seed=4)
+    L.grad(L.batch(*dev), torch.from_numpy(idx).cuda())
+    c = idx.astype(np.int64)
+    want = oppo.ppo_loss_grad(obs12[:, c], act6[:, c], logp[c], d["adv"][c], d["ret"][c], pol, val,
+                              dict(ent_coef=0.01), quantize=True)
+    gp, gv = host(L.pol.grad), host(L.val.grad)
+    wp, wv = _pad_grad(want["grad_pol"], 12, 6, True), _pad_grad(want["grad_val"], 12, 1, False)
+    pad_p = wp == 0.0
+    assert np.all(gp[pad_p] == 0.0) and np.all(gv[wv == 0.0] == 0.0)
+    _check_grads(gp, wp, 8, "policy")
+    _check_grads(gv, wv, 1, "value")
+    st = host(L.stats)
+    assert abs(st[2] - want["entropy"]) <= 1e-5 * abs(want["entropy"])
+    assert abs(st[0] - want["pg_loss"]) <= 2e-3 * max(1.0, abs(want["pg_loss"]))
+
+
+def test_ppo_training_loop_on_the_paper_task():
+    """Paper task end to end: sampled rollout with the value head, GAE, PPO updates of the
+    6-action policy; the loss falls on a fixed minibatch and the padding stays zero."""
+    require_gpu()
+    announce("ppo training loop on the paper task")
+    from paper_2512_13359_amd import AuvEnv, PpoLearner
+    from paper_2512_13359_amd import _abi as A
+    cfg = W.config("c6", n_envs=2048, T=32)
+    n, T = cfg["n_envs"], cfg["T"]
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.set_task(W.PAPER_TASK)
+    env.reset()
+    L = PpoLearner(W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.VALUE_SEED, n_in=12), lr=1e-3)
+    th0 = host(L.pol.theta).copy()
+    bufs = env.rollout_buffers(T, record=("obs", "act", "logp", "value", "reward", "done", "last_value"), value=True)
+    env.rollout(T, W.MODE_POLICY_SAMPLE, policy={"struct": L.pol.mlp}, value={"struct": L.val.mlp}, bufs=bufs)
+    adv = torch.empty(T, n, device="cuda")
+    ret = torch.empty(T, n, device="cuda")
+    A.auv_gae(T, n, bufs["reward"], bufs["value"], bufs["done"], bufs["last_value"], 0.99, 0.95, adv, ret)
+    M = T * n
+    batch = L.batch(bufs["obs"].reshape(23, M), bufs["act"].reshape(8, M), bufs["logp"].reshape(M), adv.reshape(M),
+                    ret.reshape(M))
+    fixed = torch.from_numpy(W.ppo_minibatch_idx(M, 8192, seed=0)).cuda()
+    L.grad(batch, fixed)
+    first = host(L.stats).copy()
+    assert abs(first[3]) < 1e-3
+    for _ in range(6):
+        L.update(batch, fixed)
+    L.grad(batch, fixed)
+    last = host(L.stats)
+    assert np.all(np.isfinite(last)) and last[0] + last[1] < first[0] + first[1]
+    th = host(L.pol.theta)
+    pad = th0 == 0.0
+    pad[:256 * 23] = (np.arange(256 * 23) % 23) >= 12          # W1 columns 12-22
+    assert np.all(th[pad & (th0 == 0.0)] == 0.0)
