@@ -22,8 +22,11 @@ Modules
             five-term reward with an action moving average, gravity randomisation
   ppo       clipped-surrogate PPO objective, its gradient through both MLPs (with the
             bf16 quantisation points of the MFMA path), global-norm clipping, Adam
+  shac      the SHAC actor objective over a short window of the paper task and its
+            gradient through the policy, reward, observation, RK4 + Fossen and the
+            terminal value (torch autograd on float64 tensors)
 
 Every function is pinned by a ``-m "not gpu"`` test against closed forms, invariants,
 special cases or an independent library; see the test files under ``tests/``.
 """
-from . import rng, dynamics, mlp, gae, env, ppo, paper_task  # noqa: F401
+from . import rng, dynamics, mlp, gae, env, ppo, paper_task, shac  # noqa: F401

@@ -23,7 +23,7 @@ __all__ = [
     "FLAG_DR", "FLAG_CURRENT", "FLAG_LISSAJOUS", "FLAG_STAGGER", "FLAG_TRAJ_STATE",
     "MODE_EXTERNAL", "MODE_RANDOM", "MODE_POLICY_MEAN", "MODE_POLICY_SAMPLE",
     "CONFIGS", "config", "mlp_weights", "vehicle_variant", "random_states",
-    "PPO", "ppo_draws", "ppo_minibatch_idx", "PAPER_TASK",
+    "PPO", "ppo_draws", "ppo_minibatch_idx", "PAPER_TASK", "SHAC",
 ]
 
 # --- vehicle (fp32 values; every consumer promotes them exactly) -------------------
@@ -203,3 +203,11 @@ PAPER_TASK = dict(kind=1, f_max=60.0, tau_max=10.0, w_pos=1.0, d_pos=(1.0, 1.0, 
                   w_act=0.01, w_vel=0.05, w_mavg=0.1, beta=0.8, gamma_lo=0.95, gamma_span=0.1,
                   euler_max=float(np.float32(math.pi / 3.0)))
 PAPER_POLICY_SEED = 9
+PAPER_VALUE_SEED = 10
+
+# --- SHAC on the paper task ----------------------------------------------------------
+# Short-horizon actor-critic windows (the differentiable-simulation learner of the paper):
+# h = 32 control steps per window (16 windows per 512-step episode), discount 0.99, the
+# actor gradient clipped to norm 1; the paper's best SHAC scale is 512 environments and its
+# main experiments use 4096.
+SHAC = dict(h=32, gamma=0.99, max_grad_norm=1.0, n_envs=4096, n_envs_small=512)
