@@ -298,11 +298,73 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
 
 /* One Adam step (t >= 1: steps so far, this one included) of both networks on the
  * gradients of auv_ppo_grad times stats[7]: rewrites theta, adam_m, adam_v and the bf16
- * weight copies (round to nearest even).  AUV_EINVAL, nothing enqueued, for t < 1, NULL or
- * misaligned pointers, wrong n_out, or a config out of range. */
+ * weight copies (round to nearest even).  Either network may be NULL (it is then left
+ * alone; its gradient is not read), not both.  AUV_EINVAL, nothing enqueued, for t < 1,
+ * NULL or misaligned pointers, wrong n_out, or a config out of range. */
 int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy,
                  const auv_ppo_net* value, const float* grad_policy, const float* grad_value,
                  const float* stats, void* stream);
+
+/* ---- SHAC: the actor gradient of one short window on the paper task -------------------
+ * Short-Horizon Actor-Critic (Xu et al. 2022; the differentiable-simulation learner of
+ * paper Sec. II-B, trained on the paper task of auv_set_task).  One window of h control
+ * steps of all N environments from their current state, with the policy in the loop:
+ *   a_t = mu(o_t) (+ exp(log_std) eps_t in sample mode, the noise stream of auv_rollout),
+ *   u_t = clip(a_t, -1, 1), s_{t+1} = the paper task's RK4 step, r_t its reward,
+ *   L = -(1 / (N h)) sum_i [ sum_{t<h} gamma^t r_t + gamma^h V(o(s_h)) ]
+ * and the gradient of L with respect to the policy parameters by reverse-mode
+ * differentiation through the reward, the observation, RK4 + Fossen (relative-velocity form
+ * without current; d|x|/dx = sign x), the clip (derivative 1 on [-1, 1], else 0) and the
+ * policy network (the terminal value is differentiated with respect to s_h; the value
+ * net is not trained here).  bf16 points: the forward's as auv_mlp; in the backward the
+ * cotangent of each layer's pre-activation is rounded to bf16 before it reaches the layer's
+ * weights, bias and input (bf16 MFMA, fp32 accumulation); tanh derivatives use fp32
+ * activations.  The state adjoint is carried in fp32.
+ *
+ * The window may end the episode only at its last step (the environments must not have
+ * staggered episodes, and (global_step mod H) + h <= H): there the terminal value is taken
+ * on the final state before the reset, and the environment then resets as in a rollout.
+ * Afterwards the environment buffers hold the window's end (or reset) state and
+ * global_step += h. */
+typedef struct {
+  int32_t h;            /* window length, 1 <= h <= min(64, H) control steps */
+  int32_t mode;         /* AUV_ACT_POLICY_SAMPLE, AUV_ACT_POLICY_MEAN or AUV_ACT_EXTERNAL */
+  float gamma;          /* discount, 0 < gamma <= 1 */
+  float max_grad_norm;  /* clipping factor stats[7] = min(1, c / (|grad| + 1e-6)); <= 0: 1 */
+} auv_shac_config;
+
+/* Window inputs and optional per-step outputs (device, caller-owned, [k][h][N] layouts). */
+typedef struct {
+  const float* actions; /* AUV_ACT_EXTERNAL: [8][h][N] actions before clipping (rows 0-5
+                           used); the objective is then a function of these actions */
+  float* obs;           /* [23][h][N] observation o_t each action was taken on (rows 12-22 0) */
+  float* act;           /* [8][h][N] a_t before clipping (rows 6-7 0) */
+  float* reward;        /* [h][N] r_t */
+  float* done;          /* [h][N] 1.0 where the episode ended (only possible at t = h - 1) */
+  float* grad_act;      /* [8][h][N] dL/da_t, the total derivative with respect to the action
+                           before the clip (rows 6-7 0); in policy modes also dL/dmu_t */
+  float* value_last;    /* [N] V(o(s_h)) on the final state before any reset (0 without a
+                           value net) */
+  float* grad_state0;   /* [13][N] dL/ds_0 */
+} auv_shac_buffers;
+
+/* Bytes of device workspace auv_shac_window needs for N environments and windows of h
+ * steps (-1 outside N in [1, 2^22], h in [1, 64]); about 2.3 KB per environment-step plus
+ * 90 MB. */
+int64_t auv_shac_work_bytes(int32_t n_envs, int32_t h);
+
+/* One SHAC window.  policy: the 23-256-256-8 network (a padded 12-256-256-6 net; log_std
+ * for sample mode), required except in external mode.  value: a 23-256-256-1 network or
+ * NULL (V = 0).  grad_policy: NULL or AUV_PPO_NPARAM(8) floats, overwritten with dL/dtheta
+ * in the packed layout of auv_ppo_grad (entries of padding rows and columns are 0); not
+ * allowed in external mode.  stats [8]: L, mean over envs of sum_t gamma^t r_t, mean V(o(s_h)),
+ * 0, 0, |grad|^2, 0, clipping factor (the input of auv_ppo_adam).  work:
+ * auv_shac_work_bytes(N, h) bytes, 16-byte aligned.  Deterministic (same inputs, same bits).
+ * AUV_EINVAL, nothing enqueued: a handle without the paper task, staggered episodes, more
+ * than 4 substeps, a window crossing an episode end, h out of range, wrong networks, NULL
+ * or misaligned pointers. */
+int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* policy, const auv_mlp* value,
+                    const auv_shac_buffers* out, float* grad_policy, float* stats, void* work, void* stream);
 
 /* Message for the calling thread's last error ("" if none). */
 const char* auv_last_error(void);

@@ -307,7 +307,8 @@ def window_grad(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma
     else:
         out["grad_act"] = np.stack([m.grad.numpy() for m in w["mus"]])
         out["acts"] = np.stack([a.detach().numpy() for a in w["acts"]])
-        out["grad_policy"] = {k: v.grad.numpy() for k, v in pol.items()}
+        out["grad_policy"] = {k: (v.grad.numpy() if v.grad is not None else np.zeros(tuple(v.shape)))
+                              for k, v in pol.items()}   # log_std is unused in mean mode
     return out
 
 

@@ -2,7 +2,7 @@
 
 The compute path is libauv.so (HIP kernels behind the C interface in include/auv.h);
 `_abi` binds it with ctypes under the same names; `env.AuvEnv` owns the environment
-buffers and `ppo.PpoLearner` those of the PPO update.
+buffers and `ppo.PpoLearner` those of the PPO update, `shac.ShacLearner` those of the SHAC actor.
 Importing this package loads the library and fails if it has not been built.
 """
 from . import _abi  # noqa: F401  (loads libauv.so; raises ImportError if missing)
@@ -11,3 +11,4 @@ from ._abi import (AUV_ACT_EXTERNAL, AUV_ACT_POLICY_MEAN, AUV_ACT_POLICY_SAMPLE,
                    AuvError)
 from .env import AuvEnv, upload_mlp  # noqa: F401
 from .ppo import PpoLearner, PpoNet  # noqa: F401
+from .shac import ShacLearner  # noqa: F401

@@ -69,6 +69,15 @@ class AuvPpoNet(ctypes.Structure):
     _fields_ = [("theta", _vp), ("adam_m", _vp), ("adam_v", _vp), ("w_bf16", _vp), ("n_out", ctypes.c_int32)]
 
 
+class AuvShacConfig(ctypes.Structure):
+    _fields_ = [("h", ctypes.c_int32), ("mode", ctypes.c_int32), ("gamma", _f), ("max_grad_norm", _f)]
+
+
+class AuvShacBuffers(ctypes.Structure):
+    _fields_ = [(k, _vp) for k in ("actions", "obs", "act", "reward", "done", "grad_act", "value_last",
+                                   "grad_state0")]
+
+
 def ppo_nw(n_out: int) -> int:
     """AUV_PPO_NW: packed offset of b1 (the weight matrices' length)."""
     return 256 * 23 + 256 * 256 + n_out * 256
@@ -107,6 +116,9 @@ def _load() -> ctypes.CDLL:
         "auv_ppo_grad": (ctypes.c_int, [P(AuvPpoConfig), P(AuvMlp), P(AuvMlp), P(AuvPpoBatch), _vp, i32, _vp, _vp,
                                         _vp, _vp, _vp]),
         "auv_ppo_adam": (ctypes.c_int, [P(AuvPpoConfig), i64, P(AuvPpoNet), P(AuvPpoNet), _vp, _vp, _vp, _vp]),
+        "auv_shac_work_bytes": (i64, [i32, i32]),
+        "auv_shac_window": (ctypes.c_int, [_vp, P(AuvShacConfig), P(AuvMlp), P(AuvMlp), P(AuvShacBuffers), _vp, _vp,
+                                           _vp, _vp]),
         "auv_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -204,10 +216,23 @@ def auv_ppo_grad(cfg: AuvPpoConfig, policy: AuvMlp, value: AuvMlp, batch: AuvPpo
                             stream_ptr(stream)))
 
 
-def auv_ppo_adam(cfg: AuvPpoConfig, t: int, policy: AuvPpoNet, value: AuvPpoNet, grad_policy, grad_value,
-                 stats, stream=None) -> None:
-    _check(lib.auv_ppo_adam(ctypes.byref(cfg), t, ctypes.byref(policy), ctypes.byref(value), ptr(grad_policy),
-                            ptr(grad_value), ptr(stats), stream_ptr(stream)))
+def auv_ppo_adam(cfg: AuvPpoConfig, t: int, policy: AuvPpoNet | None, value: AuvPpoNet | None, grad_policy,
+                 grad_value, stats, stream=None) -> None:
+    ref = lambda n: ctypes.byref(n) if n is not None else None  # noqa: E731
+    _check(lib.auv_ppo_adam(ctypes.byref(cfg), t, ref(policy), ref(value), ptr(grad_policy), ptr(grad_value),
+                            ptr(stats), stream_ptr(stream)))
+
+
+def auv_shac_work_bytes(n_envs: int, h: int) -> int:
+    return int(lib.auv_shac_work_bytes(n_envs, h))
+
+
+def auv_shac_window(h: int, cfg: AuvShacConfig, policy: AuvMlp | None, value: AuvMlp | None,
+                    out: AuvShacBuffers | None, grad_policy, stats, work, stream=None) -> None:
+    _check(lib.auv_shac_window(h, ctypes.byref(cfg), ctypes.byref(policy) if policy is not None else None,
+                               ctypes.byref(value) if value is not None else None,
+                               ctypes.byref(out) if out is not None else None, ptr(grad_policy), ptr(stats), ptr(work),
+                               stream_ptr(stream)))
 
 
 def auv_last_error() -> str:
@@ -259,6 +284,14 @@ def make_ppo_config(clip_eps=0.2, vf_coef=0.5, ent_coef=0.0, max_grad_norm=0.5, 
 
 def make_ppo_batch(obs, act, logp, adv, ret, M: int) -> AuvPpoBatch:
     return AuvPpoBatch(ptr(obs), ptr(act), ptr(logp), ptr(adv), ptr(ret), M)
+
+
+def make_shac_config(h: int, mode: int, gamma: float, max_grad_norm: float = 0.0) -> AuvShacConfig:
+    return AuvShacConfig(h, mode, float(np.float32(gamma)), float(np.float32(max_grad_norm)))
+
+
+def make_shac_buffers(**kw) -> AuvShacBuffers:
+    return AuvShacBuffers(**{k: ptr(v) for k, v in kw.items()})
 
 
 def make_rollout_buffers(**kw) -> AuvRolloutBuffers:

@@ -46,4 +46,18 @@ int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy,
 int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, hipStream_t s);
 int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s);
 
+// Per-workgroup partial sums of an MLP's parameter gradient (layouts of the PPO update):
+// part_w1 [G][256][32], part_b1 [G][256], part_w2 [G][256][256], part_w3t [G][256][16]
+// (dW3 transposed), part_b2 [G][256], part_b3 [G][16], part_ls [G][16] (d log_std).
+struct GradParts {
+  float *part_w1, *part_b1, *part_w2, *part_w3t, *part_b2, *part_b3, *part_ls;
+};
+// launches implemented in ppo.hip: dW2 = q(dz2) q(h1)^T over `steps` 32-sample steps of
+// half-fragment arrays (steps a multiple of 4), one partial per group; the fixed-order sum of
+// the partials into the packed gradient (+ per-block sums of squares, grad_reduce_blocks)
+int launch_dw2(const void* dz2_half, const void* h1_half, int steps, int groups, float* part_w2, hipStream_t s);
+int launch_grad_reduce(const GradParts& P, int n_out, int n_act, int G1, int G2, int G3, float* grad, float* ss,
+                       hipStream_t s);
+int grad_reduce_blocks(int n_out);
+
 }  // namespace auv

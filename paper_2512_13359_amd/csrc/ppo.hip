@@ -792,6 +792,30 @@ __global__ __launch_bounds__(256) void k_adam(int P, int nW, float* __restrict__
 }
 
 }  // namespace ppo
+
+int launch_dw2(const void* dz2_half, const void* h1_half, int steps, int groups, float* part_w2, hipStream_t s) {
+  hipLaunchKernelGGL(ppo::k_dw2, dim3(groups), dim3(64 * ppo::DW2_WAVES), 0, s, (const ppo::u32x2*)dz2_half,
+                     (const ppo::u32x2*)h1_half, steps, part_w2);
+  return check_launch("dW2");
+}
+
+int launch_grad_reduce(const GradParts& P, int n_out, int n_act, int G1, int G2, int G3, float* grad, float* ss,
+                       hipStream_t s) {
+  ppo::Work W{};
+  W.part_w1 = P.part_w1;
+  W.part_b1 = P.part_b1;
+  W.part_w2 = P.part_w2;
+  W.part_w3t = P.part_w3t;
+  W.part_b2 = P.part_b2;
+  W.part_b3 = P.part_b3;
+  W.part_ls = P.part_ls;
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(n_out)), dim3(256), 0, s, n_out, n_act, G1, G2, G3, W, 0.0f,
+                     grad, ss);
+  return check_launch("gradient reduce");
+}
+
+int grad_reduce_blocks(int n_out) { return ppo::red_blocks(n_out); }
+
 }  // namespace auv
 
 // ------------------------------------------------------------------ C interface ----
@@ -876,9 +900,11 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
   const float* grads[2] = {grad_policy, grad_value};
   const int n_outs[2] = {ACT, 1};
   if (!stats || !aligned16(stats)) return set_error(AUV_EINVAL, "auv_ppo_adam: stats NULL or not aligned");
+  if (!policy && !value) return set_error(AUV_EINVAL, "auv_ppo_adam: no network");
   for (int k = 0; k < 2; ++k) {
     const auv_ppo_net* n = nets[k];
-    if (!n || n->n_out != n_outs[k]) return set_error(AUV_EINVAL, "auv_ppo_adam: network %d missing or n_out != %d", k, n_outs[k]);
+    if (!n) continue;
+    if (n->n_out != n_outs[k]) return set_error(AUV_EINVAL, "auv_ppo_adam: network %d has n_out != %d", k, n_outs[k]);
     const void* ptrs[5] = {n->theta, n->adam_m, n->adam_v, n->w_bf16, grads[k]};
     for (int q = 0; q < 5; ++q)
       if (!ptrs[q] || !aligned16(ptrs[q])) return set_error(AUV_EINVAL, "auv_ppo_adam: network %d pointer %d NULL or not aligned", k, q);
@@ -887,6 +913,7 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
   const float bc1 = (float)(1.0 - std::pow((double)cfg->beta1, (double)t));
   const float bc2 = (float)(1.0 - std::pow((double)cfg->beta2, (double)t));
   for (int k = 0; k < 2; ++k) {
+    if (!nets[k]) continue;
     const int P = ppo::nparam(n_outs[k]), nW = HID * 23 + HID * HID + n_outs[k] * HID;
     hipLaunchKernelGGL(ppo::k_adam, dim3((P + 255) / 256), dim3(256), 0, s, P, nW, nets[k]->theta, nets[k]->adam_m,
                        nets[k]->adam_v, nets[k]->w_bf16, grads[k], stats, cfg->lr, cfg->beta1, cfg->beta2, cfg->adam_eps,
