@@ -285,6 +285,58 @@ def paper_training_measure(reps: int = 2, epochs: int = 4, minibatch: int = 2621
             "hundred_episodes_s": 100 * t}
 
 
+# Dense-contraction work per env-step of a SHAC window on the paper task's 12-256-256-6
+# policy (padding excluded): the forward, the input gradient (the same matrices
+# transposed) and the weight gradient.
+SHAC_FLOP_PER_STEP = 3 * 2 * (12 * 256 + 256 * 256 + 256 * 6)
+
+
+def shac_measure(n_envs: int, reps: int = 16) -> dict:
+    """SHAC actor windows on the paper task: h = 32 control steps of n_envs environments
+    with the sampled policy in the loop and a terminal value (auv_shac_window: forward,
+    reverse sweep through RK4 + Fossen and the policy, parameter gradient), then the actor's
+    Adam step.  Consecutive windows tile the 512-step episodes."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, ShacLearner
+
+    cfg = W.config("c6", n_envs=n_envs)
+    h = W.SHAC["h"]
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.set_task(W.PAPER_TASK)
+    env.reset()
+    L = ShacLearner(env, W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.PAPER_VALUE_SEED, n_in=12),
+                    h=h, gamma=W.SHAC["gamma"], max_grad_norm=W.SHAC["max_grad_norm"])
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    win, stp = [], []
+    for k in range(reps + 1):
+        torch.cuda.synchronize()
+        e = [ev() for _ in range(3)]
+        e[0].record()
+        L.window()
+        e[1].record()
+        L.step()
+        e[2].record()
+        torch.cuda.synchronize()
+        if k:
+            win.append(e[0].elapsed_time(e[1]) * 1e-3)
+            stp.append(e[1].elapsed_time(e[2]) * 1e-3)
+    st = L.stats.cpu().numpy()
+    assert (st == st).all(), "non-finite SHAC statistics"
+    tw = sorted(win)[len(win) // 2]
+    ts = sorted(stp)[len(stp) // 2]
+    steps = n_envs * h
+    windows_per_episode = cfg["episode_len"] // h
+    return {"workload": f"SHAC on the paper task: {n_envs} envs, windows of {h} steps (sampled policy, terminal "
+                        f"value), actor gradient through RK4 + Fossen and the 12-256-256-6 policy, Adam step",
+            "n_envs": n_envs, "h": h, "window_ms": tw * 1e3, "actor_step_ms": ts * 1e3,
+            "env_steps_per_s": steps / tw, "mfma_flop_per_env_step": SHAC_FLOP_PER_STEP,
+            "achieved_TFLOPs": SHAC_FLOP_PER_STEP * steps / tw / 1e12,
+            "frac_of_bf16_peak": SHAC_FLOP_PER_STEP * steps / tw / P_MFMA,
+            "hundred_episodes_actor_s": 100 * windows_per_episode * (tw + ts)}
+
+
 def small_configs_measure(reps: int = 3) -> dict:
     """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
     4096 envs occupy 64 of the 256 CUs, so these are occupancy-capped by N."""
@@ -327,6 +379,7 @@ def main() -> int:
     ap.add_argument("--no-ppo", action="store_true", help="skip the PPO-update measurement")
     ap.add_argument("--ppo-only", action="store_true", help="only measure the PPO update and print it")
     ap.add_argument("--paper-only", action="store_true", help="only measure the paper task (c6, training iteration)")
+    ap.add_argument("--shac-only", action="store_true", help="only measure the SHAC windows (4096 and 512 envs)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -355,6 +408,10 @@ def main() -> int:
         return 0
     if args.paper_only:
         print(json.dumps({"c6": paper_task_measure(), "paper_training": paper_training_measure()}), flush=True)
+        return 0
+    if args.shac_only:
+        print(json.dumps({"shac": [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]}),
+              flush=True)
         return 0
     cfg = W.config(args.workload)
     n, T = cfg["n_envs"], cfg["T"]
@@ -430,6 +487,7 @@ def main() -> int:
         line["ppo"] = ppo_measure()
         line["c6"] = paper_task_measure()
         line["paper_training"] = paper_training_measure()
+        line["shac"] = [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
     print(json.dumps(line), flush=True)
