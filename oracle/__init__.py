@@ -22,6 +22,8 @@ Modules
             five-term reward with an action moving average, gravity randomisation
   ppo       clipped-surrogate PPO objective, its gradient through both MLPs (with the
             bf16 quantisation points of the MFMA path), global-norm clipping, Adam
+  fluid     the inertia-box fluid model of the paper's MJX simulation (equivalent box,
+            viscous + quadratic drag, no added mass) as an alternate hydrodynamics
   shac      the SHAC actor objective over a short window of the paper task and its
             gradient through the policy, reward, observation, RK4 + Fossen and the
             terminal value (torch autograd on float64 tensors)
@@ -29,4 +31,4 @@ Modules
 Every function is pinned by a ``-m "not gpu"`` test against closed forms, invariants,
 special cases or an independent library; see the test files under ``tests/``.
 """
-from . import rng, dynamics, mlp, gae, env, ppo, paper_task, shac  # noqa: F401
+from . import rng, dynamics, fluid, mlp, gae, env, ppo, paper_task, shac  # noqa: F401

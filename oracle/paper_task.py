@@ -16,7 +16,9 @@ aligned (Sec. IV-C); 512-step episodes with references within [-2, 2] m and [-60
 Readings where the paper is silent (the same on both sides):
   * dynamics: the Fossen model of the other workloads (dynamics.py) with the buoyancy centre
     at the centre of gravity (r_b = 0), no current, no mass / damping randomisation; the
-    gravity factor gamma scales the weight: W = gamma W0, gamma ~ U[0.95, 1.05]
+    gravity factor gamma scales the weight: W = gamma W0, gamma ~ U[0.95, 1.05]; or, with
+    task["fluid"] == 1, the inertia-box fluid model of the paper's MJX setup (fluid.py: no
+    added mass, viscous + quadratic drag on the equivalent box, task density and viscosity)
   * wrench tau = [F_max u_0:3, tau_max u_3:6], u = clip(a, -1, 1)
   * reset: p0 = 0, q0 = identity, v = omega = 0; goal position U[-2, 2]^3; goal attitude from
     Z-Y-X Euler angles (roll, pitch, yaw) each U[-60, 60] degrees, q = q_z(yaw) q_y(pitch) q_x(roll)
@@ -36,6 +38,7 @@ import math
 import numpy as np
 
 from . import dynamics as dyn
+from . import fluid as fl
 from . import mlp as mlpmod
 from . import rng
 from .env import _f64
@@ -91,6 +94,9 @@ class Task:
         self.r_gfac = (t["gamma_lo"], t["gamma_span"])
         e = np.float32(t["euler_max"])
         self.r_euler = (-float(e), float(np.float32(2.0) * e))
+        self.fluid = int(t.get("fluid", 0))                 # 0 Fossen, 1 inertia box (fluid.py)
+        self.rho = f(t.get("density", fl.RHO_WATER))
+        self.mu = f(t.get("viscosity", fl.MU_WATER))
 
 
 class PaperEnv:
@@ -118,7 +124,10 @@ class PaperEnv:
         self.veh = self._vehicle()
 
     def _vehicle(self):
-        v = dyn.Vehicle(self.veh_data, self.n)
+        if self.tk.fluid == 1:
+            v = fl.InertiaBoxVehicle(self.veh_data, self.n, self.tk.rho, self.tk.mu)
+        else:
+            v = dyn.Vehicle(self.veh_data, self.n)
         v.W = _f64(self.veh_data["W"]) * self.gfac          # per-env weight [n]
         return v
 

@@ -23,7 +23,7 @@ __all__ = [
     "FLAG_DR", "FLAG_CURRENT", "FLAG_LISSAJOUS", "FLAG_STAGGER", "FLAG_TRAJ_STATE",
     "MODE_EXTERNAL", "MODE_RANDOM", "MODE_POLICY_MEAN", "MODE_POLICY_SAMPLE",
     "CONFIGS", "config", "mlp_weights", "vehicle_variant", "random_states",
-    "PPO", "ppo_draws", "ppo_minibatch_idx", "PAPER_TASK", "SHAC",
+    "PPO", "ppo_draws", "ppo_minibatch_idx", "PAPER_TASK", "PAPER_TASK_BOX", "SHAC",
 ]
 
 # --- vehicle (fp32 values; every consumer promotes them exactly) -------------------
@@ -201,7 +201,10 @@ def ppo_minibatch_idx(M: int, B: int, seed: int) -> np.ndarray:
 # project's choice: wrench limits within the thrusters' envelope, reward weights) -----------
 PAPER_TASK = dict(kind=1, f_max=60.0, tau_max=10.0, w_pos=1.0, d_pos=(1.0, 1.0, 1.5), w_att=0.5,
                   w_act=0.01, w_vel=0.05, w_mavg=0.1, beta=0.8, gamma_lo=0.95, gamma_span=0.1,
-                  euler_max=float(np.float32(math.pi / 3.0)))
+                  euler_max=float(np.float32(math.pi / 3.0)), fluid=0, density=1000.0, viscosity=1.0e-3)
+# The same task with the hydrodynamics of the paper's MJX simulation (Sec. IV-B): the
+# inertia-box fluid model in water (density 1000 kg/m^3, viscosity 1.0e-3 Pa s).
+PAPER_TASK_BOX = dict(PAPER_TASK, fluid=1)
 PAPER_POLICY_SEED = 9
 PAPER_VALUE_SEED = 10
 
