@@ -200,7 +200,8 @@ def ppo_measure(reps: int = 5) -> dict:
 def paper_task_measure(reps: int = 3) -> dict:
     """The paper's own task (12-D observation, 6-D wrench, five-term reward) at the paper's
     training scale: 4096 envs x one 512-step episode, policy mean (12-256-256-6) and random
-    actions; env-steps/s per launch."""
+    actions on the Fossen model, and the policy on the inertia-box fluid model of the paper's
+    MJX simulation; env-steps/s per launch."""
     import torch
 
     import workloads as W
@@ -211,9 +212,11 @@ def paper_task_measure(reps: int = 3) -> dict:
     pol = upload_mlp(W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12))
     out = {"workload": f"c6: paper task, {n} envs x {T} steps (one episode), {cfg['substeps']} RK4 substeps "
                        f"per {cfg['dt_control']} s, gravity randomisation, goals within 2 m / 60 deg"}
-    for name, mode, p in (("policy", W.MODE_POLICY_MEAN, pol), ("random", W.MODE_RANDOM, None)):
+    runs = (("policy", W.MODE_POLICY_MEAN, pol, W.PAPER_TASK), ("random", W.MODE_RANDOM, None, W.PAPER_TASK),
+            ("policy_inertia_box", W.MODE_POLICY_MEAN, pol, W.PAPER_TASK_BOX))
+    for name, mode, p, task in runs:
         env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
-        env.set_task(W.PAPER_TASK)
+        env.set_task(task)
         ts = []
         for k in range(reps + 1):
             env.reset()

@@ -210,6 +210,15 @@ int auv_set_sync_poll_limit(auv_env* env, uint32_t polls);
  *   loop.  Set the task before auv_reset. */
 enum { AUV_TASK_WORKLOAD = 0, AUV_TASK_PAPER = 1 };
 
+/* Hydrodynamics of the paper task.  AUV_FLUID_FOSSEN: the vehicle's added mass and linear +
+ * quadratic damping (auv_vehicle).  AUV_FLUID_INERTIA_BOX: the inertia-based fluid model of the
+ * paper's MJX simulation (Sec. IV-B): the vehicle is replaced by the uniform solid box with its
+ * mass and principal inertia, s_i = sqrt(6 (I_j + I_k - I_i) / m); no added mass; viscous
+ * drag -3 pi mu d v and torque -pi mu d^3 w (d = mean side); quadratic drag
+ * -rho/2 s_j s_k |v_i| v_i and torque -rho s_i (s_j^4 + s_k^4) / 64 |w_i| w_i.  The constants are
+ * derived on the host by auv_set_task; the kernels are the same. */
+enum { AUV_FLUID_FOSSEN = 0, AUV_FLUID_INERTIA_BOX = 1 };
+
 typedef struct {
   int32_t kind;          /* AUV_TASK_* */
   float f_max, tau_max;  /* N, N m at |u| = 1 (> 0) */
@@ -217,10 +226,14 @@ typedef struct {
   float beta;            /* moving-average factor, 0 <= beta < 1 */
   float gamma_lo, gamma_span;   /* gravity factor range, gamma_lo > 0, span >= 0 */
   float euler_max;       /* goal Euler angle bound, rad, 0 <= euler_max <= pi */
+  int32_t fluid;         /* AUV_FLUID_* */
+  float density;         /* kg/m^3 (> 0), AUV_FLUID_INERTIA_BOX only */
+  float viscosity;       /* Pa s (>= 0), AUV_FLUID_INERTIA_BOX only */
 } auv_task;
 
-/* Selects the task of a handle (no GPU call).  AUV_EINVAL for values out of range, or for
- * AUV_TASK_PAPER with AUV_F_DR, AUV_F_CURRENT or AUV_F_LISSAJOUS set (not part of that task). */
+/* Selects the task of a handle (no GPU call).  AUV_EINVAL for values out of range, for
+ * AUV_TASK_PAPER with AUV_F_DR, AUV_F_CURRENT or AUV_F_LISSAJOUS set (not part of that task), or
+ * for AUV_FLUID_INERTIA_BOX with an inertia no solid box has (I_i >= I_j + I_k). */
 int auv_set_task(auv_env* env, const auv_task* task);
 
 /* ---- PPO update of the policy and value MLPs on one minibatch ------------------------

@@ -86,6 +86,18 @@ def terminal_speed(F: float, lin: float, quad: float) -> float:
     return (-lin + math.sqrt(lin * lin + 4.0 * quad * F)) / (2.0 * quad)
 
 
+def speed_from_rest(F: float, t, mass: float, lin: float, quad: float):
+    """Speed along one axis of mass dv/dt = F - lin v - quad |v| v from v(0) = 0 (closed form):
+    with the roots v+ > 0 > v- of quad v^2 + lin v - |F| = 0 and k = quad (v+ - v-) / mass,
+    v = sign(F) (v+ - r v-) / (1 - r),  r = (v+ / v-) exp(-k t)."""
+    t = np.asarray(t, np.float64)
+    a = abs(F)
+    disc = math.sqrt(lin * lin + 4.0 * quad * a)
+    vp, vm = (-lin + disc) / (2.0 * quad), (-lin - disc) / (2.0 * quad)
+    r = (vp / vm) * np.exp(-quad * (vp - vm) * t / mass)
+    return math.copysign(1.0, F) * (vp - r * vm) / (1.0 - r)
+
+
 def spin_down(w0: float, t, inertia: float, lin: float, quad: float):
     """Angular rate of I dw/dt = -(lin + quad |w|) w from w0 > 0 (closed form):
     w(t) = lin / (quad ((1 + lin / (quad w0)) exp(lin t / I) - 1))."""

@@ -18,6 +18,7 @@ AUV_OK, AUV_EINVAL, AUV_ENODEV, AUV_ELAUNCH, AUV_ERUNTIME = 0, -1, -2, -3, -4
 AUV_ACT_EXTERNAL, AUV_ACT_RANDOM, AUV_ACT_POLICY_MEAN, AUV_ACT_POLICY_SAMPLE = 0, 1, 2, 3
 AUV_F_DR, AUV_F_CURRENT, AUV_F_LISSAJOUS, AUV_F_STAGGER = 1, 2, 4, 8
 AUV_TASK_WORKLOAD, AUV_TASK_PAPER = 0, 1
+AUV_FLUID_FOSSEN, AUV_FLUID_INERTIA_BOX = 0, 1
 OBS_DIM, ACT_DIM, STATE_DIM, PARAM_DIM, HIDDEN, ENVS_PER_GROUP = 23, 8, 13, 24, 256, 64
 
 _f = ctypes.c_float
@@ -52,7 +53,8 @@ class AuvRolloutBuffers(ctypes.Structure):
 class AuvTask(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("f_max", _f), ("tau_max", _f), ("w_pos", _f), ("d_pos", _f * 3),
                 ("w_att", _f), ("w_act", _f), ("w_vel", _f), ("w_mavg", _f), ("beta", _f), ("gamma_lo", _f),
-                ("gamma_span", _f), ("euler_max", _f)]
+                ("gamma_span", _f), ("euler_max", _f), ("fluid", ctypes.c_int32), ("density", _f),
+                ("viscosity", _f)]
 
 
 class AuvPpoConfig(ctypes.Structure):
@@ -266,7 +268,7 @@ def make_env_buffers(state, params, ep_step, episode, obs) -> AuvEnvBuffers:
 
 def make_task(task: dict) -> AuvTask:
     """auv_task from a dict (kind, f_max, tau_max, w_pos, d_pos, w_att, w_act, w_vel, w_mavg, beta,
-    gamma_lo, gamma_span, euler_max)."""
+    gamma_lo, gamma_span, euler_max; fluid, density, viscosity)."""
     t = AuvTask()
     for k, v in task.items():
         if k == "d_pos":

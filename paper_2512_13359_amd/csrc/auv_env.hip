@@ -391,6 +391,7 @@ int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buff
   for (int k = 0; k < 3; ++k) V.Brb[k] = veh->B * veh->r_b[k];
   V.f_max = veh->f_max;
   std::memcpy(V.alloc, veh->alloc, sizeof V.alloc);
+  e->veh_base = V;
   EnvArgs& E = e->E;
   E.state = bufs->state;
   E.params = bufs->params;
@@ -432,6 +433,7 @@ int auv_set_task(auv_env* env, const auv_task* t) {
   if (!env || !t) return set_error(AUV_EINVAL, "auv_set_task: NULL argument");
   if (t->kind == AUV_TASK_WORKLOAD) {
     env->E.task = TASK_WORKLOAD;
+    env->veh = env->veh_base;
     return AUV_OK;
   }
   if (t->kind != AUV_TASK_PAPER) return set_error(AUV_EINVAL, "auv_set_task: unknown task kind %d", t->kind);
@@ -446,6 +448,32 @@ int auv_set_task(auv_env* env, const auv_task* t) {
   if (!(t->gamma_lo > 0.0f) || !std::isfinite(t->gamma_lo)) return set_error(AUV_EINVAL, "auv_set_task: gamma_lo must be > 0");
   if (!(t->euler_max >= 0.0f && t->euler_max <= 3.14159274f))
     return set_error(AUV_EINVAL, "auv_set_task: euler_max must be in [0, pi]");
+  VehArgs V = env->veh_base;
+  if (t->fluid == AUV_FLUID_INERTIA_BOX) {
+    if (!(t->density > 0.0f) || !std::isfinite(t->density) || !(t->viscosity >= 0.0f) || !std::isfinite(t->viscosity))
+      return set_error(AUV_EINVAL, "auv_set_task: density must be > 0 and viscosity >= 0");
+    // the uniform solid box with the vehicle's mass and principal inertia
+    const double m = V.m, I[3] = {V.inertia[0], V.inertia[1], V.inertia[2]};
+    double box[3];
+    for (int i = 0; i < 3; ++i) {
+      const double arg = 6.0 * (I[(i + 1) % 3] + I[(i + 2) % 3] - I[i]) / m;
+      if (!(arg > 0.0)) return set_error(AUV_EINVAL, "auv_set_task: no solid box has this inertia (I_i >= I_j + I_k)");
+      box[i] = std::sqrt(arg);
+    }
+    const double rho = t->density, mu = t->viscosity, pi = 3.14159265358979323846;
+    const double d = (box[0] + box[1] + box[2]) / 3.0;
+    for (int i = 0; i < 3; ++i) {
+      const double sj = box[(i + 1) % 3], sk = box[(i + 2) % 3];
+      V.added_mass[i] = V.added_mass[3 + i] = 0.0f;
+      V.lin_damp[i] = (float)(3.0 * pi * mu * d);            // Stokes drag of the sphere of diameter d
+      V.lin_damp[3 + i] = (float)(pi * mu * d * d * d);      // Stokes torque
+      V.quad_damp[i] = (float)(0.5 * rho * sj * sk);         // pressure drag on the face normal to i
+      V.quad_damp[3 + i] = (float)(rho * box[i] * (sj * sj * sj * sj + sk * sk * sk * sk) / 64.0);
+    }
+  } else if (t->fluid != AUV_FLUID_FOSSEN) {
+    return set_error(AUV_EINVAL, "auv_set_task: unknown fluid model %d", t->fluid);
+  }
+  env->veh = V;
   TaskArgs& k = env->E.tk;
   k.f_max = t->f_max;
   k.tau_max = t->tau_max;

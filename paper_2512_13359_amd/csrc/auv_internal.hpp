@@ -14,7 +14,8 @@
 
 struct auv_env {
   auv_config cfg;
-  auv::VehArgs veh;
+  auv::VehArgs veh;        // vehicle constants of the launches (task-dependent)
+  auv::VehArgs veh_base;   // the vehicle as given to auv_create
   auv::EnvArgs E;
   int64_t global_step;
 };

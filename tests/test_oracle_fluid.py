@@ -60,9 +60,13 @@ def test_terminal_speed_and_start_without_added_mass():
     tau = np.array([[F], [0], [0], [0], [0], [0]], np.float64)
     d0 = dyn.rhs(x, tau, v, np.zeros((3, 1)))
     assert np.isclose(d0[7, 0], F / float(np.float32(11.5)), rtol=1e-14)          # no added mass
-    for _ in range(2000):                                                          # 20 s
-        x = dyn.rk4_substep(x, tau, v, np.zeros((3, 1)), 0.01)
     c = v.fluid
+    m = float(np.float32(11.5))
+    for k in range(2000):                                                          # 20 s
+        x = dyn.rk4_substep(x, tau, v, np.zeros((3, 1)), 0.01)
+        if k % 200 == 199:
+            t = (k + 1) * 0.01
+            assert abs(x[7, 0] - fl.speed_from_rest(F, t, m, c["lin"][0], c["quad"][0])) <= 1e-9
     assert abs(x[7, 0] - fl.terminal_speed(F, c["lin"][0], c["quad"][0])) <= 1e-9
     assert np.allclose(x[8:13, 0], 0.0, atol=1e-12) and np.allclose(x[3:7, 0], [1, 0, 0, 0], atol=1e-12)
 
