@@ -10,6 +10,7 @@ import ctypes
 import os
 
 import numpy as np
+import torch  # noqa: F401  (brings up the HIP runtime before libauv registers its kernels)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libauv.so")

@@ -68,6 +68,7 @@ struct WinArgs {
   NetF pol, val;
   const float* log_std;
   float *ck, *acts, *J, *Jr, *vl, *gls;
+  f32x4 *h2s, *h2v;                    // hidden-2 activations: policy [h][G] wave-steps, value [G]
   u32x2 *x_half, *h1_half, *h2_half, *gy_half, *dz2_half, *dz1_half;
   int Np;
   const float* ext;
@@ -75,13 +76,17 @@ struct WinArgs {
 };
 
 struct Lds {
+  bf16x8 W[128][64];      // the policy's W2 fragments (forward sweep), then its W2^T (reverse sweep)
   __bf16 X[64][32];       // layer-1 inputs per environment
   float Y[64][8];         // network outputs per environment
   __bf16 G[64][8];        // q(dL/dy) per environment
   float GX[64][32];       // input gradient per environment
-  bf16x8 Dz[8][NT][64];   // q(dz2) B fragments of the W2^T product
   __bf16 T[32 * TS];      // transpose buffer [feature][environment]
 };
+
+// Hidden-2 activations (fp32) of one wave-step, kept by the forward for the backward:
+// [32-feature chunk p][M-tile 2p or 2p + 1][N-tile][lane], 64 KB.
+constexpr int H2_F4 = 8 * 2 * NT * 64;
 
 // ------------------------------------------------------------------ fragments ---------
 __global__ __launch_bounds__(256) void k_frags(const uint16_t* __restrict__ w, int n_out, bf16x8* __restrict__ out) {
@@ -142,6 +147,16 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
 
 __device__ __forceinline__ bf16x8 fr(const NetF& N, int idx, int lane) { return N.f[idx * 64 + lane]; }
 
+// The window kernel's workgroup is one wave.  The LDS operations of a wave complete in the
+// order they are issued, so exchanging data between its lanes through LDS needs only that the
+// compiler keep the accesses in program order: a wavefront-scope fence and wave barrier (no
+// workgroup barrier, whose fence would also wait for every outstanding global load and store).
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Hidden layer 1 of the wave's 64 environments as the B operand of layer 2: H1[K step][N-tile].
 __device__ __forceinline__ void layer1(const NetF& N, const bf16x8 X[NT], int lane, bf16x8 H1[8][NT]) {
   const int g = lane >> 4;
@@ -154,14 +169,15 @@ __device__ __forceinline__ void layer1(const NetF& N, const bf16x8 X[NT], int la
   }
 }
 
-// Pre-activations of hidden-2 features 32 p .. 32 p + 31 (M-tiles 2p, 2p + 1).
-__device__ __forceinline__ void layer2_chunk(const NetF& N, const bf16x8 H1[8][NT], int p, int lane, f32x4 z0[NT],
+// Pre-activations of hidden-2 features 32 p .. 32 p + 31 (M-tiles 2p, 2p + 1); w2: the 128
+// W2 fragments (in LDS, or the network's array in global memory).
+__device__ __forceinline__ void layer2_chunk(const bf16x8* w2, const bf16x8 H1[8][NT], int p, int lane, f32x4 z0[NT],
                                              f32x4 z1[NT]) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) z0[nt] = z1[nt] = zero4();
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
-    const bf16x8 a0 = fr(N, F_W2 + 16 * p + s, lane), a1 = fr(N, F_W2 + 16 * p + 8 + s, lane);
+    const bf16x8 a0 = w2[(16 * p + s) * 64 + lane], a1 = w2[(16 * p + 8 + s) * 64 + lane];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       z0[nt] = mfma(a0, H1[s][nt], z0[nt]);
@@ -170,8 +186,10 @@ __device__ __forceinline__ void layer2_chunk(const NetF& N, const bf16x8 H1[8][N
   }
 }
 
-// Network outputs y (lane (g, r): rows 4g .. 4g + 3 of environment 16 nt + r).
-__device__ __forceinline__ void mlp_forward(const NetF& N, const bf16x8 X[NT], int lane, f32x4 y[NT]) {
+// Network outputs y (lane (g, r): rows 4g .. 4g + 3 of environment 16 nt + r).  w2: the
+// W2 fragments to read; h2: where this wave-step's hidden-2 activations go (H2_F4 f32x4).
+__device__ __forceinline__ void mlp_forward(const NetF& N, const bf16x8* w2, const bf16x8 X[NT], int lane, f32x4 y[NT],
+                                            f32x4* __restrict__ h2) {
   const int g = lane >> 4;
   bf16x8 H1[8][NT];
   layer1(N, X, lane, H1);
@@ -180,11 +198,20 @@ __device__ __forceinline__ void mlp_forward(const NetF& N, const bf16x8 X[NT], i
 #pragma unroll 1
   for (int p = 0; p < 8; ++p) {
     f32x4 z0[NT], z1[NT];
-    layer2_chunk(N, H1, p, lane, z0, z1);
+    layer2_chunk(w2, H1, p, lane, z0, z1);
     const f32x4 b0 = bias_k(N.b + HID, 32 * p + 4 * g), b1 = bias_k(N.b + HID, 32 * p + 16 + 4 * g);
     const bf16x8 w3 = fr(N, F_W3 + p, lane);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) y[nt] = mfma(w3, act_frag(z0[nt], z1[nt], b0, b1), y[nt]);
+    for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        z0[nt][i] = tanh_bias(z0[nt][i], b0[i]);
+        z1[nt][i] = tanh_bias(z1[nt][i], b1[i]);
+      }
+      h2[((2 * p) * NT + nt) * 64 + lane] = z0[nt];
+      h2[((2 * p + 1) * NT + nt) * 64 + lane] = z1[nt];
+      y[nt] = mfma(w3, pack8(z0[nt], z1[nt]), y[nt]);
+    }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -208,7 +235,7 @@ struct HalfOut {
 __device__ __forceinline__ void store_pair(Lds& S, const f32x4 v0[NT], const f32x4 v1[NT], int lane, u32x2* dst,
                                            size_t tile0, int c) {
   const int g = lane >> 4, r = lane & 15;
-  __syncthreads();   // earlier readers of the buffer are done
+  lds_sync();   // earlier readers of the buffer are done
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -216,7 +243,7 @@ __device__ __forceinline__ void store_pair(Lds& S, const f32x4 v0[NT], const f32
       S.T[(4 * g + i) * TS + 16 * nt + r] = (__bf16)v0[nt][i];
       S.T[(16 + 4 * g + i) * TS + 16 * nt + r] = (__bf16)v1[nt][i];
     }
-  __syncthreads();
+  lds_sync();
 #pragma unroll
   for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
@@ -225,33 +252,25 @@ __device__ __forceinline__ void store_pair(Lds& S, const f32x4 v0[NT], const f32
           *reinterpret_cast<const u32x2*>(&S.T[(16 * hf + r) * TS + 16 * nt + 4 * g]);
 }
 
-// Forward recomputed from the layer-1 operand X and backward from q(dL/dy) (GY, B operand
-// with K = the output rows): the input gradient gx[M-tile][N-tile] (lane (g, r): inputs
-// 16 m + 4 g + i of environment 16 nt + r) and, with H.on, the step's operands of the
-// weight gradient.
-__device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8 X[NT], const bf16x8 GY[NT], int lane, Lds& S,
-                                             f32x4 gx[2][NT], const HalfOut& H) {
+// Backward from q(dL/dy) (GY, B operand with K = the output rows) given the layer-1 operand X
+// and the step's stored hidden-2 activations h2: the input gradient gx[M-tile][N-tile] (lane
+// (g, r): inputs 16 m + 4 g + i of environment 16 nt + r) and, with H.on, the step's operands
+// of the weight gradient.  w2t: the 128 W2^T fragments to read.  Hidden layer 1 is recomputed
+// from X (one K step per 32 features).
+__device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, const bf16x8 X[NT], const bf16x8 GY[NT],
+                                             int lane, Lds& S, f32x4 gx[2][NT], const HalfOut& H,
+                                             const f32x4* __restrict__ h2) {
   const int g = lane >> 4;
-  bf16x8 H1[8][NT];
-  layer1(N, X, lane, H1);
-  // hidden 2: dz2 = (W3^T q(gy)) (1 - h2^2), chunk by chunk of 32 features
-#pragma unroll 1
+  // hidden 2: dz2 = (W3^T q(gy)) (1 - h2^2), as the B operand of the W2^T product
+  bf16x8 dz[8][NT];
+#pragma unroll
   for (int p = 0; p < 8; ++p) {
-    f32x4 z0[NT], z1[NT];
-    layer2_chunk(N, H1, p, lane, z0, z1);
-    const f32x4 b0 = bias_k(N.b + HID, 32 * p + 4 * g), b1 = bias_k(N.b + HID, 32 * p + 16 + 4 * g);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        z0[nt][i] = tanh_bias(z0[nt][i], b0[i]);
-        z1[nt][i] = tanh_bias(z1[nt][i], b1[i]);
-      }
-    if (H.on) store_pair(S, z0, z1, lane, H.h2, H.tile0, p);
+    f32x4 z0[NT], z1[NT], d0[NT], d1[NT];
     const bf16x8 t0 = fr(N, F_W3T + 2 * p, lane), t1 = fr(N, F_W3T + 2 * p + 1, lane);
-    f32x4 d0[NT], d1[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      z0[nt] = h2[((2 * p) * NT + nt) * 64 + lane];
+      z1[nt] = h2[((2 * p + 1) * NT + nt) * 64 + lane];
       d0[nt] = mfma(t0, GY[nt], zero4());
       d1[nt] = mfma(t1, GY[nt], zero4());
 #pragma unroll
@@ -259,11 +278,13 @@ __device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8 X[NT], 
         d0[nt][i] *= 1.0f - z0[nt][i] * z0[nt][i];
         d1[nt][i] *= 1.0f - z1[nt][i] * z1[nt][i];
       }
-      S.Dz[p][nt][lane] = pack8(d0[nt], d1[nt]);
+      dz[p][nt] = pack8(d0[nt], d1[nt]);
     }
-    if (H.on) store_pair(S, d0, d1, lane, H.dz2, H.tile0, p);
+    if (H.on) {
+      store_pair(S, z0, z1, lane, H.h2, H.tile0, p);
+      store_pair(S, d0, d1, lane, H.dz2, H.tile0, p);
+    }
   }
-  __syncthreads();   // every q(dz2) fragment written
   // hidden 1: dz1 = (W2^T q(dz2)) (1 - h1^2), h1 recomputed; gx = W1^T q(dz1)
 #pragma unroll
   for (int m = 0; m < 2; ++m)
@@ -276,12 +297,11 @@ __device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8 X[NT], 
     for (int nt = 0; nt < NT; ++nt) e0[nt] = e1[nt] = zero4();
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
-      const bf16x8 a0 = fr(N, F_W2T + 16 * q + p, lane), a1 = fr(N, F_W2T + 16 * q + 8 + p, lane);
+      const bf16x8 a0 = w2t[(16 * q + p) * 64 + lane], a1 = w2t[(16 * q + 8 + p) * 64 + lane];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const bf16x8 bz = S.Dz[p][nt][lane];
-        e0[nt] = mfma(a0, bz, e0[nt]);
-        e1[nt] = mfma(a1, bz, e1[nt]);
+        e0[nt] = mfma(a0, dz[p][nt], e0[nt]);
+        e1[nt] = mfma(a1, dz[p][nt], e1[nt]);
       }
     }
     const bf16x8 w0 = fr(N, F_W1 + 2 * q, lane), w1 = fr(N, F_W1 + 2 * q + 1, lane);
@@ -312,6 +332,14 @@ __device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8 X[NT], 
       for (int m = 0; m < 2; ++m) gx[m][nt] = mfma(fr(N, F_W1T + 8 * m + q, lane), bz, gx[m][nt]);
     }
   }
+}
+
+// The 128 fragments starting at `first` of a network's array into LDS (every lane its slots).
+__device__ __forceinline__ void fill_lds(Lds& S, const NetF& N, int first, int lane) {
+  lds_sync();   // earlier readers of S.W are done
+#pragma unroll 8
+  for (int f = 0; f < 128; ++f) S.W[f][lane] = N.f[(first + f) * 64 + lane];
+  lds_sync();
 }
 
 // ---------------------------------------------------------- lane <-> fragment moves ----
@@ -503,6 +531,7 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
   for (int j = 0; j < 6; ++j) sig[j] = MODE == MODE_SAMPLE ? expf(A.log_std[j]) : 0.0f;
 
   // ---------------------------------------------------------------- forward sweep
+  if (MODE != MODE_EXTERNAL) fill_lds(S, A.pol, F_W2, lane);
   float Jr = 0.0f;
   for (int t = 0; t < h; ++t) {
     ck_store(A.ck, Np, t, i, x, ab);
@@ -512,15 +541,15 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
       for (int j = 0; j < 6; ++j) a[j] = A.ext[((size_t)j * h + t) * Nz + ic];
     } else {
-      __syncthreads();
+      lds_sync();
       put_inputs(S, lane, o);
-      __syncthreads();
+      lds_sync();
       bf16x8 X[NT];
       input_frags(S, lane, X);
       f32x4 y[NT];
-      mlp_forward(A.pol, X, lane, y);
+      mlp_forward(A.pol, &S.W[0][0], X, lane, y, A.h2s + ((size_t)t * gridDim.x + blockIdx.x) * H2_F4);
       put_outputs(S, lane, y);
-      __syncthreads();
+      lds_sync();
 #pragma unroll
       for (int j = 0; j < 6; ++j) a[j] = S.Y[lane][j];
       if (MODE == MODE_SAMPLE) {
@@ -567,29 +596,30 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
   for (int k = 0; k < 12; ++k) go_h[k] = 0.0f;
   float vlast = 0.0f;
   if (A.has_val) {
-    __syncthreads();
+    lds_sync();
     put_inputs(S, lane, oh);
-    __syncthreads();
+    lds_sync();
     bf16x8 X[NT];
     input_frags(S, lane, X);
     f32x4 y[NT];
-    mlp_forward(A.val, X, lane, y);
+    f32x4* h2v = A.h2v + (size_t)blockIdx.x * H2_F4;
+    mlp_forward(A.val, A.val.f + F_W2 * 64, X, lane, y, h2v);
     put_outputs(S, lane, y);
     float gy[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) gy[j] = 0.0f;
     gy[0] = valid ? -powf(A.gamma, (float)h) * A.inv_nh : 0.0f;
     put_gy(S, lane, gy);
-    __syncthreads();
+    lds_sync();
     vlast = S.Y[lane][0];
     bf16x8 GY[NT];
     gy_frags(S, lane, GY);
     f32x4 gx[2][NT];
     const HalfOut off{nullptr, nullptr, nullptr, nullptr, 0, false};
-    mlp_backward(A.val, X, GY, lane, S, gx, off);
-    __syncthreads();
+    mlp_backward(A.val, A.val.f + F_W2T * 64, X, GY, lane, S, gx, off, h2v);
+    lds_sync();
     put_gx(S, lane, gx);
-    __syncthreads();
+    lds_sync();
 #pragma unroll
     for (int k = 0; k < 12; ++k) go_h[k] = S.GX[lane][k];
   }
@@ -640,6 +670,7 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
   }
 
   // ---------------------------------------------------------------- reverse sweep
+  if (MODE != MODE_EXTERNAL) fill_lds(S, A.pol, F_W2T, lane);
   adj::X13<float> lam;
   adj::zero(lam);
   adj::observe_vjp(x, pg, qg, go_h, lam);
@@ -710,10 +741,10 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
       // the policy's input gradient at o_t = o(s_t)
       float ot[12];
       adj::observe(x0, pg, qg, ot);
-      __syncthreads();
+      lds_sync();
       put_inputs(S, lane, ot);
       put_gy(S, lane, ga);
-      __syncthreads();
+      lds_sync();
       bf16x8 X[NT], GY[NT];
       input_frags(S, lane, X);
       gy_frags(S, lane, GY);
@@ -721,10 +752,11 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
       if (A.want_grad) store_input_halves(S, lane, A.x_half, A.gy_half, tile0);
       const HalfOut H{A.h1_half, A.h2_half, A.dz2_half, A.dz1_half, tile0, A.want_grad != 0};
       f32x4 gx[2][NT];
-      mlp_backward(A.pol, X, GY, lane, S, gx, H);
-      __syncthreads();
+      mlp_backward(A.pol, &S.W[0][0], X, GY, lane, S, gx, H,
+                   A.h2s + ((size_t)t * gridDim.x + blockIdx.x) * H2_F4);
+      lds_sync();
       put_gx(S, lane, gx);
-      __syncthreads();
+      lds_sync();
       float gxo[12];
 #pragma unroll
       for (int k = 0; k < 12; ++k) gxo[k] = S.GX[lane][k];
@@ -879,7 +911,7 @@ __global__ __launch_bounds__(256) void k_zero(uint32_t* __restrict__ p, size_t n
 
 // ------------------------------------------------------------------ workspace ----------
 inline size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
-constexpr int WORK_PARTS = 20;
+constexpr int WORK_PARTS = 22;
 constexpr int MAX_GROUPS = 256;
 
 struct Shape {
@@ -912,7 +944,9 @@ inline size_t work_layout(int N, int h, size_t off[WORK_PARTS]) {
       G * HID * 16 * 4, G * HID * 4,        // 15 part_w3t, 16 part_b2
       G * 16 * 4 + G * 16 * 4,              // 17 part_b3 + part_ls
       G * HID * HID * 4,                    // 18 part_w2
-      4096 * 4};                            // 19 per-block sums of squares
+      4096 * 4,                             // 19 per-block sums of squares
+      (size_t)h * (Np / 64) * H2_F4 * 16,   // 20 policy hidden-2 activations
+      (Np / 64) * H2_F4 * 16};              // 21 value hidden-2 activations
   size_t o = 0;
   for (int k = 0; k < WORK_PARTS; ++k) {
     off[k] = o;
@@ -1007,6 +1041,8 @@ int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* pol
   A.h2_half = (u32x2*)at(10);
   A.dz2_half = (u32x2*)at(11);
   A.dz1_half = (u32x2*)at(12);
+  A.h2s = (f32x4*)at(20);
+  A.h2v = (f32x4*)at(21);
   A.Np = sh.Np;
   if (out) {
     A.ext = out->actions;
