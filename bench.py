@@ -295,10 +295,11 @@ SHAC_FLOP_PER_STEP = 3 * 2 * (12 * 256 + 256 * 256 + 256 * 6)
 
 
 def shac_measure(n_envs: int, reps: int = 16) -> dict:
-    """SHAC actor windows on the paper task: h = 32 control steps of n_envs environments
-    with the sampled policy in the loop and a terminal value (auv_shac_window: forward,
-    reverse sweep through RK4 + Fossen and the policy, parameter gradient), then the actor's
-    Adam step.  Consecutive windows tile the 512-step episodes."""
+    """SHAC on the paper task: windows of h = 32 control steps of n_envs environments with the
+    sampled policy in the loop and a terminal value (auv_shac_window: forward, reverse sweep
+    through RK4 + Fossen and the policy, parameter gradient), the actor's Adam step, and the
+    critic's regression on the window's TD(lambda) targets (16 passes x 4 minibatches of
+    value-only gradient + Adam).  Consecutive windows tile the 512-step episodes."""
     import torch
 
     import workloads as W
@@ -312,23 +313,29 @@ def shac_measure(n_envs: int, reps: int = 16) -> dict:
     L = ShacLearner(env, W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.PAPER_VALUE_SEED, n_in=12),
                     h=h, gamma=W.SHAC["gamma"], max_grad_norm=W.SHAC["max_grad_norm"])
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    win, stp = [], []
+    win, stp, crit = [], [], []
     for k in range(reps + 1):
         torch.cuda.synchronize()
-        e = [ev() for _ in range(3)]
+        e = [ev() for _ in range(4)]
         e[0].record()
         L.window()
         e[1].record()
         L.step()
         e[2].record()
+        if k < 3:   # the critic's regression (16 passes x 4 minibatches) on the first windows only
+            L.critic_update(iterations=16, batches=4, seed=k)
+        e[3].record()
         torch.cuda.synchronize()
         if k:
             win.append(e[0].elapsed_time(e[1]) * 1e-3)
             stp.append(e[1].elapsed_time(e[2]) * 1e-3)
+            if k < 3:
+                crit.append(e[2].elapsed_time(e[3]) * 1e-3)
     st = L.stats.cpu().numpy()
     assert (st == st).all(), "non-finite SHAC statistics"
     tw = sorted(win)[len(win) // 2]
     ts = sorted(stp)[len(stp) // 2]
+    tc = sorted(crit)[len(crit) // 2]
     steps = n_envs * h
     windows_per_episode = cfg["episode_len"] // h
     return {"workload": f"SHAC on the paper task: {n_envs} envs, windows of {h} steps (sampled policy, terminal "
@@ -337,7 +344,9 @@ def shac_measure(n_envs: int, reps: int = 16) -> dict:
             "env_steps_per_s": steps / tw, "mfma_flop_per_env_step": SHAC_FLOP_PER_STEP,
             "achieved_TFLOPs": SHAC_FLOP_PER_STEP * steps / tw / 1e12,
             "frac_of_bf16_peak": SHAC_FLOP_PER_STEP * steps / tw / P_MFMA,
-            "hundred_episodes_actor_s": 100 * windows_per_episode * (tw + ts)}
+            "critic_ms": tc * 1e3, "iteration_ms": (tw + ts + tc) * 1e3,
+            "hundred_episodes_actor_s": 100 * windows_per_episode * (tw + ts),
+            "hundred_episodes_s": 100 * windows_per_episode * (tw + ts + tc)}
 
 
 def small_configs_measure(reps: int = 3) -> dict:

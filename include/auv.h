@@ -296,7 +296,9 @@ typedef struct {
 int64_t auv_ppo_work_bytes(int32_t B);
 
 /* Loss and gradients of one minibatch: entries idx[0..B-1] (int32 sample indices into the
- * batch; values outside [0, M) are clamped into it).  Overwrites grad_policy
+ * batch; values outside [0, M) are clamped into it).  policy may be NULL: then only the value
+ * loss and its gradient are computed (grad_policy, act, logp and adv are not read; stats[0],
+ * [3], [4], [5] are 0 and the entropy term is absent), e.g. for a critic's regression.  Overwrites grad_policy
  * [AUV_PPO_NPARAM(8)], grad_value [AUV_PPO_NPARAM(1)] and stats [8]: surrogate loss, value
  * loss, entropy, approximate KL (mean of logp_old - logp), fraction of samples whose
  * gradient the clip removes, squared gradient norms of policy and value, and the clipping

@@ -212,9 +212,10 @@ def auv_ppo_work_bytes(B: int) -> int:
     return int(lib.auv_ppo_work_bytes(B))
 
 
-def auv_ppo_grad(cfg: AuvPpoConfig, policy: AuvMlp, value: AuvMlp, batch: AuvPpoBatch, idx, B: int,
+def auv_ppo_grad(cfg: AuvPpoConfig, policy: AuvMlp | None, value: AuvMlp, batch: AuvPpoBatch, idx, B: int,
                  grad_policy, grad_value, stats, work, stream=None) -> None:
-    _check(lib.auv_ppo_grad(ctypes.byref(cfg), ctypes.byref(policy), ctypes.byref(value), ctypes.byref(batch),
+    _check(lib.auv_ppo_grad(ctypes.byref(cfg), ctypes.byref(policy) if policy is not None else None,
+                            ctypes.byref(value), ctypes.byref(batch),
                             ptr(idx), B, ptr(grad_policy), ptr(grad_value), ptr(stats), ptr(work),
                             stream_ptr(stream)))
 

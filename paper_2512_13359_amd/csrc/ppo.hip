@@ -761,7 +761,8 @@ __global__ __launch_bounds__(64) void k_finalize(int G1p, int G1v, Work W, int n
   vs = wave_sum(vs);
   if (lane == 0) {
     float ent = 0.0f;
-    for (int j = 0; j < hp.n_act; ++j) ent += log_std[j] + 0.5f * (1.0f + LOG_2PI);
+    if (log_std)
+      for (int j = 0; j < hp.n_act; ++j) ent += log_std[j] + 0.5f * (1.0f + LOG_2PI);
     stats[0] = pg * hp.inv_B;
     stats[1] = 0.5f * hp.vf_coef * vs * hp.inv_B;
     stats[2] = ent;
@@ -852,12 +853,18 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
                  const int32_t* idx, int32_t B, float* grad_policy, float* grad_value, float* stats, void* work,
                  void* stream) {
   if (int rc = check_ppo_config(cfg)) return rc;
-  if (int rc = check_net(policy, ACT, "auv_ppo_grad policy")) return rc;
+  const bool with_policy = policy != nullptr;
+  if (with_policy) {
+    if (int rc = check_net(policy, ACT, "auv_ppo_grad policy")) return rc;
+    if (!policy->log_std || !aligned16(policy->log_std))
+      return set_error(AUV_EINVAL, "auv_ppo_grad: policy needs an aligned log_std");
+  }
   if (int rc = check_net(value, 1, "auv_ppo_grad value")) return rc;
-  if (!policy->log_std || !aligned16(policy->log_std)) return set_error(AUV_EINVAL, "auv_ppo_grad: policy needs an aligned log_std");
   if (B < 1 || B > PPO_MAX_B) return set_error(AUV_EINVAL, "auv_ppo_grad: B must be in [1, %d], got %d", PPO_MAX_B, B);
   if (!batch || batch->M < 1 || batch->M > INT32_MAX) return set_error(AUV_EINVAL, "auv_ppo_grad: batch M must be in [1, 2^31)");
-  const void* ptrs[10] = {batch->obs, batch->act, batch->logp, batch->adv, batch->ret, idx, grad_policy, grad_value, stats, work};
+  const void* ptrs[10] = {batch->obs, with_policy ? batch->act : batch->obs, with_policy ? batch->logp : batch->obs,
+                          with_policy ? batch->adv : batch->obs, batch->ret, idx,
+                          with_policy ? grad_policy : grad_value, grad_value, stats, work};
   for (int k = 0; k < 10; ++k)
     if (!ptrs[k] || !aligned16(ptrs[k])) return set_error(AUV_EINVAL, "auv_ppo_grad: pointer %d NULL or not 16-byte aligned", k);
   hipStream_t s = (hipStream_t)stream;
@@ -869,26 +876,28 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
                    cfg->normalize_adv ? 1 : 0, cfg->n_actions ? cfg->n_actions : ACT};
   const ppo::Batch D{batch->obs, batch->act, batch->logp, batch->adv, batch->ret, (size_t)batch->M};
   const int rb = ppo::red_blocks(ACT);
-  if (hp.normalize) {
-    hipLaunchKernelGGL(ppo::k_adv_partial, dim3(ppo::ADV_BLOCKS), dim3(256), 0, s, batch->adv, idx, B, (int)batch->M,
-                       W.adv_part);
-    hipLaunchKernelGGL(ppo::k_adv_final, dim3(1), dim3(64), 0, s, W.adv_part, B, W.advstat);
-  }
   constexpr int FPW = ppo::FPW, TH = 64 * HID / FPW;
-  hipLaunchKernelGGL((ppo::k_fwd_bwd<8, FPW>), dim3(G1), dim3(TH), 0, s, policy->w, policy->b, policy->log_std, D, idx,
-                     B, tiles, hp, W, 0);
-  hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
-  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G3, W, cfg->ent_coef,
-                     grad_policy, W.part_ss);
+  if (with_policy) {
+    if (hp.normalize) {
+      hipLaunchKernelGGL(ppo::k_adv_partial, dim3(ppo::ADV_BLOCKS), dim3(256), 0, s, batch->adv, idx, B, (int)batch->M,
+                         W.adv_part);
+      hipLaunchKernelGGL(ppo::k_adv_final, dim3(1), dim3(64), 0, s, W.adv_part, B, W.advstat);
+    }
+    hipLaunchKernelGGL((ppo::k_fwd_bwd<8, FPW>), dim3(G1), dim3(TH), 0, s, policy->w, policy->b, policy->log_std, D,
+                       idx, B, tiles, hp, W, 0);
+    hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
+    hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+    hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G3, W, cfg->ent_coef,
+                       grad_policy, W.part_ss);
+  }
   hipLaunchKernelGGL((ppo::k_fwd_bwd<1, FPW>), dim3(G1), dim3(TH), 0, s, value->w, value->b, (const float*)nullptr, D,
                      idx, B, tiles, hp, W, 1);
   hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, value->w, value->b, D, idx, B, tiles, W);
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, G1, G1, G3, W, 0.0f,
                      grad_value, W.part_ss + rb);
-  hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, G1, G1, W, rb, ppo::red_blocks(1), rb, policy->log_std, hp,
-                     stats);
+  hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, with_policy ? G1 : 0, G1, W, with_policy ? rb : 0,
+                     ppo::red_blocks(1), rb, with_policy ? policy->log_std : (const float*)nullptr, hp, stats);
   return check_launch("auv_ppo_grad");
 }
 

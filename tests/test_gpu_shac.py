@@ -283,3 +283,35 @@ def test_shac_full_size_sampled_envs():
     scale = idx.size / n
     assert rel_err(got["reward"][:, idx], want["rewards"]).max() <= 2e-3
     assert _block_err(ga[:, :, idx], want["grad_act"] * scale) <= 5e-2
+
+
+def test_shac_critic_regression():
+    """The critic's value-only gradient equals the value part of a full PPO gradient call on
+    the same minibatch (same kernels, bit for bit); TD(lambda) targets are consistent
+    (R = A + V); fitting the window's targets lowers the value loss."""
+    n, h = 130, 6
+    announce(f"SHAC critic n={n} h={h}")
+    require_gpu()
+    from paper_2512_13359_amd import _abi as A
+    _, g, _ = _setup(n, seed=14)
+    L = _learner(g, h)
+    L.window()
+    L.targets()
+    assert float(torch.max(torch.abs(L.ret - L.values - L.adv))) <= 1e-6 * float(torch.max(torch.abs(L.ret)))
+    M = h * n
+    b = L._last
+    batch = A.make_ppo_batch(b["obs"], b["obs"], L.values, L.adv, L.ret, M)
+    idx = torch.arange(0, 256, dtype=torch.int32, device="cuda")
+    work = torch.empty(A.auv_ppo_work_bytes(256), dtype=torch.uint8, device="cuda")
+    gv1, st1 = torch.zeros_like(L.grad_v), torch.zeros(8, device="cuda")
+    A.auv_ppo_grad(L.critic_cfg, None, L.val.mlp, batch, idx, 256, None, gv1, st1, work)
+    gp, gv2, st2 = torch.zeros_like(L.grad), torch.zeros_like(L.grad_v), torch.zeros(8, device="cuda")
+    pbatch = A.make_ppo_batch(b["obs"], torch.zeros(8, M, device="cuda"), torch.zeros(M, device="cuda"), L.adv, L.ret, M)
+    A.auv_ppo_grad(L.critic_cfg, L.pol.mlp, L.val.mlp, pbatch, idx, 256, gp, gv2, st2, work)
+    assert torch.equal(gv1, gv2)
+    assert host(st1)[1] == host(st2)[1] and host(st1)[0] == 0.0
+    before = float(torch.mean((L.values - L.ret) ** 2))
+    L.critic_update(iterations=8, batches=4)
+    A.auv_mlp_forward(L.val.mlp, M, b["obs"], L.values)
+    after = float(torch.mean((L.values - L.ret) ** 2))
+    assert after < 0.8 * before, (before, after)
