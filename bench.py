@@ -94,7 +94,8 @@ def cpu_baseline(cfg: dict, n_steps: int) -> dict:
 def c5_measure(reps: int = 3) -> dict:
     """PPO-buffer workload (65536 envs x 64 steps, sampled actions, value head, staggered
     episodes): rollout time and write bandwidth of the structure-of-arrays buffer, then the
-    GAE scan with its inputs evicted from the Infinity Cache (cold) and resident (warm)."""
+    GAE scan with its inputs evicted from the Infinity Cache (cold) and resident (warm), each
+    timed over six back-to-back scans."""
     import torch
 
     import workloads as W
@@ -123,22 +124,33 @@ def c5_measure(reps: int = 3) -> dict:
     buf_bytes = (A.OBS_DIM + A.ACT_DIM + 4) * 4 * T * n + 4 * n
     adv = torch.empty(T, n, device="cuda")
     ret = torch.empty(T, n, device="cuda")
-    scratch = torch.empty(1 << 27, device="cuda")   # 512 MiB, evicts the 256 MB Infinity Cache
+    # 512 MiB swept by a read before a cold measurement: it evicts the 256 MB Infinity Cache and,
+    # unlike a write, leaves no dirty lines whose write-back the measured scans would pay for
+    scratch = torch.ones(1 << 27, device="cuda")
     gae_bytes = 20 * T * n + 4 * n
+    # K copies of the scan's inputs (6 x 50 MB, more than the Infinity Cache holds): cold = K
+    # back-to-back scans of the K copies after the cache was flushed, warm = K scans of one
+    # resident copy; per-scan time = events around the K launches / K (launch overhead amortised)
+    K = 6
+    copies = [[bufs[k].clone() for k in ("reward", "value", "done", "last_value")] for _ in range(K)]
     res = {}
     for kind in ("cold", "warm"):
         ts = []
         for _ in range(reps):
             if kind == "cold":
-                scratch.fill_(1.0)
+                scratch.sum()
+            else:
+                A.auv_gae(T, n, *copies[0], 0.99, 0.95, adv, ret)
             torch.cuda.synchronize()
             e0, e1 = ev(), ev()
             e0.record()
-            A.auv_gae(T, n, bufs["reward"], bufs["value"], bufs["done"], bufs["last_value"], 0.99, 0.95, adv, ret)
+            for c in range(K):
+                A.auv_gae(T, n, *copies[c if kind == "cold" else 0], 0.99, 0.95, adv, ret)
             e1.record()
             torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e-3)
+            ts.append(e0.elapsed_time(e1) * 1e-3 / K)
         res[kind] = sorted(ts)[len(ts) // 2]
+    del copies
     return {"workload": f"c5: {n} envs x {T} steps, sampled actions + value head, staggered episodes, "
                         f"PPO buffer (obs 23, act 8, logp, value, reward, done fp32), GAE gamma 0.99 lambda 0.95",
             "rollout_ms": t_roll * 1e3, "env_steps_per_s": n * T / t_roll,

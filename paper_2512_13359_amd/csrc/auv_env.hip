@@ -305,6 +305,67 @@ __global__ __launch_bounds__(256) void k_gae(int T, int n, const float* __restri
   }
 }
 
+// Segmented backward GAE for T <= 16 L.  The recursion A_t = delta_t + c_t A_{t+1}, with
+// c_t = gamma lambda (1 - d_t) and delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t, is linear in
+// A: over a segment of steps [t0, t1) it gives A_t = alpha_t + beta_t A_{t1}, alpha from the
+// recursion started at 0, beta_t = c_t ... c_{t1-1}.  Wave w of a workgroup takes segment w
+// (L steps) of the workgroup's 64 environments, so the scan of one environment is spread over
+// up to 16 waves and every load is issued at once; the waves exchange (alpha, beta) of their
+// first step through LDS, and each folds the later segments, last one first, into the A that
+// enters its own segment.  Same arithmetic per step as k_gae; the fold adds one multiply-add.
+template <int L>
+__global__ __launch_bounds__(1024) void k_gae_seg(int T, int n, const float* __restrict__ rew,
+                                                  const float* __restrict__ val, const float* __restrict__ dn,
+                                                  const float* __restrict__ last, float gamma, float gl,
+                                                  float* __restrict__ adv, float* __restrict__ ret) {
+  __shared__ float2 pair[16][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, S = blockDim.x >> 6;
+  const int i = blockIdx.x * 64 + lane;
+  const bool valid = i < n;
+  const size_t N = (size_t)n, ic = (size_t)(valid ? i : n - 1);
+  const int t0 = w * L, t1 = min(T, t0 + L);
+  float r[L], v[L], d[L];
+#pragma unroll
+  for (int k = 0; k < L; ++k) {   // unconditional loads from clamped steps: all in flight at once
+    const size_t ti = (size_t)min(t0 + k, T - 1) * N + ic;
+    r[k] = rew[ti];
+    v[k] = val[ti];
+    d[k] = dn[ti];
+  }
+  float vnext = t1 < T ? val[(size_t)t1 * N + ic] : last[ic];
+  float a = 0.0f, b = 1.0f;
+#pragma unroll
+  for (int k = L - 1; k >= 0; --k) {
+    if (t0 + k < t1) {
+      const float nd = 1.0f - d[k];
+      const float delta = r[k] + gamma * nd * vnext - v[k];
+      const float c = gl * nd;
+      a = delta + c * a;
+      b = c * b;
+      vnext = v[k];
+    }
+    r[k] = a;   // alpha_t
+    d[k] = b;   // beta_t
+  }
+  pair[w][lane] = make_float2(a, b);
+  __syncthreads();
+  float ain = 0.0f;
+  for (int s2 = S - 1; s2 > w; --s2) {
+    const float2 q = pair[s2][lane];
+    ain = q.x + q.y * ain;
+  }
+  if (valid) {
+#pragma unroll
+    for (int k = 0; k < L; ++k)
+      if (t0 + k < t1) {
+        const size_t ti = (size_t)(t0 + k) * N + i;
+        const float A = r[k] + d[k] * ain;
+        adv[ti] = A;
+        ret[ti] = A + v[k];
+      }
+  }
+}
+
 int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s) {
   hipLaunchKernelGGL(k_stats_reduce, dim3((3 * T + 63) / 64), dim3(64 * RED_WAVES), 0, s, work, T, G, stats);
   return check_launch("stats reduce");
@@ -605,8 +666,20 @@ int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value, 
     if (!p[k] || !aligned16(p[k])) return set_error(AUV_EINVAL, "auv_gae: buffer %d NULL or misaligned", k);
   if (!std::isfinite(gamma) || !std::isfinite(lambda))
     return set_error(AUV_EINVAL, "auv_gae: gamma and lambda must be finite");
-  hipLaunchKernelGGL(k_gae, dim3((n_envs + 255) / 256), dim3(256), 0, (hipStream_t)stream, T, n_envs,
-                     reward, value, done, last_value, gamma, gamma * lambda, adv, ret);
+  hipStream_t s = (hipStream_t)stream;
+  const int groups = (n_envs + 63) / 64;
+  if (T <= 16 * 16) {
+    const int S = (T + 15) / 16;
+    hipLaunchKernelGGL(k_gae_seg<16>, dim3(groups), dim3(64 * S), 0, s, T, n_envs, reward, value, done, last_value,
+                       gamma, gamma * lambda, adv, ret);
+  } else if (T <= 16 * 32) {
+    const int S = (T + 31) / 32;
+    hipLaunchKernelGGL(k_gae_seg<32>, dim3(groups), dim3(64 * S), 0, s, T, n_envs, reward, value, done, last_value,
+                       gamma, gamma * lambda, adv, ret);
+  } else {
+    hipLaunchKernelGGL(k_gae, dim3((n_envs + 255) / 256), dim3(256), 0, s, T, n_envs, reward, value, done,
+                       last_value, gamma, gamma * lambda, adv, ret);
+  }
   return check_launch("auv_gae");
 }
 

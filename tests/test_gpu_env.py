@@ -217,7 +217,9 @@ def test_checkpoint_resume_bit_exact():
 def test_gae_parity():
     require_gpu()
     from paper_2512_13359_amd import _abi as A
-    for T, n in ((64, 65536), (37, 1001), (1, 5)):
+    # segmented scan with 16-step segments (T <= 256), 32-step segments (T <= 512), and the
+    # one-lane-per-env scan beyond; ragged env counts and partial last segments
+    for T, n in ((64, 65536), (37, 1001), (1, 5), (256, 300), (512, 4096), (300, 777), (600, 130)):
         announce(f"gae T={T} n={n}")
         r = np.random.default_rng(T)
         rew = r.normal(size=(T, n)).astype(np.float32)
