@@ -7,15 +7,24 @@
 // Kernels, in launch order:
 //   k_frags        the bf16 weights of each network rearranged into the MFMA A fragments
 //                  that the window kernel reads (W1, W2, W3 and their transposes)
-//   k_window<mode> one wave per 64 environments (one lane each), the whole window in one
-//                  launch: forward sweep (policy on MFMA, RK4 of the paper task, reward,
-//                  checkpoints of every step's state and action average), terminal value
-//                  and its input gradient, the environment update (reset where the window
-//                  ends the episode), then the reverse sweep: per step, the state adjoint
-//                  through reward, observation and RK4 (shac_adjoint.hpp), the clip, and the
-//                  policy's input gradient (forward recomputed from the checkpoint, then
-//                  backward on MFMA).  It stores every step's bf16 operands of the weight
-//                  gradient (q(o), q(h1), q(h2), q(gy), q(dz2), q(dz1)) as "half fragments"
+//   k_window<mode> one workgroup of four waves per 16 environments, the whole window in one
+//                  launch.  Every wave steps the physics of all 16 environments (lane r and
+//                  its copies r + 16, r + 32, r + 48 hold environment r), so each wave has
+//                  the observations, actions and adjoints it needs without an exchange;
+//                  the networks are split by hidden feature, wave w owning features
+//                  64 w .. 64 w + 63 of both hidden layers (its 64 rows of W2, then of W2^T,
+//                  in LDS).  At workgroup barriers the waves exchange through LDS only the
+//                  output partials (one barrier per forward step), q(dz2) and the
+//                  input-gradient partials (two per reverse step).  Forward sweep: policy
+//                  on MFMA, RK4 of the paper task, reward, checkpoints of every step's state
+//                  and action average, every wave's hidden-2 activations; terminal value and
+//                  its input gradient; the environment update (reset where the window ends
+//                  the episode); reverse sweep: per step, the state adjoint through reward,
+//                  observation and RK4 (shac_adjoint.hpp), the clip, and the policy's input
+//                  gradient (backward on MFMA from the stored hidden-2 activations).  Each
+//                  wave stores the bf16 operands of the weight gradient of its features
+//                  (q(h1), q(h2), q(dz2), q(dz1); wave 0 also q(o), q(gy)) as "half
+//                  fragments"
 //   k_dw2          (PPO update) dW2 = sum q(dz2) q(h1)^T over all N h samples
 //   k_wsmall       dW1, dW3, the bias gradients and d log_std, per workgroup
 //   k_reduce       (PPO update) fixed-order sums of the partials -> packed gradient
@@ -23,10 +32,10 @@
 //
 // MFMA layout as in mlp_mfma.hpp (v_mfma_f32_16x16x32_bf16, lane l = 16 g + r, K slot
 // (g, j) = feature 16 (j / 4) + 4 g + j % 4 of a 32-wide K step).  In the window kernel
-// the N dimension is the wave's 64 environments (four N-tiles), M the output features.
+// the N dimension is the workgroup's 16 environments (one N-tile), M the output features.
 // A half fragment (8 bytes, lane (g, r)) holds feature r of a 16-feature tile for
-// samples 4g .. 4g + 3 of a 16-sample tile; sample tile (t, workgroup, n-tile) =
-// (t G + workgroup) 4 + n-tile, G = workgroups.
+// samples 4g .. 4g + 3 of a 16-sample tile; sample tile (t, workgroup) = t G + workgroup,
+// G = workgroups.
 #include <cmath>
 
 #include "auv_internal.hpp"
@@ -38,10 +47,12 @@ namespace shac {
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-constexpr int NT = 4;                    // 16-environment N-tiles per wave
+constexpr int EPG = 16;                  // environments per workgroup (one MFMA N-tile)
+constexpr int WAVES = 4;                 // waves per workgroup; wave w owns hidden features 64 w ..
+constexpr int WF = 32;                   // W2 (or W2^T) fragments of one wave: 4 M-tiles x 8 K steps
 constexpr int MAX_H = 64;                // window length bound
 constexpr int MAX_S = 4;                 // RK4 substeps per control step bound
-constexpr int TS = 68;                   // bf16 row stride of the transpose buffer
+constexpr int TS = 20;                   // bf16 row stride of a transpose buffer
 constexpr int CK = 19;                   // checkpoint rows: state (13) and action average (6)
 constexpr int MODE_EXTERNAL = 0, MODE_MEAN = 2, MODE_SAMPLE = 3;
 
@@ -68,7 +79,7 @@ struct WinArgs {
   NetF pol, val;
   const float* log_std;
   float *ck, *acts, *J, *Jr, *vl, *gls;
-  f32x4 *h2s, *h2v;                    // hidden-2 activations: policy [h][G] wave-steps, value [G]
+  f32x4* h2s;                          // policy hidden-2 activations [h][G][wave][M-tile][lane]
   u32x2 *x_half, *h1_half, *h2_half, *gy_half, *dz2_half, *dz1_half;
   int Np;
   const float* ext;
@@ -76,17 +87,19 @@ struct WinArgs {
 };
 
 struct Lds {
-  bf16x8 W[128][64];      // the policy's W2 fragments (forward sweep), then its W2^T (reverse sweep)
-  __bf16 X[64][32];       // layer-1 inputs per environment
-  float Y[64][8];         // network outputs per environment
-  __bf16 G[64][8];        // q(dL/dy) per environment
-  float GX[64][32];       // input gradient per environment
-  __bf16 T[32 * TS];      // transpose buffer [feature][environment]
+  bf16x8 W[WAVES][WF][64];    // per wave: its W2 fragments (forward sweep), then its W2^T ones (reverse)
+  __bf16 X[WAVES][EPG][32];   // per wave: layer-1 inputs of the 16 environments
+  __bf16 G[WAVES][EPG][8];    // per wave: q(dL/dy)
+  __bf16 T[WAVES][32 * TS];   // per wave: transpose buffer [feature][environment]
+  float Y[2][WAVES][EPG][8];  // output partials of each wave (two buffers, alternate steps)
+  bf16x8 DZ[8][64];           // q(dz2) of all 256 features as the B operand (K step s: 32 s ..)
+  float GX[WAVES][EPG][16];   // input-gradient partials of each wave (inputs 0..15)
 };
+static_assert(sizeof(Lds) <= 160 * 1024, "window kernel LDS exceeds a CU's 160 KB");
 
-// Hidden-2 activations (fp32) of one wave-step, kept by the forward for the backward:
-// [32-feature chunk p][M-tile 2p or 2p + 1][N-tile][lane], 64 KB.
-constexpr int H2_F4 = 8 * 2 * NT * 64;
+// Hidden-2 activations (fp32) of one wave and step, kept by the forward for the backward:
+// [M-tile m][lane], features 64 w + 16 m + 4 g + i of environment r, 4 KB.
+constexpr int H2_F4 = 4 * 64;
 
 // ------------------------------------------------------------------ fragments ---------
 __global__ __launch_bounds__(256) void k_frags(const uint16_t* __restrict__ w, int n_out, bf16x8* __restrict__ out) {
@@ -126,7 +139,7 @@ __global__ __launch_bounds__(256) void k_frags(const uint16_t* __restrict__ w, i
   out[e] = v;
 }
 
-// ------------------------------------------------------------------ wave MLP ----------
+// ------------------------------------------------------------------ network pieces ----
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.0f, 0.0f, 0.0f, 0.0f}; }
 
 // biases rows r0 .. r0 + 3, times 2 log2 e (the argument scaling of tanh_bias)
@@ -145,206 +158,173 @@ __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
   return f;
 }
 
+__device__ __forceinline__ bf16x8 join2(u32x2 a, u32x2 b) {
+  return __builtin_bit_cast(bf16x8, (uint32_t __attribute__((ext_vector_type(4)))){a.x, a.y, b.x, b.y});
+}
+
 __device__ __forceinline__ bf16x8 fr(const NetF& N, int idx, int lane) { return N.f[idx * 64 + lane]; }
 
-// The window kernel's workgroup is one wave.  The LDS operations of a wave complete in the
-// order they are issued, so exchanging data between its lanes through LDS needs only that the
-// compiler keep the accesses in program order: a wavefront-scope fence and wave barrier (no
-// workgroup barrier, whose fence would also wait for every outstanding global load and store).
+// Exchange between the lanes of one wave through LDS: the LDS operations of a wave complete
+// in the order they are issued, so this needs only that the compiler keep the accesses in
+// program order (a wavefront-scope fence and wave barrier).
 __device__ __forceinline__ void lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Hidden layer 1 of the wave's 64 environments as the B operand of layer 2: H1[K step][N-tile].
-__device__ __forceinline__ void layer1(const NetF& N, const bf16x8 X[NT], int lane, bf16x8 H1[8][NT]) {
+// Exchange between the waves of the workgroup: every wave's LDS writes before the barrier are
+// seen by every wave after it.  The fences cover LDS only, so the barrier does not wait for
+// the waves' outstanding global stores.
+__device__ __forceinline__ void wg_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Hidden layer 1 of the 16 environments, all 256 features, as the B operand of layer 2:
+// H1[K step p] = features 32 p .. 32 p + 31.
+__device__ __forceinline__ void layer1(const NetF& N, const bf16x8& X, int lane, bf16x8 H1[8]) {
   const int g = lane >> 4;
 #pragma unroll
   for (int p = 0; p < 8; ++p) {
-    const bf16x8 a0 = fr(N, F_W1 + 2 * p, lane), a1 = fr(N, F_W1 + 2 * p + 1, lane);
     const f32x4 b0 = bias_k(N.b, 32 * p + 4 * g), b1 = bias_k(N.b, 32 * p + 16 + 4 * g);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) H1[p][nt] = act_frag(mfma(a0, X[nt], zero4()), mfma(a1, X[nt], zero4()), b0, b1);
+    H1[p] = act_frag(mfma(fr(N, F_W1 + 2 * p, lane), X, zero4()), mfma(fr(N, F_W1 + 2 * p + 1, lane), X, zero4()),
+                     b0, b1);
   }
 }
 
-// Pre-activations of hidden-2 features 32 p .. 32 p + 31 (M-tiles 2p, 2p + 1); w2: the 128
-// W2 fragments (in LDS, or the network's array in global memory).
-__device__ __forceinline__ void layer2_chunk(const bf16x8* w2, const bf16x8 H1[8][NT], int p, int lane, f32x4 z0[NT],
-                                             f32x4 z1[NT]) {
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) z0[nt] = z1[nt] = zero4();
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    const bf16x8 a0 = w2[(16 * p + s) * 64 + lane], a1 = w2[(16 * p + 8 + s) * 64 + lane];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      z0[nt] = mfma(a0, H1[s][nt], z0[nt]);
-      z1[nt] = mfma(a1, H1[s][nt], z1[nt]);
-    }
-  }
-}
-
-// Network outputs y (lane (g, r): rows 4g .. 4g + 3 of environment 16 nt + r).  w2: the
-// W2 fragments to read; h2: where this wave-step's hidden-2 activations go (H2_F4 f32x4).
-__device__ __forceinline__ void mlp_forward(const NetF& N, const bf16x8* w2, const bf16x8 X[NT], int lane, f32x4 y[NT],
-                                            f32x4* __restrict__ h2) {
+// Wave w's part of the forward pass: its hidden-2 activations h2[m] (fp32 after tanh; lane
+// (g, r): features 64 w + 16 m + 4 g + i of environment r) and, returned, its partial of the
+// outputs over those 64 features (lane (g, r): rows 4 g .. 4 g + 3).  w2: the wave's 32 W2
+// fragments [M-tile m][K step s] (in LDS, or the network's array in global memory).
+__device__ __forceinline__ f32x4 mlp_forward(const NetF& N, const bf16x8* w2, const bf16x8& X, int w, int lane,
+                                             f32x4 h2[4]) {
   const int g = lane >> 4;
-  bf16x8 H1[8][NT];
+  bf16x8 H1[8];
   layer1(N, X, lane, H1);
+  f32x4 z[4] = {zero4(), zero4(), zero4(), zero4()};
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) y[nt] = zero4();
-#pragma unroll 1
-  for (int p = 0; p < 8; ++p) {
-    f32x4 z0[NT], z1[NT];
-    layer2_chunk(w2, H1, p, lane, z0, z1);
-    const f32x4 b0 = bias_k(N.b + HID, 32 * p + 4 * g), b1 = bias_k(N.b + HID, 32 * p + 16 + 4 * g);
-    const bf16x8 w3 = fr(N, F_W3 + p, lane);
+  for (int s = 0; s < 8; ++s)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
+    for (int m = 0; m < 4; ++m) z[m] = mfma(w2[(8 * m + s) * 64 + lane], H1[s], z[m]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        z0[nt][i] = tanh_bias(z0[nt][i], b0[i]);
-        z1[nt][i] = tanh_bias(z1[nt][i], b1[i]);
-      }
-      h2[((2 * p) * NT + nt) * 64 + lane] = z0[nt];
-      h2[((2 * p + 1) * NT + nt) * 64 + lane] = z1[nt];
-      y[nt] = mfma(w3, pack8(z0[nt], z1[nt]), y[nt]);
-    }
+  for (int m = 0; m < 4; ++m) {
+    const f32x4 bk = bias_k(N.b + HID, 64 * w + 16 * m + 4 * g);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) h2[m][i] = tanh_bias(z[m][i], bk[i]);
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 4 * g + i;
-    const float b3 = row < N.n_out ? N.b[2 * HID + row] : 0.0f;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) y[nt][i] += b3;
-  }
+  const f32x4 y = mfma(fr(N, F_W3 + 2 * w, lane), pack8(h2[0], h2[1]), zero4());
+  return mfma(fr(N, F_W3 + 2 * w + 1, lane), pack8(h2[2], h2[3]), y);
 }
 
 // Where the reverse sweep writes the weight-gradient operands of one step.
 struct HalfOut {
   u32x2 *h1, *h2, *dz2, *dz1;
-  size_t tile0;   // first of the wave's four sample tiles
+  size_t tile;   // the workgroup's sample tile of this step
   bool on;
 };
 
 // D values of the M-tile pair (2c, 2c + 1) (features 32 c + 4 g + i and 32 c + 16 + 4 g + i,
-// environment 16 nt + r) -> bf16 half fragments of feature tiles 2c, 2c + 1 of the wave's
-// four sample tiles (16 feature tiles per sample tile).
-__device__ __forceinline__ void store_pair(Lds& S, const f32x4 v0[NT], const f32x4 v1[NT], int lane, u32x2* dst,
-                                           size_t tile0, int c) {
+// environment r) -> bf16 half fragments of feature tiles 2c, 2c + 1 of the sample tile,
+// through wave w's transpose buffer.
+__device__ __forceinline__ void store_pair(Lds& S, int w, const f32x4& v0, const f32x4& v1, int lane, u32x2* dst,
+                                           size_t tile, int c) {
   const int g = lane >> 4, r = lane & 15;
+  __bf16* T = S.T[w];
   lds_sync();   // earlier readers of the buffer are done
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      S.T[(4 * g + i) * TS + 16 * nt + r] = (__bf16)v0[nt][i];
-      S.T[(16 + 4 * g + i) * TS + 16 * nt + r] = (__bf16)v1[nt][i];
-    }
+  for (int i = 0; i < 4; ++i) {
+    T[(4 * g + i) * TS + r] = (__bf16)v0[i];
+    T[(16 + 4 * g + i) * TS + r] = (__bf16)v1[i];
+  }
   lds_sync();
 #pragma unroll
   for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      dst[((tile0 + nt) * 16 + 2 * c + hf) * 64 + lane] =
-          *reinterpret_cast<const u32x2*>(&S.T[(16 * hf + r) * TS + 16 * nt + 4 * g]);
+    dst[(tile * 16 + 2 * c + hf) * 64 + lane] = *reinterpret_cast<const u32x2*>(&T[(16 * hf + r) * TS + 4 * g]);
 }
 
-// Backward from q(dL/dy) (GY, B operand with K = the output rows) given the layer-1 operand X
-// and the step's stored hidden-2 activations h2: the input gradient gx[M-tile][N-tile] (lane
-// (g, r): inputs 16 m + 4 g + i of environment 16 nt + r) and, with H.on, the step's operands
-// of the weight gradient.  w2t: the 128 W2^T fragments to read.  Hidden layer 1 is recomputed
-// from X (one K step per 32 features).
-__device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, const bf16x8 X[NT], const bf16x8 GY[NT],
-                                             int lane, Lds& S, f32x4 gx[2][NT], const HalfOut& H,
-                                             const f32x4* __restrict__ h2) {
-  const int g = lane >> 4;
-  // hidden 2: dz2 = (W3^T q(gy)) (1 - h2^2), as the B operand of the W2^T product
-  bf16x8 dz[8][NT];
+// Wave w's part of the backward pass from q(dL/dy) (GY, B operand with K = the output rows),
+// the layer-1 operand X and the wave's hidden-2 activations h2: dz2 of its features, given
+// to the other waves through LDS; dz1 = (W2^T q(dz2)) (1 - h1^2) of its hidden-1 features
+// (h1 recomputed from X); its partial of the input gradient W1^T q(dz1), and the sum of the
+// four waves' partials in wave order, gxo (inputs 0..11 of environment r).  With H.on it
+// also stores the weight-gradient operands of its features.  w2t: the wave's 32 W2^T
+// fragments [M-tile m][K step s].
+__device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, const bf16x8& X, const bf16x8& GY,
+                                             const f32x4 h2[4], int w, int lane, Lds& S, const HalfOut& H,
+                                             float gxo[12]) {
+  const int g = lane >> 4, r = lane & 15;
+  // hidden 2 (this wave's features): dz2 = (W3^T q(gy)) (1 - h2^2)
+  f32x4 d[4];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    f32x4 z0[NT], z1[NT], d0[NT], d1[NT];
-    const bf16x8 t0 = fr(N, F_W3T + 2 * p, lane), t1 = fr(N, F_W3T + 2 * p + 1, lane);
+  for (int m = 0; m < 4; ++m) {
+    d[m] = mfma(fr(N, F_W3T + 4 * w + m, lane), GY, zero4());
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      z0[nt] = h2[((2 * p) * NT + nt) * 64 + lane];
-      z1[nt] = h2[((2 * p + 1) * NT + nt) * 64 + lane];
-      d0[nt] = mfma(t0, GY[nt], zero4());
-      d1[nt] = mfma(t1, GY[nt], zero4());
+    for (int i = 0; i < 4; ++i) d[m][i] *= 1.0f - h2[m][i] * h2[m][i];
+  }
+  S.DZ[2 * w][lane] = pack8(d[0], d[1]);
+  S.DZ[2 * w + 1][lane] = pack8(d[2], d[3]);
+  if (H.on) {
+    store_pair(S, w, h2[0], h2[1], lane, H.h2, H.tile, 2 * w);
+    store_pair(S, w, h2[2], h2[3], lane, H.h2, H.tile, 2 * w + 1);
+    store_pair(S, w, d[0], d[1], lane, H.dz2, H.tile, 2 * w);
+    store_pair(S, w, d[2], d[3], lane, H.dz2, H.tile, 2 * w + 1);
+  }
+  wg_sync();
+  // hidden 1 (this wave's features): dz1 = (W2^T q(dz2)) (1 - h1^2), h1 recomputed
+  bf16x8 dz[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        d0[nt][i] *= 1.0f - z0[nt][i] * z0[nt][i];
-        d1[nt][i] *= 1.0f - z1[nt][i] * z1[nt][i];
-      }
-      dz[p][nt] = pack8(d0[nt], d1[nt]);
-    }
-    if (H.on) {
-      store_pair(S, z0, z1, lane, H.h2, H.tile0, p);
-      store_pair(S, d0, d1, lane, H.dz2, H.tile0, p);
+  for (int s = 0; s < 8; ++s) dz[s] = S.DZ[s][lane];
+  f32x4 e[4] = {zero4(), zero4(), zero4(), zero4()};
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int m = 0; m < 4; ++m) e[m] = mfma(w2t[(8 * m + s) * 64 + lane], dz[s], e[m]);
+  f32x4 k[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const f32x4 y = mfma(fr(N, F_W1 + 4 * w + m, lane), X, zero4());
+    const f32x4 bk = bias_k(N.b, 64 * w + 16 * m + 4 * g);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      k[m][i] = tanh_bias(y[i], bk[i]);
+      e[m][i] *= 1.0f - k[m][i] * k[m][i];
     }
   }
-  // hidden 1: dz1 = (W2^T q(dz2)) (1 - h1^2), h1 recomputed; gx = W1^T q(dz1)
+  if (H.on) {
+    store_pair(S, w, k[0], k[1], lane, H.h1, H.tile, 2 * w);
+    store_pair(S, w, k[2], k[3], lane, H.h1, H.tile, 2 * w + 1);
+    store_pair(S, w, e[0], e[1], lane, H.dz1, H.tile, 2 * w);
+    store_pair(S, w, e[2], e[3], lane, H.dz1, H.tile, 2 * w + 1);
+  }
+  // input gradient: the partial over this wave's hidden-1 features (M-tile 0: inputs 0..15)
+  f32x4 gx = mfma(fr(N, F_W1T + 2 * w, lane), pack8(e[0], e[1]), zero4());
+  gx = mfma(fr(N, F_W1T + 2 * w + 1, lane), pack8(e[2], e[3]), gx);
+  *reinterpret_cast<f32x4*>(&S.GX[w][r][4 * g]) = gx;
+  wg_sync();
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int j = 0; j < 12; ++j) {
+    float s = S.GX[0][r][j];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) gx[m][nt] = zero4();
-#pragma unroll 1
-  for (int q = 0; q < 8; ++q) {
-    f32x4 e0[NT], e1[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) e0[nt] = e1[nt] = zero4();
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      const bf16x8 a0 = w2t[(16 * q + p) * 64 + lane], a1 = w2t[(16 * q + 8 + p) * 64 + lane];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        e0[nt] = mfma(a0, dz[p][nt], e0[nt]);
-        e1[nt] = mfma(a1, dz[p][nt], e1[nt]);
-      }
-    }
-    const bf16x8 w0 = fr(N, F_W1 + 2 * q, lane), w1 = fr(N, F_W1 + 2 * q + 1, lane);
-    const f32x4 c0 = bias_k(N.b, 32 * q + 4 * g), c1 = bias_k(N.b, 32 * q + 16 + 4 * g);
-    f32x4 k0[NT], k1[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const f32x4 y0 = mfma(w0, X[nt], zero4()), y1 = mfma(w1, X[nt], zero4());
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        k0[nt][i] = tanh_bias(y0[i], c0[i]);
-        k1[nt][i] = tanh_bias(y1[i], c1[i]);
-      }
-    }
-    if (H.on) store_pair(S, k0, k1, lane, H.h1, H.tile0, q);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        e0[nt][i] *= 1.0f - k0[nt][i] * k0[nt][i];
-        e1[nt][i] *= 1.0f - k1[nt][i] * k1[nt][i];
-      }
-    if (H.on) store_pair(S, e0, e1, lane, H.dz1, H.tile0, q);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const bf16x8 bz = pack8(e0[nt], e1[nt]);
-#pragma unroll
-      for (int m = 0; m < 2; ++m) gx[m][nt] = mfma(fr(N, F_W1T + 8 * m + q, lane), bz, gx[m][nt]);
-    }
+    for (int v = 1; v < WAVES; ++v) s += S.GX[v][r][j];
+    gxo[j] = s;
   }
 }
 
-// The 128 fragments starting at `first` of a network's array into LDS (every lane its slots).
-__device__ __forceinline__ void fill_lds(Lds& S, const NetF& N, int first, int lane) {
-  lds_sync();   // earlier readers of S.W are done
+// The wave's 32 fragments of a network's array, starting at fragment `first`, into its LDS slice.
+__device__ __forceinline__ void fill_w(Lds& S, const NetF& N, int first, int w, int lane) {
+  lds_sync();   // earlier readers of the slice (this wave) are done
 #pragma unroll 8
-  for (int f = 0; f < 128; ++f) S.W[f][lane] = N.f[(first + f) * 64 + lane];
+  for (int f = 0; f < WF; ++f) S.W[w][f][lane] = N.f[(first + f) * 64 + lane];
   lds_sync();
 }
 
 // ---------------------------------------------------------- lane <-> fragment moves ----
-// This lane's 12 inputs (bf16) into row `lane` of S.X (rows 12..31 zero).
-__device__ __forceinline__ void put_inputs(Lds& S, int lane, const float o[12]) {
+// The 12 inputs (bf16) of environment `lane` into row `lane` of wave w's S.X (rows 12..31
+// zero); lanes 0..15 write.
+__device__ __forceinline__ void put_inputs(Lds& S, int w, int lane, const float o[12]) {
+  if (lane >= EPG) return;
   bf16x8 a, b, z;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -352,73 +332,55 @@ __device__ __forceinline__ void put_inputs(Lds& S, int lane, const float o[12]) 
     b[j] = (__bf16)(j < 4 ? o[8 + j] : 0.0f);
     z[j] = (__bf16)0.0f;
   }
-  bf16x8* row = reinterpret_cast<bf16x8*>(&S.X[lane][0]);
+  bf16x8* row = reinterpret_cast<bf16x8*>(&S.X[w][lane][0]);
   row[0] = a;
   row[1] = b;
   row[2] = z;
   row[3] = z;
 }
 
-__device__ __forceinline__ void input_frags(const Lds& S, int lane, bf16x8 X[NT]) {
+__device__ __forceinline__ bf16x8 input_frag(const Lds& S, int w, int lane) {
   const int g = lane >> 4, r = lane & 15;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const u32x2 lo = *reinterpret_cast<const u32x2*>(&S.X[16 * nt + r][4 * g]);
-    const u32x2 hi = *reinterpret_cast<const u32x2*>(&S.X[16 * nt + r][16 + 4 * g]);
-    X[nt] = __builtin_bit_cast(bf16x8, (uint32_t __attribute__((ext_vector_type(4)))){lo.x, lo.y, hi.x, hi.y});
-  }
+  return join2(*reinterpret_cast<const u32x2*>(&S.X[w][r][4 * g]),
+               *reinterpret_cast<const u32x2*>(&S.X[w][r][16 + 4 * g]));
 }
 
-// q(dL/dy) of this lane's environment (rows >= 6 zero) into S.G; B operand fragments.
-__device__ __forceinline__ void put_gy(Lds& S, int lane, const float gy[8]) {
+// q(dL/dy) of environment `lane` (rows >= 6 zero) into wave w's S.G; lanes 0..15 write.
+__device__ __forceinline__ void put_gy(Lds& S, int w, int lane, const float gy[8]) {
+  if (lane >= EPG) return;
   bf16x8 v;
 #pragma unroll
   for (int j = 0; j < 8; ++j) v[j] = (__bf16)gy[j];
-  *reinterpret_cast<bf16x8*>(&S.G[lane][0]) = v;
+  *reinterpret_cast<bf16x8*>(&S.G[w][lane][0]) = v;
 }
 
-__device__ __forceinline__ void gy_frags(const Lds& S, int lane, bf16x8 GY[NT]) {
+__device__ __forceinline__ bf16x8 gy_frag(const Lds& S, int w, int lane) {
   const int g = lane >> 4, r = lane & 15;
+  const u32x2 lo = g < 2 ? *reinterpret_cast<const u32x2*>(&S.G[w][r][4 * g]) : u32x2{0u, 0u};
+  return join2(lo, u32x2{0u, 0u});
+}
+
+// Output row j of environment r: the waves' partials summed in wave order.
+__device__ __forceinline__ float out_sum(const Lds& S, int b, int r, int j) {
+  float s = S.Y[b][0][r][j];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    u32x2 lo = u32x2{0u, 0u};
-    if (g < 2) lo = *reinterpret_cast<const u32x2*>(&S.G[16 * nt + r][4 * g]);
-    GY[nt] = __builtin_bit_cast(bf16x8, (uint32_t __attribute__((ext_vector_type(4)))){lo.x, lo.y, 0u, 0u});
+  for (int v = 1; v < WAVES; ++v) s += S.Y[b][v][r][j];
+  return s;
+}
+
+// Half fragments of wave 0's layer-1 inputs (feature tiles 0, 1) and of q(gy) (one tile).
+__device__ __forceinline__ void store_input_halves(const Lds& S, int lane, u32x2* xh, u32x2* gh, size_t tile) {
+  const int g = lane >> 4, r = lane & 15;
+  bf16x4 v;
+#pragma unroll
+  for (int ft = 0; ft < 2; ++ft) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) v[s] = S.X[0][4 * g + s][16 * ft + r];
+    xh[(tile * 2 + ft) * 64 + lane] = __builtin_bit_cast(u32x2, v);
   }
-}
-
-// Output rows of y to S.Y (rows 0..7 of each environment).
-__device__ __forceinline__ void put_outputs(Lds& S, int lane, const f32x4 y[NT]) {
-  const int g = lane >> 4, r = lane & 15;
-  if (g < 2)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) *reinterpret_cast<f32x4*>(&S.Y[16 * nt + r][4 * g]) = y[nt];
-}
-
-__device__ __forceinline__ void put_gx(Lds& S, int lane, const f32x4 gx[2][NT]) {
-  const int g = lane >> 4, r = lane & 15;
-#pragma unroll
-  for (int m = 0; m < 2; ++m)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) *reinterpret_cast<f32x4*>(&S.GX[16 * nt + r][16 * m + 4 * g]) = gx[m][nt];
-}
-
-// Half fragments of the layer-1 inputs (feature tiles 0, 1) and of q(gy) (one tile).
-__device__ __forceinline__ void store_input_halves(const Lds& S, int lane, u32x2* xh, u32x2* gh, size_t tile0) {
-  const int g = lane >> 4, r = lane & 15;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    bf16x4 v;
-#pragma unroll
-    for (int ft = 0; ft < 2; ++ft) {
-#pragma unroll
-      for (int s = 0; s < 4; ++s) v[s] = S.X[16 * nt + 4 * g + s][16 * ft + r];
-      xh[((tile0 + nt) * 2 + ft) * 64 + lane] = __builtin_bit_cast(u32x2, v);
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) v[s] = r < 8 ? S.G[16 * nt + 4 * g + s][r & 7] : (__bf16)0.0f;
-    gh[(tile0 + nt) * 64 + lane] = __builtin_bit_cast(u32x2, v);
-  }
+  for (int s = 0; s < 4; ++s) v[s] = r < 8 ? S.G[0][4 * g + s][r & 7] : (__bf16)0.0f;
+  gh[tile * 64 + lane] = __builtin_bit_cast(u32x2, v);
 }
 
 // ------------------------------------------------------------------ environment --------
@@ -495,13 +457,16 @@ __device__ __forceinline__ void ck_load(const float* ck, size_t Np, int t, int i
 
 // ------------------------------------------------------------------ window kernel ------
 template <int MODE>
-__global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs A) {
+__global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, WinArgs A) {
   __shared__ Lds S;
-  const int lane = threadIdx.x;
-  const int i = blockIdx.x * 64 + lane;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  const int i = blockIdx.x * EPG + r;
   const int N = E.n;
   const bool valid = i < N;
-  const int ic = valid ? i : N - 1;   // idle lanes step a copy of the last environment
+  const bool lead = threadIdx.x < EPG;   // the lanes that write the per-environment results
+  const int ic = valid ? i : N - 1;      // idle slots step a copy of the last environment
   const size_t Nz = (size_t)N, Np = (size_t)A.Np;
   const int h = A.steps;
   const uint32_t gid = E.env_offset + (uint32_t)i;
@@ -526,15 +491,22 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
   for (int j = 0; j < 6; ++j) ab[j] = E.obs[(12 + j) * Nz + ic];
   const bool ends = ep + h == E.H;
-  float sig[6];
+  float sig[6], b3[6];
 #pragma unroll
-  for (int j = 0; j < 6; ++j) sig[j] = MODE == MODE_SAMPLE ? expf(A.log_std[j]) : 0.0f;
+  for (int j = 0; j < 6; ++j) {
+    sig[j] = MODE == MODE_SAMPLE ? expf(A.log_std[j]) : 0.0f;
+    b3[j] = MODE != MODE_EXTERNAL ? A.pol.b[2 * HID + j] : 0.0f;
+  }
+  // this wave's hidden-2 activations of step t
+  auto h2_at = [&](int t) {
+    return A.h2s + (((size_t)t * gridDim.x + blockIdx.x) * WAVES + w) * H2_F4 + lane;
+  };
 
   // ---------------------------------------------------------------- forward sweep
-  if (MODE != MODE_EXTERNAL) fill_lds(S, A.pol, F_W2, lane);
+  if (MODE != MODE_EXTERNAL) fill_w(S, A.pol, F_W2 + WF * w, w, lane);
   float Jr = 0.0f;
   for (int t = 0; t < h; ++t) {
-    ck_store(A.ck, Np, t, i, x, ab);
+    if (lead) ck_store(A.ck, Np, t, i, x, ab);
     float o[12], a[6];
     adj::observe(x, pg, qg, o);
     if (MODE == MODE_EXTERNAL) {
@@ -542,16 +514,19 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
       for (int j = 0; j < 6; ++j) a[j] = A.ext[((size_t)j * h + t) * Nz + ic];
     } else {
       lds_sync();
-      put_inputs(S, lane, o);
+      put_inputs(S, w, lane, o);
       lds_sync();
-      bf16x8 X[NT];
-      input_frags(S, lane, X);
-      f32x4 y[NT];
-      mlp_forward(A.pol, &S.W[0][0], X, lane, y, A.h2s + ((size_t)t * gridDim.x + blockIdx.x) * H2_F4);
-      put_outputs(S, lane, y);
-      lds_sync();
+      const bf16x8 X = input_frag(S, w, lane);
+      f32x4 h2[4];
+      const f32x4 y = mlp_forward(A.pol, &S.W[w][0][0], X, w, lane, h2);
+      f32x4* hs = h2_at(t);
 #pragma unroll
-      for (int j = 0; j < 6; ++j) a[j] = S.Y[lane][j];
+      for (int m = 0; m < 4; ++m) hs[m * 64] = h2[m];
+      const int b = t & 1;
+      if (g < 2) *reinterpret_cast<f32x4*>(&S.Y[b][w][r][4 * g]) = y;
+      wg_sync();
+#pragma unroll
+      for (int j = 0; j < 6; ++j) a[j] = out_sum(S, b, r, j) + b3[j];
       if (MODE == MODE_SAMPLE) {
         float eps[6];
         paper_noise(E, gid, A.step0 + (uint32_t)t, eps);
@@ -559,9 +534,10 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
         for (int j = 0; j < 6; ++j) a[j] = __builtin_fmaf(sig[j], eps[j], a[j]);
       }
     }
+    if (lead)
 #pragma unroll
-    for (int j = 0; j < 6; ++j) A.acts[((size_t)t * 6 + j) * Np + i] = a[j];
-    if (valid) {
+      for (int j = 0; j < 6; ++j) A.acts[((size_t)t * 6 + j) * Np + i] = a[j];
+    if (lead && valid) {
       const size_t at = (size_t)t * Nz + i, rs = (size_t)h * Nz;
       if (A.o_obs)
 #pragma unroll
@@ -581,12 +557,13 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
     for (int j = 0; j < 6; ++j) ab[j] = __builtin_fmaf(K.beta, ab[j], (1.0f - K.beta) * u[j]);
     Jr = __builtin_fmaf(powf(A.gamma, (float)t), rw, Jr);
-    if (valid) {
+    if (lead && valid) {
       if (A.o_reward) A.o_reward[(size_t)t * Nz + i] = rw;
       if (A.o_done) A.o_done[(size_t)t * Nz + i] = (t == h - 1 && ends) ? 1.0f : 0.0f;
     }
   }
-  ck_store(A.ck, Np, h, i, x, ab);   // the final state, before any reset
+  if (lead) ck_store(A.ck, Np, h, i, x, ab);   // the final state, before any reset
+  __syncthreads();   // wave 0's checkpoints and actions are read by every wave in the reverse sweep
 
   // ------------------------------------------------ terminal value, its input gradient
   float oh[12];
@@ -596,36 +573,27 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
   for (int k = 0; k < 12; ++k) go_h[k] = 0.0f;
   float vlast = 0.0f;
   if (A.has_val) {
-    lds_sync();
-    put_inputs(S, lane, oh);
-    lds_sync();
-    bf16x8 X[NT];
-    input_frags(S, lane, X);
-    f32x4 y[NT];
-    f32x4* h2v = A.h2v + (size_t)blockIdx.x * H2_F4;
-    mlp_forward(A.val, A.val.f + F_W2 * 64, X, lane, y, h2v);
-    put_outputs(S, lane, y);
     float gy[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) gy[j] = 0.0f;
     gy[0] = valid ? -powf(A.gamma, (float)h) * A.inv_nh : 0.0f;
-    put_gy(S, lane, gy);
     lds_sync();
-    vlast = S.Y[lane][0];
-    bf16x8 GY[NT];
-    gy_frags(S, lane, GY);
-    f32x4 gx[2][NT];
+    put_inputs(S, w, lane, oh);
+    put_gy(S, w, lane, gy);
+    lds_sync();
+    const bf16x8 X = input_frag(S, w, lane), GY = gy_frag(S, w, lane);
+    f32x4 h2[4];
+    const f32x4 y = mlp_forward(A.val, A.val.f + (size_t)(F_W2 + WF * w) * 64, X, w, lane, h2);
+    const int b = h & 1;
+    if (g < 2) *reinterpret_cast<f32x4*>(&S.Y[b][w][r][4 * g]) = y;
+    wg_sync();
+    vlast = out_sum(S, b, r, 0) + A.val.b[2 * HID];
     const HalfOut off{nullptr, nullptr, nullptr, nullptr, 0, false};
-    mlp_backward(A.val, A.val.f + F_W2T * 64, X, GY, lane, S, gx, off, h2v);
-    lds_sync();
-    put_gx(S, lane, gx);
-    lds_sync();
-#pragma unroll
-    for (int k = 0; k < 12; ++k) go_h[k] = S.GX[lane][k];
+    mlp_backward(A.val, A.val.f + (size_t)(F_W2T + WF * w) * 64, X, GY, h2, w, lane, S, off, go_h);
   }
 
   // ------------------------------------------- environment update (reset at the episode end)
-  if (valid) {
+  if (lead && valid) {
     adj::X13<float> xn = x;
     float abn[6], on[12];
 #pragma unroll
@@ -633,11 +601,12 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
     for (int k = 0; k < 12; ++k) on[k] = oh[k];
     int epn = ep + h;
+    uint32_t epi = episode;
     if (ends) {
-      episode += 1u;
+      epi += 1u;
       State xs;
       Params Pn;
-      paper_reset_draws(E, gid, episode, xs, Pn);
+      paper_reset_draws(E, gid, epi, xs, Pn);
       store_params(E.params, N, i, Pn);
 #pragma unroll
       for (int k = 0; k < 3; ++k) {
@@ -665,17 +634,23 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
     for (int j = 0; j < 6; ++j) E.obs[(12 + j) * Nz + i] = abn[j];
     E.ep_step[i] = epn;
-    E.episode[i] = episode;
+    E.episode[i] = epi;
     if (A.o_vlast) A.o_vlast[i] = vlast;
   }
 
   // ---------------------------------------------------------------- reverse sweep
-  if (MODE != MODE_EXTERNAL) fill_lds(S, A.pol, F_W2T, lane);
+  if (MODE != MODE_EXTERNAL) fill_w(S, A.pol, F_W2T + WF * w, w, lane);
   adj::X13<float> lam;
   adj::zero(lam);
   adj::observe_vjp(x, pg, qg, go_h, lam);
   float lab[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f}, gls[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   for (int t = h - 1; t >= 0; --t) {
+    f32x4 h2[4];
+    if (MODE != MODE_EXTERNAL) {   // issued first: the loads complete during the state adjoint
+      const f32x4* hs = h2_at(t);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) h2[m] = hs[m * 64];
+    }
     adj::X13<float> x0;
     float abt[6], a[6], u[6], tau[6];
     ck_load(A.ck, Np, t, i, x0, abt);
@@ -728,7 +703,7 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
     for (int j = 0; j < 6; ++j) ga[j] = (a[j] >= -1.0f && a[j] <= 1.0f) ? gu[j] : 0.0f;
     ga[6] = ga[7] = 0.0f;
-    if (valid && A.o_gact)
+    if (lead && valid && A.o_gact)
 #pragma unroll
       for (int k = 0; k < 8; ++k) A.o_gact[((size_t)k * h + t) * Nz + i] = ga[k];
     if (MODE != MODE_EXTERNAL) {
@@ -742,30 +717,21 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
       float ot[12];
       adj::observe(x0, pg, qg, ot);
       lds_sync();
-      put_inputs(S, lane, ot);
-      put_gy(S, lane, ga);
+      put_inputs(S, w, lane, ot);
+      put_gy(S, w, lane, ga);
       lds_sync();
-      bf16x8 X[NT], GY[NT];
-      input_frags(S, lane, X);
-      gy_frags(S, lane, GY);
-      const size_t tile0 = ((size_t)t * gridDim.x + blockIdx.x) * NT;
-      if (A.want_grad) store_input_halves(S, lane, A.x_half, A.gy_half, tile0);
-      const HalfOut H{A.h1_half, A.h2_half, A.dz2_half, A.dz1_half, tile0, A.want_grad != 0};
-      f32x4 gx[2][NT];
-      mlp_backward(A.pol, &S.W[0][0], X, GY, lane, S, gx, H,
-                   A.h2s + ((size_t)t * gridDim.x + blockIdx.x) * H2_F4);
-      lds_sync();
-      put_gx(S, lane, gx);
-      lds_sync();
+      const bf16x8 X = input_frag(S, w, lane), GY = gy_frag(S, w, lane);
+      const size_t tile = (size_t)t * gridDim.x + blockIdx.x;
+      if (A.want_grad && w == 0) store_input_halves(S, lane, A.x_half, A.gy_half, tile);
+      const HalfOut H{A.h1_half, A.h2_half, A.dz2_half, A.dz1_half, tile, A.want_grad != 0};
       float gxo[12];
-#pragma unroll
-      for (int k = 0; k < 12; ++k) gxo[k] = S.GX[lane][k];
+      mlp_backward(A.pol, &S.W[w][0][0], X, GY, h2, w, lane, S, H, gxo);
       adj::observe_vjp(x0, pg, qg, gxo, lam);
     }
 #pragma unroll
     for (int j = 0; j < 6; ++j) lab[j] = gab[j];
   }
-  if (valid && A.o_gs0) {
+  if (lead && valid && A.o_gs0) {
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
       A.o_gs0[k * Nz + i] = lam.p[k];
@@ -775,11 +741,13 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 #pragma unroll
     for (int k = 0; k < 4; ++k) A.o_gs0[(3 + k) * Nz + i] = lam.q[k];
   }
-  A.J[i] = valid ? __builtin_fmaf(powf(A.gamma, (float)h), vlast, Jr) : 0.0f;
-  A.Jr[i] = valid ? Jr : 0.0f;
-  A.vl[i] = valid ? vlast : 0.0f;
+  if (lead) {
+    A.J[i] = valid ? __builtin_fmaf(powf(A.gamma, (float)h), vlast, Jr) : 0.0f;
+    A.Jr[i] = valid ? Jr : 0.0f;
+    A.vl[i] = valid ? vlast : 0.0f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) A.gls[j * Np + i] = (valid && j < 6) ? gls[j] : 0.0f;
+    for (int j = 0; j < 8; ++j) A.gls[j * Np + i] = (valid && j < 6) ? gls[j] : 0.0f;
+  }
 }
 
 // ------------------------------------------------------------------ small products -----
@@ -787,10 +755,6 @@ __global__ __launch_bounds__(64, 1) void k_window(EnvArgs E, VehArgs V, WinArgs 
 // dW1 = sum q(dz1) q(o)^T, dW3^T = sum q(h2) q(gy)^T, db1 = sum q(dz1), db2 = sum q(dz2),
 // db3 = sum q(gy); and d log_std = sum over this workgroup's share of the environments.
 // Four waves: wave w owns hidden features 64 w .. 64 w + 63 (M-tiles 4w .. 4w + 3).
-__device__ __forceinline__ bf16x8 join2(u32x2 a, u32x2 b) {
-  return __builtin_bit_cast(bf16x8, (uint32_t __attribute__((ext_vector_type(4)))){a.x, a.y, b.x, b.y});
-}
-
 __device__ __forceinline__ float sum8(const bf16x8& v) {
   float s = 0.0f;
 #pragma unroll
@@ -911,7 +875,7 @@ __global__ __launch_bounds__(256) void k_zero(uint32_t* __restrict__ p, size_t n
 
 // ------------------------------------------------------------------ workspace ----------
 inline size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
-constexpr int WORK_PARTS = 22;
+constexpr int WORK_PARTS = 21;
 constexpr int MAX_GROUPS = 256;
 
 struct Shape {
@@ -920,9 +884,9 @@ struct Shape {
 
 inline Shape shape_of(int N, int h, int cus) {
   Shape s;
-  s.NG = (N + 63) / 64;
-  s.Np = 64 * s.NG;
-  s.tiles = h * s.NG * NT;
+  s.NG = (N + EPG - 1) / EPG;
+  s.Np = EPG * s.NG;
+  s.tiles = h * s.NG;
   s.tiles_p = (s.tiles + 7) / 8 * 8;     // whole rounds of the dW2 loop (4 steps of 2 tiles)
   s.steps = s.tiles_p / 2;
   s.GS = std::max(1, std::min({MAX_GROUPS, s.steps, cus}));
@@ -945,8 +909,7 @@ inline size_t work_layout(int N, int h, size_t off[WORK_PARTS]) {
       G * 16 * 4 + G * 16 * 4,              // 17 part_b3 + part_ls
       G * HID * HID * 4,                    // 18 part_w2
       4096 * 4,                             // 19 per-block sums of squares
-      (size_t)h * (Np / 64) * H2_F4 * 16,   // 20 policy hidden-2 activations
-      (Np / 64) * H2_F4 * 16};              // 21 value hidden-2 activations
+      (size_t)h * (Np / EPG) * WAVES * H2_F4 * 16};   // 20 policy hidden-2 activations
   size_t o = 0;
   for (int k = 0; k < WORK_PARTS; ++k) {
     off[k] = o;
@@ -1042,7 +1005,6 @@ int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* pol
   A.dz2_half = (u32x2*)at(11);
   A.dz1_half = (u32x2*)at(12);
   A.h2s = (f32x4*)at(20);
-  A.h2v = (f32x4*)at(21);
   A.Np = sh.Np;
   if (out) {
     A.ext = out->actions;
@@ -1055,11 +1017,11 @@ int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* pol
     A.o_gs0 = out->grad_state0;
   }
   if (mode == AUV_ACT_EXTERNAL)
-    hipLaunchKernelGGL(k_window<MODE_EXTERNAL>, dim3(sh.NG), dim3(64), 0, s, env->E, env->veh, A);
+    hipLaunchKernelGGL(k_window<MODE_EXTERNAL>, dim3(sh.NG), dim3(64 * WAVES), 0, s, env->E, env->veh, A);
   else if (mode == AUV_ACT_POLICY_MEAN)
-    hipLaunchKernelGGL(k_window<MODE_MEAN>, dim3(sh.NG), dim3(64), 0, s, env->E, env->veh, A);
+    hipLaunchKernelGGL(k_window<MODE_MEAN>, dim3(sh.NG), dim3(64 * WAVES), 0, s, env->E, env->veh, A);
   else
-    hipLaunchKernelGGL(k_window<MODE_SAMPLE>, dim3(sh.NG), dim3(64), 0, s, env->E, env->veh, A);
+    hipLaunchKernelGGL(k_window<MODE_SAMPLE>, dim3(sh.NG), dim3(64 * WAVES), 0, s, env->E, env->veh, A);
 
   const int rb = grad_reduce_blocks(ACT);
   float* ss = (float*)at(19);
