@@ -364,8 +364,8 @@ typedef struct {
 } auv_shac_buffers;
 
 /* Bytes of device workspace auv_shac_window needs for N environments and windows of h
- * steps (-1 outside N in [1, 2^22], h in [1, 64]); about 2.3 KB per environment-step plus
- * 90 MB. */
+ * steps (-1 outside N in [1, 2^22], h in [1, 64]); about 3.3 KB per environment-step plus
+ * 81 MB. */
 int64_t auv_shac_work_bytes(int32_t n_envs, int32_t h);
 
 /* One SHAC window.  policy: the 23-256-256-8 network (a padded 12-256-256-6 net; log_std
