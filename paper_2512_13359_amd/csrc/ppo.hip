@@ -719,12 +719,20 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, in
   const int g0 = w * G / 4, g1 = (w + 1) * G / 4;
   float acc = 0.0f;
   int wg = g0;
-  for (; wg + 8 <= g1; wg += 8) {
-    float v[8];
+  // sequential sum in group order, with 16 (then 4) loads in flight
+  for (; wg + 16 <= g1; wg += 16) {
+    float v[16];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = src[(size_t)(wg + u) * stride];
+    for (int u = 0; u < 16; ++u) v[u] = src[(size_t)(wg + u) * stride];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) acc += v[u];
+    for (int u = 0; u < 16; ++u) acc += v[u];
+  }
+  for (; wg + 4 <= g1; wg += 4) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = src[(size_t)(wg + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc += v[u];
   }
   for (; wg < g1; ++wg) acc += src[(size_t)wg * stride];
   part[w][lane] = acc;
@@ -738,28 +746,40 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, in
 }
 
 // stats: [0] surrogate loss, [1] value loss, [2] entropy, [3] approx KL, [4] clipped
-// fraction, [5] |grad policy|^2, [6] |grad value|^2, [7] clipping factor.  One wave; every
-// sum in a fixed order.
-__global__ __launch_bounds__(64) void k_finalize(int G1p, int G1v, Work W, int nbp, int nbv, int rb,
-                                                 const float* __restrict__ log_std, Hp hp, float* __restrict__ stats) {
-  const int lane = threadIdx.x;
+// fraction, [5] |grad policy|^2, [6] |grad value|^2, [7] clipping factor.  One workgroup of
+// four waves; every sum in a fixed order (thread-strided with four loads in flight, then over
+// each wave, then the waves' sums in wave order).
+__global__ __launch_bounds__(256) void k_finalize(int G1p, int G1v, Work W, int nbp, int nbv, int rb,
+                                                  const float* __restrict__ log_std, Hp hp, float* __restrict__ stats) {
+  __shared__ float part[4][6];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   float sp = 0.0f, sv = 0.0f, pg = 0.0f, kl = 0.0f, cl = 0.0f, vs = 0.0f;
-  for (int k = lane; k < nbp; k += 64) sp += W.part_ss[k];
-  for (int k = lane; k < nbv; k += 64) sv += W.part_ss[rb + k];
-  for (int k = lane; k < G1p; k += 64) {
+#pragma unroll 4
+  for (int k = tid; k < nbp; k += 256) sp += W.part_ss[k];
+#pragma unroll 4
+  for (int k = tid; k < nbv; k += 256) sv += W.part_ss[rb + k];
+  for (int k = tid; k < G1p; k += 256) {
     const float* q = W.part_stats + (size_t)k * STATS;
     pg += q[0];
     kl += q[1];
     cl += q[2];
   }
-  for (int k = lane; k < G1v; k += 64) vs += W.part_stats[((size_t)MAX_GROUPS + k) * STATS + 3];
-  sp = wave_sum(sp);
-  sv = wave_sum(sv);
-  pg = wave_sum(pg);
-  kl = wave_sum(kl);
-  cl = wave_sum(cl);
-  vs = wave_sum(vs);
-  if (lane == 0) {
+  for (int k = tid; k < G1v; k += 256) vs += W.part_stats[((size_t)MAX_GROUPS + k) * STATS + 3];
+  const float v[6] = {wave_sum(sp), wave_sum(sv), wave_sum(pg), wave_sum(kl), wave_sum(cl), wave_sum(vs)};
+  if (lane == 0)
+#pragma unroll
+    for (int j = 0; j < 6; ++j) part[wv][j] = v[j];
+  __syncthreads();
+  if (tid == 0) {
+    float t[6];
+#pragma unroll
+    for (int j = 0; j < 6; ++j) t[j] = ((part[0][j] + part[1][j]) + part[2][j]) + part[3][j];
+    sp = t[0];
+    sv = t[1];
+    pg = t[2];
+    kl = t[3];
+    cl = t[4];
+    vs = t[5];
     float ent = 0.0f;
     if (log_std)
       for (int j = 0; j < hp.n_act; ++j) ent += log_std[j] + 0.5f * (1.0f + LOG_2PI);
@@ -896,7 +916,7 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, G1, G1, G3, W, 0.0f,
                      grad_value, W.part_ss + rb);
-  hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(64), 0, s, with_policy ? G1 : 0, G1, W, with_policy ? rb : 0,
+  hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? G1 : 0, G1, W, with_policy ? rb : 0,
                      ppo::red_blocks(1), rb, with_policy ? policy->log_std : (const float*)nullptr, hp, stats);
   return check_launch("auv_ppo_grad");
 }

@@ -841,23 +841,36 @@ __global__ __launch_bounds__(256) void k_wsmall(const u32x2* __restrict__ x_half
 
 // stats: [0] loss, [1] mean over envs of sum_t gamma^t r_t, [2] mean V(o_h), [5] |grad|^2,
 // [7] clipping factor min(1, c / (|grad| + 1e-6)) (1 without clipping or without gradient).
-__global__ __launch_bounds__(64) void k_finalize(const float* __restrict__ J, const float* __restrict__ Jr,
-                                                 const float* __restrict__ vl, int N, float inv_nh,
-                                                 const float* __restrict__ ss, int nss, float max_norm,
-                                                 float* __restrict__ stats) {
-  const int lane = threadIdx.x;
+// One workgroup of four waves; every sum in a fixed order (thread-strided with four loads in
+// flight, then over each wave, then the waves' sums in wave order).
+__global__ __launch_bounds__(256) void k_finalize(const float* __restrict__ J, const float* __restrict__ Jr,
+                                                  const float* __restrict__ vl, int N, float inv_nh,
+                                                  const float* __restrict__ ss, int nss, float max_norm,
+                                                  float* __restrict__ stats) {
+  __shared__ float part[4][4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   float sj = 0.0f, sr = 0.0f, sv = 0.0f, sg = 0.0f;
-  for (int k = lane; k < N; k += 64) {
+#pragma unroll 4
+  for (int k = tid; k < N; k += 256) {
     sj += J[k];
     sr += Jr[k];
     sv += vl[k];
   }
-  for (int k = lane; k < nss; k += 64) sg += ss[k];
-  sj = wave_sum(sj);
-  sr = wave_sum(sr);
-  sv = wave_sum(sv);
-  sg = wave_sum(sg);
-  if (lane == 0) {
+#pragma unroll 4
+  for (int k = tid; k < nss; k += 256) sg += ss[k];
+  const float v[4] = {wave_sum(sj), wave_sum(sr), wave_sum(sv), wave_sum(sg)};
+  if (lane == 0)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) part[wv][j] = v[j];
+  __syncthreads();
+  if (tid == 0) {
+    float t[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) t[j] = ((part[0][j] + part[1][j]) + part[2][j]) + part[3][j];
+    sj = t[0];
+    sr = t[1];
+    sv = t[2];
+    sg = t[3];
     stats[0] = -sj * inv_nh;
     stats[1] = sr / (float)N;
     stats[2] = sv / (float)N;
@@ -1049,7 +1062,7 @@ int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* pol
                        A.gls, sh.steps, sh.Np, P);
     if (int rc = launch_grad_reduce(P, ACT, 6, sh.GS, sh.GS, sh.G3, grad_policy, ss, s)) return rc;
   }
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(64), 0, s, A.J, A.Jr, A.vl, N, A.inv_nh, ss, grad_policy ? rb : 0,
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, s, A.J, A.Jr, A.vl, N, A.inv_nh, ss, grad_policy ? rb : 0,
                      cfg->max_grad_norm, stats);
   const int rc = check_launch("auv_shac_window");
   if (rc == AUV_OK) env->global_step += h;
