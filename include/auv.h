@@ -364,7 +364,7 @@ typedef struct {
 } auv_shac_buffers;
 
 /* Bytes of device workspace auv_shac_window needs for N environments and windows of h
- * steps (-1 outside N in [1, 2^22], h in [1, 64]); about 3.3 KB per environment-step plus
+ * steps (-1 outside N in [1, 2^22], h in [1, 64]); about 3.4 KB per environment-step plus
  * 81 MB. */
 int64_t auv_shac_work_bytes(int32_t n_envs, int32_t h);
 

@@ -78,7 +78,7 @@ struct WinArgs {
   float gamma;
   NetF pol, val;
   const float* log_std;
-  float *ck, *acts, *J, *Jr, *vl, *gls;
+  float *ck, *sub, *acts, *J, *Jr, *vl, *gls;     // sub: RK4 substep start states [h][MAX_S - 1][13][Np]
   f32x4* h2s;                          // policy hidden-2 activations [h][G][wave][M-tile][lane]
   u32x2 *x_half, *h1_half, *h2_half, *gy_half, *dz2_half, *dz1_half;
   int Np;
@@ -441,6 +441,44 @@ __device__ __forceinline__ void ck_store(float* ck, size_t Np, int t, int i, con
   for (int k = 0; k < 6; ++k) c[(13 + k) * Np] = ab[k];
 }
 
+// Start state of RK4 substep s (1 .. substeps - 1) of step t: [t][s - 1][13 rows][Np].
+__device__ __forceinline__ void sub_store(float* sub, size_t Np, int t, int s, int i, const adj::X13<float>& x) {
+  float* c = sub + ((size_t)t * (MAX_S - 1) + (s - 1)) * 13 * Np + i;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    c[k * Np] = x.p[k];
+    c[(7 + k) * Np] = x.v[k];
+    c[(10 + k) * Np] = x.w[k];
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) c[(3 + k) * Np] = x.q[k];
+}
+
+__device__ __forceinline__ void sub_load(const float* sub, size_t Np, int t, int s, int i, adj::X13<float>& x) {
+  const float* c = sub + ((size_t)t * (MAX_S - 1) + (s - 1)) * 13 * Np + i;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    x.p[k] = c[k * Np];
+    x.v[k] = c[(7 + k) * Np];
+    x.w[k] = c[(10 + k) * Np];
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) x.q[k] = c[(3 + k) * Np];
+}
+
+// The state part of checkpoint t.
+__device__ __forceinline__ void ck_load_state(const float* ck, size_t Np, int t, int i, adj::X13<float>& x) {
+  const float* c = ck + (size_t)t * CK * Np + i;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    x.p[k] = c[k * Np];
+    x.v[k] = c[(7 + k) * Np];
+    x.w[k] = c[(10 + k) * Np];
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) x.q[k] = c[(3 + k) * Np];
+}
+
 __device__ __forceinline__ void ck_load(const float* ck, size_t Np, int t, int i, adj::X13<float>& x, float ab[6]) {
   const float* c = ck + (size_t)t * CK * Np + i;
 #pragma unroll
@@ -550,7 +588,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
 #pragma unroll
     for (int j = 0; j < 6; ++j) u[j] = fminf(fmaxf(a[j], -1.0f), 1.0f);
     adj::wrench(K, u, tau);
-    for (int s = 0; s < E.substeps; ++s) adj::substep(M, tau, E.h, x);
+    for (int s = 0; s < E.substeps; ++s) {
+      if (s > 0 && lead) sub_store(A.sub, Np, t, s, i, x);
+      adj::substep(M, tau, E.h, x);
+    }
     float o1[12];
     adj::observe(x, pg, qg, o1);
     const float rw = adj::reward(K, o1, u, ab);
@@ -651,31 +692,22 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
 #pragma unroll
       for (int m = 0; m < 4; ++m) h2[m] = hs[m * 64];
     }
-    adj::X13<float> x0;
+    // the step's start state, its substep start states and its end state (the next
+    // checkpoint), as the forward computed them; rows of substeps beyond E.substeps are
+    // loaded (in bounds) but not used
+    adj::X13<float> xs[MAX_S], x1;
     float abt[6], a[6], u[6], tau[6];
-    ck_load(A.ck, Np, t, i, x0, abt);
+    ck_load(A.ck, Np, t, i, xs[0], abt);
+#pragma unroll
+    for (int s = 1; s < MAX_S; ++s) sub_load(A.sub, Np, t, s, i, xs[s]);
+    ck_load_state(A.ck, Np, t + 1, i, x1);
+    const adj::X13<float>& x0 = xs[0];
 #pragma unroll
     for (int j = 0; j < 6; ++j) {
       a[j] = A.acts[((size_t)t * 6 + j) * Np + i];
       u[j] = fminf(fmaxf(a[j], -1.0f), 1.0f);
     }
     adj::wrench(K, u, tau);
-    // substep start states (recomputed), then the step's end state
-    adj::X13<float> xs[MAX_S];
-    xs[0] = x0;
-#pragma unroll
-    for (int s = 1; s < MAX_S; ++s)
-      if (s < E.substeps) {
-        xs[s] = xs[s - 1];
-        adj::substep(M, tau, E.h, xs[s]);
-      }
-    adj::X13<float> x1 = xs[0];
-#pragma unroll
-    for (int s = 0; s < MAX_S; ++s)
-      if (s == E.substeps - 1) {
-        x1 = xs[s];
-        adj::substep(M, tau, E.h, x1);
-      }
     // reward r_t(o(s_{t+1}), u_t, abar_t) with weight -gamma^t / (N h)
     const float cr = valid ? -powf(A.gamma, (float)t) * A.inv_nh : 0.0f;
     float o1[12], go[12], gu[6] = {0, 0, 0, 0, 0, 0}, gab[6] = {0, 0, 0, 0, 0, 0};
@@ -888,7 +920,7 @@ __global__ __launch_bounds__(256) void k_zero(uint32_t* __restrict__ p, size_t n
 
 // ------------------------------------------------------------------ workspace ----------
 inline size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
-constexpr int WORK_PARTS = 21;
+constexpr int WORK_PARTS = 22;
 constexpr int MAX_GROUPS = 256;
 
 struct Shape {
@@ -922,7 +954,8 @@ inline size_t work_layout(int N, int h, size_t off[WORK_PARTS]) {
       G * 16 * 4 + G * 16 * 4,              // 17 part_b3 + part_ls
       G * HID * HID * 4,                    // 18 part_w2
       4096 * 4,                             // 19 per-block sums of squares
-      (size_t)h * (Np / EPG) * WAVES * H2_F4 * 16};   // 20 policy hidden-2 activations
+      (size_t)h * (Np / EPG) * WAVES * H2_F4 * 16,   // 20 policy hidden-2 activations
+      (size_t)h * (MAX_S - 1) * 13 * Np * 4};        // 21 RK4 substep start states
   size_t o = 0;
   for (int k = 0; k < WORK_PARTS; ++k) {
     off[k] = o;
@@ -1018,6 +1051,7 @@ int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* pol
   A.dz2_half = (u32x2*)at(11);
   A.dz1_half = (u32x2*)at(12);
   A.h2s = (f32x4*)at(20);
+  A.sub = (float*)at(21);
   A.Np = sh.Np;
   if (out) {
     A.ext = out->actions;
