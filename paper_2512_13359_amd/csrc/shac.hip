@@ -13,9 +13,10 @@
 //                  the observations, actions and adjoints it needs without an exchange;
 //                  the networks are split by hidden feature, wave w owning features
 //                  64 w .. 64 w + 63 of both hidden layers (its 64 rows of W2, then of W2^T,
-//                  in LDS).  At workgroup barriers the waves exchange through LDS only the
-//                  output partials (one barrier per forward step), q(dz2) and the
-//                  input-gradient partials (two per reverse step).  Forward sweep: policy
+//                  in LDS; its small weights in registers).  At workgroup barriers the waves
+//                  exchange through LDS only hidden layer 1 and the output partials (two
+//                  barriers per forward step), q(dz2) and the input-gradient partials (two
+//                  per reverse step).  Forward sweep: policy
 //                  on MFMA, RK4 of the paper task, reward, checkpoints of every step's state
 //                  and action average, every wave's hidden-2 activations; terminal value and
 //                  its input gradient; the environment update (reset where the window ends
@@ -92,7 +93,8 @@ struct Lds {
   __bf16 G[WAVES][EPG][8];    // per wave: q(dL/dy)
   __bf16 T[WAVES][32 * TS];   // per wave: transpose buffer [feature][environment]
   float Y[2][WAVES][EPG][8];  // output partials of each wave (two buffers, alternate steps)
-  bf16x8 DZ[8][64];           // q(dz2) of all 256 features as the B operand (K step s: 32 s ..)
+  bf16x8 DZ[8][64];           // a B operand of all 256 hidden features (K step s: 32 s ..): hidden 1
+                              // (forward), q(dz2) (reverse)
   float GX[WAVES][EPG][16];   // input-gradient partials of each wave (inputs 0..15)
 };
 static_assert(sizeof(Lds) <= 160 * 1024, "window kernel LDS exceeds a CU's 160 KB");
@@ -182,40 +184,75 @@ __device__ __forceinline__ void wg_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Hidden layer 1 of the 16 environments, all 256 features, as the B operand of layer 2:
-// H1[K step p] = features 32 p .. 32 p + 31.
-__device__ __forceinline__ void layer1(const NetF& N, const bf16x8& X, int lane, bf16x8 H1[8]) {
+// The small weights of wave w's features, loaded once per sweep so that the loops issue no
+// weight loads: for the forward, its W1 rows (M-tiles 4w .. 4w + 3), their layer-1 and
+// layer-2 biases (times 2 log2 e; lane (g, r): rows 16 m + 4 g .. + 3) and its two K steps of
+// W3; for the backward, its W3^T M-tiles, its W1 rows and layer-1 biases, and its two K steps
+// of W1^T (M-tile 0: inputs 0..15).
+struct OwnF {
+  bf16x8 w1[4], w3[2];
+  f32x4 b1[4], b2[4];
+};
+struct OwnB {
+  bf16x8 w3t[4], w1[4], w1t[2];
+  f32x4 b1[4];
+};
+
+__device__ __forceinline__ OwnF own_fwd(const NetF& N, int w, int lane) {
   const int g = lane >> 4;
+  OwnF o;
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const f32x4 b0 = bias_k(N.b, 32 * p + 4 * g), b1 = bias_k(N.b, 32 * p + 16 + 4 * g);
-    H1[p] = act_frag(mfma(fr(N, F_W1 + 2 * p, lane), X, zero4()), mfma(fr(N, F_W1 + 2 * p + 1, lane), X, zero4()),
-                     b0, b1);
+  for (int m = 0; m < 4; ++m) {
+    o.w1[m] = fr(N, F_W1 + 4 * w + m, lane);
+    o.b1[m] = bias_k(N.b, 64 * w + 16 * m + 4 * g);
+    o.b2[m] = bias_k(N.b + HID, 64 * w + 16 * m + 4 * g);
   }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) o.w3[j] = fr(N, F_W3 + 2 * w + j, lane);
+  return o;
 }
 
-// Wave w's part of the forward pass: its hidden-2 activations h2[m] (fp32 after tanh; lane
-// (g, r): features 64 w + 16 m + 4 g + i of environment r) and, returned, its partial of the
-// outputs over those 64 features (lane (g, r): rows 4 g .. 4 g + 3).  w2: the wave's 32 W2
-// fragments [M-tile m][K step s] (in LDS, or the network's array in global memory).
-__device__ __forceinline__ f32x4 mlp_forward(const NetF& N, const bf16x8* w2, const bf16x8& X, int w, int lane,
-                                             f32x4 h2[4]) {
+__device__ __forceinline__ OwnB own_bwd(const NetF& N, int w, int lane) {
   const int g = lane >> 4;
+  OwnB o;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    o.w3t[m] = fr(N, F_W3T + 4 * w + m, lane);
+    o.w1[m] = fr(N, F_W1 + 4 * w + m, lane);
+    o.b1[m] = bias_k(N.b, 64 * w + 16 * m + 4 * g);
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) o.w1t[j] = fr(N, F_W1T + 2 * w + j, lane);
+  return o;
+}
+
+// Wave w's part of the forward pass.  Layer 1 of its 64 features goes to the other waves
+// through S.DZ (the K steps 2w, 2w + 1 of layer 2's B operand); then its hidden-2
+// activations h2[m] (fp32 after tanh; lane (g, r): features 64 w + 16 m + 4 g + i of
+// environment r) and, returned, its partial of the outputs over those 64 features (lane
+// (g, r): rows 4 g .. 4 g + 3).  w2: the wave's 32 W2 fragments [M-tile m][K step s] (in
+// LDS, or the network's array in global memory).
+__device__ __forceinline__ f32x4 mlp_forward(const OwnF& O, const bf16x8* w2, const bf16x8& X, int w, int lane,
+                                             Lds& S, f32x4 h2[4]) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    S.DZ[2 * w + j][lane] = act_frag(mfma(O.w1[2 * j], X, zero4()), mfma(O.w1[2 * j + 1], X, zero4()),
+                                     O.b1[2 * j], O.b1[2 * j + 1]);
+  wg_sync();
   bf16x8 H1[8];
-  layer1(N, X, lane, H1);
+#pragma unroll
+  for (int s = 0; s < 8; ++s) H1[s] = S.DZ[s][lane];
   f32x4 z[4] = {zero4(), zero4(), zero4(), zero4()};
 #pragma unroll
   for (int s = 0; s < 8; ++s)
 #pragma unroll
     for (int m = 0; m < 4; ++m) z[m] = mfma(w2[(8 * m + s) * 64 + lane], H1[s], z[m]);
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const f32x4 bk = bias_k(N.b + HID, 64 * w + 16 * m + 4 * g);
+  for (int m = 0; m < 4; ++m)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) h2[m][i] = tanh_bias(z[m][i], bk[i]);
-  }
-  const f32x4 y = mfma(fr(N, F_W3 + 2 * w, lane), pack8(h2[0], h2[1]), zero4());
-  return mfma(fr(N, F_W3 + 2 * w + 1, lane), pack8(h2[2], h2[3]), y);
+    for (int i = 0; i < 4; ++i) h2[m][i] = tanh_bias(z[m][i], O.b2[m][i]);
+  const f32x4 y = mfma(O.w3[0], pack8(h2[0], h2[1]), zero4());
+  return mfma(O.w3[1], pack8(h2[2], h2[3]), y);
 }
 
 // Where the reverse sweep writes the weight-gradient operands of one step.
@@ -251,7 +288,7 @@ __device__ __forceinline__ void store_pair(Lds& S, int w, const f32x4& v0, const
 // four waves' partials in wave order, gxo (inputs 0..11 of environment r).  With H.on it
 // also stores the weight-gradient operands of its features.  w2t: the wave's 32 W2^T
 // fragments [M-tile m][K step s].
-__device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, const bf16x8& X, const bf16x8& GY,
+__device__ __forceinline__ void mlp_backward(const OwnB& O, const bf16x8* w2t, const bf16x8& X, const bf16x8& GY,
                                              const f32x4 h2[4], int w, int lane, Lds& S, const HalfOut& H,
                                              float gxo[12]) {
   const int g = lane >> 4, r = lane & 15;
@@ -259,7 +296,7 @@ __device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, c
   f32x4 d[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    d[m] = mfma(fr(N, F_W3T + 4 * w + m, lane), GY, zero4());
+    d[m] = mfma(O.w3t[m], GY, zero4());
 #pragma unroll
     for (int i = 0; i < 4; ++i) d[m][i] *= 1.0f - h2[m][i] * h2[m][i];
   }
@@ -284,11 +321,10 @@ __device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, c
   f32x4 k[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    const f32x4 y = mfma(fr(N, F_W1 + 4 * w + m, lane), X, zero4());
-    const f32x4 bk = bias_k(N.b, 64 * w + 16 * m + 4 * g);
+    const f32x4 y = mfma(O.w1[m], X, zero4());
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      k[m][i] = tanh_bias(y[i], bk[i]);
+      k[m][i] = tanh_bias(y[i], O.b1[m][i]);
       e[m][i] *= 1.0f - k[m][i] * k[m][i];
     }
   }
@@ -299,8 +335,8 @@ __device__ __forceinline__ void mlp_backward(const NetF& N, const bf16x8* w2t, c
     store_pair(S, w, e[2], e[3], lane, H.dz1, H.tile, 2 * w + 1);
   }
   // input gradient: the partial over this wave's hidden-1 features (M-tile 0: inputs 0..15)
-  f32x4 gx = mfma(fr(N, F_W1T + 2 * w, lane), pack8(e[0], e[1]), zero4());
-  gx = mfma(fr(N, F_W1T + 2 * w + 1, lane), pack8(e[2], e[3]), gx);
+  f32x4 gx = mfma(O.w1t[0], pack8(e[0], e[1]), zero4());
+  gx = mfma(O.w1t[1], pack8(e[2], e[3]), gx);
   *reinterpret_cast<f32x4*>(&S.GX[w][r][4 * g]) = gx;
   wg_sync();
 #pragma unroll
@@ -541,7 +577,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
   };
 
   // ---------------------------------------------------------------- forward sweep
-  if (MODE != MODE_EXTERNAL) fill_w(S, A.pol, F_W2 + WF * w, w, lane);
+  OwnF of{};
+  if (MODE != MODE_EXTERNAL) {
+    fill_w(S, A.pol, F_W2 + WF * w, w, lane);
+    of = own_fwd(A.pol, w, lane);
+  }
   float Jr = 0.0f;
   for (int t = 0; t < h; ++t) {
     if (lead) ck_store(A.ck, Np, t, i, x, ab);
@@ -556,7 +596,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
       lds_sync();
       const bf16x8 X = input_frag(S, w, lane);
       f32x4 h2[4];
-      const f32x4 y = mlp_forward(A.pol, &S.W[w][0][0], X, w, lane, h2);
+      const f32x4 y = mlp_forward(of, &S.W[w][0][0], X, w, lane, S, h2);
       f32x4* hs = h2_at(t);
 #pragma unroll
       for (int m = 0; m < 4; ++m) hs[m * 64] = h2[m];
@@ -624,13 +664,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
     lds_sync();
     const bf16x8 X = input_frag(S, w, lane), GY = gy_frag(S, w, lane);
     f32x4 h2[4];
-    const f32x4 y = mlp_forward(A.val, A.val.f + (size_t)(F_W2 + WF * w) * 64, X, w, lane, h2);
+    const f32x4 y = mlp_forward(own_fwd(A.val, w, lane), A.val.f + (size_t)(F_W2 + WF * w) * 64, X, w, lane, S, h2);
     const int b = h & 1;
     if (g < 2) *reinterpret_cast<f32x4*>(&S.Y[b][w][r][4 * g]) = y;
     wg_sync();
     vlast = out_sum(S, b, r, 0) + A.val.b[2 * HID];
     const HalfOut off{nullptr, nullptr, nullptr, nullptr, 0, false};
-    mlp_backward(A.val, A.val.f + (size_t)(F_W2T + WF * w) * 64, X, GY, h2, w, lane, S, off, go_h);
+    mlp_backward(own_bwd(A.val, w, lane), A.val.f + (size_t)(F_W2T + WF * w) * 64, X, GY, h2, w, lane, S, off, go_h);
   }
 
   // ------------------------------------------- environment update (reset at the episode end)
@@ -680,7 +720,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
   }
 
   // ---------------------------------------------------------------- reverse sweep
-  if (MODE != MODE_EXTERNAL) fill_w(S, A.pol, F_W2T + WF * w, w, lane);
+  OwnB ob{};
+  if (MODE != MODE_EXTERNAL) {
+    fill_w(S, A.pol, F_W2T + WF * w, w, lane);
+    ob = own_bwd(A.pol, w, lane);
+  }
   adj::X13<float> lam;
   adj::zero(lam);
   adj::observe_vjp(x, pg, qg, go_h, lam);
@@ -757,7 +801,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
       if (A.want_grad && w == 0) store_input_halves(S, lane, A.x_half, A.gy_half, tile);
       const HalfOut H{A.h1_half, A.h2_half, A.dz2_half, A.dz1_half, tile, A.want_grad != 0};
       float gxo[12];
-      mlp_backward(A.pol, &S.W[w][0][0], X, GY, h2, w, lane, S, H, gxo);
+      mlp_backward(ob, &S.W[w][0][0], X, GY, h2, w, lane, S, H, gxo);
       adj::observe_vjp(x0, pg, qg, gxo, lam);
     }
 #pragma unroll
