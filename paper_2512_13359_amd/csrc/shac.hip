@@ -490,8 +490,8 @@ __device__ __forceinline__ void sub_store(float* sub, size_t Np, int t, int s, i
   for (int k = 0; k < 4; ++k) c[(3 + k) * Np] = x.q[k];
 }
 
-__device__ __forceinline__ void sub_load(const float* sub, size_t Np, int t, int s, int i, adj::X13<float>& x) {
-  const float* c = sub + ((size_t)t * (MAX_S - 1) + (s - 1)) * 13 * Np + i;
+// 13 state rows at stride Np from c.
+__device__ __forceinline__ void state_load(const float* c, size_t Np, adj::X13<float>& x) {
 #pragma unroll
   for (int k = 0; k < 3; ++k) {
     x.p[k] = c[k * Np];
@@ -504,15 +504,13 @@ __device__ __forceinline__ void sub_load(const float* sub, size_t Np, int t, int
 
 // The state part of checkpoint t.
 __device__ __forceinline__ void ck_load_state(const float* ck, size_t Np, int t, int i, adj::X13<float>& x) {
-  const float* c = ck + (size_t)t * CK * Np + i;
-#pragma unroll
-  for (int k = 0; k < 3; ++k) {
-    x.p[k] = c[k * Np];
-    x.v[k] = c[(7 + k) * Np];
-    x.w[k] = c[(10 + k) * Np];
-  }
-#pragma unroll
-  for (int k = 0; k < 4; ++k) x.q[k] = c[(3 + k) * Np];
+  state_load(ck + (size_t)t * CK * Np + i, Np, x);
+}
+
+// Start state of RK4 substep s of step t: checkpoint t for s = 0, else the stored substep
+// start state (the same row order and stride).
+__device__ __forceinline__ void start_load(const WinArgs& A, size_t Np, int t, int s, int i, adj::X13<float>& x) {
+  state_load(s == 0 ? A.ck + (size_t)t * CK * Np + i : A.sub + ((size_t)t * (MAX_S - 1) + (s - 1)) * 13 * Np + i, Np, x);
 }
 
 __device__ __forceinline__ void ck_load(const float* ck, size_t Np, int t, int i, adj::X13<float>& x, float ab[6]) {
@@ -736,16 +734,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
 #pragma unroll
       for (int m = 0; m < 4; ++m) h2[m] = hs[m * 64];
     }
-    // the step's start state, its substep start states and its end state (the next
-    // checkpoint), as the forward computed them; rows of substeps beyond E.substeps are
-    // loaded (in bounds) but not used
-    adj::X13<float> xs[MAX_S], x1;
+    // the step's start and end states (checkpoints t and t + 1) as the forward computed them
+    adj::X13<float> x0, x1;
     float abt[6], a[6], u[6], tau[6];
-    ck_load(A.ck, Np, t, i, xs[0], abt);
-#pragma unroll
-    for (int s = 1; s < MAX_S; ++s) sub_load(A.sub, Np, t, s, i, xs[s]);
+    ck_load(A.ck, Np, t, i, x0, abt);
     ck_load_state(A.ck, Np, t + 1, i, x1);
-    const adj::X13<float>& x0 = xs[0];
 #pragma unroll
     for (int j = 0; j < 6; ++j) {
       a[j] = A.acts[((size_t)t * 6 + j) * Np + i];
@@ -764,11 +757,18 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
       gab[j] += K.beta * lab[j];
       gu[j] += (1.0f - K.beta) * lab[j];
     }
-    // RK4 substeps in reverse
+    // RK4 substeps in reverse, each from its stored start state (loaded one substep ahead);
+    // one copy of the substep adjoint in the loop keeps the code within the instruction cache
     float gtau[6] = {0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int s = MAX_S - 1; s >= 0; --s)
-      if (s < E.substeps) adj::substep_vjp(M, tau, E.h, xs[s], lam, gtau);
+    adj::X13<float> xs;
+    start_load(A, Np, t, E.substeps - 1, i, xs);
+#pragma unroll 1
+    for (int s = E.substeps - 1; s >= 0; --s) {
+      adj::X13<float> xn;
+      start_load(A, Np, t, s > 0 ? s - 1 : 0, i, xn);
+      adj::substep_vjp(M, tau, E.h, xs, lam, gtau);
+      xs = xn;
+    }
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
       gu[j] += K.f_max * gtau[j];
