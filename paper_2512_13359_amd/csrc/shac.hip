@@ -854,25 +854,48 @@ __global__ __launch_bounds__(256) void k_wsmall(const u32x2* __restrict__ x_half
     b1[mt] = b2[mt] = 0.0f;
   }
   auto at = [&](int tile, int ft, int nft) { return ((size_t)tile * nft + ft) * 64 + lane; };
+  // operands of one K step (sample tiles 2u, 2u + 1), loaded one K step ahead
+  struct In {
+    u32x2 x[2][2], gy[2], d1[4][2], h2[4][2], d2[4][2];
+  };
+  auto load = [&](int u, In& v) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int tl = 2 * u + k;
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) v.x[nt][k] = x_half[at(tl, nt, 2)];
+      v.gy[k] = gy_half[at(tl, 0, 1)];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int ft = 4 * w + mt;
+        v.d1[mt][k] = dz1_half[at(tl, ft, 16)];
+        v.h2[mt][k] = h2_half[at(tl, ft, 16)];
+        v.d2[mt][k] = dz2_half[at(tl, ft, 16)];
+      }
+    }
+  };
+  In cur;
+  if (u0 < u1) load(u0, cur);
   for (int u = u0; u < u1; ++u) {
-    const int t0 = 2 * u, t1 = 2 * u + 1;
+    In nxt;
+    load(min(u + 1, u1 - 1), nxt);   // unconditional (clamped), so no wait covers it early
     bf16x8 xb[2];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) xb[nt] = join2(x_half[at(t0, nt, 2)], x_half[at(t1, nt, 2)]);
-    const bf16x8 gb = join2(gy_half[at(t0, 0, 1)], gy_half[at(t1, 0, 1)]);
+    for (int nt = 0; nt < 2; ++nt) xb[nt] = join2(cur.x[nt][0], cur.x[nt][1]);
+    const bf16x8 gb = join2(cur.gy[0], cur.gy[1]);
     if (w == 0) b3 += sum8(gb);
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      const int ft = 4 * w + mt;
-      const bf16x8 d1 = join2(dz1_half[at(t0, ft, 16)], dz1_half[at(t1, ft, 16)]);
-      const bf16x8 h2 = join2(h2_half[at(t0, ft, 16)], h2_half[at(t1, ft, 16)]);
-      const bf16x8 d2 = join2(dz2_half[at(t0, ft, 16)], dz2_half[at(t1, ft, 16)]);
+      const bf16x8 d1 = join2(cur.d1[mt][0], cur.d1[mt][1]);
+      const bf16x8 h2 = join2(cur.h2[mt][0], cur.h2[mt][1]);
+      const bf16x8 d2 = join2(cur.d2[mt][0], cur.d2[mt][1]);
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) w1[mt][nt] = mfma(d1, xb[nt], w1[mt][nt]);
       w3[mt] = mfma(h2, gb, w3[mt]);
       b1[mt] += sum8(d1);
       b2[mt] += sum8(d2);
     }
+    cur = nxt;
   }
   const int G = blockIdx.x;
 #pragma unroll
