@@ -54,6 +54,7 @@ class ShacLearner:
         self.ret = torch.zeros(self.h, n, **f32)
         self._no_done = torch.zeros(self.h, n, **f32)
         self._critic_work = None
+        self._idx_host = None
         self.t = 0
         self.t_critic = 0
 
@@ -100,10 +101,27 @@ class ShacLearner:
         b = self._last
         batch = A.make_ppo_batch(b["obs"], b["obs"], self.values, self.adv, self.ret, M)
         rng = np.random.Generator(np.random.PCG64(seed))
-        for _ in range(iterations):
-            blocks = rng.permutation(M // 16)
-            idx = torch.from_numpy((blocks[:, None] * 16 + np.arange(16)[None, :]).ravel().astype(np.int32)).to(
-                self.values.device)
+        # each iteration's indices go through one of two pinned host slots and an asynchronous
+        # copy, so the host prepares the next permutation while the device works on this one
+        nb = M // 16
+        if self._idx_host is None or self._idx_host.shape[1] != nb * 16:
+            self._idx_host = torch.empty((2, nb * 16), dtype=torch.int32, pin_memory=True)
+            self._idx_dev = torch.empty((2, nb * 16), dtype=torch.int32, device=self.values.device)
+            self._idx_copied = [None, None]
+        ar16 = np.arange(16, dtype=np.int32)
+        cur = torch.cuda.current_stream(self.values.device) if stream is None else stream
+        for it in range(iterations):
+            k = it & 1
+            if self._idx_copied[k] is not None:
+                self._idx_copied[k].synchronize()          # this slot's previous copy has run
+            host = self._idx_host[k].numpy().reshape(nb, 16)
+            np.add(rng.permutation(nb).astype(np.int32)[:, None] * 16, ar16, out=host)
+            with torch.cuda.stream(cur):
+                self._idx_dev[k].copy_(self._idx_host[k], non_blocking=True)
+                ev = torch.cuda.Event()
+                ev.record(cur)
+            self._idx_copied[k] = ev
+            idx = self._idx_dev[k]
             for j in range(batches):
                 A.auv_ppo_grad(self.critic_cfg, None, self.val.mlp, batch, idx[j * B:(j + 1) * B], B, None, self.grad_v,
                                self.critic_stats, self._critic_work, stream)
