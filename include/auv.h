@@ -320,6 +320,28 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
                  const auv_ppo_net* value, const float* grad_policy, const float* grad_value,
                  const float* stats, void* stream);
 
+/* A value net's regression over a batch in one call (SHAC's critic update, paper Sec. II-B;
+ * the value loss of auv_ppo_grad): `iterations` passes, each shuffling the M / 16 blocks of
+ * 16 consecutive samples (Fisher-Yates, Knuth TAOCP Vol. 2 Algorithm P, driven by a
+ * SplitMix64 stream started at `seed`) and taking `batches` minibatches of B = 16 floor(M / 16
+ * / batches) samples from the front of that order; each minibatch is one auv_ppo_grad with the
+ * policy left out and one auv_ppo_adam step of value_net (steps t0 + 1, t0 + 2, ...).  value
+ * is value_net's auv_mlp view; batch: obs and ret are read (M = batch->M).  The host
+ * shuffles the next pass while the device runs the current one: a pass's indices are
+ * written into one half of host_stage (int32 [2][16 floor(M / 16)], pinned host memory
+ * owned by the caller) and copied asynchronously into the workspace.  The call returns when
+ * every copy has been made (the device may still run the last minibatches); grad_value
+ * [AUV_PPO_NPARAM(1)] and stats [8] then hold the last minibatch's results.  work:
+ * auv_ppo_fit_work_bytes(M, batches) bytes (-1 unless 16 <= M <= 2^28 and 1 <= batches <=
+ * M / 16), 16-byte aligned.  Deterministic for a given seed.  AUV_EINVAL, nothing
+ * enqueued: sizes out of range, NULL or misaligned pointers, iterations < 1, t0 < 0, or what
+ * auv_ppo_grad / auv_ppo_adam reject. */
+int64_t auv_ppo_fit_work_bytes(int64_t M, int32_t batches);
+int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv_ppo_net* value_net,
+                      const auv_ppo_batch* batch, int32_t iterations, int32_t batches, uint64_t seed,
+                      int64_t t0, int32_t* host_stage, float* grad_value, float* stats, void* work,
+                      void* stream);
+
 /* ---- SHAC: the actor gradient of one short window on the paper task -------------------
  * Short-Horizon Actor-Critic (Xu et al. 2022; the differentiable-simulation learner of
  * paper Sec. II-B, trained on the paper task of auv_set_task).  One window of h control

@@ -119,6 +119,9 @@ def _load() -> ctypes.CDLL:
         "auv_ppo_grad": (ctypes.c_int, [P(AuvPpoConfig), P(AuvMlp), P(AuvMlp), P(AuvPpoBatch), _vp, i32, _vp, _vp,
                                         _vp, _vp, _vp]),
         "auv_ppo_adam": (ctypes.c_int, [P(AuvPpoConfig), i64, P(AuvPpoNet), P(AuvPpoNet), _vp, _vp, _vp, _vp]),
+        "auv_ppo_fit_work_bytes": (i64, [i64, i32]),
+        "auv_ppo_fit_value": (ctypes.c_int, [P(AuvPpoConfig), P(AuvMlp), P(AuvPpoNet), P(AuvPpoBatch), i32, i32,
+                                             ctypes.c_uint64, i64, _vp, _vp, _vp, _vp, _vp]),
         "auv_shac_work_bytes": (i64, [i32, i32]),
         "auv_shac_window": (ctypes.c_int, [_vp, P(AuvShacConfig), P(AuvMlp), P(AuvMlp), P(AuvShacBuffers), _vp, _vp,
                                            _vp, _vp]),
@@ -225,6 +228,18 @@ def auv_ppo_adam(cfg: AuvPpoConfig, t: int, policy: AuvPpoNet | None, value: Auv
     ref = lambda n: ctypes.byref(n) if n is not None else None  # noqa: E731
     _check(lib.auv_ppo_adam(ctypes.byref(cfg), t, ref(policy), ref(value), ptr(grad_policy), ptr(grad_value),
                             ptr(stats), stream_ptr(stream)))
+
+
+def auv_ppo_fit_work_bytes(M: int, batches: int) -> int:
+    return int(lib.auv_ppo_fit_work_bytes(M, batches))
+
+
+def auv_ppo_fit_value(cfg: AuvPpoConfig, value: AuvMlp, value_net: AuvPpoNet, batch: AuvPpoBatch, iterations: int,
+                      batches: int, seed: int, t0: int, host_stage, grad_value, stats, work, stream=None) -> None:
+    """host_stage: pinned CPU int32 tensor of 2 * 16 * (M // 16) entries."""
+    _check(lib.auv_ppo_fit_value(ctypes.byref(cfg), ctypes.byref(value), ctypes.byref(value_net), ctypes.byref(batch),
+                                 iterations, batches, seed, t0, ptr(host_stage), ptr(grad_value), ptr(stats), ptr(work),
+                                 stream_ptr(stream)))
 
 
 def auv_shac_work_bytes(n_envs: int, h: int) -> int:

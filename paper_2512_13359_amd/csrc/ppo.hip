@@ -28,6 +28,7 @@
 // r); a per-wave LDS transpose turns them into "half fragments" (lane (g, r): feature r of a
 // 16-feature tile, samples 4g..4g+3 of a 16-sample tile, 8 bytes).
 #include <cmath>
+#include <vector>
 
 #include "auv_internal.hpp"
 #include "mlp_mfma.hpp"
@@ -949,6 +950,85 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
                        bc1, bc2);
   }
   return check_launch("auv_ppo_adam");
+}
+
+// Minibatch size of a regression pass: whole 16-sample blocks, the same number per minibatch.
+static int32_t fit_batch(int64_t M, int32_t batches) { return (int32_t)(M / 16 / batches * 16); }
+
+int64_t auv_ppo_fit_work_bytes(int64_t M, int32_t batches) {
+  if (M < 16 || M > ((int64_t)1 << 28) || batches < 1 || M / 16 < batches) return -1;
+  const int64_t w = auv_ppo_work_bytes(fit_batch(M, batches));
+  if (w < 0) return -1;
+  return (int64_t)ppo::align256((size_t)w) + 2 * (M / 16) * 16 * (int64_t)sizeof(int32_t);
+}
+
+// SplitMix64 (Steele, Lea and Flood 2014): the generator of the passes' shuffles.
+static inline uint64_t splitmix64(uint64_t& s) {
+  uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv_ppo_net* value_net,
+                      const auv_ppo_batch* batch, int32_t iterations, int32_t batches, uint64_t seed, int64_t t0,
+                      int32_t* host_stage, float* grad_value, float* stats, void* work, void* stream) {
+  if (int rc = check_ppo_config(cfg)) return rc;
+  if (int rc = check_net(value, 1, "auv_ppo_fit_value value")) return rc;
+  if (!value_net || value_net->n_out != 1 || !batch || !host_stage || !work || !aligned16(work))
+    return set_error(AUV_EINVAL, "auv_ppo_fit_value: NULL or misaligned network, batch, host_stage or work");
+  if (iterations < 1 || t0 < 0) return set_error(AUV_EINVAL, "auv_ppo_fit_value: iterations >= 1 and t0 >= 0 required");
+  const int64_t M = batch->M;
+  if (auv_ppo_fit_work_bytes(M, batches) < 0)
+    return set_error(AUV_EINVAL, "auv_ppo_fit_value: need 16 <= M <= 2^28 and 1 <= batches <= M / 16");
+  const int32_t B = fit_batch(M, batches);
+  const int64_t nb = M / 16, n = nb * 16;
+  size_t off = ppo::align256((size_t)auv_ppo_work_bytes(B));
+  int32_t* dev_idx = (int32_t*)((char*)work + off);   // [2][n] sample indices, one slot per pass parity
+  hipStream_t s = (hipStream_t)stream;
+  hipEvent_t copied[2];
+  for (int k = 0; k < 2; ++k)
+    if (hipEventCreateWithFlags(&copied[k], hipEventDisableTiming) != hipSuccess)
+      return set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventCreate failed");
+  bool pending[2] = {false, false};
+  std::vector<int32_t> perm((size_t)nb);
+  uint64_t rs = seed;
+  int rc = AUV_OK;
+  for (int p = 0; p < iterations && rc == AUV_OK; ++p) {
+    const int k = p & 1;
+    // Fisher-Yates shuffle of the blocks (Knuth, TAOCP Vol. 2, Sec. 3.4.2, Algorithm P), the
+    // index j uniform in [0, i] by the multiply-shift of a 32-bit draw
+    for (int64_t b = 0; b < nb; ++b) perm[b] = (int32_t)b;
+    for (int64_t i = nb - 1; i > 0; --i) {
+      const uint64_t j = ((splitmix64(rs) >> 32) * (uint64_t)(i + 1)) >> 32;
+      std::swap(perm[i], perm[j]);
+    }
+    if (pending[k] && hipEventSynchronize(copied[k]) != hipSuccess) {   // the slot's last copy has run
+      rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventSynchronize failed");
+      break;
+    }
+    int32_t* stage = host_stage + k * n;
+    for (int64_t b = 0; b < nb; ++b)
+      for (int r = 0; r < 16; ++r) stage[b * 16 + r] = perm[b] * 16 + r;
+    int32_t* idx = dev_idx + k * n;
+    if (hipMemcpyAsync(idx, stage, (size_t)n * sizeof(int32_t), hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipEventRecord(copied[k], s) != hipSuccess) {
+      rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: index copy failed");
+      break;
+    }
+    pending[k] = true;
+    for (int j = 0; j < batches && rc == AUV_OK; ++j) {
+      rc = auv_ppo_grad(cfg, nullptr, value, batch, idx + (int64_t)j * B, B, nullptr, grad_value, stats, work, stream);
+      if (rc == AUV_OK)
+        rc = auv_ppo_adam(cfg, t0 + 1 + (int64_t)p * batches + j, nullptr, value_net, nullptr, grad_value, stats, stream);
+    }
+  }
+  for (int k = 0; k < 2; ++k) {   // the caller may reuse host_stage once the call returns
+    if (pending[k] && hipEventSynchronize(copied[k]) != hipSuccess && rc == AUV_OK)
+      rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventSynchronize failed");
+    (void)hipEventDestroy(copied[k]);
+  }
+  return rc;
 }
 
 }  // extern "C"

@@ -5,11 +5,10 @@ weight copy), the gradients, statistics and workspace buffers, and the window's 
 observations, rewards and values.  Calls auv_shac_window (one window's actor loss and policy
 gradient), auv_ppo_adam with the value net left out (the actor step), and for the critic
 auv_mlp_forward (values of the window's observations), auv_gae (TD(lambda) targets) and
-auv_ppo_grad / auv_ppo_adam with the policy left out (value regression).  Memory management
+auv_ppo_fit_value (the value regression).  Memory management
 and argument marshalling only."""
 from __future__ import annotations
 
-import numpy as np
 import torch
 
 from . import _abi as A
@@ -54,6 +53,7 @@ class ShacLearner:
         self.ret = torch.zeros(self.h, n, **f32)
         self._no_done = torch.zeros(self.h, n, **f32)
         self._critic_work = None
+        self._critic_shape = None
         self._idx_host = None
         self.t = 0
         self.t_critic = 0
@@ -88,43 +88,20 @@ class ShacLearner:
                   self.adv, self.ret, stream)
 
     def critic_update(self, iterations: int = 16, batches: int = 4, seed: int = 0, stream=None) -> None:
-        """Value regression on the last window: `iterations` passes, each over `batches`
-        minibatches of a seeded permutation of the window's h N samples (16-sample blocks),
-        each a value-only gradient and Adam step of the value net."""
+        """Value regression on the last window (auv_ppo_fit_value): `iterations` passes, each
+        over `batches` minibatches of a seeded shuffle of the window's h N samples (16-sample
+        blocks), each a value-only gradient and Adam step of the value net."""
         self.targets(stream)
         M = self.h * self.n
-        B = (M // 16 // batches) * 16          # whole 16-sample blocks per minibatch
-        if B < 16:
+        if A.auv_ppo_fit_work_bytes(M, batches) < 0:
             raise ValueError("too few samples for this many minibatches")
-        if self._critic_work is None:
-            self._critic_work = torch.empty(A.auv_ppo_work_bytes(B), dtype=torch.uint8, device=self.values.device)
+        if self._critic_work is None or self._critic_shape != (M, batches):
+            self._critic_work = torch.empty(A.auv_ppo_fit_work_bytes(M, batches), dtype=torch.uint8,
+                                            device=self.values.device)
+            self._idx_host = torch.empty(2 * 16 * (M // 16), dtype=torch.int32, pin_memory=True)
+            self._critic_shape = (M, batches)
         b = self._last
         batch = A.make_ppo_batch(b["obs"], b["obs"], self.values, self.adv, self.ret, M)
-        rng = np.random.Generator(np.random.PCG64(seed))
-        # each iteration's indices go through one of two pinned host slots and an asynchronous
-        # copy, so the host prepares the next permutation while the device works on this one
-        nb = M // 16
-        if self._idx_host is None or self._idx_host.shape[1] != nb * 16:
-            self._idx_host = torch.empty((2, nb * 16), dtype=torch.int32, pin_memory=True)
-            self._idx_dev = torch.empty((2, nb * 16), dtype=torch.int32, device=self.values.device)
-            self._idx_copied = [None, None]
-        ar16 = np.arange(16, dtype=np.int32)
-        cur = torch.cuda.current_stream(self.values.device) if stream is None else stream
-        for it in range(iterations):
-            k = it & 1
-            if self._idx_copied[k] is not None:
-                self._idx_copied[k].synchronize()          # this slot's previous copy has run
-            host = self._idx_host[k].numpy().reshape(nb, 16)
-            np.add(rng.permutation(nb).astype(np.int32)[:, None] * 16, ar16, out=host)
-            with torch.cuda.stream(cur):
-                self._idx_dev[k].copy_(self._idx_host[k], non_blocking=True)
-                ev = torch.cuda.Event()
-                ev.record(cur)
-            self._idx_copied[k] = ev
-            idx = self._idx_dev[k]
-            for j in range(batches):
-                A.auv_ppo_grad(self.critic_cfg, None, self.val.mlp, batch, idx[j * B:(j + 1) * B], B, None, self.grad_v,
-                               self.critic_stats, self._critic_work, stream)
-                self.t_critic += 1
-                A.auv_ppo_adam(self.critic_cfg, self.t_critic, None, self.val.net, None, self.grad_v, self.critic_stats,
-                               stream)
+        A.auv_ppo_fit_value(self.critic_cfg, self.val.mlp, self.val.net, batch, iterations, batches, seed,
+                            self.t_critic, self._idx_host, self.grad_v, self.critic_stats, self._critic_work, stream)
+        self.t_critic += iterations * batches

@@ -315,3 +315,66 @@ def test_shac_critic_regression():
     A.auv_mlp_forward(L.val.mlp, M, b["obs"], L.values)
     after = float(torch.mean((L.values - L.ret) ** 2))
     assert after < 0.8 * before, (before, after)
+
+
+def _splitmix64(state):
+    """SplitMix64 (Steele, Lea and Flood 2014): (next state, output)."""
+    m = (1 << 64) - 1
+    state = (state + 0x9E3779B97F4A7C15) & m
+    z = state
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & m
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & m
+    return state, z ^ (z >> 31)
+
+
+def _fit_indices(M, iterations, seed):
+    """The passes' sample orders of auv_ppo_fit_value, restated: Fisher-Yates over the M // 16
+    blocks (j uniform in [0, i] by the multiply-shift of the draw's high 32 bits)."""
+    nb, st, out = M // 16, seed, []
+    for _ in range(iterations):
+        perm = list(range(nb))
+        for i in range(nb - 1, 0, -1):
+            st, r = _splitmix64(st)
+            j = ((r >> 32) * (i + 1)) >> 32
+            perm[i], perm[j] = perm[j], perm[i]
+        out.append((np.array(perm, np.int64)[:, None] * 16 + np.arange(16)).ravel().astype(np.int32))
+    return out
+
+
+def test_ppo_fit_value_matches_stepwise_calls():
+    """auv_ppo_fit_value equals the same value-only gradient + Adam steps issued one call at
+    a time with the shuffles restated in Python (bit for bit), and rejects bad sizes."""
+    n, h, iterations, batches, seed = 130, 6, 3, 4, 12345
+    announce(f"PPO fit value n={n} h={h} iterations={iterations}")
+    require_gpu()
+    from paper_2512_13359_amd import _abi as A
+    from paper_2512_13359_amd.ppo import PpoNet
+    _, g, _ = _setup(n, seed=14)
+    L = _learner(g, h)
+    L.window()
+    L.targets()
+    M = h * n
+    b = L._last
+    batch = A.make_ppo_batch(b["obs"], b["obs"], L.values, L.adv, L.ret, M)
+    val = W.mlp_weights(1, W.PAPER_VALUE_SEED, n_in=12)
+    net1, net2 = PpoNet(val, "cuda"), PpoNet(val, "cuda")
+    work = torch.empty(A.auv_ppo_fit_work_bytes(M, batches), dtype=torch.uint8, device="cuda")
+    stage = torch.empty(2 * 16 * (M // 16), dtype=torch.int32, pin_memory=True)
+    g1, s1 = torch.zeros(A.ppo_nparam(1), device="cuda"), torch.zeros(8, device="cuda")
+    A.auv_ppo_fit_value(L.critic_cfg, net1.mlp, net1.net, batch, iterations, batches, seed, 5, stage, g1, s1, work)
+    B = (M // 16 // batches) * 16
+    g2, s2 = torch.zeros_like(g1), torch.zeros_like(s1)
+    w2 = torch.empty(A.auv_ppo_work_bytes(B), dtype=torch.uint8, device="cuda")
+    t = 5
+    for order in _fit_indices(M, iterations, seed):
+        idx = torch.from_numpy(order).cuda()
+        for j in range(batches):
+            A.auv_ppo_grad(L.critic_cfg, None, net2.mlp, batch, idx[j * B:(j + 1) * B], B, None, g2, s2, w2)
+            t += 1
+            A.auv_ppo_adam(L.critic_cfg, t, None, net2.net, None, g2, s2)
+    torch.cuda.synchronize()
+    assert torch.equal(net1.theta, net2.theta) and torch.equal(net1.w_bf16, net2.w_bf16)
+    assert torch.equal(g1, g2) and torch.equal(s1, s2)
+    assert A.auv_ppo_fit_work_bytes(15, 1) == -1 and A.auv_ppo_fit_work_bytes(64, 5) == -1
+    with pytest.raises(A.AuvError):
+        A.auv_ppo_fit_value(L.critic_cfg, net1.mlp, net1.net, batch, 0, batches, seed, 0, stage, g1, s1, work)
