@@ -163,6 +163,31 @@ def test_shac_policy_gradient_matches_oracle(mode):
     assert np.isclose(stats[7], min(1.0, 1.0 / (np.sqrt(stats[5]) + 1e-6)), rtol=1e-6)
 
 
+@pytest.mark.parametrize("n,h", [(1, 1), (17, 2), (16, 3)])
+def test_shac_small_and_ragged(n, h):
+    """One environment and a one-step window (15 idle slots of the workgroup), a batch one
+    environment past a workgroup (a second group with one live slot), and exactly one group:
+    sampled-policy windows against the oracle, with the same tolerances as the larger test."""
+    gamma = 0.99
+    announce(f"SHAC small window n={n} h={h}")
+    require_gpu()
+    cfg, g, start = _setup(n, seed=31 + n)
+    pol, val = _nets()
+    L = _learner(g, h, gamma)
+    out = dict(grad_act=_dev(8, h, n), reward=_dev(h, n))
+    L.window(mode=3, out=out)
+    want = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, gamma, 3, policy_net=pol, value_net=val,
+                         quantize=True)
+    assert rel_err(host(out["reward"]), want["rewards"]).max() <= 1e-3
+    ga = np.transpose(host(out["grad_act"])[0:6], (1, 0, 2))
+    assert _block_err(ga, want["grad_act"]) <= 2e-2
+    blocks, pad = _unpad(host(L.grad))
+    assert np.all(pad == 0)
+    for k in blocks:
+        assert _block_err(blocks[k], want["grad_policy"][k]) <= 5e-3, k
+    assert abs(host(L.stats)[0] - want["loss"]) <= 1e-3 * abs(want["loss"])
+
+
 def test_shac_window_ends_episode_then_resets():
     """8-step episodes, 4-step windows: the second window ends the episode at its last step;
     its terminal value is taken before the reset, then every env starts episode 1 as the
