@@ -988,8 +988,10 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
   hipStream_t s = (hipStream_t)stream;
   hipEvent_t copied[2];
   for (int k = 0; k < 2; ++k)
-    if (hipEventCreateWithFlags(&copied[k], hipEventDisableTiming) != hipSuccess)
+    if (hipEventCreateWithFlags(&copied[k], hipEventDisableTiming) != hipSuccess) {
+      if (k == 1) (void)hipEventDestroy(copied[0]);
       return set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventCreate failed");
+    }
   bool pending[2] = {false, false};
   std::vector<int32_t> perm((size_t)nb);
   uint64_t rs = seed;
