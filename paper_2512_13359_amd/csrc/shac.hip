@@ -16,13 +16,14 @@
 //                  in LDS; its small weights in registers).  At workgroup barriers the waves
 //                  exchange through LDS only hidden layer 1 and the output partials (two
 //                  barriers per forward step), q(dz2) and the input-gradient partials (two
-//                  per reverse step).  Forward sweep: policy
-//                  on MFMA, RK4 of the paper task, reward, checkpoints of every step's state
-//                  and action average, every wave's hidden-2 activations; terminal value and
-//                  its input gradient; the environment update (reset where the window ends
-//                  the episode); reverse sweep: per step, the state adjoint through reward,
-//                  observation and RK4 (shac_adjoint.hpp), the clip, and the policy's input
-//                  gradient (backward on MFMA from the stored hidden-2 activations).  Each
+//                  per reverse step).  Forward sweep: policy on MFMA, RK4 of the paper
+//                  task, reward, checkpoints of every step's state, RK4 substep start
+//                  states and action average, every wave's hidden-2 activations; terminal
+//                  value and its input gradient; the environment update (reset where the
+//                  window ends the episode); reverse sweep: per step, the state adjoint
+//                  through reward, observation and RK4 (shac_adjoint.hpp; each substep's
+//                  adjoint starts from its stored start state), the clip, and the policy's
+//                  input gradient (backward on MFMA from the stored hidden-2 activations).  Each
 //                  wave stores the bf16 operands of the weight gradient of its features
 //                  (q(h1), q(h2), q(dz2), q(dz1); wave 0 also q(o), q(gy)) as "half
 //                  fragments"
