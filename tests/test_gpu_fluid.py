@@ -9,6 +9,7 @@ import torch
 
 import workloads as W
 from oracle import fluid as fl
+from oracle import mlp as omlp
 from oracle import paper_task as P
 from oracle import shac as S
 from tests.gpu_util import announce, gpu_env, host, quat_aligned, rel_err, require_gpu
@@ -50,6 +51,32 @@ def test_box_model_random_rollout_matches_oracle():
     fb = f.rollout_buffers(T, record=("traj_state",))
     f.rollout(T, W.MODE_RANDOM, bufs=fb)
     assert np.max(np.abs(host(fb["traj_state"]) - got["traj_state"])) > 1e-2
+
+
+def test_box_model_policy_rollout_matches_oracle():
+    """The 12-256-256-6 policy (mean) in closed loop on the box model, a ragged batch with one
+    episode end: every action is a valid bf16-policy output for the observation it was taken
+    on, and under the GPU's actions the oracle's box model reproduces every reward, episode end
+    and state."""
+    require_gpu()
+    from paper_2512_13359_amd import upload_mlp
+    pol = W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12)
+    n, T = 200 + 3, 40
+    cfg = W.config("c6", n_envs=n, episode_len=25)
+    announce(f"inertia-box policy rollout n={n} T={T}")
+    g, o = _pair(cfg)
+    bufs = g.rollout_buffers(T, record=("obs", "act", "reward", "done", "traj_state"))
+    g.rollout(T, W.MODE_POLICY_MEAN, policy=upload_mlp(pol), bufs=bufs)
+    got = {k: host(v) for k, v in bufs.items()}
+    act, obs = got["act"][0:6], got["obs"][0:12]
+    err = omlp.nearest_valid_error(act.reshape(6, -1), obs.reshape(12, -1).astype(np.float64), pol, 1e-6)
+    assert err.max() <= 2e-4
+    rec = o.rollout(T, P.MODE_EXTERNAL, external=np.transpose(act, (1, 0, 2)).astype(np.float64), record_state=True)
+    assert np.array_equal(got["done"], rec["done"].astype(np.float32))
+    traj = got["traj_state"].copy()
+    traj[3:7] = quat_aligned(traj[3:7], rec["traj_state"][3:7])
+    assert rel_err(traj, rec["traj_state"]).max() <= 1e-3
+    assert rel_err(got["reward"], rec["reward"]).max() <= 1e-3
 
 
 def test_box_model_terminal_speeds():
