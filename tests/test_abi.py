@@ -89,6 +89,26 @@ def test_argument_errors_before_any_launch():
     assert A.auv_stats_work_floats(65, 2) == 3 * 2 * 4 * 2
 
 
+def test_value_regression_sizes_and_argument_errors():
+    """auv_ppo_fit_work_bytes: -1 outside 16 <= M <= 2^28, 1 <= batches <= M / 16; else the
+    minibatch workspace plus two index slots.  auv_ppo_fit_value rejects bad arguments on the
+    host (no GPU needed)."""
+    from paper_2512_13359_amd import _abi as A
+    assert A.auv_ppo_fit_work_bytes(15, 1) == -1 and A.auv_ppo_fit_work_bytes(64, 5) == -1
+    assert A.auv_ppo_fit_work_bytes(64, 0) == -1 and A.auv_ppo_fit_work_bytes((1 << 28) + 16, 1) == -1
+    M, b = 131072, 4
+    B = M // 16 // b * 16
+    base = A.auv_ppo_work_bytes(B)
+    assert A.auv_ppo_fit_work_bytes(M, b) == (base + 255) // 256 * 256 + 2 * M * 4
+    cfg = A.make_ppo_config(vf_coef=2.0, ent_coef=0.0, max_grad_norm=0.0, normalize_adv=False)
+    net = A.AuvPpoNet(0x1000, 0x1000, 0x1000, 0x1000, 1)
+    mlp = A.AuvMlp()
+    batch = A.AuvPpoBatch()
+    rc = A.lib.auv_ppo_fit_value(ctypes.byref(cfg), ctypes.byref(mlp), ctypes.byref(net), ctypes.byref(batch), 1, 1, 0,
+                                 0, 0x1000, 0x1000, 0x1000, 0x1000, None)
+    assert rc == A.AUV_EINVAL
+
+
 def test_binding_structs_match_header_sizes():
     from paper_2512_13359_amd import _abi as A
     assert ctypes.sizeof(A.AuvVehicle) == 4 * (1 + 3 + 6 + 6 + 6 + 2 + 3 + 1 + 48)
