@@ -681,13 +681,38 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
       for (int nt = 0; nt < 8; ++nt) out[(64 * mr + 16 * mt + 4 * g + i) * HID + 128 * nc + 16 * nt + r] = acc[mt][nt][i];
 }
 
+// One Adam step of packed entry e with gradient g (k_adam's update; the bf16 copy of the
+// weight matrices rounded to nearest even).  A fused step (theta set) runs in k_reduce.
+struct AdamFuse {
+  float *theta = nullptr, *mom = nullptr, *vel = nullptr;
+  uint16_t* wbf = nullptr;
+  int nW = 0;
+  float lr = 0.0f, b1 = 0.0f, b2 = 0.0f, eps = 1.0f, bc1 = 1.0f, bc2 = 1.0f;
+  float clip = 1.0f;   // fused step: the clipping factor (a kernel argument, 1 without clipping)
+};
+
+// g0: the raw gradient entry; the step uses g0 times the clipping factor `clip` (the same
+// operations in k_adam and in the fused step, so both give the same bits).
+__device__ __forceinline__ void adam_entry(const AdamFuse& A, int e, float g0, float clip) {
+  const float g = g0 * clip;
+  // explicit fused multiply-adds: no contraction left to the compiler, which could fuse the
+  // moment updates differently in the two kernels
+  const float m = __builtin_fmaf(A.b1, A.mom[e], (1.0f - A.b1) * g);
+  const float v = __builtin_fmaf(A.b2, A.vel[e], ((1.0f - A.b2) * g) * g);
+  const float th = A.theta[e] - A.lr * (m / A.bc1) / (sqrtf(v / A.bc2) + A.eps);
+  A.mom[e] = m;
+  A.vel[e] = v;
+  A.theta[e] = th;
+  if (e < A.nW) A.wbf[e] = __builtin_bit_cast(uint16_t, (__bf16)th);
+}
+
 // Packed gradient of one network = fixed-order sums of the partials, and per-block sums of
 // squares for the global norm.  A block owns 64 gradient entries (one per lane); its four
 // waves each sum a contiguous quarter of the workgroup partials with eight loads in flight,
 // then wave 0 adds the quarters in wave order.  G1: forward/backward groups (dW3, db2, db3,
 // d log_std), G2: dz1 groups (dW1, db1), G3: dW2 groups.
 __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, int G2, int G3, Work W, float ent_coef,
-                                                float* __restrict__ grad, float* __restrict__ ss) {
+                                                float* __restrict__ grad, float* __restrict__ ss, AdamFuse A) {
   __shared__ float part[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int e = blockIdx.x * RED_ELEMS + lane;
@@ -740,7 +765,10 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, in
   __syncthreads();
   if (w == 0) {
     const float v = e < P ? part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane] + add : 0.0f;
-    if (e < P) grad[e] = v;
+    if (e < P) {
+      grad[e] = v;
+      if (A.theta) adam_entry(A, e, v, A.clip);   // fused step: no gradient clipping (factor 1)
+    }
     const float s2 = wave_sum(v * v);
     if (lane == 0) ss[blockIdx.x] = s2;
   }
@@ -803,14 +831,19 @@ __global__ __launch_bounds__(256) void k_adam(int P, int nW, float* __restrict__
                                               float lr, float b1, float b2, float eps, float bc1, float bc2) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= P) return;
-  const float g = grad[e] * stats[7];
-  const float m = b1 * mom[e] + (1.0f - b1) * g;
-  const float v = b2 * vel[e] + (1.0f - b2) * g * g;
-  const float th = theta[e] - lr * (m / bc1) / (sqrtf(v / bc2) + eps);
-  mom[e] = m;
-  vel[e] = v;
-  theta[e] = th;
-  if (e < nW) wbf[e] = __builtin_bit_cast(uint16_t, (__bf16)th);
+  AdamFuse A;
+  A.theta = theta;
+  A.mom = mom;
+  A.vel = vel;
+  A.wbf = wbf;
+  A.nW = nW;
+  A.lr = lr;
+  A.b1 = b1;
+  A.b2 = b2;
+  A.eps = eps;
+  A.bc1 = bc1;
+  A.bc2 = bc2;
+  adam_entry(A, e, grad[e], stats[7]);
 }
 
 }  // namespace ppo
@@ -832,7 +865,7 @@ int launch_grad_reduce(const GradParts& P, int n_out, int n_act, int G1, int G2,
   W.part_b3 = P.part_b3;
   W.part_ls = P.part_ls;
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(n_out)), dim3(256), 0, s, n_out, n_act, G1, G2, G3, W, 0.0f,
-                     grad, ss);
+                     grad, ss, ppo::AdamFuse{});
   return check_launch("gradient reduce");
 }
 
@@ -862,17 +895,10 @@ static int check_ppo_config(const auv_ppo_config* c) {
 
 constexpr int32_t PPO_MAX_B = 1 << 24;
 
-extern "C" {
-
-int64_t auv_ppo_work_bytes(int32_t B) {
-  if (B < 1 || B > PPO_MAX_B) return -1;
-  size_t off[ppo::WORK_PARTS];
-  return (int64_t)ppo::work_layout(B, off);
-}
-
-int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp* value, const auv_ppo_batch* batch,
-                 const int32_t* idx, int32_t B, float* grad_policy, float* grad_value, float* stats, void* work,
-                 void* stream) {
+// The argument checks of auv_ppo_grad (nothing enqueued on failure).
+static int check_grad_args(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp* value,
+                           const auv_ppo_batch* batch, const int32_t* idx, int32_t B, const float* grad_policy,
+                           const float* grad_value, const float* stats, const void* work) {
   if (int rc = check_ppo_config(cfg)) return rc;
   const bool with_policy = policy != nullptr;
   if (with_policy) {
@@ -888,7 +914,16 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
                           with_policy ? grad_policy : grad_value, grad_value, stats, work};
   for (int k = 0; k < 10; ++k)
     if (!ptrs[k] || !aligned16(ptrs[k])) return set_error(AUV_EINVAL, "auv_ppo_grad: pointer %d NULL or not 16-byte aligned", k);
-  hipStream_t s = (hipStream_t)stream;
+  return AUV_OK;
+}
+
+// The launches of one minibatch gradient (arguments checked).  fuse.theta set: the value net's
+// reduce also takes that net's Adam step (valid only without gradient clipping: the factor
+// is 1).  finalize: launch the statistics kernel (loss sums, norms, clipping factor).
+static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp* value,
+                       const auv_ppo_batch* batch, const int32_t* idx, int32_t B, float* grad_policy, float* grad_value,
+                       float* stats, void* work, hipStream_t s, const ppo::AdamFuse& fuse, bool finalize) {
+  const bool with_policy = policy != nullptr;
   const int tiles = ppo::padded(B) / 16, steps = ppo::padded(B) / 32;
   const int cus = std::min(compute_units(), ppo::MAX_GROUPS);
   const int G1 = std::min(cus, tiles), G3 = std::min(cus, steps / ppo::DW2_DEPTH);
@@ -909,17 +944,34 @@ int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp
     hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
     hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
     hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G3, W, cfg->ent_coef,
-                       grad_policy, W.part_ss);
+                       grad_policy, W.part_ss, ppo::AdamFuse{});
   }
   hipLaunchKernelGGL((ppo::k_fwd_bwd<1, FPW>), dim3(G1), dim3(TH), 0, s, value->w, value->b, (const float*)nullptr, D,
                      idx, B, tiles, hp, W, 1);
   hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, value->w, value->b, D, idx, B, tiles, W);
   hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, G1, G1, G3, W, 0.0f,
-                     grad_value, W.part_ss + rb);
-  hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? G1 : 0, G1, W, with_policy ? rb : 0,
-                     ppo::red_blocks(1), rb, with_policy ? policy->log_std : (const float*)nullptr, hp, stats);
+                     grad_value, W.part_ss + rb, fuse);
+  if (finalize)
+    hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? G1 : 0, G1, W, with_policy ? rb : 0,
+                       ppo::red_blocks(1), rb, with_policy ? policy->log_std : (const float*)nullptr, hp, stats);
   return check_launch("auv_ppo_grad");
+}
+
+extern "C" {
+
+int64_t auv_ppo_work_bytes(int32_t B) {
+  if (B < 1 || B > PPO_MAX_B) return -1;
+  size_t off[ppo::WORK_PARTS];
+  return (int64_t)ppo::work_layout(B, off);
+}
+
+int auv_ppo_grad(const auv_ppo_config* cfg, const auv_mlp* policy, const auv_mlp* value, const auv_ppo_batch* batch,
+                 const int32_t* idx, int32_t B, float* grad_policy, float* grad_value, float* stats, void* work,
+                 void* stream) {
+  if (int rc = check_grad_args(cfg, policy, value, batch, idx, B, grad_policy, grad_value, stats, work)) return rc;
+  return grad_launch(cfg, policy, value, batch, idx, B, grad_policy, grad_value, stats, work, (hipStream_t)stream,
+                     ppo::AdamFuse{}, true);
 }
 
 int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy, const auv_ppo_net* value,
@@ -983,6 +1035,16 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
     return set_error(AUV_EINVAL, "auv_ppo_fit_value: need 16 <= M <= 2^28 and 1 <= batches <= M / 16");
   const int32_t B = fit_batch(M, batches);
   const int64_t nb = M / 16, n = nb * 16;
+  {
+    const void* np[5] = {value_net->theta, value_net->adam_m, value_net->adam_v, value_net->w_bf16, stats};
+    for (const void* q : np)
+      if (!q || !aligned16(q)) return set_error(AUV_EINVAL, "auv_ppo_fit_value: value_net or stats pointer NULL or misaligned");
+  }
+  // every minibatch's arguments except its indices (device, 16-byte aligned: B is a multiple of 16)
+  if (int rc = check_grad_args(cfg, nullptr, value, batch, (const int32_t*)((char*)work + ppo::align256((size_t)auv_ppo_work_bytes(B))),
+                               B, nullptr, grad_value, stats, work))
+    return rc;
+  const bool fuse_adam = !(cfg->max_grad_norm > 0.0f);
   size_t off = ppo::align256((size_t)auv_ppo_work_bytes(B));
   int32_t* dev_idx = (int32_t*)((char*)work + off);   // [2][n] sample indices, one slot per pass parity
   hipStream_t s = (hipStream_t)stream;
@@ -1020,9 +1082,27 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
     }
     pending[k] = true;
     for (int j = 0; j < batches && rc == AUV_OK; ++j) {
-      rc = auv_ppo_grad(cfg, nullptr, value, batch, idx + (int64_t)j * B, B, nullptr, grad_value, stats, work, stream);
-      if (rc == AUV_OK)
-        rc = auv_ppo_adam(cfg, t0 + 1 + (int64_t)p * batches + j, nullptr, value_net, nullptr, grad_value, stats, stream);
+      const int64_t t = t0 + 1 + (int64_t)p * batches + j;
+      const int32_t* ij = idx + (int64_t)j * B;
+      const bool last = p == iterations - 1 && j == batches - 1;
+      if (fuse_adam) {   // no clipping: each reduce block takes the Adam step of its entries
+        ppo::AdamFuse A;
+        A.theta = value_net->theta;
+        A.mom = value_net->adam_m;
+        A.vel = value_net->adam_v;
+        A.wbf = value_net->w_bf16;
+        A.nW = HID * 23 + HID * HID + HID;
+        A.lr = cfg->lr;
+        A.b1 = cfg->beta1;
+        A.b2 = cfg->beta2;
+        A.eps = cfg->adam_eps;
+        A.bc1 = (float)(1.0 - std::pow((double)cfg->beta1, (double)t));
+        A.bc2 = (float)(1.0 - std::pow((double)cfg->beta2, (double)t));
+        rc = grad_launch(cfg, nullptr, value, batch, ij, B, nullptr, grad_value, stats, work, s, A, last);
+      } else {
+        rc = grad_launch(cfg, nullptr, value, batch, ij, B, nullptr, grad_value, stats, work, s, ppo::AdamFuse{}, true);
+        if (rc == AUV_OK) rc = auv_ppo_adam(cfg, t, nullptr, value_net, nullptr, grad_value, stats, stream);
+      }
     }
   }
   for (int k = 0; k < 2; ++k) {   // the caller may reuse host_stage once the call returns

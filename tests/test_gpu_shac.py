@@ -398,7 +398,9 @@ def test_ppo_fit_value_matches_stepwise_calls():
             t += 1
             A.auv_ppo_adam(L.critic_cfg, t, None, net2.net, None, g2, s2)
     torch.cuda.synchronize()
-    assert torch.equal(net1.theta, net2.theta) and torch.equal(net1.w_bf16, net2.w_bf16)
+    d = (net1.theta - net2.theta).abs()
+    assert torch.equal(net1.theta, net2.theta), (float(d.max()), int((d > 0).sum()), int(d.numel()))
+    assert torch.equal(net1.w_bf16, net2.w_bf16)
     assert torch.equal(g1, g2) and torch.equal(s1, s2)
     assert A.auv_ppo_fit_work_bytes(15, 1) == -1 and A.auv_ppo_fit_work_bytes(64, 5) == -1
     with pytest.raises(A.AuvError):
