@@ -325,7 +325,9 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
  * 16 consecutive samples (Fisher-Yates, Knuth TAOCP Vol. 2 Algorithm P, driven by a
  * SplitMix64 stream started at `seed`) and taking `batches` minibatches of B = 16 floor(M / 16
  * / batches) samples from the front of that order; each minibatch is one auv_ppo_grad with the
- * policy left out and one auv_ppo_adam step of value_net (steps t0 + 1, t0 + 2, ...).  value
+ * policy left out and one auv_ppo_adam step of value_net (steps t0 + 1, t0 + 2, ...); without
+ * gradient clipping (max_grad_norm <= 0) the Adam step runs inside the gradient's last kernel,
+ * with the same bits as the separate calls.  value
  * is value_net's auv_mlp view; batch: obs and ret are read (M = batch->M).  The host
  * shuffles the next pass while the device runs the current one: a pass's indices are
  * written into one half of host_stage (int32 [2][16 floor(M / 16)], pinned host memory
