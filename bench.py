@@ -404,6 +404,7 @@ def main() -> int:
     ap.add_argument("--ppo-only", action="store_true", help="only measure the PPO update and print it")
     ap.add_argument("--paper-only", action="store_true", help="only measure the paper task (c6, training iteration)")
     ap.add_argument("--shac-only", action="store_true", help="only measure the SHAC windows (4096 and 512 envs)")
+    ap.add_argument("--c5-only", action="store_true", help="only measure the PPO-buffer rollout and GAE (c5)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -432,6 +433,9 @@ def main() -> int:
         return 0
     if args.paper_only:
         print(json.dumps({"c6": paper_task_measure(), "paper_training": paper_training_measure()}), flush=True)
+        return 0
+    if args.c5_only:
+        print(json.dumps({"c5": c5_measure()}), flush=True)
         return 0
     if args.shac_only:
         print(json.dumps({"shac": [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]}),
