@@ -392,6 +392,47 @@ def small_configs_measure(reps: int = 3) -> dict:
     return out
 
 
+SWEEP_ENVS = (64, 256, 1024, 4096, 8192, 16384, 32768, 65536)
+
+
+def sweep_measure(reps: int = 3) -> list:
+    """The headline workload's rollout (policy mean, 4 RK4 substeps, Lissajous references,
+    2000 control steps) at environment counts from 64 to 65536: launch time by HIP events
+    (median of reps after one warm-up launch), env-steps/s and the fraction of the same
+    per-env-step lower bound as the headline line (report only)."""
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, upload_mlp
+
+    pol = upload_mlp(W.mlp_weights(8, W.POLICY_SEED))
+    t_lb = F_MFMA / P_MFMA + F_VALU / P_VALU + N_TRANS / P_TRANS
+    out = []
+    for n in SWEEP_ENVS:
+        cfg = W.config("c4", n_envs=n)
+        T = cfg["T"]
+        env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+        env.reset()
+        bufs = env.rollout_buffers(T, record=("stats",))
+        times = []
+        for k in range(reps + 1):
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            env.rollout(T, cfg["mode"], policy=pol, bufs=bufs)
+            e1.record()
+            torch.cuda.synchronize()
+            if k:
+                times.append(e0.elapsed_time(e1) * 1e-3)
+        t = sorted(times)[len(times) // 2]
+        assert torch.isfinite(bufs["stats"]).all(), f"non-finite statistics at {n} envs"
+        out.append({"n_envs": n, "control_steps": T, "launch_ms": t * 1e3, "env_steps_per_s": n * T / t,
+                    "frac": t_lb * n * T / t})
+        print(json.dumps({"sweep_point": out[-1]}), file=sys.stderr, flush=True)
+        del env, bufs
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -405,6 +446,8 @@ def main() -> int:
     ap.add_argument("--paper-only", action="store_true", help="only measure the paper task (c6, training iteration)")
     ap.add_argument("--shac-only", action="store_true", help="only measure the SHAC windows (4096 and 512 envs)")
     ap.add_argument("--c5-only", action="store_true", help="only measure the PPO-buffer rollout and GAE (c5)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only measure the headline rollout at 64 to 65536 envs and print it")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -436,6 +479,9 @@ def main() -> int:
         return 0
     if args.c5_only:
         print(json.dumps({"c5": c5_measure()}), flush=True)
+        return 0
+    if args.sweep:
+        print(json.dumps({"sweep": sweep_measure()}), flush=True)
         return 0
     if args.shac_only:
         print(json.dumps({"shac": [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]}),
@@ -511,6 +557,7 @@ def main() -> int:
     if not args.no_c5:
         line["c5"] = c5_measure()
         line.update(small_configs_measure())
+        line["sweep"] = sweep_measure()
     if not args.no_ppo and not args.no_c5:
         line["ppo"] = ppo_measure()
         line["c6"] = paper_task_measure()
