@@ -7,11 +7,12 @@
 //   k_adv_partial   per-block sums of the minibatch's advantages and their squares (fp64)
 //   k_adv_final     mean and 1 / (std + 1e-8) from those sums
 //   k_fwd_bwd<n>    per 16-sample tile: forward, loss, dL/dy, dz2 = (W3^T q(dL/dy)) (1 - h2^2);
-//                   writes q(dz2) and q(h1) for the next two kernels; accumulates dW3, db2,
+//                   writes q(dz2) for the next two kernels; accumulates dW3, db2,
 //                   db3, d log_std and the loss sums per workgroup
 //   k_dz1           per tile: dh1 = W2^T q(dz2), dz1 = dh1 (1 - h1^2) with h1 recomputed from
 //                   the input; accumulates dW1 = q(dz1) q(x)^T and db1 per workgroup
-//   k_dw2           dW2 = q(dz2) q(h1)^T, split over the samples (K), one 256 x 256 partial
+//   k_dw2           dW2 = q(dz2) q(h1)^T with q(h1) recomputed from the inputs, split over the
+//                   samples (K), one 256 x 256 partial
 //                   per workgroup held in accumulator registers
 //   k_reduce        fixed-order sums of the per-workgroup partials -> packed gradient, and
 //                   per-block sums of squares
@@ -66,7 +67,6 @@ struct Work {
   double* adv_part;     // [ADV_BLOCKS][2] sums of A and A^2
   bf16x8* dz2_frag;     // [Bp/16][8 K tiles][64 lanes] q(dz2) as layer-2 B fragments
   u32x2* dz2_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz2) half fragments
-  u32x2* h1_half;       // [Bp/16][16 feature tiles][64 lanes] q(h1) half fragments
   float* part_w3t;      // [G][256 f][16 j] dW3^T
   float* part_b2;       // [G][256]
   float* part_b3;       // [G][16]
@@ -91,11 +91,11 @@ inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * H
 inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_ELEMS; }
 
 // Byte offsets of the workspace parts for a minibatch of B; returns the total.
-constexpr int WORK_PARTS = 14;
+constexpr int WORK_PARTS = 13;
 inline size_t work_layout(int B, size_t off[WORK_PARTS]) {
   const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
   const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS,
-                            Bp * HID * 2, Bp * HID * 2, Bp * HID * 2,
+                            Bp * HID * 2, Bp * HID * 2,
                             G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
                             G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
                             2 * (size_t)red_blocks(8) * 4};
@@ -116,16 +116,15 @@ inline Work work_at(void* base, int B) {
   W.adv_part = (double*)(p + off[1]);
   W.dz2_frag = (bf16x8*)(p + off[2]);
   W.dz2_half = (u32x2*)(p + off[3]);
-  W.h1_half = (u32x2*)(p + off[4]);
-  W.part_w3t = (float*)(p + off[5]);
-  W.part_b2 = (float*)(p + off[6]);
-  W.part_b3 = (float*)(p + off[7]);
-  W.part_ls = (float*)(p + off[8]);
-  W.part_stats = (float*)(p + off[9]);
-  W.part_w1 = (float*)(p + off[10]);
-  W.part_b1 = (float*)(p + off[11]);
-  W.part_w2 = (float*)(p + off[12]);
-  W.part_ss = (float*)(p + off[13]);
+  W.part_w3t = (float*)(p + off[4]);
+  W.part_b2 = (float*)(p + off[5]);
+  W.part_b3 = (float*)(p + off[6]);
+  W.part_ls = (float*)(p + off[7]);
+  W.part_stats = (float*)(p + off[8]);
+  W.part_w1 = (float*)(p + off[9]);
+  W.part_b1 = (float*)(p + off[10]);
+  W.part_w2 = (float*)(p + off[11]);
+  W.part_ss = (float*)(p + off[12]);
   return W;
 }
 
@@ -344,9 +343,6 @@ __global__ __launch_bounds__(64 * HID / FPW, 1) void k_fwd_bwd(const uint16_t* _
     tile_layer1<FPW>(R, x, S.b1k, m, lane, own);
 #pragma unroll
     for (int kt = 0; kt < KO; ++kt) S.h[KO * m + kt][lane] = own[kt];
-    put_b<KO>(T, g, r, own);                  // q(h1) -> half fragments for dW2
-#pragma unroll
-    for (int ft = 0; ft < MT; ++ft) W.h1_half[((size_t)t * 16 + MT * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
     __syncthreads();
     f32x4 acc[MT];
     tile_layer2_own<FPW>(R, own, acc);
@@ -615,17 +611,41 @@ __global__ __launch_bounds__(64 * HID / FPW, 1) void k_dz1(const uint16_t* __res
     }
 }
 
+// Where k_dw2 takes its q(h1) operand from.  With `w` null it reads stored half fragments
+// (h1_half, which the SHAC window kernel writes); otherwise it recomputes them from the
+// minibatch's inputs (obs rows of samples idx[..], clamped as in the forward kernel) and the network's
+// layer 1 (W1 at w, b1 at b), with the forward kernel's arithmetic (one MFMA over the 23
+// inputs, bias and tanh in fp32, bf16 rounding), so that the operand is the same.
+struct H1Src {
+  const u32x2* h1_half;
+  const uint16_t* w;
+  const float* b;
+  const float* obs;
+  size_t M;
+  const int32_t* idx;
+  int B;
+};
+
 // dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup.  Eight waves, two per
 // SIMD: wave w owns rows 64 (w % 4) .. + 63 (4 M-tiles, A fragments loaded directly) and
 // columns 128 (w / 4) .. + 127 (8 N-tiles), 128 accumulators.  The 16 B fragments of a step
-// are shared: wave w loads N-tiles 2w, 2w+1 into LDS (two buffers, one barrier per step) and
-// reads its eight.  A step's 32 products take far less time than a load's latency, so loads
-// run DW2_DEPTH steps ahead in a ring of register sets (the loop unrolled by DW2_DEPTH); they
-// are unconditional (the step index clamped) so that every wait covers only its own set.
-__global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restrict__ dz2_half,
-                                                           const u32x2* __restrict__ h1_half, int steps,
+// are shared: wave w provides N-tiles 2w, 2w+1 through LDS (two buffers, one barrier per step)
+// and reads its eight.  A step's 32 products take far less time than a load's latency, so
+// loads run DW2_DEPTH steps ahead in a ring of register sets (the loop unrolled by DW2_DEPTH);
+// they are unconditional (the step index clamped) so that every wait covers only its own set.
+// RECOMP: wave w computes its two N-tiles of q(h1) from the inputs: D = x W1^T (the input
+// fragment as the A operand) gives lane (g, r) feature r at samples 4g .. 4g+3, which is the
+// half-fragment layout.  The input fragments of a step (two 16-sample tiles) are shared too:
+// wave w loads K slots 2 (w % 4), 2 (w % 4) + 1 of tile w / 4 four steps ahead of the step's
+// products (sample indices eight steps ahead) and rounds them to bf16 into LDS two steps
+// ahead; q(h1) of a step is computed after the products of the step before it.
+template <bool RECOMP>
+__global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restrict__ dz2_half, H1Src H, int steps,
                                                            float* __restrict__ part_w2) {
   __shared__ bf16x8 Bs[2][16][64];
+  __shared__ bf16x8 Xs[RECOMP ? 2 : 1][2][64];
+  __shared__ bf16x8 W1s[RECOMP ? 16 : 1][64];   // layer-1 fragments of the 16 N-tiles
+  __shared__ float B1s[RECOMP ? 16 : 1][64];     // their biases x 2 log2 e
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int mr = w & 3, nc = w >> 2;
@@ -639,34 +659,125 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
     for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = f32x4{0, 0, 0, 0};
   if (u0 < u1) {
     auto at = [&](int tile, int ft) { return ((size_t)tile * 16 + ft) * 64 + lane; };
-    bf16x8 A[DW2_DEPTH][4], Bo[DW2_DEPTH][2];
-    auto load = [&](int u, int j) __attribute__((always_inline)) {
+    // A ring: DW2_DEPTH steps, two with RECOMP (whose longer steps cover the latency with
+    // fewer registers)
+    constexpr int DA = RECOMP ? 2 : DW2_DEPTH;
+    bf16x8 A[DA][4], Bo[DW2_DEPTH][2];
+    // RECOMP: this wave's share of the inputs: tile xh of a step, K slots xj, xj + 1; inputs
+    // of two steps (X, ring of 2) and sample indices of four (ix, ring of DW2_DEPTH).  Its
+    // layer-1 fragments and biases (features 16 (2w + q) + r) sit in LDS, read by itself only.
+    const int xh = w >> 2, xj = 2 * (w & 3);
+    const int xr0 = min(kslot(g, xj), 22), xr1 = min(kslot(g, xj + 1), 22);
+    const bool xk0 = kslot(g, xj) < 23, xk1 = kslot(g, xj + 1) < 23;
+    float X[2][2];
+    int ix[DW2_DEPTH];
+    const int Mi = (int)H.M;
+    auto idx_load = [&](int u, int slot) __attribute__((always_inline)) {
+      ix[slot] = raw_index(H.idx, 2 * min(u, u1 - 1) + xh, r, H.B);
+    };
+    auto x_load = [&](int slot_ix, int slot_x) __attribute__((always_inline)) {
+      const size_t ss = (size_t)clamp_sample(ix[slot_ix], Mi);
+      X[slot_x][0] = H.obs[(size_t)xr0 * H.M + ss];
+      X[slot_x][1] = H.obs[(size_t)xr1 * H.M + ss];
+    };
+    // this wave's two input values of a step, as bf16, into input buffer xb
+    auto x_put = [&](int slot_x, int xb) __attribute__((always_inline)) {
+      __bf16* dst = reinterpret_cast<__bf16*>(&Xs[xb][xh][lane]) + xj;
+      dst[0] = (__bf16)(xk0 ? X[slot_x][0] : 0.0f);
+      dst[1] = (__bf16)(xk1 ? X[slot_x][1] : 0.0f);
+    };
+    auto a_load = [&](int u, int j) __attribute__((always_inline)) {
       u = min(u, u1 - 1);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
         A[j][mt] = join(dz2_half[at(2 * u, 4 * mr + mt)], dz2_half[at(2 * u + 1, 4 * mr + mt)]);
+      if (!RECOMP) {
 #pragma unroll
-      for (int q = 0; q < 2; ++q) Bo[j][q] = join(h1_half[at(2 * u, 2 * w + q)], h1_half[at(2 * u + 1, 2 * w + q)]);
+        for (int q = 0; q < 2; ++q)
+          Bo[j][q] = join(H.h1_half[at(2 * u, 2 * w + q)], H.h1_half[at(2 * u + 1, 2 * w + q)]);
+      }
     };
+    // q(h1) of this wave's N-tiles for the step whose input fragments are in input buffer xb,
+    // into B buffer bb (one N-tile at a time, to keep few registers live)
+    auto recompute = [&](int xb, int bb) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < DW2_DEPTH; ++j) load(u0 + j, j);
+      for (int q = 0; q < 2; ++q) {
+        const bf16x8 w1 = W1s[2 * w + q][lane];
+        const float bk = B1s[2 * w + q][lane];
+        const f32x4 d0 = mfma(Xs[xb][0][lane], w1, f32x4{0, 0, 0, 0});
+        const f32x4 d1 = mfma(Xs[xb][1][lane], w1, f32x4{0, 0, 0, 0});
+        bf16x8 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          o[i] = (__bf16)tanh_bias(d0[i], bk);
+          o[4 + i] = (__bf16)tanh_bias(d1[i], bk);
+        }
+        Bs[bb][2 * w + q][lane] = o;
+      }
+    };
+    if (RECOMP) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int f = 16 * (2 * w + q) + r;
+        bf16x8 w1;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const int k = kslot(g, jj);
+          w1[jj] = k < 23 ? bf16_of_bits(H.w[f * 23 + k]) : bf16_of_bits(0);
+        }
+        W1s[2 * w + q][lane] = w1;
+        B1s[2 * w + q][lane] = H.b[f] * TWO_LOG2E;
+      }
+      // steps u0 .. u0 + 3: inputs of u0 into buffer 0, q(h1) of u0 into B buffer 0, inputs
+      // of u0 + 1 into buffer 1, those of u0 + 2 and u0 + 3 in registers; then the sample
+      // indices of u0 + 4 .. u0 + 7
+#pragma unroll
+      for (int j = 0; j < DW2_DEPTH; ++j) idx_load(u0 + j, j);
+      x_load(0, 0);
+      x_load(1, 1);
+      x_put(0, 0);
+      x_load(2, 0);
+      __syncthreads();
+      recompute(0, 0);
+      x_put(1, 1);
+      x_load(3, 1);
+#pragma unroll
+      for (int j = 0; j < DW2_DEPTH; ++j) idx_load(u0 + DW2_DEPTH + j, j);
+    }
+#pragma unroll
+    for (int j = 0; j < DA; ++j) a_load(u0 + j, j);
     // u1 - u0 is a multiple of DW2_DEPTH (padded minibatch, rounded share), so a round has no
     // branch; the first round is peeled so that both paths into the loop header have the same
     // loads in flight (the prologue's own load order would otherwise set the header's wait).
+    // RECOMP, at the top of step s = u + j: this wave's q(h1) of s is in B buffer s % 2 and its
+    // inputs of s + 1 in input buffer (s + 1) % 2 (both published by the step's barrier);
+    // registers X[s % 2] and X[(s + 1) % 2] hold its inputs of s + 2 and s + 3, ix[s % 4] the
+    // sample indices of s + 4.  After the step's products (A[j] is free until its reload):
+    // q(h1) of s + 1 from input buffer (s + 1) % 2 into B buffer (s + 1) % 2, inputs of s + 2
+    // into input buffer s % 2, then the loads of s + 4's inputs and s + 8's indices.  A buffer
+    // written in step s was last read before step s's barrier.
     auto round = [&](int u) __attribute__((always_inline)) {
 #pragma unroll
       for (int j = 0; j < DW2_DEPTH; ++j) {
         const int b = j & 1;
+        if (!RECOMP) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) Bs[b][2 * w + q][lane] = Bo[j][q];
+          for (int q = 0; q < 2; ++q) Bs[b][2 * w + q][lane] = Bo[j][q];
+        }
         __syncthreads();   // this step's B fragments visible; readers of this buffer two steps ago are done
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) {
           const bf16x8 bf = Bs[b][8 * nc + nt][lane];
 #pragma unroll
-          for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[j][mt], bf, acc[mt][nt]);
+          for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[j % DA][mt], bf, acc[mt][nt]);
         }
-        load(u + j + DW2_DEPTH, j);
+        if (RECOMP) {
+          recompute(b ^ 1, b ^ 1);
+          x_put(b, b);
+          x_load(j, b);
+          idx_load(u + j + 2 * DW2_DEPTH, j);
+        }
+        a_load(u + j + DA, j % DA);
       }
     };
     round(u0);
@@ -849,8 +960,9 @@ __global__ __launch_bounds__(256) void k_adam(int P, int nW, float* __restrict__
 }  // namespace ppo
 
 int launch_dw2(const void* dz2_half, const void* h1_half, int steps, int groups, float* part_w2, hipStream_t s) {
-  hipLaunchKernelGGL(ppo::k_dw2, dim3(groups), dim3(64 * ppo::DW2_WAVES), 0, s, (const ppo::u32x2*)dz2_half,
-                     (const ppo::u32x2*)h1_half, steps, part_w2);
+  const ppo::H1Src H{(const ppo::u32x2*)h1_half, nullptr, nullptr, nullptr, 0, nullptr, 0};
+  hipLaunchKernelGGL(ppo::k_dw2<false>, dim3(groups), dim3(64 * ppo::DW2_WAVES), 0, s, (const ppo::u32x2*)dz2_half, H,
+                     steps, part_w2);
   return check_launch("dW2");
 }
 
@@ -942,14 +1054,16 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
     hipLaunchKernelGGL((ppo::k_fwd_bwd<8, FPW>), dim3(G1), dim3(TH), 0, s, policy->w, policy->b, policy->log_std, D,
                        idx, B, tiles, hp, W, 0);
     hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
-    hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+    const ppo::H1Src H{nullptr, policy->w, policy->b, D.obs, D.M, idx, B};
+    hipLaunchKernelGGL(ppo::k_dw2<true>, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, H, steps, W.part_w2);
     hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G3, W, cfg->ent_coef,
                        grad_policy, W.part_ss, ppo::AdamFuse{});
   }
   hipLaunchKernelGGL((ppo::k_fwd_bwd<1, FPW>), dim3(G1), dim3(TH), 0, s, value->w, value->b, (const float*)nullptr, D,
                      idx, B, tiles, hp, W, 1);
   hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, value->w, value->b, D, idx, B, tiles, W);
-  hipLaunchKernelGGL(ppo::k_dw2, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, W.h1_half, steps, W.part_w2);
+  const ppo::H1Src Hv{nullptr, value->w, value->b, D.obs, D.M, idx, B};
+  hipLaunchKernelGGL(ppo::k_dw2<true>, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, Hv, steps, W.part_w2);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, G1, G1, G3, W, 0.0f,
                      grad_value, W.part_ss + rb, fuse);
   if (finalize)
