@@ -18,6 +18,17 @@ rigid-body Coriolis matrix is written independently of linear velocity):
     dp/dt = R(q) v,             dq/dt = 1/2 [-eps^T ; eta I + S(eps)] omega
 All matrices are built explicitly and the mass matrix is solved with numpy.linalg.solve.
 
+The same model has a second textbook form, selected by rhs(..., form=FORM_MIXED): the
+rigid-body terms act on the absolute velocity and only the hydrodynamic terms on the
+relative one,
+    M_RB dnu/dt + C_RB(nu) nu + M_A dnu_r/dt + C_A(nu_r) nu_r + D(nu_r) nu_r + g(q) = tau,
+with dnu_r/dt = dnu/dt - dnu_c/dt and dnu_c/dt = d(R^T c_w)/dt = -omega x R^T c_w.  For a
+constant irrotational current and this C_RB the two forms are the same equations (the
+difference M_RB dnu_c/dt + C_RB(nu) nu - C_RB(nu_r) nu_r vanishes), so they agree to
+rounding for every current and bit for bit at c_w = 0.  FORM_NO_CURRENT_RATE is the
+relative form without the dnu_c/dt term, the simplification many simulators make; it is
+kept only so that tests can show which pins reject it.
+
 Arrays are batched over environments along the LAST axis for states ([13, n]) and along
 the FIRST axis for matrices ([n, 6, 6]).
 """
@@ -125,32 +136,44 @@ class Vehicle:
         return np.concatenate([f, mom], axis=1)
 
 
-def rhs(x: np.ndarray, tau: np.ndarray, veh: Vehicle, c_w: np.ndarray) -> np.ndarray:
-    """dx/dt for states x [13, n], body wrench tau [6, n], world current c_w [3, n]."""
+FORM_RELATIVE, FORM_MIXED, FORM_NO_CURRENT_RATE = "relative", "mixed", "no_current_rate"
+
+
+def rhs(x: np.ndarray, tau: np.ndarray, veh: Vehicle, c_w: np.ndarray, form: str = FORM_RELATIVE) -> np.ndarray:
+    """dx/dt for states x [13, n], body wrench tau [6, n], world current c_w [3, n]; `form`
+    selects one of the two equivalent forms of the equations (module docstring)."""
     p, q, v, w = x[0:3], x[3:7], x[7:10], x[10:13]
     R = rotation(q)                                                    # [n, 3, 3]
     c_b = np.einsum("nji,jn->ni", R, c_w)                              # R^T c_w, [n, 3]
     nu = np.concatenate([v.T, w.T], axis=1)                            # [n, 6]
     nu_r = nu - np.concatenate([c_b, np.zeros_like(c_b)], axis=1)
-    lhs_terms = (np.einsum("nij,nj->ni", veh.C_RB(nu_r), nu_r)
-                 + np.einsum("nij,nj->ni", veh.C_A(nu_r), nu_r)
-                 + np.einsum("nij,nj->ni", veh.D(nu_r), nu_r)
-                 + veh.g(R))
-    nu_r_dot = np.linalg.solve(veh.M, (tau.T - lhs_terms)[..., None])[..., 0]   # [n, 6]
     nu_c_dot = np.concatenate([-np.cross(w.T, c_b), np.zeros_like(c_b)], axis=1)
-    nu_dot = nu_r_dot + nu_c_dot
+    ca = np.einsum("nij,nj->ni", veh.C_A(nu_r), nu_r)
+    dm = np.einsum("nij,nj->ni", veh.D(nu_r), nu_r)
+    gr = veh.g(R)
+    if form == FORM_MIXED:
+        # (M_RB + M_A) dnu/dt = tau - C_RB(nu) nu - C_A(nu_r) nu_r - D(nu_r) nu_r - g + M_A dnu_c/dt
+        lhs_terms = np.einsum("nij,nj->ni", veh.C_RB(nu), nu) + ca + dm + gr
+        f = (tau.T - lhs_terms) + np.einsum("nij,nj->ni", veh.M_A, nu_c_dot)
+        nu_dot = np.linalg.solve(veh.M, f[..., None])[..., 0]
+    elif form in (FORM_RELATIVE, FORM_NO_CURRENT_RATE):
+        lhs_terms = np.einsum("nij,nj->ni", veh.C_RB(nu_r), nu_r) + ca + dm + gr
+        nu_r_dot = np.linalg.solve(veh.M, (tau.T - lhs_terms)[..., None])[..., 0]   # [n, 6]
+        nu_dot = nu_r_dot + nu_c_dot if form == FORM_RELATIVE else nu_r_dot
+    else:
+        raise ValueError(f"unknown form {form!r}")
     p_dot = np.einsum("nij,jn->in", R, v)
     q_dot = np.einsum("nij,jn->in", quat_rate_matrix(q), w)
     return np.concatenate([p_dot, q_dot, nu_dot.T], axis=0)
 
 
-def rk4_substep(x, tau, veh, c_w, h):
+def rk4_substep(x, tau, veh, c_w, h, form=FORM_RELATIVE):
     """Classic four-stage Runge-Kutta step of size h with the wrench held constant,
     followed by renormalisation of the quaternion (stage quaternions are not normalised)."""
-    k1 = rhs(x, tau, veh, c_w)
-    k2 = rhs(x + 0.5 * h * k1, tau, veh, c_w)
-    k3 = rhs(x + 0.5 * h * k2, tau, veh, c_w)
-    k4 = rhs(x + h * k3, tau, veh, c_w)
+    k1 = rhs(x, tau, veh, c_w, form)
+    k2 = rhs(x + 0.5 * h * k1, tau, veh, c_w, form)
+    k3 = rhs(x + 0.5 * h * k2, tau, veh, c_w, form)
+    k4 = rhs(x + h * k3, tau, veh, c_w, form)
     xn = x + (h / 6.0) * (k1 + 2.0 * k2 + 2.0 * k3 + k4)
     xn[3:7] /= np.linalg.norm(xn[3:7], axis=0, keepdims=True)
     return xn

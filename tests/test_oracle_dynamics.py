@@ -304,3 +304,119 @@ def test_allocation_table_matches_geometry():
     assert np.linalg.matrix_rank(Tm) == 6
     wrench_max = 40.0 * np.abs(Tm).sum(axis=1)
     assert np.allclose(wrench_max, [113.137, 113.137, 160.0, 34.88, 19.2, 30.207], atol=2e-3)
+
+
+def _rand_states(n, seed):
+    r = np.random.Generator(np.random.PCG64(seed))
+    q = r.standard_normal((4, n))
+    q /= np.linalg.norm(q, axis=0)
+    return _state(n=n, p=r.uniform(-2, 2, (3, n)), q=q, v=r.uniform(-1.5, 1.5, (3, n)),
+                  w=r.uniform(-1.5, 1.5, (3, n))), r
+
+
+def test_current_forms_coincide():
+    """The relative-velocity form and the mixed form (rigid-body terms on the absolute
+    velocity, hydrodynamic terms on the relative one, added-mass inertia on dnu_r/dt) are
+    the same equations for a constant irrotational current: bit-identical at c_w = 0,
+    equal to rounding for any current, with domain-randomised constants and the default
+    W != B and buoyancy offset."""
+    n = 64
+    x, r = _rand_states(n, 11)
+    veh = dyn.Vehicle(W.VEHICLE, n, s_m=r.uniform(0.8, 1.2, n), s_a=r.uniform(0.8, 1.2, n), s_d=r.uniform(0.8, 1.2, n))
+    tau = r.uniform(-50, 50, (6, n))
+    zero = np.zeros((3, n))
+    a = dyn.rhs(x, tau, veh, zero, dyn.FORM_RELATIVE)
+    b = dyn.rhs(x, tau, veh, zero, dyn.FORM_MIXED)
+    assert np.array_equal(a, b)
+    c_w = r.uniform(-0.3, 0.3, (3, n))
+    a = dyn.rhs(x, tau, veh, c_w, dyn.FORM_RELATIVE)
+    b = dyn.rhs(x, tau, veh, c_w, dyn.FORM_MIXED)
+    assert np.allclose(a, b, rtol=1e-12, atol=1e-12)
+    # and the forms are not trivially equal: without dnu_c/dt the result moves
+    c = dyn.rhs(x, tau, veh, c_w, dyn.FORM_NO_CURRENT_RATE)
+    assert np.abs(c[7:10] - a[7:10]).max() > 1e-2
+    xa, xb = x.copy(), x.copy()
+    for _ in range(200):
+        xa = dyn.rk4_substep(xa, tau * 0, veh, c_w, 0.02, dyn.FORM_RELATIVE)
+        xb = dyn.rk4_substep(xb, tau * 0, veh, c_w, 0.02, dyn.FORM_MIXED)
+    assert np.allclose(xa, xb, rtol=1e-10, atol=1e-10)
+
+
+def test_current_rate_term_by_finite_difference():
+    """dnu/dt(x, c_w) - dnu/dt(x with v -> v - R^T c_w, no current) is the rate of the body-
+    frame current, d/dt R(q(t))^T c_w along dq/dt = 1/2 q (x) (0, omega): for a constant body
+    rate the attitude is q(t) = q0 (x) (cos(|w| t / 2), sin(|w| t / 2) w / |w|), rotated here
+    with scipy and differenced centrally."""
+    n = 16
+    x, r = _rand_states(n, 12)
+    veh = dyn.Vehicle(W.VEHICLE, n)
+    c_w = r.uniform(-0.3, 0.3, (3, n))
+    tau = r.uniform(-50, 50, (6, n))
+    R0 = Rotation.from_quat(np.stack([x[4], x[5], x[6], x[3]], axis=1))
+    c_b = R0.inv().apply(c_w.T).T
+    xr = x.copy()
+    xr[7:10] -= c_b
+    diff = dyn.rhs(x, tau, veh, c_w)[7:13] - dyn.rhs(xr, tau, veh, np.zeros((3, n)))[7:13]
+    dt = 1e-4
+    w = x[10:13].T
+    fd = []
+    for s in (dt, -dt):
+        Rt = R0 * Rotation.from_rotvec(w * s)          # body-frame rate: q0 (x) exp(w t / 2)
+        fd.append(Rt.inv().apply(c_w.T).T)
+    rate = (fd[0] - fd[1]) / (2 * dt)
+    assert np.allclose(diff[0:3], rate, atol=1e-7)
+    assert np.allclose(diff[3:6], 0.0, atol=1e-12)
+    assert np.abs(rate).max() > 0.05                   # the term is exercised
+
+
+def test_current_coupling_spinning_drift_closed_form():
+    """W = B, r_b = 0, no thrust, a current, body velocity equal to the current in body axes
+    (no relative flow) and a spin.  With the isotropic inertia and rotational added mass no
+    Coriolis or Munk term arises, so the relative flow stays zero while the vehicle turns:
+    the vehicle drifts with the current, p(t) = p0 + c_w t, and each body rate decays by its
+    1-DOF linear + quadratic damping closed form
+        w(t) = d_l w0 e^{-kt} / (d_l + d_q |w0| (1 - e^{-kt})),  k = d_l / (I + A),
+    with the yaw angle of a spin about the body z axis
+        psi(t) = (I + A) / d_q ln(1 + d_q w0 (1 - e^{-kt}) / d_l).
+    The drift needs the body-frame current's rate: dropping it lets p leave the line by
+    O(|c_w| psi)."""
+    vd = W.vehicle_variant(W=114.8, B=114.8, r_b=[0.0, 0.0, 0.0])
+    f = lambda v: float(np.float32(v))  # noqa: E731
+    Mrot = f(vd["inertia"][2]) + f(vd["added_mass"][5])
+    dl, dq = f(vd["lin_damp"][5]), f(vd["quad_damp"][5])
+    assert f(vd["inertia"][0]) == f(vd["inertia"][2]) and f(vd["added_mass"][3]) == f(vd["added_mass"][5])
+    r = np.random.Generator(np.random.PCG64(13))
+    n = 8
+    q0 = r.standard_normal((4, n))
+    q0 /= np.linalg.norm(q0, axis=0)
+    c_w = r.uniform(-0.3, 0.3, (3, n))
+    R0 = Rotation.from_quat(np.stack([q0[1], q0[2], q0[3], q0[0]], axis=1))
+    v0 = R0.inv().apply(c_w.T).T
+    w0 = np.zeros((3, n))
+    w0[2, :4] = r.uniform(0.5, 1.5, 4) * np.array([1, -1, 1, -1])          # spin about body z
+    w0[:, 4:] = r.uniform(-1.2, 1.2, (3, 4))                                # any direction
+    p0 = r.uniform(-2, 2, (3, n))
+    x0 = _state(n=n, p=p0, q=q0, v=v0, w=w0)
+    h, steps = 0.01, 300
+    t = h * steps
+    veh = dyn.Vehicle(vd, n)
+    traj = _run(x0, veh, steps, h, c_w=c_w)
+    xe = traj[-1]
+    k = dl / Mrot
+    e = math.exp(-k * t)
+    w_want = dl * w0 * e / (dl + dq * np.abs(w0) * (1 - e))
+    assert np.allclose(xe[10:13], w_want, rtol=1e-7, atol=1e-9)
+    assert np.allclose(xe[0:3], p0 + c_w * t, atol=1e-7)
+    assert np.allclose(xe[7:10], Rotation.from_quat(np.stack([xe[4], xe[5], xe[6], xe[3]], axis=1)).inv()
+                       .apply(c_w.T).T, atol=1e-8)
+    psi = Mrot / dq * np.log(1 + dq * np.abs(w0[2, :4]) * (1 - e) / dl) * np.sign(w0[2, :4])
+    q_want = (R0[:4] * Rotation.from_rotvec(np.stack([0 * psi, 0 * psi, psi], axis=1))).as_quat()
+    q_want = np.stack([q_want[:, 3], q_want[:, 0], q_want[:, 1], q_want[:, 2]])
+    s = np.sign(np.sum(q_want * xe[3:7, :4], axis=0))
+    assert np.allclose(xe[3:7, :4], q_want * s, atol=1e-8)
+    # without the body-frame current's rate (or with its sign flipped) the drift fails
+    for bad in (dyn.FORM_NO_CURRENT_RATE,):
+        xb = x0
+        for _ in range(steps):
+            xb = dyn.rk4_substep(xb, np.zeros((6, n)), veh, c_w, h, bad)
+        assert np.abs(xb[0:3] - (p0 + c_w * t)).max() > 1e-2
