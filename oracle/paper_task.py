@@ -99,6 +99,16 @@ class Task:
         self.mu = f(t.get("viscosity", fl.MU_WATER))
 
 
+def paper_reward(k: Task, dp, dth, om, u, abar):
+    """The five reward terms of Sec. IV-B (Eqs. 2-7) summed, per env: position error weighted by
+    D, attitude error (rotation vector), torque commands u_3:6, body rates and the deviation of
+    the clipped action u from its moving average abar (taken before this step's update):
+        r = -w_pos |D dp|^2 - w_att |dth|^2 - w_act |u_3:6|^2 - w_vel |om|^2 - w_mavg |u - abar|^2."""
+    return (-k.w_pos * np.sum((k.d_pos[:, None] * dp) ** 2, axis=0) - k.w_att * np.sum(dth * dth, axis=0)
+            - k.w_act * np.sum(u[3:6] ** 2, axis=0) - k.w_vel * np.sum(om * om, axis=0)
+            - k.w_mavg * np.sum((u - abar) ** 2, axis=0))
+
+
 class PaperEnv:
     def __init__(self, cfg: dict, vehicle: dict, task: dict):
         self.tk = Task(task)
@@ -171,13 +181,10 @@ class PaperEnv:
         self.x = dyn.integrate(self.x, tau, self.veh, self.c_w, self.dt, self.S)
         self.ep_step += 1
         obs = self.observe()
-        dp, dth, om = obs[0:3], obs[3:6], obs[9:12]
-        reward = (-k.w_pos * np.sum((k.d_pos[:, None] * dp) ** 2, axis=0) - k.w_att * np.sum(dth * dth, axis=0)
-                  - k.w_act * np.sum(u[3:6] ** 2, axis=0) - k.w_vel * np.sum(om * om, axis=0)
-                  - k.w_mavg * np.sum((u - self.abar) ** 2, axis=0))
+        reward = paper_reward(k, obs[0:3], obs[3:6], obs[9:12], u, self.abar)
         self.abar = k.beta * self.abar + (1.0 - k.beta) * u
         done = self.ep_step == self.H
-        stats = np.array([reward.sum(), float(done.sum()), np.linalg.norm(dp, axis=0).sum()])
+        stats = np.array([reward.sum(), float(done.sum()), np.linalg.norm(obs[0:3], axis=0).sum()])
         idx = np.nonzero(done)[0]
         if idx.size:
             self.episode[idx] += 1

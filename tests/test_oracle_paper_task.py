@@ -129,3 +129,36 @@ def test_random_and_sampled_action_maps():
     e8 = rng.gaussian8(e.seed, e.ids, 0)
     for c in range(3):
         assert np.array_equal(eps[c], e8[2 * c]) and np.array_equal(eps[3 + c], e8[2 * c + 1])
+
+
+def test_reward_hand_valued_case():
+    """The five reward terms on numbers worked out by hand (weights chosen as exact binary
+    fractions): w_pos 1, D = diag(1, 1, 1.5), w_att 0.5, w_act 0.25, w_vel 0.125, w_mavg 0.5.
+    dp = (1, -2, 2):     |D dp|^2 = 1 + 4 + 9 = 14                  -> 14
+    dth = (0.5, 0, 0):   0.5 * 0.25                                 -> 0.125
+    u = (0.5, 0, 0, 1, 0, -0.5): torques 1 + 0.25, times 0.25       -> 0.3125
+    om = (0, 1, -1):     0.125 * 2                                  -> 0.25
+    abar = (0.25, 0, 0, 0.5, 0, 0): |u - abar|^2 = 0.0625 + 0.25 + 0.25, times 0.5 -> 0.28125
+    reward = -(14 + 0.125 + 0.3125 + 0.25 + 0.28125) = -14.96875; with beta = 0.75 the moving
+    average becomes 0.75 abar + 0.25 u = (0.3125, 0, 0, 0.625, 0, -0.125)."""
+    task = dict(W.PAPER_TASK, w_pos=1.0, d_pos=(1.0, 1.0, 1.5), w_att=0.5, w_act=0.25, w_vel=0.125, w_mavg=0.5,
+                beta=0.75)
+    k = P.Task(task)
+    col = lambda *v: np.array(v, np.float64)[:, None]  # noqa: E731
+    dp, dth, om = col(1, -2, 2), col(0.5, 0, 0), col(0, 1, -1)
+    u, abar = col(0.5, 0, 0, 1, 0, -0.5), col(0.25, 0, 0, 0.5, 0, 0)
+    z3, z6 = col(0, 0, 0), col(0, 0, 0, 0, 0, 0)
+    assert P.paper_reward(k, dp, dth, om, u, abar)[0] == -14.96875
+    # each term alone
+    assert P.paper_reward(k, dp, z3, z3, z6, z6)[0] == -14.0
+    assert P.paper_reward(k, z3, dth, z3, z6, z6)[0] == -0.125
+    assert P.paper_reward(k, z3, z3, om, z6, z6)[0] == -0.25
+    assert P.paper_reward(k, z3, z3, z3, u, u)[0] == -0.3125        # no deviation from the average
+    assert P.paper_reward(k, z3, z3, z3, z6, abar - u)[0] == -0.28125 - 0.0   # only the average term
+    # the same numbers through one environment step: the step's reward is built from the
+    # post-step observation, the clipped action and the average before the update
+    e = _env(1)
+    e.tk = k
+    e.abar = abar.copy()
+    e.step(u)
+    assert np.array_equal(e.abar, col(0.3125, 0, 0, 0.625, 0, -0.125))
