@@ -238,7 +238,7 @@ int auv_set_task(auv_env* env, const auv_task* task);
 
 /* ---- PPO update of the policy and value MLPs on one minibatch ------------------------
  * The clipped-surrogate objective of PPO (Schulman et al. 2017; the on-policy learner of
- * paper Sec. II-B and III-A, which gives no hyperparameters), over minibatch samples b:
+ * paper Sec. III-A1, which gives no hyperparameters), over minibatch samples b:
  *   logp_b = sum_j [-((a_jb - mu_jb) / sigma_j)^2 / 2 - log sigma_j - log(2 pi) / 2],
  *            sigma = exp(log_std), mu = policy(o_b)
  *   rho_b  = exp(logp_b - logp_old_b)
@@ -320,7 +320,7 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
                  const auv_ppo_net* value, const float* grad_policy, const float* grad_value,
                  const float* stats, void* stream);
 
-/* A value net's regression over a batch in one call (SHAC's critic update, paper Sec. II-B;
+/* A value net's regression over a batch in one call (SHAC's critic update, paper Sec. III-A3;
  * the value loss of auv_ppo_grad): `iterations` passes, each shuffling the M / 16 blocks of
  * 16 consecutive samples (Fisher-Yates, Knuth TAOCP Vol. 2 Algorithm P, driven by a
  * SplitMix64 stream started at `seed`) and taking `batches` minibatches of B = 16 floor(M / 16
@@ -346,7 +346,7 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
 
 /* ---- SHAC: the actor gradient of one short window on the paper task -------------------
  * Short-Horizon Actor-Critic (Xu et al. 2022; the differentiable-simulation learner of
- * paper Sec. II-B, trained on the paper task of auv_set_task).  One window of h control
+ * paper Sec. III-A3, trained on the paper task of auv_set_task).  One window of h control
  * steps of all N environments from their current state, with the policy in the loop:
  *   a_t = mu(o_t) (+ exp(log_std) eps_t in sample mode, the noise stream of auv_rollout),
  *   u_t = clip(a_t, -1, 1), s_{t+1} = the paper task's RK4 step, r_t its reward,

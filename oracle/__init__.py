@@ -17,7 +17,7 @@ Modules
   env       reset / domain randomisation, references, observation, reward, auto-reset,
             batch statistics, rollouts (paper Sec. IV-A, IV-B, IV-C, V-A)
   mlp       bf16 round-to-nearest-even, policy / value MLP forward, Gaussian log-prob
-  gae       generalised advantage estimation (the PPO learner of Sec. III-A)
+  gae       generalised advantage estimation (the PPO learner of Sec. III-A1)
   paper_task the paper's own training task: 12-D axis-angle observation, 6-D wrench action,
             five-term reward with an action moving average, gravity randomisation
   ppo       clipped-surrogate PPO objective, its gradient through both MLPs (with the

@@ -1,6 +1,6 @@
 """Generalised advantage estimation (oracle side).
 
-The PPO learner the paper uses (Sec. III-A) consumes advantages of the fresh on-policy
+The PPO learner the paper uses (Sec. III-A1) consumes advantages of the fresh on-policy
 trajectories; GAE (Schulman et al., 2016) computes them by a backward recursion over
 the rollout:
     delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t,   V_T = V(o_T) (bootstrap value)

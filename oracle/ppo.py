@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-The paper trains its PPO agent (Sec. II-B, the on-policy family; Sec. III-A) with the
+The paper trains its PPO agent (Sec. III-A1, the on-policy learner) with the
 clipped surrogate objective of Schulman et al. (2017), which it cites, and gives no
 hyperparameters.  This module writes out that objective, its gradient through the two
 MLPs, global-norm gradient clipping and Adam (Kingma and Ba, Algorithm 1), in float64.

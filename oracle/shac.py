@@ -3,7 +3,7 @@ side, float64).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-Paper passages: the differentiable-simulation learner SHAC (Sec. II-B, Xu et al.'s
+Paper passages: the differentiable-simulation learner SHAC (Sec. III-A3, Xu et al.'s
 Short-Horizon Actor-Critic, which the paper cites) backpropagates through the dynamics
 over short sub-trajectories and closes each of them with the critic's estimate of the
 remaining return; the paper trains it on its own task (Sec. IV-B, IV-C, V-A), whose

@@ -1,6 +1,6 @@
 // PPO update of the policy and value MLPs on one minibatch: the clipped-surrogate
-// objective of PPO (Schulman et al. 2017, the on-policy learner of paper Sec. II-B and
-// III-A), its gradient through both 23-256-256-n_out networks on bf16 MFMA, global-norm
+// objective of PPO (Schulman et al. 2017, the on-policy learner of paper
+// Sec. III-A1), its gradient through both 23-256-256-n_out networks on bf16 MFMA, global-norm
 // gradient clipping and Adam (Kingma and Ba, Algorithm 1).
 //
 // Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 32):

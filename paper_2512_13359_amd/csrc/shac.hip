@@ -1,5 +1,5 @@
 // SHAC (short-horizon actor-critic; the differentiable-simulation learner of paper Sec.
-// II-B) on the paper's own task: the actor objective of one window of h control steps,
+// III-A3) on the paper's own task: the actor objective of one window of h control steps,
 //   L = -(1 / (N h)) sum_i [ sum_{t<h} gamma^t r_t^i + gamma^h V(o(s_h^i)) ],
 // and its gradient with respect to the policy parameters, by reverse-mode differentiation
 // through the reward, the observation, RK4 + Fossen and the policy network.

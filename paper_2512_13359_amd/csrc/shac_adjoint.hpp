@@ -3,7 +3,7 @@
 // right-hand side, of one RK4 substep with quaternion renormalisation, of the observation
 // (body-frame position error, rotation vector of the attitude error, velocities) and the
 // gradient of the five-term reward.  These carry the SHAC state adjoint back through a
-// window (the differentiable-simulation learner, paper Sec. II-B).
+// window (the differentiable-simulation learner, paper Sec. III-A3).
 //
 // Model (paper task): no current, centre of buoyancy at the centre of gravity, weight
 // gamma W per environment, diagonal mass matrix (body origin at the CoG):
