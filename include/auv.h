@@ -46,7 +46,8 @@ enum {
   AUV_EINVAL = -1,   /* bad argument: nothing was enqueued */
   AUV_ENODEV = -2,   /* no usable HIP device */
   AUV_ELAUNCH = -3,  /* kernel launch failed */
-  AUV_ERUNTIME = -4  /* other HIP runtime error */
+  AUV_ERUNTIME = -4, /* other HIP runtime error */
+  AUV_ENONFINITE = -5 /* auv_get_status: non-finite state (or an abandoned wait) was seen */
 };
 
 /* Action sources. */
@@ -106,6 +107,9 @@ typedef struct {
   int32_t* ep_step;   /* [N] control steps taken in the current episode */
   uint32_t* episode;  /* [N] episode index (Philox counter word 1 of the reset draws) */
   float* obs;         /* [23][N] current observation; rows 15..22 = previous clipped action */
+  uint32_t* status;   /* [2] or NULL: failure counters read (and cleared) by auv_get_status;
+                         zero them before the first launch.  [0] non-finite state components
+                         seen, [1] abandoned inter-wave waits of policy rollouts */
 } auv_env_buffers;
 
 /* MLP n_in=23 -> 256 -> 256 -> n_out, tanh hidden layers, linear output.  Every layer's
@@ -146,12 +150,16 @@ int auv_destroy(auv_env* env);
  * global_step back to 0. */
 int auv_reset(auv_env* env, void* stream);
 
-/* One control step of every environment with AUV_ACT_EXTERNAL (actions [8][N] device)
- * or AUV_ACT_RANDOM (actions ignored).  reward [N] fp32, done [N] uint8 and
+/* One control step of every environment.  Modes: AUV_ACT_EXTERNAL (actions [8][N] device),
+ * AUV_ACT_RANDOM (actions ignored), AUV_ACT_POLICY_MEAN / AUV_ACT_POLICY_SAMPLE (policy
+ * required, actions ignored; the step is the first step of auv_rollout with T = 1, bit for
+ * bit, and k such steps equal one rollout of k steps).  reward [N] fp32, done [N] uint8 and
  * stats [3] (sums over envs) are optional outputs; stats needs stats_work
- * (auv_stats_work_floats(N, 1) floats).  global_step += 1. */
-int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_t* done,
-             float* stats, float* stats_work, void* stream);
+ * (auv_stats_work_floats(N, 1) floats).  global_step += 1.  AUV_EINVAL, nothing enqueued:
+ * unknown mode, a policy in a non-policy mode or none in a policy mode, external mode
+ * without actions, misaligned buffers, stats without stats_work. */
+int auv_step(auv_env* env, int mode, const float* actions, const auv_mlp* policy, float* reward,
+             uint8_t* done, float* stats, float* stats_work, void* stream);
 
 /* T control steps of every environment in one launch.  Modes: AUV_ACT_RANDOM (actions
  * from Philox), AUV_ACT_EXTERNAL (actions from rbufs->act, read as [8][T][N]),
@@ -174,6 +182,18 @@ int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value,
  * grouping, so the two agree to fp32 rounding). */
 int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float* out,
                     void* stream);
+
+/* Failure detection (synchronises the stream).  Every environment kernel (step, rollout,
+ * SHAC window) counts the non-finite components of each environment's 13 state values
+ * where an episode ends (before the reset replaces them) and where the launch ends, and
+ * adds the count to status[0] of the handle's buffers; a policy rollout whose inter-wave
+ * wait gave up (see auv_rollout) adds 1 per affected tile to status[1].  This call waits for
+ * the work enqueued on `stream`, copies both counters to the host, clears them and returns
+ * AUV_ENONFINITE if either was nonzero, else AUV_OK.  nonfinite_count and abandoned_waits
+ * (host, either may be NULL) receive the counts since the previous call.  AUV_EINVAL: the
+ * handle has no status buffer.  AUV_ERUNTIME: the copy or the synchronisation failed.
+ * Environments are not reset on a non-finite state (their episode ends stay on schedule). */
+int auv_get_status(auv_env* env, uint32_t* nonfinite_count, uint32_t* abandoned_waits, void* stream);
 
 /* Host-side step counter (Philox counter word 1 of action and noise draws); set it to
  * resume a saved run bit-exactly together with the state buffers. */

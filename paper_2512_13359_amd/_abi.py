@@ -15,7 +15,7 @@ import torch  # noqa: F401  (brings up the HIP runtime before libauv registers i
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libauv.so")
 
-AUV_OK, AUV_EINVAL, AUV_ENODEV, AUV_ELAUNCH, AUV_ERUNTIME = 0, -1, -2, -3, -4
+AUV_OK, AUV_EINVAL, AUV_ENODEV, AUV_ELAUNCH, AUV_ERUNTIME, AUV_ENONFINITE = 0, -1, -2, -3, -4, -5
 AUV_ACT_EXTERNAL, AUV_ACT_RANDOM, AUV_ACT_POLICY_MEAN, AUV_ACT_POLICY_SAMPLE = 0, 1, 2, 3
 AUV_F_DR, AUV_F_CURRENT, AUV_F_LISSAJOUS, AUV_F_STAGGER = 1, 2, 4, 8
 AUV_TASK_WORKLOAD, AUV_TASK_PAPER = 0, 1
@@ -39,7 +39,7 @@ class AuvVehicle(ctypes.Structure):
 
 
 class AuvEnvBuffers(ctypes.Structure):
-    _fields_ = [("state", _vp), ("params", _vp), ("ep_step", _vp), ("episode", _vp), ("obs", _vp)]
+    _fields_ = [("state", _vp), ("params", _vp), ("ep_step", _vp), ("episode", _vp), ("obs", _vp), ("status", _vp)]
 
 
 class AuvMlp(ctypes.Structure):
@@ -107,7 +107,8 @@ def _load() -> ctypes.CDLL:
         "auv_create": (ctypes.c_int, [P(AuvConfig), P(AuvVehicle), P(AuvEnvBuffers), P(_vp)]),
         "auv_destroy": (ctypes.c_int, [_vp]),
         "auv_reset": (ctypes.c_int, [_vp, _vp]),
-        "auv_step": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "auv_step": (ctypes.c_int, [_vp, ctypes.c_int, _vp, P(AuvMlp), _vp, _vp, _vp, _vp, _vp]),
+        "auv_get_status": (ctypes.c_int, [_vp, P(ctypes.c_uint32), P(ctypes.c_uint32), _vp]),
         "auv_rollout": (ctypes.c_int, [_vp, i32, ctypes.c_int, P(AuvMlp), P(AuvMlp), P(AuvRolloutBuffers), _vp]),
         "auv_gae": (ctypes.c_int, [i32, i32, _vp, _vp, _vp, _vp, _f, _f, _vp, _vp, _vp]),
         "auv_mlp_forward": (ctypes.c_int, [P(AuvMlp), i32, _vp, _vp, _vp]),
@@ -172,10 +173,21 @@ def auv_reset(h: int, stream=None) -> None:
     _check(lib.auv_reset(h, stream_ptr(stream)))
 
 
-def auv_step(h: int, mode: int, actions=None, reward=None, done=None, stats=None,
+def auv_step(h: int, mode: int, actions=None, policy: AuvMlp | None = None, reward=None, done=None, stats=None,
              stats_work=None, stream=None) -> None:
-    _check(lib.auv_step(h, mode, ptr(actions), ptr(reward), ptr(done), ptr(stats), ptr(stats_work),
+    _check(lib.auv_step(h, mode, ptr(actions), None if policy is None else ctypes.byref(policy), ptr(reward),
+                        ptr(done), ptr(stats), ptr(stats_work),
                         stream_ptr(stream)))
+
+
+def auv_get_status(h: int, stream=None) -> tuple[int, int, int]:
+    """(return code, non-finite state components, abandoned waits); AUV_ENONFINITE is a
+    result here, not an exception (other failures raise)."""
+    nf, ab = ctypes.c_uint32(0), ctypes.c_uint32(0)
+    rc = lib.auv_get_status(h, ctypes.byref(nf), ctypes.byref(ab), stream_ptr(stream))
+    if rc not in (AUV_OK, AUV_ENONFINITE):
+        _check(rc)
+    return rc, nf.value, ab.value
 
 
 def auv_rollout(h: int, T: int, mode: int, policy: AuvMlp | None = None, value: AuvMlp | None = None,
@@ -279,8 +291,8 @@ def make_mlp(w, b, log_std, n_out: int) -> AuvMlp:
     return AuvMlp(ptr(w), ptr(b), ptr(log_std), n_out)
 
 
-def make_env_buffers(state, params, ep_step, episode, obs) -> AuvEnvBuffers:
-    return AuvEnvBuffers(ptr(state), ptr(params), ptr(ep_step), ptr(episode), ptr(obs))
+def make_env_buffers(state, params, ep_step, episode, obs, status=None) -> AuvEnvBuffers:
+    return AuvEnvBuffers(ptr(state), ptr(params), ptr(ep_step), ptr(episode), ptr(obs), ptr(status))
 
 
 def make_task(task: dict) -> AuvTask:

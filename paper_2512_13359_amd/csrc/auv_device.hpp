@@ -42,6 +42,7 @@ struct EnvArgs {
   uint32_t sync_polls;   // bound on the polls of one inter-wave wait (fused policy rollout)
   uint32_t task;         // TASK_WORKLOAD or TASK_PAPER
   TaskArgs tk;
+  uint32_t* status;      // [2] or null: non-finite state components seen, abandoned waits
 };
 
 // Per-step output pointers of the environment loops; any may be null.
@@ -447,6 +448,26 @@ __device__ __forceinline__ void store_params(float* __restrict__ s, int n, int i
   for (int k = 0; k < 4; ++k) s[(9 + k) * n + i] = P.qg[k];
   s[22 * n + i] = P.yaw_rate;
   s[23 * n + i] = P.yaw0;
+}
+
+// ------------------------------------------------------------ failure detection ----
+// Non-finite state components of one environment, counted where an episode ends (before
+// its reset overwrites the state) and where a launch ends, and added to status[0].  Lanes
+// with nothing to report issue no atomic, so the count costs nothing while all is finite.
+__device__ __forceinline__ uint32_t nonfinite(float x) { return __builtin_isfinite(x) ? 0u : 1u; }
+
+__device__ __forceinline__ uint32_t nonfinite_state(const State& x) {
+  uint32_t n = 0;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) n += nonfinite(x.p[k]) + nonfinite(x.v[k]) + nonfinite(x.w[k]);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) n += nonfinite(x.q[k]);
+  return n;
+}
+
+__device__ __forceinline__ void report_status(uint32_t* status, uint32_t nonfinite_count, uint32_t abandoned) {
+  if (status && nonfinite_count) atomicAdd(&status[0], nonfinite_count);
+  if (status && abandoned) atomicAdd(&status[1], abandoned);
 }
 
 // Sum over the 64 lanes of a wave in a fixed butterfly order (every lane gets the sum).

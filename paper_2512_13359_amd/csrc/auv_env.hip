@@ -87,6 +87,7 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
   const uint32_t gid = E.env_offset + (uint32_t)i;
   Lane L;
   StatsBuf SB{};
+  uint32_t nf = 0;   // non-finite state components at episode ends
   lane_load(V, E, i, valid, L);
   if (O.traj && valid) store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, L.x);
 
@@ -114,10 +115,13 @@ __global__ __launch_bounds__(64) void k_env_loop(VehArgs V, EnvArgs E, int T, ui
     }
     float reward, dist;
     bool done;
-    lane_step(V, E, gid, a, L, reward, done, dist);
+    lane_step(V, E, gid, a, L, reward, done, dist, nf);
     lane_outputs(O, SB, T, N, t, i, valid, lane, blockIdx.x, gridDim.x, reward, done, dist, L.x);
   }
-  if (valid) lane_store(E, i, L);
+  if (valid) {
+    lane_store(E, i, L);
+    report_status(E.status, nf + nonfinite_state(L.x), 0u);
+  }
 }
 
 // The same T control steps in the quad layout of quad_env.hpp (lanes 4e .. 4e + 3 hold
@@ -151,6 +155,7 @@ __global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, ui
   quad::load_env<PAPER>(V, E, K, i, valid, X, M, F);
   if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)i, c, X);
   StatsBuf SB{};
+  uint32_t nf = 0;   // non-finite state components (this lane's share) at episode ends
   for (int t = 0; t < T; ++t) {
     const size_t ti = (size_t)t * N + (size_t)i;
     if (O.obs && valid) quad::store_obs<PAPER>(O.obs, TN, ti, c, X, false);
@@ -196,6 +201,7 @@ __global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, ui
     const bool done = (X.ep == E.H);
     if (done) {   // the whole quad
       float dist0;
+      nf += quad::nonfinite_quad(c, X);
       quad::new_episode<PAPER>(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist0);
     }
     if (O.stats_work) {   // reward, done and dist are the same in the four lanes of a quad
@@ -211,7 +217,10 @@ __global__ __launch_bounds__(64) void k_env_quad(VehArgs V, EnvArgs E, int T, ui
     }
     if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)(t + 1) * N + i, c, X);
   }
-  if (valid) quad::store_env<PAPER>(E, c, i, X);
+  if (valid) {
+    quad::store_env<PAPER>(E, c, i, X);
+    report_status(E.status, nf + quad::nonfinite_quad(c, X), 0u);
+  }
 }
 
 // stats[s][t] = sum over groups g of work[s][g][t].  A block covers 64 consecutive (s, t)
@@ -398,6 +407,8 @@ static int validate_env_ptrs(const auv_env_buffers* b) {
     if (!ptrs[k]) return set_error(AUV_EINVAL, "auv_create: buffer '%s' is NULL", names[k]);
     if (!aligned16(ptrs[k])) return set_error(AUV_EINVAL, "auv_create: buffer '%s' is not 16-byte aligned", names[k]);
   }
+  if (b->status && (reinterpret_cast<uintptr_t>(b->status) & 3u))
+    return set_error(AUV_EINVAL, "auv_create: buffer 'status' is not 4-byte aligned");
   return AUV_OK;
 }
 
@@ -471,6 +482,7 @@ int auv_create(const auv_config* cfg, const auv_vehicle* veh, const auv_env_buff
   E.sync_polls = AUV_DEFAULT_SYNC_POLLS;
   E.task = TASK_WORKLOAD;
   E.tk = TaskArgs{};
+  E.status = bufs->status;
   e->global_step = 0;
   *out = e;
   return AUV_OK;
@@ -595,25 +607,58 @@ static int launch_env_loop(auv_env* env, int T, int mode, const StepOut& O, hipS
   return check_launch("environment loop");
 }
 
-int auv_step(auv_env* env, int mode, const float* actions, float* reward, uint8_t* done,
+int auv_step(auv_env* env, int mode, const float* actions, const auv_mlp* policy, float* reward, uint8_t* done,
              float* stats, float* stats_work, void* stream) {
   if (!env) return set_error(AUV_EINVAL, "auv_step: NULL handle");
-  if (mode != AUV_ACT_EXTERNAL && mode != AUV_ACT_RANDOM)
-    return set_error(AUV_EINVAL, "auv_step: mode %d not supported (external or random; use auv_rollout for policy modes)", mode);
+  const bool pol_mode = (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE);
+  if (mode != AUV_ACT_EXTERNAL && mode != AUV_ACT_RANDOM && !pol_mode)
+    return set_error(AUV_EINVAL, "auv_step: unknown mode %d", mode);
+  if (pol_mode != (policy != nullptr))
+    return set_error(AUV_EINVAL, "auv_step: a policy is required in the policy modes and only there");
   if (mode == AUV_ACT_EXTERNAL && (!actions || !aligned16(actions)))
     return set_error(AUV_EINVAL, "auv_step: external mode needs a 16-byte aligned actions buffer");
   if ((stats == nullptr) != (stats_work == nullptr))
     return set_error(AUV_EINVAL, "auv_step: stats and stats_work must be given together");
-  StepOut O{};
-  O.act = const_cast<float*>(actions);
-  O.reward = reward;
-  O.done_u8 = done;
-  O.stats_work = stats_work;
+  if ((reward && !aligned16(reward)) || (stats && !aligned16(stats)) || (stats_work && !aligned16(stats_work)))
+    return set_error(AUV_EINVAL, "auv_step: output buffers must be 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
-  if (int rc = launch_env_loop(env, 1, mode, O, s)) return rc;
-  if (stats)
-    if (int rc = launch_stats_reduce(stats_work, 1, env_loop_stats_groups(env->E), stats, s)) return rc;
+  if (pol_mode) {
+    // the policy rollout with T = 1: its reward [1][N] is this reward [N]
+    auv_rollout_buffers rb{};
+    rb.reward = reward;
+    rb.stats = stats;
+    rb.stats_work = stats_work;
+    if (int rc = launch_policy_rollout(env, 1, mode, policy, nullptr, &rb, s, done)) return rc;
+    if (stats)
+      if (int rc = launch_stats_reduce(stats_work, 1, rollout_stats_groups(env->E.n), stats, s)) return rc;
+  } else {
+    StepOut O{};
+    O.act = const_cast<float*>(actions);
+    O.reward = reward;
+    O.done_u8 = done;
+    O.stats_work = stats_work;
+    if (int rc = launch_env_loop(env, 1, mode, O, s)) return rc;
+    if (stats)
+      if (int rc = launch_stats_reduce(stats_work, 1, env_loop_stats_groups(env->E), stats, s)) return rc;
+  }
   env->global_step += 1;
+  return AUV_OK;
+}
+
+int auv_get_status(auv_env* env, uint32_t* nonfinite_count, uint32_t* abandoned_waits, void* stream) {
+  if (!env) return set_error(AUV_EINVAL, "auv_get_status: NULL handle");
+  if (!env->E.status) return set_error(AUV_EINVAL, "auv_get_status: the handle was created without a status buffer");
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t h[2] = {0u, 0u};
+  // the copy is pageable host memory: it completes before hipMemcpyAsync returns or by the
+  // synchronisation below; the counters are cleared behind it on the same stream
+  if (hipMemcpyAsync(h, env->E.status, sizeof h, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipMemsetAsync(env->E.status, 0, sizeof h, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+    return set_error(AUV_ERUNTIME, "auv_get_status: %s", hipGetErrorString(hipGetLastError()));
+  if (nonfinite_count) *nonfinite_count = h[0];
+  if (abandoned_waits) *abandoned_waits = h[1];
+  if (h[0] || h[1])
+    return set_error(AUV_ENONFINITE, "auv_get_status: %u non-finite state components, %u abandoned waits", h[0], h[1]);
   return AUV_OK;
 }
 

@@ -42,8 +42,10 @@ int env_loop_stats_groups(const EnvArgs& E);
 int compute_units();
 
 // launches implemented in auv_policy.hip
+// done_u8: optional [N] done flags of a one-step launch (auv_step's output form)
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy,
-                          const auv_mlp* value, const auv_rollout_buffers* rb, hipStream_t s);
+                          const auv_mlp* value, const auv_rollout_buffers* rb, hipStream_t s,
+                          uint8_t* done_u8 = nullptr);
 int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, hipStream_t s);
 int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s);
 

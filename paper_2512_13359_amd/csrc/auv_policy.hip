@@ -34,7 +34,48 @@ struct RolloutShared {
   unsigned obs_ready[ROLLOUT_MAX_TILES];    // per tile: observations published (1 + steps done)
   unsigned h1_ready[ROLLOUT_MAX_TILES];     // per tile: MLP waves done with hidden 1 (all, each step)
   unsigned mu_ready[ROLLOUT_MAX_TILES];     // per tile: MLP waves done with the output (all, each step)
+  float st[2][ROLLOUT_MAX_TILES][3][64];    // statistics rows of the tiles, by 64-step row parity
+  unsigned st_count[2];                     // tiles that have written a row of that parity (running count)
 };
+
+// Batch statistics of one workgroup: every physics wave parks its three wave sums of step t
+// in lane t mod 64 (StatsBuf); at the end of a 64-step row (or of the launch) the tiles'
+// rows meet in LDS, and whichever tile arrives last adds them in tile order and stores one
+// row of partials per workgroup ([3][G][T], G = workgroups).  The tiles of a workgroup stay
+// within a step or two of each other (the MLP waves serve them in turn), so rows of
+// alternating parity never overlap in LDS.
+template <int TPW>
+__device__ __forceinline__ void stats_row_combine(RolloutShared& S, StatsBuf& B, float* __restrict__ work, int T,
+                                                  int t, int lane, int k) {
+  const int slot = t & 63;
+  if (slot != 63 && t != T - 1) return;
+  const int t0 = t - slot, par = (t >> 6) & 1;
+  const size_t G = gridDim.x;
+  if (TPW == 1) {
+    if (lane <= slot) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s) work[((size_t)s * G + blockIdx.x) * T + t0 + lane] = B.v[s];
+    }
+    return;
+  }
+#pragma unroll
+  for (int s = 0; s < 3; ++s) S.st[par][k][s][lane] = B.v[s];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  unsigned before = 0;
+  if (lane == 0) before = __hip_atomic_fetch_add(&S.st_count[par], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  before = __builtin_amdgcn_readfirstlane(before);
+  if ((before + 1u) % (unsigned)TPW != 0u) return;   // not the last tile of this row
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  if (lane <= slot) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      float v = S.st[par][0][s][lane];
+#pragma unroll
+      for (int kk = 1; kk < TPW; ++kk) v += S.st[par][kk][s][lane];
+      work[((size_t)s * G + blockIdx.x) * T + t0 + lane] = v;
+    }
+  }
+}
 
 // Observation features of one environment written by the four lanes of its quad into the
 // layer-1 operand of tile nt (bf16 element stores; features 23..31 stay zero).
@@ -144,6 +185,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   if (tid < 16) S.b3[tid] = tid < ACT ? b[2 * HID + tid] : 0.0f;
   quad::stage_alloc(V, S.alloc, tid);
   if (tid < ROLLOUT_MAX_TILES) S.obs_ready[tid] = S.h1_ready[tid] = S.mu_ready[tid] = 0u;
+  if (tid < 2) S.st_count[tid] = 0u;
   __syncthreads();
   if (wave < ROLLOUT_MLP_WAVES) {
     rollout_mlp_wave<TPW>(S, T, w, b, wave, lane, E.sync_polls);
@@ -179,6 +221,8 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   };
   store_traj(0);
   StatsBuf SB{};
+  uint32_t nf = 0;          // non-finite state components (this lane's share) at episode ends
+  bool abandoned = false;   // a wait for the policy gave up (a defect): the state is poisoned
   // terms of the previous step's reward, finished in the next step's policy wait
   float pv_q = 0.0f, pv_qr = 0.0f, pv_dist = 0.0f, pv_usq = 0.0f, pv_reward = 0.0f;
   bool pv_done = false;
@@ -194,12 +238,18 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     if (valid && c == 0) {
       if (O.reward) O.reward[t1i] = reward;
       if (O.done) O.done[t1i] = pv_done ? 1.0f : 0.0f;
+      if (O.done_u8) O.done_u8[i] = pv_done ? 1 : 0;
     }
     if (O.stats_work) {   // reward, done and dist are the same in the four lanes of a quad
       const float sr = wave_sum_quads(valid ? reward : 0.0f);
       const float sd = wave_sum_quads((valid && pv_done) ? 1.0f : 0.0f);
       const float sp = wave_sum_quads(valid ? pv_dist : 0.0f);
-      stats_park(SB, O.stats_work, T, t1, lane, TPW * blockIdx.x + k, TPW * gridDim.x, sr, sd, sp);
+      if (lane == (t1 & 63)) {
+        SB.v[0] = sr;
+        SB.v[1] = sd;
+        SB.v[2] = sp;
+      }
+      stats_row_combine<TPW>(S, SB, O.stats_work, T, t1, lane, k);
     }
   };
   if (PAPER)
@@ -222,6 +272,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     if (O.obs && valid) quad::store_obs<PAPER>(O.obs, TN, ti, c, X, false);   // o_t, recorded while the MLP waves work on it
     if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1), E.sync_polls)) {   // abandoned: poison
       X.p = X.q = X.v = X.om = __builtin_nanf("");
+      abandoned = true;
       break;
     }
     // policy output for this lane's two action components (fixed-order partial sums)
@@ -308,7 +359,10 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     pv_dist = dist;
     pv_usq = usq;
     pv_done = done;
-    if (done) quad::new_episode<PAPER>(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist);   // the whole quad
+    if (done) {   // the whole quad
+      nf += quad::nonfinite_quad(c, X);
+      quad::new_episode<PAPER>(V, E, K, gid, i, valid, X, M, F, pr, qr, rc, dist);
+    }
     if (PAPER)
       put_obs_quad_paper(S, k, slot, c, X.ob, X.v, X.om);
     else
@@ -322,8 +376,10 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     }
     store_traj(t + 1);
   }
-  if (T > 0) finish_step(T - 1);
+  // the last step's outputs (steps after an abandoned wait keep whatever the buffers held)
+  if (T > 0 && !abandoned) finish_step(T - 1);
   if (valid) quad::store_env<PAPER>(E, c, i, X);
+  report_status(E.status, valid ? nf + quad::nonfinite_quad(c, X) : 0u, (abandoned && lane == 0) ? 1u : 0u);
 }
 
 // Stand-alone MLP forward over obs [23][n] -> out [n_out][n]: workgroups of four MLP waves
@@ -428,9 +484,9 @@ static int rollout_tiles_per_group(int n) {
   return n >= cus * 64 ? 4 : (n >= cus * 32 ? 2 : 1);
 }
 
-int rollout_stats_groups(int n) {
+int rollout_stats_groups(int n) {   // one partial per workgroup
   const int tpw = rollout_tiles_per_group(n);
-  return tpw * ((n + 16 * tpw - 1) / (16 * tpw));
+  return (n + 16 * tpw - 1) / (16 * tpw);
 }
 
 template <bool SAMPLE, bool PAPER>
@@ -449,7 +505,7 @@ static void launch_rollout_kernel(int tpw, int n, hipStream_t s, const VehArgs& 
 }
 
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, const auv_mlp* value,
-                          const auv_rollout_buffers* rb, hipStream_t s) {
+                          const auv_rollout_buffers* rb, hipStream_t s, uint8_t* done_u8) {
   if (int rc = check_mlp(policy, ACT, "auv_rollout policy")) return rc;
   const bool sample = (mode == AUV_ACT_POLICY_SAMPLE);
   if (sample && (!policy->log_std || !aligned16(policy->log_std)))
@@ -472,6 +528,7 @@ int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, 
   O.done = rb->done;
   O.traj = rb->traj_state;
   O.stats_work = rb->stats_work;
+  O.done_u8 = done_u8;
   const uint32_t g0 = (uint32_t)(env->global_step & 0xffffffffu);
   const int tpw = rollout_tiles_per_group(n);
   const uint16_t* w = (const uint16_t*)policy->w;

@@ -52,7 +52,7 @@ __device__ __forceinline__ void lane_store(const EnvArgs& E, int i, const Lane& 
 // previous action 0) and L.obs becomes the reset observation.
 __device__ __forceinline__ void lane_step(const VehArgs& V, const EnvArgs& E, uint32_t gid,
                                           const float a[ACT], Lane& L, float& reward, bool& done,
-                                          float& dist) {
+                                          float& dist, uint32_t& nonfinite_count) {
   float u[ACT], usq = 0.0f;
 #pragma unroll
   for (int k = 0; k < ACT; ++k) {
@@ -71,6 +71,7 @@ __device__ __forceinline__ void lane_step(const VehArgs& V, const EnvArgs& E, ui
   reward = -dist - 0.5f * theta - 0.01f * usq;
   done = (L.ep == E.H);
   if (done) {
+    nonfinite_count += nonfinite_state(L.x);   // the episode's end state, before the reset
     L.episode += 1u;
     reset_draws(E, gid, L.episode, L.x, L.P);
     make_model(V, L.P, L.M);

@@ -428,6 +428,13 @@ __device__ __forceinline__ void store_obs(float* __restrict__ obs, size_t stride
   obs[(16 + 2 * c) * stride + at] = X.u1;
 }
 
+// Non-finite state components of the quad's environment held by this lane: p, v, omega
+// components in lanes 0-2, the quaternion component in every lane (13 per environment).
+__device__ __forceinline__ uint32_t nonfinite_quad(int c, const QEnv& X) {
+  const uint32_t vec = nonfinite(X.p) + nonfinite(X.v) + nonfinite(X.om);
+  return (c < 3 ? vec : 0u) + nonfinite(X.q);
+}
+
 // The 13 state rows of X into s[k * stride + at] (p, q = (w, x, y, z), v, omega).
 __device__ __forceinline__ void store_state(float* __restrict__ s, size_t stride, size_t at, int c, const QEnv& X) {
   if (c < 3) {

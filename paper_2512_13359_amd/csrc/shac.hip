@@ -674,6 +674,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_window(EnvArgs E, VehArgs V, 
 
   // ------------------------------------------- environment update (reset at the episode end)
   if (lead && valid) {
+    uint32_t nf = 0;   // non-finite components of the window's end state, before any reset
+#pragma unroll
+    for (int k = 0; k < 3; ++k) nf += nonfinite(x.p[k]) + nonfinite(x.v[k]) + nonfinite(x.w[k]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) nf += nonfinite(x.q[k]);
+    report_status(E.status, nf, 0u);
     adj::X13<float> xn = x;
     float abn[6], on[12];
 #pragma unroll

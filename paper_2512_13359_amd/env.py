@@ -53,10 +53,11 @@ class AuvEnv:
         self.ep_step = torch.zeros(n, dtype=torch.int32, device=device)
         self.episode = torch.zeros(n, dtype=torch.int32, device=device)
         self.obs = torch.zeros(A.OBS_DIM, n, **f32)
+        self.status = torch.zeros(2, dtype=torch.int32, device=device)   # failure counters (uint32)
         self._cfg = A.make_config(n, int(cfg["substeps"]), int(cfg["episode_len"]), cfg["dt_control"],
                                   int(cfg["seed"]), int(cfg["flags"]), int(cfg.get("env_offset", 0)))
         self._veh = A.make_vehicle(vehicle, alloc)
-        self._bufs = A.make_env_buffers(self.state, self.params, self.ep_step, self.episode, self.obs)
+        self._bufs = A.make_env_buffers(self.state, self.params, self.ep_step, self.episode, self.obs, self.status)
         self.handle = A.auv_create(self._cfg, self._veh, self._bufs)
 
     def close(self):
@@ -86,16 +87,22 @@ class AuvEnv:
     def reset(self):
         A.auv_reset(self.handle)
 
-    def step(self, mode=A.AUV_ACT_RANDOM, actions=None, want_stats=False):
-        """One control step; returns (reward [N], done uint8 [N], stats [3] or None)."""
+    def step(self, mode=A.AUV_ACT_RANDOM, actions=None, want_stats=False, policy=None):
+        """One control step (policy: an upload_mlp dict in the policy modes); returns
+        (reward [N], done uint8 [N], stats [3] or None)."""
         reward = torch.empty(self.n, dtype=torch.float32, device=self.device)
         done = torch.empty(self.n, dtype=torch.uint8, device=self.device)
         stats = work = None
         if want_stats:
             stats = torch.empty(3, dtype=torch.float32, device=self.device)
             work = torch.empty(A.auv_stats_work_floats(self.n, 1), dtype=torch.float32, device=self.device)
-        A.auv_step(self.handle, mode, actions, reward, done, stats, work)
+        A.auv_step(self.handle, mode, actions, None if policy is None else policy["struct"], reward, done, stats, work)
         return reward, done, stats
+
+    def get_status(self):
+        """(non-finite state components, abandoned waits) since the last call; synchronises."""
+        _, nf, ab = A.auv_get_status(self.handle)
+        return nf, ab
 
     def rollout_buffers(self, T, record=("obs", "act", "reward", "done", "stats"), value=False):
         """Allocate the per-step output buffers named in `record`."""

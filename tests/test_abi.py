@@ -54,7 +54,8 @@ def test_create_validates_without_gpu():
            (_cfg(dt_control=-1.0), veh, _bufs(), "dt_control"),
            (_cfg(flags=1 << 10), veh, _bufs(), "flag"),
            (_cfg(), veh, _bufs(0x10004), "aligned"),
-           (_cfg(), veh, A.AuvEnvBuffers(0x10000, None, 0x20000, 0x30000, 0x40000), "NULL")]
+           (_cfg(), veh, A.AuvEnvBuffers(0x10000, None, 0x20000, 0x30000, 0x40000), "NULL"),
+           (_cfg(), veh, A.AuvEnvBuffers(0x10000, 0x11000, 0x12000, 0x13000, 0x14000, 0x15002), "status")]
     v2 = A.make_vehicle(W.vehicle_variant(m=-1.0), W.ALLOC)
     bad.append((_cfg(), v2, _bufs(), "mass"))
     v3 = A.make_vehicle(W.vehicle_variant(W=float("nan")), W.ALLOC)
@@ -74,10 +75,22 @@ def test_argument_errors_before_any_launch():
     h = A.auv_create(_cfg(), A.make_vehicle(W.VEHICLE, W.ALLOC), _bufs())
     rc = A.lib.auv_rollout(h, 0, A.AUV_ACT_RANDOM, None, None, None, None)
     assert rc == A.AUV_EINVAL and "T must be" in A.auv_last_error()
-    rc = A.lib.auv_step(h, 9, None, None, None, None, None, None)
+    rc = A.lib.auv_step(h, 9, None, None, None, None, None, None, None)
     assert rc == A.AUV_EINVAL and "mode" in A.auv_last_error()
-    rc = A.lib.auv_step(h, A.AUV_ACT_EXTERNAL, None, None, None, None, None, None)
+    rc = A.lib.auv_step(h, A.AUV_ACT_EXTERNAL, None, None, None, None, None, None, None)
     assert rc == A.AUV_EINVAL and "actions" in A.auv_last_error()
+    rc = A.lib.auv_step(h, A.AUV_ACT_POLICY_MEAN, None, None, None, None, None, None, None)
+    assert rc == A.AUV_EINVAL and "policy" in A.auv_last_error()
+    mlp = A.AuvMlp(0x1000, 0x2000, 0x3000, 8)
+    rc = A.lib.auv_step(h, A.AUV_ACT_RANDOM, None, ctypes.byref(mlp), None, None, None, None, None)
+    assert rc == A.AUV_EINVAL and "policy" in A.auv_last_error()
+    bad_net = A.AuvMlp(0x1000, 0x2000, 0x3000, 3)
+    rc = A.lib.auv_step(h, A.AUV_ACT_POLICY_MEAN, None, ctypes.byref(bad_net), None, None, None, None, None)
+    assert rc == A.AUV_EINVAL and "n_out" in A.auv_last_error()
+    # a handle without a status buffer has nothing to read: refused before any GPU call
+    nf = ctypes.c_uint32(7)
+    rc = A.lib.auv_get_status(h, ctypes.byref(nf), None, None)
+    assert rc == A.AUV_EINVAL and "status" in A.auv_last_error() and nf.value == 7
     rc = A.lib.auv_rollout(h, 10, A.AUV_ACT_RANDOM, None, None,
                            ctypes.byref(A.AuvRolloutBuffers(stats=0x1000)), None)
     assert rc == A.AUV_EINVAL and "stats_work" in A.auv_last_error()
@@ -114,5 +127,6 @@ def test_binding_structs_match_header_sizes():
     assert ctypes.sizeof(A.AuvVehicle) == 4 * (1 + 3 + 6 + 6 + 6 + 2 + 3 + 1 + 48)
     assert ctypes.sizeof(A.AuvConfig) == 32
     assert ctypes.sizeof(A.AuvRolloutBuffers) == 80
+    assert ctypes.sizeof(A.AuvEnvBuffers) == 48
     v = A.make_vehicle(W.VEHICLE, W.ALLOC)
     assert np.allclose(np.array(v.alloc).reshape(6, 8), W.ALLOC)

@@ -128,27 +128,12 @@ def test_c3_closed_loop(nets):
         assert np.allclose(s[0], got["reward"].astype(np.float64).sum(1), rtol=1e-5, atol=1e-3)
 
 
-def test_c4_full_size_sampled(nets):
-    """c4 at full size, the configuration the benchmark times: 16384 envs x 2000 steps,
-    4 substeps, Lissajous references, policy mean.  Episode ends exact for every env; the
-    policy valid on 6000 sampled (step, env) observations; for 32 envs every one of the
-    2000 transitions agrees with the oracle's control step from the GPU's state under the
-    GPU's action (1e-4, the one-step bound), and the reset draws of the episode starts
-    agree with the oracle's own."""
-    pol, _, dpol, _ = nets
-    cfg = W.config("c4")
-    n, T = cfg["n_envs"], cfg["T"]
-    announce(f"c4 full size n={n} T={T}")
-    g, got = _policy_rollout(cfg, T, dpol, ("obs", "act", "reward", "done", "traj_state"))
-    r = np.random.default_rng(0)
-    idx = r.choice(T * n, 6000, replace=False)
-    assert _check_mu_on_gpu_obs(pol, got, idx) <= TOL_VALID
-    d = got["done"]
-    assert np.array_equal(np.nonzero(d.any(axis=1))[0], [499, 999, 1499, 1999])
-    assert np.all(d[[499, 999, 1499, 1999]] == 1)
-    off = 9000
-    sl = slice(off, off + 32)
-    o = oracle_env(W.config("c4", n_envs=32, env_offset=off))
+def _teacher_forced(cfg, got, off, n_slice, T):
+    """Worst per-transition errors of envs [off, off + n_slice): each of the T transitions
+    against the oracle's control step from the GPU's state under the GPU's action (state,
+    reward, next observation; and whether any done flag differs)."""
+    sl = slice(off, off + n_slice)
+    o = oracle_env(dict(cfg, n_envs=n_slice, env_offset=off))
     o.reset()
     traj = got["traj_state"][:, :, sl].astype(np.float64)
     worst = np.zeros(4)
@@ -161,6 +146,30 @@ def test_c4_full_size_sampled(nets):
              rel_err(got["obs"][:, t + 1, sl], obs).max() if t + 1 < T else 0.0,
              float(np.any(done != (got["done"][t, sl] == 1)))]
         worst = np.maximum(worst, e)
+    return worst
+
+
+def test_c4_full_size_sampled(nets):
+    """c4 at full size, the configuration the benchmark times: 16384 envs x 2000 steps,
+    4 substeps, Lissajous references, policy mean.  Episode ends exact for every env; the
+    policy valid on 6000 sampled (step, env) observations; every one of the 2000
+    transitions agrees with the oracle's control step from the GPU's state under the GPU's
+    action (1e-4, the one-step bound) for the 64 envs of one workgroup (all four of its
+    physics tiles), and the reset draws of the episode starts agree with the oracle's own."""
+    pol, _, dpol, _ = nets
+    cfg = W.config("c4")
+    n, T = cfg["n_envs"], cfg["T"]
+    announce(f"c4 full size n={n} T={T}")
+    g, got = _policy_rollout(cfg, T, dpol, ("obs", "act", "reward", "done", "traj_state"))
+    r = np.random.default_rng(0)
+    idx = r.choice(T * n, 6000, replace=False)
+    assert _check_mu_on_gpu_obs(pol, got, idx) <= TOL_VALID
+    d = got["done"]
+    assert np.array_equal(np.nonzero(d.any(axis=1))[0], [499, 999, 1499, 1999])
+    assert np.all(d[[499, 999, 1499, 1999]] == 1)
+    off = 141 * 64                  # workgroup 141: tiles 0-3
+    sl = slice(off, off + 64)
+    worst = _teacher_forced(cfg, got, off, 64, T)
     announce(f"c4 per-transition worst: state {worst[0]:.2e} reward {worst[1]:.2e} obs {worst[2]:.2e}")
     assert worst[3] == 0
     assert worst[0] <= 1e-4 and worst[1] <= 1e-4 and worst[2] <= 1e-4
@@ -283,3 +292,59 @@ def test_abandoned_waits_end_the_launch(nets):
     g.reset()
     g.rollout(20, W.MODE_POLICY_MEAN, policy=dpol)
     assert np.isfinite(host(g.state)).all()
+
+
+def _stats_rows_check(got, final_obs, check_dist):
+    """Rows of the batch statistics against fp64 sums of the GPU's own per-env values:
+    reward and |dp| (the norm of the post-step observation's first three rows, on steps
+    without an episode end) to 1e-5 relative, done exactly."""
+    s = got["stats"].astype(np.float64)
+    rew = got["reward"].astype(np.float64)
+    want_r = rew.sum(1)
+    assert np.all(np.abs(s[0] - want_r) <= 1e-5 * np.abs(rew).sum(1)), np.abs(s[0] - want_r).max()
+    assert np.array_equal(s[1], got["done"].astype(np.float64).sum(1))
+    if check_dist:
+        post = np.concatenate([got["obs"][0:3, 1:], final_obs[0:3, None]], axis=1).astype(np.float64)
+        want_p = np.sqrt((post ** 2).sum(0)).sum(1)
+        assert np.all(np.abs(s[2] - want_p) <= 1e-5 * want_p), np.abs(s[2] - want_p).max()
+
+
+@pytest.mark.parametrize("n", [16384 + 17, 8192 + 37])
+def test_rollout_statistics_all_rows(nets, n):
+    """Batch statistics of the fused rollout at four and at two tiles per workgroup, the
+    configurations of every benchmarked size from 8192 envs up, with a ragged last workgroup
+    (tiles partly or wholly empty): 80 steps cross a 64-step row of the partials and end in a
+    partial row.  Without episode ends all three rows are checked; with staggered episodes
+    (about 16 % of the envs end one within the launch, sampled actions) reward and done."""
+    pol, _, dpol, _ = nets
+    T = 80
+    for stagger in (False, True):
+        announce(f"rollout statistics n={n} T={T} stagger={stagger}")
+        cfg = W.config("c4", n_envs=n, T=T)
+        if stagger:
+            cfg["flags"] |= W.FLAG_STAGGER
+        mode = W.MODE_POLICY_SAMPLE if stagger else W.MODE_POLICY_MEAN
+        g, got = _policy_rollout(cfg, T, dpol, ("obs", "reward", "done", "stats"), mode=mode)
+        if stagger:
+            assert got["done"].sum() > 0.1 * n
+        else:
+            assert got["done"].sum() == 0
+        _stats_rows_check(got, host(g.obs), check_dist=not stagger)
+
+
+def test_two_tile_rollout_parity(nets):
+    """Two 16-env tiles per workgroup (the instantiation for 8192 to 16383 envs): every action a
+    valid policy output on 6000 sampled observations; every transition of the 64 envs of two
+    whole workgroups against the oracle's control step (1e-4), across an episode end."""
+    pol, _, dpol, _ = nets
+    n, T = 8192 + 37, 60
+    announce(f"two-tile rollout n={n} T={T}")
+    cfg = W.config("c4", n_envs=n, T=T, episode_len=41)
+    g, got = _policy_rollout(cfg, T, dpol, ("obs", "act", "reward", "done", "traj_state"))
+    idx = np.random.default_rng(2).choice(T * n, 6000, replace=False)
+    assert _check_mu_on_gpu_obs(pol, got, idx) <= TOL_VALID
+    assert np.array_equal(np.nonzero(got["done"].any(axis=1))[0], [40])
+    for off in (32 * 100, n - 37 - 27):    # workgroups 100-101; the last three (the last one ragged)
+        worst = _teacher_forced(cfg, got, off, 64, T)
+        announce(f"  envs {off}..{off + 63}: state {worst[0]:.2e} reward {worst[1]:.2e} obs {worst[2]:.2e}")
+        assert worst[3] == 0 and worst[0] <= 1e-4 and worst[1] <= 1e-4 and worst[2] <= 1e-4

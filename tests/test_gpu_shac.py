@@ -7,9 +7,8 @@ environment update.  Closed loop (policy mean / sample): every policy parameter'
 dL/dmu_t, the actions.  Episode end at the window's last step: terminal value before the
 reset, the reset itself, and the refusal of a window that would cross an episode end.  At
 the full 4096-environment, 32-step size: sampled environments against the oracle run on
-those environments alone (each environment's window depends only on itself), and the
-d log_std and d b3 entries against sums of the kernel's own per-step gradients with the
-oracle's noise.
+those environments alone (each environment's window depends only on itself); every gradient
+block of 32- and 64-step windows against the oracle at 256 and 33 environments.
 
 Tolerances: the kernel carries the adjoint in fp32 against the oracle's fp64; where a
 cotangent or activation sits within fp32 error of a bf16 rounding midpoint, the two sides
@@ -274,10 +273,42 @@ def test_shac_is_deterministic():
     assert np.array_equal(grads[0], grads[1])
 
 
+@pytest.mark.parametrize("n,h", [(256, 32), (33, 64)])
+def test_shac_long_window_matches_oracle(n, h):
+    """Windows of the benchmark's length (32 steps, at 256 environments) and of the longest
+    allowed (64 steps): every block of the policy gradient, dL/dmu_t, the loss and the
+    gradient norm against the oracle (sample mode).  These windows run the checkpoint ring
+    of the forward sweep and the reverse sweep over every stored substep."""
+    gamma = W.SHAC["gamma"]
+    announce(f"SHAC long window n={n} h={h}")
+    require_gpu()
+    cfg, g, start = _setup(n, seed=40 + h)
+    pol, val = _nets()
+    L = _learner(g, h, gamma)
+    out = dict(grad_act=_dev(8, h, n), reward=_dev(h, n))
+    L.window(mode=3, out=out)
+    want = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, gamma, 3, policy_net=pol, value_net=val,
+                         quantize=True)
+    assert rel_err(host(out["reward"]), want["rewards"]).max() <= 1e-3
+    ga = np.transpose(host(out["grad_act"])[0:6], (1, 0, 2))
+    ga_err = _block_err(ga, want["grad_act"])
+    blocks, pad = _unpad(host(L.grad))
+    assert np.all(pad == 0)
+    errs = {k: _block_err(blocks[k], want["grad_policy"][k]) for k in blocks}
+    announce(f"  dL/dmu error {ga_err:.2e}, block errors {errs}")
+    assert ga_err <= 2e-2
+    for k, e in errs.items():
+        assert e <= 5e-3, (k, e)
+    stats = host(L.stats)
+    assert abs(stats[0] - want["loss"]) <= 1e-3 * abs(want["loss"])
+    gn = np.sqrt(sum(float(np.sum(want["grad_policy"][k] ** 2)) for k in want["grad_policy"]))
+    assert abs(np.sqrt(stats[5]) - gn) <= 1e-2 * gn
+
+
 def test_shac_full_size_sampled_envs():
     """4096 environments x 32 steps (sample mode): 24 sampled environments against the
-    oracle run on those environments alone; d log_std and d b3 against sums of the kernel's
-    own dL/da with the oracle's noise (sum over every env and step)."""
+    oracle run on those environments alone (every gradient block at this window length is
+    compared with the oracle at 256 environments, test_shac_long_window_matches_oracle)."""
     n, h, gamma = W.SHAC["n_envs"], W.SHAC["h"], W.SHAC["gamma"]
     announce(f"SHAC full size n={n} h={h}")
     require_gpu()
@@ -291,14 +322,7 @@ def test_shac_full_size_sampled_envs():
     assert np.all(pad == 0) and all(np.all(np.isfinite(v)) for v in blocks.values())
     stats = host(L.stats)
     assert np.all(np.isfinite(stats)) and 0.0 < stats[7] <= 1.0
-    # d log_std_j = sum_{t,i} dL/da_j sigma_j eps_j
-    sig = np.exp(np.asarray(pol["log_std"], np.float32)[:6].astype(np.float64))
-    eps = np.stack([S.noise(cfg["seed"], np.arange(n), t) for t in range(h)])        # [h, 6, n]
     ga = np.transpose(got["grad_act"][0:6], (1, 0, 2)).astype(np.float64)
-    want_ls = np.sum(ga * eps, axis=(0, 2)) * sig
-    assert np.max(np.abs(blocks["log_std"] - want_ls)) <= 1e-4 * np.max(np.abs(want_ls))
-    want_b3 = np.sum(omlp.bf16_round(ga), axis=(0, 2))
-    assert np.max(np.abs(blocks["b3"] - want_b3)) <= 1e-4 * np.max(np.abs(want_b3))
     # sampled environments: the oracle on those columns alone (the loss scale 1/(N h) is the full N's)
     idx = np.unique(np.concatenate([np.linspace(0, n - 1, 22).astype(int), [1, n - 2]]))
     sub = {k: (v[..., idx] if isinstance(v, np.ndarray) and v.shape[-1] == n else v) for k, v in start.items()}
