@@ -40,6 +40,14 @@ Readings (the paper is silent; the device path takes the same):
     operators are the identity.
   * the terminal value is differentiated the same way; the value net's own parameters are
     not trained by this objective (SHAC fits the critic separately)
+
+Teacher forcing (window(..., forced=...)): a closed-loop window's trajectory is not unique
+under bf16 rounding (a hidden value within rounding error of a bf16 midpoint may round either
+way), so two correct implementations drift apart over a long window.  Given a trajectory
+(the states after each step and the actions taken), the forward replaces each state and
+action by the given value while keeping its derivative, x <- x + (x_given - x) held constant
+in the backward.  The result is the same objective's gradient linearised along the given
+trajectory; with the oracle's own trajectory it is the plain gradient.
 """
 from __future__ import annotations
 
@@ -236,14 +244,20 @@ def noise(seed: int, env_ids, step: int) -> np.ndarray:
 
 
 # ---- one window ------------------------------------------------------------------------
+def _force(v: torch.Tensor, given) -> torch.Tensor:
+    """v with the value `given` and the derivative of v (module docstring, teacher forcing)."""
+    return v + (_t(given) - v).detach()
+
+
 def window(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma: float, mode: int,
            policy: dict | None = None, value: dict | None = None, external=None, quantize: bool = True,
-           grad_state0: bool = False) -> dict:
+           grad_state0: bool = False, forced: dict | None = None) -> dict:
     """Forward of one window (torch graph kept for the backward).
 
     start: {x [13, n], abar [6, n], p_goal [3, n], q_goal [4, n], gfac [n], step (global step
     of the window's first action), env_ids [n]} as float64 numpy arrays (ints for the last
-    two); policy / value: net_params dicts (12 inputs; 6 and 1 outputs); external [h][6][n].
+    two); policy / value: net_params dicts (12 inputs; 6 and 1 outputs); external [h][6][n];
+    forced: None or {x [h][13][n] states after each step, a [h][6][n] actions} (teacher forcing).
     Returns tensors: loss, per-env J, rewards [h, n], actions a [h][6, n] (leaves in EXTERNAL
     mode), mu [h][6, n], the final state and abar, and V of the final observation."""
     x = _t(start["x"]).clone().requires_grad_(grad_state0)
@@ -270,9 +284,13 @@ def window(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma: flo
             if mode == MODE_POLICY_SAMPLE:
                 eps = _t(noise(int(cfg["seed"]), start["env_ids"], int(start["step"]) + t))
                 a = mu + torch.exp(policy["log_std"])[:, None] * eps
+            if forced is not None:
+                a = _force(a, forced["a"][t])
         u = clip_action(a)
         tau = torch.cat([fm * u[0:3], tm * u[3:6]], 0)
         x = step_dynamics(x, tau, veh, dt, S)
+        if forced is not None:
+            x = _force(x, forced["x"][t])
         o = observe(x, pg, qg)
         r = reward(task, o, u, abar)
         abar = beta * abar + (1.0 - beta) * u
@@ -289,7 +307,7 @@ def window(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma: flo
 
 def window_grad(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma: float, mode: int,
                 policy_net: dict | None = None, value_net: dict | None = None, external=None,
-                quantize: bool = True) -> dict:
+                quantize: bool = True, forced: dict | None = None) -> dict:
     """Loss and gradients of one window as float64 numpy arrays: grad_policy {W1, W2, W3,
     b1, b2, b3, log_std} (12-input, 6-output shapes), grad_act [h][6][n] (dL/da_t before the
     clip: the external actions' gradient, or the policy outputs' total derivative dL/dmu_t
@@ -297,7 +315,8 @@ def window_grad(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma
     [13][n], and the forward's rewards [h][n], J [n], v_last [n], final state [13][n] and abar."""
     pol = net_params(policy_net, 6, requires_grad=True) if policy_net is not None else None
     val = net_params(value_net, 1) if value_net is not None else None
-    w = window(start, cfg, vehicle, task, h, gamma, mode, pol, val, external, quantize, grad_state0=True)
+    w = window(start, cfg, vehicle, task, h, gamma, mode, pol, val, external, quantize, grad_state0=True,
+               forced=forced)
     w["loss"].backward()
     out = dict(loss=float(w["loss"].detach()), rewards=w["rewards"].detach().numpy(), J=w["J"].detach().numpy(),
                v_last=w["v_last"].detach().numpy(), x=w["x"].detach().numpy(), abar=w["abar"].detach().numpy(),

@@ -273,29 +273,58 @@ def test_shac_is_deterministic():
     assert np.array_equal(grads[0], grads[1])
 
 
+def _states_from_obs(obs, p_goal, q_goal):
+    """States [13, ...] behind paper-task observations [12, ...]: p = p_goal - R dp_b, q = q_goal
+    (x) q_err^-1 with q_err = exp(rotation vector / 2), v and omega as observed (scipy's
+    rotations; the sign of q is immaterial to the dynamics' outputs)."""
+    from scipy.spatial.transform import Rotation
+    shp = obs.shape[1:]
+    o = obs.reshape(12, -1).astype(np.float64)
+    m = o.shape[1]
+    pg = np.broadcast_to(p_goal[:, None, :], (3,) + shp).reshape(3, m) if len(shp) == 2 else p_goal
+    qg = np.broadcast_to(q_goal[:, None, :], (4,) + shp).reshape(4, m) if len(shp) == 2 else q_goal
+    Rg = Rotation.from_quat(np.stack([qg[1], qg[2], qg[3], qg[0]], axis=1))
+    R = Rg * Rotation.from_rotvec(o[3:6].T).inv()
+    qx = R.as_quat()
+    x = np.zeros((13, m))
+    x[0:3] = pg - R.apply(o[0:3].T).T
+    x[3:7] = np.stack([qx[:, 3], qx[:, 0], qx[:, 1], qx[:, 2]])
+    x[7:13] = o[6:12]
+    return x.reshape((13,) + shp)
+
+
 @pytest.mark.parametrize("n,h", [(256, 32), (33, 64)])
 def test_shac_long_window_matches_oracle(n, h):
     """Windows of the benchmark's length (32 steps, at 256 environments) and of the longest
-    allowed (64 steps): every block of the policy gradient, dL/dmu_t, the loss and the
-    gradient norm against the oracle (sample mode).  These windows run the checkpoint ring
-    of the forward sweep and the reverse sweep over every stored substep."""
+    allowed (64 steps): every block of the policy gradient, dL/dmu_t, the rewards, the loss and
+    the gradient norm against the oracle (sample mode).  These windows run the checkpoint ring
+    of the forward sweep and the reverse sweep over every stored substep.  Over this many
+    closed-loop steps bf16 rounding flips let the GPU's and the oracle's trajectories drift
+    apart (both correct), so the oracle is teacher-forced onto the GPU's trajectory: its states
+    rebuilt from the recorded observations (and the final state buffer), its actions the
+    recorded ones; the gradient is then the objective's along that trajectory."""
     gamma = W.SHAC["gamma"]
     announce(f"SHAC long window n={n} h={h}")
     require_gpu()
     cfg, g, start = _setup(n, seed=40 + h)
     pol, val = _nets()
     L = _learner(g, h, gamma)
-    out = dict(grad_act=_dev(8, h, n), reward=_dev(h, n))
+    out = dict(grad_act=_dev(8, h, n), reward=_dev(h, n), obs=_dev(23, h, n), act=_dev(8, h, n))
     L.window(mode=3, out=out)
+    got = {k: host(v) for k, v in out.items()}
+    xs = np.concatenate([_states_from_obs(got["obs"][0:12, 1:], start["p_goal"], start["q_goal"]),
+                         host(g.state).astype(np.float64)[:, None]], axis=1)           # [13, h, n]
+    forced = dict(x=np.transpose(xs, (1, 0, 2)), a=np.transpose(got["act"][0:6], (1, 0, 2)).astype(np.float64))
     want = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, gamma, 3, policy_net=pol, value_net=val,
-                         quantize=True)
-    assert rel_err(host(out["reward"]), want["rewards"]).max() <= 1e-3
-    ga = np.transpose(host(out["grad_act"])[0:6], (1, 0, 2))
+                         quantize=True, forced=forced)
+    rerr = rel_err(got["reward"], want["rewards"]).max()
+    ga = np.transpose(got["grad_act"][0:6], (1, 0, 2))
     ga_err = _block_err(ga, want["grad_act"])
     blocks, pad = _unpad(host(L.grad))
     assert np.all(pad == 0)
     errs = {k: _block_err(blocks[k], want["grad_policy"][k]) for k in blocks}
-    announce(f"  dL/dmu error {ga_err:.2e}, block errors {errs}")
+    announce(f"  reward {rerr:.2e}, dL/dmu {ga_err:.2e}, block errors {errs}")
+    assert rerr <= 1e-4
     assert ga_err <= 2e-2
     for k, e in errs.items():
         assert e <= 5e-3, (k, e)

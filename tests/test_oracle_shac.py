@@ -204,3 +204,41 @@ def test_terminal_value_and_discount_enter_linearly():
     b = S.window(start, cfg, W.VEHICLE, W.PAPER_TASK, h, gamma, S.MODE_POLICY_MEAN, S.net_params(pol, 6), None)
     dv = gamma ** h * float(a["v_last"].detach().sum()) / (n * h)
     assert abs((float(b["loss"].detach()) - float(a["loss"].detach())) - dv) <= 1e-14
+
+
+def test_teacher_forcing_along_own_trajectory_is_the_plain_gradient():
+    """Forcing the window onto its own trajectory changes nothing (the replacement keeps the
+    value and the derivative); forcing it onto a perturbed trajectory moves the rewards to that
+    trajectory's and the gradient by a comparably small amount."""
+    pol, val = _nets()
+    _, start = _moving_start(12, seed=21)
+    cfg = dict(CFG, n_envs=12)
+    h = 7
+    w = S.window(start, cfg, W.VEHICLE, W.PAPER_TASK, h, 0.99, S.MODE_POLICY_SAMPLE, S.net_params(pol, 6),
+                 S.net_params(val, 1), quantize=True)
+    acts = [a.detach().numpy() for a in w["acts"]]
+    # the states after each step under those actions (the forward's own step, replayed)
+    xs, x = [], torch.as_tensor(start["x"])
+    veh = S.Vehicle(W.VEHICLE, start["gfac"])
+    f32 = lambda v: float(np.float32(v))  # noqa: E731
+    for t in range(h):
+        u = S.clip_action(torch.as_tensor(acts[t]))
+        tau = torch.cat([f32(W.PAPER_TASK["f_max"]) * u[0:3], f32(W.PAPER_TASK["tau_max"]) * u[3:6]], 0)
+        x = S.step_dynamics(x, tau, veh, f32(cfg["dt_control"]), cfg["substeps"])
+        xs.append(x.numpy().copy())
+    assert np.array_equal(xs[-1], w["x"].detach().numpy())
+    plain = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, 0.99, S.MODE_POLICY_SAMPLE, pol, val)
+    forced = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, 0.99, S.MODE_POLICY_SAMPLE, pol, val,
+                           forced=dict(x=np.stack(xs), a=np.stack(acts)))
+    for k in plain["grad_policy"]:
+        assert np.allclose(forced["grad_policy"][k], plain["grad_policy"][k], rtol=1e-10, atol=1e-14), k
+    assert np.allclose(forced["rewards"], plain["rewards"], rtol=1e-12, atol=1e-14)
+    # a perturbed trajectory: the rewards follow it, the gradient moves a little
+    r = np.random.default_rng(5)
+    xp = np.stack(xs) + 1e-4 * r.standard_normal(np.stack(xs).shape)
+    pert = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, 0.99, S.MODE_POLICY_SAMPLE, pol, val,
+                         forced=dict(x=xp, a=np.stack(acts)))
+    assert not np.allclose(pert["rewards"], plain["rewards"], rtol=1e-9, atol=0)
+    for k in plain["grad_policy"]:
+        g0 = plain["grad_policy"][k]
+        assert np.max(np.abs(pert["grad_policy"][k] - g0)) <= 1e-2 * np.max(np.abs(g0)), k
