@@ -249,6 +249,16 @@ def _force(v: torch.Tensor, given) -> torch.Tensor:
     return v + (_t(given) - v).detach()
 
 
+def _force_state(x: torch.Tensor, given) -> torch.Tensor:
+    """_force for states [13, n]: q and -q are the same attitude, and the derivative of the
+    computed state is that of its own quaternion, so the given quaternion takes the sign
+    nearest the computed one first."""
+    g = np.array(given, np.float64)
+    s = np.where(np.sum(g[3:7] * x[3:7].detach().numpy(), axis=0) < 0.0, -1.0, 1.0)
+    g[3:7] *= s[None, :]
+    return _force(x, g)
+
+
 def window(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma: float, mode: int,
            policy: dict | None = None, value: dict | None = None, external=None, quantize: bool = True,
            grad_state0: bool = False, forced: dict | None = None) -> dict:
@@ -290,7 +300,7 @@ def window(start: dict, cfg: dict, vehicle: dict, task: dict, h: int, gamma: flo
         tau = torch.cat([fm * u[0:3], tm * u[3:6]], 0)
         x = step_dynamics(x, tau, veh, dt, S)
         if forced is not None:
-            x = _force(x, forced["x"][t])
+            x = _force_state(x, forced["x"][t])
         o = observe(x, pg, qg)
         r = reward(task, o, u, abar)
         abar = beta * abar + (1.0 - beta) * u

@@ -233,6 +233,14 @@ def test_teacher_forcing_along_own_trajectory_is_the_plain_gradient():
     for k in plain["grad_policy"]:
         assert np.allclose(forced["grad_policy"][k], plain["grad_policy"][k], rtol=1e-10, atol=1e-14), k
     assert np.allclose(forced["rewards"], plain["rewards"], rtol=1e-12, atol=1e-14)
+    # the same trajectory with some quaternions given as -q (the same attitudes)
+    flip = np.stack(xs).copy()
+    flip[1::2, 3:7, ::3] *= -1.0
+    forced2 = S.window_grad(start, cfg, W.VEHICLE, W.PAPER_TASK, h, 0.99, S.MODE_POLICY_SAMPLE, pol, val,
+                            forced=dict(x=flip, a=np.stack(acts)))
+    for k in plain["grad_policy"]:
+        assert np.allclose(forced2["grad_policy"][k], plain["grad_policy"][k], rtol=1e-10, atol=1e-14), k
+    assert np.allclose(forced2["grad_act"], plain["grad_act"], rtol=1e-10, atol=1e-14)
     # a perturbed trajectory: the rewards follow it, the gradient moves a little
     r = np.random.default_rng(5)
     xp = np.stack(xs) + 1e-4 * r.standard_normal(np.stack(xs).shape)
