@@ -170,6 +170,24 @@ int auv_step(auv_env* env, int mode, const float* actions, const auv_mlp* policy
 int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy,
                 const auv_mlp* value, const auv_rollout_buffers* rbufs, void* stream);
 
+/* auv_rollout for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same launches and
+ * results, with the batch-statistics partials held in a device array of the library's own
+ * (AUV_STATIC_STATS_FLOATS floats, 8 MiB, on every GPU the library runs on, kept until the
+ * process ends) instead of rbufs->stats_work, which must be NULL.  Statistics of T steps need
+ * 3 T G floats of it, G = the launch's partial groups: ceil(N / 16) for the random / external
+ * modes up to 32768 envs, else ceil(N / 64); in the policy modes ceil(N / 16) below 8192 envs,
+ * ceil(N / 32) below 16384, else ceil(N / 64) (on a 256-CU device).  Every call on a GPU shares
+ * its array; each call rewrites the partials it reads, so nothing needs clearing, but calls
+ * that overlap on one GPU (any handle, stream or thread) race and must be ordered by the
+ * caller.  Calls no hipMalloc, hipFree or allocating library routine; the array's device
+ * address is looked up once per device on the first call there.  AUV_EINVAL, nothing
+ * enqueued: stats_work given, 3 T G beyond AUV_STATIC_STATS_FLOATS, or what auv_rollout
+ * rejects. */
+#define AUV_STATIC_STATS_FLOATS (2 * 1024 * 1024)
+int auv_rollout_static(auv_env* env, int32_t T, int mode, const auv_mlp* policy,
+                       const auv_mlp* value, const auv_rollout_buffers* rbufs, void* stream);
+
 /* Generalised advantage estimation over a [T][N] rollout (backward scan per env):
  * delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t, V_T = last_value;
  * A_t = delta_t + gamma lambda (1 - d_t) A_{t+1}, A_T = 0; ret_t = A_t + V_t. */

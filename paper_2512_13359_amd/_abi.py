@@ -20,6 +20,7 @@ AUV_ACT_EXTERNAL, AUV_ACT_RANDOM, AUV_ACT_POLICY_MEAN, AUV_ACT_POLICY_SAMPLE = 0
 AUV_F_DR, AUV_F_CURRENT, AUV_F_LISSAJOUS, AUV_F_STAGGER = 1, 2, 4, 8
 AUV_TASK_WORKLOAD, AUV_TASK_PAPER = 0, 1
 AUV_FLUID_FOSSEN, AUV_FLUID_INERTIA_BOX = 0, 1
+AUV_STATIC_STATS_FLOATS = 2 * 1024 * 1024
 OBS_DIM, ACT_DIM, STATE_DIM, PARAM_DIM, HIDDEN, ENVS_PER_GROUP = 23, 8, 13, 24, 256, 64
 
 _f = ctypes.c_float
@@ -110,6 +111,8 @@ def _load() -> ctypes.CDLL:
         "auv_step": (ctypes.c_int, [_vp, ctypes.c_int, _vp, P(AuvMlp), _vp, _vp, _vp, _vp, _vp]),
         "auv_get_status": (ctypes.c_int, [_vp, P(ctypes.c_uint32), P(ctypes.c_uint32), _vp]),
         "auv_rollout": (ctypes.c_int, [_vp, i32, ctypes.c_int, P(AuvMlp), P(AuvMlp), P(AuvRolloutBuffers), _vp]),
+        "auv_rollout_static": (ctypes.c_int, [_vp, i32, ctypes.c_int, P(AuvMlp), P(AuvMlp), P(AuvRolloutBuffers),
+                                              _vp]),
         "auv_gae": (ctypes.c_int, [i32, i32, _vp, _vp, _vp, _vp, _f, _f, _vp, _vp, _vp]),
         "auv_mlp_forward": (ctypes.c_int, [P(AuvMlp), i32, _vp, _vp, _vp]),
         "auv_get_global_step": (i64, [_vp]),
@@ -195,6 +198,13 @@ def auv_rollout(h: int, T: int, mode: int, policy: AuvMlp | None = None, value: 
     _check(lib.auv_rollout(h, T, mode, None if policy is None else ctypes.byref(policy),
                            None if value is None else ctypes.byref(value),
                            None if rbufs is None else ctypes.byref(rbufs), stream_ptr(stream)))
+
+
+def auv_rollout_static(h: int, T: int, mode: int, policy: AuvMlp | None = None, value: AuvMlp | None = None,
+                       rbufs: AuvRolloutBuffers | None = None, stream=None) -> None:
+    _check(lib.auv_rollout_static(h, T, mode, None if policy is None else ctypes.byref(policy),
+                                  None if value is None else ctypes.byref(value),
+                                  None if rbufs is None else ctypes.byref(rbufs), stream_ptr(stream)))
 
 
 def auv_gae(T: int, n_envs: int, reward, value, done, last_value, gamma: float, lam: float,

@@ -2,6 +2,7 @@
 // GAE) and the C interface.  The policy-driven fused rollout lives in auv_policy.hip.
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "auv_internal.hpp"
 #include "quad_env.hpp"
@@ -662,26 +663,70 @@ int auv_get_status(auv_env* env, uint32_t* nonfinite_count, uint32_t* abandoned_
   return AUV_OK;
 }
 
-int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const auv_mlp* value,
-                const auv_rollout_buffers* rb, void* stream) {
-  if (!env) return set_error(AUV_EINVAL, "auv_rollout: NULL handle");
-  if (T < 1) return set_error(AUV_EINVAL, "auv_rollout: T must be >= 1, got %d", T);
+}  // extern "C"
+
+// Statistics partials of auv_rollout_static, for callers that cannot allocate: a device
+// array of the library's own, one per GPU it runs on (held until the process ends).  In host
+// code `scratch` names a host-side stand-in, not device memory: its device address comes from
+// hipGetSymbolAddress, taken once per device on the first call there and kept per device.
+static __device__ __align__(256) float scratch[AUV_STATIC_STATS_FLOATS];
+static std::mutex g_scratch_mu;
+constexpr int MAX_DEVICES = 64;
+static float* g_scratch_ptr[MAX_DEVICES] = {};
+
+static int scratch_on_current_device(float** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES)
+    return set_error(AUV_ENODEV, "auv_rollout_static: no usable current device");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(AUV_ERUNTIME, "auv_rollout_static: hipGetSymbolAddress failed: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return AUV_OK;
+}
+
+// auv_rollout and auv_rollout_static: the same launches; the second takes the statistics
+// workspace from the library's device array instead of rbufs->stats_work.
+static int rollout_impl(const char* fn, auv_env* env, int32_t T, int mode, const auv_mlp* policy,
+                        const auv_mlp* value, const auv_rollout_buffers* rb_in, void* stream, bool static_work) {
+  if (!env) return set_error(AUV_EINVAL, "%s: NULL handle", fn);
+  if (T < 1) return set_error(AUV_EINVAL, "%s: T must be >= 1, got %d", fn, T);
   if ((int64_t)T * env->E.n * 23 > ((int64_t)1 << 40))
-    return set_error(AUV_EINVAL, "auv_rollout: T * N too large");
-  auv_rollout_buffers none{};
-  if (!rb) rb = &none;
-  if ((rb->stats == nullptr) != (rb->stats_work == nullptr))
-    return set_error(AUV_EINVAL, "auv_rollout: stats and stats_work must be given together");
+    return set_error(AUV_EINVAL, "%s: T * N too large", fn);
+  auv_rollout_buffers rbuf{};
+  if (rb_in) rbuf = *rb_in;
+  const auv_rollout_buffers* rb = &rbuf;
+  if (static_work) {
+    if (rb->stats_work) return set_error(AUV_EINVAL, "%s: stats_work must be NULL (the library's array is used)", fn);
+  } else if ((rb->stats == nullptr) != (rb->stats_work == nullptr)) {
+    return set_error(AUV_EINVAL, "%s: stats and stats_work must be given together", fn);
+  }
   const void* outs[10] = {rb->obs, rb->act, rb->logp, rb->value, rb->reward, rb->done,
                           rb->last_value, rb->traj_state, rb->stats, rb->stats_work};
   for (int k = 0; k < 10; ++k)
-    if (outs[k] && !aligned16(outs[k])) return set_error(AUV_EINVAL, "auv_rollout: output buffer %d not 16-byte aligned", k);
+    if (outs[k] && !aligned16(outs[k])) return set_error(AUV_EINVAL, "%s: output buffer %d not 16-byte aligned", fn, k);
+  const bool env_loop = (mode == AUV_ACT_EXTERNAL || mode == AUV_ACT_RANDOM);
+  const bool pol_mode = (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE);
+  if (!env_loop && !pol_mode) return set_error(AUV_EINVAL, "%s: unknown mode %d", fn, mode);
+  const int G = env_loop ? env_loop_stats_groups(env->E) : rollout_stats_groups(env->E.n);
+  if (static_work && rb->stats) {
+    const int64_t need = (int64_t)3 * T * G;
+    if (need > AUV_STATIC_STATS_FLOATS)
+      return set_error(AUV_EINVAL, "%s: statistics need %lld floats of partials (3 T G, G = %d), the maximum is %d", fn,
+                       (long long)need, G, AUV_STATIC_STATS_FLOATS);
+    if (int rc = scratch_on_current_device(&rbuf.stats_work)) return rc;
+  }
   hipStream_t s = (hipStream_t)stream;
-  if (mode == AUV_ACT_EXTERNAL || mode == AUV_ACT_RANDOM) {
+  if (env_loop) {
     if (mode == AUV_ACT_EXTERNAL && !rb->act)
-      return set_error(AUV_EINVAL, "auv_rollout: external mode reads actions from rbufs->act");
+      return set_error(AUV_EINVAL, "%s: external mode reads actions from rbufs->act", fn);
     if (policy || value || rb->logp || rb->value || rb->last_value)
-      return set_error(AUV_EINVAL, "auv_rollout: networks, logp and value outputs need a policy mode");
+      return set_error(AUV_EINVAL, "%s: networks, logp and value outputs need a policy mode", fn);
     StepOut O{};
     O.obs = rb->obs;
     O.act = rb->act;
@@ -690,17 +735,25 @@ int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const 
     O.traj = rb->traj_state;
     O.stats_work = rb->stats_work;
     if (int rc = launch_env_loop(env, T, mode, O, s)) return rc;
-    if (rb->stats)
-      if (int rc = launch_stats_reduce(rb->stats_work, T, env_loop_stats_groups(env->E), rb->stats, s)) return rc;
-  } else if (mode == AUV_ACT_POLICY_MEAN || mode == AUV_ACT_POLICY_SAMPLE) {
-    if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
-    if (rb->stats)   // one partial per wave of 16 environments
-      if (int rc = launch_stats_reduce(rb->stats_work, T, rollout_stats_groups(env->E.n), rb->stats, s)) return rc;
   } else {
-    return set_error(AUV_EINVAL, "auv_rollout: unknown mode %d", mode);
+    if (int rc = launch_policy_rollout(env, T, mode, policy, value, rb, s)) return rc;
   }
+  if (rb->stats)   // one partial per group (workgroup or wave) of the launch
+    if (int rc = launch_stats_reduce(rb->stats_work, T, G, rb->stats, s)) return rc;
   env->global_step += T;
   return AUV_OK;
+}
+
+extern "C" {
+
+int auv_rollout(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const auv_mlp* value,
+                const auv_rollout_buffers* rb, void* stream) {
+  return rollout_impl("auv_rollout", env, T, mode, policy, value, rb, stream, false);
+}
+
+int auv_rollout_static(auv_env* env, int32_t T, int mode, const auv_mlp* policy, const auv_mlp* value,
+                       const auv_rollout_buffers* rb, void* stream) {
+  return rollout_impl("auv_rollout_static", env, T, mode, policy, value, rb, stream, true);
 }
 
 int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value, const float* done,
