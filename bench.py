@@ -68,8 +68,22 @@ def recorded_traffic():
         return None
 
 
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(cfg: dict, n_steps: int) -> dict:
-    """The fp64 oracle on a bounded sample of the same workload (host cores)."""
+    """The fp64 oracle on a bounded sample of the same workload (host cores): all envs of the
+    workload over a prefix of n_steps control steps (min(T, 100) for the closed-loop
+    workloads), BLAS threads = the cores this process may run on."""
+    import numpy as np
     import threadpoolctl
 
     import workloads as W
@@ -79,16 +93,18 @@ def cpu_baseline(cfg: dict, n_steps: int) -> dict:
     cores = len(os.sched_getaffinity(0))
     with threadpoolctl.threadpool_limits(limits=cores):
         info = threadpoolctl.threadpool_info()
-        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        blas = [f"{i.get('internal_api', '?')} {i.get('version', '?')} ({i.get('num_threads', '?')} threads)"
+                for i in info if i.get("user_api") == "blas"]
         pol = W.mlp_weights(8, W.POLICY_SEED)
         e = oenv.Env(cfg, W.VEHICLE, W.ALLOC)
         e.reset()
         t0 = time.perf_counter()
         e.rollout(n_steps, cfg["mode"], policy=pol)
         dt = time.perf_counter() - t0
-    return {"value": n * n_steps / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} envs x {n_steps} control steps of the same workload (fp64 NumPy, "
-                      f"{dt:.1f} s)"}
+    return {"value": n * n_steps / dt, "unit": "env-steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} envs x the first {n_steps} control steps of the same workload (fp64 NumPy, "
+                      f"{dt:.1f} s)",
+            "cpu_model": _cpu_model(), "numpy": np.__version__, "blas": blas}
 
 
 def c5_measure(reps: int = 3) -> dict:
@@ -392,6 +408,37 @@ def small_configs_measure(reps: int = 3) -> dict:
     return out
 
 
+def probe_rates(reps: int = 3) -> dict:
+    """Throughput of the units that bound the rollout (auv_probe_rate): v_exp_f32, v_rcp_f32
+    and v_fma_f32 in lane operations per second, bf16 MFMA in FLOP/s, each from the median of
+    reps launches of 2048 workgroups (eight waves per SIMD) after one warm-up."""
+    import torch
+
+    from paper_2512_13359_amd import _abi as A
+
+    blocks = 2048
+    sink = torch.empty(blocks * 256, device="cuda")
+    out = {}
+    for name, kind, iters in (("exp_lane_ops_per_s", A.AUV_PROBE_EXP, 20000), ("rcp_lane_ops_per_s", A.AUV_PROBE_RCP, 20000),
+                              ("fma_lane_ops_per_s", A.AUV_PROBE_FMA, 40000),
+                              ("mfma_bf16_flop_per_s", A.AUV_PROBE_MFMA_BF16, 200)):
+        times = []
+        for k in range(reps + 1):
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            A.auv_probe_rate(kind, blocks, iters, sink)
+            e1.record()
+            torch.cuda.synchronize()
+            if k:
+                times.append(e0.elapsed_time(e1) * 1e-3)
+        t = sorted(times)[len(times) // 2]
+        ops = blocks * 4 * 8 * iters * 16384 if kind == A.AUV_PROBE_MFMA_BF16 else blocks * 256 * 8 * iters
+        out[name] = ops / t
+        out[name.replace("_per_s", "_ms")] = t * 1e3
+    return out
+
+
 SWEEP_ENVS = (64, 256, 1024, 4096, 8192, 16384, 32768, 65536)
 
 
@@ -439,7 +486,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c4", choices=["c3", "c4"])
-    ap.add_argument("--cpu-steps", type=int, default=50, help="oracle control steps for the CPU baseline (0: skip)")
+    ap.add_argument("--cpu-steps", type=int, default=100,
+                    help="oracle control steps for the CPU baseline, at most T (0: skip)")
     ap.add_argument("--no-c5", action="store_true", help="skip the PPO-buffer (c5) rollout and GAE measurement")
     ap.add_argument("--no-ppo", action="store_true", help="skip the PPO-update measurement")
     ap.add_argument("--ppo-only", action="store_true", help="only measure the PPO update and print it")
@@ -448,6 +496,8 @@ def main() -> int:
     ap.add_argument("--c5-only", action="store_true", help="only measure the PPO-buffer rollout and GAE (c5)")
     ap.add_argument("--sweep", action="store_true",
                     help="only measure the headline rollout at 64 to 65536 envs and print it")
+    ap.add_argument("--probe-rates", action="store_true",
+                    help="only measure the exp / rcp / fma / bf16 MFMA unit rates (auv_probe_rate) and print them")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -482,6 +532,9 @@ def main() -> int:
         return 0
     if args.sweep:
         print(json.dumps({"sweep": sweep_measure()}), flush=True)
+        return 0
+    if args.probe_rates:
+        print(json.dumps({"unit_rates": probe_rates()}), flush=True)
         return 0
     if args.shac_only:
         print(json.dumps({"shac": [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]}),
@@ -564,7 +617,7 @@ def main() -> int:
         line["paper_training"] = paper_training_measure()
         line["shac"] = [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]
     if args.cpu_steps > 0:
-        line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_steps)
+        line["cpu_baseline"] = cpu_baseline(cfg, min(args.cpu_steps, T))
     print(json.dumps(line), flush=True)
     return 0
 

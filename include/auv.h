@@ -213,6 +213,29 @@ int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float*
  * Environments are not reset on a non-finite state (their episode ends stay on schedule). */
 int auv_get_status(auv_env* env, uint32_t* nonfinite_count, uint32_t* abandoned_waits, void* stream);
 
+/* The kernels' own number conversions applied to n 32-bit words (device, caller-owned,
+ * 16-byte aligned), one output float per word, for checking them bit for bit against their
+ * definitions:
+ *   AUV_CONV_UNIFORM        (w >> 8) 2^-24, in [0, 1)            (every uniform draw)
+ *   AUV_CONV_UNIFORM_OPEN0  ((w >> 8) + 1) 2^-24, in (0, 1]     (the Box-Muller radius input)
+ *   AUV_CONV_AFFINE         lo + span (w >> 8) 2^-24 rounded once to fp32 (fused multiply-add;
+ *                           the randomisation draws, with their fp32 (lo, span))
+ *   AUV_CONV_BF16           the fp32 value with bits w rounded to bf16, nearest even (the
+ *                           conversion of every MLP layer input), widened back to fp32
+ * AUV_EINVAL, nothing enqueued: unknown kind, n outside [1, 2^31], NULL or misaligned buffers. */
+enum { AUV_CONV_UNIFORM = 0, AUV_CONV_UNIFORM_OPEN0 = 1, AUV_CONV_AFFINE = 2, AUV_CONV_BF16 = 3 };
+int auv_convert(int kind, int64_t n, const uint32_t* in, float lo, float span, float* out, void* stream);
+
+/* Throughput probe of the units that bound the fused rollout: `blocks` workgroups of 256
+ * threads, each lane running `iters` iterations of 8 independent chains of one instruction
+ * (AUV_PROBE_EXP: v_exp_f32, AUV_PROBE_RCP: v_rcp_f32, AUV_PROBE_FMA: v_fma_f32;
+ * AUV_PROBE_MFMA_BF16: v_mfma_f32_16x16x32_bf16, per wave).  The caller times the launch:
+ * lane operations = 256 blocks iters 8 (MFMA: blocks 4 iters 8 instructions of 16384 FLOP).
+ * sink: 256 blocks floats (device) that keep the results live.  AUV_EINVAL for an unknown
+ * kind, blocks outside [1, 2^20], iters < 1, a NULL or misaligned sink. */
+enum { AUV_PROBE_EXP = 0, AUV_PROBE_RCP = 1, AUV_PROBE_FMA = 2, AUV_PROBE_MFMA_BF16 = 3 };
+int auv_probe_rate(int kind, int32_t blocks, int32_t iters, float* sink, void* stream);
+
 /* Host-side step counter (Philox counter word 1 of action and noise draws); set it to
  * resume a saved run bit-exactly together with the state buffers. */
 int64_t auv_get_global_step(const auv_env* env);

@@ -21,6 +21,8 @@ AUV_F_DR, AUV_F_CURRENT, AUV_F_LISSAJOUS, AUV_F_STAGGER = 1, 2, 4, 8
 AUV_TASK_WORKLOAD, AUV_TASK_PAPER = 0, 1
 AUV_FLUID_FOSSEN, AUV_FLUID_INERTIA_BOX = 0, 1
 AUV_STATIC_STATS_FLOATS = 2 * 1024 * 1024
+AUV_CONV_UNIFORM, AUV_CONV_UNIFORM_OPEN0, AUV_CONV_AFFINE, AUV_CONV_BF16 = 0, 1, 2, 3
+AUV_PROBE_EXP, AUV_PROBE_RCP, AUV_PROBE_FMA, AUV_PROBE_MFMA_BF16 = 0, 1, 2, 3
 OBS_DIM, ACT_DIM, STATE_DIM, PARAM_DIM, HIDDEN, ENVS_PER_GROUP = 23, 8, 13, 24, 256, 64
 
 _f = ctypes.c_float
@@ -113,6 +115,8 @@ def _load() -> ctypes.CDLL:
         "auv_rollout": (ctypes.c_int, [_vp, i32, ctypes.c_int, P(AuvMlp), P(AuvMlp), P(AuvRolloutBuffers), _vp]),
         "auv_rollout_static": (ctypes.c_int, [_vp, i32, ctypes.c_int, P(AuvMlp), P(AuvMlp), P(AuvRolloutBuffers),
                                               _vp]),
+        "auv_convert": (ctypes.c_int, [ctypes.c_int, i64, _vp, _f, _f, _vp, _vp]),
+        "auv_probe_rate": (ctypes.c_int, [ctypes.c_int, i32, i32, _vp, _vp]),
         "auv_gae": (ctypes.c_int, [i32, i32, _vp, _vp, _vp, _vp, _f, _f, _vp, _vp, _vp]),
         "auv_mlp_forward": (ctypes.c_int, [P(AuvMlp), i32, _vp, _vp, _vp]),
         "auv_get_global_step": (i64, [_vp]),
@@ -205,6 +209,14 @@ def auv_rollout_static(h: int, T: int, mode: int, policy: AuvMlp | None = None, 
     _check(lib.auv_rollout_static(h, T, mode, None if policy is None else ctypes.byref(policy),
                                   None if value is None else ctypes.byref(value),
                                   None if rbufs is None else ctypes.byref(rbufs), stream_ptr(stream)))
+
+
+def auv_convert(kind: int, n: int, inp, lo: float, span: float, out, stream=None) -> None:
+    _check(lib.auv_convert(kind, n, ptr(inp), lo, span, ptr(out), stream_ptr(stream)))
+
+
+def auv_probe_rate(kind: int, blocks: int, iters: int, sink, stream=None) -> None:
+    _check(lib.auv_probe_rate(kind, blocks, iters, ptr(sink), stream_ptr(stream)))
 
 
 def auv_gae(T: int, n_envs: int, reward, value, done, last_value, gamma: float, lam: float,

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libauv.so")
-SOURCES = ["auv_env.hip", "auv_policy.hip", "ppo.hip", "shac.hip"]
+SOURCES = ["auv_env.hip", "auv_policy.hip", "ppo.hip", "shac.hip", "rate_probe.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -376,6 +376,26 @@ __global__ __launch_bounds__(1024) void k_gae_seg(int T, int n, const float* __r
   }
 }
 
+// The number conversions of the kernels, one per element, for checks against their
+// definitions (auv_convert): the same inline functions and the same bf16 cast.
+constexpr int CONV_UNIFORM = 0, CONV_UNIFORM_OPEN0 = 1, CONV_AFFINE = 2, CONV_BF16 = 3;
+__global__ __launch_bounds__(256) void k_convert(int kind, int64_t n, const uint32_t* __restrict__ in, float lo,
+                                                 float span, float* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const uint32_t w = in[i];
+    float v;
+    if (kind == CONV_UNIFORM)
+      v = u01(w);
+    else if (kind == CONV_UNIFORM_OPEN0)
+      v = u01_open0(w);
+    else if (kind == CONV_AFFINE)
+      v = affine(lo, span, u01(w));
+    else
+      v = (float)(__bf16)__uint_as_float(w);
+    out[i] = v;
+  }
+}
+
 int launch_stats_reduce(const float* work, int T, int G, float* stats, hipStream_t s) {
   hipLaunchKernelGGL(k_stats_reduce, dim3((3 * T + 63) / 64), dim3(64 * RED_WAVES), 0, s, work, T, G, stats);
   return check_launch("stats reduce");
@@ -779,6 +799,17 @@ int auv_gae(int32_t T, int32_t n_envs, const float* reward, const float* value, 
                        last_value, gamma, gamma * lambda, adv, ret);
   }
   return check_launch("auv_gae");
+}
+
+int auv_convert(int kind, int64_t n, const uint32_t* in, float lo, float span, float* out, void* stream) {
+  if (kind < CONV_UNIFORM || kind > CONV_BF16) return set_error(AUV_EINVAL, "auv_convert: unknown kind %d", kind);
+  if (n < 1 || n > ((int64_t)1 << 31)) return set_error(AUV_EINVAL, "auv_convert: n must be in [1, 2^31]");
+  if (!in || !out || !aligned16(in) || !aligned16(out))
+    return set_error(AUV_EINVAL, "auv_convert: buffers must be non-NULL and 16-byte aligned");
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(k_convert, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0, (hipStream_t)stream,
+                     kind, n, in, lo, span, out);
+  return check_launch("auv_convert");
 }
 
 int auv_mlp_forward(const auv_mlp* net, int32_t n_envs, const float* obs, float* out, void* stream) {
