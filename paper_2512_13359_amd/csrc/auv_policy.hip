@@ -382,72 +382,143 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
   report_status(E.status, valid ? nf + quad::nonfinite_quad(c, X) : 0u, (abandoned && lane == 0) ? 1u : 0u);
 }
 
-// Stand-alone MLP forward over obs [23][n] -> out [n_out][n]: workgroups of four MLP waves
-// (64 hidden features each, weights in registers, mlp_tile.hpp), two per CU, persistent
-// over 16-environment tiles.  Each wave builds the tile's layer-1 operand straight from
-// HBM (the next tile's loads are issued before this tile's math); hidden 1 and the output
-// partials meet in LDS with two barriers per tile.
-constexpr int FWD_WAVES = 4;
-constexpr int FWD_THREADS = 64 * FWD_WAVES;
+// Stand-alone MLP forward over obs [23][n] -> out [n_out][n] (auv_mlp_forward and the value
+// head of a rollout): one workgroup of MLPW_WAVES waves per CU, persistent.  The network's bf16
+// weights sit in LDS in MFMA A-operand order (152 KB), and each wave runs the whole network
+// on groups of MLPW_NT 16-sample tiles on its own: no exchange and no barrier in the loop,
+// and every weight fragment read from LDS feeds MLPW_NT MFMAs.  Per group and wave: layer 1
+// (16 M-tiles x 1 K step), the 256 hidden-1 activations as the eight K-tile fragments of the
+// next layer (act_frag), then per pair of layer-2 M-tiles its 8 K steps, the pair's
+// activations as one hidden-2 K-tile fragment and at once its layer-3 MFMA.  The next
+// group's inputs are loaded while this group's layers 2 and 3 run.
+constexpr int MLPW_WAVES = 8;
+constexpr int MLPW_NT = 2;   // 16-sample tiles per wave and group
 
-__global__ __launch_bounds__(FWD_THREADS, 2) void k_mlp(const uint16_t* __restrict__ w, const float* __restrict__ b,
-                                                        int n_out, int n, const float* __restrict__ obs,
-                                                        float* __restrict__ out) {
-  __shared__ bf16x8 h[8][64];                     // hidden-1 operand of the tile [K tile][lane]
-  __shared__ float mu[FWD_WAVES][16][NOUT_PAD];   // output partials [wave][env][row]
-  __shared__ float b1k[HID];
-  __shared__ float b3[16];
+struct MlpWideShared {
+  bf16x8 w1[16][64];      // layer 1 [M-tile][lane] (K = the 32 padded inputs)
+  bf16x8 w2[16][8][64];   // layer 2 [M-tile][K step][lane]
+  bf16x8 w3[8][64];       // layer 3 [K step][lane] (rows = outputs, n_out of 16 used)
+  float b1k[HID];         // hidden-1 biases x 2 log2 e
+  float b2k[HID];         // hidden-2 biases x 2 log2 e
+  float b3[16];
+};
+
+__global__ __launch_bounds__(64 * MLPW_WAVES, 2) void k_mlp(const uint16_t* __restrict__ w,
+                                                           const float* __restrict__ b, int n_out, int n,
+                                                           const float* __restrict__ obs, float* __restrict__ out) {
+  __shared__ MlpWideShared S;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
-  TileMlpRegs<64> R;
-  tile_mlp_load<64>(w, b, n_out, m, lane, R);
-  if (tid < HID) b1k[tid] = b[tid] * TWO_LOG2E;
-  if (tid < 16) b3[tid] = tid < n_out ? b[2 * HID + tid] : 0.0f;
+  {   // weights -> A fragments: lane (g, r) of fragment (M-tile mt, K step kt) holds row
+      // 16 mt + r, inputs 32 kt + kslot(g, j)
+    const uint16_t* W1 = w;
+    const uint16_t* W2 = w + HID * 23;
+    const uint16_t* W3 = W2 + HID * HID;
+    constexpr int F1 = 16, F2 = 16 * 8, F3 = 8;
+    for (int e = tid; e < (F1 + F2 + F3) * 64; e += 64 * MLPW_WAVES) {
+      const int f = e >> 6, l = e & 63, lg = l >> 4, lr = l & 15;
+      bf16x8 v;
+      if (f < F1) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int k = kslot(lg, j);
+          v[j] = k < 23 ? bf16_of_bits(W1[(16 * f + lr) * 23 + k]) : bf16_of_bits(0);
+        }
+        S.w1[f][l] = v;
+      } else if (f < F1 + F2) {
+        const int mt = (f - F1) >> 3, kt = (f - F1) & 7;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = bf16_of_bits(W2[(16 * mt + lr) * HID + 32 * kt + kslot(lg, j)]);
+        S.w2[mt][kt][l] = v;
+      } else {
+        const int kt = f - F1 - F2;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          v[j] = lr < n_out ? bf16_of_bits(W3[lr * HID + 32 * kt + kslot(lg, j)]) : bf16_of_bits(0);
+        S.w3[kt][l] = v;
+      }
+    }
+    for (int i = tid; i < HID; i += 64 * MLPW_WAVES) {
+      S.b1k[i] = b[i] * TWO_LOG2E;
+      S.b2k[i] = b[HID + i] * TWO_LOG2E;
+    }
+    if (tid < 16) S.b3[tid] = tid < n_out ? b[2 * HID + tid] : 0.0f;
+  }
   __syncthreads();
+
   const size_t N = (size_t)n;
   const int tiles = (n + 15) / 16;
-  // This lane's 8 layer-1 operand values of a tile: unconditional loads from a clamped,
-  // valid address (so that they stay in flight while the previous tile is computed), masked
-  // to zero when converted.
-  struct XRaw { float v[8]; };
-  auto load_x = [&](int tile) {
+  const int groups = (tiles + MLPW_NT - 1) / MLPW_NT;
+  const int stride = gridDim.x * MLPW_WAVES;
+  // This lane's 8 layer-1 inputs of each tile of a group: unconditional loads from clamped,
+  // valid addresses (so that they stay in flight), masked to zero when converted.
+  struct XRaw { float v[MLPW_NT][8]; };
+  auto load_x = [&](int grp) {
     XRaw x;
-    const int i = min(tile * 16 + r, n - 1);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x.v[j] = obs[min(kslot(g, j), OBS - 1) * N + i];
+    for (int nt = 0; nt < MLPW_NT; ++nt) {
+      const int i = min((grp * MLPW_NT + nt) * 16 + r, n - 1);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x.v[nt][j] = obs[min(kslot(g, j), OBS - 1) * N + i];
+    }
     return x;
   };
-  auto to_operand = [&](const XRaw& x, int tile) {
-    bf16x8 o;
-    const bool ok = tile < tiles && tile * 16 + r < n;
+  int grp = blockIdx.x * MLPW_WAVES + wave;
+  XRaw xr = load_x(min(grp, groups - 1));
+  for (; grp < groups; grp += stride) {
+    bf16x8 x[MLPW_NT];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = (__bf16)((ok && kslot(g, j) < OBS) ? x.v[j] : 0.0f);
-    return o;
-  };
-  XRaw xr = load_x(blockIdx.x);
-  for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-    const bf16x8 x = to_operand(xr, tile);
-    xr = load_x(tile + gridDim.x);   // next tile, in flight during this one
-    bf16x8 own[2];
-    tile_layer1<64>(R, x, b1k, m, lane, own);
-    h[2 * m][lane] = own[0];
-    h[2 * m + 1][lane] = own[1];
-    f32x4 acc[4];
-    tile_layer2_own<64>(R, own, acc);
-    __syncthreads();                              // h complete
-    const f32x4 o = tile_layer23<64>(R, acc, [&](int kt) { return h[kt][lane]; }, m);
-    if (g < 2) *reinterpret_cast<f32x4*>(&mu[m][r][4 * g]) = o;
-    __syncthreads();                              // mu complete; h free for the next tile
-    if (m == 0) {                                 // rows g and g + 4 of env r, partials in wave order
-      const int i = tile * 16 + r;
+    for (int nt = 0; nt < MLPW_NT; ++nt) {
+      const bool ok = (grp * MLPW_NT + nt) * 16 + r < n;
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int row = g + 4 * hh;
-        float y = mu[0][r][row];
+      for (int j = 0; j < 8; ++j) x[nt][j] = (__bf16)((ok && kslot(g, j) < OBS) ? xr.v[nt][j] : 0.0f);
+    }
+    // layer 1: the hidden-1 K-tile fragments h1[kt] (M-tiles 2 kt, 2 kt + 1)
+    bf16x8 h1[8][MLPW_NT];
 #pragma unroll
-        for (int q = 1; q < FWD_WAVES; ++q) y += mu[q][r][row];
-        if (row < n_out && i < n) out[row * N + i] = b3[row] + y;
+    for (int kt = 0; kt < 8; ++kt) {
+      const bf16x8 a0 = S.w1[2 * kt][lane], a1 = S.w1[2 * kt + 1][lane];
+      const f32x4 ba = *reinterpret_cast<const f32x4*>(&S.b1k[32 * kt + 4 * g]);
+      const f32x4 bb = *reinterpret_cast<const f32x4*>(&S.b1k[32 * kt + 16 + 4 * g]);
+#pragma unroll
+      for (int nt = 0; nt < MLPW_NT; ++nt)
+        h1[kt][nt] = act_frag(mfma(a0, x[nt], f32x4{0, 0, 0, 0}), mfma(a1, x[nt], f32x4{0, 0, 0, 0}), ba, bb);
+      __builtin_amdgcn_sched_barrier(0);   // one K tile at a time: bounds the live accumulators
+    }
+    xr = load_x(min(grp + stride, groups - 1));   // the next group, in flight during layers 2 and 3
+    // layers 2 and 3, one pair of layer-2 M-tiles (= one hidden-2 K tile) at a time
+    f32x4 o[MLPW_NT];
+#pragma unroll
+    for (int nt = 0; nt < MLPW_NT; ++nt) o[nt] = f32x4{0, 0, 0, 0};
+#pragma unroll 1
+    for (int k2 = 0; k2 < 8; ++k2) {
+      f32x4 c0[MLPW_NT], c1[MLPW_NT];
+#pragma unroll
+      for (int nt = 0; nt < MLPW_NT; ++nt) c0[nt] = c1[nt] = f32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int kt = 0; kt < 8; ++kt) {
+        const bf16x8 a0 = S.w2[2 * k2][kt][lane], a1 = S.w2[2 * k2 + 1][kt][lane];
+#pragma unroll
+        for (int nt = 0; nt < MLPW_NT; ++nt) {
+          c0[nt] = mfma(a0, h1[kt][nt], c0[nt]);
+          c1[nt] = mfma(a1, h1[kt][nt], c1[nt]);
+        }
+      }
+      const f32x4 ba = *reinterpret_cast<const f32x4*>(&S.b2k[32 * k2 + 4 * g]);
+      const f32x4 bb = *reinterpret_cast<const f32x4*>(&S.b2k[32 * k2 + 16 + 4 * g]);
+      const bf16x8 a3 = S.w3[k2][lane];
+#pragma unroll
+      for (int nt = 0; nt < MLPW_NT; ++nt) o[nt] = mfma(a3, act_frag(c0[nt], c1[nt], ba, bb), o[nt]);
+    }
+    // lane (g, r) holds output rows 4 g .. 4 g + 3 of sample r of each tile
+#pragma unroll
+    for (int nt = 0; nt < MLPW_NT; ++nt) {
+      const int i = (grp * MLPW_NT + nt) * 16 + r;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int row = 4 * g + q;
+        if (row < n_out && i < n) out[row * N + i] = S.b3[row] + o[nt][q];
       }
     }
   }
@@ -464,15 +535,17 @@ static int check_mlp(const auv_mlp* net, int n_out_want, const char* what) {
   return AUV_OK;
 }
 
-static int mlp_grid(int n) {   // two resident workgroups per CU
-  const int tiles = (n + 15) / 16;
-  return tiles < 512 ? tiles : 512;
+static int mlp_grid(int n) {   // one workgroup per CU (its weights fill the LDS)
+  const int groups = ((n + 15) / 16 + MLPW_NT - 1) / MLPW_NT;
+  const int wgs = (groups + MLPW_WAVES - 1) / MLPW_WAVES;
+  const int cus = compute_units();
+  return wgs < cus ? wgs : cus;
 }
 
 int launch_mlp_forward(const auv_mlp* net, int n, const float* obs, float* out, hipStream_t s) {
   if (int rc = check_mlp(net, 0, "auv_mlp_forward")) return rc;
-  hipLaunchKernelGGL(k_mlp, dim3(mlp_grid(n)), dim3(FWD_THREADS), 0, s, (const uint16_t*)net->w, net->b, net->n_out, n,
-                     obs, out);
+  hipLaunchKernelGGL(k_mlp, dim3(mlp_grid(n)), dim3(64 * MLPW_WAVES), 0, s, (const uint16_t*)net->w, net->b,
+                     net->n_out, n, obs, out);
   return check_launch("auv_mlp_forward");
 }
 
