@@ -29,11 +29,12 @@ F_MFMA = 2 * (23 * 256 + 256 * 256 + 256 * 8)      # 146,944
 F_VALU = 4815
 N_TRANS = 1024
 # MI355X peaks: published dense bf16 MFMA and fp32 vector rates; transcendentals
-# (v_exp_f32, v_rcp_f32) issue at half the fp32 lane rate on gfx950 (8 cycles per wave64
-# instruction, measured): 256 CU x 4 SIMD x 16 lanes x 2.4 GHz / 2.
+# (v_exp_f32, v_rcp_f32) issue at a quarter of the fp32 FMA lane rate, 8 lanes per SIMD per
+# clock: 256 CU x 4 SIMD x 8 lanes x 2.4 GHz (auv_probe_rate measures 0.86 of it,
+# profiles/unit_rate_probe.txt).
 P_MFMA = 2.5e15
 P_VALU = 157.3e12
-P_TRANS = 256 * 4 * 16 * 2.4e9 / 2
+P_TRANS = 256 * 4 * 8 * 2.4e9
 HBM_PEAK = 8.0e12
 
 # The translation unit of the rollout kernel (auv_policy.hip and everything it includes).
@@ -379,7 +380,8 @@ def shac_measure(n_envs: int, reps: int = 16) -> dict:
 
 def small_configs_measure(reps: int = 3) -> dict:
     """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
-    4096 envs occupy 64 of the 256 CUs, so these are occupancy-capped by N."""
+    4096 envs are 256 one-wave blocks of the quad-layout loop (c2) or 256 one-tile workgroups of
+    the fused rollout (c3): a quarter of the SIMDs carry physics, so both are capped by N."""
     import torch
 
     import workloads as W
@@ -566,7 +568,9 @@ def main() -> int:
     value = env_steps * args.steps / wall
     per_env_step_s = launch_s / env_steps
     t_lb = F_MFMA / P_MFMA + F_VALU / P_VALU + N_TRANS / P_TRANS
-    f_alg = F_MFMA + F_VALU
+    # the bound's work in bf16-MFMA-equivalent FLOP: each unit's work scaled to the time it
+    # takes at its peak, expressed at the MFMA peak (so peak = the published 2.5 PFLOP/s)
+    f_eq = t_lb * P_MFMA
     traffic = recorded_traffic()
     line = {
         "metric": METRIC,
@@ -591,13 +595,17 @@ def main() -> int:
         },
         "roofline": {
             "bound": "alu",
-            "achieved": f_alg / per_env_step_s / 1e12,
-            "peak": f_alg / t_lb / 1e12,
+            "achieved": f_eq / per_env_step_s / 1e12,
+            "peak": P_MFMA / 1e12,
             "unit": "TFLOP/s",
+            "unit_note": "bf16-MFMA-equivalent: per env-step MFMA FLOP + fp32 VALU FLOP x (2500/157.3) + "
+                         "transcendentals x (2500/19.66), the sum-of-units bound at the MFMA peak",
             "frac": t_lb / per_env_step_s,
             "traffic": traffic,
             "kernel": "k_policy_rollout",
             "launch_ms": launch_s * 1e3,
+            "unit_peaks": {"mfma_bf16_tflops": P_MFMA / 1e12, "valu_fp32_tflops": P_VALU / 1e12,
+                           "trans_tops": P_TRANS / 1e12},
             "per_env_step": {"mfma_flop": F_MFMA, "valu_flop": F_VALU, "trans_ops": N_TRANS},
             "unit_utilisation": {
                 "mfma": F_MFMA / per_env_step_s / P_MFMA,
