@@ -172,7 +172,9 @@ __device__ __forceinline__ void rollout_mlp_wave(RolloutShared& S, int T, const 
 // quad_env.hpp).  Each tile runs its own chain obs -> MLP -> action -> physics -> obs,
 // ordered by LDS counters instead of workgroup barriers, so the physics of one tile
 // overlaps the MLP of the others; with four tiles every SIMD holds one wave of each kind.
-template <bool SAMPLE, int TPW, bool PAPER>
+// REC: per-step records are requested (obs, act, logp, reward, done, traj); without them the
+// loop tests none of those pointers (the statistics workspace is tested either way).
+template <bool SAMPLE, int TPW, bool PAPER, bool REC>
 __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(VehArgs V, EnvArgs E, int T, uint32_t gstep0,
                                                            StepOut O, const uint16_t* __restrict__ w,
                                                            const float* __restrict__ b,
@@ -217,7 +219,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     sig1 = expf(lsd1);
   }
   auto store_traj = [&](int t1) {
-    if (O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)t1 * N + i, c, X);
+    if (REC && O.traj && valid) quad::store_state(O.traj, (size_t)(T + 1) * N, (size_t)t1 * N + i, c, X);
   };
   store_traj(0);
   StatsBuf SB{};
@@ -235,7 +237,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       reward = -pv_dist - 0.5f * theta - 0.01f * pv_usq;
     }
     const size_t t1i = (size_t)t1 * N + (size_t)i;
-    if (valid && c == 0) {
+    if (REC && valid && c == 0) {
       if (O.reward) O.reward[t1i] = reward;
       if (O.done) O.done[t1i] = pv_done ? 1.0f : 0.0f;
       if (O.done_u8) O.done_u8[i] = pv_done ? 1 : 0;
@@ -269,7 +271,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
     quad::QRefCols rc;
     if (!PAPER) rc = quad::ref_columns(K, qr);
     if (t > 0) finish_step(t - 1);
-    if (O.obs && valid) quad::store_obs<PAPER>(O.obs, TN, ti, c, X, false);   // o_t, recorded while the MLP waves work on it
+    if (REC && O.obs && valid) quad::store_obs<PAPER>(O.obs, TN, ti, c, X, false);   // o_t, recorded while the MLP waves work on it
     if (!wait_for(&S.mu_ready[k], (unsigned)ROLLOUT_MLP_WAVES * (unsigned)(t + 1), E.sync_polls)) {   // abandoned: poison
       X.p = X.q = X.v = X.om = __builtin_nanf("");
       abandoned = true;
@@ -323,7 +325,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       a0 = __builtin_fmaf(sig0, e0, a0);
       a1 = __builtin_fmaf(sig1, e1, a1);
     }
-    if (O.act && valid && acts) {
+    if (REC && O.act && valid && acts) {
       O.act[ra0 * TN + ti] = a0;
       O.act[ra1 * TN + ti] = a1;
     }
@@ -369,7 +371,7 @@ __global__ __launch_bounds__(rollout_threads<TPW>(), 1) void k_policy_rollout(Ve
       put_obs_quad(S, k, slot, c, X.ob, X.v, X.om, X.u0, X.u1);
     publish(&S.obs_ready[k], lane);
     // outputs of step t that the next observation does not need
-    if (SAMPLE && O.logp) {   // lane 3 of the paper task adds zeros
+    if (SAMPLE && REC && O.logp) {   // lane 3 of the paper task adds zeros
       const float lp = quad::qsum((-0.5f * e0 * e0 - lsd0) + (-0.5f * e1 * e1 - lsd1)) -
                        (PAPER ? 3.0f : 4.0f) * 1.83787706640934548f;
       if (valid && c == 0) O.logp[ti] = lp;
@@ -562,19 +564,29 @@ int rollout_stats_groups(int n) {   // one partial per workgroup
   return (n + 16 * tpw - 1) / (16 * tpw);
 }
 
+template <bool SAMPLE, bool PAPER, bool REC>
+static void launch_rollout_tpw(int tpw, int n, hipStream_t s, const VehArgs& V, const EnvArgs& E, int T, uint32_t g0,
+                               const StepOut& O, const uint16_t* w, const float* b, const float* log_std) {
+  const dim3 grid((n + 16 * tpw - 1) / (16 * tpw));
+  if (tpw == 4)
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 4, PAPER, REC>), grid, dim3(rollout_threads<4>()), 0, s, V, E, T, g0,
+                       O, w, b, log_std);
+  else if (tpw == 2)
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 2, PAPER, REC>), grid, dim3(rollout_threads<2>()), 0, s, V, E, T, g0,
+                       O, w, b, log_std);
+  else
+    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 1, PAPER, REC>), grid, dim3(rollout_threads<1>()), 0, s, V, E, T, g0,
+                       O, w, b, log_std);
+}
+
 template <bool SAMPLE, bool PAPER>
 static void launch_rollout_kernel(int tpw, int n, hipStream_t s, const VehArgs& V, const EnvArgs& E, int T, uint32_t g0,
                                   const StepOut& O, const uint16_t* w, const float* b, const float* log_std) {
-  const dim3 grid((n + 16 * tpw - 1) / (16 * tpw));
-  if (tpw == 4)
-    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 4, PAPER>), grid, dim3(rollout_threads<4>()), 0, s, V, E, T, g0, O,
-                       w, b, log_std);
-  else if (tpw == 2)
-    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 2, PAPER>), grid, dim3(rollout_threads<2>()), 0, s, V, E, T, g0, O,
-                       w, b, log_std);
+  const bool rec = O.obs || O.act || O.logp || O.reward || O.done || O.done_u8 || O.traj;
+  if (rec)
+    launch_rollout_tpw<SAMPLE, PAPER, true>(tpw, n, s, V, E, T, g0, O, w, b, log_std);
   else
-    hipLaunchKernelGGL((k_policy_rollout<SAMPLE, 1, PAPER>), grid, dim3(rollout_threads<1>()), 0, s, V, E, T, g0, O,
-                       w, b, log_std);
+    launch_rollout_tpw<SAMPLE, PAPER, false>(tpw, n, s, V, E, T, g0, O, w, b, log_std);
 }
 
 int launch_policy_rollout(auv_env* env, int T, int mode, const auv_mlp* policy, const auv_mlp* value,
