@@ -76,6 +76,10 @@ struct Work {
   float* part_b1;       // [G][256]
   float* part_w2;       // [G][256 m][256 k]
   float* part_ss;       // [2 nets][reduce blocks]
+  // value-only gradient (k_vtile / k_vwgrad): half fragments of one minibatch
+  u32x2* h1_half;       // [Bp/16][16 feature tiles][64 lanes] q(h1)
+  u32x2* dz1_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz1)
+  u32x2* x_half;        // [Bp/16][2 input tiles][64 lanes] q(x)
 };
 
 constexpr int MAX_GROUPS = 256;
@@ -91,14 +95,15 @@ inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * H
 inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_ELEMS; }
 
 // Byte offsets of the workspace parts for a minibatch of B; returns the total.
-constexpr int WORK_PARTS = 13;
+constexpr int WORK_PARTS = 16;
 inline size_t work_layout(int B, size_t off[WORK_PARTS]) {
   const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
   const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS,
                             Bp * HID * 2, Bp * HID * 2,
                             G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
                             G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
-                            2 * (size_t)red_blocks(8) * 4};
+                            2 * (size_t)red_blocks(8) * 4,
+                            Bp * HID * 2, Bp * HID * 2, Bp * 32 * 2};
   size_t o = 0;
   for (int k = 0; k < WORK_PARTS; ++k) {
     off[k] = o;
@@ -125,6 +130,9 @@ inline Work work_at(void* base, int B) {
   W.part_b1 = (float*)(p + off[10]);
   W.part_w2 = (float*)(p + off[11]);
   W.part_ss = (float*)(p + off[12]);
+  W.h1_half = (u32x2*)(p + off[13]);
+  W.dz1_half = (u32x2*)(p + off[14]);
+  W.x_half = (u32x2*)(p + off[15]);
   return W;
 }
 
@@ -792,6 +800,447 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
       for (int nt = 0; nt < 8; ++nt) out[(64 * mr + 16 * mt + 4 * g + i) * HID + 128 * nc + 16 * nt + r] = acc[mt][nt][i];
 }
 
+// ------------------------------------------------------------------ value-only gradient ---
+// The value network's gradient on one minibatch, for the value-only fits of SHAC's critic,
+// in two kernels and without a 256 x 256 partial per tile workgroup:
+//   k_vtile   one wave per 16-sample tile, the network's bf16 weights in LDS: forward, squared
+//             error, dz2 and dz1 (tanh derivatives from the fp32 activations); db1, db2, dW3,
+//             db3 and the error sum per workgroup; q(x), q(h1), q(dz2), q(dz1) stored as half
+//             fragments (lane (g, r): feature r of a 16-feature tile, samples 4 g .. 4 g + 3)
+//   k_vwgrad  dW2 = q(dz2) q(h1)^T and dW1 = q(dz1) q(x)^T, a product over the samples, one
+//             partial per chunk of the minibatch
+// then k_reduce (and with it the fused Adam step) as for the other gradients.
+//
+// Layer 1 runs feature-major (D = W1 X: lane (g, r) gets features 4 g + i of an M-tile at
+// sample r, pairs of which are the next layer's operand, as in the rollout).  Layer 2 runs
+// sample-major (D = q(H1)^T W2^T, the layer-1 pairs as the A operand and the W2 fragments as
+// the B operand): lane (g, r) gets z2 feature r of a 16-feature tile at samples 4 g + i, so
+// that the sums over samples of the bias and output-weight gradients are in-lane and the
+// tile's values are already half fragments.  The input gradient dh1 = W2^T q(dz2) is
+// sample-major too, with A = q(dz2) in the feature-major pair layout and B = W2 indexed
+// [z2 feature][h1 feature], which ds_read_b64_tr_b16 reads out of the forward's fragments.
+// A 16 x 16 block changes layout through an MFMA with a 0/1 selection matrix, which is
+// exact (one nonzero product per output).
+constexpr int VT_WAVES = 8;
+constexpr int VW_WAVES = 8;
+constexpr int VW_MAX_CHUNKS = 64;
+
+struct VtWeights {
+  bf16x8 w1[16][64];      // layer 1 A fragments [M-tile][lane] (K = the 32 padded inputs)
+  bf16x8 w2[16][8][64];   // layer 2 A fragments [M-tile][K tile][lane]
+  float w3[HID];          // output weights (bf16 values)
+  float b1k[HID];         // hidden-1 biases x 2 log2 e
+  float b2k[HID];         // hidden-2 biases x 2 log2 e
+};
+union VtShared {
+  VtWeights s;
+  struct {
+    float v[VT_WAVES][3][HID];   // [wave][db1, db2, dW3][feature]
+    float sc[VT_WAVES][2][4];    // [wave][db3, squared error][lane row g]
+  } red;
+};
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// ds_read_b64_tr_b16: within each 16-lane group, lane 16 b + 4 a + c receives as its element
+// e the element c of the four 16-bit values that lane 16 b + 4 e + a addresses.
+__device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// LDS slot of lane l's 16 bytes in a W2 fragment: l XOR 4 (l / 16).  The forward reads (16
+// lanes at a time, 16 bytes each) stay on distinct banks, and the transposing reads below, whose
+// four source lanes 16 apart address slots 16 apart, no longer all meet on one bank.
+__device__ __forceinline__ int w2_slot(int l) { return l ^ (4 * (l >> 4)); }
+
+// B fragment of the sample-major input gradient: lane (g, r) gets W2[32 kt + kslot(g, j)]
+// [16 nt + r].  Forward fragment w2[m][k][l] lane l = (g', r') holds W2[16 m + r'][32 k +
+// kslot(g', j')] (at slot w2_slot(l)); this lane, as the source lane 16 sg + 4 se + sa of the
+// transposing read, addresses W2[32 kt + 16 h + 4 sg + se][16 nt + 4 sa .. + 3], the half
+// (nt odd) of lane 16 sa + 4 sg + se of fragment (2 kt + h, nt / 2).
+__device__ __forceinline__ bf16x8 w2t_frag(const bf16x8 (*w2)[8][64], int kt, int nt, int lane) {
+  const int src = w2_slot(16 * (lane & 3) + 4 * (lane >> 4) + ((lane >> 2) & 3));
+  const char* p0 = reinterpret_cast<const char*>(&w2[2 * kt][nt >> 1][src]) + 8 * (nt & 1);
+  const char* p1 = reinterpret_cast<const char*>(&w2[2 * kt + 1][nt >> 1][src]) + 8 * (nt & 1);
+  return join(lds_read_tr16(p0), lds_read_tr16(p1));
+}
+
+// The 0/1 selection operand: lane (g, r) holds 1 in slot 4 h + r % 4 when g = r / 4.  As B
+// with a feature-major pair as A it picks features 16 h + n (pair -> half fragments); as B
+// with a half fragment (slots 4..7 zero) as A it gives the feature-major D layout.
+__device__ __forceinline__ bf16x8 select_frag(int g, int r, int h) {
+  bf16x8 f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (__bf16)((g == (r >> 2) && j == 4 * h + (r & 3)) ? 1.0f : 0.0f);
+  return f;
+}
+
+// Reduce-scatter over the four lane rows: afterwards lane (g, r) holds in out[k] the sum over
+// the rows of v[4 g + k], added in the order (v_g + v_(g^2)) + (v_(g^1) + v_(g^3)).
+__device__ __forceinline__ void rows_reduce_scatter(const float v[16], float out[4], int g) {
+  float w[8];
+  const bool hi = g >= 2, odd = g & 1;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const float keep = hi ? v[k + 8] : v[k], send = hi ? v[k] : v[k + 8];
+    w[k] = keep + __shfl_xor(send, 32);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float keep = odd ? w[k + 4] : w[k], send = odd ? w[k] : w[k + 4];
+    out[k] = keep + __shfl_xor(send, 16);
+  }
+}
+
+__device__ __forceinline__ u32x2 pack4(const f32x4& v) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  bf16x4 q;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) q[i] = (__bf16)v[i];
+  return __builtin_bit_cast(u32x2, q);
+}
+
+__global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __restrict__ w, const float* __restrict__ b,
+                                                            Batch D, const int32_t* __restrict__ idx, int B, int tiles,
+                                                            Hp hp, Work W) {
+  __shared__ VtShared U;
+  VtWeights& S = U.s;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  const int Mi = (int)D.M;
+  const size_t M = D.M;
+  // inputs of a tile: this lane's 8 layer-1 inputs of sample r and the returns of samples
+  // 4 g .. 4 g + 3 (unconditional loads from clamped entries, masked on use)
+  struct In {
+    float x[8], rt[4];
+  };
+  auto load_in = [&](int t) __attribute__((always_inline)) {
+    In in;
+    const size_t sr = (size_t)clamp_sample(raw_index(idx, t, r, B), Mi);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(g, j), 22) * M + sr];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) in.rt[i] = D.ret[clamp_sample(raw_index(idx, t, 4 * g + i, B), Mi)];
+    return in;
+  };
+  int t = blockIdx.x * VT_WAVES + wave;
+  const int stride = gridDim.x * VT_WAVES;
+  In cur = load_in(min(t, tiles - 1));   // in flight while the weights are staged
+  {   // weights -> A fragments (lane (g, r) of fragment (M-tile, K tile) holds row 16 mt + r,
+      // inputs 32 kt + kslot(g, j)); every load is issued before the first LDS store, so that
+      // the staging costs about one memory latency
+    const uint16_t* W1 = w;
+    const uint16_t* W2 = w + HID * 23;
+    const uint16_t* W3 = W2 + HID * HID;
+    constexpr int P2 = 16 * 8 * 64 / (64 * VT_WAVES), P1 = 16 * 64 / (64 * VT_WAVES);
+    uint2 v2[P2][2];
+    uint16_t v1[P1][8];
+#pragma unroll
+    for (int q = 0; q < P2; ++q) {   // W2 row 16 mt + r, columns 32 kt + 4 g .. + 3 and + 16
+      const int e = tid + q * 64 * VT_WAVES, f = e >> 6, l = e & 63;
+      const uint16_t* row = W2 + (16 * (f >> 3) + (l & 15)) * HID + 32 * (f & 7) + 4 * (l >> 4);
+      v2[q][0] = *reinterpret_cast<const uint2*>(row);
+      v2[q][1] = *reinterpret_cast<const uint2*>(row + 16);
+    }
+#pragma unroll
+    for (int q = 0; q < P1; ++q) {
+      const int e = tid + q * 64 * VT_WAVES, f = e >> 6, l = e & 63;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = kslot(l >> 4, j);
+        v1[q][j] = k < 23 ? W1[(16 * f + (l & 15)) * 23 + k] : (uint16_t)0;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < P2; ++q) {
+      const int e = tid + q * 64 * VT_WAVES, f = e >> 6, l = e & 63;
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      S.w2[f >> 3][f & 7][w2_slot(l)] = __builtin_bit_cast(bf16x8, u32x4{v2[q][0].x, v2[q][0].y, v2[q][1].x, v2[q][1].y});
+    }
+#pragma unroll
+    for (int q = 0; q < P1; ++q) {
+      const int e = tid + q * 64 * VT_WAVES, f = e >> 6, l = e & 63;
+      bf16x8 v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = bf16_of_bits(v1[q][j]);
+      S.w1[f][l] = v;
+    }
+    for (int i = tid; i < HID; i += 64 * VT_WAVES) {
+      S.w3[i] = (float)bf16_of_bits(W3[i]);
+      S.b1k[i] = b[i] * TWO_LOG2E;
+      S.b2k[i] = b[HID + i] * TWO_LOG2E;
+    }
+  }
+  const float b3 = b[2 * HID];
+  const bf16x8 I0 = select_frag(g, r, 0), I1 = select_frag(g, r, 1);
+  const f32x4 zero = f32x4{0, 0, 0, 0};
+  const int w2s = w2_slot(lane);
+  // db1, db2 and dW3 of features 16 (4 g + k) + r, k = 0..3 (see rows_reduce_scatter)
+  float sb1[4] = {0, 0, 0, 0}, sb2[4] = {0, 0, 0, 0}, sw3[4] = {0, 0, 0, 0};
+  float db3 = 0.0f, sq = 0.0f;
+  __syncthreads();
+
+  for (; t < tiles; t += stride) {
+    const In nxt = load_in(min(t + stride, tiles - 1));
+    const size_t tb = (size_t)t * 16;
+    const bool vr = t * 16 + r < B;
+    bf16x8 x;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = (__bf16)((vr && kslot(g, j) < 23) ? cur.x[j] : 0.0f);
+    W.x_half[((size_t)t * 2) * 64 + lane] = pack4(mfma(x, I0, zero));
+    W.x_half[((size_t)t * 2 + 1) * 64 + lane] = pack4(mfma(x, I1, zero));
+
+    // ---- layer 1, feature-major: the pairs h1[kt] (features 32 kt + kslot(g, j), sample r)
+    bf16x8 h1[8];
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt) {
+      const f32x4 ba = *reinterpret_cast<const f32x4*>(&S.b1k[32 * kt + 4 * g]);
+      const f32x4 bb = *reinterpret_cast<const f32x4*>(&S.b1k[32 * kt + 16 + 4 * g]);
+      h1[kt] = act_frag(mfma(S.w1[2 * kt][lane], x, zero), mfma(S.w1[2 * kt + 1][lane], x, zero), ba, bb);
+    }
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt) {
+      W.h1_half[(tb + 2 * kt) * 64 + lane] = pack4(mfma(h1[kt], I0, zero));
+      W.h1_half[(tb + 2 * kt + 1) * 64 + lane] = pack4(mfma(h1[kt], I1, zero));
+    }
+
+    // ---- layer 2, sample-major (z2 feature 16 nt + r, samples 4 g + i), and the value
+    // (the next feature tile's eight weight fragments are read during this one's products)
+    f32x4 h2[16];
+    float yp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    bf16x8 wf[2][8];
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt) wf[0][kt] = S.w2[0][kt][w2s];
+#pragma unroll
+    for (int nt = 0; nt < 16; ++nt) {
+      if (nt + 1 < 16) {
+#pragma unroll
+        for (int kt = 0; kt < 8; ++kt) wf[(nt + 1) & 1][kt] = S.w2[nt + 1][kt][w2s];
+      }
+      f32x4 acc = zero;
+#pragma unroll
+      for (int kt = 0; kt < 8; ++kt) acc = mfma(h1[kt], wf[nt & 1][kt], acc);
+      const float bk = S.b2k[16 * nt + r], w3 = S.w3[16 * nt + r];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float h = tanh_bias(acc[i], bk);
+        h2[nt][i] = h;
+        yp[i] = __builtin_fmaf(w3, (float)(__bf16)h, yp[i]);
+      }
+      __builtin_amdgcn_sched_barrier(0);   // one feature tile at a time: bounds the live fragments
+    }
+    // V(s) and dL/dV for samples 4 g + i (every lane of a row holds them)
+    float gq[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float y = row_sum16(yp[i]) + b3;
+      const bool vs = t * 16 + 4 * g + i < B;
+      const float e = y - cur.rt[i];
+      const float gy = vs ? hp.vf_coef * hp.inv_B * e : 0.0f;
+      gq[i] = (float)(__bf16)gy;
+      if (r == 0 && vs) {
+        db3 += gy;
+        sq += e * e;
+      }
+    }
+
+    // ---- dz2 = (W3^T q(gy)) (1 - h2^2); db2 and dW3 in-lane; q(dz2) as half fragments and,
+    // through the selection MFMA, as the feature-major pairs of the input gradient
+    bf16x8 dzf[8];
+    float db2[16], dw3[16];
+#pragma unroll
+    for (int nt = 0; nt < 16; ++nt) {
+      const float w3 = S.w3[16 * nt + r];
+      f32x4 dz;
+      float a3 = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        dz[i] = (w3 * gq[i]) * (1.0f - h2[nt][i] * h2[nt][i]);
+        a3 = __builtin_fmaf(gq[i], (float)(__bf16)h2[nt][i], a3);
+      }
+      db2[nt] = (dz[0] + dz[1]) + (dz[2] + dz[3]);
+      dw3[nt] = a3;
+      const u32x2 q = pack4(dz);
+      W.dz2_half[(tb + nt) * 64 + lane] = q;
+      const f32x4 d = mfma(low_half(q), I0, zero);   // features 16 nt + 4 g + i, sample r
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dzf[nt >> 1][4 * (nt & 1) + i] = (__bf16)d[i];
+    }
+    {
+      float o2[4], o3[4];
+      rows_reduce_scatter(db2, o2, g);
+      rows_reduce_scatter(dw3, o3, g);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        sb2[k] += o2[k];
+        sw3[k] += o3[k];
+      }
+    }
+
+    // ---- dh1 = W2^T q(dz2) sample-major, dz1 = dh1 (1 - h1^2) with h1 recomputed
+    // sample-major from the inputs, db1 in-lane, q(dz1) as half fragments
+    // (the next tile's transposed fragments are read during this one's products)
+    float db1[16];
+    bf16x8 tf[2][8];
+#pragma unroll
+    for (int kt = 0; kt < 8; ++kt) tf[0][kt] = w2t_frag(S.w2, kt, 0, lane);
+#pragma unroll
+    for (int nt = 0; nt < 16; ++nt) {
+      if (nt + 1 < 16) {
+#pragma unroll
+        for (int kt = 0; kt < 8; ++kt) tf[(nt + 1) & 1][kt] = w2t_frag(S.w2, kt, nt + 1, lane);
+      }
+      f32x4 acc = zero;
+#pragma unroll
+      for (int kt = 0; kt < 8; ++kt) acc = mfma(dzf[kt], tf[nt & 1][kt], acc);
+      const f32x4 z1 = mfma(x, S.w1[nt][lane], zero);
+      const float bk = S.b1k[16 * nt + r];
+      f32x4 dz;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float h = tanh_bias(z1[i], bk);
+        dz[i] = acc[i] * (1.0f - h * h);
+      }
+      db1[nt] = (dz[0] + dz[1]) + (dz[2] + dz[3]);
+      W.dz1_half[(tb + nt) * 64 + lane] = pack4(dz);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    {
+      float o1[4];
+      rows_reduce_scatter(db1, o1, g);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) sb1[k] += o1[k];
+    }
+    cur = nxt;
+  }
+
+  // ---- per-workgroup sums, in a fixed order (over the waves)
+  __syncthreads();   // every wave is done with the weights: their LDS holds the sums now
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int f = 16 * (4 * g + k) + r;
+    U.red.v[wave][0][f] = sb1[k];
+    U.red.v[wave][1][f] = sb2[k];
+    U.red.v[wave][2][f] = sw3[k];
+  }
+  if (r == 0) {
+    U.red.sc[wave][0][g] = db3;
+    U.red.sc[wave][1][g] = sq;
+  }
+  __syncthreads();
+  const int wg = blockIdx.x;
+  for (int o = tid; o < 3 * HID; o += 64 * VT_WAVES) {
+    const int q = o / HID, f = o - q * HID;
+    float v = 0.0f;
+#pragma unroll
+    for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.v[wv][q][f];
+    if (q == 0)
+      W.part_b1[(size_t)wg * HID + f] = v;
+    else if (q == 1)
+      W.part_b2[(size_t)wg * HID + f] = v;
+    else
+      W.part_w3t[((size_t)wg * HID + f) * 16] = v;
+  }
+  if (tid < 2) {
+    float v = 0.0f;
+    for (int wv = 0; wv < VT_WAVES; ++wv)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) v += U.red.sc[wv][tid][gg];
+    if (tid == 0)
+      W.part_b3[wg * 16] = v;
+    else
+      W.part_stats[((size_t)MAX_GROUPS + wg) * STATS + 3] = v;
+  }
+}
+
+// dW2 = q(dz2) q(h1)^T and dW1 = q(dz1) q(x)^T over the 32-sample steps of one chunk of the
+// minibatch, for one block of 64 gradient rows: workgroup (row block p, chunk c), eight
+// waves; wave w accumulates rows 64 p .. + 63 x dW2 columns 32 w .. + 31 (8 accumulators) and
+// the dW1 tile (rows 64 p + 16 (w % 4), inputs 16 (w / 4)).  The q(dz2), q(dz1) and q(x)
+// fragments of a step are shared through LDS (two buffers, one barrier per step); each wave
+// loads its own q(h1) fragments.  A step's nine products take far less than a load's
+// latency, so each thread's loads run VW_DEPTH steps ahead in a ring of register sets, issued
+// unconditionally (step index clamped) so that every wait covers only its own set.  The four
+// row blocks of a chunk are workgroups 8 apart, which the dispatcher places on one XCD, so
+// that its L2 serves their common q(h1) and q(x).  `chunks` is a multiple of 8; grid =
+// 4 chunks.
+constexpr int VW_DEPTH = 8;
+__global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(Work W, int steps, int chunks) {
+  __shared__ bf16x8 Ad[2][4][64];   // q(dz2) A fragments: rows 64 p + 16 mt
+  __shared__ bf16x8 A1[2][4][64];   // q(dz1) A fragments: rows 64 p + 16 mt
+  __shared__ bf16x8 Xb[2][2][64];   // q(x) B fragments: inputs 16 it + r
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r = lane & 15;
+  const int bid = blockIdx.x, jj = bid >> 3;
+  const int p = jj & 3, c = (jj >> 2) * 8 + (bid & 7);
+  const int per = (steps + chunks - 1) / chunks;
+  const int u0 = min(steps, c * per), u1 = min(steps, u0 + per);
+  f32x4 acc[4][2], acc1 = f32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) acc[mt][0] = acc[mt][1] = f32x4{0, 0, 0, 0};
+  if (u0 < u1) {
+    auto at = [&](int tile, int ft, int nft) { return ((size_t)tile * nft + ft) * 64 + lane; };
+    // staging: wave w copies q(dz2) (w < 4) or q(dz1) (w >= 4) row tile w % 4 of the block,
+    // waves 0 and 1 also q(x) input tile w
+    const u32x2* sa = w < 4 ? W.dz2_half : W.dz1_half;
+    const int smt = 4 * p + (w & 3);
+    struct Step {
+      bf16x8 a, x, h[2];
+    };
+    auto load = [&](int u, Step& R) __attribute__((always_inline)) {
+      u = min(u, u1 - 1);
+      R.a = join(sa[at(2 * u, smt, 16)], sa[at(2 * u + 1, smt, 16)]);
+      if (w < 2) R.x = join(W.x_half[at(2 * u, w, 2)], W.x_half[at(2 * u + 1, w, 2)]);
+#pragma unroll
+      for (int q = 0; q < 2; ++q) R.h[q] = join(W.h1_half[at(2 * u, 2 * w + q, 16)], W.h1_half[at(2 * u + 1, 2 * w + q, 16)]);
+    };
+    Step R[VW_DEPTH];
+#pragma unroll
+    for (int j = 0; j < VW_DEPTH; ++j) load(u0 + j, R[j]);
+    for (int u = u0; u < u1; u += VW_DEPTH) {
+#pragma unroll
+      for (int j = 0; j < VW_DEPTH; ++j) {
+        if (u + j < u1) {   // uniform over the workgroup
+          const int buf = j & 1;   // last read in the step before the previous barrier
+          if (w < 4)
+            Ad[buf][w][lane] = R[j].a;
+          else
+            A1[buf][w - 4][lane] = R[j].a;
+          if (w < 2) Xb[buf][w][lane] = R[j].x;
+          __syncthreads();
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt) {
+            const bf16x8 af = Ad[buf][mt][lane];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) acc[mt][q] = mfma(af, R[j].h[q], acc[mt][q]);
+          }
+          acc1 = mfma(A1[buf][w & 3][lane], Xb[buf][w >> 2][lane], acc1);
+        }
+        load(u + j + VW_DEPTH, R[j]);
+      }
+    }
+  }
+  float* o2 = W.part_w2 + (size_t)c * HID * HID;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o2[(64 * p + 16 * mt + 4 * g + i) * HID + 16 * (2 * w + q) + r] = acc[mt][q][i];
+  float* o1 = W.part_w1 + (size_t)c * HID * 32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o1[(64 * p + 16 * (w & 3) + 4 * g + i) * 32 + 16 * (w >> 2) + r] = acc1[i];
+}
+
+// Chunks of the value-only weight gradient: 8 to VW_MAX_CHUNKS, about one per 16 steps.
+inline int vw_chunks(int steps) {
+  const int c = (steps / 16 + 7) / 8 * 8;
+  return c < 8 ? 8 : (c > VW_MAX_CHUNKS ? VW_MAX_CHUNKS : c);
+}
+
 // One Adam step of packed entry e with gradient g (k_adam's update; the bf16 copy of the
 // weight matrices rounded to nearest even).  A fused step (theta set) runs in k_reduce.
 struct AdamFuse {
@@ -821,8 +1270,8 @@ __device__ __forceinline__ void adam_entry(const AdamFuse& A, int e, float g0, f
 // squares for the global norm.  A block owns 64 gradient entries (one per lane); its four
 // waves each sum a contiguous quarter of the workgroup partials with eight loads in flight,
 // then wave 0 adds the quarters in wave order.  G1: forward/backward groups (dW3, db2, db3,
-// d log_std), G2: dz1 groups (dW1, db1), G3: dW2 groups.
-__global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, int G2, int G3, Work W, float ent_coef,
+// d log_std), G2: dW1 groups, Gb1: db1 groups, G3: dW2 groups.
+__global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, int G2, int Gb1, int G3, Work W, float ent_coef,
                                                 float* __restrict__ grad, float* __restrict__ ss, AdamFuse A) {
   __shared__ float part[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -844,7 +1293,7 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, in
       const int j = q / HID, f = q - HID * j;
       src = W.part_w3t + f * 16 + j, stride = (size_t)HID * 16, G = G1;
     } else if ((q -= nW3) < HID) {
-      src = W.part_b1 + q, stride = HID, G = G2;
+      src = W.part_b1 + q, stride = HID, G = Gb1;
     } else if ((q -= HID) < HID) {
       src = W.part_b2 + q, stride = HID, G = G1;
     } else if ((q -= HID) < n_out) {
@@ -976,7 +1425,7 @@ int launch_grad_reduce(const GradParts& P, int n_out, int n_act, int G1, int G2,
   W.part_b2 = P.part_b2;
   W.part_b3 = P.part_b3;
   W.part_ls = P.part_ls;
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(n_out)), dim3(256), 0, s, n_out, n_act, G1, G2, G3, W, 0.0f,
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(n_out)), dim3(256), 0, s, n_out, n_act, G1, G2, G2, G3, W, 0.0f,
                      grad, ss, ppo::AdamFuse{});
   return check_launch("gradient reduce");
 }
@@ -1056,18 +1505,19 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
     hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
     const ppo::H1Src H{nullptr, policy->w, policy->b, D.obs, D.M, idx, B};
     hipLaunchKernelGGL(ppo::k_dw2<true>, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, H, steps, W.part_w2);
-    hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G3, W, cfg->ent_coef,
+    hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G1, G3, W, cfg->ent_coef,
                        grad_policy, W.part_ss, ppo::AdamFuse{});
   }
-  hipLaunchKernelGGL((ppo::k_fwd_bwd<1, FPW>), dim3(G1), dim3(TH), 0, s, value->w, value->b, (const float*)nullptr, D,
-                     idx, B, tiles, hp, W, 1);
-  hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, value->w, value->b, D, idx, B, tiles, W);
-  const ppo::H1Src Hv{nullptr, value->w, value->b, D.obs, D.M, idx, B};
-  hipLaunchKernelGGL(ppo::k_dw2<true>, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, Hv, steps, W.part_w2);
-  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, G1, G1, G3, W, 0.0f,
+  // value network: per-tile forward / backward, the weight-gradient product, the reduce
+  const int GV = std::min(cus, (tiles + ppo::VT_WAVES - 1) / ppo::VT_WAVES);
+  const int chunks = ppo::vw_chunks(steps);
+  hipLaunchKernelGGL(ppo::k_vtile, dim3(GV), dim3(64 * ppo::VT_WAVES), 0, s, value->w, value->b, D, idx, B, tiles, hp,
+                     W);
+  hipLaunchKernelGGL(ppo::k_vwgrad, dim3(4 * chunks), dim3(64 * ppo::VW_WAVES), 0, s, W, steps, chunks);
+  hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, GV, chunks, GV, chunks, W, 0.0f,
                      grad_value, W.part_ss + rb, fuse);
   if (finalize)
-    hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? G1 : 0, G1, W, with_policy ? rb : 0,
+    hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? G1 : 0, GV, W, with_policy ? rb : 0,
                        ppo::red_blocks(1), rb, with_policy ? policy->log_std : (const float*)nullptr, hp, stats);
   return check_launch("auv_ppo_grad");
 }
