@@ -912,22 +912,35 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
   const int Mi = (int)D.M;
   const size_t M = D.M;
   // inputs of a tile: this lane's 8 layer-1 inputs of sample r and the returns of samples
-  // 4 g .. 4 g + 3 (unconditional loads from clamped entries, masked on use)
+  // 4 g .. 4 g + 3 (unconditional loads from clamped entries, masked on use).  The next tile's
+  // sample indices are loaded at the top of a tile and its inputs at the start of the input
+  // gradient, where few registers are live: held any earlier they would be spilled, and every
+  // spill of a loaded value waits for the load.
+  struct Idx {
+    int s[5];
+  };
   struct In {
     float x[8], rt[4];
   };
-  auto load_in = [&](int t) __attribute__((always_inline)) {
+  auto load_idx = [&](int t) __attribute__((always_inline)) {
+    Idx q;
+    q.s[0] = raw_index(idx, t, r, B);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) q.s[1 + i] = raw_index(idx, t, 4 * g + i, B);
+    return q;
+  };
+  auto load_in = [&](const Idx& q) __attribute__((always_inline)) {
     In in;
-    const size_t sr = (size_t)clamp_sample(raw_index(idx, t, r, B), Mi);
+    const size_t sr = (size_t)clamp_sample(q.s[0], Mi);
 #pragma unroll
     for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(g, j), 22) * M + sr];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) in.rt[i] = D.ret[clamp_sample(raw_index(idx, t, 4 * g + i, B), Mi)];
+    for (int i = 0; i < 4; ++i) in.rt[i] = D.ret[clamp_sample(q.s[1 + i], Mi)];
     return in;
   };
   int t = blockIdx.x * VT_WAVES + wave;
   const int stride = gridDim.x * VT_WAVES;
-  In cur = load_in(min(t, tiles - 1));   // in flight while the weights are staged
+  In cur = load_in(load_idx(min(t, tiles - 1)));   // in flight while the weights are staged
   {   // weights -> A fragments (lane (g, r) of fragment (M-tile, K tile) holds row 16 mt + r,
       // inputs 32 kt + kslot(g, j)); every load is issued before the first LDS store, so that
       // the staging costs about one memory latency
@@ -974,7 +987,6 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     }
   }
   const float b3 = b[2 * HID];
-  const bf16x8 I0 = select_frag(g, r, 0), I1 = select_frag(g, r, 1);
   const f32x4 zero = f32x4{0, 0, 0, 0};
   const int w2s = w2_slot(lane);
   // db1, db2 and dW3 of features 16 (4 g + k) + r, k = 0..3 (see rows_reduce_scatter)
@@ -983,14 +995,14 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
   __syncthreads();
 
   for (; t < tiles; t += stride) {
-    const In nxt = load_in(min(t + stride, tiles - 1));
+    const Idx nq = load_idx(min(t + stride, tiles - 1));
     const size_t tb = (size_t)t * 16;
     const bool vr = t * 16 + r < B;
     bf16x8 x;
 #pragma unroll
     for (int j = 0; j < 8; ++j) x[j] = (__bf16)((vr && kslot(g, j) < 23) ? cur.x[j] : 0.0f);
-    W.x_half[((size_t)t * 2) * 64 + lane] = pack4(mfma(x, I0, zero));
-    W.x_half[((size_t)t * 2 + 1) * 64 + lane] = pack4(mfma(x, I1, zero));
+    W.x_half[((size_t)t * 2) * 64 + lane] = pack4(mfma(x, select_frag(g, r, 0), zero));
+    W.x_half[((size_t)t * 2 + 1) * 64 + lane] = pack4(mfma(x, select_frag(g, r, 1), zero));
 
     // ---- layer 1, feature-major: the pairs h1[kt] (features 32 kt + kslot(g, j), sample r)
     bf16x8 h1[8];
@@ -1002,26 +1014,26 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     }
 #pragma unroll
     for (int kt = 0; kt < 8; ++kt) {
-      W.h1_half[(tb + 2 * kt) * 64 + lane] = pack4(mfma(h1[kt], I0, zero));
-      W.h1_half[(tb + 2 * kt + 1) * 64 + lane] = pack4(mfma(h1[kt], I1, zero));
+      W.h1_half[(tb + 2 * kt) * 64 + lane] = pack4(mfma(h1[kt], select_frag(g, r, 0), zero));
+      W.h1_half[(tb + 2 * kt + 1) * 64 + lane] = pack4(mfma(h1[kt], select_frag(g, r, 1), zero));
     }
 
     // ---- layer 2, sample-major (z2 feature 16 nt + r, samples 4 g + i), and the value
-    // (the next feature tile's eight weight fragments are read during this one's products)
+    // (each weight fragment's register is refilled with the next feature tile's fragment as
+    // soon as its product is issued: a one-tile-deep prefetch in eight registers sets)
     f32x4 h2[16];
     float yp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    bf16x8 wf[2][8];
+    bf16x8 wf[8];
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt) wf[0][kt] = S.w2[0][kt][w2s];
+    for (int kt = 0; kt < 8; ++kt) wf[kt] = S.w2[0][kt][w2s];
 #pragma unroll
     for (int nt = 0; nt < 16; ++nt) {
-      if (nt + 1 < 16) {
-#pragma unroll
-        for (int kt = 0; kt < 8; ++kt) wf[(nt + 1) & 1][kt] = S.w2[nt + 1][kt][w2s];
-      }
       f32x4 acc = zero;
 #pragma unroll
-      for (int kt = 0; kt < 8; ++kt) acc = mfma(h1[kt], wf[nt & 1][kt], acc);
+      for (int kt = 0; kt < 8; ++kt) {
+        acc = mfma(h1[kt], wf[kt], acc);
+        if (nt + 1 < 16) wf[kt] = S.w2[nt + 1][kt][w2s];
+      }
       const float bk = S.b2k[16 * nt + r], w3 = S.w3[16 * nt + r];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -1064,7 +1076,7 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
       dw3[nt] = a3;
       const u32x2 q = pack4(dz);
       W.dz2_half[(tb + nt) * 64 + lane] = q;
-      const f32x4 d = mfma(low_half(q), I0, zero);   // features 16 nt + 4 g + i, sample r
+      const f32x4 d = mfma(low_half(q), select_frag(g, r, 0), zero);   // features 16 nt + 4 g + i, sample r
 #pragma unroll
       for (int i = 0; i < 4; ++i) dzf[nt >> 1][4 * (nt & 1) + i] = (__bf16)d[i];
     }
@@ -1081,20 +1093,20 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
 
     // ---- dh1 = W2^T q(dz2) sample-major, dz1 = dh1 (1 - h1^2) with h1 recomputed
     // sample-major from the inputs, db1 in-lane, q(dz1) as half fragments
-    // (the next tile's transposed fragments are read during this one's products)
+    const In nxt = load_in(nq);
+    // (the transposed fragments are prefetched one feature tile ahead the same way)
     float db1[16];
-    bf16x8 tf[2][8];
+    bf16x8 tf[8];
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt) tf[0][kt] = w2t_frag(S.w2, kt, 0, lane);
+    for (int kt = 0; kt < 8; ++kt) tf[kt] = w2t_frag(S.w2, kt, 0, lane);
 #pragma unroll
     for (int nt = 0; nt < 16; ++nt) {
-      if (nt + 1 < 16) {
-#pragma unroll
-        for (int kt = 0; kt < 8; ++kt) tf[(nt + 1) & 1][kt] = w2t_frag(S.w2, kt, nt + 1, lane);
-      }
       f32x4 acc = zero;
 #pragma unroll
-      for (int kt = 0; kt < 8; ++kt) acc = mfma(dzf[kt], tf[nt & 1][kt], acc);
+      for (int kt = 0; kt < 8; ++kt) {
+        acc = mfma(dzf[kt], tf[kt], acc);
+        if (nt + 1 < 16) tf[kt] = w2t_frag(S.w2, kt, nt + 1, lane);
+      }
       const f32x4 z1 = mfma(x, S.w1[nt][lane], zero);
       const float bk = S.b1k[16 * nt + r];
       f32x4 dz;
