@@ -3,7 +3,8 @@
 // Sec. III-A1), its gradient through both 23-256-256-n_out networks on bf16 MFMA, global-norm
 // gradient clipping and Adam (Kingma and Ba, Algorithm 1).
 //
-// Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 32):
+// Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 128); the
+// policy network:
 //   k_adv_partial   per-block sums of the minibatch's advantages and their squares (fp64)
 //   k_adv_final     mean and 1 / (std + 1e-8) from those sums
 //   k_fwd_bwd<n>    per 16-sample tile: forward, loss, dL/dy, dz2 = (W3^T q(dL/dy)) (1 - h2^2);
@@ -16,6 +17,13 @@
 //                   per workgroup held in accumulator registers
 //   k_reduce        fixed-order sums of the per-workgroup partials -> packed gradient, and
 //                   per-block sums of squares
+// then the value network (also every minibatch of auv_ppo_fit_value):
+//   k_vtile         per 16-sample tile and wave, the weights in LDS: forward, squared error,
+//                   dz2, dz1; the bias and output-weight gradient sums; half fragments of
+//                   q(x), q(h1), q(dz2), q(dz1) for the weight-gradient product
+//   k_vwgrad        dW2 and dW1 per (64-row block, chunk of the minibatch)
+//   k_reduce        as above (with the Adam step fused in a value-only fit)
+// and last
 //   k_finalize      loss statistics, gradient norms, the clipping factor
 //   k_adam          one Adam step and the bf16 weight copy
 // Every sum has a fixed order, so a call is bit-for-bit repeatable.
