@@ -950,8 +950,8 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
   const int stride = gridDim.x * VT_WAVES;
   In cur = load_in(load_idx(min(t, tiles - 1)));   // in flight while the weights are staged
   {   // weights -> A fragments (lane (g, r) of fragment (M-tile, K tile) holds row 16 mt + r,
-      // inputs 32 kt + kslot(g, j)); every load is issued before the first LDS store, so that
-      // the staging costs about one memory latency
+      // inputs 32 kt + kslot(g, j); W2's at slot w2_slot(lane)); every load is issued before
+      // the first LDS store, so that the loads overlap
     const uint16_t* W1 = w;
     const uint16_t* W2 = w + HID * 23;
     const uint16_t* W3 = W2 + HID * HID;
@@ -1184,8 +1184,8 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
 // latency, so each thread's loads run VW_DEPTH steps ahead in a ring of register sets, issued
 // unconditionally (step index clamped) so that every wait covers only its own set.  The four
 // row blocks of a chunk are workgroups 8 apart, which the dispatcher places on one XCD, so
-// that its L2 serves their common q(h1) and q(x).  `chunks` is a multiple of 8; grid =
-// 4 chunks.
+// that their common q(h1) and q(x) can come from its L2.  `chunks` is a multiple of 8;
+// grid = 4 chunks.
 constexpr int VW_DEPTH = 8;
 __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(Work W, int steps, int chunks) {
   __shared__ bf16x8 Ad[2][4][64];   // q(dz2) A fragments: rows 64 p + 16 mt
