@@ -392,7 +392,9 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
  * is value_net's auv_mlp view; batch: obs and ret are read (M = batch->M).  The host
  * shuffles the next pass while the device runs the current one: a pass's indices are
  * written into one half of host_stage (int32 [2][16 floor(M / 16)], pinned host memory
- * owned by the caller) and copied asynchronously into the workspace.  The call returns when
+ * owned by the caller) and copied asynchronously into the workspace, on a copy stream of the
+ * library's own (one per device, created on first use, default priority) that events order
+ * against `stream`, so that the copy runs beside the previous pass's kernels.  The call returns when
  * every copy has been made (the device may still run the last minibatches); grad_value
  * [AUV_PPO_NPARAM(1)] and stats [8] then hold the last minibatch's results.  work:
  * auv_ppo_fit_work_bytes(M, batches) bytes (-1 unless 16 <= M <= 2^28 and 1 <= batches <=

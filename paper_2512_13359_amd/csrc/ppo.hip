@@ -37,6 +37,7 @@
 // r); a per-wave LDS transpose turns them into "half fragments" (lane (g, r): feature r of a
 // 16-feature tile, samples 4g..4g+3 of a 16-sample tile, 8 bytes).
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "auv_internal.hpp"
@@ -1598,6 +1599,30 @@ int64_t auv_ppo_fit_work_bytes(int64_t M, int32_t batches) {
   return (int64_t)ppo::align256((size_t)w) + 2 * (M / 16) * 16 * (int64_t)sizeof(int32_t);
 }
 
+// The stream auv_ppo_fit_value uploads its shuffled indices on, one per device (default
+// priority, not synchronising with the null stream), created on first use there and kept until
+// the process ends; events order it against the caller's stream, so that a pass's upload runs
+// during the previous pass's kernels instead of between them.
+static std::mutex g_copy_mu;
+constexpr int FIT_MAX_DEVICES = 64;
+static hipStream_t g_copy_stream[FIT_MAX_DEVICES] = {};
+
+static int copy_stream_on_current_device(hipStream_t* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= FIT_MAX_DEVICES)
+    return set_error(AUV_ENODEV, "auv_ppo_fit_value: no usable current device");
+  std::lock_guard<std::mutex> lock(g_copy_mu);
+  if (!g_copy_stream[dev]) {
+    hipStream_t cs = nullptr;
+    const hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+    if (e != hipSuccess || !cs)
+      return set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipStreamCreateWithFlags failed: %s", hipGetErrorString(e));
+    g_copy_stream[dev] = cs;
+  }
+  *out = g_copy_stream[dev];
+  return AUV_OK;
+}
+
 // SplitMix64 (Steele, Lea and Flood 2014): the generator of the passes' shuffles.
 static inline uint64_t splitmix64(uint64_t& s) {
   uint64_t z = (s += 0x9E3779B97F4A7C15ull);
@@ -1632,13 +1657,19 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
   size_t off = ppo::align256((size_t)auv_ppo_work_bytes(B));
   int32_t* dev_idx = (int32_t*)((char*)work + off);   // [2][n] sample indices, one slot per pass parity
   hipStream_t s = (hipStream_t)stream;
-  hipEvent_t copied[2];
-  for (int k = 0; k < 2; ++k)
-    if (hipEventCreateWithFlags(&copied[k], hipEventDisableTiming) != hipSuccess) {
-      if (k == 1) (void)hipEventDestroy(copied[0]);
+  hipStream_t cs = nullptr;
+  if (int rc = copy_stream_on_current_device(&cs)) return rc;
+  // copied[k]: slot k's last upload has run (host slot free, device slot filled);
+  // consumed[k]: the kernels that read device slot k last have run
+  hipEvent_t ev[4];
+  for (int k = 0; k < 4; ++k)
+    if (hipEventCreateWithFlags(&ev[k], hipEventDisableTiming) != hipSuccess) {
+      for (int q = 0; q < k; ++q) (void)hipEventDestroy(ev[q]);
       return set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventCreate failed");
     }
-  bool pending[2] = {false, false};
+  hipEvent_t* copied = ev;
+  hipEvent_t* consumed = ev + 2;
+  bool pending[2] = {false, false}, used[2] = {false, false};
   std::vector<int32_t> perm((size_t)nb);
   uint64_t rs = seed;
   int rc = AUV_OK;
@@ -1659,8 +1690,11 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
     for (int64_t b = 0; b < nb; ++b)
       for (int r = 0; r < 16; ++r) stage[b * 16 + r] = perm[b] * 16 + r;
     int32_t* idx = dev_idx + k * n;
-    if (hipMemcpyAsync(idx, stage, (size_t)n * sizeof(int32_t), hipMemcpyHostToDevice, s) != hipSuccess ||
-        hipEventRecord(copied[k], s) != hipSuccess) {
+    // the upload waits for the pass that read this device slot last, the pass's kernels wait
+    // for the upload
+    if ((used[k] && hipStreamWaitEvent(cs, consumed[k], 0) != hipSuccess) ||
+        hipMemcpyAsync(idx, stage, (size_t)n * sizeof(int32_t), hipMemcpyHostToDevice, cs) != hipSuccess ||
+        hipEventRecord(copied[k], cs) != hipSuccess || hipStreamWaitEvent(s, copied[k], 0) != hipSuccess) {
       rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: index copy failed");
       break;
     }
@@ -1688,12 +1722,17 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
         if (rc == AUV_OK) rc = auv_ppo_adam(cfg, t, nullptr, value_net, nullptr, grad_value, stats, stream);
       }
     }
+    if (rc == AUV_OK) {
+      if (hipEventRecord(consumed[k], s) != hipSuccess)
+        rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventRecord failed");
+      else
+        used[k] = true;
+    }
   }
-  for (int k = 0; k < 2; ++k) {   // the caller may reuse host_stage once the call returns
+  for (int k = 0; k < 2; ++k)   // the caller may reuse host_stage once the call returns
     if (pending[k] && hipEventSynchronize(copied[k]) != hipSuccess && rc == AUV_OK)
       rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventSynchronize failed");
-    (void)hipEventDestroy(copied[k]);
-  }
+  for (int k = 0; k < 4; ++k) (void)hipEventDestroy(ev[k]);
   return rc;
 }
 
