@@ -421,8 +421,9 @@ def _fit_indices(M, iterations, seed):
 
 def test_ppo_fit_value_matches_stepwise_calls():
     """auv_ppo_fit_value equals the same value-only gradient + Adam steps issued one call at
-    a time with the shuffles restated in Python (bit for bit), and rejects bad sizes."""
-    n, h, iterations, batches, seed = 130, 6, 3, 4, 12345
+    a time with the shuffles restated in Python (bit for bit; the index uploads reuse each of
+    their two slots), and rejects bad sizes."""
+    n, h, iterations, batches, seed = 130, 6, 6, 4, 12345   # six passes: each index slot reused twice
     announce(f"PPO fit value n={n} h={h} iterations={iterations}")
     require_gpu()
     from paper_2512_13359_amd import _abi as A
