@@ -105,9 +105,15 @@ static_assert(sizeof(Lds) <= 160 * 1024, "window kernel LDS exceeds a CU's 160 K
 constexpr int H2_F4 = 4 * 64;
 
 // ------------------------------------------------------------------ fragments ---------
-__global__ __launch_bounds__(256) void k_frags(const uint16_t* __restrict__ w, int n_out, bf16x8* __restrict__ out) {
+// blockIdx.y selects the network: 0 the policy (w, n_out, out), 1 the value net (w1, n_out1,
+// out1), so that both are rearranged in one launch.
+__global__ __launch_bounds__(256) void k_frags(const uint16_t* __restrict__ w0, int n_out0, bf16x8* __restrict__ out0,
+                                               const uint16_t* __restrict__ w1, int n_out1, bf16x8* __restrict__ out1) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= F_END * 64) return;
+  const uint16_t* w = blockIdx.y ? w1 : w0;
+  const int n_out = blockIdx.y ? n_out1 : n_out0;
+  bf16x8* out = blockIdx.y ? out1 : out0;
   const int f = e >> 6, lane = e & 63, g = lane >> 4, r = lane & 15;
   const uint16_t* W1 = w;
   const uint16_t* W2 = w + HID * 23;
@@ -1099,8 +1105,17 @@ int auv_shac_window(auv_env* env, const auv_shac_config* cfg, const auv_mlp* pol
   auto at = [&](int k) { return (void*)(base + off[k]); };
   bf16x8* frags = (bf16x8*)at(0);
   const int fb = (F_END * 64 + 255) / 256;
-  if (!ext) hipLaunchKernelGGL(k_frags, dim3(fb), dim3(256), 0, s, policy->w, ACT, frags);
-  if (value) hipLaunchKernelGGL(k_frags, dim3(fb), dim3(256), 0, s, value->w, 1, frags + F_END * 64);
+  // both networks' fragments in one launch (grid y: the networks given, the policy first)
+  {
+    const uint16_t* wn[2] = {nullptr, nullptr};
+    int no[2] = {0, 0};
+    bf16x8* dst[2] = {nullptr, nullptr};
+    int nn = 0;
+    if (!ext) wn[nn] = policy->w, no[nn] = ACT, dst[nn++] = frags;
+    if (value) wn[nn] = value->w, no[nn] = 1, dst[nn++] = frags + F_END * 64;
+    if (nn > 0)
+      hipLaunchKernelGGL(k_frags, dim3(fb, nn), dim3(256), 0, s, wn[0], no[0], dst[0], wn[1], no[1], dst[1]);
+  }
 
   WinArgs A{};
   A.steps = h;
