@@ -1660,15 +1660,20 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
   hipStream_t cs = nullptr;
   if (int rc = copy_stream_on_current_device(&cs)) return rc;
   // copied[k]: slot k's last upload has run (host slot free, device slot filled);
-  // consumed[k]: the kernels that read device slot k last have run
-  hipEvent_t ev[4];
-  for (int k = 0; k < 4; ++k)
+  // consumed[k]: the kernels that read device slot k last have run; entry: everything enqueued
+  // on `stream` before this call (an earlier call's last passes may still read the slots)
+  hipEvent_t ev[5];
+  for (int k = 0; k < 5; ++k)
     if (hipEventCreateWithFlags(&ev[k], hipEventDisableTiming) != hipSuccess) {
       for (int q = 0; q < k; ++q) (void)hipEventDestroy(ev[q]);
       return set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventCreate failed");
     }
   hipEvent_t* copied = ev;
   hipEvent_t* consumed = ev + 2;
+  if (hipEventRecord(ev[4], s) != hipSuccess || hipStreamWaitEvent(cs, ev[4], 0) != hipSuccess) {
+    for (int q = 0; q < 5; ++q) (void)hipEventDestroy(ev[q]);
+    return set_error(AUV_ERUNTIME, "auv_ppo_fit_value: ordering the uploads after earlier work failed");
+  }
   bool pending[2] = {false, false}, used[2] = {false, false};
   std::vector<int32_t> perm((size_t)nb);
   uint64_t rs = seed;
@@ -1732,7 +1737,7 @@ int auv_ppo_fit_value(const auv_ppo_config* cfg, const auv_mlp* value, const auv
   for (int k = 0; k < 2; ++k)   // the caller may reuse host_stage once the call returns
     if (pending[k] && hipEventSynchronize(copied[k]) != hipSuccess && rc == AUV_OK)
       rc = set_error(AUV_ERUNTIME, "auv_ppo_fit_value: hipEventSynchronize failed");
-  for (int k = 0; k < 4; ++k) (void)hipEventDestroy(ev[k]);
+  for (int k = 0; k < 5; ++k) (void)hipEventDestroy(ev[k]);
   return rc;
 }
 

@@ -419,6 +419,49 @@ def _fit_indices(M, iterations, seed):
     return out
 
 
+def test_ppo_fit_value_back_to_back_calls():
+    """Two auv_ppo_fit_value calls issued back to back on one workspace, with no
+    synchronisation between them, equal the same steps issued one call at a time (bit for
+    bit): the second call's first index upload (slot 0) waits for the first call's last pass,
+    which read slot 0 too."""
+    n, h, iterations, batches = 130, 6, 3, 4
+    announce(f"PPO fit value back to back n={n} h={h} iterations={iterations}")
+    require_gpu()
+    from paper_2512_13359_amd import _abi as A
+    from paper_2512_13359_amd.ppo import PpoNet
+    _, g, _ = _setup(n, seed=15)
+    L = _learner(g, h)
+    L.window()
+    L.targets()
+    M = h * n
+    b = L._last
+    batch = A.make_ppo_batch(b["obs"], b["obs"], L.values, L.adv, L.ret, M)
+    val = W.mlp_weights(1, W.PAPER_VALUE_SEED, n_in=12)
+    net1, net2 = PpoNet(val, "cuda"), PpoNet(val, "cuda")
+    work = torch.empty(A.auv_ppo_fit_work_bytes(M, batches), dtype=torch.uint8, device="cuda")
+    stage = torch.empty(2 * 16 * (M // 16), dtype=torch.int32, pin_memory=True)
+    g1, s1 = torch.zeros(A.ppo_nparam(1), device="cuda"), torch.zeros(8, device="cuda")
+    seeds = (777, 778)
+    A.auv_ppo_fit_value(L.critic_cfg, net1.mlp, net1.net, batch, iterations, batches, seeds[0], 0, stage, g1, s1, work)
+    A.auv_ppo_fit_value(L.critic_cfg, net1.mlp, net1.net, batch, iterations, batches, seeds[1], iterations * batches,
+                        stage, g1, s1, work)
+    B = (M // 16 // batches) * 16
+    g2, s2 = torch.zeros_like(g1), torch.zeros_like(s1)
+    w2 = torch.empty(A.auv_ppo_work_bytes(B), dtype=torch.uint8, device="cuda")
+    t = 0
+    for seed in seeds:
+        for order in _fit_indices(M, iterations, seed):
+            idx = torch.from_numpy(order).cuda()
+            for j in range(batches):
+                A.auv_ppo_grad(L.critic_cfg, None, net2.mlp, batch, idx[j * B:(j + 1) * B], B, None, g2, s2, w2)
+                t += 1
+                A.auv_ppo_adam(L.critic_cfg, t, None, net2.net, None, g2, s2)
+    torch.cuda.synchronize()
+    d = (net1.theta - net2.theta).abs()
+    assert torch.equal(net1.theta, net2.theta), (float(d.max()), int((d > 0).sum()), int(d.numel()))
+    assert torch.equal(g1, g2) and torch.equal(s1, s2)
+
+
 def test_ppo_fit_value_matches_stepwise_calls():
     """auv_ppo_fit_value equals the same value-only gradient + Adam steps issued one call at
     a time with the shuffles restated in Python (bit for bit; the index uploads reuse each of
