@@ -19,9 +19,10 @@
 //                   per-block sums of squares
 // then the value network (also every minibatch of auv_ppo_fit_value):
 //   k_vtile         per 16-sample tile and wave, the weights in LDS: forward, squared error,
-//                   dz2, dz1; the bias and output-weight gradient sums; half fragments of
-//                   q(x), q(h1), q(dz2), q(dz1) for the weight-gradient product
-//   k_vwgrad        dW2 and dW1 per (64-row block, chunk of the minibatch)
+//                   dz2, dz1; the bias and output-weight gradient sums; q(x) as the layer-1
+//                   operand and half fragments of q(dz2), q(dz1) for the weight-gradient product
+//   k_vwgrad        dW2 and dW1 per (64- or 128-row block, chunk of the minibatch), q(h1)
+//                   recomputed from q(x)
 //   k_reduce        as above (with the Adam step fused in a value-only fit)
 // and last
 //   k_finalize      loss statistics, gradient norms, the clipping factor
@@ -85,10 +86,12 @@ struct Work {
   float* part_b1;       // [G][256]
   float* part_w2;       // [G][256 m][256 k]
   float* part_ss;       // [2 nets][reduce blocks]
-  // value-only gradient (k_vtile / k_vwgrad): half fragments of one minibatch
-  u32x2* h1_half;       // [Bp/16][16 feature tiles][64 lanes] q(h1)
-  u32x2* dz1_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz1)
-  u32x2* x_half;        // [Bp/16][2 input tiles][64 lanes] q(x)
+  // value-only gradient (k_vtile / k_vwgrad) of one minibatch
+  u32x2* dz1_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz1) half fragments
+  bf16x8* x_frag;       // [Bp/16][64 lanes] q(x) as the layer-1 operand (lane (g, r): inputs
+                        // kslot(g, j) of sample r, zero past the 23 inputs and the batch)
+  u32x2* h1_half;       // [Bp/16][16 feature tiles][64 lanes] q(h1) half fragments, stored only
+                        // below VW_RECOMP_STEPS steps (above, k_vwgrad recomputes q(h1))
 };
 
 constexpr int MAX_GROUPS = 256;
@@ -104,15 +107,19 @@ inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * H
 inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_ELEMS; }
 
 // Byte offsets of the workspace parts for a minibatch of B; returns the total.
+// From this many 32-sample steps on, the value-only weight gradient recomputes q(h1) instead
+// of storing it (see k_vwgrad).
+constexpr int VW_RECOMP_STEPS = 4096;
 constexpr int WORK_PARTS = 16;
 inline size_t work_layout(int B, size_t off[WORK_PARTS]) {
   const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
+  const bool recomp = (int)(Bp / 32) >= VW_RECOMP_STEPS;
   const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS,
                             Bp * HID * 2, Bp * HID * 2,
                             G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
                             G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
                             2 * (size_t)red_blocks(8) * 4,
-                            Bp * HID * 2, Bp * HID * 2, Bp * 32 * 2};
+                            Bp * HID * 2, Bp / 16 * 64 * 16, recomp ? 0 : Bp * HID * 2};
   size_t o = 0;
   for (int k = 0; k < WORK_PARTS; ++k) {
     off[k] = o;
@@ -139,9 +146,9 @@ inline Work work_at(void* base, int B) {
   W.part_b1 = (float*)(p + off[10]);
   W.part_w2 = (float*)(p + off[11]);
   W.part_ss = (float*)(p + off[12]);
-  W.h1_half = (u32x2*)(p + off[13]);
-  W.dz1_half = (u32x2*)(p + off[14]);
-  W.x_half = (u32x2*)(p + off[15]);
+  W.dz1_half = (u32x2*)(p + off[13]);
+  W.x_frag = (bf16x8*)(p + off[14]);
+  W.h1_half = (u32x2*)(p + off[15]);
   return W;
 }
 
@@ -814,10 +821,12 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
 // in two kernels and without a 256 x 256 partial per tile workgroup:
 //   k_vtile   one wave per 16-sample tile, the network's bf16 weights in LDS: forward, squared
 //             error, dz2 and dz1 (tanh derivatives from the fp32 activations); db1, db2, dW3,
-//             db3 and the error sum per workgroup; q(x), q(h1), q(dz2), q(dz1) stored as half
-//             fragments (lane (g, r): feature r of a 16-feature tile, samples 4 g .. 4 g + 3)
+//             db3 and the error sum per workgroup; q(x) stored as the layer-1 operand, q(dz2)
+//             and q(dz1) as half fragments (lane (g, r): feature r of a 16-feature tile,
+//             samples 4 g .. 4 g + 3)
 //   k_vwgrad  dW2 = q(dz2) q(h1)^T and dW1 = q(dz1) q(x)^T, a product over the samples, one
-//             partial per chunk of the minibatch
+//             partial per chunk of the minibatch; q(h1) recomputed from q(x) with layer 1's
+//             arithmetic, so that it has the forward's bits
 // then k_reduce (and with it the fused Adam step) as for the other gradients.
 //
 // Layer 1 runs feature-major (D = W1 X: lane (g, r) gets features 4 g + i of an M-tile at
@@ -832,7 +841,7 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
 // exact (one nonzero product per output).
 constexpr int VT_WAVES = 8;
 constexpr int VW_WAVES = 8;
-constexpr int VW_MAX_CHUNKS = 64;
+constexpr int VW_MAX_CHUNKS = 128;
 
 struct VtWeights {
   bf16x8 w1[16][64];      // layer 1 A fragments [M-tile][lane] (K = the 32 padded inputs)
@@ -910,6 +919,7 @@ __device__ __forceinline__ u32x2 pack4(const f32x4& v) {
   return __builtin_bit_cast(u32x2, q);
 }
 
+template <bool H1>
 __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __restrict__ w, const float* __restrict__ b,
                                                             Batch D, const int32_t* __restrict__ idx, int B, int tiles,
                                                             Hp hp, Work W) {
@@ -1010,8 +1020,7 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     bf16x8 x;
 #pragma unroll
     for (int j = 0; j < 8; ++j) x[j] = (__bf16)((vr && kslot(g, j) < 23) ? cur.x[j] : 0.0f);
-    W.x_half[((size_t)t * 2) * 64 + lane] = pack4(mfma(x, select_frag(g, r, 0), zero));
-    W.x_half[((size_t)t * 2 + 1) * 64 + lane] = pack4(mfma(x, select_frag(g, r, 1), zero));
+    W.x_frag[(size_t)t * 64 + lane] = x;
 
     // ---- layer 1, feature-major: the pairs h1[kt] (features 32 kt + kslot(g, j), sample r)
     bf16x8 h1[8];
@@ -1021,10 +1030,12 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
       const f32x4 bb = *reinterpret_cast<const f32x4*>(&S.b1k[32 * kt + 16 + 4 * g]);
       h1[kt] = act_frag(mfma(S.w1[2 * kt][lane], x, zero), mfma(S.w1[2 * kt + 1][lane], x, zero), ba, bb);
     }
+    if (H1) {   // q(h1) as half fragments, for the weight-gradient product of small minibatches
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt) {
-      W.h1_half[(tb + 2 * kt) * 64 + lane] = pack4(mfma(h1[kt], select_frag(g, r, 0), zero));
-      W.h1_half[(tb + 2 * kt + 1) * 64 + lane] = pack4(mfma(h1[kt], select_frag(g, r, 1), zero));
+      for (int kt = 0; kt < 8; ++kt) {
+        W.h1_half[(tb + 2 * kt) * 64 + lane] = pack4(mfma(h1[kt], select_frag(g, r, 0), zero));
+        W.h1_half[(tb + 2 * kt + 1) * 64 + lane] = pack4(mfma(h1[kt], select_frag(g, r, 1), zero));
+      }
     }
 
     // ---- layer 2, sample-major (z2 feature 16 nt + r, samples 4 g + i), and the value
@@ -1177,89 +1188,176 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
 }
 
 // dW2 = q(dz2) q(h1)^T and dW1 = q(dz1) q(x)^T over the 32-sample steps of one chunk of the
-// minibatch, for one block of 64 gradient rows: workgroup (row block p, chunk c), eight
-// waves; wave w accumulates rows 64 p .. + 63 x dW2 columns 32 w .. + 31 (8 accumulators) and
-// the dW1 tile (rows 64 p + 16 (w % 4), inputs 16 (w / 4)).  The q(dz2), q(dz1) and q(x)
-// fragments of a step are shared through LDS (two buffers, one barrier per step); each wave
-// loads its own q(h1) fragments.  A step's nine products take far less than a load's
-// latency, so each thread's loads run VW_DEPTH steps ahead in a ring of register sets, issued
-// unconditionally (step index clamped) so that every wait covers only its own set.  The four
-// row blocks of a chunk are workgroups 8 apart, which the dispatcher places on one XCD, so
-// that their common q(h1) and q(x) can come from its L2.  `chunks` is a multiple of 8;
-// grid = 4 chunks.
-constexpr int VW_DEPTH = 8;
-__global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(Work W, int steps, int chunks) {
-  __shared__ bf16x8 Ad[2][4][64];   // q(dz2) A fragments: rows 64 p + 16 mt
-  __shared__ bf16x8 A1[2][4][64];   // q(dz1) A fragments: rows 64 p + 16 mt
-  __shared__ bf16x8 Xb[2][2][64];   // q(x) B fragments: inputs 16 it + r
+// minibatch, for one block of ROWS (64 or 128) gradient rows: workgroup (row block p, chunk
+// c), eight waves; wave w accumulates rows ROWS p .. + ROWS - 1 x dW2 columns 32 w .. + 31
+// (ROWS / 8 accumulators) and ROWS / 64 tiles of dW1 (rows ROWS p + 16 (k % MT), inputs
+// 16 (k / MT), k = w, w + 8).  The q(dz2) and q(dz1) fragments of a step are shared through
+// LDS (two buffers, one barrier per step), and so is dW1's q(x) operand, which waves 0 and 1
+// take from the stored layer-1 operand through the selection MFMA.  Each wave loads its own
+// q(h1) columns (RECOMP false) or recomputes them from that operand (RECOMP true): D = q(x)
+// W1^T (the input fragment as the A operand, W1's fragment as B) gives lane (g, r) feature
+// 16 (2 w + q) + r at samples 4 g .. 4 g + 3, the half-fragment layout of dW2's B operand,
+// with the products and the K-slot order of the forward's D = W1 q(x) (the MFMA gives the
+// same bits with its operands swapped); bias, tanh and the bf16 rounding are the forward's
+// too, so q(h1) has the forward's bits.  A step's products take far less than a load's latency, so
+// each thread's loads run DEPTH steps ahead in a ring of register sets, issued unconditionally
+// (step index clamped) so that every wait covers only its own set.  The row blocks of a chunk
+// are workgroups 8 apart, which the dispatcher places on one XCD, so that their common q(h1)
+// and q(x) come from its L2.  Every row block reads (or recomputes) all of the chunk's q(h1);
+// the rate at which the workgroups fetch from L2 bounds the kernel at the full minibatch,
+// where 128-row blocks with q(h1) recomputed take 20 % less time than 64-row blocks reading
+// it, at the price of twice the chunk partials for the same number of workgroups.  At small
+// minibatches the recomputation in four row blocks costs more than the loads it saves.
+// `chunks` is a multiple of 8; grid = (256 / ROWS) chunks.
+template <int ROWS, bool RECOMP>
+__global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __restrict__ w1, const float* __restrict__ b,
+                                                            Work W, int steps, int chunks) {
+  constexpr int MT = ROWS / 16;              // row tiles of the block
+  constexpr int NB = HID / ROWS;             // row blocks of a chunk
+  constexpr int SPW = 2 * MT / VW_WAVES;     // q(dz2) / q(dz1) row tiles staged by each wave
+  constexpr int DEPTH = ROWS == 64 ? 8 : 4;  // steps of loads in flight (register ring)
+  __shared__ bf16x8 Ad[2][MT][64];   // q(dz2) A fragments: rows ROWS p + 16 mt
+  __shared__ bf16x8 A1[2][MT][64];   // q(dz1) A fragments: rows ROWS p + 16 mt
+  __shared__ bf16x8 Xb[2][2][64];    // q(x) B fragments: inputs 16 it + r
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
   const int bid = blockIdx.x, jj = bid >> 3;
-  const int p = jj & 3, c = (jj >> 2) * 8 + (bid & 7);
+  const int p = jj % NB, c = (jj / NB) * 8 + (bid & 7);
   const int per = (steps + chunks - 1) / chunks;
   const int u0 = min(steps, c * per), u1 = min(steps, u0 + per);
-  f32x4 acc[4][2], acc1 = f32x4{0, 0, 0, 0};
+  f32x4 acc[MT][2], acc1[SPW];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) acc[mt][0] = acc[mt][1] = f32x4{0, 0, 0, 0};
+  for (int mt = 0; mt < MT; ++mt) acc[mt][0] = acc[mt][1] = f32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int k = 0; k < SPW; ++k) acc1[k] = f32x4{0, 0, 0, 0};
   if (u0 < u1) {
+    // layer 1 of this wave's q(h1) columns: B fragment lane (g, r) = W1[16 (2 w + q) + r]
+    // [kslot(g, j)] (zero past the 23 inputs), bias x 2 log2 e of feature 16 (2 w + q) + r
+    bf16x8 w1f[2];
+    float b1k[2];
+#pragma unroll
+    for (int q = 0; q < (RECOMP ? 2 : 0); ++q) {
+      const int f = 16 * (2 * w + q) + r;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = kslot(g, j);
+        w1f[q][j] = k < 23 ? bf16_of_bits(w1[f * 23 + k]) : bf16_of_bits(0);
+      }
+      b1k[q] = b[f] * TWO_LOG2E;
+    }
+    const f32x4 zero = f32x4{0, 0, 0, 0};
     auto at = [&](int tile, int ft, int nft) { return ((size_t)tile * nft + ft) * 64 + lane; };
-    // staging: wave w copies q(dz2) (w < 4) or q(dz1) (w >= 4) row tile w % 4 of the block,
-    // waves 0 and 1 also q(x) input tile w
-    const u32x2* sa = w < 4 ? W.dz2_half : W.dz1_half;
-    const int smt = 4 * p + (w & 3);
+    // staging: wave w copies the row tiles k = w + 8 s of the block's 2 MT (q(dz2) tiles, then
+    // q(dz1) tiles); the step's two q(x) fragments
     struct Step {
-      bf16x8 a, x, h[2];
+      bf16x8 a[SPW], x[2], h[RECOMP ? 1 : 2];
     };
     auto load = [&](int u, Step& R) __attribute__((always_inline)) {
       u = min(u, u1 - 1);
-      R.a = join(sa[at(2 * u, smt, 16)], sa[at(2 * u + 1, smt, 16)]);
-      if (w < 2) R.x = join(W.x_half[at(2 * u, w, 2)], W.x_half[at(2 * u + 1, w, 2)]);
 #pragma unroll
-      for (int q = 0; q < 2; ++q) R.h[q] = join(W.h1_half[at(2 * u, 2 * w + q, 16)], W.h1_half[at(2 * u + 1, 2 * w + q, 16)]);
+      for (int q = 0; q < SPW; ++q) {
+        const int k = w + VW_WAVES * q;
+        const u32x2* sa = k < MT ? W.dz2_half : W.dz1_half;
+        const int smt = MT * p + k % MT;
+        R.a[q] = join(sa[at(2 * u, smt, 16)], sa[at(2 * u + 1, smt, 16)]);
+      }
+      if (RECOMP || w < 2) {   // (without the recomputation only dW1's two staging waves need q(x))
+#pragma unroll
+        for (int h = 0; h < 2; ++h) R.x[h] = W.x_frag[(size_t)(2 * u + h) * 64 + lane];
+      }
+      if (!RECOMP) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          R.h[q % (RECOMP ? 1 : 2)] = join(W.h1_half[at(2 * u, 2 * w + q, 16)], W.h1_half[at(2 * u + 1, 2 * w + q, 16)]);
+      }
     };
-    Step R[VW_DEPTH];
+    Step R[DEPTH];
 #pragma unroll
-    for (int j = 0; j < VW_DEPTH; ++j) load(u0 + j, R[j]);
-    for (int u = u0; u < u1; u += VW_DEPTH) {
+    for (int j = 0; j < DEPTH; ++j) load(u0 + j, R[j]);
+    for (int u = u0; u < u1; u += DEPTH) {
 #pragma unroll
-      for (int j = 0; j < VW_DEPTH; ++j) {
+      for (int j = 0; j < DEPTH; ++j) {
         if (u + j < u1) {   // uniform over the workgroup
           const int buf = j & 1;   // last read in the step before the previous barrier
-          if (w < 4)
-            Ad[buf][w][lane] = R[j].a;
-          else
-            A1[buf][w - 4][lane] = R[j].a;
-          if (w < 2) Xb[buf][w][lane] = R[j].x;
+          // this wave's q(h1) B fragments of the step (tiles 2 u + h -> slots 4 h .. 4 h + 3)
+          bf16x8 hf[2];
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            if (!RECOMP) {
+              hf[q] = R[j].h[q % (RECOMP ? 1 : 2)];
+              continue;
+            }
+            u32x2 half[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const f32x4 z = mfma(R[j].x[h], w1f[q], zero);
+              f32x4 a;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) a[i] = tanh_bias(z[i], b1k[q]);
+              half[h] = pack4(a);
+            }
+            hf[q] = join(half[0], half[1]);
+          }
+#pragma unroll
+          for (int q = 0; q < SPW; ++q) {
+            const int k = w + VW_WAVES * q;
+            if (k < MT)
+              Ad[buf][k][lane] = R[j].a[q];
+            else
+              A1[buf][k - MT][lane] = R[j].a[q];
+          }
+          if (w < 2)
+            Xb[buf][w][lane] = join(pack4(mfma(R[j].x[0], select_frag(g, r, w), zero)),
+                                    pack4(mfma(R[j].x[1], select_frag(g, r, w), zero)));
           __syncthreads();
 #pragma unroll
-          for (int mt = 0; mt < 4; ++mt) {
+          for (int mt = 0; mt < MT; ++mt) {
             const bf16x8 af = Ad[buf][mt][lane];
 #pragma unroll
-            for (int q = 0; q < 2; ++q) acc[mt][q] = mfma(af, R[j].h[q], acc[mt][q]);
+            for (int q = 0; q < 2; ++q) acc[mt][q] = mfma(af, hf[q], acc[mt][q]);
           }
-          acc1 = mfma(A1[buf][w & 3][lane], Xb[buf][w >> 2][lane], acc1);
+#pragma unroll
+          for (int q = 0; q < SPW; ++q) {
+            const int k = w + VW_WAVES * q;
+            acc1[q] = mfma(A1[buf][k % MT][lane], Xb[buf][k / MT][lane], acc1[q]);
+          }
         }
-        load(u + j + VW_DEPTH, R[j]);
+        load(u + j + DEPTH, R[j]);
       }
     }
   }
   float* o2 = W.part_w2 + (size_t)c * HID * HID;
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int q = 0; q < 2; ++q)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o2[(64 * p + 16 * mt + 4 * g + i) * HID + 16 * (2 * w + q) + r] = acc[mt][q][i];
+      for (int i = 0; i < 4; ++i) o2[(ROWS * p + 16 * mt + 4 * g + i) * HID + 16 * (2 * w + q) + r] = acc[mt][q][i];
   float* o1 = W.part_w1 + (size_t)c * HID * 32;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) o1[(64 * p + 16 * (w & 3) + 4 * g + i) * 32 + 16 * (w >> 2) + r] = acc1[i];
+  for (int q = 0; q < SPW; ++q) {
+    const int k = w + VW_WAVES * q;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o1[(ROWS * p + 16 * (k % MT) + 4 * g + i) * 32 + 16 * (k / MT) + r] = acc1[q][i];
+  }
 }
 
-// Chunks of the value-only weight gradient: 8 to VW_MAX_CHUNKS, about one per 16 steps.
-inline int vw_chunks(int steps) {
+// Chunks of the value-only weight gradient and its row-block height: from VW_RECOMP_STEPS
+// steps of 32 samples up, 128-row blocks with q(h1) recomputed and about one chunk per 64
+// steps (up to 128 chunks, 256 workgroups); below that, 64-row blocks reading the stored
+// q(h1) and about one chunk per 16 steps (8 to 64 chunks), which keeps the chunk partials
+// small against the data at the small sizes.
+struct VwPlan {
+  int rows, chunks;
+};
+inline VwPlan vw_plan(int steps) {
+  if (steps >= VW_RECOMP_STEPS) {
+    const int c = (steps / 64 + 7) / 8 * 8;
+    return {128, c > VW_MAX_CHUNKS ? VW_MAX_CHUNKS : c};
+  }
   const int c = (steps / 16 + 7) / 8 * 8;
-  return c < 8 ? 8 : (c > VW_MAX_CHUNKS ? VW_MAX_CHUNKS : c);
+  return {64, c < 8 ? 8 : (c > 64 ? 64 : c)};
 }
 
 // One Adam step of packed entry e with gradient g (k_adam's update; the bf16 copy of the
@@ -1531,10 +1629,19 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
   }
   // value network: per-tile forward / backward, the weight-gradient product, the reduce
   const int GV = std::min(cus, (tiles + ppo::VT_WAVES - 1) / ppo::VT_WAVES);
-  const int chunks = ppo::vw_chunks(steps);
-  hipLaunchKernelGGL(ppo::k_vtile, dim3(GV), dim3(64 * ppo::VT_WAVES), 0, s, value->w, value->b, D, idx, B, tiles, hp,
-                     W);
-  hipLaunchKernelGGL(ppo::k_vwgrad, dim3(4 * chunks), dim3(64 * ppo::VW_WAVES), 0, s, W, steps, chunks);
+  const ppo::VwPlan vp = ppo::vw_plan(steps);
+  const int chunks = vp.chunks;
+  if (vp.rows == 128) {
+    hipLaunchKernelGGL(ppo::k_vtile<false>, dim3(GV), dim3(64 * ppo::VT_WAVES), 0, s, value->w, value->b, D, idx, B,
+                       tiles, hp, W);
+    hipLaunchKernelGGL((ppo::k_vwgrad<128, true>), dim3(2 * chunks), dim3(64 * ppo::VW_WAVES), 0, s, value->w,
+                       value->b, W, steps, chunks);
+  } else {
+    hipLaunchKernelGGL(ppo::k_vtile<true>, dim3(GV), dim3(64 * ppo::VT_WAVES), 0, s, value->w, value->b, D, idx, B,
+                       tiles, hp, W);
+    hipLaunchKernelGGL((ppo::k_vwgrad<64, false>), dim3(4 * chunks), dim3(64 * ppo::VW_WAVES), 0, s, value->w,
+                       value->b, W, steps, chunks);
+  }
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, GV, chunks, GV, chunks, W, 0.0f,
                      grad_value, W.part_ss + rb, fuse);
   if (finalize)
