@@ -962,19 +962,21 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
   In cur = load_in(load_idx(min(t, tiles - 1)));   // in flight while the weights are staged
   {   // weights -> A fragments (lane (g, r) of fragment (M-tile, K tile) holds row 16 mt + r,
       // inputs 32 kt + kslot(g, j); W2's at slot w2_slot(lane)); every load is issued before
-      // the first LDS store, so that the loads overlap
+      // the first LDS store, so that the loads overlap.  W2 is read in 16-byte pieces of a row
+      // (32 consecutive threads per row: every wave load is 1 KiB of two whole rows); the
+      // piece of row 16 mt + r at columns 32 kt + o .. + 7 (o = 0, 8, 16, 24) is the half o / 16
+      // (K slots 4 (o / 16) .. + 3) of lanes 16 g + r and 16 (g + 1) + r, g = (o % 16) / 4.
     const uint16_t* W1 = w;
     const uint16_t* W2 = w + HID * 23;
     const uint16_t* W3 = W2 + HID * HID;
-    constexpr int P2 = 16 * 8 * 64 / (64 * VT_WAVES), P1 = 16 * 64 / (64 * VT_WAVES);
-    uint2 v2[P2][2];
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    constexpr int P2 = HID * HID / 8 / (64 * VT_WAVES), P1 = 16 * 64 / (64 * VT_WAVES);
+    u32x4 v2[P2];
     uint16_t v1[P1][8];
 #pragma unroll
-    for (int q = 0; q < P2; ++q) {   // W2 row 16 mt + r, columns 32 kt + 4 g .. + 3 and + 16
-      const int e = tid + q * 64 * VT_WAVES, f = e >> 6, l = e & 63;
-      const uint16_t* row = W2 + (16 * (f >> 3) + (l & 15)) * HID + 32 * (f & 7) + 4 * (l >> 4);
-      v2[q][0] = *reinterpret_cast<const uint2*>(row);
-      v2[q][1] = *reinterpret_cast<const uint2*>(row + 16);
+    for (int q = 0; q < P2; ++q) {
+      const int e = tid + q * 64 * VT_WAVES;
+      v2[q] = *reinterpret_cast<const u32x4*>(W2 + (e >> 5) * HID + 8 * (e & 31));
     }
 #pragma unroll
     for (int q = 0; q < P1; ++q) {
@@ -987,9 +989,11 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     }
 #pragma unroll
     for (int q = 0; q < P2; ++q) {
-      const int e = tid + q * 64 * VT_WAVES, f = e >> 6, l = e & 63;
-      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-      S.w2[f >> 3][f & 7][w2_slot(l)] = __builtin_bit_cast(bf16x8, u32x4{v2[q][0].x, v2[q][0].y, v2[q][1].x, v2[q][1].y});
+      const int e = tid + q * 64 * VT_WAVES, rw = e >> 5, c = 8 * (e & 31);
+      const int o = c & 31, g0 = (o & 15) >> 2, rr = rw & 15;
+      char* frag = reinterpret_cast<char*>(&S.w2[rw >> 4][c >> 5][0]) + 8 * (o >> 4);
+      *reinterpret_cast<uint2*>(frag + 16 * w2_slot(16 * g0 + rr)) = uint2{v2[q].x, v2[q].y};
+      *reinterpret_cast<uint2*>(frag + 16 * w2_slot(16 * (g0 + 1) + rr)) = uint2{v2[q].z, v2[q].w};
     }
 #pragma unroll
     for (int q = 0; q < P1; ++q) {
