@@ -210,6 +210,27 @@ def test_ppo_full_minibatch_size(setup):
     assert st[4] == pytest.approx(want["clip_frac"], abs=0.5 / B)
 
 
+def test_ppo_grad_ragged_past_the_recompute_switch(setup):
+    """131072 - 100 samples: padded to 4096 steps of 32, where the value net's weight gradient
+    switches to 128-row blocks with q(h1) recomputed from q(x); 100 padding samples run through
+    that path (zero dz2, tanh(b1) as q(h1)) and must add nothing.  Every gradient tensor
+    against the oracle."""
+    netp, netv, pol, val, _, _, _, PpoLearner = setup
+    B = 131072 - 100
+    M = B + 16 * 64 + 5
+    announce(f"ppo ragged minibatch past the recompute switch B={B} M={M}")
+    buf = _buffer(M, 21, pol)
+    dev = {k: torch.from_numpy(np.ascontiguousarray(v)).cuda() for k, v in buf.items()}
+    L = PpoLearner(netp, netv)
+    idx = np.random.default_rng(21).permutation(M)[:B].astype(np.int32)
+    L.grad(L.batch(dev["obs"], dev["act"], dev["logp"], dev["adv"], dev["ret"]), torch.from_numpy(idx).cuda())
+    cols = idx.astype(np.int64)
+    want = oppo.ppo_loss_grad(buf["obs"][:, cols], buf["act"][:, cols], buf["logp"][cols], buf["adv"][cols],
+                              buf["ret"][cols], pol, val, quantize=True)
+    _check_grads(host(L.pol.grad), want["grad_pol"], 8, "policy")
+    _check_grads(host(L.val.grad), want["grad_val"], 1, "value")
+
+
 def test_adam_writes_the_weights_the_rollout_reads(setup):
     """After an Adam step the auv_mlp view of a PpoNet (bf16 copy + fp32 tail of theta) is the
     updated network: auv_mlp_forward through it matches the oracle forward of the updated
