@@ -1253,7 +1253,8 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
     const f32x4 zero = f32x4{0, 0, 0, 0};
     auto at = [&](int tile, int ft, int nft) { return ((size_t)tile * nft + ft) * 64 + lane; };
     // staging: wave w copies the row tiles k = w + 8 s of the block's 2 MT (q(dz2) tiles, then
-    // q(dz1) tiles); the step's two q(x) fragments
+    // q(dz1) tiles).  The step's two q(x) fragments are loaded by every wave when it recomputes
+    // q(h1), otherwise by waves 0 and 1 only (dW1's operand).
     struct Step {
       bf16x8 a[SPW], x[2], h[RECOMP ? 1 : 2];
     };
@@ -1266,14 +1267,14 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
         const int smt = MT * p + k % MT;
         R.a[q] = join(sa[at(2 * u, smt, 16)], sa[at(2 * u + 1, smt, 16)]);
       }
-      if (RECOMP || w < 2) {   // (without the recomputation only dW1's two staging waves need q(x))
+      if (RECOMP || w < 2) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) R.x[h] = W.x_frag[(size_t)(2 * u + h) * 64 + lane];
       }
-      if (!RECOMP) {
+      if constexpr (!RECOMP) {
 #pragma unroll
         for (int q = 0; q < 2; ++q)
-          R.h[q % (RECOMP ? 1 : 2)] = join(W.h1_half[at(2 * u, 2 * w + q, 16)], W.h1_half[at(2 * u + 1, 2 * w + q, 16)]);
+          R.h[q] = join(W.h1_half[at(2 * u, 2 * w + q, 16)], W.h1_half[at(2 * u + 1, 2 * w + q, 16)]);
       }
     };
     Step R[DEPTH];
@@ -1288,8 +1289,8 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
           bf16x8 hf[2];
 #pragma unroll
           for (int q = 0; q < 2; ++q) {
-            if (!RECOMP) {
-              hf[q] = R[j].h[q % (RECOMP ? 1 : 2)];
+            if constexpr (!RECOMP) {
+              hf[q] = R[j].h[q];
               continue;
             }
             u32x2 half[2];
