@@ -521,6 +521,8 @@ def main() -> int:
                     help="only measure the headline rollout at 64 to 65536 envs and print it")
     ap.add_argument("--probe-rates", action="store_true",
                     help="only measure the exp / rcp / fma / bf16 MFMA unit rates (auv_probe_rate) and print them")
+    ap.add_argument("--no-spin-up", action="store_true",
+                    help="skip the 0.4 s of headline rollouts run before anything is measured")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -544,7 +546,8 @@ def main() -> int:
     from paper_2512_13359_amd import AuvEnv, upload_mlp
 
     torch.cuda.set_device(0)
-    spin_up()
+    if not args.no_spin_up:
+        spin_up()
     if args.ppo_only:
         print(json.dumps({"ppo": ppo_measure()}), flush=True)
         return 0
