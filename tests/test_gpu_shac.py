@@ -462,6 +462,47 @@ def test_ppo_fit_value_back_to_back_calls():
     assert torch.equal(g1, g2) and torch.equal(s1, s2)
 
 
+def test_ppo_fit_value_large_minibatches_match_stepwise_calls():
+    """Minibatches of 131072 samples (4096 steps of 32: the value-only weight gradient in its
+    128-row form with q(h1) recomputed, 64 chunks, then the reduce with the fused Adam step):
+    auv_ppo_fit_value equals the same gradient + Adam calls issued one at a time, bit for bit.
+    Synthetic seeded batch of 262144 samples, two passes of two minibatches."""
+    require_gpu()
+    from paper_2512_13359_amd import _abi as A
+    from paper_2512_13359_amd.ppo import PpoNet
+    M, iterations, batches, seed = 262144, 2, 2, 777
+    announce(f"PPO fit value large minibatches M={M} batches={batches} iterations={iterations}")
+    rng = np.random.default_rng(31)
+    obs = torch.from_numpy(rng.standard_normal((23, M)).astype(np.float32)).cuda()
+    val_old = torch.from_numpy(rng.standard_normal(M).astype(np.float32)).cuda()
+    adv = torch.from_numpy(rng.standard_normal(M).astype(np.float32)).cuda()
+    ret = torch.from_numpy(rng.standard_normal(M).astype(np.float32)).cuda()
+    batch = A.make_ppo_batch(obs, obs, val_old, adv, ret, M)
+    cfg = A.make_ppo_config(vf_coef=2.0, ent_coef=0.0, max_grad_norm=0.0, lr=1e-3, normalize_adv=False)
+    val = W.mlp_weights(1, W.VALUE_SEED)
+    net1, net2 = PpoNet(val, "cuda"), PpoNet(val, "cuda")
+    work = torch.empty(A.auv_ppo_fit_work_bytes(M, batches), dtype=torch.uint8, device="cuda")
+    stage = torch.empty(2 * M, dtype=torch.int32, pin_memory=True)
+    g1, s1 = torch.zeros(A.ppo_nparam(1), device="cuda"), torch.zeros(8, device="cuda")
+    A.auv_ppo_fit_value(cfg, net1.mlp, net1.net, batch, iterations, batches, seed, 0, stage, g1, s1, work)
+    B = M // batches
+    g2, s2 = torch.zeros_like(g1), torch.zeros_like(s1)
+    w2 = torch.empty(A.auv_ppo_work_bytes(B), dtype=torch.uint8, device="cuda")
+    t = 0
+    for order in _fit_indices(M, iterations, seed):
+        idx = torch.from_numpy(order).cuda()
+        for j in range(batches):
+            A.auv_ppo_grad(cfg, None, net2.mlp, batch, idx[j * B:(j + 1) * B], B, None, g2, s2, w2)
+            t += 1
+            A.auv_ppo_adam(cfg, t, None, net2.net, None, g2, s2)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(net1.theta).all())
+    d = (net1.theta - net2.theta).abs()
+    assert torch.equal(net1.theta, net2.theta), (float(d.max()), int((d > 0).sum()), int(d.numel()))
+    assert torch.equal(net1.w_bf16, net2.w_bf16)
+    assert torch.equal(g1, g2) and torch.equal(s1, s2)
+
+
 def test_ppo_fit_value_matches_stepwise_calls():
     """auv_ppo_fit_value equals the same value-only gradient + Adam steps issued one call at
     a time with the shuffles restated in Python (bit for bit; the index uploads reuse each of
