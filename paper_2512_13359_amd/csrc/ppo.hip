@@ -3,30 +3,24 @@
 // Sec. III-A1), its gradient through both 23-256-256-n_out networks on bf16 MFMA, global-norm
 // gradient clipping and Adam (Kingma and Ba, Algorithm 1).
 //
-// Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 128); the
-// policy network:
+// Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 128); for the
+// policy network first:
 //   k_adv_partial   per-block sums of the minibatch's advantages and their squares (fp64)
 //   k_adv_final     mean and 1 / (std + 1e-8) from those sums
-//   k_fwd_bwd<n>    per 16-sample tile: forward, loss, dL/dy, dz2 = (W3^T q(dL/dy)) (1 - h2^2);
-//                   writes q(dz2) for the next two kernels; accumulates dW3, db2,
-//                   db3, d log_std and the loss sums per workgroup
-//   k_dz1           per tile: dh1 = W2^T q(dz2), dz1 = dh1 (1 - h1^2) with h1 recomputed from
-//                   the input; accumulates dW1 = q(dz1) q(x)^T and db1 per workgroup
-//   k_dw2           dW2 = q(dz2) q(h1)^T with q(h1) recomputed from the inputs, split over the
-//                   samples (K), one 256 x 256 partial
-//                   per workgroup held in accumulator registers
-//   k_reduce        fixed-order sums of the per-workgroup partials -> packed gradient, and
-//                   per-block sums of squares
-// then the value network (also every minibatch of auv_ppo_fit_value):
-//   k_vtile         per 16-sample tile and wave, the weights in LDS: forward, squared error,
-//                   dz2, dz1; the bias and output-weight gradient sums; q(x) as the layer-1
-//                   operand and half fragments of q(dz2), q(dz1) for the weight-gradient product
+// then for each network (the value net alone in every minibatch of auv_ppo_fit_value):
+//   k_vtile<n>      per 16-sample tile and wave, the weights in LDS: forward, loss (clipped
+//                   surrogate for n = 8, squared error for n = 1), dL/dy, dz2, dz1; the sums of
+//                   the bias and output-layer gradients (and of d log sigma and the loss
+//                   statistics); q(x) as the layer-1 operand and half fragments of q(dz2),
+//                   q(dz1) for the weight-gradient product
 //   k_vwgrad        dW2 and dW1 per (64- or 128-row block, chunk of the minibatch), q(h1)
-//                   recomputed from q(x)
-//   k_reduce        as above (with the Adam step fused in a value-only fit)
+//                   stored or recomputed from q(x)
+//   k_reduce        fixed-order sums of the partials -> packed gradient, and per-block sums of
+//                   squares (with the Adam step fused in a value-only fit)
 // and last
 //   k_finalize      loss statistics, gradient norms, the clipping factor
 //   k_adam          one Adam step and the bf16 weight copy
+// k_dw2 (dW2 from stored q(dz2) and q(h1)) serves SHAC's actor gradient.
 // Every sum has a fixed order, so a call is bit-for-bit repeatable.
 //
 // MFMA operand layouts as in mlp_mfma.hpp (v_mfma_f32_16x16x32_bf16; lane l = 16 g + r;
@@ -35,21 +29,19 @@
 // step is sample kslot(g, j), so a lane's first four slots are samples 4g..4g+3 of the
 // first 16-sample tile and its last four the same samples of the second tile.  Activations
 // come out of a product as D fragments (lane (g, r): features 4g..4g+3 of an M-tile, sample
-// r); a per-wave LDS transpose turns them into "half fragments" (lane (g, r): feature r of a
-// 16-feature tile, samples 4g..4g+3 of a 16-sample tile, 8 bytes).
+// r) or, with the operands in the other order, as "half fragments" (lane (g, r): feature r of
+// a 16-feature tile, samples 4g..4g+3 of a 16-sample tile, 8 bytes).
 #include <cmath>
 #include <mutex>
+#include <type_traits>
 #include <vector>
 
 #include "auv_internal.hpp"
 #include "mlp_mfma.hpp"
-#include "mlp_tile.hpp"
 
 namespace auv {
 namespace ppo {
 
-constexpr int FPW = 32;             // hidden features per wave of the per-tile kernels (HID / FPW waves)
-constexpr int TPAD = 20;            // bf16 row stride of the transpose buffers (8-byte aligned rows)
 constexpr int STATS = 4;            // per-workgroup loss sums: surrogate, log-ratio, clipped count, squared error
 constexpr float LOG_2PI = 1.83787706640934548f;
 
@@ -75,7 +67,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));   // four bf16: a ha
 struct Work {
   float* advstat;       // [2] mean, 1 / (std + 1e-8)
   double* adv_part;     // [ADV_BLOCKS][2] sums of A and A^2
-  bf16x8* dz2_frag;     // [Bp/16][8 K tiles][64 lanes] q(dz2) as layer-2 B fragments
   u32x2* dz2_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz2) half fragments
   float* part_w3t;      // [G][256 f][16 j] dW3^T
   float* part_b2;       // [G][256]
@@ -86,7 +77,6 @@ struct Work {
   float* part_b1;       // [G][256]
   float* part_w2;       // [G][256 m][256 k]
   float* part_ss;       // [2 nets][reduce blocks]
-  // value-only gradient (k_vtile / k_vwgrad) of one minibatch
   u32x2* dz1_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz1) half fragments
   bf16x8* x_frag;       // [Bp/16][64 lanes] q(x) as the layer-1 operand (lane (g, r): inputs
                         // kslot(g, j) of sample r, zero past the 23 inputs and the batch)
@@ -100,22 +90,21 @@ constexpr int ADV_BLOCKS = 256;
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr int DW2_WAVES = 8, DW2_DEPTH = 4;
-// Minibatch padded to whole rounds of the dW2 loop (DW2_DEPTH steps of 32 samples); padding
-// samples carry zero dz2 and so add nothing.
+// Minibatch padded to a multiple of 128 samples (whole rounds of four 32-sample steps of the
+// weight-gradient products); padding samples carry zero dz2 and dz1 and so add nothing.
 inline int padded(int B) { return (B + 32 * DW2_DEPTH - 1) / (32 * DW2_DEPTH) * (32 * DW2_DEPTH); }
 inline int nparam(int n_out) { return HID * 23 + HID * HID + n_out * HID + 2 * HID + n_out + (n_out == 8 ? 8 : 0); }
 inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_ELEMS; }
 
 // Byte offsets of the workspace parts for a minibatch of B; returns the total.
-// From this many 32-sample steps on, the value-only weight gradient recomputes q(h1) instead
-// of storing it (see k_vwgrad).
+// From this many 32-sample steps on, the weight-gradient product recomputes q(h1) instead of
+// storing it (see k_vwgrad).
 constexpr int VW_RECOMP_STEPS = 4096;
-constexpr int WORK_PARTS = 16;
+constexpr int WORK_PARTS = 15;
 inline size_t work_layout(int B, size_t off[WORK_PARTS]) {
   const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
   const bool recomp = (int)(Bp / 32) >= VW_RECOMP_STEPS;
-  const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS,
-                            Bp * HID * 2, Bp * HID * 2,
+  const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS, Bp * HID * 2,
                             G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
                             G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
                             2 * (size_t)red_blocks(8) * 4,
@@ -135,20 +124,19 @@ inline Work work_at(void* base, int B) {
   Work W;
   W.advstat = (float*)(p + off[0]);
   W.adv_part = (double*)(p + off[1]);
-  W.dz2_frag = (bf16x8*)(p + off[2]);
-  W.dz2_half = (u32x2*)(p + off[3]);
-  W.part_w3t = (float*)(p + off[4]);
-  W.part_b2 = (float*)(p + off[5]);
-  W.part_b3 = (float*)(p + off[6]);
-  W.part_ls = (float*)(p + off[7]);
-  W.part_stats = (float*)(p + off[8]);
-  W.part_w1 = (float*)(p + off[9]);
-  W.part_b1 = (float*)(p + off[10]);
-  W.part_w2 = (float*)(p + off[11]);
-  W.part_ss = (float*)(p + off[12]);
-  W.dz1_half = (u32x2*)(p + off[13]);
-  W.x_frag = (bf16x8*)(p + off[14]);
-  W.h1_half = (u32x2*)(p + off[15]);
+  W.dz2_half = (u32x2*)(p + off[2]);
+  W.part_w3t = (float*)(p + off[3]);
+  W.part_b2 = (float*)(p + off[4]);
+  W.part_b3 = (float*)(p + off[5]);
+  W.part_ls = (float*)(p + off[6]);
+  W.part_stats = (float*)(p + off[7]);
+  W.part_w1 = (float*)(p + off[8]);
+  W.part_b1 = (float*)(p + off[9]);
+  W.part_w2 = (float*)(p + off[10]);
+  W.part_ss = (float*)(p + off[11]);
+  W.dz1_half = (u32x2*)(p + off[12]);
+  W.x_frag = (bf16x8*)(p + off[13]);
+  W.h1_half = (u32x2*)(p + off[14]);
   return W;
 }
 
@@ -162,10 +150,6 @@ __device__ __forceinline__ float row_sum16(float v) {
   return v;
 }
 
-__device__ __forceinline__ u32x2 half_of(const __bf16* T, int row, int g) {
-  return *reinterpret_cast<const u32x2*>(&T[row * TPAD + 4 * g]);
-}
-
 // Eight bf16 from two half fragments (first: K slots 0-3, second: slots 4-7).
 __device__ __forceinline__ bf16x8 join(u32x2 a, u32x2 b) {
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -174,37 +158,10 @@ __device__ __forceinline__ bf16x8 join(u32x2 a, u32x2 b) {
 
 __device__ __forceinline__ bf16x8 low_half(u32x2 a) { return join(a, u32x2{0u, 0u}); }
 
-// D-fragment values v[mt][i] (feature 16 mt + 4 g + i, sample r), rounded to bf16, into
-// this wave's transpose buffer T[feature][sample].
-template <int MT>
-__device__ __forceinline__ void put_d(__bf16* T, int g, int r, const f32x4 v[MT]) {
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) T[(16 * mt + 4 * g + i) * TPAD + r] = (__bf16)v[mt][i];
-}
-
-// The same for B fragments of KO K tiles (feature 32 kt + kslot(g, j), sample r).
-template <int KO>
-__device__ __forceinline__ void put_b(__bf16* T, int g, int r, const bf16x8 f[KO]) {
-#pragma unroll
-  for (int kt = 0; kt < KO; ++kt)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) T[(32 * kt + kslot(g, j)) * TPAD + r] = f[kt][j];
-}
-
 // Buffer sample of minibatch entry b (indices outside [0, M) are clamped into it).
 __device__ __forceinline__ int sample_of(const int32_t* __restrict__ idx, int b, int M) {
   return min(max(idx[b], 0), M - 1);
 }
-
-// What lane (g, r) reads of tile sample r: observation rows kslot(g, j), action rows
-// 4g .. 4g+3 (policy lanes g < 2), log-prob, advantage and return.  Every load is issued
-// unconditionally from a valid address (rows and entries clamped), so a tile's loads can be
-// in flight while the previous tile is computed; what lies outside is masked on use.
-struct TileIn {
-  float x[8], a[4], lp, ad, rt;
-};
 
 // Raw index of entry r of tile t (entries past B read entry B - 1).  Loaded a tile ahead of
 // its use, unconditionally, and clamped into [0, M) only where it is used.
@@ -213,27 +170,6 @@ __device__ __forceinline__ int raw_index(const int32_t* __restrict__ idx, int t,
 }
 
 __device__ __forceinline__ int clamp_sample(int raw, int M) { return min(max(raw, 0), M - 1); }
-
-template <bool POLICY, bool VALUE>
-__device__ __forceinline__ void tile_in_load(const Batch& D, int s, int g, TileIn& in) {
-  const size_t M = D.M, ss = (size_t)s;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(g, j), 22) * M + ss];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) in.a[i] = POLICY ? D.act[(size_t)((4 * g + i) & 7) * M + ss] : 0.0f;
-  in.lp = POLICY ? D.logp[ss] : 0.0f;
-  in.ad = POLICY ? D.adv[ss] : 0.0f;
-  in.rt = VALUE ? D.ret[ss] : 0.0f;
-}
-
-// Layer-1 operand: input features kslot(g, j), zero beyond the 23 inputs and for padding
-// samples.
-__device__ __forceinline__ bf16x8 input_frag(const TileIn& in, bool valid, int g) {
-  bf16x8 x;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) x[j] = (__bf16)((valid && kslot(g, j) < 23) ? in.x[j] : 0.0f);
-  return x;
-}
 
 // ------------------------------------------------------------------ kernels ----------
 // Advantage sums over the minibatch: block k sums entries k*256 + tid (stride 256 blocks x
@@ -284,398 +220,24 @@ __global__ __launch_bounds__(64) void k_adv_final(const double* __restrict__ par
   }
 }
 
-template <int FPW>
-struct FwdShared {
-  static constexpr int NWV = HID / FPW;
-  bf16x8 h[8][64];             // hidden-1 tiles of the current sample tile [K tile][lane]
-  f32x4 o[NWV][64];            // output split-K partials [wave][lane]
-  float b1k[HID];
-  float b3[16];
-  __bf16 T[NWV][FPW * TPAD];   // per-wave transpose buffer [feature][sample]
-  __bf16 Gy[NWV][8 * TPAD];    // per-wave q(dL/dy) transposed [output row][sample]
-};
-
-// Forward, loss and the output-side backward of one network over 16-sample tiles: HID / FPW
-// waves, wave m owning hidden features FPW m .. FPW m + FPW - 1 (MT = FPW / 16 M-tiles, KO =
-// FPW / 32 K tiles of the next layer).  NOUT = 8: the policy and the clipped surrogate;
-// NOUT = 1: the value net and the squared error.
-template <int NOUT, int FPW>
-__global__ __launch_bounds__(64 * HID / FPW, 1) void k_fwd_bwd(const uint16_t* __restrict__ w, const float* __restrict__ b,
-                                                         const float* __restrict__ log_std, Batch D,
-                                                         const int32_t* __restrict__ idx, int B, int tiles, Hp hp,
-                                                         Work W, int net) {
-  constexpr int NWV = HID / FPW, MT = FPW / 16, KO = FPW / 32;
-  __shared__ FwdShared<FPW> S;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = lane >> 4, r = lane & 15;
-  TileMlpRegs<FPW> R;
-  tile_mlp_load<FPW>(w, b, NOUT, m, lane, R);
-  // W3^T fragments: A[f = FPW m + 16 mt + r][slot (g, j)] = W3[kslot(g, j)][f]
-  const uint16_t* W3 = w + HID * 23 + HID * HID;
-  bf16x8 w3t[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = kslot(g, j);
-      w3t[mt][j] = k < NOUT ? bf16_of_bits(W3[k * HID + FPW * m + 16 * mt + r]) : bf16_of_bits(0);
-    }
-  if (tid < HID) S.b1k[tid] = b[tid] * TWO_LOG2E;
-  if (tid < 16) S.b3[tid] = tid < NOUT ? b[2 * HID + tid] : 0.0f;
-  // policy: this lane's four action rows 4g .. 4g+3 (lanes g < 2)
-  float ls[4] = {0, 0, 0, 0}, ivar[4] = {0, 0, 0, 0};
-  if (NOUT == 8 && g < 2) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ls[i] = log_std[4 * g + i];
-      ivar[i] = expf(-2.0f * ls[i]);
-    }
-  }
-  float mean = 0.0f, inv_std = 1.0f;
-  if (NOUT == 8 && hp.normalize) {
-    mean = W.advstat[0];
-    inv_std = W.advstat[1];
-  }
-  f32x4 dw3[MT], db2[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) dw3[mt] = db2[mt] = f32x4{0, 0, 0, 0};
-  float db3[4] = {0, 0, 0, 0}, dls[4] = {0, 0, 0, 0}, st[STATS] = {0, 0, 0, 0};
-  __bf16* T = S.T[m];
-  __bf16* Gy = S.Gy[m];
-  const int Mi = (int)D.M;
-  // inputs of this workgroup's first tile, and the raw indices of its second.  Every
-  // prefetch below is unconditional (tile and entry indices clamped): a load under a branch
-  // whose result is used at the join would make the wave wait for all loads in flight.
-  TileIn cur;
-  tile_in_load<NOUT == 8, NOUT == 1>(D, clamp_sample(raw_index(idx, blockIdx.x, r, B), Mi), g, cur);
-  int raw_nxt = raw_index(idx, blockIdx.x + gridDim.x, r, B);
-  __syncthreads();
-
-  // The tile body is peeled for the workgroup's first tile so that every path into the
-  // loop arrives with the same memory operations in flight (loads of the next tile, then
-  // this tile's stores): the waits inside then cover only the loads they need.
-  auto tile = [&](int t) __attribute__((always_inline)) {
-    const bool valid = t * 16 + r < B;
-    // next tile's inputs (its indices were loaded one tile ago) and the indices after it
-    TileIn nxt;
-    tile_in_load<NOUT == 8, NOUT == 1>(D, clamp_sample(raw_nxt, Mi), g, nxt);
-    const int raw_nxt2 = raw_index(idx, t + 2 * gridDim.x, r, B);
-    // ---- forward
-    const bf16x8 x = input_frag(cur, valid, g);
-    bf16x8 own[KO];
-    tile_layer1<FPW>(R, x, S.b1k, m, lane, own);
-#pragma unroll
-    for (int kt = 0; kt < KO; ++kt) S.h[KO * m + kt][lane] = own[kt];
-    __syncthreads();
-    f32x4 acc[MT];
-    tile_layer2_own<FPW>(R, own, acc);
-#pragma unroll
-    for (int kk = KO; kk < 8; ++kk) {
-      const bf16x8 hb = S.h[(KO * m + kk) & 7][lane];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma(R.w2[mt][kk], hb, acc[mt]);
-    }
-    f32x4 h2[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) h2[mt][i] = tanh_bias(acc[mt][i], R.b2[mt][i]);
-    bf16x8 u2[KO];
-#pragma unroll
-    for (int kt = 0; kt < KO; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        u2[kt][i] = (__bf16)h2[2 * kt][i];
-        u2[kt][4 + i] = (__bf16)h2[2 * kt + 1][i];
-      }
-    f32x4 o = f32x4{0, 0, 0, 0};
-#pragma unroll
-    for (int kt = 0; kt < KO; ++kt) o = mfma(R.w3[kt], u2[kt], o);
-    S.o[m][lane] = o;
-    put_b<KO>(T, g, r, u2);                   // q(h2) -> half fragments for dW3
-    __syncthreads();
-    f32x4 y = *reinterpret_cast<const f32x4*>(&S.b3[4 * g]);
-#pragma unroll
-    for (int ww = 0; ww < NWV; ++ww) y += S.o[ww][lane];
-
-    // ---- loss: dL/dy for this lane's output rows 4g .. 4g+3 of sample r
-    float gy[4] = {0, 0, 0, 0};
-    if (NOUT == 8) {
-      float a[4], d[4], zz[4], part = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool used = g < 2 && 4 * g + i < hp.n_act;
-        a[i] = (valid && used) ? cur.a[i] : 0.0f;
-        d[i] = used ? a[i] - y[i] : 0.0f;
-        zz[i] = d[i] * d[i] * ivar[i];
-        part += used ? -0.5f * zz[i] - ls[i] : 0.0f;
-      }
-      const float logp = part + __shfl_xor(part, 16) - 0.5f * (float)hp.n_act * LOG_2PI;   // lanes r and r + 16
-      const bool lv = valid && g < 2;
-      const float lpo = lv ? cur.lp : 0.0f;
-      const float ah = lv ? (hp.normalize ? (cur.ad - mean) * inv_std : cur.ad) : 0.0f;
-      const float rho = expf(logp - lpo);
-      const float unc = rho * ah;
-      const float clp = fminf(fmaxf(rho, 1.0f - hp.clip_eps), 1.0f + hp.clip_eps) * ah;
-      const bool active = unc <= clp;
-      const float coef = (lv && active) ? -ah * rho * hp.inv_B : 0.0f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) gy[i] = coef * d[i] * ivar[i];
-      if (m == 0) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          db3[i] += gy[i];
-          dls[i] += 4 * g + i < hp.n_act ? coef * (zz[i] - 1.0f) : 0.0f;
-        }
-        if (lv && g == 0) {
-          st[0] += -fminf(unc, clp);
-          st[1] += lpo - logp;
-          st[2] += active ? 0.0f : 1.0f;
-        }
-      }
-    } else {
-      if (valid && g == 0) {
-        const float e = y[0] - cur.rt;
-        gy[0] = hp.vf_coef * hp.inv_B * e;
-        if (m == 0) {
-          db3[0] += gy[0];
-          st[3] += e * e;
-        }
-      }
-    }
-    bf16x8 gyf;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) gyf[j] = (__bf16)(j < 4 ? gy[j] : 0.0f);
-
-    // ---- dW3^T += q(h2) q(gy)^T over the tile's samples (K slots 4..7 empty)
-    if (g < 2) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) Gy[(4 * g + i) * TPAD + r] = gyf[i];
-    }
-    const bf16x8 bgy = r < NOUT ? low_half(half_of(Gy, r, g)) : bf16x8{};
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) dw3[mt] = mfma(low_half(half_of(T, 16 * mt + r, g)), bgy, dw3[mt]);
-
-    // ---- dz2 = (W3^T q(gy)) (1 - h2^2), this wave's features
-    f32x4 dz[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const f32x4 dh = mfma(w3t[mt], gyf, f32x4{0, 0, 0, 0});
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dz[mt][i] = dh[i] * (1.0f - h2[mt][i] * h2[mt][i]);
-      db2[mt] += dz[mt];
-    }
-#pragma unroll
-    for (int kt = 0; kt < KO; ++kt) {         // layer-2 B fragments of this wave's K tiles
-      bf16x8 f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f[i] = (__bf16)dz[2 * kt][i];
-        f[4 + i] = (__bf16)dz[2 * kt + 1][i];
-      }
-      W.dz2_frag[((size_t)t * 8 + KO * m + kt) * 64 + lane] = f;
-    }
-    put_d<MT>(T, g, r, dz);
-#pragma unroll
-    for (int ft = 0; ft < MT; ++ft) W.dz2_half[((size_t)t * 16 + MT * m + ft) * 64 + lane] = half_of(T, 16 * ft + r, g);
-    cur = nxt;
-    raw_nxt = raw_nxt2;
-  };
-  if ((int)blockIdx.x < tiles) {
-    tile(blockIdx.x);
-    for (int t = blockIdx.x + gridDim.x; t < tiles; t += gridDim.x) tile(t);
-  }
-
-  // ---- per-workgroup partials
-  const int wg = blockIdx.x;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int f = FPW * m + 16 * mt + 4 * g + i;
-      W.part_w3t[((size_t)wg * HID + f) * 16 + r] = dw3[mt][i];
-      const float v = row_sum16(db2[mt][i]);
-      if (r == 0) W.part_b2[(size_t)wg * HID + f] = v;
-    }
-  if (m == 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float v = row_sum16(db3[i]), u = row_sum16(dls[i]);
-      if (r == 0 && g < 2) {
-        W.part_b3[wg * 16 + 4 * g + i] = v;
-        W.part_ls[wg * 16 + 4 * g + i] = u;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < STATS; ++q) {
-      const float v = row_sum16(st[q]);
-      if (lane == 0) W.part_stats[((size_t)net * MAX_GROUPS + wg) * STATS + q] = v;
-    }
-  }
-}
-
-// dh1 = W2^T q(dz2) for this wave's hidden-1 features k (FPW m .. FPW m + FPW - 1), dz1, and
-// the layer-1 weight and bias gradients.
-template <int FPW>
-__global__ __launch_bounds__(64 * HID / FPW, 1) void k_dz1(const uint16_t* __restrict__ w, const float* __restrict__ b,
-                                                           Batch D, const int32_t* __restrict__ idx, int B, int tiles,
-                                                           Work W) {
-  constexpr int NWV = HID / FPW, MT = FPW / 16;
-  __shared__ __attribute__((aligned(16))) float b1k[HID];              // read as f32x4
-  __shared__ __attribute__((aligned(16))) __bf16 Ts[NWV][FPW * TPAD];  // rows read as 8-byte halves
-  __shared__ __attribute__((aligned(16))) __bf16 Xs[NWV][32 * TPAD];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int m = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = lane >> 4, r = lane & 15;
-  const uint16_t* W1 = w;
-  const uint16_t* W2 = w + HID * 23;
-  bf16x8 w1[MT], w2t[MT][8];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int k = FPW * m + 16 * mt + r;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int i = kslot(g, j);
-      w1[mt][j] = i < 23 ? bf16_of_bits(W1[k * 23 + i]) : bf16_of_bits(0);
-    }
-#pragma unroll
-    for (int kt = 0; kt < 8; ++kt)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) w2t[mt][kt][j] = bf16_of_bits(W2[(32 * kt + kslot(g, j)) * HID + k]);
-  }
-  if (tid < HID) b1k[tid] = b[tid] * TWO_LOG2E;
-  f32x4 dw1[MT][2], db1[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    db1[mt] = dw1[mt][0] = dw1[mt][1] = f32x4{0, 0, 0, 0};
-  }
-  __bf16* T = Ts[m];
-  __bf16* X = Xs[m];
-  __syncthreads();
-  f32x4 b1[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) b1[mt] = *reinterpret_cast<const f32x4*>(&b1k[FPW * m + 16 * mt + 4 * g]);
-  // inputs and q(dz2) fragments of the first tile, raw indices of the second (prefetches
-  // unconditional, as in k_fwd_bwd)
-  const int Mi = (int)D.M;
-  TileIn cur;
-  bf16x8 zf[8];
-  auto load_dz2 = [&](int t, bf16x8* z) {
-    const size_t tc = (size_t)min(t, tiles - 1);
-#pragma unroll
-    for (int kt = 0; kt < 8; ++kt) z[kt] = W.dz2_frag[(tc * 8 + kt) * 64 + lane];
-  };
-  tile_in_load<false, false>(D, clamp_sample(raw_index(idx, blockIdx.x, r, B), Mi), g, cur);
-  load_dz2(blockIdx.x, zf);
-  int raw_nxt = raw_index(idx, blockIdx.x + gridDim.x, r, B);
-
-  // The tile body is peeled for the workgroup's first tile so that every path into the
-  // loop arrives with the same memory operations in flight (loads of the next tile, then
-  // this tile's stores): the waits inside then cover only the loads they need.
-  auto tile = [&](int t) __attribute__((always_inline)) {
-    const bool valid = t * 16 + r < B;
-    TileIn nxt;
-    bf16x8 zn[8];
-    tile_in_load<false, false>(D, clamp_sample(raw_nxt, Mi), g, nxt);
-    load_dz2(t + gridDim.x, zn);
-    const int raw_nxt2 = raw_index(idx, t + 2 * gridDim.x, r, B);
-    const bf16x8 x = input_frag(cur, valid, g);
-    f32x4 acc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0, 0, 0, 0};
-#pragma unroll
-    for (int kt = 0; kt < 8; ++kt)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma(w2t[mt][kt], zf[kt], acc[mt]);
-    f32x4 dz[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const f32x4 z1 = mfma(w1[mt], x, f32x4{0, 0, 0, 0});
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float h = tanh_bias(z1[i], b1[mt][i]);
-        dz[mt][i] = acc[mt][i] * (1.0f - h * h);
-      }
-      db1[mt] += dz[mt];
-    }
-    // dW1 += q(dz1) q(x)^T over the tile's samples (K slots 4..7 empty)
-    put_d<MT>(T, g, r, dz);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) X[kslot(g, j) * TPAD + r] = x[j];
-    bf16x8 bx[2];
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) bx[nt] = low_half(half_of(X, 16 * nt + r, g));
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const bf16x8 a = low_half(half_of(T, 16 * mt + r, g));
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) dw1[mt][nt] = mfma(a, bx[nt], dw1[mt][nt]);
-    }
-    cur = nxt;
-#pragma unroll
-    for (int kt = 0; kt < 8; ++kt) zf[kt] = zn[kt];
-    raw_nxt = raw_nxt2;
-  };
-  if ((int)blockIdx.x < tiles) {
-    tile(blockIdx.x);
-    for (int t = blockIdx.x + gridDim.x; t < tiles; t += gridDim.x) tile(t);
-  }
-
-  const int wg = blockIdx.x;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = FPW * m + 16 * mt + 4 * g + i;
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) W.part_w1[((size_t)wg * HID + k) * 32 + 16 * nt + r] = dw1[mt][nt][i];
-      const float v = row_sum16(db1[mt][i]);
-      if (r == 0) W.part_b1[(size_t)wg * HID + k] = v;
-    }
-}
-
-// Where k_dw2 takes its q(h1) operand from.  With `w` null it reads stored half fragments
-// (h1_half, which the SHAC window kernel writes); otherwise it recomputes them from the
-// minibatch's inputs (obs rows of samples idx[..], clamped as in the forward kernel) and the network's
-// layer 1 (W1 at w, b1 at b), with the forward kernel's arithmetic (one MFMA over the 23
-// inputs, bias and tanh in fp32, bf16 rounding), so that the operand is the same.
-struct H1Src {
-  const u32x2* h1_half;
-  const uint16_t* w;
-  const float* b;
-  const float* obs;
-  size_t M;
-  const int32_t* idx;
-  int B;
-};
-
-// dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup.  Eight waves, two per
-// SIMD: wave w owns rows 64 (w % 4) .. + 63 (4 M-tiles, A fragments loaded directly) and
-// columns 128 (w / 4) .. + 127 (8 N-tiles), 128 accumulators.  The 16 B fragments of a step
-// are shared: wave w provides N-tiles 2w, 2w+1 through LDS (two buffers, one barrier per step)
-// and reads its eight.  A step's 32 products take far less time than a load's latency, so
-// loads run DW2_DEPTH steps ahead in a ring of register sets (the loop unrolled by DW2_DEPTH);
-// they are unconditional (the step index clamped) so that every wait covers only its own set.
-// RECOMP: wave w computes its two N-tiles of q(h1) from the inputs: D = x W1^T (the input
-// fragment as the A operand) gives lane (g, r) feature r at samples 4g .. 4g+3, which is the
-// half-fragment layout.  The input fragments of a step (two 16-sample tiles) are shared too:
-// wave w loads K slots 2 (w % 4), 2 (w % 4) + 1 of tile w / 4 four steps ahead of the step's
-// products (sample indices eight steps ahead) and rounds them to bf16 into LDS two steps
-// ahead; q(h1) of a step is computed after the products of the step before it.
-template <bool RECOMP>
-__global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restrict__ dz2_half, H1Src H, int steps,
+// dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup, from stored half
+// fragments of both (SHAC's actor gradient).  Eight waves, two per SIMD: wave w owns rows
+// 64 (w % 4) .. + 63 (4 M-tiles, A fragments loaded directly) and columns 128 (w / 4) .. + 127
+// (8 N-tiles), 128 accumulators.  The 16 B fragments of a step are shared: wave w provides
+// N-tiles 2w, 2w+1 through LDS (two buffers, one barrier per step) and reads its eight.  A
+// step's 32 products take far less time than a load's latency, so loads run DW2_DEPTH steps
+// ahead in a ring of register sets (the loop unrolled by DW2_DEPTH); they are unconditional
+// (the step index clamped) so that every wait covers only its own set.
+__global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restrict__ dz2_half,
+                                                           const u32x2* __restrict__ h1_half, int steps,
                                                            float* __restrict__ part_w2) {
   __shared__ bf16x8 Bs[2][16][64];
-  __shared__ bf16x8 Xs[RECOMP ? 2 : 1][2][64];
-  __shared__ bf16x8 W1s[RECOMP ? 16 : 1][64];   // layer-1 fragments of the 16 N-tiles
-  __shared__ float B1s[RECOMP ? 16 : 1][64];     // their biases x 2 log2 e
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int mr = w & 3, nc = w >> 2;
-  const int g = lane >> 4, r = lane & 15;
   const int per = (steps / DW2_DEPTH + gridDim.x - 1) / gridDim.x * DW2_DEPTH;   // steps % DW2_DEPTH == 0
   const int u0 = blockIdx.x * per, u1 = min(steps, u0 + per);
+  const int g = lane >> 4, r = lane & 15;
   f32x4 acc[4][8];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt)
@@ -683,125 +245,36 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
     for (int nt = 0; nt < 8; ++nt) acc[mt][nt] = f32x4{0, 0, 0, 0};
   if (u0 < u1) {
     auto at = [&](int tile, int ft) { return ((size_t)tile * 16 + ft) * 64 + lane; };
-    // A ring: DW2_DEPTH steps, two with RECOMP (whose longer steps cover the latency with
-    // fewer registers)
-    constexpr int DA = RECOMP ? 2 : DW2_DEPTH;
-    bf16x8 A[DA][4], Bo[DW2_DEPTH][2];
-    // RECOMP: this wave's share of the inputs: tile xh of a step, K slots xj, xj + 1; inputs
-    // of two steps (X, ring of 2) and sample indices of four (ix, ring of DW2_DEPTH).  Its
-    // layer-1 fragments and biases (features 16 (2w + q) + r) sit in LDS, read by itself only.
-    const int xh = w >> 2, xj = 2 * (w & 3);
-    const int xr0 = min(kslot(g, xj), 22), xr1 = min(kslot(g, xj + 1), 22);
-    const bool xk0 = kslot(g, xj) < 23, xk1 = kslot(g, xj + 1) < 23;
-    float X[2][2];
-    int ix[DW2_DEPTH];
-    const int Mi = (int)H.M;
-    auto idx_load = [&](int u, int slot) __attribute__((always_inline)) {
-      ix[slot] = raw_index(H.idx, 2 * min(u, u1 - 1) + xh, r, H.B);
-    };
-    auto x_load = [&](int slot_ix, int slot_x) __attribute__((always_inline)) {
-      const size_t ss = (size_t)clamp_sample(ix[slot_ix], Mi);
-      X[slot_x][0] = H.obs[(size_t)xr0 * H.M + ss];
-      X[slot_x][1] = H.obs[(size_t)xr1 * H.M + ss];
-    };
-    // this wave's two input values of a step, as bf16, into input buffer xb
-    auto x_put = [&](int slot_x, int xb) __attribute__((always_inline)) {
-      __bf16* dst = reinterpret_cast<__bf16*>(&Xs[xb][xh][lane]) + xj;
-      dst[0] = (__bf16)(xk0 ? X[slot_x][0] : 0.0f);
-      dst[1] = (__bf16)(xk1 ? X[slot_x][1] : 0.0f);
-    };
+    bf16x8 A[DW2_DEPTH][4], Bo[DW2_DEPTH][2];
     auto a_load = [&](int u, int j) __attribute__((always_inline)) {
       u = min(u, u1 - 1);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
         A[j][mt] = join(dz2_half[at(2 * u, 4 * mr + mt)], dz2_half[at(2 * u + 1, 4 * mr + mt)]);
-      if (!RECOMP) {
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
-          Bo[j][q] = join(H.h1_half[at(2 * u, 2 * w + q)], H.h1_half[at(2 * u + 1, 2 * w + q)]);
-      }
+      for (int q = 0; q < 2; ++q)
+        Bo[j][q] = join(h1_half[at(2 * u, 2 * w + q)], h1_half[at(2 * u + 1, 2 * w + q)]);
     };
-    // q(h1) of this wave's N-tiles for the step whose input fragments are in input buffer xb,
-    // into B buffer bb (one N-tile at a time, to keep few registers live)
-    auto recompute = [&](int xb, int bb) __attribute__((always_inline)) {
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const bf16x8 w1 = W1s[2 * w + q][lane];
-        const float bk = B1s[2 * w + q][lane];
-        const f32x4 d0 = mfma(Xs[xb][0][lane], w1, f32x4{0, 0, 0, 0});
-        const f32x4 d1 = mfma(Xs[xb][1][lane], w1, f32x4{0, 0, 0, 0});
-        bf16x8 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          o[i] = (__bf16)tanh_bias(d0[i], bk);
-          o[4 + i] = (__bf16)tanh_bias(d1[i], bk);
-        }
-        Bs[bb][2 * w + q][lane] = o;
-      }
-    };
-    if (RECOMP) {
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int f = 16 * (2 * w + q) + r;
-        bf16x8 w1;
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          const int k = kslot(g, jj);
-          w1[jj] = k < 23 ? bf16_of_bits(H.w[f * 23 + k]) : bf16_of_bits(0);
-        }
-        W1s[2 * w + q][lane] = w1;
-        B1s[2 * w + q][lane] = H.b[f] * TWO_LOG2E;
-      }
-      // steps u0 .. u0 + 3: inputs of u0 into buffer 0, q(h1) of u0 into B buffer 0, inputs
-      // of u0 + 1 into buffer 1, those of u0 + 2 and u0 + 3 in registers; then the sample
-      // indices of u0 + 4 .. u0 + 7
-#pragma unroll
-      for (int j = 0; j < DW2_DEPTH; ++j) idx_load(u0 + j, j);
-      x_load(0, 0);
-      x_load(1, 1);
-      x_put(0, 0);
-      x_load(2, 0);
-      __syncthreads();
-      recompute(0, 0);
-      x_put(1, 1);
-      x_load(3, 1);
-#pragma unroll
-      for (int j = 0; j < DW2_DEPTH; ++j) idx_load(u0 + DW2_DEPTH + j, j);
-    }
-#pragma unroll
-    for (int j = 0; j < DA; ++j) a_load(u0 + j, j);
+    for (int j = 0; j < DW2_DEPTH; ++j) a_load(u0 + j, j);
     // u1 - u0 is a multiple of DW2_DEPTH (padded minibatch, rounded share), so a round has no
     // branch; the first round is peeled so that both paths into the loop header have the same
     // loads in flight (the prologue's own load order would otherwise set the header's wait).
-    // RECOMP, at the top of step s = u + j: this wave's q(h1) of s is in B buffer s % 2 and its
-    // inputs of s + 1 in input buffer (s + 1) % 2 (both published by the step's barrier);
-    // registers X[s % 2] and X[(s + 1) % 2] hold its inputs of s + 2 and s + 3, ix[s % 4] the
-    // sample indices of s + 4.  After the step's products (A[j] is free until its reload):
-    // q(h1) of s + 1 from input buffer (s + 1) % 2 into B buffer (s + 1) % 2, inputs of s + 2
-    // into input buffer s % 2, then the loads of s + 4's inputs and s + 8's indices.  A buffer
-    // written in step s was last read before step s's barrier.
+    // A buffer written in step s was last read before step s's barrier.
     auto round = [&](int u) __attribute__((always_inline)) {
 #pragma unroll
       for (int j = 0; j < DW2_DEPTH; ++j) {
         const int b = j & 1;
-        if (!RECOMP) {
 #pragma unroll
-          for (int q = 0; q < 2; ++q) Bs[b][2 * w + q][lane] = Bo[j][q];
-        }
+        for (int q = 0; q < 2; ++q) Bs[b][2 * w + q][lane] = Bo[j][q];
         __syncthreads();   // this step's B fragments visible; readers of this buffer two steps ago are done
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) {
           const bf16x8 bf = Bs[b][8 * nc + nt][lane];
 #pragma unroll
-          for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[j % DA][mt], bf, acc[mt][nt]);
+          for (int mt = 0; mt < 4; ++mt) acc[mt][nt] = mfma(A[j][mt], bf, acc[mt][nt]);
         }
-        if (RECOMP) {
-          recompute(b ^ 1, b ^ 1);
-          x_put(b, b);
-          x_load(j, b);
-          idx_load(u + j + 2 * DW2_DEPTH, j);
-        }
-        a_load(u + j + DA, j % DA);
+        a_load(u + j + DW2_DEPTH, j);
       }
     };
     round(u0);
@@ -816,14 +289,14 @@ __global__ __launch_bounds__(64 * DW2_WAVES, 1) void k_dw2(const u32x2* __restri
       for (int nt = 0; nt < 8; ++nt) out[(64 * mr + 16 * mt + 4 * g + i) * HID + 128 * nc + 16 * nt + r] = acc[mt][nt][i];
 }
 
-// ------------------------------------------------------------------ value-only gradient ---
-// The value network's gradient on one minibatch, for the value-only fits of SHAC's critic,
-// in two kernels and without a 256 x 256 partial per tile workgroup:
-//   k_vtile   one wave per 16-sample tile, the network's bf16 weights in LDS: forward, squared
-//             error, dz2 and dz1 (tanh derivatives from the fp32 activations); db1, db2, dW3,
-//             db3 and the error sum per workgroup; q(x) stored as the layer-1 operand, q(dz2)
-//             and q(dz1) as half fragments (lane (g, r): feature r of a 16-feature tile,
-//             samples 4 g .. 4 g + 3)
+// ------------------------------------------------------------------ network gradient ------
+// The gradient of one network (policy or value net) on one minibatch, in two kernels and
+// without a 256 x 256 partial per tile workgroup:
+//   k_vtile   one wave per 16-sample tile, the network's bf16 weights in LDS: forward, loss,
+//             dz2 and dz1 (tanh derivatives from the fp32 activations); db1, db2, dW3, db3
+//             (and d log sigma) and the loss sums per workgroup; q(x) stored as the layer-1
+//             operand, q(dz2) and q(dz1) as half fragments (lane (g, r): feature r of a
+//             16-feature tile, samples 4 g .. 4 g + 3)
 //   k_vwgrad  dW2 = q(dz2) q(h1)^T and dW1 = q(dz1) q(x)^T, a product over the samples, one
 //             partial per chunk of the minibatch; q(h1) recomputed from q(x) with layer 1's
 //             arithmetic, so that it has the forward's bits
@@ -855,6 +328,28 @@ union VtShared {
   struct {
     float v[VT_WAVES][3][HID];   // [wave][db1, db2, dW3][feature]
     float sc[VT_WAVES][2][4];    // [wave][db3, squared error][lane row g]
+  } red;
+};
+
+// The policy's (eight outputs): W3 in the two operand orders of its products, b3 and the
+// action-noise constants next to the hidden layers' weights.
+struct PtWeights {
+  bf16x8 w1[16][64];
+  bf16x8 w2[16][8][64];
+  bf16x8 w3a[8][32];      // output-layer B fragments [K tile][8 g + output]: W3[o][32 kt + kslot(g, j)]
+  uint16_t w3t[HID][8];   // W3 transposed [feature][output] (the input-gradient operand)
+  float b1k[HID];
+  float b2k[HID];
+  float b3[8];
+  float ls[8], ivar[8];   // log sigma and 1 / sigma^2 per action
+};
+union PtShared {
+  PtWeights s;
+  struct {
+    float v[VT_WAVES][2][HID];     // [wave][db1, db2][feature]
+    float w3[VT_WAVES][HID][8];    // [wave][feature][output] dW3^T
+    float sc[VT_WAVES][2][8];      // [wave][db3, d log sigma][output]
+    float st[VT_WAVES][3];         // [wave][surrogate, log-ratio, clipped count]
   } red;
 };
 
@@ -894,6 +389,16 @@ __device__ __forceinline__ bf16x8 select_frag(int g, int r, int h) {
   return f;
 }
 
+// The same for gy: lane (g, r) holds 1 in slot r % 4 when g = (r % 8) / 4.  As B with q(gy)
+// as A (K slots 0..3 of lane rows g < 2: outputs 4 g .. 4 g + 3 of sample r) it gives lane
+// (g, r) the value of output r % 8 at samples 4 g .. 4 g + 3.
+__device__ __forceinline__ bf16x8 select_out8(int g, int r) {
+  bf16x8 f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (__bf16)((g == ((r & 7) >> 2) && j == (r & 3)) ? 1.0f : 0.0f);
+  return f;
+}
+
 // Reduce-scatter over the four lane rows: afterwards lane (g, r) holds in out[k] the sum over
 // the rows of v[4 g + k], added in the order (v_g + v_(g^2)) + (v_(g^1) + v_(g^3)).
 __device__ __forceinline__ void rows_reduce_scatter(const float v[16], float out[4], int g) {
@@ -919,42 +424,73 @@ __device__ __forceinline__ u32x2 pack4(const f32x4& v) {
   return __builtin_bit_cast(u32x2, q);
 }
 
-template <bool H1>
+// One wave per 16-sample tile, the network's bf16 weights in LDS (see above).  NOUT = 1: the
+// value net and the squared error; NOUT = 8: the policy and the clipped surrogate, whose
+// output layer and its gradients run on MFMA as well:
+//   y^T = W3 q(h2)             A = W3 fragments (rows: outputs), B = q(h2) as feature-major
+//                              pairs (the sample-major h2 through the selection MFMA), so that
+//                              lane (g, r), g < 2, gets outputs 4 g + i of sample r;
+//   dh2 = q(gy) W3             A = q(gy) in that layout (K slots 0..3: outputs 4 g .. 4 g + 3),
+//                              B = W3^T read from LDS: sample-major like h2;
+//   dW3^T += q(h2) q(gy)^T     two feature tiles per product: K slots 0..3 hold samples of
+//                              feature tile 2 p, slots 4..7 of tile 2 p + 1, and the B operand
+//                              puts q(gy) in columns 0..7 for the first and 8..15 for the second,
+//                              so that eight accumulators hold all 256 x 8 entries.
+template <int NOUT, bool H1>
 __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __restrict__ w, const float* __restrict__ b,
-                                                            Batch D, const int32_t* __restrict__ idx, int B, int tiles,
-                                                            Hp hp, Work W) {
-  __shared__ VtShared U;
-  VtWeights& S = U.s;
+                                                            const float* __restrict__ log_std, Batch D,
+                                                            const int32_t* __restrict__ idx, int B, int tiles, Hp hp,
+                                                            Work W) {
+  constexpr bool POL = NOUT == 8;
+  static_assert(NOUT == 1 || NOUT == 8, "value net or policy");
+  __shared__ std::conditional_t<POL, PtShared, VtShared> U;
+  auto& S = U.s;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
   const int Mi = (int)D.M;
   const size_t M = D.M;
-  // inputs of a tile: this lane's 8 layer-1 inputs of sample r and the returns of samples
-  // 4 g .. 4 g + 3 (unconditional loads from clamped entries, masked on use).  The next tile's
-  // sample indices are loaded at the top of a tile and its inputs at the start of the input
-  // gradient, where few registers are live: held any earlier they would be spilled, and every
-  // spill of a loaded value waits for the load.
+  // inputs of a tile: this lane's 8 layer-1 inputs of sample r and, for the value net, the
+  // returns of samples 4 g .. 4 g + 3; for the policy, actions 4 g .. 4 g + 3 (lanes g < 2),
+  // old log-probability and advantage of sample r (unconditional loads from clamped entries,
+  // masked on use).  The next tile's sample indices are loaded at the top of a tile and its
+  // inputs at the start of the input gradient, where few registers are live: held any earlier
+  // they would be spilled, and every spill of a loaded value waits for the load.
   struct Idx {
-    int s[5];
+    int s[POL ? 1 : 5];
   };
   struct In {
-    float x[8], rt[4];
+    float x[8], rt[POL ? 1 : 4], a[POL ? 4 : 1], lp, ad;
   };
   auto load_idx = [&](int t) __attribute__((always_inline)) {
     Idx q;
     q.s[0] = raw_index(idx, t, r, B);
+    if constexpr (!POL) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) q.s[1 + i] = raw_index(idx, t, 4 * g + i, B);
+      for (int i = 0; i < 4; ++i) q.s[1 + i] = raw_index(idx, t, 4 * g + i, B);
+    }
     return q;
   };
   auto load_in = [&](const Idx& q) __attribute__((always_inline)) {
     In in;
     const size_t sr = (size_t)clamp_sample(q.s[0], Mi);
+    // the row offsets (row x M) are formed here, a few operations per load: hoisted out of
+    // the loop they would hold up to 24 registers, which the compiler spills, and every
+    // reload of a spilled offset waits for the tile's stores issued before it
+    size_t Mr = M;
+    int gr = g;
+    asm volatile("" : "+s"(Mr), "+v"(gr));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(g, j), 22) * M + sr];
+    for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(gr, j), 22) * Mr + sr];
+    if constexpr (POL) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) in.rt[i] = D.ret[clamp_sample(q.s[1 + i], Mi)];
+      for (int i = 0; i < 4; ++i) in.a[i] = D.act[(size_t)((4 * gr + i) & 7) * Mr + sr];
+      in.lp = D.logp[sr];
+      in.ad = D.adv[sr];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) in.rt[i] = D.ret[clamp_sample(q.s[1 + i], Mi)];
+    }
     return in;
   };
   int t = blockIdx.x * VT_WAVES + wave;
@@ -1004,18 +540,47 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
       S.w1[f][l] = v;
     }
     for (int i = tid; i < HID; i += 64 * VT_WAVES) {
-      S.w3[i] = (float)bf16_of_bits(W3[i]);
+      if constexpr (!POL) S.w3[i] = (float)bf16_of_bits(W3[i]);
       S.b1k[i] = b[i] * TWO_LOG2E;
       S.b2k[i] = b[HID + i] * TWO_LOG2E;
     }
+    if constexpr (POL) {
+      // W3[o][f] at W3[o * HID + f]: output-layer fragments, one per thread (K tile tid / 32,
+      // lane row (tid / 8) % 4, output tid % 8), and the transposed copy
+      if (tid < 8 * 32) {
+        const int kt = tid >> 5, gg = (tid >> 3) & 3, o = tid & 7;
+        bf16x8 v;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = bf16_of_bits(W3[o * HID + 32 * kt + kslot(gg, j)]);
+        S.w3a[kt][8 * gg + o] = v;
+      }
+      for (int e = tid; e < 8 * HID; e += 64 * VT_WAVES) S.w3t[e >> 3][e & 7] = W3[(e & 7) * HID + (e >> 3)];
+      if (tid < 8) {
+        const float ls = log_std[tid];
+        S.b3[tid] = b[2 * HID + tid];
+        S.ls[tid] = ls;
+        S.ivar[tid] = expf(-2.0f * ls);
+      }
+    }
   }
-  const float b3 = b[2 * HID];
   const f32x4 zero = f32x4{0, 0, 0, 0};
   const int w2s = w2_slot(lane);
-  // db1, db2 and dW3 of features 16 (4 g + k) + r, k = 0..3 (see rows_reduce_scatter)
+  // db1, db2 and (value net) dW3 of features 16 (4 g + k) + r, k = 0..3 (see rows_reduce_scatter)
   float sb1[4] = {0, 0, 0, 0}, sb2[4] = {0, 0, 0, 0}, sw3[4] = {0, 0, 0, 0};
   float db3 = 0.0f, sq = 0.0f;
+  // policy: dW3^T (lane (g, r): features 16 (2 p + r / 8) + 4 g + i, output r % 8), and per lane
+  // (g < 2) the sums of db3 and d log sigma of outputs 4 g + i and the loss statistics (g = 0)
+  f32x4 aw3[POL ? 8 : 1];
+  float pb3[4] = {0, 0, 0, 0}, pls[4] = {0, 0, 0, 0}, st[3] = {0, 0, 0};
+#pragma unroll
+  for (int p = 0; p < (POL ? 8 : 1); ++p) aw3[p] = zero;
+  float mean = 0.0f, inv_std = 1.0f;
+  if (POL && hp.normalize) {
+    mean = W.advstat[0];
+    inv_std = W.advstat[1];
+  }
   __syncthreads();
+  const float b3 = POL ? 0.0f : b[2 * HID];
 
   for (; t < tiles; t += stride) {
     const Idx nq = load_idx(min(t + stride, tiles - 1));
@@ -1042,11 +607,12 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
       }
     }
 
-    // ---- layer 2, sample-major (z2 feature 16 nt + r, samples 4 g + i), and the value
+    // ---- layer 2, sample-major (z2 feature 16 nt + r, samples 4 g + i), and the output
     // (each weight fragment's register is refilled with the next feature tile's fragment as
     // soon as its product is issued: a one-tile-deep prefetch in eight registers sets)
     f32x4 h2[16];
     float yp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    f32x4 yt = zero;
     bf16x8 wf[8];
 #pragma unroll
     for (int kt = 0; kt < 8; ++kt) wf[kt] = S.w2[0][kt][w2s];
@@ -1058,46 +624,117 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
         acc = mfma(h1[kt], wf[kt], acc);
         if (nt + 1 < 16) wf[kt] = S.w2[nt + 1][kt][w2s];
       }
-      const float bk = S.b2k[16 * nt + r], w3 = S.w3[16 * nt + r];
+      const float bk = S.b2k[16 * nt + r];
+      if constexpr (POL) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float h = tanh_bias(acc[i], bk);
-        h2[nt][i] = h;
-        yp[i] = __builtin_fmaf(w3, (float)(__bf16)h, yp[i]);
+        for (int i = 0; i < 4; ++i) h2[nt][i] = tanh_bias(acc[i], bk);
+        if (nt & 1) {   // the pair of feature tiles nt - 1, nt: q(h2) feature-major, then W3 q(h2)
+          const f32x4 d0 = mfma(low_half(pack4(h2[nt - 1])), select_frag(g, r, 0), zero);
+          const f32x4 d1 = mfma(low_half(pack4(h2[nt])), select_frag(g, r, 0), zero);
+          bf16x8 pr;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pr[i] = (__bf16)d0[i];
+            pr[4 + i] = (__bf16)d1[i];
+          }
+          const bf16x8 wa = S.w3a[nt >> 1][8 * g + (r & 7)];
+          yt = mfma(r < 8 ? wa : bf16x8{}, pr, yt);
+        }
+      } else {
+        const float w3 = S.w3[16 * nt + r];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float h = tanh_bias(acc[i], bk);
+          h2[nt][i] = h;
+          yp[i] = __builtin_fmaf(w3, (float)(__bf16)h, yp[i]);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);   // one feature tile at a time: bounds the live fragments
     }
-    // V(s) and dL/dV for samples 4 g + i (every lane of a row holds them)
+
+    // ---- the loss and dL/dy.  Value net: V(s) and dL/dV for samples 4 g + i (every lane of a
+    // row holds them).  Policy: lanes g < 2 hold outputs 4 g + i of sample r; gy as the A
+    // operand of dh2, and (through a selection MFMA) as the B operand of dW3
     float gq[4];
+    bf16x8 gyf, gyb;
+    if constexpr (POL) {
+      const int o0 = 4 * (g & 1);
+      const f32x4 y = yt + *reinterpret_cast<const f32x4*>(&S.b3[o0]);
+      const f32x4 lsv = *reinterpret_cast<const f32x4*>(&S.ls[o0]);
+      const f32x4 ivv = *reinterpret_cast<const f32x4*>(&S.ivar[o0]);
+      float d[4], zz[4], part = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float y = row_sum16(yp[i]) + b3;
-      const bool vs = t * 16 + 4 * g + i < B;
-      const float e = y - cur.rt[i];
-      const float gy = vs ? hp.vf_coef * hp.inv_B * e : 0.0f;
-      gq[i] = (float)(__bf16)gy;
-      if (r == 0 && vs) {
-        db3 += gy;
-        sq += e * e;
+      for (int i = 0; i < 4; ++i) {
+        const bool used = g < 2 && 4 * g + i < hp.n_act;
+        const float a = (vr && used) ? cur.a[i] : 0.0f;
+        d[i] = used ? a - y[i] : 0.0f;
+        zz[i] = d[i] * d[i] * ivv[i];
+        part += used ? -0.5f * zz[i] - lsv[i] : 0.0f;
+      }
+      const float logp = part + __shfl_xor(part, 16) - 0.5f * (float)hp.n_act * LOG_2PI;   // lanes r and r + 16
+      const bool lv = vr && g < 2;
+      const float lpo = lv ? cur.lp : 0.0f;
+      const float ah = lv ? (hp.normalize ? (cur.ad - mean) * inv_std : cur.ad) : 0.0f;
+      const float rho = expf(logp - lpo);
+      const float unc = rho * ah;
+      const float clp = fminf(fmaxf(rho, 1.0f - hp.clip_eps), 1.0f + hp.clip_eps) * ah;
+      const bool active = unc <= clp;
+      const float coef = (lv && active) ? -ah * rho * hp.inv_B : 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        gq[i] = coef * d[i] * ivv[i];
+        pb3[i] += gq[i];
+        pls[i] += 4 * g + i < hp.n_act ? coef * (zz[i] - 1.0f) : 0.0f;
+      }
+      if (lv && g == 0) {
+        st[0] += -fminf(unc, clp);
+        st[1] += lpo - logp;
+        st[2] += active ? 0.0f : 1.0f;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) gyf[j] = (__bf16)(j < 4 ? gq[j] : 0.0f);
+      // lane (g, r): q(gy) of output r % 8 at samples 4 g + i
+      const u32x2 gt = pack4(mfma(gyf, select_out8(g, r), zero));
+      gyb = r < 8 ? join(gt, u32x2{0u, 0u}) : join(u32x2{0u, 0u}, gt);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float y = row_sum16(yp[i]) + b3;
+        const bool vs = t * 16 + 4 * g + i < B;
+        const float e = y - cur.rt[i];
+        const float gy = vs ? hp.vf_coef * hp.inv_B * e : 0.0f;
+        gq[i] = (float)(__bf16)gy;
+        if (r == 0 && vs) {
+          db3 += gy;
+          sq += e * e;
+        }
       }
     }
 
-    // ---- dz2 = (W3^T q(gy)) (1 - h2^2); db2 and dW3 in-lane; q(dz2) as half fragments and,
-    // through the selection MFMA, as the feature-major pairs of the input gradient
+    // ---- dz2 = (W3^T q(gy)) (1 - h2^2); db2 (and the value net's dW3) in-lane; q(dz2) as half
+    // fragments and, through the selection MFMA, as the feature-major pairs of the input gradient
     bf16x8 dzf[8];
     float db2[16], dw3[16];
 #pragma unroll
     for (int nt = 0; nt < 16; ++nt) {
-      const float w3 = S.w3[16 * nt + r];
       f32x4 dz;
-      float a3 = 0.0f;
+      if constexpr (POL) {
+        const u32x2 wt = *reinterpret_cast<const u32x2*>(&S.w3t[16 * nt + r][4 * (g & 1)]);
+        const f32x4 dh = mfma(gyf, g < 2 ? low_half(wt) : bf16x8{}, zero);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        dz[i] = (w3 * gq[i]) * (1.0f - h2[nt][i] * h2[nt][i]);
-        a3 = __builtin_fmaf(gq[i], (float)(__bf16)h2[nt][i], a3);
+        for (int i = 0; i < 4; ++i) dz[i] = dh[i] * (1.0f - h2[nt][i] * h2[nt][i]);
+        if (nt & 1) aw3[nt >> 1] = mfma(join(pack4(h2[nt - 1]), pack4(h2[nt])), gyb, aw3[nt >> 1]);
+      } else {
+        const float w3 = S.w3[16 * nt + r];
+        float a3 = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dz[i] = (w3 * gq[i]) * (1.0f - h2[nt][i] * h2[nt][i]);
+          a3 = __builtin_fmaf(gq[i], (float)(__bf16)h2[nt][i], a3);
+        }
+        dw3[nt] = a3;
       }
       db2[nt] = (dz[0] + dz[1]) + (dz[2] + dz[3]);
-      dw3[nt] = a3;
       const u32x2 q = pack4(dz);
       W.dz2_half[(tb + nt) * 64 + lane] = q;
       const f32x4 d = mfma(low_half(q), select_frag(g, r, 0), zero);   // features 16 nt + 4 g + i, sample r
@@ -1105,13 +742,15 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
       for (int i = 0; i < 4; ++i) dzf[nt >> 1][4 * (nt & 1) + i] = (__bf16)d[i];
     }
     {
-      float o2[4], o3[4];
+      float o2[4];
       rows_reduce_scatter(db2, o2, g);
-      rows_reduce_scatter(dw3, o3, g);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        sb2[k] += o2[k];
-        sw3[k] += o3[k];
+      for (int k = 0; k < 4; ++k) sb2[k] += o2[k];
+      if constexpr (!POL) {
+        float o3[4];
+        rows_reduce_scatter(dw3, o3, g);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) sw3[k] += o3[k];
       }
     }
 
@@ -1154,40 +793,92 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
 
   // ---- per-workgroup sums, in a fixed order (over the waves)
   __syncthreads();   // every wave is done with the weights: their LDS holds the sums now
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int f = 16 * (4 * g + k) + r;
-    U.red.v[wave][0][f] = sb1[k];
-    U.red.v[wave][1][f] = sb2[k];
-    U.red.v[wave][2][f] = sw3[k];
-  }
-  if (r == 0) {
-    U.red.sc[wave][0][g] = db3;
-    U.red.sc[wave][1][g] = sq;
-  }
-  __syncthreads();
   const int wg = blockIdx.x;
-  for (int o = tid; o < 3 * HID; o += 64 * VT_WAVES) {
-    const int q = o / HID, f = o - q * HID;
-    float v = 0.0f;
+  if constexpr (POL) {
 #pragma unroll
-    for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.v[wv][q][f];
-    if (q == 0)
-      W.part_b1[(size_t)wg * HID + f] = v;
-    else if (q == 1)
-      W.part_b2[(size_t)wg * HID + f] = v;
-    else
-      W.part_w3t[((size_t)wg * HID + f) * 16] = v;
-  }
-  if (tid < 2) {
-    float v = 0.0f;
-    for (int wv = 0; wv < VT_WAVES; ++wv)
+    for (int k = 0; k < 4; ++k) {
+      const int f = 16 * (4 * g + k) + r;
+      U.red.v[wave][0][f] = sb1[k];
+      U.red.v[wave][1][f] = sb2[k];
+    }
 #pragma unroll
-      for (int gg = 0; gg < 4; ++gg) v += U.red.sc[wv][tid][gg];
-    if (tid == 0)
-      W.part_b3[wg * 16] = v;
-    else
-      W.part_stats[((size_t)MAX_GROUPS + wg) * STATS + 3] = v;
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) U.red.w3[wave][16 * (2 * p + (r >> 3)) + 4 * g + i][r & 7] = aw3[p][i];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v = row_sum16(pb3[i]), u = row_sum16(pls[i]);
+      if (r == 0 && g < 2) {
+        U.red.sc[wave][0][4 * g + i] = v;
+        U.red.sc[wave][1][4 * g + i] = u;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const float v = row_sum16(st[q]);
+      if (lane == 0) U.red.st[wave][q] = v;
+    }
+    __syncthreads();
+    for (int o = tid; o < 2 * HID; o += 64 * VT_WAVES) {
+      const int q = o / HID, f = o - q * HID;
+      float v = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.v[wv][q][f];
+      (q == 0 ? W.part_b1 : W.part_b2)[(size_t)wg * HID + f] = v;
+    }
+    for (int o = tid; o < 8 * HID; o += 64 * VT_WAVES) {
+      const int f = o >> 3, j = o & 7;
+      float v = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.w3[wv][f][j];
+      W.part_w3t[((size_t)wg * HID + f) * 16 + j] = v;
+    }
+    if (tid < 16) {
+      const int q = tid >> 3, o = tid & 7;
+      float v = 0.0f;
+      for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.sc[wv][q][o];
+      (q == 0 ? W.part_b3 : W.part_ls)[wg * 16 + o] = v;
+    } else if (tid < 16 + 3) {
+      const int q = tid - 16;
+      float v = 0.0f;
+      for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.st[wv][q];
+      W.part_stats[(size_t)wg * STATS + q] = v;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int f = 16 * (4 * g + k) + r;
+      U.red.v[wave][0][f] = sb1[k];
+      U.red.v[wave][1][f] = sb2[k];
+      U.red.v[wave][2][f] = sw3[k];
+    }
+    if (r == 0) {
+      U.red.sc[wave][0][g] = db3;
+      U.red.sc[wave][1][g] = sq;
+    }
+    __syncthreads();
+    for (int o = tid; o < 3 * HID; o += 64 * VT_WAVES) {
+      const int q = o / HID, f = o - q * HID;
+      float v = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < VT_WAVES; ++wv) v += U.red.v[wv][q][f];
+      if (q == 0)
+        W.part_b1[(size_t)wg * HID + f] = v;
+      else if (q == 1)
+        W.part_b2[(size_t)wg * HID + f] = v;
+      else
+        W.part_w3t[((size_t)wg * HID + f) * 16] = v;
+    }
+    if (tid < 2) {
+      float v = 0.0f;
+      for (int wv = 0; wv < VT_WAVES; ++wv)
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg) v += U.red.sc[wv][tid][gg];
+      if (tid == 0)
+        W.part_b3[wg * 16] = v;
+      else
+        W.part_stats[((size_t)MAX_GROUPS + wg) * STATS + 3] = v;
+    }
   }
 }
 
@@ -1348,7 +1039,7 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
   }
 }
 
-// Chunks of the value-only weight gradient and its row-block height: from VW_RECOMP_STEPS
+// Chunks of the weight-gradient product and its row-block height: from VW_RECOMP_STEPS
 // steps of 32 samples up, 128-row blocks with q(h1) recomputed and about one chunk per 64
 // steps (up to 128 chunks, 256 workgroups); below that, 64-row blocks reading the stored
 // q(h1) and about one chunk per 16 steps (8 to 64 chunks), which keeps the chunk partials
@@ -1533,9 +1224,8 @@ __global__ __launch_bounds__(256) void k_adam(int P, int nW, float* __restrict__
 }  // namespace ppo
 
 int launch_dw2(const void* dz2_half, const void* h1_half, int steps, int groups, float* part_w2, hipStream_t s) {
-  const ppo::H1Src H{(const ppo::u32x2*)h1_half, nullptr, nullptr, nullptr, 0, nullptr, 0};
-  hipLaunchKernelGGL(ppo::k_dw2<false>, dim3(groups), dim3(64 * ppo::DW2_WAVES), 0, s, (const ppo::u32x2*)dz2_half, H,
-                     steps, part_w2);
+  hipLaunchKernelGGL(ppo::k_dw2, dim3(groups), dim3(64 * ppo::DW2_WAVES), 0, s, (const ppo::u32x2*)dz2_half,
+                     (const ppo::u32x2*)h1_half, steps, part_w2);
   return check_launch("dW2");
 }
 
@@ -1611,46 +1301,48 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
   const bool with_policy = policy != nullptr;
   const int tiles = ppo::padded(B) / 16, steps = ppo::padded(B) / 32;
   const int cus = std::min(compute_units(), ppo::MAX_GROUPS);
-  const int G1 = std::min(cus, tiles), G3 = std::min(cus, steps / ppo::DW2_DEPTH);
   const ppo::Work W = ppo::work_at(work, B);
   const ppo::Hp hp{cfg->clip_eps, cfg->vf_coef,       cfg->ent_coef, cfg->max_grad_norm, 1.0f / (float)B,
                    cfg->normalize_adv ? 1 : 0, cfg->n_actions ? cfg->n_actions : ACT};
   const ppo::Batch D{batch->obs, batch->act, batch->logp, batch->adv, batch->ret, (size_t)batch->M};
   const int rb = ppo::red_blocks(ACT);
-  constexpr int FPW = ppo::FPW, TH = 64 * HID / FPW;
+  // per network: the per-tile kernel (GV workgroups of VT_WAVES waves) and the weight-gradient
+  // product (chunk partials), then the reduce of both kinds of partials
+  const int GV = std::min(cus, (tiles + ppo::VT_WAVES - 1) / ppo::VT_WAVES);
+  const ppo::VwPlan vp = ppo::vw_plan(steps);
+  const int chunks = vp.chunks;
+  const dim3 vt_block(64 * ppo::VT_WAVES), vw_block(64 * ppo::VW_WAVES);
+  auto tile_grad = [&](const auv_mlp* net, bool pol) {
+    const float* ls = pol ? net->log_std : nullptr;
+    if (vp.rows == 128) {
+      if (pol)
+        hipLaunchKernelGGL((ppo::k_vtile<8, false>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
+      else
+        hipLaunchKernelGGL((ppo::k_vtile<1, false>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
+      hipLaunchKernelGGL((ppo::k_vwgrad<128, true>), dim3(2 * chunks), vw_block, 0, s, net->w, net->b, W, steps, chunks);
+    } else {
+      if (pol)
+        hipLaunchKernelGGL((ppo::k_vtile<8, true>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
+      else
+        hipLaunchKernelGGL((ppo::k_vtile<1, true>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
+      hipLaunchKernelGGL((ppo::k_vwgrad<64, false>), dim3(4 * chunks), vw_block, 0, s, net->w, net->b, W, steps, chunks);
+    }
+  };
   if (with_policy) {
     if (hp.normalize) {
       hipLaunchKernelGGL(ppo::k_adv_partial, dim3(ppo::ADV_BLOCKS), dim3(256), 0, s, batch->adv, idx, B, (int)batch->M,
                          W.adv_part);
       hipLaunchKernelGGL(ppo::k_adv_final, dim3(1), dim3(64), 0, s, W.adv_part, B, W.advstat);
     }
-    hipLaunchKernelGGL((ppo::k_fwd_bwd<8, FPW>), dim3(G1), dim3(TH), 0, s, policy->w, policy->b, policy->log_std, D,
-                       idx, B, tiles, hp, W, 0);
-    hipLaunchKernelGGL(ppo::k_dz1<FPW>, dim3(G1), dim3(TH), 0, s, policy->w, policy->b, D, idx, B, tiles, W);
-    const ppo::H1Src H{nullptr, policy->w, policy->b, D.obs, D.M, idx, B};
-    hipLaunchKernelGGL(ppo::k_dw2<true>, dim3(G3), dim3(64 * ppo::DW2_WAVES), 0, s, W.dz2_half, H, steps, W.part_w2);
-    hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, G1, G1, G1, G3, W, cfg->ent_coef,
+    tile_grad(policy, true);
+    hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, GV, chunks, GV, chunks, W, cfg->ent_coef,
                        grad_policy, W.part_ss, ppo::AdamFuse{});
   }
-  // value network: per-tile forward / backward, the weight-gradient product, the reduce
-  const int GV = std::min(cus, (tiles + ppo::VT_WAVES - 1) / ppo::VT_WAVES);
-  const ppo::VwPlan vp = ppo::vw_plan(steps);
-  const int chunks = vp.chunks;
-  if (vp.rows == 128) {
-    hipLaunchKernelGGL(ppo::k_vtile<false>, dim3(GV), dim3(64 * ppo::VT_WAVES), 0, s, value->w, value->b, D, idx, B,
-                       tiles, hp, W);
-    hipLaunchKernelGGL((ppo::k_vwgrad<128, true>), dim3(2 * chunks), dim3(64 * ppo::VW_WAVES), 0, s, value->w,
-                       value->b, W, steps, chunks);
-  } else {
-    hipLaunchKernelGGL(ppo::k_vtile<true>, dim3(GV), dim3(64 * ppo::VT_WAVES), 0, s, value->w, value->b, D, idx, B,
-                       tiles, hp, W);
-    hipLaunchKernelGGL((ppo::k_vwgrad<64, false>), dim3(4 * chunks), dim3(64 * ppo::VW_WAVES), 0, s, value->w,
-                       value->b, W, steps, chunks);
-  }
+  tile_grad(value, false);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, GV, chunks, GV, chunks, W, 0.0f,
                      grad_value, W.part_ss + rb, fuse);
   if (finalize)
-    hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? G1 : 0, GV, W, with_policy ? rb : 0,
+    hipLaunchKernelGGL(ppo::k_finalize, dim3(1), dim3(256), 0, s, with_policy ? GV : 0, GV, W, with_policy ? rb : 0,
                        ppo::red_blocks(1), rb, with_policy ? policy->log_std : (const float*)nullptr, hp, stats);
   return check_launch("auv_ppo_grad");
 }
