@@ -608,21 +608,25 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     }
 
     // ---- layer 2, sample-major (z2 feature 16 nt + r, samples 4 g + i), and the output
-    // (each weight fragment's register is refilled with the next feature tile's fragment as
-    // soon as its product is issued: a one-tile-deep prefetch in eight registers sets)
+    // (each weight fragment's register is refilled with the fragment WD products ahead as soon
+    // as its product is issued: a prefetch ring of WD register sets, one feature tile deep for
+    // the value net; half that for the policy, whose output-layer work and dW3 accumulators
+    // would otherwise not fit the registers without spills)
     f32x4 h2[16];
     float yp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 yt = zero;
-    bf16x8 wf[8];
+    constexpr int WD = POL ? 4 : 8;
+    bf16x8 wf[WD];
 #pragma unroll
-    for (int kt = 0; kt < 8; ++kt) wf[kt] = S.w2[0][kt][w2s];
+    for (int kt = 0; kt < WD; ++kt) wf[kt] = S.w2[0][kt][w2s];
 #pragma unroll
     for (int nt = 0; nt < 16; ++nt) {
       f32x4 acc = zero;
 #pragma unroll
       for (int kt = 0; kt < 8; ++kt) {
-        acc = mfma(h1[kt], wf[kt], acc);
-        if (nt + 1 < 16) wf[kt] = S.w2[nt + 1][kt][w2s];
+        acc = mfma(h1[kt], wf[kt % WD], acc);
+        const int nx = 8 * nt + kt + WD;
+        if (nx < 128) wf[kt % WD] = S.w2[nx >> 3][nx & 7][w2s];
       }
       const float bk = S.b2k[16 * nt + r];
       if constexpr (POL) {
@@ -658,7 +662,8 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     float gq[4];
     bf16x8 gyf, gyb;
     if constexpr (POL) {
-      const int o0 = 4 * (g & 1);
+      int o0 = 4 * (g & 1);
+      asm volatile("" : "+v"(o0));   // formed here rather than held (and spilled) across tiles
       const f32x4 y = yt + *reinterpret_cast<const f32x4*>(&S.b3[o0]);
       const f32x4 lsv = *reinterpret_cast<const f32x4*>(&S.ls[o0]);
       const f32x4 ivv = *reinterpret_cast<const f32x4*>(&S.ivar[o0]);
