@@ -5,8 +5,8 @@
 //
 // Kernels, in launch order for one minibatch of B samples (Bp = B rounded up to 128); for the
 // policy network first:
-//   k_adv_partial   per-block sums of the minibatch's advantages and their squares (fp64)
-//   k_adv_final     mean and 1 / (std + 1e-8) from those sums
+//   k_adv_partial   per-block sums of the minibatch's advantages and their squares (fp64;
+//                   the policy's k_vtile turns them into the mean and 1 / (std + 1e-8))
 // then for each network (the value net alone in every minibatch of auv_ppo_fit_value):
 //   k_vtile<n>      per 16-sample tile and wave, the weights in LDS: forward, loss (clipped
 //                   surrogate for n = 8, squared error for n = 1), dL/dy, dz2, dz1; the sums of
@@ -65,7 +65,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));   // four bf16: a ha
 
 // Workspace of one call (offsets in bytes from the caller's buffer; every part 256-aligned).
 struct Work {
-  float* advstat;       // [2] mean, 1 / (std + 1e-8)
   double* adv_part;     // [ADV_BLOCKS][2] sums of A and A^2
   u32x2* dz2_half;      // [Bp/16][16 feature tiles][64 lanes] q(dz2) half fragments
   float* part_w3t;      // [G][256 f][16 j] dW3^T
@@ -100,11 +99,11 @@ inline int red_blocks(int n_out) { return (nparam(n_out) + RED_ELEMS - 1) / RED_
 // From this many 32-sample steps on, the weight-gradient product recomputes q(h1) instead of
 // storing it (see k_vwgrad).
 constexpr int VW_RECOMP_STEPS = 4096;
-constexpr int WORK_PARTS = 15;
+constexpr int WORK_PARTS = 14;
 inline size_t work_layout(int B, size_t off[WORK_PARTS]) {
   const size_t Bp = (size_t)padded(B), G = MAX_GROUPS;
   const bool recomp = (int)(Bp / 32) >= VW_RECOMP_STEPS;
-  const size_t sizes[WORK_PARTS] = {2 * sizeof(float), 2 * sizeof(double) * ADV_BLOCKS, Bp * HID * 2,
+  const size_t sizes[WORK_PARTS] = {2 * sizeof(double) * ADV_BLOCKS, Bp * HID * 2,
                             G * HID * 16 * 4, G * HID * 4, G * 16 * 4, G * 16 * 4, 2 * G * STATS * 4,
                             G * HID * 32 * 4, G * HID * 4, G * HID * HID * 4,
                             2 * (size_t)red_blocks(8) * 4,
@@ -122,21 +121,20 @@ inline Work work_at(void* base, int B) {
   work_layout(B, off);
   char* p = (char*)base;
   Work W;
-  W.advstat = (float*)(p + off[0]);
-  W.adv_part = (double*)(p + off[1]);
-  W.dz2_half = (u32x2*)(p + off[2]);
-  W.part_w3t = (float*)(p + off[3]);
-  W.part_b2 = (float*)(p + off[4]);
-  W.part_b3 = (float*)(p + off[5]);
-  W.part_ls = (float*)(p + off[6]);
-  W.part_stats = (float*)(p + off[7]);
-  W.part_w1 = (float*)(p + off[8]);
-  W.part_b1 = (float*)(p + off[9]);
-  W.part_w2 = (float*)(p + off[10]);
-  W.part_ss = (float*)(p + off[11]);
-  W.dz1_half = (u32x2*)(p + off[12]);
-  W.x_frag = (bf16x8*)(p + off[13]);
-  W.h1_half = (u32x2*)(p + off[14]);
+  W.adv_part = (double*)(p + off[0]);
+  W.dz2_half = (u32x2*)(p + off[1]);
+  W.part_w3t = (float*)(p + off[2]);
+  W.part_b2 = (float*)(p + off[3]);
+  W.part_b3 = (float*)(p + off[4]);
+  W.part_ls = (float*)(p + off[5]);
+  W.part_stats = (float*)(p + off[6]);
+  W.part_w1 = (float*)(p + off[7]);
+  W.part_b1 = (float*)(p + off[8]);
+  W.part_w2 = (float*)(p + off[9]);
+  W.part_ss = (float*)(p + off[10]);
+  W.dz1_half = (u32x2*)(p + off[11]);
+  W.x_frag = (bf16x8*)(p + off[12]);
+  W.h1_half = (u32x2*)(p + off[13]);
   return W;
 }
 
@@ -200,9 +198,10 @@ __global__ __launch_bounds__(256) void k_adv_partial(const float* __restrict__ a
   }
 }
 
-// mean = S1 / B, population variance = S2 / B - mean^2, inv_std = 1 / (sqrt(var) + 1e-8).
-__global__ __launch_bounds__(64) void k_adv_final(const double* __restrict__ part, int B, float* __restrict__ out) {
-  const int lane = threadIdx.x;
+// mean = S1 / B, population variance = S2 / B - mean^2, inv_std = 1 / (sqrt(var) + 1e-8), from
+// the per-block sums, by one wave (a butterfly sum: every lane gets the same bits); returned
+// as wave-uniform values.
+__device__ __forceinline__ void adv_stats(const double* __restrict__ part, int B, int lane, float& mean, float& inv_std) {
   double s1 = 0.0, s2 = 0.0;
   for (int k = lane; k < ADV_BLOCKS; k += 64) {
     s1 += part[2 * k];
@@ -213,11 +212,10 @@ __global__ __launch_bounds__(64) void k_adv_final(const double* __restrict__ par
     s1 += __shfl_xor(s1, o);
     s2 += __shfl_xor(s2, o);
   }
-  if (lane == 0) {
-    const double mean = s1 / B, var = fmax(s2 / B - mean * mean, 0.0);
-    out[0] = (float)mean;
-    out[1] = (float)(1.0 / (sqrt(var) + 1e-8));
-  }
+  const double m = s1 / B, var = fmax(s2 / B - m * m, 0.0);
+  mean = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, (float)m)));
+  inv_std = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                          __builtin_bit_cast(int, (float)(1.0 / (sqrt(var) + 1e-8)))));
 }
 
 // dW2 = q(dz2) q(h1)^T over 32-sample steps [u0, u1) of this workgroup, from stored half
@@ -575,10 +573,7 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
 #pragma unroll
   for (int p = 0; p < (POL ? 8 : 1); ++p) aw3[p] = zero;
   float mean = 0.0f, inv_std = 1.0f;
-  if (POL && hp.normalize) {
-    mean = W.advstat[0];
-    inv_std = W.advstat[1];
-  }
+  if (POL && hp.normalize) adv_stats(W.adv_part, B, lane, mean, inv_std);   // every wave, the same bits
   __syncthreads();
   const float b3 = POL ? 0.0f : b[2 * HID];
 
@@ -1203,27 +1198,34 @@ __global__ __launch_bounds__(256) void k_finalize(int G1p, int G1v, Work W, int 
   }
 }
 
-// One Adam step on P packed parameters with gradient grad * stats[7]; the first nW (the
-// weight matrices) are also written to the bf16 copy, rounded to nearest even.
-__global__ __launch_bounds__(256) void k_adam(int P, int nW, float* __restrict__ theta, float* __restrict__ mom,
-                                              float* __restrict__ vel, uint16_t* __restrict__ wbf,
-                                              const float* __restrict__ grad, const float* __restrict__ stats,
+// One Adam step on the P packed parameters of each of up to two networks with gradient
+// grad * stats[7]; the first nW (the weight matrices) are also written to the bf16 copy,
+// rounded to nearest even.  Blocks [0, blocks0) step the first network, the rest the second.
+struct AdamNet {
+  int P = 0, nW = 0;
+  float *theta = nullptr, *mom = nullptr, *vel = nullptr;
+  uint16_t* wbf = nullptr;
+  const float* grad = nullptr;
+};
+__global__ __launch_bounds__(256) void k_adam(AdamNet n0, AdamNet n1, int blocks0, const float* __restrict__ stats,
                                               float lr, float b1, float b2, float eps, float bc1, float bc2) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= P) return;
+  const bool second = (int)blockIdx.x >= blocks0;
+  const AdamNet n = second ? n1 : n0;
+  const int e = ((int)blockIdx.x - (second ? blocks0 : 0)) * 256 + threadIdx.x;
+  if (e >= n.P) return;
   AdamFuse A;
-  A.theta = theta;
-  A.mom = mom;
-  A.vel = vel;
-  A.wbf = wbf;
-  A.nW = nW;
+  A.theta = n.theta;
+  A.mom = n.mom;
+  A.vel = n.vel;
+  A.wbf = n.wbf;
+  A.nW = n.nW;
   A.lr = lr;
   A.b1 = b1;
   A.b2 = b2;
   A.eps = eps;
   A.bc1 = bc1;
   A.bc2 = bc2;
-  adam_entry(A, e, grad[e], stats[7]);
+  adam_entry(A, e, n.grad[e], stats[7]);
 }
 
 }  // namespace ppo
@@ -1337,7 +1339,6 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
     if (hp.normalize) {
       hipLaunchKernelGGL(ppo::k_adv_partial, dim3(ppo::ADV_BLOCKS), dim3(256), 0, s, batch->adv, idx, B, (int)batch->M,
                          W.adv_part);
-      hipLaunchKernelGGL(ppo::k_adv_final, dim3(1), dim3(64), 0, s, W.adv_part, B, W.advstat);
     }
     tile_grad(policy, true);
     hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, GV, chunks, GV, chunks, W, cfg->ent_coef,
@@ -1388,13 +1389,23 @@ int auv_ppo_adam(const auv_ppo_config* cfg, int64_t t, const auv_ppo_net* policy
   hipStream_t s = (hipStream_t)stream;
   const float bc1 = (float)(1.0 - std::pow((double)cfg->beta1, (double)t));
   const float bc2 = (float)(1.0 - std::pow((double)cfg->beta2, (double)t));
+  // both networks in one launch (the policy's blocks first)
+  ppo::AdamNet an[2];
+  int blocks[2] = {0, 0}, m = 0;
   for (int k = 0; k < 2; ++k) {
     if (!nets[k]) continue;
-    const int P = ppo::nparam(n_outs[k]), nW = HID * 23 + HID * HID + n_outs[k] * HID;
-    hipLaunchKernelGGL(ppo::k_adam, dim3((P + 255) / 256), dim3(256), 0, s, P, nW, nets[k]->theta, nets[k]->adam_m,
-                       nets[k]->adam_v, nets[k]->w_bf16, grads[k], stats, cfg->lr, cfg->beta1, cfg->beta2, cfg->adam_eps,
-                       bc1, bc2);
+    ppo::AdamNet& a = an[m];
+    a.P = ppo::nparam(n_outs[k]);
+    a.nW = HID * 23 + HID * HID + n_outs[k] * HID;
+    a.theta = nets[k]->theta;
+    a.mom = nets[k]->adam_m;
+    a.vel = nets[k]->adam_v;
+    a.wbf = nets[k]->w_bf16;
+    a.grad = grads[k];
+    blocks[m++] = (a.P + 255) / 256;
   }
+  hipLaunchKernelGGL(ppo::k_adam, dim3(blocks[0] + blocks[1]), dim3(256), 0, s, an[0], an[1], blocks[0], stats, cfg->lr,
+                     cfg->beta1, cfg->beta2, cfg->adam_eps, bc1, bc2);
   return check_launch("auv_ppo_adam");
 }
 
