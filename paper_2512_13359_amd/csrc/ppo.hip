@@ -1067,14 +1067,16 @@ struct AdamFuse {
 };
 
 // g0: the raw gradient entry; the step uses g0 times the clipping factor `clip` (the same
-// operations in k_adam and in the fused step, so both give the same bits).
-__device__ __forceinline__ void adam_entry(const AdamFuse& A, int e, float g0, float clip) {
+// operations in k_adam and in the fused step, so both give the same bits).  th0, m0, v0: the
+// entry's parameter and moments before the step (loaded by the caller, early where it can).
+__device__ __forceinline__ void adam_entry(const AdamFuse& A, int e, float g0, float clip, float th0, float m0,
+                                           float v0) {
   const float g = g0 * clip;
   // explicit fused multiply-adds: no contraction left to the compiler, which could fuse the
   // moment updates differently in the two kernels
-  const float m = __builtin_fmaf(A.b1, A.mom[e], (1.0f - A.b1) * g);
-  const float v = __builtin_fmaf(A.b2, A.vel[e], ((1.0f - A.b2) * g) * g);
-  const float th = A.theta[e] - A.lr * (m / A.bc1) / (sqrtf(v / A.bc2) + A.eps);
+  const float m = __builtin_fmaf(A.b1, m0, (1.0f - A.b1) * g);
+  const float v = __builtin_fmaf(A.b2, v0, ((1.0f - A.b2) * g) * g);
+  const float th = th0 - A.lr * (m / A.bc1) / (sqrtf(v / A.bc2) + A.eps);
   A.mom[e] = m;
   A.vel[e] = v;
   A.theta[e] = th;
@@ -1117,6 +1119,11 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, in
       src = W.part_ls + (q - n_out), stride = 16, G = G1, add = q - n_out < n_act ? -ent_coef : 0.0f;
     }
   }
+  // the fused Adam step's parameter and moments, loaded before the partial sums so that their
+  // round trip overlaps the sums' (unconditionally, from a readable array without a fused step)
+  const int ec = min(e, P - 1);
+  const float th0 = (A.theta ? A.theta : grad)[ec], m0 = (A.theta ? A.mom : grad)[ec],
+              v0 = (A.theta ? A.vel : grad)[ec];
   const int g0 = w * G / 4, g1 = (w + 1) * G / 4;
   float acc = 0.0f;
   int wg = g0;
@@ -1142,7 +1149,7 @@ __global__ __launch_bounds__(256) void k_reduce(int n_out, int n_act, int G1, in
     const float v = e < P ? part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane] + add : 0.0f;
     if (e < P) {
       grad[e] = v;
-      if (A.theta) adam_entry(A, e, v, A.clip);   // fused step: no gradient clipping (factor 1)
+      if (A.theta) adam_entry(A, e, v, A.clip, th0, m0, v0);   // fused step: no gradient clipping (factor 1)
     }
     const float s2 = wave_sum(v * v);
     if (lane == 0) ss[blockIdx.x] = s2;
@@ -1225,7 +1232,7 @@ __global__ __launch_bounds__(256) void k_adam(AdamNet n0, AdamNet n1, int blocks
   A.eps = eps;
   A.bc1 = bc1;
   A.bc2 = bc2;
-  adam_entry(A, e, n.grad[e], stats[7]);
+  adam_entry(A, e, n.grad[e], stats[7], n.theta[e], n.mom[e], n.vel[e]);
 }
 
 }  // namespace ppo
