@@ -44,10 +44,13 @@ COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_policy_rollout_c4_counters.txt
 
 
 def source_hash() -> str:
+    """Hash of the rollout kernel's sources and of the build script (its compile flags)."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2512_13359_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
+    with open(os.path.join(ROOT, "paper_2512_13359_amd", "build.py"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()[:16]
 
 
