@@ -43,14 +43,22 @@ KERNEL_SOURCES = ["auv_policy.hip", "auv_internal.hpp", "auv_device.hpp", "env_l
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_policy_rollout_c4_counters.txt")
 
 
+def rollout_flags() -> list:
+    """The compile flags of the rollout's source, as the build script sets them."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("auv_build", os.path.join(ROOT, "paper_2512_13359_amd", "build.py"))
+    m = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(m)
+    return list(m.HIPCC_FLAGS) + list(m.EXTRA_FLAGS.get(KERNEL_SOURCES[0], []))
+
+
 def source_hash() -> str:
-    """Hash of the rollout kernel's sources and of the build script (its compile flags)."""
+    """Hash of the rollout kernel's sources and of its compile flags."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2512_13359_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
-    with open(os.path.join(ROOT, "paper_2512_13359_amd", "build.py"), "rb") as fh:
-        h.update(fh.read())
+    h.update(" ".join(rollout_flags()).encode())
     return h.hexdigest()[:16]
 
 
