@@ -334,7 +334,7 @@ union VtShared {
 struct PtWeights {
   bf16x8 w1[16][64];
   bf16x8 w2[16][8][64];
-  bf16x8 w3a[8][32];      // output-layer B fragments [K tile][8 g + output]: W3[o][32 kt + kslot(g, j)]
+  bf16x8 w3a[8][32];      // output-layer A fragments [K tile][8 g + output]: W3[o][32 kt + kslot(g, j)]
   uint16_t w3t[HID][8];   // W3 transposed [feature][output] (the input-gradient operand)
   float b1k[HID];
   float b2k[HID];
