@@ -119,7 +119,7 @@ def cpu_baseline(cfg: dict, n_steps: int) -> dict:
             "cpu_model": _cpu_model(), "numpy": np.__version__, "blas": blas}
 
 
-def c5_measure(reps: int = 3) -> dict:
+def c5_measure(reps: int = 3, rollout_reps: int = 7) -> dict:
     """PPO-buffer workload (65536 envs x 64 steps, sampled actions, value head, staggered
     episodes): rollout time and write bandwidth of the structure-of-arrays buffer, then the
     GAE scan with its inputs evicted from the Infinity Cache (cold) and resident (warm), each
@@ -138,7 +138,7 @@ def c5_measure(reps: int = 3) -> dict:
     bufs = env.rollout_buffers(T, record=("obs", "act", "logp", "value", "reward", "done", "last_value"))
     ev = lambda: torch.cuda.Event(enable_timing=True)
     times = []
-    for k in range(reps + 1):
+    for k in range(rollout_reps + 1):   # median of seven launches after one warm-up
         env.reset()
         torch.cuda.synchronize()
         e0, e1 = ev(), ev()
