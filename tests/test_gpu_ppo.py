@@ -309,19 +309,20 @@ def _pad_grad(g: np.ndarray, n_in: int, n_out: int, policy: bool) -> np.ndarray:
     return oppo.pack(q)
 
 
-def test_ppo_six_action_policy_of_the_paper_task():
+@pytest.mark.parametrize("M,B", [(5000, 2000), (W.PPO["B"] + 16 * 64 + 3, W.PPO["B"] - 37)])
+def test_ppo_six_action_policy_of_the_paper_task(M, B):
     """The paper task's 12-256-256-6 policy and 12-256-256-1 value net in the padded layout:
     gradients against the oracle of the unpadded networks (padding entries exactly zero),
     with NaN in the unused action rows and zeros in observation rows 12-22 (as a paper-task
-    rollout records them)."""
+    rollout records them).  B = 2000 takes the small-minibatch path (q(h1) stored); 262144 - 37,
+    the paper-task training minibatch made ragged, the full-size path (q(h1) recomputed)."""
     require_gpu()
-    announce("ppo six-action policy")
+    announce(f"ppo six-action policy M={M} B={B}")
     from paper_2512_13359_amd import PpoLearner
     netp = W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12)
     netv = W.mlp_weights(1, W.VALUE_SEED, n_in=12)
     pol, val = _oracle_params(netp), _oracle_params(netv)
     pol["log_std"] = np.asarray(netp["log_std"], np.float32)[:6].astype(np.float64)
-    M, B = 5000, 2000
     d = W.ppo_draws(M, 21)
     obs12 = d["obs"][:12]
     mu, _ = oppo.mlp_forward_cache(obs12.astype(np.float64), pol, quantize=True)
