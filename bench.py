@@ -340,6 +340,62 @@ def paper_training_measure(reps: int = 2, epochs: int = 4, minibatch: int = 2621
             "hundred_episodes_s": 100 * t}
 
 
+def paper_learning_measure(iters: int = 150, epochs: int = 4, minibatch: int = 262144) -> dict:
+    """PPO training on the paper's own task at its training scale (4096 envs x one 512-step
+    episode per iteration, GAE, `epochs` passes of minibatch updates), from the seeded initial
+    networks: the mean step reward of each iteration's rollout, and the wall clock of the whole
+    run (host work included)."""
+    import time
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, PpoLearner
+    from paper_2512_13359_amd import _abi as A
+
+    cfg = W.config("c6")
+    n, T = cfg["n_envs"], cfg["T"]
+    M = n * T
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.set_task(W.PAPER_TASK)
+    env.reset()
+    P = W.PPO
+    L = PpoLearner(W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.VALUE_SEED, n_in=12),
+                   **{k: P[k] for k in ("clip_eps", "vf_coef", "ent_coef", "max_grad_norm", "lr", "beta1", "beta2",
+                                        "adam_eps", "normalize_adv")})
+    bufs = env.rollout_buffers(T, record=("obs", "act", "logp", "value", "reward", "done", "last_value"), value=True)
+    adv = torch.empty(T, n, device="cuda")
+    ret = torch.empty(T, n, device="cuda")
+    batch = L.batch(bufs["obs"].reshape(23, M), bufs["act"].reshape(8, M), bufs["logp"].reshape(M), adv.reshape(M),
+                    ret.reshape(M))
+    n_mb = M // minibatch
+    rng = np.random.default_rng(0)
+    perms = [torch.from_numpy(W.ppo_minibatch_idx(M, M, seed=int(rng.integers(1 << 30)))).cuda() for _ in range(16)]
+    rewards = torch.empty(iters, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.time()
+    for it in range(iters):
+        env.rollout(T, W.MODE_POLICY_SAMPLE, policy={"struct": L.pol.mlp}, value={"struct": L.val.mlp}, bufs=bufs)
+        A.auv_gae(T, n, bufs["reward"], bufs["value"], bufs["done"], bufs["last_value"], 0.99, 0.95, adv, ret)
+        rewards[it] = bufs["reward"].mean()
+        for ep in range(epochs):
+            perm = perms[(it * epochs + ep) % len(perms)]
+            for j in range(n_mb):
+                L.update(batch, perm[j * minibatch:(j + 1) * minibatch])
+    torch.cuda.synchronize()
+    wall = time.time() - t0
+    r = rewards.cpu().numpy()
+    st = L.stats.cpu().numpy()
+    assert np.isfinite(r).all() and (st == st).all(), "non-finite training statistics"
+    marks = sorted({0, iters // 3, 2 * iters // 3, iters - 1})
+    return {"workload": f"paper task PPO training from the seeded networks: {iters} iterations of {n} envs x {T} "
+                        f"steps (sampled, value head), GAE, {epochs} epochs x {n_mb} minibatches of {minibatch}",
+            "iterations": iters, "wall_s": wall, "ms_per_iteration": wall / iters * 1e3,
+            "mean_step_reward": {str(k): float(r[k]) for k in marks},
+            "last_value_loss": float(st[1]), "last_entropy": float(st[2]), "last_approx_kl": float(st[3])}
+
+
 # Dense-contraction work per env-step of a SHAC window on the paper task's 12-256-256-6
 # policy (padding excluded): the forward, the input gradient (the same matrices
 # transposed) and the weight gradient.
@@ -537,7 +593,8 @@ def main() -> int:
     ap.add_argument("--no-c5", action="store_true", help="skip the PPO-buffer (c5) rollout and GAE measurement")
     ap.add_argument("--no-ppo", action="store_true", help="skip the PPO-update measurement")
     ap.add_argument("--ppo-only", action="store_true", help="only measure the PPO update and print it")
-    ap.add_argument("--paper-only", action="store_true", help="only measure the paper task (c6, training iteration)")
+    ap.add_argument("--paper-only", action="store_true",
+                    help="only measure the paper task (c6, training iteration, 150 training iterations)")
     ap.add_argument("--shac-only", action="store_true", help="only measure the SHAC windows (4096 and 512 envs)")
     ap.add_argument("--c5-only", action="store_true", help="only measure the PPO-buffer rollout and GAE (c5)")
     ap.add_argument("--sweep", action="store_true",
@@ -575,7 +632,8 @@ def main() -> int:
         print(json.dumps({"ppo": ppo_measure()}), flush=True)
         return 0
     if args.paper_only:
-        print(json.dumps({"c6": paper_task_measure(), "paper_training": paper_training_measure()}), flush=True)
+        print(json.dumps({"c6": paper_task_measure(), "paper_training": paper_training_measure(),
+                          "paper_learning": paper_learning_measure()}), flush=True)
         return 0
     if args.c5_only:
         print(json.dumps({"c5": c5_measure()}), flush=True)
@@ -671,6 +729,7 @@ def main() -> int:
         line["ppo"] = ppo_measure()
         line["c6"] = paper_task_measure()
         line["paper_training"] = paper_training_measure()
+        line["paper_learning"] = paper_learning_measure()
         line["shac"] = [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, min(args.cpu_steps, T))
