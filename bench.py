@@ -457,6 +457,47 @@ def shac_measure(n_envs: int, reps: int = 16) -> dict:
             "hundred_episodes_s": 100 * windows_per_episode * (tw + ts + tc)}
 
 
+def shac_learning_measure(n_envs: int, windows: int = 320) -> dict:
+    """SHAC training on the paper task from the seeded networks: `windows` iterations (window,
+    actor step, critic update of 16 x 4 minibatches), consecutive windows tiling the 512-step
+    episodes; the mean step reward of each window and of each episode's 16 windows, and the
+    wall clock of the whole run (host work included)."""
+    import time
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2512_13359_amd import AuvEnv, ShacLearner
+
+    cfg = W.config("c6", n_envs=n_envs)
+    h = W.SHAC["h"]
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.set_task(W.PAPER_TASK)
+    env.reset()
+    L = ShacLearner(env, W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.PAPER_VALUE_SEED, n_in=12),
+                    h=h, gamma=W.SHAC["gamma"], max_grad_norm=W.SHAC["max_grad_norm"])
+    r = torch.empty(windows, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.time()
+    for k in range(windows):
+        L.window()
+        r[k] = L.rec["reward"].mean()
+        L.step()
+        L.critic_update(iterations=16, batches=4, seed=k)
+    torch.cuda.synchronize()
+    wall = time.time() - t0
+    rr = r.cpu().numpy()
+    wpe = cfg["episode_len"] // h
+    ep = rr[:(windows // wpe) * wpe].reshape(-1, wpe).mean(axis=1)
+    assert np.isfinite(rr).all() and np.isfinite(L.stats.cpu().numpy()).all(), "non-finite SHAC training"
+    return {"workload": f"SHAC training on the paper task from the seeded networks: {n_envs} envs, {windows} windows "
+                        f"of {h} steps ({len(ep)} episodes), actor step and critic update (16 x 4 minibatches) each",
+            "n_envs": n_envs, "windows": windows, "wall_s": wall, "ms_per_window": wall / windows * 1e3,
+            "first_windows_mean_step_reward": [float(x) for x in rr[:4]],
+            "episode_mean_step_reward": {str(i): float(ep[i]) for i in sorted({0, 1, len(ep) // 2, len(ep) - 1})}}
+
+
 def small_configs_measure(reps: int = 3) -> dict:
     """The 4096-env workloads (random actions c2, policy mean c3): env-steps/s per launch.
     4096 envs are 256 one-wave blocks of the quad-layout loop (c2) or 256 one-tile workgroups of
@@ -731,6 +772,7 @@ def main() -> int:
         line["paper_training"] = paper_training_measure()
         line["paper_learning"] = paper_learning_measure()
         line["shac"] = [shac_measure(W.SHAC["n_envs"]), shac_measure(W.SHAC["n_envs_small"])]
+        line["shac_learning"] = shac_learning_measure(W.SHAC["n_envs"])
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(cfg, min(args.cpu_steps, T))
     print(json.dumps(line), flush=True)

@@ -543,3 +543,31 @@ def test_ppo_fit_value_matches_stepwise_calls():
     assert A.auv_ppo_fit_work_bytes(15, 1) == -1 and A.auv_ppo_fit_work_bytes(64, 5) == -1
     with pytest.raises(A.AuvError):
         A.auv_ppo_fit_value(L.critic_cfg, net1.mlp, net1.net, batch, 0, batches, seed, 0, stage, g1, s1, work)
+
+
+def test_shac_learns_the_paper_task():
+    """End-to-end learning: SHAC on the paper task from the seeded networks at 512 envs, 160
+    windows (ten 512-step episodes), each followed by the actor's Adam step and the critic's
+    regression.  The reward gradient through the simulation improves the policy within the
+    first few windows, and the episodes' mean step reward keeps improving after that."""
+    require_gpu()
+    announce("shac learns the paper task")
+    from paper_2512_13359_amd import AuvEnv, ShacLearner
+    cfg = W.config("c6", n_envs=512)
+    env = AuvEnv(cfg, W.VEHICLE, W.ALLOC)
+    env.set_task(W.PAPER_TASK)
+    env.reset()
+    L = ShacLearner(env, W.mlp_weights(6, W.PAPER_POLICY_SEED, n_in=12), W.mlp_weights(1, W.PAPER_VALUE_SEED, n_in=12),
+                    h=W.SHAC["h"], gamma=W.SHAC["gamma"], max_grad_norm=W.SHAC["max_grad_norm"])
+    r = []
+    for k in range(160):
+        L.window()
+        r.append(float(L.rec["reward"].mean()))
+        L.step()
+        L.critic_update(iterations=16, batches=4, seed=k)
+    r = np.array(r)
+    ep = r.reshape(-1, cfg["episode_len"] // W.SHAC["h"]).mean(axis=1)
+    print(f"    first windows {np.round(r[:4], 3)}, episode means {np.round(ep, 3)}")
+    assert np.isfinite(r).all() and np.isfinite(host(L.stats)).all()
+    assert r[0] < -4.0 and r[3] > 0.5 * r[0]
+    assert ep[-1] > 0.5 * ep[0] and ep[-1] > ep[1] + 0.02
