@@ -434,7 +434,9 @@ __device__ __forceinline__ u32x2 pack4(const f32x4& v) {
 //                              feature tile 2 p, slots 4..7 of tile 2 p + 1, and the B operand
 //                              puts q(gy) in columns 0..7 for the first and 8..15 for the second,
 //                              so that eight accumulators hold all 256 x 8 entries.
-template <int NOUT, bool H1>
+// XP: the value net's pass after the policy's in the same update reads q(x) from x_frag, which
+// the policy's pass wrote for the same tiles, in place of gathering the observations again.
+template <int NOUT, bool H1, bool XP = false>
 __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __restrict__ w, const float* __restrict__ b,
                                                             const float* __restrict__ log_std, Batch D,
                                                             const int32_t* __restrict__ idx, int B, int tiles, Hp hp,
@@ -456,13 +458,16 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
   // they would be spilled, and every spill of a loaded value waits for the load.
   struct Idx {
     int s[POL ? 1 : 5];
+    int t;
   };
   struct In {
-    float x[8], rt[POL ? 1 : 4], a[POL ? 4 : 1], lp, ad;
+    float x[XP ? 1 : 8], rt[POL ? 1 : 4], a[POL ? 4 : 1], lp, ad;
+    bf16x8 xf;
   };
   auto load_idx = [&](int t) __attribute__((always_inline)) {
     Idx q;
-    q.s[0] = raw_index(idx, t, r, B);
+    q.t = t;
+    q.s[0] = XP ? 0 : raw_index(idx, t, r, B);
     if constexpr (!POL) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) q.s[1 + i] = raw_index(idx, t, 4 * g + i, B);
@@ -478,8 +483,12 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     size_t Mr = M;
     int gr = g;
     asm volatile("" : "+s"(Mr), "+v"(gr));
+    if constexpr (XP) {
+      in.xf = W.x_frag[(size_t)q.t * 64 + lane];   // the layer-1 operand the policy's pass stored
+    } else {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(gr, j), 22) * Mr + sr];
+      for (int j = 0; j < 8; ++j) in.x[j] = D.obs[(size_t)min(kslot(gr, j), 22) * Mr + sr];
+    }
     if constexpr (POL) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) in.a[i] = D.act[(size_t)((4 * gr + i) & 7) * Mr + sr];
@@ -582,9 +591,13 @@ __global__ __launch_bounds__(64 * VT_WAVES, 1) void k_vtile(const uint16_t* __re
     const size_t tb = (size_t)t * 16;
     const bool vr = t * 16 + r < B;
     bf16x8 x;
+    if constexpr (XP) {
+      x = cur.xf;
+    } else {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] = (__bf16)((vr && kslot(g, j) < 23) ? cur.x[j] : 0.0f);
-    W.x_frag[(size_t)t * 64 + lane] = x;
+      for (int j = 0; j < 8; ++j) x[j] = (__bf16)((vr && kslot(g, j) < 23) ? cur.x[j] : 0.0f);
+      W.x_frag[(size_t)t * 64 + lane] = x;
+    }
 
     // ---- layer 1, feature-major: the pairs h1[kt] (features 32 kt + kslot(g, j), sample r)
     bf16x8 h1[8];
@@ -1326,17 +1339,22 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
   const ppo::VwPlan vp = ppo::vw_plan(steps);
   const int chunks = vp.chunks;
   const dim3 vt_block(64 * ppo::VT_WAVES), vw_block(64 * ppo::VW_WAVES);
-  auto tile_grad = [&](const auv_mlp* net, bool pol) {
+  // xp: the value net's pass takes q(x) from the policy's pass instead of gathering it again
+  auto tile_grad = [&](const auv_mlp* net, bool pol, bool xp) {
     const float* ls = pol ? net->log_std : nullptr;
     if (vp.rows == 128) {
       if (pol)
         hipLaunchKernelGGL((ppo::k_vtile<8, false>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
+      else if (xp)
+        hipLaunchKernelGGL((ppo::k_vtile<1, false, true>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
       else
         hipLaunchKernelGGL((ppo::k_vtile<1, false>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
       hipLaunchKernelGGL((ppo::k_vwgrad<128, true>), dim3(2 * chunks), vw_block, 0, s, net->w, net->b, W, steps, chunks);
     } else {
       if (pol)
         hipLaunchKernelGGL((ppo::k_vtile<8, true>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
+      else if (xp)
+        hipLaunchKernelGGL((ppo::k_vtile<1, true, true>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
       else
         hipLaunchKernelGGL((ppo::k_vtile<1, true>), dim3(GV), vt_block, 0, s, net->w, net->b, ls, D, idx, B, tiles, hp, W);
       hipLaunchKernelGGL((ppo::k_vwgrad<64, false>), dim3(4 * chunks), vw_block, 0, s, net->w, net->b, W, steps, chunks);
@@ -1347,11 +1365,11 @@ static int grad_launch(const auv_ppo_config* cfg, const auv_mlp* policy, const a
       hipLaunchKernelGGL(ppo::k_adv_partial, dim3(ppo::ADV_BLOCKS), dim3(256), 0, s, batch->adv, idx, B, (int)batch->M,
                          W.adv_part);
     }
-    tile_grad(policy, true);
+    tile_grad(policy, true, false);
     hipLaunchKernelGGL(ppo::k_reduce, dim3(rb), dim3(256), 0, s, ACT, hp.n_act, GV, chunks, GV, chunks, W, cfg->ent_coef,
                        grad_policy, W.part_ss, ppo::AdamFuse{});
   }
-  tile_grad(value, false);
+  tile_grad(value, false, with_policy);
   hipLaunchKernelGGL(ppo::k_reduce, dim3(ppo::red_blocks(1)), dim3(256), 0, s, 1, 1, GV, chunks, GV, chunks, W, 0.0f,
                      grad_value, W.part_ss + rb, fuse);
   if (finalize)
