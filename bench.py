@@ -430,14 +430,15 @@ def shac_measure(n_envs: int, reps: int = 16) -> dict:
         e[1].record()
         L.step()
         e[2].record()
-        if k < 3:   # the critic's regression (16 passes x 4 minibatches) on the first windows only
+        if k < 6:   # the critic's regression (16 passes x 4 minibatches) on the first windows only:
+            # five timed, since one host stall among its 256 launches can double a sample
             L.critic_update(iterations=16, batches=4, seed=k)
         e[3].record()
         torch.cuda.synchronize()
         if k:
             win.append(e[0].elapsed_time(e[1]) * 1e-3)
             stp.append(e[1].elapsed_time(e[2]) * 1e-3)
-            if k < 3:
+            if k < 6:
                 crit.append(e[2].elapsed_time(e[3]) * 1e-3)
     st = L.stats.cpu().numpy()
     assert (st == st).all(), "non-finite SHAC statistics"

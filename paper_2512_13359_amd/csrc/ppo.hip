@@ -927,6 +927,7 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
   __shared__ bf16x8 Ad[2][MT][64];   // q(dz2) A fragments: rows ROWS p + 16 mt
   __shared__ bf16x8 A1[2][MT][64];   // q(dz1) A fragments: rows ROWS p + 16 mt
   __shared__ bf16x8 Xb[2][2][64];    // q(x) B fragments: inputs 16 it + r
+  __shared__ bf16x8 Xr[RECOMP ? 2 : 1][2][64];   // q(x) A fragments of the recomputation
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r = lane & 15;
@@ -957,8 +958,9 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
     const f32x4 zero = f32x4{0, 0, 0, 0};
     auto at = [&](int tile, int ft, int nft) { return ((size_t)tile * nft + ft) * 64 + lane; };
     // staging: wave w copies the row tiles k = w + 8 s of the block's 2 MT (q(dz2) tiles, then
-    // q(dz1) tiles).  The step's two q(x) fragments are loaded by every wave when it recomputes
-    // q(h1), otherwise by waves 0 and 1 only (dW1's operand).
+    // q(dz1) tiles).  Waves 0 and 1 load the step's two q(x) fragments (dW1's operand) and,
+    // when q(h1) is recomputed, pass them one step ahead through LDS (Xr) to every wave: read
+    // by all eight waves from L2 they were as many bytes as the q(dz) tiles.
     struct Step {
       bf16x8 a[SPW], x[2], h[RECOMP ? 1 : 2];
     };
@@ -971,7 +973,7 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
         const int smt = MT * p + k % MT;
         R.a[q] = join(sa[at(2 * u, smt, 16)], sa[at(2 * u + 1, smt, 16)]);
       }
-      if (RECOMP || w < 2) {
+      if (w < 2) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) R.x[h] = W.x_frag[(size_t)(2 * u + h) * 64 + lane];
       }
@@ -984,6 +986,10 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
     Step R[DEPTH];
 #pragma unroll
     for (int j = 0; j < DEPTH; ++j) load(u0 + j, R[j]);
+    if constexpr (RECOMP) {   // the first step's q(x), then one step ahead (below)
+      if (w < 2) Xr[0][w][lane] = w == 0 ? R[0].x[0] : R[0].x[1];
+      __syncthreads();
+    }
     for (int u = u0; u < u1; u += DEPTH) {
 #pragma unroll
       for (int j = 0; j < DEPTH; ++j) {
@@ -1000,7 +1006,7 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
             u32x2 half[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-              const f32x4 z = mfma(R[j].x[h], w1f[q], zero);
+              const f32x4 z = mfma(Xr[RECOMP ? buf : 0][h][lane], w1f[q], zero);
               f32x4 a;
 #pragma unroll
               for (int i = 0; i < 4; ++i) a[i] = tanh_bias(z[i], b1k[q]);
@@ -1016,9 +1022,14 @@ __global__ __launch_bounds__(64 * VW_WAVES, 1) void k_vwgrad(const uint16_t* __r
             else
               A1[buf][k - MT][lane] = R[j].a[q];
           }
-          if (w < 2)
+          if (w < 2) {
             Xb[buf][w][lane] = join(pack4(mfma(R[j].x[0], select_frag(g, r, w), zero)),
                                     pack4(mfma(R[j].x[1], select_frag(g, r, w), zero)));
+            // the next step's q(x) for every wave's recomputation (ring slot j + 1 holds step
+            // u + j + 1; buffer buf ^ 1 was last read before the previous barrier)
+            if (RECOMP && u + j + 1 < u1)
+              Xr[buf ^ 1][w][lane] = w == 0 ? R[(j + 1) % DEPTH].x[0] : R[(j + 1) % DEPTH].x[1];
+          }
           __syncthreads();
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
